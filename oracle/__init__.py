@@ -1,0 +1,178 @@
+"""Oracle for the DeepShift shift operators -- TEST INFRASTRUCTURE ONLY.
+
+Python access (ctypes, numpy arrays on the host) to the plain-loop C oracle in
+``oracle.c``. Only the tests, ``__graft_entry__.smoke()`` and the benchmark's
+CPU-baseline leg may import this package; the product library and its Python
+binding never do.
+
+Every function takes host numpy arrays in the layouts documented in
+``oracle.c``: activations int32 (fixed point, any F), weight codes uint8
+(``sign << 4 | shift_code``), optional int32 bias.
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+import subprocess
+
+import numpy as np
+
+_DIR = os.path.dirname(os.path.abspath(__file__))
+_SRC = os.path.join(_DIR, "oracle.c")
+_LIB = os.path.join(_DIR, "liboracle.so")
+_lib = None
+
+_P = ctypes.c_void_p
+_I = ctypes.c_int64
+
+
+def build(force: bool = False) -> str:
+    """Compile ``oracle.c`` into ``liboracle.so`` (gcc, OpenMP)."""
+    if force or not os.path.exists(_LIB) or os.path.getmtime(_LIB) < os.path.getmtime(_SRC):
+        tmp = _LIB + f".tmp{os.getpid()}"
+        subprocess.check_call(["gcc", "-O2", "-fopenmp", "-fPIC", "-shared", "-std=c99",
+                               "-Wall", "-Wextra", "-o", tmp, _SRC])
+        os.replace(tmp, _LIB)
+    return _LIB
+
+
+def _load():
+    global _lib
+    if _lib is None:
+        lib = ctypes.CDLL(build())
+        lib.oracle_term.restype = ctypes.c_int64
+        lib.oracle_term.argtypes = [ctypes.c_int32, ctypes.c_uint8]
+        lib.oracle_linear_shift.argtypes = [_P, _P, _P, _P, _I, _I, _I]
+        lib.oracle_conv2d_shift.argtypes = [_P, _P, _P, _P] + [_I] * 11
+        lib.oracle_conv2d_shift_points.argtypes = [_P, _P, _P] + [_I] * 11 + [_P, _I, _P]
+        lib.oracle_linear_shift_points.argtypes = [_P, _P, _P, _I, _I, _I, _P, _I, _P]
+        lib.oracle_conv2d_mul.argtypes = [_P, _P, _P, _P] + [_I] * 11
+        lib.oracle_pack_codes.argtypes = [_P, _I, _I, _P]
+        lib.oracle_unpack_codes.argtypes = [_P, _I, _I, _P]
+        _lib = lib
+    return _lib
+
+
+def _ptr(a):
+    return None if a is None else a.ctypes.data
+
+
+def _c(a, dtype):
+    if a is None:
+        return None
+    return np.ascontiguousarray(a, dtype=dtype)
+
+
+def set_threads(n: int) -> None:
+    """Number of OpenMP threads the oracle uses (0 = library default)."""
+    try:
+        omp = ctypes.CDLL("libgomp.so.1")
+        if n > 0:
+            omp.omp_set_num_threads(ctypes.c_int(n))
+    except OSError:
+        pass
+
+
+def max_threads() -> int:
+    try:
+        omp = ctypes.CDLL("libgomp.so.1")
+        return int(omp.omp_get_max_threads())
+    except OSError:
+        return 1
+
+
+def term(x: int, code: int) -> int:
+    """flip(floor(x * 2**-shift), sign) for one activation and one code."""
+    return int(_load().oracle_term(int(x), int(code)))
+
+
+def linear_shift(x, codes, bias=None):
+    """LinearShift: x [batch, in] int32, codes [out, in] uint8 -> y [batch, out] int32."""
+    x = _c(x, np.int32); codes = _c(codes, np.uint8); bias = _c(bias, np.int32)
+    batch, fin = x.shape
+    fout, fin2 = codes.shape
+    assert fin == fin2 and (bias is None or bias.shape == (fout,))
+    y = np.empty((batch, fout), np.int32)
+    _load().oracle_linear_shift(_ptr(x), _ptr(codes), _ptr(bias), _ptr(y), batch, fin, fout)
+    return y
+
+
+def out_size(h, pad, r, stride):
+    return (h + 2 * pad - r) // stride + 1
+
+
+def conv2d_shift(x, codes, bias=None, r=3, s=None, stride=1, pad=0):
+    """ConvShift: x [N, C, H, W] int32, codes [K, C*R*S] uint8 -> y [N, K, OH, OW].
+
+    ``stride`` and ``pad`` are ints or (h, w) pairs.
+    """
+    s = r if s is None else s
+    sh, sw = (stride, stride) if np.isscalar(stride) else stride
+    ph, pw = (pad, pad) if np.isscalar(pad) else pad
+    x = _c(x, np.int32); codes = _c(codes, np.uint8); bias = _c(bias, np.int32)
+    N, C, H, W = x.shape
+    K = codes.shape[0]
+    assert codes.shape == (K, C * r * s) or codes.shape == (K, C, r, s)
+    OH, OW = out_size(H, ph, r, sh), out_size(W, pw, s, sw)
+    y = np.empty((N, K, OH, OW), np.int32)
+    _load().oracle_conv2d_shift(_ptr(x), _ptr(codes), _ptr(bias), _ptr(y),
+                                N, C, H, W, K, r, s, sh, sw, ph, pw)
+    return y
+
+
+def conv2d_shift_points(x, codes, bias, idx, r=3, s=None, stride=1, pad=0):
+    """Selected outputs y.flat[idx] of ``conv2d_shift`` (idx int64 flat indices)."""
+    s = r if s is None else s
+    sh, sw = (stride, stride) if np.isscalar(stride) else stride
+    ph, pw = (pad, pad) if np.isscalar(pad) else pad
+    x = _c(x, np.int32); codes = _c(codes, np.uint8); bias = _c(bias, np.int32)
+    idx = _c(idx, np.int64)
+    N, C, H, W = x.shape
+    K = codes.shape[0]
+    out = np.empty(idx.shape, np.int32)
+    _load().oracle_conv2d_shift_points(_ptr(x), _ptr(codes), _ptr(bias), N, C, H, W, K, r, s,
+                                       sh, sw, ph, pw, _ptr(idx), idx.size, _ptr(out))
+    return out
+
+
+def linear_shift_points(x, codes, bias, idx):
+    """Selected outputs y.flat[idx] of ``linear_shift``."""
+    x = _c(x, np.int32); codes = _c(codes, np.uint8); bias = _c(bias, np.int32)
+    idx = _c(idx, np.int64)
+    batch, fin = x.shape
+    out = np.empty(idx.shape, np.int32)
+    _load().oracle_linear_shift_points(_ptr(x), _ptr(codes), _ptr(bias), batch, fin,
+                                       codes.shape[0], _ptr(idx), idx.size, _ptr(out))
+    return out
+
+
+def conv2d_mul(x, wts, bias=None, r=3, s=None, stride=1, pad=0):
+    """Multiplication-based comparison: y = wrap32(b + sum x*w), int32 weights [K, C*R*S]."""
+    s = r if s is None else s
+    sh, sw = (stride, stride) if np.isscalar(stride) else stride
+    ph, pw = (pad, pad) if np.isscalar(pad) else pad
+    x = _c(x, np.int32); wts = _c(wts, np.int32); bias = _c(bias, np.int32)
+    N, C, H, W = x.shape
+    K = wts.shape[0]
+    OH, OW = out_size(H, ph, r, sh), out_size(W, pw, s, sw)
+    y = np.empty((N, K, OH, OW), np.int32)
+    _load().oracle_conv2d_mul(_ptr(x), _ptr(wts), _ptr(bias), _ptr(y), N, C, H, W, K, r, s,
+                              sh, sw, ph, pw)
+    return y
+
+
+def pack_codes(codes):
+    """codes [rows, cols] uint8 -> packed [rows, ceil(cols/6)] uint32."""
+    codes = _c(codes, np.uint8)
+    rows, cols = codes.shape
+    out = np.empty((rows, (cols + 5) // 6), np.uint32)
+    _load().oracle_pack_codes(_ptr(codes), rows, cols, _ptr(out))
+    return out
+
+
+def unpack_codes(packed, cols):
+    packed = _c(packed, np.uint32)
+    rows = packed.shape[0]
+    out = np.empty((rows, cols), np.uint8)
+    _load().oracle_unpack_codes(_ptr(packed), rows, cols, _ptr(out))
+    return out

@@ -1,0 +1,218 @@
+/*
+ * Oracle for the DeepShift shift operators -- TEST INFRASTRUCTURE ONLY.
+ *
+ * A plain, slow CPU implementation of what LinearShift and ConvShift compute
+ * at inference time. Only the tests, the smoke check and the benchmark's CPU
+ * baseline use it; the product library never calls it and shares no code
+ * with it.
+ *
+ * What is computed (DeepShift, Section 3, Eqs. 1-3; Figure 1a; Section 4):
+ *   Each weight is flip(2^p, s) with p an integer power and s a ternary sign
+ *   (Eq. 3). Multiplying a fixed-point activation x by 2^p is a bitwise shift
+ *   (Eq. 1); the powers used are 0 .. -14, so every shift is a right shift by
+ *   -p. The sign flip (Eq. 2) negates, keeps or zeroes the shifted value, and
+ *   the products are summed as in an ordinary linear layer or convolution,
+ *   plus a bias (Section 3, Y = W X + b and Y = W (*) X + b).
+ *
+ * Readings where the paper is silent (each one is also listed in the design
+ * notes of this project):
+ *   - A right shift of a negative x rounds toward minus infinity (an
+ *     arithmetic shift): term = floor(x * 2^p). The paper equates the shift
+ *     with the multiplication, which is exact only when the low bits are 0.
+ *   - The shift is applied first and the sign flip second: -(floor(x*2^p)).
+ *   - Weight code (uint8): bit 4 = sign (1 means negate), bits 0-3 = shift
+ *     code c; c in 0..14 means p = -c; c = 15 means a zero weight whatever
+ *     the sign bit (the ternary zero of Eq. 2 within the 5-bit budget of
+ *     Section 4).
+ *   - Sums are formed exactly (int64 here) and wrapped once to int32
+ *     (two's complement, modulo 2^32).
+ *   - Bias is optional (NULL) and is added once per output.
+ *   - Packed layout: six 5-bit codes per uint32 word, code j of the word in
+ *     bits [5j, 5j+5), bits 30-31 zero; each weight row starts a new word and
+ *     its last word is filled with code 15.
+ *
+ * The floor is computed by integer division, not by the shift operator, so
+ * the oracle does not rely on how C shifts negative numbers.
+ *
+ * Parity status: every function here is pinned by the CPU test suite
+ * (brute force with exact rationals, the closed form against a float64
+ * library convolution on inputs divisible by 2^15, a library arithmetic
+ * shift, the one-sided rounding bound, zero-code and sign-flip invariants,
+ * and hand-derived packed words).
+ */
+#include <stdint.h>
+#include <stddef.h>
+
+/* floor(x / 2^c) for 0 <= c <= 14, by integer division (Eq. 1, reading: floor). */
+static int64_t floor_div_pow2(int64_t x, int c)
+{
+    int64_t d = (int64_t)1 << c;
+    int64_t q = x / d;            /* C division truncates toward zero */
+    if (x % d != 0 && x < 0)
+        q -= 1;                   /* move truncation down to the floor */
+    return q;
+}
+
+/* One weight applied to one activation: flip(floor(x * 2^p), s) (Eqs. 1-3). */
+int64_t oracle_term(int32_t x, uint8_t code)
+{
+    int shift = code & 15;
+    int negative = (code >> 4) & 1;
+    if (shift == 15)
+        return 0;                 /* zero weight (s = 0 in Eq. 2) */
+    int64_t t = floor_div_pow2((int64_t)x, shift);
+    return negative ? -t : t;
+}
+
+/* Two's-complement wrap of an exact sum to int32 (modulo 2^32). */
+static int32_t wrap32(int64_t v)
+{
+    uint32_t u = (uint32_t)(uint64_t)v;
+    return (int32_t)u;            /* gcc: modulo conversion */
+}
+
+/* LinearShift, Y = W~ X + b (Section 3): x [batch][in], codes [out][in],
+ * bias [out] or NULL, y [batch][out]. */
+void oracle_linear_shift(const int32_t *x, const uint8_t *codes, const int32_t *bias,
+                         int32_t *y, int64_t batch, int64_t in, int64_t out)
+{
+    #pragma omp parallel for schedule(dynamic, 1)
+    for (int64_t b = 0; b < batch; ++b) {
+        for (int64_t o = 0; o < out; ++o) {
+            int64_t acc = bias ? (int64_t)bias[o] : 0;
+            for (int64_t i = 0; i < in; ++i)
+                acc += oracle_term(x[b * in + i], codes[o * in + i]);
+            y[b * out + o] = wrap32(acc);
+        }
+    }
+}
+
+/* ConvShift output element (n, k, oh, ow): Y = W~ (*) X + b (Section 3).
+ * x [N][C][H][W], codes [K][C][R][S] (flattened rows of C*R*S), zero padding. */
+static int32_t conv_point(const int32_t *x, const uint8_t *codes, const int32_t *bias,
+                          int64_t C, int64_t H, int64_t W, int64_t R, int64_t S,
+                          int64_t sh, int64_t sw, int64_t ph, int64_t pw,
+                          int64_t n, int64_t k, int64_t oh, int64_t ow)
+{
+    int64_t acc = bias ? (int64_t)bias[k] : 0;
+    for (int64_t c = 0; c < C; ++c)
+        for (int64_t r = 0; r < R; ++r)
+            for (int64_t s = 0; s < S; ++s) {
+                int64_t ih = oh * sh - ph + r;
+                int64_t iw = ow * sw - pw + s;
+                if (ih < 0 || ih >= H || iw < 0 || iw >= W)
+                    continue;     /* zero padding contributes nothing */
+                int32_t xv = x[((n * C + c) * H + ih) * W + iw];
+                uint8_t code = codes[((k * C + c) * R + r) * S + s];
+                acc += oracle_term(xv, code);
+            }
+    return wrap32(acc);
+}
+
+static int64_t out_dim(int64_t in, int64_t pad, int64_t k, int64_t stride)
+{
+    return (in + 2 * pad - k) / stride + 1;
+}
+
+void oracle_conv2d_shift(const int32_t *x, const uint8_t *codes, const int32_t *bias,
+                         int32_t *y, int64_t N, int64_t C, int64_t H, int64_t W,
+                         int64_t K, int64_t R, int64_t S, int64_t sh, int64_t sw,
+                         int64_t ph, int64_t pw)
+{
+    int64_t OH = out_dim(H, ph, R, sh), OW = out_dim(W, pw, S, sw);
+    #pragma omp parallel for collapse(2) schedule(dynamic, 1)
+    for (int64_t n = 0; n < N; ++n)
+        for (int64_t k = 0; k < K; ++k)
+            for (int64_t oh = 0; oh < OH; ++oh)
+                for (int64_t ow = 0; ow < OW; ++ow)
+                    y[((n * K + k) * OH + oh) * OW + ow] =
+                        conv_point(x, codes, bias, C, H, W, R, S, sh, sw, ph, pw,
+                                   n, k, oh, ow);
+}
+
+/* Selected outputs of a convolution: idx holds flattened indices into y
+ * [N][K][OH][OW]; out[i] receives y[idx[i]]. */
+void oracle_conv2d_shift_points(const int32_t *x, const uint8_t *codes, const int32_t *bias,
+                                int64_t N, int64_t C, int64_t H, int64_t W, int64_t K,
+                                int64_t R, int64_t S, int64_t sh, int64_t sw, int64_t ph,
+                                int64_t pw, const int64_t *idx, int64_t npts, int32_t *out)
+{
+    int64_t OH = out_dim(H, ph, R, sh), OW = out_dim(W, pw, S, sw);
+    (void)N;
+    #pragma omp parallel for schedule(dynamic, 16)
+    for (int64_t i = 0; i < npts; ++i) {
+        int64_t t = idx[i];
+        int64_t ow = t % OW; t /= OW;
+        int64_t oh = t % OH; t /= OH;
+        int64_t k = t % K;   t /= K;
+        out[i] = conv_point(x, codes, bias, C, H, W, R, S, sh, sw, ph, pw, t, k, oh, ow);
+    }
+}
+
+/* Selected outputs of a linear layer: idx into y [batch][out]. */
+void oracle_linear_shift_points(const int32_t *x, const uint8_t *codes, const int32_t *bias,
+                                int64_t batch, int64_t in, int64_t out_features,
+                                const int64_t *idx, int64_t npts, int32_t *out)
+{
+    (void)batch;
+    #pragma omp parallel for schedule(dynamic, 16)
+    for (int64_t i = 0; i < npts; ++i) {
+        int64_t b = idx[i] / out_features, o = idx[i] % out_features;
+        int64_t acc = bias ? (int64_t)bias[o] : 0;
+        for (int64_t j = 0; j < in; ++j)
+            acc += oracle_term(x[b * in + j], codes[o * in + j]);
+        out[i] = wrap32(acc);
+    }
+}
+
+/* Multiplication-based comparison operator: y = wrap32(b + sum x * w) with
+ * int32 weights, products and sums exact. Same layouts as the shift ops. */
+void oracle_conv2d_mul(const int32_t *x, const int32_t *wts, const int32_t *bias, int32_t *y,
+                       int64_t N, int64_t C, int64_t H, int64_t W, int64_t K, int64_t R,
+                       int64_t S, int64_t sh, int64_t sw, int64_t ph, int64_t pw)
+{
+    int64_t OH = out_dim(H, ph, R, sh), OW = out_dim(W, pw, S, sw);
+    #pragma omp parallel for collapse(2) schedule(dynamic, 1)
+    for (int64_t n = 0; n < N; ++n)
+        for (int64_t k = 0; k < K; ++k)
+            for (int64_t oh = 0; oh < OH; ++oh)
+                for (int64_t ow = 0; ow < OW; ++ow) {
+                    int64_t acc = bias ? (int64_t)bias[k] : 0;
+                    for (int64_t c = 0; c < C; ++c)
+                        for (int64_t r = 0; r < R; ++r)
+                            for (int64_t s = 0; s < S; ++s) {
+                                int64_t ih = oh * sh - ph + r, iw = ow * sw - pw + s;
+                                if (ih < 0 || ih >= H || iw < 0 || iw >= W)
+                                    continue;
+                                acc += (int64_t)x[((n * C + c) * H + ih) * W + iw] *
+                                       (int64_t)wts[((k * C + c) * R + r) * S + s];
+                            }
+                    y[((n * K + k) * OH + oh) * OW + ow] = wrap32(acc);
+                }
+}
+
+/* Packed layout (reading: see header): rows x cols codes -> rows x ceil(cols/6)
+ * words. Codes must be < 32. */
+void oracle_pack_codes(const uint8_t *codes, int64_t rows, int64_t cols, uint32_t *packed)
+{
+    int64_t wpr = (cols + 5) / 6;
+    for (int64_t r = 0; r < rows; ++r)
+        for (int64_t w = 0; w < wpr; ++w) {
+            uint32_t word = 0;
+            for (int64_t j = 0; j < 6; ++j) {
+                int64_t col = w * 6 + j;
+                uint32_t code = col < cols ? codes[r * cols + col] : 15u;
+                word |= (code & 31u) << (5 * j);
+            }
+            packed[r * wpr + w] = word;
+        }
+}
+
+void oracle_unpack_codes(const uint32_t *packed, int64_t rows, int64_t cols, uint8_t *codes)
+{
+    int64_t wpr = (cols + 5) / 6;
+    for (int64_t r = 0; r < rows; ++r)
+        for (int64_t col = 0; col < cols; ++col)
+            codes[r * cols + col] =
+                (uint8_t)((packed[r * wpr + col / 6] >> (5 * (col % 6))) & 31u);
+}

@@ -1,0 +1,100 @@
+"""The oracle's pins must catch plausible mistakes.
+
+Each case plants one mistake into a copy of the oracle's C source (on the CPU,
+in a temporary directory), builds it, and runs the pin checks of
+``test_oracle_pins`` against the mutated build: at least one check must fail.
+"""
+import importlib.util
+import os
+import shutil
+
+import pytest
+
+import tests.test_oracle_pins as pins
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+SRC = os.path.join(ROOT, "oracle", "oracle.c")
+
+MUTATIONS = {
+    "truncate_instead_of_floor": ("q -= 1;", "q -= 0;"),
+    "negate_then_shift": ("int64_t t = floor_div_pow2((int64_t)x, shift);",
+                          "int64_t t = floor_div_pow2(negative ? -(int64_t)x : (int64_t)x, shift);"
+                          " if (negative) return t;"),
+    "zero_code_as_shift_15": ("if (shift == 15)\n        return 0;", "if (shift == 99)\n        return 0;"),
+    "sign_ignored": ("return negative ? -t : t;", "return t;"),
+    "conv_bias_dropped": ("int64_t acc = bias ? (int64_t)bias[k] : 0;\n    for (int64_t c = 0; c < C; ++c)\n        for (int64_t r",
+                          "int64_t acc = 0;\n    for (int64_t c = 0; c < C; ++c)\n        for (int64_t r"),
+    "kernel_r_s_transposed": ("codes[((k * C + c) * R + r) * S + s]", "codes[((k * C + c) * S + s) * R + r]"),
+    "input_h_w_transposed": ("int32_t xv = x[((n * C + c) * H + ih) * W + iw];",
+                             "int32_t xv = x[((n * C + c) * W + iw) * H + ih];"),
+    "stride_h_w_swapped": ("int64_t ih = oh * sh - ph + r;", "int64_t ih = oh * sw - ph + r;"),
+    "pad_off_by_one": ("int64_t iw = ow * sw - pw + s;\n                if", "int64_t iw = ow * sw - pw + s + 1;\n                if"),
+    "saturate_instead_of_wrap": ("uint32_t u = (uint32_t)(uint64_t)v;\n    return (int32_t)u;",
+                                 "return v > 2147483647 ? 2147483647 : (v < -2147483647 - 1 ? -2147483647 - 1 : (int32_t)v);"),
+    "linear_codes_transposed": ("acc += oracle_term(x[b * in + i], codes[o * in + i]);",
+                                "acc += oracle_term(x[b * in + i], codes[(i * out + o) % (in * out)]);"),
+    "pack_pad_with_zero": ("col < cols ? codes[r * cols + col] : 15u;", "col < cols ? codes[r * cols + col] : 0u;"),
+    "pack_bit_offset": ("word |= (code & 31u) << (5 * j);", "word |= (code & 31u) << (5 * (5 - j));"),
+    "drop_last_term": ("for (int64_t s = 0; s < S; ++s) {\n                int64_t ih",
+                       "for (int64_t s = 0; s < S - (c == C - 1 && r == R - 1); ++s) {\n                int64_t ih"),
+}
+
+CHECKS = [
+    (pins.test_term_matches_exact_rational_floor, ()),
+    (pins.test_term_reading_examples, ()),
+    (pins.test_conv_bruteforce_tiny, (0,)),
+    (pins.test_linear_bruteforce_tiny, ()),
+    *[(pins.test_conv_closed_form_exact_shifts, (s,)) for s in pins.CLOSED_SHAPES],
+    (pins.test_linear_closed_form_exact_shifts, ()),
+    (pins.test_single_term_equals_numpy_right_shift, ()),
+    *[(pins.test_one_sided_rounding_bound, (p,)) for p in ("pos", "neg", "mixed")],
+    (pins.test_zero_codes_contribute_nothing, ()),
+    (pins.test_sign_flip_negates_sum, ()),
+    (pins.test_linear_equals_1x1_conv, ()),
+    (pins.test_wraparound_extremes, ()),
+    (pins.test_pack_layout_bitstream, ()),
+    (pins.test_pack_literal_words, ()),
+]
+
+
+def load_mutant(tmp_path, name):
+    old, new = MUTATIONS[name]
+    text = open(SRC).read()
+    assert text.count(old) == 1, f"mutation site for {name} not unique"
+    d = tmp_path / name
+    d.mkdir()
+    src = d / "oracle.c"
+    src.write_text(text.replace(old, new))
+    shutil.copy(os.path.join(ROOT, "oracle", "__init__.py"), d / "__init__.py")
+    spec = importlib.util.spec_from_file_location(f"oracle_{name}", d / "__init__.py")
+    mod = importlib.util.module_from_spec(spec)
+    spec.loader.exec_module(mod)
+    mod.build(force=True)
+    return mod
+
+
+@pytest.mark.parametrize("name", sorted(MUTATIONS))
+def test_pins_catch_mutation(tmp_path, monkeypatch, name):
+    mod = load_mutant(tmp_path, name)
+    monkeypatch.setattr(pins, "oracle", mod)
+    failed = []
+    for fn, args in CHECKS:
+        try:
+            fn(*args)
+        except AssertionError:
+            failed.append(fn.__name__)
+    assert failed, f"no pin caught the mutation {name}"
+
+
+def test_unmutated_copy_passes(tmp_path, monkeypatch):
+    d = tmp_path / "clean"
+    d.mkdir()
+    shutil.copy(SRC, d / "oracle.c")
+    shutil.copy(os.path.join(ROOT, "oracle", "__init__.py"), d / "__init__.py")
+    spec = importlib.util.spec_from_file_location("oracle_clean", d / "__init__.py")
+    mod = importlib.util.module_from_spec(spec)
+    spec.loader.exec_module(mod)
+    mod.build(force=True)
+    monkeypatch.setattr(pins, "oracle", mod)
+    for fn, args in CHECKS:
+        fn(*args)

@@ -1,0 +1,379 @@
+"""Pins for the oracle: each test checks it against something other than itself.
+
+* brute force with exact rational arithmetic (``fractions.Fraction``) on tiny
+  inputs: the weight is the real number flip(2**p, s) and each term is
+  floor(x * w) for a positive weight, -floor(x * |w|) for a negative one;
+* the closed form: on activations divisible by 2**15 every shift is exact, so
+  the result equals a float64 library convolution (``torch.nn.functional``)
+  with weights sign * 2**p (DeepShift Eq. 3) -- this pins layout, stride,
+  padding and indexing;
+* numpy's arithmetic right shift on a 1x1 single-channel case (the floor
+  reading of Eq. 1, and shift-then-negate);
+* the one-sided rounding bound against the float64 result on signed inputs,
+  which separates floor from truncation and shift-then-negate from
+  negate-then-shift;
+* invariants: zero codes contribute nothing, flipping every sign negates the
+  weighted sum, LinearShift equals a 1x1 ConvShift;
+* the packed layout rebuilt bit by bit with ``numpy.packbits``.
+"""
+import math
+from fractions import Fraction
+
+import numpy as np
+import pytest
+import torch
+import torch.nn.functional as F
+
+import oracle
+from paper_1905_13298_amd.workloads import random_codes
+
+I32_MIN, I32_MAX = -(2 ** 31), 2 ** 31 - 1
+
+
+def wrap(v: int) -> int:
+    return ((v + 2 ** 31) % 2 ** 32) - 2 ** 31
+
+
+def weight_value(code: int) -> Fraction:
+    """flip(2**p, s) as an exact rational (Eq. 3)."""
+    shift, neg = code & 15, (code >> 4) & 1
+    if shift == 15:
+        return Fraction(0)
+    mag = Fraction(1, 2 ** shift)
+    return -mag if neg else mag
+
+
+def brute_term(x: int, code: int) -> int:
+    w = weight_value(code)
+    if w >= 0:
+        return math.floor(x * w)
+    return -math.floor(x * (-w))
+
+
+def weights_f64(codes):
+    """Dequantised weights sign * 2**p as float64 (zero codes give 0)."""
+    shift = (codes & 15).astype(np.int64)
+    neg = (codes >> 4) & 1
+    w = np.where(shift == 15, 0.0, np.ldexp(1.0, -np.minimum(shift, 14)))
+    return np.where(neg == 1, -w, w)
+
+
+def torch_conv_f64(x, codes, bias, r, s, stride, pad):
+    K = codes.shape[0]
+    C = x.shape[1]
+    w = torch.from_numpy(weights_f64(codes).reshape(K, C, r, s))
+    b = None if bias is None else torch.from_numpy(bias.astype(np.float64))
+    y = F.conv2d(torch.from_numpy(x.astype(np.float64)), w, b, stride=stride, padding=pad)
+    return y.numpy()
+
+
+# ---------------------------------------------------------------------------
+# single term
+
+
+def test_term_matches_exact_rational_floor():
+    rng = np.random.default_rng(100)
+    xs = [0, 1, -1, 2, -2, 5, -5, 7, -7, 2 ** 14, -(2 ** 14), 2 ** 15 - 1, -(2 ** 15) + 1,
+          I32_MAX, I32_MIN, I32_MAX - 1, I32_MIN + 1]
+    xs += rng.integers(I32_MIN, I32_MAX, 200, endpoint=True).tolist()
+    for code in range(32):
+        for x in xs:
+            assert oracle.term(x, code) == brute_term(x, code), (x, code)
+
+
+def test_term_reading_examples():
+    # floor, not truncation: -5 >> 1 is -3; shift first, then negate: -(5 >> 1) = -2
+    assert oracle.term(-5, 1) == -3
+    assert oracle.term(5, 16 | 1) == -2
+    assert oracle.term(-5, 16 | 1) == 3
+    # code 15 is a zero weight whatever the sign bit
+    assert oracle.term(123456, 15) == 0 and oracle.term(-123456, 31) == 0
+
+
+# ---------------------------------------------------------------------------
+# brute force on tiny shapes
+
+
+def brute_conv(x, codes, bias, r, s, stride, pad):
+    N, C, H, W = x.shape
+    K = codes.shape[0]
+    sh, sw = stride
+    ph, pw = pad
+    OH, OW = (H + 2 * ph - r) // sh + 1, (W + 2 * pw - s) // sw + 1
+    cw = codes.reshape(K, C, r, s)
+    # zero-padded copy as Python ints
+    padded = [[[[0] * (W + 2 * pw) for _ in range(H + 2 * ph)] for _ in range(C)]
+              for _ in range(N)]
+    for n in range(N):
+        for c in range(C):
+            for i in range(H):
+                for j in range(W):
+                    padded[n][c][i + ph][j + pw] = int(x[n, c, i, j])
+    y = np.zeros((N, K, OH, OW), np.int64)
+    for n in range(N):
+        for k in range(K):
+            for oh in range(OH):
+                for ow in range(OW):
+                    tot = 0 if bias is None else int(bias[k])
+                    for c in range(C):
+                        for i in range(r):
+                            for j in range(s):
+                                tot += brute_term(padded[n][c][oh * sh + i][ow * sw + j],
+                                                  int(cw[k, c, i, j]))
+                    y[n, k, oh, ow] = wrap(tot)
+    return y.astype(np.int32)
+
+
+def tiny_cases(count, seed):
+    rng = np.random.default_rng(seed)
+    for _ in range(count):
+        r, s = int(rng.integers(1, 4)), int(rng.integers(1, 4))
+        sh, sw = int(rng.integers(1, 4)), int(rng.integers(1, 4))
+        ph, pw = int(rng.integers(0, 3)), int(rng.integers(0, 3))
+        H = int(rng.integers(max(1, r - 2 * ph), 7))
+        W = int(rng.integers(max(1, s - 2 * pw), 7))
+        N, C, K = (int(v) for v in rng.integers(1, 4, 3))
+        signed = bool(rng.integers(0, 2))
+        lo = -(2 ** 20) if signed else 0
+        x = rng.integers(lo, 2 ** 20, (N, C, H, W)).astype(np.int32)
+        codes = rng.integers(0, 32, (K, C * r * s)).astype(np.uint8)
+        bias = rng.integers(-(2 ** 16), 2 ** 16, K).astype(np.int32) if rng.integers(0, 2) else None
+        yield x, codes, bias, r, s, (sh, sw), (ph, pw)
+
+
+@pytest.mark.parametrize("seed", range(4))
+def test_conv_bruteforce_tiny(seed):
+    for x, codes, bias, r, s, stride, pad in tiny_cases(30, 1000 + seed):
+        got = oracle.conv2d_shift(x, codes, bias, r=r, s=s, stride=stride, pad=pad)
+        want = brute_conv(x, codes, bias, r, s, stride, pad)
+        np.testing.assert_array_equal(got, want)
+
+
+def test_linear_bruteforce_tiny():
+    rng = np.random.default_rng(7)
+    for _ in range(40):
+        B, I, O = (int(v) for v in rng.integers(1, 9, 3))
+        x = rng.integers(-(2 ** 24), 2 ** 24, (B, I)).astype(np.int32)
+        codes = rng.integers(0, 32, (O, I)).astype(np.uint8)
+        bias = rng.integers(-(2 ** 16), 2 ** 16, O).astype(np.int32)
+        got = oracle.linear_shift(x, codes, bias)
+        for b in range(B):
+            for o in range(O):
+                tot = int(bias[o]) + sum(brute_term(int(x[b, i]), int(codes[o, i]))
+                                         for i in range(I))
+                assert got[b, o] == wrap(tot)
+
+
+# ---------------------------------------------------------------------------
+# closed form: exact shifts equal a float64 library convolution
+
+
+CLOSED_SHAPES = [
+    # N, C, H, W, K, r, s, stride, pad
+    (2, 3, 9, 7, 4, 3, 3, (1, 1), (1, 1)),
+    (1, 5, 11, 10, 3, 3, 3, (2, 2), (1, 1)),
+    (2, 2, 13, 12, 5, 7, 7, (2, 2), (3, 3)),
+    (3, 8, 6, 6, 6, 1, 1, (1, 1), (0, 0)),
+    (2, 8, 7, 9, 6, 1, 1, (2, 2), (0, 0)),
+    (1, 4, 8, 11, 3, 2, 3, (1, 2), (0, 2)),
+    (1, 3, 10, 6, 2, 3, 1, (3, 1), (2, 0)),
+]
+
+
+@pytest.mark.parametrize("shape", CLOSED_SHAPES)
+def test_conv_closed_form_exact_shifts(shape):
+    N, C, H, W, K, r, s, stride, pad = shape
+    rng = np.random.default_rng(sum(shape[:7]))
+    m = rng.integers(-(2 ** 8), 2 ** 8, (N, C, H, W))
+    x = (m * 2 ** 15).astype(np.int32)          # every shift by <= 14 is exact
+    codes = random_codes(rng, (K, C * r * s), zero_frac=0.15)
+    bias = rng.integers(-(2 ** 16), 2 ** 16, K).astype(np.int32)
+    got = oracle.conv2d_shift(x, codes, bias, r=r, s=s, stride=stride, pad=pad)
+    want = torch_conv_f64(x, codes, bias, r, s, stride, pad)
+    assert np.all(want == np.round(want))
+    np.testing.assert_array_equal(got.astype(np.float64), want)
+
+
+def test_linear_closed_form_exact_shifts():
+    rng = np.random.default_rng(11)
+    B, I, O = 6, 70, 9
+    x = (rng.integers(-(2 ** 8), 2 ** 8, (B, I)) * 2 ** 15).astype(np.int32)
+    codes = random_codes(rng, (O, I), zero_frac=0.2)
+    bias = rng.integers(-(2 ** 16), 2 ** 16, O).astype(np.int32)
+    got = oracle.linear_shift(x, codes, bias)
+    want = (torch.from_numpy(x.astype(np.float64)) @ torch.from_numpy(weights_f64(codes)).T
+            + torch.from_numpy(bias.astype(np.float64))).numpy()
+    np.testing.assert_array_equal(got.astype(np.float64), want)
+
+
+# ---------------------------------------------------------------------------
+# library arithmetic shift (floor) and shift-then-negate
+
+
+def test_single_term_equals_numpy_right_shift():
+    rng = np.random.default_rng(3)
+    x = rng.integers(I32_MIN, I32_MAX, (1, 1, 20, 20), endpoint=True).astype(np.int32)
+    for shift in range(15):
+        for neg in (0, 1):
+            codes = np.array([[neg << 4 | shift]], np.uint8)
+            got = oracle.conv2d_shift(x, codes, None, r=1)
+            want = np.right_shift(x, shift)            # arithmetic shift of int32
+            if neg:
+                want = np.negative(want.astype(np.int64))
+                want = ((want + 2 ** 31) % 2 ** 32 - 2 ** 31).astype(np.int32)
+            np.testing.assert_array_equal(got, want)
+
+
+@pytest.mark.parametrize("polarity", ["pos", "neg", "mixed"])
+def test_one_sided_rounding_bound(polarity):
+    """D = Y - exact: each positive term adds an error in (-1, 0], each negative
+    term one in [0, 1). So -n_pos < D <= 0 for positive weights and
+    0 <= D < n_neg for negative ones."""
+    rng = np.random.default_rng({"pos": 1, "neg": 2, "mixed": 3}[polarity])
+    N, C, H, W, K, r = 2, 6, 9, 9, 5, 3
+    x = rng.integers(-(2 ** 20), 2 ** 20, (N, C, H, W)).astype(np.int32)
+    shift = rng.integers(1, 15, (K, C * r * r)).astype(np.uint8)
+    if polarity == "pos":
+        sign = np.zeros_like(shift)
+    elif polarity == "neg":
+        sign = np.ones_like(shift)
+    else:
+        sign = rng.integers(0, 2, shift.shape).astype(np.uint8)
+    codes = (sign << 4 | shift).astype(np.uint8)
+    got = oracle.conv2d_shift(x, codes, None, r=r, stride=1, pad=1).astype(np.float64)
+    exact = torch_conv_f64(x, codes, None, r, r, 1, 1)
+    D = got - exact
+    ones = np.ones((N, C, H, W))
+    # n_pos / n_neg per output: count in-bounds positive / negative terms
+    ind_pos = np.where(sign == 0, 0, 15).astype(np.uint8)   # code 0 -> weight 1, 15 -> 0
+    ind_neg = np.where(sign == 1, 0, 15).astype(np.uint8)
+    n_pos = torch_conv_f64(ones, ind_pos, None, r, r, 1, 1)
+    n_neg = torch_conv_f64(ones, ind_neg, None, r, r, 1, 1)
+    assert np.all(D > -n_pos - 1e-9) and np.all(D < n_neg + 1e-9)
+    assert np.all((D <= 0) | (n_neg > 0)) and np.all((D >= 0) | (n_pos > 0))
+    if polarity == "pos":
+        assert np.all(D <= 0) and np.any(D < 0)
+    if polarity == "neg":
+        assert np.all(D >= 0) and np.any(D > 0)
+
+
+# ---------------------------------------------------------------------------
+# invariants
+
+
+def test_zero_codes_contribute_nothing():
+    rng = np.random.default_rng(5)
+    x = rng.integers(I32_MIN, I32_MAX, (2, 4, 6, 6), endpoint=True).astype(np.int32)
+    codes = (rng.integers(0, 2, (3, 36)) << 4 | 15).astype(np.uint8)
+    bias = rng.integers(I32_MIN, I32_MAX, 3, endpoint=True).astype(np.int32)
+    y = oracle.conv2d_shift(x, codes, bias, r=3, pad=1)
+    np.testing.assert_array_equal(y, np.broadcast_to(bias[None, :, None, None], y.shape))
+    y0 = oracle.conv2d_shift(x, codes, None, r=3, pad=1)
+    assert not y0.any()
+
+
+def test_sign_flip_negates_sum():
+    rng = np.random.default_rng(6)
+    x = rng.integers(I32_MIN // 4, I32_MAX // 4, (2, 5, 8, 8)).astype(np.int32)
+    codes = random_codes(rng, (4, 45), zero_frac=0.1)
+    bias = rng.integers(-(2 ** 20), 2 ** 20, 4).astype(np.int32)
+    flipped = codes ^ np.uint8(16)
+    y = oracle.conv2d_shift(x, codes, bias, r=3, pad=1).astype(np.int64)
+    yf = oracle.conv2d_shift(x, flipped, bias, r=3, pad=1).astype(np.int64)
+    b = bias[None, :, None, None].astype(np.int64)
+    lhs = (yf - b) % 2 ** 32
+    rhs = (-(y - b)) % 2 ** 32
+    np.testing.assert_array_equal(lhs, rhs)
+
+
+def test_linear_equals_1x1_conv():
+    rng = np.random.default_rng(8)
+    x = rng.integers(I32_MIN, I32_MAX, (5, 37), endpoint=True).astype(np.int32)
+    codes = random_codes(rng, (11, 37))
+    bias = rng.integers(I32_MIN, I32_MAX, 11, endpoint=True).astype(np.int32)
+    yl = oracle.linear_shift(x, codes, bias)
+    yc = oracle.conv2d_shift(x.reshape(5, 37, 1, 1), codes, bias, r=1)
+    np.testing.assert_array_equal(yl, yc.reshape(5, 11))
+
+
+def test_wraparound_extremes():
+    # p = 0 weights on extreme activations: the exact sum wraps modulo 2**32
+    x = np.array([[I32_MAX, I32_MAX, I32_MAX, I32_MIN, I32_MIN, 7]], np.int32)
+    codes = np.array([[0, 0, 0, 16, 16, 16],      # +,+,+,-,-,-
+                      [16, 16, 16, 0, 0, 0]], np.uint8)
+    bias = np.array([I32_MAX, I32_MIN], np.int32)
+    y = oracle.linear_shift(x, codes, bias)
+    s0 = I32_MAX + 3 * I32_MAX - 2 * I32_MIN - 7
+    s1 = I32_MIN - 3 * I32_MAX + 2 * I32_MIN + 7
+    assert y[0, 0] == wrap(s0) and y[0, 1] == wrap(s1)
+
+
+def test_points_agree_with_full():
+    rng = np.random.default_rng(9)
+    x = rng.integers(0, 2 ** 22, (2, 6, 11, 11)).astype(np.int32)
+    codes = random_codes(rng, (5, 6 * 9))
+    y = oracle.conv2d_shift(x, codes, None, r=3, stride=2, pad=1)
+    idx = rng.choice(y.size, 50, replace=False)
+    np.testing.assert_array_equal(
+        oracle.conv2d_shift_points(x, codes, None, idx, r=3, stride=2, pad=1), y.flat[idx])
+    xl = rng.integers(-(2 ** 22), 2 ** 22, (4, 33)).astype(np.int32)
+    cl = random_codes(rng, (7, 33))
+    bl = rng.integers(-99, 99, 7).astype(np.int32)
+    yl = oracle.linear_shift(xl, cl, bl)
+    idx = rng.choice(yl.size, 10, replace=False)
+    np.testing.assert_array_equal(oracle.linear_shift_points(xl, cl, bl, idx), yl.flat[idx])
+
+
+def test_mul_comparison_closed_form():
+    rng = np.random.default_rng(10)
+    x = rng.integers(-(2 ** 10), 2 ** 10, (2, 4, 9, 9)).astype(np.int32)
+    w = rng.integers(-(2 ** 10), 2 ** 10, (3, 36)).astype(np.int32)
+    b = rng.integers(-(2 ** 10), 2 ** 10, 3).astype(np.int32)
+    got = oracle.conv2d_mul(x, w, b, r=3, stride=2, pad=1)
+    want = F.conv2d(torch.from_numpy(x.astype(np.float64)),
+                    torch.from_numpy(w.reshape(3, 4, 3, 3).astype(np.float64)),
+                    torch.from_numpy(b.astype(np.float64)), stride=2, padding=1).numpy()
+    np.testing.assert_array_equal(got.astype(np.float64), want)
+    # products that overflow int32 wrap once, modulo 2**32
+    xb = np.full((1, 1, 1, 1), 2 ** 30, np.int32)
+    wb = np.full((1, 1), 8, np.int32)
+    assert oracle.conv2d_mul(xb, wb, None, r=1)[0, 0, 0, 0] == wrap(2 ** 33)
+
+
+# ---------------------------------------------------------------------------
+# packed layout, rebuilt from a little-endian bit stream
+
+
+def bitstream_pack(codes):
+    rows, cols = codes.shape
+    wpr = (cols + 5) // 6
+    out = np.zeros((rows, wpr), np.uint32)
+    for r in range(rows):
+        padded = np.full(wpr * 6, 15, np.uint8)
+        padded[:cols] = codes[r]
+        bits = []
+        for w in range(wpr):
+            for j in range(6):
+                v = int(padded[w * 6 + j])
+                bits += [(v >> b) & 1 for b in range(5)]
+            bits += [0, 0]                      # bits 30 and 31
+        by = np.packbits(np.array(bits, np.uint8), bitorder="little")
+        out[r] = by.view("<u4")
+    return out
+
+
+def test_pack_layout_bitstream():
+    rng = np.random.default_rng(12)
+    for cols in (1, 5, 6, 7, 12, 13, 147, 576):
+        codes = rng.integers(0, 32, (3, cols)).astype(np.uint8)
+        got = oracle.pack_codes(codes)
+        np.testing.assert_array_equal(got, bitstream_pack(codes))
+        assert not np.any(got >> 30)
+        np.testing.assert_array_equal(oracle.unpack_codes(got, cols), codes)
+
+
+def test_pack_literal_words():
+    # codes 1..6 in one word: 1 + 2*2^5 + 3*2^10 + 4*2^15 + 5*2^20 + 6*2^25
+    assert oracle.pack_codes(np.array([[1, 2, 3, 4, 5, 6]], np.uint8))[0, 0] == 0x0C520C41
+    # one code 31 then five padding codes 15: 31 + 15*(2^5+2^10+2^15+2^20+2^25)
+    assert oracle.pack_codes(np.array([[31]], np.uint8))[0, 0] == 0x1EF7BDFF
