@@ -1,0 +1,143 @@
+/*
+ * deepshift.h -- C ABI of the DeepShift shift-operator library for AMD
+ * Instinct MI355X (gfx950).
+ *
+ * The library computes the inference forward pass of the two DeepShift
+ * operators, LinearShift and ConvShift (Elhoushi et al., "DeepShift: Towards
+ * Multiplication-Less Neural Networks", Section 3). Every weight is
+ * flip(2^p, s) (Eq. 3): a power of two p in {0, -1, ..., -14} and a ternary
+ * sign s in {-1, 0, +1} (Eq. 2), stored in 5 bits (Section 4). Activations
+ * and bias are fixed point (Section 4 uses 32 bits with 16 fractional bits).
+ * Each multiply-accumulate becomes an arithmetic right shift, an optional
+ * negation and an integer add (Figure 1a, Eq. 1).
+ *
+ * Exact semantics of one term (the readings this library takes where the
+ * paper is silent):
+ *     term(x, code) = 0                       if shift_code == 15
+ *                   = -(x >> shift_code)      if sign bit set
+ *                   =  (x >> shift_code)      otherwise
+ * where ">>" is the arithmetic (flooring) right shift of a signed int32, and
+ * outputs are  y = bias + sum of terms, computed modulo 2^32 (two's
+ * complement wrap-around of int32). The result does not depend on the
+ * number of fractional bits F: every weight is a dimensionless power of two
+ * <= 1, so y carries the same F as x and bias.
+ *
+ * Weight codes (unpacked form, one uint8 per weight):
+ *     bit 4    sign (1 = negative)
+ *     bits 0-3 shift code: 0..14 means p = -code, 15 means a zero weight
+ *              (whatever the sign bit)
+ *     bits 5-7 must be 0
+ * Packed form (what the compute entry points read): each weight row is
+ * stored in ds_packed_row_words(cols) uint32 words, six codes per word, code
+ * j of a word in bits [5j, 5j+5), bits 30-31 zero, and the last word of a row
+ * filled up with code 15. Rows follow each other with no gap.
+ *
+ * Ownership and memory: the caller owns every buffer. Compute entry points
+ * take device pointers on the current HIP device; the pack/unpack helpers
+ * take host pointers. y must not overlap any input. The compute entry points
+ * allocate device scratch memory (decoded weights) in stream order from a
+ * library-owned memory pool and free it in stream order.
+ *
+ * Errors: arguments are validated before any device work. On a validation
+ * error nothing is written and nothing is launched. Compute entry points are
+ * asynchronous with respect to the host: they enqueue work on `stream`
+ * (a hipStream_t; NULL = the default stream) and return. A failure reported
+ * by the HIP runtime while enqueueing returns DS_ERR_HIP;
+ * ds_last_error_message() then describes it. No exception crosses the ABI.
+ */
+#ifndef DEEPSHIFT_H
+#define DEEPSHIFT_H
+
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef enum ds_status {
+    DS_SUCCESS = 0,
+    DS_ERR_NULL_POINTER = 1,     /* a required pointer is NULL */
+    DS_ERR_INVALID_SHAPE = 2,    /* a size is <= 0, or an output size would be <= 0 */
+    DS_ERR_INVALID_ARG = 3,      /* bad stride/pad/frac_bits/flags, overlap, or a
+                                    buffer that is not device memory of the size needed */
+    DS_ERR_BUFFER_TOO_SMALL = 4, /* a host output buffer is shorter than required */
+    DS_ERR_INVALID_CODE = 5,     /* a weight code >= 32 */
+    DS_ERR_HIP = 6,              /* the HIP runtime reported an error */
+    DS_ERR_UNSUPPORTED = 7       /* a tensor has 2^31 or more elements */
+} ds_status;
+
+/* Number of uint32 words one packed row of `cols` codes occupies:
+ * ceil(cols / 6). Returns -1 when cols <= 0. */
+int64_t ds_packed_row_words(int64_t cols);
+
+/* Pack host codes [rows][cols] (uint8, layout above) into host words
+ * [rows][ds_packed_row_words(cols)] (the 5-bit weight format of Section 4).
+ * packed_words is the capacity of `packed` in words.
+ * Errors: NULL pointer, rows/cols <= 0, capacity too small, any code >= 32
+ * (DS_ERR_INVALID_CODE, nothing written). */
+ds_status ds_pack_shift_weights(const uint8_t *codes, int64_t rows, int64_t cols,
+                                uint32_t *packed, int64_t packed_words);
+
+/* Inverse of ds_pack_shift_weights (host memory). codes_len is the capacity
+ * of `codes` in bytes. Words with bits 30-31 set give DS_ERR_INVALID_CODE. */
+ds_status ds_unpack_shift_weights(const uint32_t *packed, int64_t rows, int64_t cols,
+                                  uint8_t *codes, int64_t codes_len);
+
+/* LinearShift forward (Section 3, Y = W~ X + b with W~ = flip(2^P, S), Eq. 3):
+ *     y[b][o] = bias[o] + sum_i term(x[b][i], code[o][i])    (mod 2^32)
+ * x        device int32 [batch][in_features], fixed point with frac_bits F
+ * w_packed device uint32 [out_features][ds_packed_row_words(in_features)]
+ * bias     device int32 [out_features] with the same F, or NULL for none
+ * y        device int32 [batch][out_features], written (not accumulated)
+ * frac_bits in [0, 31]: the F of x, bias and y (validated, not used by the math)
+ * flags    reserved, must be 0
+ * stream   hipStream_t to enqueue on (NULL = default stream) */
+ds_status ds_linear_shift(const int32_t *x, const uint32_t *w_packed, const int32_t *bias,
+                          int32_t *y, int64_t batch, int64_t in_features, int64_t out_features,
+                          int32_t frac_bits, uint32_t flags, void *stream);
+
+/* ConvShift forward (Section 3, Y = W~ (*) X + b; Figure 1c), a 2-D
+ * cross-correlation with zero padding, as an ordinary convolution layer:
+ *     y[n][k][oh][ow] = bias[k] + sum_{c,r,s} term(x[n][c][ih][iw], code[k][c][r][s])
+ *     ih = oh*stride_h - pad_h + r,  iw = ow*stride_w - pad_w + s
+ * (positions outside the input contribute nothing), modulo 2^32.
+ * x        device int32 [n][c][h][w] (NCHW), fixed point with frac_bits F
+ * w_packed device uint32 [k][ds_packed_row_words(c*r*s)]; weight row k holds
+ *          the codes in (c, r, s) order, s fastest
+ * bias     device int32 [k] or NULL
+ * y        device int32 [n][k][oh][ow],
+ *          oh = (h + 2*pad_h - r)/stride_h + 1, ow = (w + 2*pad_w - s)/stride_w + 1
+ * stride_* >= 1, pad_* >= 0; frac_bits, flags, stream as for ds_linear_shift. */
+ds_status ds_conv2d_shift(const int32_t *x, const uint32_t *w_packed, const int32_t *bias,
+                          int32_t *y, int64_t n, int64_t c, int64_t h, int64_t w,
+                          int64_t k, int64_t r, int64_t s,
+                          int32_t stride_h, int32_t stride_w, int32_t pad_h, int32_t pad_w,
+                          int32_t frac_bits, uint32_t flags, void *stream);
+
+/* Multiplication-based comparison operators. Not part of DeepShift: they run
+ * the same tiling as the shift operators with a 32-bit integer multiply in
+ * place of the shift, so that the two inner loops can be timed side by side
+ * (the paper compares its shift kernels with a multiplication-based kernel,
+ * Section 6, GPU implementation). Weights are plain int32 [k][c*r*s]
+ * (or [out][in]) on the device:
+ *     y = bias + sum x * w    (products and sum modulo 2^32) */
+ds_status ds_conv2d_mul_i32(const int32_t *x, const int32_t *w, const int32_t *bias,
+                            int32_t *y, int64_t n, int64_t c, int64_t h, int64_t w_,
+                            int64_t k, int64_t r, int64_t s,
+                            int32_t stride_h, int32_t stride_w, int32_t pad_h, int32_t pad_w,
+                            uint32_t flags, void *stream);
+ds_status ds_linear_mul_i32(const int32_t *x, const int32_t *w, const int32_t *bias, int32_t *y,
+                            int64_t batch, int64_t in_features, int64_t out_features,
+                            uint32_t flags, void *stream);
+
+/* Static text for a status code. */
+const char *ds_status_string(ds_status status);
+
+/* Detail of the last error returned on the calling thread ("" if none). */
+const char *ds_last_error_message(void);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* DEEPSHIFT_H */

@@ -1,0 +1,77 @@
+"""ctypes binding of ``libdeepshift.so`` (the C ABI declared in include/deepshift.h).
+
+The functions keep the C names and arguments; they only convert Python values
+to C types and turn a non-zero status into ``DeepShiftError``. Loading builds
+the library first when it has not been built yet.
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+import threading
+
+from . import build as _build
+
+_lock = threading.Lock()
+_lib = None
+
+_P = ctypes.c_void_p
+_I64 = ctypes.c_int64
+_I32 = ctypes.c_int32
+_U32 = ctypes.c_uint32
+
+SIGNATURES = {
+    "ds_packed_row_words": (_I64, [_I64]),
+    "ds_pack_shift_weights": (ctypes.c_int, [_P, _I64, _I64, _P, _I64]),
+    "ds_unpack_shift_weights": (ctypes.c_int, [_P, _I64, _I64, _P, _I64]),
+    "ds_linear_shift": (ctypes.c_int, [_P, _P, _P, _P, _I64, _I64, _I64, _I32, _U32, _P]),
+    "ds_conv2d_shift": (ctypes.c_int, [_P, _P, _P, _P] + [_I64] * 7 + [_I32] * 4 + [_I32, _U32, _P]),
+    "ds_conv2d_mul_i32": (ctypes.c_int, [_P, _P, _P, _P] + [_I64] * 7 + [_I32] * 4 + [_U32, _P]),
+    "ds_linear_mul_i32": (ctypes.c_int, [_P, _P, _P, _P, _I64, _I64, _I64, _U32, _P]),
+    "ds_status_string": (ctypes.c_char_p, [ctypes.c_int]),
+    "ds_last_error_message": (ctypes.c_char_p, []),
+}
+
+STATUS = {
+    0: "DS_SUCCESS", 1: "DS_ERR_NULL_POINTER", 2: "DS_ERR_INVALID_SHAPE",
+    3: "DS_ERR_INVALID_ARG", 4: "DS_ERR_BUFFER_TOO_SMALL", 5: "DS_ERR_INVALID_CODE",
+    6: "DS_ERR_HIP", 7: "DS_ERR_UNSUPPORTED",
+}
+
+
+class DeepShiftError(RuntimeError):
+    def __init__(self, status: int, message: str):
+        super().__init__(f"{STATUS.get(status, status)}: {message}")
+        self.status = status
+        self.name = STATUS.get(status, str(status))
+
+
+def library_path() -> str:
+    return _build.LIB
+
+
+def lib():
+    """The loaded library (built on first use when no build exists)."""
+    global _lib
+    with _lock:
+        if _lib is None:
+            if not os.path.exists(_build.LIB):
+                _build.build()
+            handle = ctypes.CDLL(_build.LIB)
+            for name, (res, args) in SIGNATURES.items():
+                fn = getattr(handle, name)
+                fn.restype = res
+                fn.argtypes = args
+            _lib = handle
+    return _lib
+
+
+def check(status: int) -> None:
+    if status != 0:
+        msg = lib().ds_last_error_message().decode()
+        raise DeepShiftError(status, msg)
+
+
+def call(name: str, *args) -> None:
+    """Call a status-returning entry point and raise on failure."""
+    check(getattr(lib(), name)(*args))

@@ -1,0 +1,124 @@
+// Entry points of the shift operators (DeepShift Section 3, LinearShift and
+// ConvShift) and their argument checks. LinearShift runs as a ConvShift with
+// H = W = R = S = 1: x [batch][in] is x [n][c][1][1] and y [batch][out] is
+// y [n][k][1][1], so both operators share every kernel.
+#include <hip/hip_runtime.h>
+
+#include "common.hpp"
+#include "conv_plan.hpp"
+
+namespace ds {
+
+bool device_range_ok(const void *p, int64_t bytes)
+{
+    hipDeviceptr_t base = nullptr;
+    size_t size = 0;
+    if (hipMemGetAddressRange(&base, &size, const_cast<void *>(p)) != hipSuccess) {
+        (void)hipGetLastError();  // clear the sticky error of a failed lookup
+        return false;
+    }
+    auto b = reinterpret_cast<uintptr_t>(base), q = reinterpret_cast<uintptr_t>(p);
+    return q >= b && q - b + uint64_t(bytes) <= uint64_t(size);
+}
+
+// Validates a convolution problem (both operators) and fills `g`.
+static ds_status check_conv(const void *x, const void *wts, const void *bias, const void *y,
+                            int64_t n, int64_t c, int64_t h, int64_t w, int64_t k, int64_t r,
+                            int64_t s, int32_t sh, int32_t sw, int32_t ph, int32_t pw,
+                            int32_t frac_bits, uint32_t flags, bool packed, ConvGeom &g)
+{
+    if (!x || !wts || !y) return fail(DS_ERR_NULL_POINTER, "x, weights and y must not be NULL");
+    if (n <= 0 || c <= 0 || h <= 0 || w <= 0 || k <= 0 || r <= 0 || s <= 0)
+        return fail(DS_ERR_INVALID_SHAPE, "all sizes must be > 0");
+    if (sh < 1 || sw < 1) return fail(DS_ERR_INVALID_ARG, "stride must be >= 1");
+    if (ph < 0 || pw < 0) return fail(DS_ERR_INVALID_ARG, "padding must be >= 0");
+    if (frac_bits < 0 || frac_bits > 31) return fail(DS_ERR_INVALID_ARG, "frac_bits must be in [0, 31]");
+    if (flags != 0) return fail(DS_ERR_INVALID_ARG, "flags must be 0");
+    if (h + 2 * int64_t(ph) < r || w + 2 * int64_t(pw) < s)
+        return fail(DS_ERR_INVALID_SHAPE, "kernel larger than the padded input");
+    const int64_t oh = (h + 2 * int64_t(ph) - r) / sh + 1;
+    const int64_t ow = (w + 2 * int64_t(pw) - s) / sw + 1;
+    const int64_t crs = prod({c, r, s});
+    const int64_t xe = prod({n, c, h, w}), ye = prod({n, k, oh, ow});
+    const int64_t we = packed ? prod({k, row_words(crs)}) : prod({k, crs});
+    if (crs < 0 || xe < 0 || ye < 0 || we < 0 || crs > kMaxElems || xe > kMaxElems ||
+        ye > kMaxElems || we > kMaxElems || prod({k, crs}) > kMaxElems)
+        return fail(DS_ERR_UNSUPPORTED, "tensors with 2^31 or more elements are not supported");
+    const int64_t xb = 4 * xe, yb = 4 * ye, wb = 4 * we, bb = 4 * k;
+    if (overlap(y, yb, x, xb) || overlap(y, yb, wts, wb) || overlap(y, yb, bias, bb))
+        return fail(DS_ERR_INVALID_ARG, "y overlaps an input");
+    if (!device_range_ok(x, xb)) return fail(DS_ERR_INVALID_ARG, "x is not a device buffer of %lld bytes", (long long)xb);
+    if (!device_range_ok(wts, wb)) return fail(DS_ERR_INVALID_ARG, "weights are not a device buffer of %lld bytes", (long long)wb);
+    if (!device_range_ok(y, yb)) return fail(DS_ERR_INVALID_ARG, "y is not a device buffer of %lld bytes", (long long)yb);
+    if (bias && !device_range_ok(bias, bb)) return fail(DS_ERR_INVALID_ARG, "bias is not a device buffer of %lld bytes", (long long)bb);
+    g = ConvGeom{int(n), int(c), int(h), int(w), int(k), int(r), int(s), sh, sw, ph, pw,
+                 int(oh), int(ow), int(crs)};
+    return DS_SUCCESS;
+}
+
+static ds_status hip_status(hipError_t e, const char *what)
+{
+    if (e == hipSuccess) return ok();
+    return fail(DS_ERR_HIP, "%s: %s", what, hipGetErrorString(e));
+}
+
+}  // namespace ds
+
+using namespace ds;
+
+extern "C" ds_status ds_conv2d_shift(const int32_t *x, const uint32_t *w_packed, const int32_t *bias,
+                                     int32_t *y, int64_t n, int64_t c, int64_t h, int64_t w,
+                                     int64_t k, int64_t r, int64_t s, int32_t stride_h,
+                                     int32_t stride_w, int32_t pad_h, int32_t pad_w,
+                                     int32_t frac_bits, uint32_t flags, void *stream)
+{
+    ConvGeom g;
+    ds_status st = check_conv(x, w_packed, bias, y, n, c, h, w, k, r, s, stride_h, stride_w,
+                              pad_h, pad_w, frac_bits, flags, true, g);
+    if (st != DS_SUCCESS) return st;
+    return hip_status(run_conv(g, x, w_packed, nullptr, bias, y, Inner::Shift,
+                               static_cast<hipStream_t>(stream)),
+                      "ds_conv2d_shift");
+}
+
+extern "C" ds_status ds_linear_shift(const int32_t *x, const uint32_t *w_packed, const int32_t *bias,
+                                     int32_t *y, int64_t batch, int64_t in_features,
+                                     int64_t out_features, int32_t frac_bits, uint32_t flags,
+                                     void *stream)
+{
+    ConvGeom g;
+    ds_status st = check_conv(x, w_packed, bias, y, batch, in_features, 1, 1, out_features, 1, 1,
+                              1, 1, 0, 0, frac_bits, flags, true, g);
+    if (st != DS_SUCCESS) return st;
+    return hip_status(run_conv(g, x, w_packed, nullptr, bias, y, Inner::Shift,
+                               static_cast<hipStream_t>(stream)),
+                      "ds_linear_shift");
+}
+
+extern "C" ds_status ds_conv2d_mul_i32(const int32_t *x, const int32_t *wts, const int32_t *bias,
+                                       int32_t *y, int64_t n, int64_t c, int64_t h, int64_t w,
+                                       int64_t k, int64_t r, int64_t s, int32_t stride_h,
+                                       int32_t stride_w, int32_t pad_h, int32_t pad_w,
+                                       uint32_t flags, void *stream)
+{
+    ConvGeom g;
+    ds_status st = check_conv(x, wts, bias, y, n, c, h, w, k, r, s, stride_h, stride_w, pad_h,
+                              pad_w, 0, flags, false, g);
+    if (st != DS_SUCCESS) return st;
+    return hip_status(run_conv(g, x, nullptr, wts, bias, y, Inner::Mul,
+                               static_cast<hipStream_t>(stream)),
+                      "ds_conv2d_mul_i32");
+}
+
+extern "C" ds_status ds_linear_mul_i32(const int32_t *x, const int32_t *wts, const int32_t *bias,
+                                       int32_t *y, int64_t batch, int64_t in_features,
+                                       int64_t out_features, uint32_t flags, void *stream)
+{
+    ConvGeom g;
+    ds_status st = check_conv(x, wts, bias, y, batch, in_features, 1, 1, out_features, 1, 1, 1,
+                              1, 0, 0, 0, flags, false, g);
+    if (st != DS_SUCCESS) return st;
+    return hip_status(run_conv(g, x, nullptr, wts, bias, y, Inner::Mul,
+                               static_cast<hipStream_t>(stream)),
+                      "ds_linear_mul_i32");
+}

@@ -1,0 +1,130 @@
+"""PyTorch-facing wrappers of the C ABI.
+
+PyTorch provides the device memory and the stream; every computation runs in
+the HIP library. Tensors must be contiguous int32 CUDA (ROCm) tensors; packed
+weights are int32 tensors holding the uint32 words bit for bit.
+"""
+from __future__ import annotations
+
+import numpy as np
+import torch
+
+from ._native import DeepShiftError, call, lib
+
+__all__ = ["DeepShiftError", "packed_row_words", "pack_shift_weights", "unpack_shift_weights",
+           "linear_shift", "conv2d_shift", "linear_mul_i32", "conv2d_mul_i32", "out_size"]
+
+
+def packed_row_words(cols: int) -> int:
+    return int(lib().ds_packed_row_words(int(cols)))
+
+
+def pack_shift_weights(codes) -> np.ndarray:
+    """Host codes [rows, cols] (uint8, sign << 4 | shift) -> packed words [rows, ceil(cols/6)]."""
+    codes = np.ascontiguousarray(codes, dtype=np.uint8)
+    if codes.ndim != 2:
+        codes = codes.reshape(codes.shape[0], -1)
+    rows, cols = codes.shape
+    out = np.empty((rows, max(packed_row_words(cols), 0)), dtype=np.uint32)
+    call("ds_pack_shift_weights", codes.ctypes.data, rows, cols, out.ctypes.data, out.size)
+    return out
+
+
+def unpack_shift_weights(packed, cols: int) -> np.ndarray:
+    packed = np.ascontiguousarray(packed, dtype=np.uint32)
+    rows = packed.shape[0]
+    out = np.empty((rows, cols), dtype=np.uint8)
+    call("ds_unpack_shift_weights", packed.ctypes.data, rows, cols, out.ctypes.data, out.size)
+    return out
+
+
+def _dev_i32(t: torch.Tensor, name: str) -> torch.Tensor:
+    if not isinstance(t, torch.Tensor) or not t.is_cuda:
+        raise TypeError(f"{name} must be a device tensor")
+    if t.dtype not in (torch.int32, torch.uint32):
+        raise TypeError(f"{name} must be int32, got {t.dtype}")
+    if not t.is_contiguous():
+        raise ValueError(f"{name} must be contiguous")
+    return t
+
+
+def _ptr(t):
+    return None if t is None else t.data_ptr()
+
+
+def _stream(dev: torch.device) -> int:
+    return torch.cuda.current_stream(dev).cuda_stream
+
+
+def out_size(size: int, pad: int, k: int, stride: int) -> int:
+    return (size + 2 * pad - k) // stride + 1
+
+
+def _pair(v):
+    return (int(v), int(v)) if np.isscalar(v) else (int(v[0]), int(v[1]))
+
+
+def linear_shift(x: torch.Tensor, w_packed: torch.Tensor, bias: torch.Tensor | None = None,
+                 frac_bits: int = 16, out: torch.Tensor | None = None) -> torch.Tensor:
+    """LinearShift: y[b, o] = bias[o] + sum_i term(x[b, i], code[o, i]) (int32, mod 2^32)."""
+    _dev_i32(x, "x"); _dev_i32(w_packed, "w_packed")
+    if bias is not None:
+        _dev_i32(bias, "bias")
+    batch, fin = x.shape
+    fout = w_packed.shape[0]
+    y = out if out is not None else torch.empty((batch, fout), dtype=torch.int32, device=x.device)
+    _dev_i32(y, "out")
+    with torch.cuda.device(x.device):
+        call("ds_linear_shift", _ptr(x), _ptr(w_packed), _ptr(bias), _ptr(y), batch, fin, fout,
+             frac_bits, 0, _stream(x.device))
+    return y
+
+
+def conv2d_shift(x: torch.Tensor, w_packed: torch.Tensor, bias: torch.Tensor | None,
+                 kernel_size, stride=1, padding=0, frac_bits: int = 16,
+                 out: torch.Tensor | None = None) -> torch.Tensor:
+    """ConvShift (NCHW): y[n, k, oh, ow] = bias[k] + sum_{c,r,s} term(x[...], code[k, c, r, s])."""
+    _dev_i32(x, "x"); _dev_i32(w_packed, "w_packed")
+    if bias is not None:
+        _dev_i32(bias, "bias")
+    r, s = _pair(kernel_size)
+    sh, sw = _pair(stride)
+    ph, pw = _pair(padding)
+    n, c, h, w = x.shape
+    k = w_packed.shape[0]
+    oh, ow = out_size(h, ph, r, sh), out_size(w, pw, s, sw)
+    y = out if out is not None else torch.empty((n, k, max(oh, 0), max(ow, 0)), dtype=torch.int32,
+                                                device=x.device)
+    _dev_i32(y, "out")
+    with torch.cuda.device(x.device):
+        call("ds_conv2d_shift", _ptr(x), _ptr(w_packed), _ptr(bias), _ptr(y), n, c, h, w, k, r, s,
+             sh, sw, ph, pw, frac_bits, 0, _stream(x.device))
+    return y
+
+
+def linear_mul_i32(x, w, bias=None, out=None):
+    """Multiplication-based comparison: y = bias + x @ w.T (int32, mod 2^32)."""
+    _dev_i32(x, "x"); _dev_i32(w, "w")
+    batch, fin = x.shape
+    fout = w.shape[0]
+    y = out if out is not None else torch.empty((batch, fout), dtype=torch.int32, device=x.device)
+    with torch.cuda.device(x.device):
+        call("ds_linear_mul_i32", _ptr(x), _ptr(w), _ptr(bias), _ptr(y), batch, fin, fout, 0,
+             _stream(x.device))
+    return y
+
+
+def conv2d_mul_i32(x, w, bias, kernel_size, stride=1, padding=0, out=None):
+    """Multiplication-based comparison convolution with int32 weights [K, C*R*S]."""
+    _dev_i32(x, "x"); _dev_i32(w, "w")
+    r, s = _pair(kernel_size)
+    sh, sw = _pair(stride)
+    ph, pw = _pair(padding)
+    n, c, h, wd = x.shape
+    k = w.shape[0]
+    oh, ow = out_size(h, ph, r, sh), out_size(wd, pw, s, sw)
+    y = out if out is not None else torch.empty((n, k, oh, ow), dtype=torch.int32, device=x.device)
+    with torch.cuda.device(x.device):
+        call("ds_conv2d_mul_i32", _ptr(x), _ptr(w), _ptr(bias), _ptr(y), n, c, h, wd, k, r, s,
+             sh, sw, ph, pw, 0, _stream(x.device))
+    return y

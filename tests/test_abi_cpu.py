@@ -1,0 +1,145 @@
+"""C-ABI checks that need no GPU: symbols, packing, and argument validation.
+
+Validation runs before any device access, so NULL pointers, bad shapes and
+bad arguments are rejected here with the documented status and nothing is
+written. Compute calls themselves need a GPU and live in the gpu suite.
+"""
+import ctypes
+import os
+import re
+
+import numpy as np
+import pytest
+
+import oracle
+from paper_1905_13298_amd import _native, ops
+from paper_1905_13298_amd.workloads import random_codes
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+HEADER = os.path.join(ROOT, "include", "deepshift.h")
+
+OK, NULLP, SHAPE, ARG, SMALL, CODE, HIP, UNSUP = range(8)
+FAKE = 0x10000  # never dereferenced: every case below fails validation first
+
+
+def declared_functions():
+    text = open(HEADER).read()
+    text = re.sub(r"/\*.*?\*/", "", text, flags=re.S)
+    return sorted(set(re.findall(r"\b(ds_\w+)\s*\(", text)))
+
+
+def test_header_symbols_exported():
+    names = declared_functions()
+    assert len(names) >= 9
+    lib = ctypes.CDLL(_native.library_path())
+    for name in names:
+        assert hasattr(lib, name), name
+    assert set(names) == set(_native.SIGNATURES)
+
+
+def test_status_strings():
+    lib = _native.lib()
+    seen = set()
+    for st in range(8):
+        s = lib.ds_status_string(st).decode()
+        assert s and s != "unknown status"
+        seen.add(s)
+    assert len(seen) == 8
+    assert lib.ds_status_string(99).decode() == "unknown status"
+
+
+def test_packed_row_words():
+    lib = _native.lib()
+    for cols, words in [(1, 1), (6, 1), (7, 2), (12, 2), (13, 3), (147, 25), (4096, 683)]:
+        assert lib.ds_packed_row_words(cols) == words
+    assert lib.ds_packed_row_words(0) == -1 and lib.ds_packed_row_words(-5) == -1
+
+
+@pytest.mark.parametrize("cols", [1, 5, 6, 7, 13, 64, 147, 576, 1152, 4096])
+def test_pack_matches_oracle_layout(cols):
+    rng = np.random.default_rng(cols)
+    codes = rng.integers(0, 32, (5, cols)).astype(np.uint8)
+    got = ops.pack_shift_weights(codes)
+    np.testing.assert_array_equal(got, oracle.pack_codes(codes))
+    np.testing.assert_array_equal(ops.unpack_shift_weights(got, cols), codes)
+
+
+def test_pack_errors_write_nothing():
+    lib = _native.lib()
+    codes = np.zeros((2, 7), np.uint8)
+    out = np.full(4, 0xDEADBEEF, np.uint32)
+    p, o = codes.ctypes.data, out.ctypes.data
+    assert lib.ds_pack_shift_weights(None, 2, 7, o, 4) == NULLP
+    assert lib.ds_pack_shift_weights(p, 2, 7, None, 4) == NULLP
+    assert lib.ds_pack_shift_weights(p, 0, 7, o, 4) == SHAPE
+    assert lib.ds_pack_shift_weights(p, 2, -1, o, 4) == SHAPE
+    assert lib.ds_pack_shift_weights(p, 2, 7, o, 3) == SMALL
+    codes[1, 6] = 32
+    assert lib.ds_pack_shift_weights(p, 2, 7, o, 4) == CODE
+    assert "32" in lib.ds_last_error_message().decode()
+    assert np.all(out == 0xDEADBEEF)
+    codes[1, 6] = 31
+    assert lib.ds_pack_shift_weights(p, 2, 7, o, 4) == OK
+    assert lib.ds_last_error_message().decode() == ""
+
+
+def test_unpack_errors():
+    lib = _native.lib()
+    words = np.array([[0x0C520C41]], np.uint32)
+    out = np.full(6, 0xAA, np.uint8)
+    assert lib.ds_unpack_shift_weights(words.ctypes.data, 1, 6, out.ctypes.data, 5) == SMALL
+    bad = np.array([[1 << 30]], np.uint32)
+    assert lib.ds_unpack_shift_weights(bad.ctypes.data, 1, 6, out.ctypes.data, 6) == CODE
+    assert np.all(out == 0xAA)
+    assert lib.ds_unpack_shift_weights(words.ctypes.data, 1, 6, out.ctypes.data, 6) == OK
+    np.testing.assert_array_equal(out, [1, 2, 3, 4, 5, 6])
+
+
+def conv(**kw):
+    a = dict(x=FAKE, w=FAKE + 4096, b=None, y=FAKE + 8192, n=1, c=2, h=5, wd=5, k=3, r=3, s=3,
+             sh=1, sw=1, ph=1, pw=1, f=16, flags=0)
+    a.update(kw)
+    return _native.lib().ds_conv2d_shift(a["x"], a["w"], a["b"], a["y"], a["n"], a["c"], a["h"],
+                                          a["wd"], a["k"], a["r"], a["s"], a["sh"], a["sw"],
+                                          a["ph"], a["pw"], a["f"], a["flags"], None)
+
+
+def test_conv_validation_codes():
+    assert conv(x=None) == NULLP
+    assert conv(w=None) == NULLP
+    assert conv(y=None) == NULLP
+    for key in ("n", "c", "h", "wd", "k", "r", "s"):
+        assert conv(**{key: 0}) == SHAPE, key
+        assert conv(**{key: -2}) == SHAPE, key
+    assert conv(r=9, ph=1) == SHAPE           # kernel larger than padded input
+    assert conv(sh=0) == ARG and conv(sw=-1) == ARG
+    assert conv(ph=-1) == ARG
+    assert conv(f=-1) == ARG and conv(f=32) == ARG
+    assert conv(flags=1) == ARG
+    assert conv(n=1 << 20, c=1 << 12, h=1, wd=1) == UNSUP
+    assert conv(k=1 << 17, c=1 << 14, r=1, s=1, ph=0, pw=0) == UNSUP
+    # y overlapping x
+    assert conv(y=FAKE + 4) == ARG
+    assert "overlap" in _native.lib().ds_last_error_message().decode()
+
+
+def test_linear_and_mul_validation_codes():
+    lib = _native.lib()
+    assert lib.ds_linear_shift(None, FAKE, None, FAKE * 4, 2, 3, 4, 16, 0, None) == NULLP
+    assert lib.ds_linear_shift(FAKE, FAKE * 2, None, FAKE * 4, 0, 3, 4, 16, 0, None) == SHAPE
+    assert lib.ds_linear_shift(FAKE, FAKE * 2, None, FAKE * 4, 2, 3, 4, 40, 0, None) == ARG
+    assert lib.ds_linear_shift(FAKE, FAKE * 2, None, FAKE * 4, 2, 3, 4, 16, 2, None) == ARG
+    assert lib.ds_linear_mul_i32(FAKE, None, None, FAKE * 4, 2, 3, 4, 0, None) == NULLP
+    assert lib.ds_conv2d_mul_i32(FAKE, FAKE * 2, None, FAKE * 4, 1, 1, 4, 4, 1, 3, 3,
+                                 0, 1, 0, 0, 0, None) == ARG
+
+
+def test_host_pointers_rejected_without_gpu_access():
+    """Host memory is not a device buffer: DS_ERR_INVALID_ARG (HIP lookup fails)."""
+    x = np.zeros((2, 4), np.int32)
+    w = ops.pack_shift_weights(random_codes(np.random.default_rng(0), (3, 4)))
+    y = np.full((2, 3), 7, np.int32)
+    st = _native.lib().ds_linear_shift(x.ctypes.data, w.ctypes.data, None, y.ctypes.data,
+                                        2, 4, 3, 16, 0, None)
+    assert st in (ARG, HIP)
+    assert np.all(y == 7)
