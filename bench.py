@@ -1,0 +1,267 @@
+"""Benchmark of the DeepShift shift operators on one MI355X.
+
+A step is one pass of every layer of the workload (each layer's ConvShift or
+LinearShift call on its own seeded input, all inputs resident in HBM).
+Prints ONE JSON line:
+  value       whole-step throughput in G shift-accumulates/s (dense SAC =
+              output elements x reduction terms, zero weights included)
+  roofline    the dominant kernel against the int32 VALU roofline
+              (2 VALU instructions per shift-accumulate)
+  cpu_baseline the oracle on the host cores, on a prefix (small batch) of
+              the same seeded inputs
+  mul_i32     the multiplication-based comparison kernel (same tiling) on the
+              same layers
+
+Usage: python bench.py [--gpus 1] [--steps K] [--warmup W] [--workload resnet50]
+"""
+from __future__ import annotations
+
+import argparse
+import json
+import os
+import sys
+import time
+
+import numpy as np
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+WORKLOADS = {"linear_small": 0, "conv_single": 1, "linear_fc6": 2, "resnet18": 3, "resnet50": 4}
+
+# MI355X: 256 CUs, 4 SIMD16 per CU -> 64 int32 lane-ops per clock per CU, 2.4 GHz peak clock.
+CUS, LANES_PER_CU, CLOCK_GHZ = 256, 64, 2.4
+INT32_OPS_PEAK_T = CUS * LANES_PER_CU * CLOCK_GHZ / 1000.0        # 39.32 T int32 ops/s
+SAC_PEAK_T = INT32_OPS_PEAK_T / 2.0                                  # 19.66 T SAC/s
+HBM_PEAK_GBS = 8000.0
+
+
+def kernel_variant(layer) -> str:
+    """The tiled-kernel instance the library's planner picks for a layer (mirrors
+    run_conv in conv_kernels.hip): staging mode, pixels per lane, chunk, taps."""
+    if layer.kind == "linear" or (layer.h == 1 and layer.w == 1 and layer.r == 1 and layer.s == 1
+                                  and layer.pad == 0):
+        return "rowmajor_tm4_cc16"
+    if layer.r == 1 and layer.s == 1 and layer.pad == 0:
+        return "point_tm8_cc8"
+    tm = 4 if layer.s == 7 else 8
+    P = 64 * tm
+    VH, IWP = layer.h + 2 * layer.pad, layer.w + 2 * layer.pad
+    ohow = layer.oh * layer.ow
+    nq = layer.n * ohow
+    best = 0
+    for q0 in range(0, nq, P):
+        ql = min(q0 + P, nq) - 1
+        v0 = (q0 // ohow) * VH + ((q0 % ohow) // layer.ow) * layer.stride
+        vl = (ql // ohow) * VH + ((ql % ohow) // layer.ow) * layer.stride + layer.r
+        best = max(best, vl - v0)
+    per_c = best * IWP * 4
+    for cc in (8, 4, 2):
+        if cc == 8 and layer.s != 3:
+            continue
+        if cc * per_c <= 64 * 1024:
+            return f"window_tm{tm}_cc{cc}_s{layer.s}"
+    return "direct"
+
+
+def algorithmic_bytes(layer) -> int:
+    """Bytes a call must move at least: x, y, packed weights (ceil(CRS/6) words per row), bias."""
+    wpr = (layer.crs + 5) // 6
+    b = 4 * int(np.prod(layer.x_shape)) + 4 * int(np.prod(layer.y_shape)) + 4 * layer.k * wpr
+    return b + (4 * layer.k if layer.bias else 0)
+
+
+def parse():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=5)
+    ap.add_argument("--warmup", type=int, default=2)
+    ap.add_argument("--workload", default="resnet50", choices=sorted(WORKLOADS))
+    ap.add_argument("--cpu-batch", type=int, default=None,
+                    help="batch of the oracle sample (default: sized for ~10-30 s)")
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--no-mul", action="store_true")
+    ap.add_argument("--layers-out", default=None, help="write per-layer timings (JSON) here")
+    return ap.parse_args()
+
+
+def main():
+    args = parse()
+    if args.gpus != 1:
+        print(f"bench.py runs on one GPU only (asked for {args.gpus}); the shift operators need "
+              "no cross-GPU exchange for a layer, see the design notes for how they shard.",
+              file=sys.stderr)
+        sys.exit(2)
+
+    import torch
+    from paper_1905_13298_amd import ops
+    from paper_1905_13298_amd import workloads as W
+
+    cfg = WORKLOADS[args.workload]
+    seed = W.CONFIG_SEEDS[cfg]
+    layers = W.config_layers(cfg)
+    dev = torch.device("cuda:0")
+    torch.cuda.set_device(dev)
+
+    # ---- inputs, resident in HBM before timing
+    t0 = time.time()
+    res = []
+    for li, L in enumerate(layers):
+        x, codes, bias = W.gen_layer(L, seed, li)
+        wp = ops.pack_shift_weights(codes).view(np.int32)
+        xt = torch.from_numpy(x).to(dev)
+        wt = torch.from_numpy(wp).to(dev)
+        bt = None if bias is None else torch.from_numpy(bias).to(dev)
+        yt = torch.empty(L.y_shape, dtype=torch.int32, device=dev)
+        res.append((L, xt, wt, bt, yt))
+        del x, codes, bias
+    torch.cuda.synchronize()
+    print(f"# inputs ready in {time.time() - t0:.1f} s", file=sys.stderr, flush=True)
+
+    def run_layer(L, xt, wt, bt, yt):
+        if L.kind == "linear":
+            ops.linear_shift(xt, wt, bt, out=yt)
+        else:
+            ops.conv2d_shift(xt, wt, bt, (L.r, L.s), L.stride, L.pad, out=yt)
+
+    for _ in range(args.warmup):
+        for r in res:
+            run_layer(*r)
+    torch.cuda.synchronize()
+
+    stream = torch.cuda.current_stream(dev)
+    ev = [[(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True))
+           for _ in res] for _ in range(args.steps)]
+    t_start = torch.cuda.Event(enable_timing=True)
+    t_end = torch.cuda.Event(enable_timing=True)
+    torch.cuda.synchronize()
+    t_start.record(stream)
+    for s in range(args.steps):
+        for li, r in enumerate(res):
+            ev[s][li][0].record(stream)
+            run_layer(*r)
+            ev[s][li][1].record(stream)
+    t_end.record(stream)
+    torch.cuda.synchronize()
+    total_ms = t_start.elapsed_time(t_end)
+    ms_per_step = total_ms / args.steps
+
+    sac_step = sum(L.sac for L in layers)
+    value = sac_step / (ms_per_step * 1e-3) / 1e9
+
+    per_layer = []
+    for li, L in enumerate(layers):
+        d = np.array([ev[s][li][0].elapsed_time(ev[s][li][1]) for s in range(args.steps)])
+        med = float(np.median(d))
+        per_layer.append({
+            "layer": L.name, "kind": L.kind, "variant": kernel_variant(L),
+            "shape": {"n": L.n, "c": L.c, "h": L.h, "w": L.w, "k": L.k, "r": L.r, "s": L.s,
+                      "stride": L.stride, "pad": L.pad},
+            "sac": L.sac, "ms_median": med, "ms_mean": float(d.mean()), "ms_min": float(d.min()),
+            "gsac_s": L.sac / (med * 1e-3) / 1e9,
+            "frac_sac_peak": L.sac / (med * 1e-3) / 1e12 / SAC_PEAK_T,
+            "hbm_gbs": algorithmic_bytes(L) / (med * 1e-3) / 1e9,
+        })
+
+    # ---- dominant kernel: the tiled-kernel instance with the most time per step
+    groups = {}
+    for li, (L, *_rest) in enumerate(res):
+        g = groups.setdefault(kernel_variant(L), {"sac": 0, "ms": 0.0, "launches": 0, "bytes": 0})
+        g["sac"] += L.sac
+        g["ms"] += float(np.mean([ev[s][li][0].elapsed_time(ev[s][li][1])
+                                  for s in range(args.steps)]))
+        g["launches"] += 1
+        g["bytes"] += algorithmic_bytes(L)
+    dom_name, dom = max(groups.items(), key=lambda kv: kv[1]["ms"])
+    achieved = dom["sac"] / (dom["ms"] * 1e-3) / 1e12
+    roofline = {
+        "bound": "alu", "achieved": round(achieved, 4), "peak": round(SAC_PEAK_T, 4),
+        "unit": "TSAC/s", "frac": round(achieved / SAC_PEAK_T, 4), "traffic": None,
+        "kernel": dom_name, "launches_per_step": dom["launches"],
+        "avg_launch_ms": round(dom["ms"] / dom["launches"], 5),
+        "sac_per_launch_avg": dom["sac"] // dom["launches"],
+        "int32_ops_frac": round(2 * achieved / INT32_OPS_PEAK_T, 4),
+        "hbm_gbs_algorithmic": round(dom["bytes"] / (dom["ms"] * 1e-3) / 1e9, 1),
+        "timed_span": "library call (weight decode + tiled kernel) per launch",
+    }
+
+    # ---- multiplication-based comparison kernel, same tiling, same layers
+    mul = None
+    if not args.no_mul:
+        mres = []
+        g = torch.Generator(device=dev)
+        g.manual_seed(seed)
+        for (L, xt, wt, bt, yt) in res:
+            wm = torch.randint(-(1 << 15), 1 << 15, (L.k, L.crs), dtype=torch.int32, device=dev,
+                               generator=g)
+            mres.append((L, xt, wm, bt, yt))
+
+        def run_mul(L, xt, wm, bt, yt):
+            if L.kind == "linear":
+                ops.linear_mul_i32(xt, wm, bt, out=yt)
+            else:
+                ops.conv2d_mul_i32(xt, wm, bt, (L.r, L.s), L.stride, L.pad, out=yt)
+
+        for r in mres:
+            run_mul(*r)
+        torch.cuda.synchronize()
+        a = torch.cuda.Event(enable_timing=True)
+        b = torch.cuda.Event(enable_timing=True)
+        a.record(stream)
+        for _ in range(args.steps):
+            for r in mres:
+                run_mul(*r)
+        b.record(stream)
+        torch.cuda.synchronize()
+        mul_ms = a.elapsed_time(b) / args.steps
+        mul = {"ms_per_step": round(mul_ms, 4), "gmac_s": round(sac_step / (mul_ms * 1e-3) / 1e9, 1),
+               "shift_speedup": round(mul_ms / ms_per_step, 3),
+               "inner_op": "v_mul_lo_u32 + v_add_u32 (int32, mod 2^32)"}
+        del mres
+
+    # ---- CPU baseline: the oracle on the host cores, same layers at a small batch
+    cpu = None
+    if not args.no_cpu_baseline:
+        import oracle
+        del res
+        torch.cuda.empty_cache()
+        nthreads = oracle.max_threads()
+        cpu_batch = args.cpu_batch
+        if cpu_batch is None:
+            cpu_batch = {0: 8, 1: 1, 2: 256, 3: 8, 4: 4}[cfg]
+        sample_sac = 0
+        cpu_total = 0.0
+        for li, L in enumerate(layers):
+            Ls = L.with_batch(min(cpu_batch, L.n))
+            x, codes, bias = W.gen_layer(Ls, seed, li)
+            t1 = time.perf_counter()
+            if Ls.kind == "linear":
+                oracle.linear_shift(x, codes, bias)
+            else:
+                oracle.conv2d_shift(x, codes, bias, r=Ls.r, s=Ls.s, stride=Ls.stride, pad=Ls.pad)
+            cpu_total += time.perf_counter() - t1
+            sample_sac += Ls.sac
+        cpu = {"value": round(sample_sac / cpu_total / 1e9, 3), "unit": "GSAC/s",
+               "cores": nthreads, "kind": "oracle",
+               "sample": f"every layer of the workload at batch {cpu_batch} "
+                         f"({sample_sac / 1e9:.2f} G SAC, {cpu_total:.1f} s)"}
+
+    out = {
+        "metric": "G shift-accumulates/s per layer and % of int32 VALU peak on one MI355X",
+        "value": round(value, 2), "unit": "GSAC/s", "n_gpus": 1, "steps": args.steps,
+        "warmup": args.warmup, "ms_per_step": round(ms_per_step, 4), "higher_is_better": True,
+        "scaling": "weak", "vs_baseline": None, "dtype": "i32", "data": "synthetic",
+        "frac_sac_peak": round(value / 1000.0 / SAC_PEAK_T, 4),
+        "config": {"workload": W.CONFIG_NAMES[cfg], "layers": len(layers),
+                   "batch": layers[0].n, "frac_bits": W.FRAC_BITS,
+                   "sac_per_step": sac_step, "parallelism": "single GPU"},
+        "roofline": roofline, "cpu_baseline": cpu, "mul_i32": mul,
+    }
+    if args.layers_out:
+        with open(args.layers_out, "w") as f:
+            json.dump({"workload": W.CONFIG_NAMES[cfg], "layers": per_layer}, f, indent=1)
+    print(json.dumps(out), flush=True)
+
+
+if __name__ == "__main__":
+    main()
