@@ -37,31 +37,12 @@ HBM_PEAK_GBS = 8000.0
 
 
 def kernel_variant(layer) -> str:
-    """The tiled-kernel instance the library's planner picks for a layer (mirrors
-    run_conv in conv_kernels.hip): staging mode, pixels per lane, chunk, taps."""
-    if layer.kind == "linear" or (layer.h == 1 and layer.w == 1 and layer.r == 1 and layer.s == 1
-                                  and layer.pad == 0):
-        return "rowmajor_tm4_cc16"
-    if layer.r == 1 and layer.s == 1 and layer.pad == 0:
-        return "point_tm8_cc8"
-    tm = 4 if layer.s == 7 else 8
-    P = 64 * tm
-    VH, IWP = layer.h + 2 * layer.pad, layer.w + 2 * layer.pad
-    ohow = layer.oh * layer.ow
-    nq = layer.n * ohow
-    best = 0
-    for q0 in range(0, nq, P):
-        ql = min(q0 + P, nq) - 1
-        v0 = (q0 // ohow) * VH + ((q0 % ohow) // layer.ow) * layer.stride
-        vl = (ql // ohow) * VH + ((ql % ohow) // layer.ow) * layer.stride + layer.r
-        best = max(best, vl - v0)
-    per_c = best * IWP * 4
-    for cc in (8, 4, 2):
-        if cc == 8 and layer.s != 3:
-            continue
-        if cc * per_c <= 64 * 1024:
-            return f"window_tm{tm}_cc{cc}_s{layer.s}"
-    return "direct"
+    """The kernel the library runs for a layer, as the library itself names it."""
+    from paper_1905_13298_amd import ops
+    if layer.kind == "linear":
+        return ops.describe_conv2d(layer.n, layer.c, 1, 1, layer.k, 1)
+    return ops.describe_conv2d(layer.n, layer.c, layer.h, layer.w, layer.k, (layer.r, layer.s),
+                               layer.stride, layer.pad)
 
 
 def algorithmic_bytes(layer) -> int:
@@ -166,7 +147,8 @@ def main():
     # ---- dominant kernel: the tiled-kernel instance with the most time per step
     groups = {}
     for li, (L, *_rest) in enumerate(res):
-        g = groups.setdefault(kernel_variant(L), {"sac": 0, "ms": 0.0, "launches": 0, "bytes": 0})
+        name = kernel_variant(L).rsplit(" splits", 1)[0]   # one kernel instance
+        g = groups.setdefault(name, {"sac": 0, "ms": 0.0, "launches": 0, "bytes": 0})
         g["sac"] += L.sac
         g["ms"] += float(np.mean([ev[s][li][0].elapsed_time(ev[s][li][1])
                                   for s in range(args.steps)]))

@@ -130,6 +130,16 @@ ds_status ds_linear_mul_i32(const int32_t *x, const int32_t *w, const int32_t *b
                             int64_t batch, int64_t in_features, int64_t out_features,
                             uint32_t flags, void *stream);
 
+/* Names, without launching anything, the kernel ds_conv2d_shift (or
+ * ds_linear_shift, as a 1x1 convolution with h = w = 1) runs for a problem
+ * of this shape on the current device, e.g. "tiled point tm8 cc8 splits1"
+ * or "direct". Writes a NUL-terminated string of at most len bytes into buf.
+ * Shape arguments are validated as for ds_conv2d_shift; no device memory is
+ * touched. For profiling and tests. */
+ds_status ds_conv2d_shift_describe(int64_t n, int64_t c, int64_t h, int64_t w, int64_t k,
+                                   int64_t r, int64_t s, int32_t stride_h, int32_t stride_w,
+                                   int32_t pad_h, int32_t pad_w, char *buf, int64_t len);
+
 /* Static text for a status code. */
 const char *ds_status_string(ds_status status);
 

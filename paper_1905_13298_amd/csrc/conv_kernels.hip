@@ -28,6 +28,8 @@
 #include <hip/hip_runtime.h>
 
 #include <algorithm>
+#include <cmath>
+#include <cstdio>
 #include <cstdlib>
 #include <mutex>
 
@@ -212,23 +214,47 @@ fill_init_kernel(const int32_t *__restrict__ init, int32_t *__restrict__ y, int6
 
 // ---------------------------------------------------------------------------
 // Tiled kernel.
+//
+// Staging. Each chunk of CC input channels is copied from HBM straight into
+// LDS with buffer loads that write LDS (buffer_load_dword ... lds): one
+// instruction moves 64 consecutive LDS words, lane l supplying the word at
+// its own global offset. Lanes whose element lies in the zero padding, past
+// the last pixel or past the input get an offset beyond the buffer's size,
+// and the hardware returns 0 for them; channels past C use a buffer of size
+// 0. The LDS holds two chunks: while chunk t is computed, chunk t+1 is in
+// flight, and one barrier per chunk hands the buffers over.
+//
+// Sign check. After its copies land, each wave ORs the words it brought in
+// and publishes whether any was negative; the barrier makes the four flags
+// visible, and the chunk takes the two-instruction path when all are clear.
 
 enum StageMode : int {
-    MODE_WINDOW = 0,    // r x s window with padding: LDS holds padded input rows
-    MODE_POINT = 1,     // 1x1, no padding, NCHW: LDS holds X[c][q] (lanes load pixels)
-    MODE_ROWMAJOR = 2,  // h = w = 1 (LinearShift): LDS holds X[c][q] (lanes load features)
+    MODE_WINDOW = 0,  // r x s taps with padding: LDS holds padded input rows of the tile
+    MODE_POINT = 1,   // 1x1 taps, no padding: LDS holds X[c][q]; covers LinearShift (h = w = 1)
 };
+
+constexpr uint32_t kOOB = 0x80000000u;       // buffer offset past every valid input byte
+constexpr int kRsrcWord3 = 0x00020000;       // raw buffer, 32-bit data (gfx9 family)
 
 struct TiledParams {
     int N, C, H, W, K, R, S, sh, sw, ph, pw, OH, OW;
     int OHOW, NQ, HW;
     int Jpad;           // decoded row length (chunks * CC * R * S)
     int VH, IWP;        // padded input height / width (window mode)
-    int slots_max;      // LDS rows per channel (window mode)
+    int PLANE;          // LDS words per channel per chunk (window mode, multiple of 64)
     int tiles_p, tiles_k, chunks_per_split, nchunks;
     int atomic_out;     // split-K: add partial sums atomically into y
-    FastDiv div_ohow, div_ow, div_vh;
+    int x_bytes;        // size of x in bytes (< 2^31)
+    FastDiv div_ohow, div_ow, div_vh, div_iwp;
 };
+
+typedef __attribute__((address_space(3))) void *lds_ptr_t;
+
+__device__ __forceinline__ void copy_to_lds(__amdgpu_buffer_rsrc_t r, int32_t *dst, uint32_t voff,
+                                            uint32_t soff)
+{
+    __builtin_amdgcn_raw_ptr_buffer_load_lds(r, (lds_ptr_t)dst, 4, voff, soff, 0, 0);
+}
 
 // acc[i][t] += term(xv[i], d[t]) for one tap j and TN channels.
 template <Inner OP, bool SIGNED, int TM, int TN>
@@ -257,14 +283,14 @@ __device__ __forceinline__ void sac_step(uint32_t (&acc)[TM][TN], const int32_t 
 }
 
 template <Inner OP, bool SIGNED, int TM, int TN, int CC, int SK>
-__device__ __forceinline__ void compute_window(uint32_t (&acc)[TM][TN], const int32_t *lds,
+__device__ __forceinline__ void compute_window(uint32_t (&acc)[TM][TN], const int32_t *buf,
                                                const int (&base)[TM],
-                                               const int32_t *__restrict__ wk, int R,
-                                               int slots_max, int IWP)
+                                               const int32_t *__restrict__ wk, int R, int PLANE,
+                                               int IWP)
 {
     for (int c = 0; c < CC; ++c) {
         for (int r = 0; r < R; ++r) {
-            const int rowoff = (c * slots_max + r) * IWP;
+            const int rowoff = c * PLANE + r * IWP;
             int addr[TM];
 #pragma unroll
             for (int i = 0; i < TM; ++i) addr[i] = base[i] + rowoff;
@@ -272,7 +298,7 @@ __device__ __forceinline__ void compute_window(uint32_t (&acc)[TM][TN], const in
             for (int s = 0; s < SK; ++s) {
                 int32_t xv[TM];
 #pragma unroll
-                for (int i = 0; i < TM; ++i) xv[i] = lds[addr[i] + s];
+                for (int i = 0; i < TM; ++i) xv[i] = buf[addr[i] + s];
                 sac_step<OP, SIGNED, TM, TN>(acc, xv, wk + s * TN);
             }
             wk += SK * TN;
@@ -280,33 +306,36 @@ __device__ __forceinline__ void compute_window(uint32_t (&acc)[TM][TN], const in
     }
 }
 
-template <Inner OP, bool SIGNED, int TM, int TN, int CC, int PL>
-__device__ __forceinline__ void compute_point(uint32_t (&acc)[TM][TN], const int32_t *lds,
+template <Inner OP, bool SIGNED, int TM, int TN, int CC>
+__device__ __forceinline__ void compute_point(uint32_t (&acc)[TM][TN], const int32_t *buf,
                                               int lane, const int32_t *__restrict__ wk)
 {
+    constexpr int P = 64 * TM;
 #pragma unroll
     for (int c = 0; c < CC; ++c) {
         int32_t xv[TM];
 #pragma unroll
-        for (int i = 0; i < TM; ++i) xv[i] = lds[c * PL + i * 64 + lane];
+        for (int i = 0; i < TM; ++i) xv[i] = buf[c * P + i * 64 + lane];
         sac_step<OP, SIGNED, TM, TN>(acc, xv, wk + c * TN);
     }
 }
 
-template <Inner OP, int MODE, int TM, int TN, int CC, int SK>
+// GW: copy segments (64 LDS words) per wave and channel, window mode.
+template <Inner OP, int MODE, int TM, int TN, int CC, int SK, int GW>
 __global__ void __launch_bounds__(256)
 tiled_kernel(const int32_t *__restrict__ x, const int32_t *__restrict__ wd,
              const int32_t *__restrict__ init, int32_t *__restrict__ y, const TiledParams p)
 {
     extern __shared__ int32_t lds[];
-    __shared__ int sflag[2];
+    __shared__ int neg_flag[2][4];
     constexpr int P = 64 * TM;
-    constexpr int PL = MODE == MODE_ROWMAJOR ? P + 1 : P;  // odd stride: transposed writes
+    constexpr int NV = MODE == MODE_WINDOW ? GW : TM;   // staging offsets per lane
     const int tid = threadIdx.x, lane = tid & 63;
     // The wave index is the same for all lanes of a wave; saying so lets every
-    // quantity derived from it (this wave's channels, its weight rows) live in
-    // scalar registers.
+    // quantity derived from it (this wave's channels, its weight rows, its copy
+    // segments) live in scalar registers.
     const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+    const int BUF = MODE == MODE_WINDOW ? CC * p.PLANE : CC * P;
 
     // Block order: consecutive tiles on one XCD (blocks are dealt to the 8 XCDs
     // round-robin) share a pixel tile, so its input stays in that XCD's L2.
@@ -322,9 +351,15 @@ tiled_kernel(const int32_t *__restrict__ x, const int32_t *__restrict__ wd,
     const int kw = ct * 4 * TN + wave * TN;  // first output channel of this wave
     const int32_t *__restrict__ wrow = wd + size_t(kw / TN) * p.Jpad * TN;
 
-    // Per-lane output pixels q = q0 + i*64 + lane.
-    int yoff[TM], base[TM], goff[TM];
-    int vbase = 0, slots = 0;
+    const __amdgpu_buffer_rsrc_t xr = __builtin_amdgcn_make_buffer_rsrc(
+        const_cast<int32_t *>(x), short(0), p.x_bytes, kRsrcWord3);
+    const __amdgpu_buffer_rsrc_t zr = __builtin_amdgcn_make_buffer_rsrc(
+        const_cast<int32_t *>(x), short(0), 0, kRsrcWord3);
+
+    // Per-lane output pixels q = q0 + i*64 + lane, and the staging offsets.
+    int yoff[TM], base[TM];
+    uint32_t voff[NV];
+    int vbase = 0, nseg = 0;
     if constexpr (MODE == MODE_WINDOW) {
         const int n0 = fdiv(q0, p.div_ohow);
         const int oh0 = fdiv(q0 - n0 * p.OHOW, p.div_ow);
@@ -332,14 +367,29 @@ tiled_kernel(const int32_t *__restrict__ x, const int32_t *__restrict__ wd,
         const int ql = min(q0 + P, p.NQ) - 1;
         const int nl = fdiv(ql, p.div_ohow);
         const int ohl = fdiv(ql - nl * p.OHOW, p.div_ow);
-        slots = nl * p.VH + ohl * p.sh + p.R - vbase;
+        const int live = (nl * p.VH + ohl * p.sh + p.R - vbase) * p.IWP;  // words per channel
+        nseg = (live + 63) >> 6;
+#pragma unroll
+        for (int g = 0; g < GW; ++g) {
+            const int e = (wave + 4 * g) * 64 + lane;
+            voff[g] = kOOB;
+            if (e < live) {
+                const int slot = fdiv(e, p.div_iwp);
+                const int iw = e - slot * p.IWP - p.pw;
+                const int vv = vbase + slot;
+                const int n = fdiv(vv, p.div_vh);
+                const int ih = vv - n * p.VH - p.ph;
+                if (ih >= 0 && ih < p.H && iw >= 0 && iw < p.W)
+                    voff[g] = uint32_t(((n * p.C) * p.HW + ih * p.W + iw) * 4);
+            }
+        }
     }
 #pragma unroll
     for (int i = 0; i < TM; ++i) {
         const int q = q0 + i * 64 + lane;
         yoff[i] = -1;
         base[i] = 0;
-        goff[i] = -1;
+        if constexpr (MODE == MODE_POINT) voff[i] = kOOB;
         if (q < p.NQ) {
             const int n = fdiv(q, p.div_ohow);
             const int pix = q - n * p.OHOW;
@@ -349,9 +399,57 @@ tiled_kernel(const int32_t *__restrict__ x, const int32_t *__restrict__ wd,
             if constexpr (MODE == MODE_WINDOW)
                 base[i] = (n * p.VH + oh * p.sh - vbase) * p.IWP + ow * p.sw;
             if constexpr (MODE == MODE_POINT)
-                goff[i] = n * p.C * p.HW + oh * p.sh * p.W + ow * p.sw;
+                voff[i] = uint32_t((n * p.C * p.HW + oh * p.sh * p.W + ow * p.sw) * 4);
         }
     }
+
+    // Copies of one chunk into LDS buffer `bf`: this wave's share.
+    auto issue = [&](int ch, int bf) {
+        int32_t *dst = lds + bf * BUF;
+        if constexpr (MODE == MODE_WINDOW) {
+            for (int c = 0; c < CC; ++c) {
+                const int cc = ch * CC + c;
+                const __amdgpu_buffer_rsrc_t r = cc < p.C ? xr : zr;
+                const uint32_t soff = cc < p.C ? uint32_t(cc * p.HW * 4) : 0u;
+#pragma unroll
+                for (int g = 0; g < GW; ++g) {
+                    const int seg = wave + 4 * g;
+                    if (seg < nseg) copy_to_lds(r, dst + c * p.PLANE + seg * 64, voff[g], soff);
+                }
+            }
+        } else {
+#pragma unroll
+            for (int cw = 0; cw < CC / 4; ++cw) {
+                const int c = wave + 4 * cw;
+                const int cc = ch * CC + c;
+                const __amdgpu_buffer_rsrc_t r = cc < p.C ? xr : zr;
+                const uint32_t soff = cc < p.C ? uint32_t(cc * p.HW * 4) : 0u;
+#pragma unroll
+                for (int i = 0; i < TM; ++i) copy_to_lds(r, dst + c * P + i * 64, voff[i], soff);
+            }
+        }
+    };
+    // Wait for this wave's copies into buffer `bf`, then publish the OR of their signs.
+    auto check = [&](int bf) {
+        asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
+        const int32_t *src = lds + bf * BUF;
+        int32_t o = 0;
+        if constexpr (MODE == MODE_WINDOW) {
+            for (int c = 0; c < CC; ++c)
+#pragma unroll
+                for (int g = 0; g < GW; ++g) {
+                    const int seg = wave + 4 * g;
+                    if (seg < nseg) o |= src[c * p.PLANE + seg * 64 + lane];
+                }
+        } else {
+#pragma unroll
+            for (int cw = 0; cw < CC / 4; ++cw)
+#pragma unroll
+                for (int i = 0; i < TM; ++i) o |= src[(wave + 4 * cw) * P + i * 64 + lane];
+        }
+        const bool any = __any(o < 0);
+        if (lane == 0) neg_flag[bf][wave] = any ? 1 : 0;
+    };
 
     uint32_t acc[TM][TN];
 #pragma unroll
@@ -361,100 +459,32 @@ tiled_kernel(const int32_t *__restrict__ x, const int32_t *__restrict__ wd,
 
     const int ch_begin = z * p.chunks_per_split;
     const int ch_end = min(p.nchunks, ch_begin + p.chunks_per_split);
-    if (tid == 0) sflag[0] = sflag[1] = 0;
 
+    issue(ch_begin, 0);
+    check(0);
+    __syncthreads();
     for (int ch = ch_begin; ch < ch_end; ++ch) {
-        const int c0 = ch * CC;
-        int32_t neg = 0;
-        __syncthreads();  // the previous chunk is no longer being read
-
-        if constexpr (MODE == MODE_WINDOW) {
-            const int JJ = (p.IWP + 63) >> 6;
-            for (int c = 0; c < CC; ++c) {
-                const int cc = c0 + c;
-                for (int jj = 0; jj < JJ; ++jj) {
-                    const int u = lane + 64 * jj;
-                    const int iw = u - p.pw;
-                    const bool colok = u < p.IWP && iw >= 0 && iw < p.W;
-                    for (int s0 = wave; s0 < slots; s0 += 32) {
-                        int32_t v[8];
-#pragma unroll
-                        for (int e = 0; e < 8; ++e) {
-                            const int slot = s0 + 4 * e;
-                            v[e] = 0;
-                            if (slot < slots && cc < p.C) {
-                                const int vv = vbase + slot;
-                                const int n = fdiv(vv, p.div_vh);
-                                const int ih = vv - n * p.VH - p.ph;
-                                if (ih >= 0 && ih < p.H && colok)
-                                    v[e] = x[(n * p.C + cc) * p.HW + ih * p.W + iw];
-                            }
-                        }
-#pragma unroll
-                        for (int e = 0; e < 8; ++e) {
-                            const int slot = s0 + 4 * e;
-                            if (slot < slots && u < p.IWP) {
-                                lds[(c * p.slots_max + slot) * p.IWP + u] = v[e];
-                                neg |= v[e];
-                            }
-                        }
-                    }
-                }
-            }
-        } else if constexpr (MODE == MODE_POINT) {
-            constexpr int CW = CC / 4;
-            int32_t v[TM][CW];
-#pragma unroll
-            for (int i = 0; i < TM; ++i)
-#pragma unroll
-                for (int cw = 0; cw < CW; ++cw) {
-                    const int cc = c0 + wave + 4 * cw;
-                    v[i][cw] = (goff[i] >= 0 && cc < p.C) ? x[goff[i] + cc * p.HW] : 0;
-                }
-#pragma unroll
-            for (int i = 0; i < TM; ++i)
-#pragma unroll
-                for (int cw = 0; cw < CW; ++cw) {
-                    lds[(wave + 4 * cw) * PL + i * 64 + lane] = v[i][cw];
-                    neg |= v[i][cw];
-                }
-        } else {  // MODE_ROWMAJOR: lanes cover CC consecutive features of 64/CC rows
-            constexpr int RPW = 64 / CC;        // rows per wave instruction
-            constexpr int RR = P / (4 * RPW);   // rounds per thread
-            const int cl = lane % CC, rs = lane / CC;
-            const int cc = c0 + cl;
-            int32_t v[RR];
-#pragma unroll
-            for (int rr = 0; rr < RR; ++rr) {
-                const int q = q0 + rr * 4 * RPW + wave * RPW + rs;
-                v[rr] = (q < p.NQ && cc < p.C) ? x[q * p.C + cc] : 0;
-            }
-#pragma unroll
-            for (int rr = 0; rr < RR; ++rr) {
-                lds[cl * PL + rr * 4 * RPW + wave * RPW + rs] = v[rr];
-                neg |= v[rr];
-            }
-        }
-        if constexpr (OP == Inner::Shift) {
-            if (neg < 0) sflag[ch & 1] = 1;  // a negative input in this chunk
-        }
-        __syncthreads();
-        const bool sgn = OP == Inner::Shift && sflag[ch & 1] != 0;
-        if (tid == 0) sflag[(ch + 1) & 1] = 0;  // read by nobody until the next barrier
-
+        const int bf = (ch - ch_begin) & 1;
+        const bool more = ch + 1 < ch_end;
+        if (more) issue(ch + 1, bf ^ 1);
+        const bool sgn = OP == Inner::Shift &&
+                         (neg_flag[bf][0] | neg_flag[bf][1] | neg_flag[bf][2] | neg_flag[bf][3]);
+        const int32_t *buf = lds + bf * BUF;
         const int32_t *__restrict__ wk =
-            wrow + size_t(c0) * (MODE == MODE_WINDOW ? p.R * SK : 1) * TN;
+            wrow + size_t(ch * CC) * (MODE == MODE_WINDOW ? p.R * SK : 1) * TN;
         if constexpr (MODE == MODE_WINDOW) {
             if (sgn)
-                compute_window<OP, true, TM, TN, CC, SK>(acc, lds, base, wk, p.R, p.slots_max, p.IWP);
+                compute_window<OP, true, TM, TN, CC, SK>(acc, buf, base, wk, p.R, p.PLANE, p.IWP);
             else
-                compute_window<OP, false, TM, TN, CC, SK>(acc, lds, base, wk, p.R, p.slots_max, p.IWP);
+                compute_window<OP, false, TM, TN, CC, SK>(acc, buf, base, wk, p.R, p.PLANE, p.IWP);
         } else {
             if (sgn)
-                compute_point<OP, true, TM, TN, CC, PL>(acc, lds, lane, wk);
+                compute_point<OP, true, TM, TN, CC>(acc, buf, lane, wk);
             else
-                compute_point<OP, false, TM, TN, CC, PL>(acc, lds, lane, wk);
+                compute_point<OP, false, TM, TN, CC>(acc, buf, lane, wk);
         }
+        if (more) check(bf ^ 1);
+        __syncthreads();
     }
 
     // Epilogue: y[n][k][pix] for this wave's channels; lanes store consecutive pixels.
@@ -478,61 +508,73 @@ tiled_kernel(const int32_t *__restrict__ x, const int32_t *__restrict__ wd,
 // ---------------------------------------------------------------------------
 // Planning and launch.
 
-constexpr int kTN = 8;          // output channels per wave (scalar weights per tap)
+constexpr int kTN = 8;              // output channels per wave (scalar weights per tap)
 constexpr int kLdsLimit = 64 * 1024;
-constexpr int kTargetBlocks = 512;  // at least two workgroups per CU (256 CUs)
+constexpr int kCUs = 256;           // compute units of an MI355X
+constexpr int kMinBlocks = 1024;    // four workgroups (16 waves) per CU
 
-template <Inner OP, int MODE, int TM, int TN, int CC, int SK>
-static hipError_t launch_tiled(const TiledParams &p, int grid, size_t lds_bytes,
-                               const int32_t *x, const int32_t *wd, const int32_t *init,
-                               int32_t *y, hipStream_t st)
+struct Variant {
+    int mode, tm, cc, sk, gw;
+};
+
+// The compiled instances. Window mode: GW copy segments per wave cover planes of
+// up to 4*GW*64 words per channel.
+static const Variant kVariants[] = {
+    {MODE_POINT, 8, 8, 1, 0},  {MODE_POINT, 4, 8, 1, 0},
+    {MODE_WINDOW, 8, 4, 3, 8}, {MODE_WINDOW, 8, 2, 3, 8}, {MODE_WINDOW, 4, 4, 3, 8},
+    {MODE_WINDOW, 4, 2, 3, 8}, {MODE_WINDOW, 4, 1, 3, 16},
+    {MODE_WINDOW, 4, 2, 7, 24}, {MODE_WINDOW, 4, 1, 7, 24},
+    {MODE_WINDOW, 4, 2, 1, 16}, {MODE_WINDOW, 4, 2, 2, 16}, {MODE_WINDOW, 4, 2, 5, 16},
+    {MODE_WINDOW, 4, 1, 5, 24},
+};
+
+template <Inner OP, int MODE, int TM, int CC, int SK, int GW>
+static hipError_t launch_tiled(const TiledParams &p, int grid, size_t lds, const int32_t *x,
+                               const int32_t *wd, const int32_t *init, int32_t *y, hipStream_t st)
 {
-    hipLaunchKernelGGL((tiled_kernel<OP, MODE, TM, TN, CC, SK>), dim3(grid), dim3(256), lds_bytes,
+    hipLaunchKernelGGL((tiled_kernel<OP, MODE, TM, kTN, CC, SK, GW>), dim3(grid), dim3(256), lds,
                        st, x, wd, init, y, p);
     return hipGetLastError();
 }
-
-struct Variant {
-    int mode, tm, cc, sk;
-};
 
 template <Inner OP>
 static hipError_t dispatch_tiled(const Variant &v, const TiledParams &p, int grid, size_t lds,
                                  const int32_t *x, const int32_t *wd, const int32_t *init,
                                  int32_t *y, hipStream_t st)
 {
-#define DS_CASE(M, TM, CC, SK)                                                               \
-    if (v.mode == M && v.tm == TM && v.cc == CC && v.sk == SK)                               \
-        return launch_tiled<OP, M, TM, kTN, CC, SK>(p, grid, lds, x, wd, init, y, st);
-    DS_CASE(MODE_ROWMAJOR, 4, 16, 1)
-    DS_CASE(MODE_POINT, 8, 8, 1)
-    DS_CASE(MODE_WINDOW, 8, 8, 3)
-    DS_CASE(MODE_WINDOW, 8, 4, 3)
-    DS_CASE(MODE_WINDOW, 8, 2, 3)
-    DS_CASE(MODE_WINDOW, 8, 4, 1)
-    DS_CASE(MODE_WINDOW, 8, 2, 1)
-    DS_CASE(MODE_WINDOW, 8, 4, 2)
-    DS_CASE(MODE_WINDOW, 8, 2, 2)
-    DS_CASE(MODE_WINDOW, 8, 4, 5)
-    DS_CASE(MODE_WINDOW, 8, 2, 5)
-    DS_CASE(MODE_WINDOW, 4, 4, 7)
-    DS_CASE(MODE_WINDOW, 4, 2, 7)
+#define DS_CASE(M, TM, CC, SK, GW)                                                           \
+    if (v.mode == M && v.tm == TM && v.cc == CC && v.sk == SK && v.gw == GW)                 \
+        return launch_tiled<OP, M, TM, CC, SK, GW>(p, grid, lds, x, wd, init, y, st);
+    DS_CASE(MODE_POINT, 8, 8, 1, 0)
+    DS_CASE(MODE_POINT, 4, 8, 1, 0)
+    DS_CASE(MODE_WINDOW, 8, 4, 3, 8)
+    DS_CASE(MODE_WINDOW, 8, 2, 3, 8)
+    DS_CASE(MODE_WINDOW, 4, 4, 3, 8)
+    DS_CASE(MODE_WINDOW, 4, 2, 3, 8)
+    DS_CASE(MODE_WINDOW, 4, 1, 3, 16)
+    DS_CASE(MODE_WINDOW, 4, 2, 7, 24)
+    DS_CASE(MODE_WINDOW, 4, 1, 7, 24)
+    DS_CASE(MODE_WINDOW, 4, 2, 1, 16)
+    DS_CASE(MODE_WINDOW, 4, 2, 2, 16)
+    DS_CASE(MODE_WINDOW, 4, 2, 5, 16)
+    DS_CASE(MODE_WINDOW, 4, 1, 5, 24)
 #undef DS_CASE
     return hipErrorInvalidValue;
 }
 
-// Largest LDS row count per channel over all pixel tiles of the window mode.
-static int window_slots_max(const ConvGeom &g, int P, int VH)
+// Largest number of padded input rows (per channel) any pixel tile of P
+// output pixels needs in window mode.
+static int window_rows_max(const ConvGeom &g, int P, int VH)
 {
     const int64_t NQ = int64_t(g.n) * g.oh * g.ow, OHOW = int64_t(g.oh) * g.ow;
-    int best = 0;
+    int64_t best = 0;
     for (int64_t q0 = 0; q0 < NQ; q0 += P) {
         const int64_t ql = std::min(q0 + P, NQ) - 1;
         const int64_t v0 = (q0 / OHOW) * VH + ((q0 % OHOW) / g.ow) * g.sh;
         const int64_t vl = (ql / OHOW) * VH + ((ql % OHOW) / g.ow) * g.sh + g.r;
-        best = int(std::max<int64_t>(best, vl - v0));
+        best = std::max(best, vl - v0);
     }
-    return best;
+    return int(best);
 }
 
 static hipError_t run_direct(const ConvGeom &g, const int32_t *x, const uint32_t *wp,
@@ -551,65 +593,131 @@ static hipError_t run_direct(const ConvGeom &g, const int32_t *x, const uint32_t
     return hipGetLastError();
 }
 
-hipError_t run_conv(const ConvGeom &g, const int32_t *x, const uint32_t *wp, const int32_t *wi,
-                    const int32_t *bias, int32_t *y, Inner op, hipStream_t st)
+// Picks the tiled instance for a problem: v.mode < 0 when none fits.
+static Variant choose_variant(const ConvGeom &g, int &plane, size_t &lds)
 {
-    const bool rowmajor = g.h == 1 && g.w == 1 && g.r == 1 && g.s == 1 && g.ph == 0 && g.pw == 0;
-    const bool point = !rowmajor && g.r == 1 && g.s == 1 && g.ph == 0 && g.pw == 0;
+    const int64_t NQ = int64_t(g.n) * g.oh * g.ow;
+    const bool point = g.r == 1 && g.s == 1 && g.ph == 0 && g.pw == 0;
+    plane = 0;
+    lds = 0;
+    const int fv = forced_variant();
+    if (point) {
+        const int tm = fv == 8 && NQ > 256 ? 8 : 4;
+        lds = size_t(2) * 8 * 64 * tm * 4;
+        return Variant{MODE_POINT, tm, 8, 1, 0};
+    }
     const int VH = g.h + 2 * g.ph, IWP = g.w + 2 * g.pw;
-
-    Variant v{-1, 0, 0, 0};
-    int slots_max = 0;
-    size_t lds = 0;
-    if (rowmajor) {
-        v = Variant{MODE_ROWMAJOR, 4, 16, 1};
-        lds = size_t(16) * (64 * 4 + 1) * 4;
-    } else if (point) {
-        v = Variant{MODE_POINT, 8, 8, 1};
-        lds = size_t(8) * 64 * 8 * 4;
-    } else if (g.s == 1 || g.s == 2 || g.s == 3 || g.s == 5 || g.s == 7) {
-        const int tm = g.s == 7 ? 4 : 8;
-        slots_max = window_slots_max(g, 64 * tm, VH);
-        const int per_c = slots_max * IWP * 4;
-        const int cc_opts[3] = {8, 4, 2};
-        for (int cc : cc_opts) {
-            if (cc == 8 && g.s != 3) continue;
-            if (size_t(cc) * per_c <= size_t(kLdsLimit)) {
-                v = Variant{MODE_WINDOW, tm, cc, g.s};
-                lds = size_t(cc) * per_c;
-                break;
+    const int order[2][2] = {{4, 8}, {8, 4}};
+    for (int tm : order[fv == 8 ? 1 : 0]) {
+        const int rows = window_rows_max(g, 64 * tm, VH);
+        const int64_t live = int64_t(rows) * IWP;
+        const int pl = int((live + 63) / 64 * 64);
+        // Among the instances that fit, take the one that pads the fewest input
+        // channels up to whole chunks, then the largest chunk; prefer leaving LDS
+        // room for several workgroups per CU.
+        for (int budget : {48 * 1024, kLdsLimit}) {
+            const Variant *best = nullptr;
+            int best_pad = 0;
+            for (const Variant &v : kVariants) {
+                if (v.mode != MODE_WINDOW || v.tm != tm || v.sk != g.s) continue;
+                if (live > int64_t(4) * v.gw * 64) continue;
+                if (size_t(2) * v.cc * pl * 4 > size_t(budget)) continue;
+                const int pad = (g.c + v.cc - 1) / v.cc * v.cc - g.c;
+                if (!best || pad < best_pad || (pad == best_pad && v.cc > best->cc)) {
+                    best = &v;
+                    best_pad = pad;
+                }
+            }
+            if (best) {
+                plane = pl;
+                lds = size_t(2) * best->cc * pl * 4;
+                return *best;
             }
         }
     }
-    const int fv = forced_variant();
-    if (v.mode < 0 || fv == 0) return run_direct(g, x, wp, wi, bias, y, op, st);
+    return Variant{-1, 0, 0, 0, 0};
+}
 
+// Split-K factor and chunks per split for a tiled launch.
+static void plan_splits(const ConvGeom &g, const Variant &v, int &tiles_p, int &tiles_k,
+                        int &nchunks, int &splits, int &cps)
+{
     const int P = 64 * v.tm;
+    nchunks = (g.c + v.cc - 1) / v.cc;
+    tiles_k = (g.k + 4 * kTN - 1) / (4 * kTN);
+    const int64_t NQ = int64_t(g.n) * g.oh * g.ow;
+    tiles_p = int((NQ + P - 1) / P);
+    // Split the reduction when the tiles alone leave CUs idle: take the smallest
+    // split that gives at least kMinBlocks workgroups and spreads them over the
+    // CUs with at least 90 % balance (mean over maximum workgroups per CU),
+    // keeping at least two chunks per split.
+    const int64_t g0 = int64_t(tiles_p) * tiles_k;
+    splits = 1;
+    for (int s = 1; s <= 16 && s <= std::max(1, nchunks / 2); ++s) {
+        const int64_t wgs = g0 * s;
+        const double per_cu = double(wgs) / kCUs;
+        const double balance = per_cu / std::ceil(per_cu);
+        splits = s;
+        if (wgs >= kMinBlocks && balance >= 0.9) break;
+    }
+    cps = (nchunks + splits - 1) / splits;
+    splits = (nchunks + cps - 1) / cps;
+}
+
+static bool use_direct(const ConvGeom &g, const Variant &v)
+{
+    const int64_t x_bytes = int64_t(g.n) * g.c * g.h * g.w * 4;
+    return v.mode < 0 || x_bytes >= (int64_t(1) << 31) || forced_variant() == 0;
+}
+
+void describe_conv(const ConvGeom &g, char *buf, size_t len)
+{
+    int plane = 0;
+    size_t lds = 0;
+    const Variant v = choose_variant(g, plane, lds);
+    if (use_direct(g, v)) {
+        snprintf(buf, len, "direct");
+        return;
+    }
+    int tiles_p, tiles_k, nchunks, splits, cps;
+    plan_splits(g, v, tiles_p, tiles_k, nchunks, splits, cps);
+    if (v.mode == MODE_POINT)
+        snprintf(buf, len, "tiled point tm%d cc%d splits%d", v.tm, v.cc, splits);
+    else
+        snprintf(buf, len, "tiled window tm%d cc%d s%d gw%d splits%d", v.tm, v.cc, v.sk, v.gw,
+                 splits);
+}
+
+hipError_t run_conv(const ConvGeom &g, const int32_t *x, const uint32_t *wp, const int32_t *wi,
+                    const int32_t *bias, int32_t *y, Inner op, hipStream_t st)
+{
+    const int64_t x_bytes = int64_t(g.n) * g.c * g.h * g.w * 4;
+    int plane = 0;
+    size_t lds = 0;
+    const Variant v = choose_variant(g, plane, lds);
+    if (use_direct(g, v)) return run_direct(g, x, wp, wi, bias, y, op, st);
+
     const int RS = g.r * g.s;
-    const int nchunks = (g.c + v.cc - 1) / v.cc;
+    int tiles_p, tiles_k, nchunks, splits, cps;
+    plan_splits(g, v, tiles_p, tiles_k, nchunks, splits, cps);
     const int Jpad = nchunks * v.cc * RS;
-    const int tiles_k = (g.k + 4 * kTN - 1) / (4 * kTN);
     const int Kpad = tiles_k * 4 * kTN;
     const int64_t NQ = int64_t(g.n) * g.oh * g.ow;
-    const int tiles_p = int((NQ + P - 1) / P);
-    int splits = 1;
-    const int64_t g0 = int64_t(tiles_p) * tiles_k;
-    if (g0 < kTargetBlocks) splits = int(std::min<int64_t>(nchunks, (kTargetBlocks + g0 - 1) / g0));
-    const int cps = (nchunks + splits - 1) / splits;
-    splits = (nchunks + cps - 1) / cps;
-    const int64_t grid = g0 * splits;
+    const int64_t grid = int64_t(tiles_p) * tiles_k * splits;
     if (grid > INT32_MAX) return hipErrorInvalidValue;
 
     TiledParams p;
     p.N = g.n; p.C = g.c; p.H = g.h; p.W = g.w; p.K = g.k; p.R = g.r; p.S = g.s;
     p.sh = g.sh; p.sw = g.sw; p.ph = g.ph; p.pw = g.pw; p.OH = g.oh; p.OW = g.ow;
     p.OHOW = g.oh * g.ow; p.NQ = int(NQ); p.HW = g.h * g.w;
-    p.Jpad = Jpad; p.VH = VH; p.IWP = IWP; p.slots_max = slots_max;
+    p.Jpad = Jpad; p.VH = g.h + 2 * g.ph; p.IWP = g.w + 2 * g.pw; p.PLANE = plane;
     p.tiles_p = tiles_p; p.tiles_k = tiles_k; p.chunks_per_split = cps; p.nchunks = nchunks;
     p.atomic_out = splits > 1;
+    p.x_bytes = int(x_bytes);
     p.div_ohow = make_fastdiv(uint32_t(p.OHOW));
     p.div_ow = make_fastdiv(uint32_t(g.ow));
-    p.div_vh = make_fastdiv(uint32_t(VH));
+    p.div_vh = make_fastdiv(uint32_t(p.VH));
+    p.div_iwp = make_fastdiv(uint32_t(p.IWP));
 
     // Scratch: init[Kpad] then wd[Kpad][Jpad].
     const size_t init_bytes = (size_t(Kpad) * 4 + 255) & ~size_t(255);

@@ -25,9 +25,13 @@ hipError_t run_conv(const ConvGeom &g, const int32_t *x, const uint32_t *wpacked
                     const int32_t *wint, const int32_t *bias, int32_t *y, Inner op,
                     hipStream_t stream);
 
-// Kernel variant forced for testing: -1 = automatic choice, 0 = the
-// one-thread-per-output kernel, 1 = the tiled kernel. Set from the environment
-// variable DS_FORCE_VARIANT when the library loads.
+// Short name of the kernel run_conv would launch for g (see ds_conv2d_shift_describe).
+void describe_conv(const ConvGeom &g, char *buf, size_t len);
+
+// Kernel variant forced for testing and tuning, from the environment variable
+// DS_FORCE_VARIANT (read once): unset or -1 = automatic choice, 0 = the
+// one-thread-per-output kernel, 8 = tiled kernels with 8 pixels per lane
+// where an instance exists (the default is 4).
 int forced_variant();
 
 }  // namespace ds

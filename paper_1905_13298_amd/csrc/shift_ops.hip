@@ -21,19 +21,15 @@ bool device_range_ok(const void *p, int64_t bytes)
     return q >= b && q - b + uint64_t(bytes) <= uint64_t(size);
 }
 
-// Validates a convolution problem (both operators) and fills `g`.
-static ds_status check_conv(const void *x, const void *wts, const void *bias, const void *y,
-                            int64_t n, int64_t c, int64_t h, int64_t w, int64_t k, int64_t r,
-                            int64_t s, int32_t sh, int32_t sw, int32_t ph, int32_t pw,
-                            int32_t frac_bits, uint32_t flags, bool packed, ConvGeom &g)
+// Validates the sizes of a convolution problem and fills `g` (no pointers).
+static ds_status check_shape(int64_t n, int64_t c, int64_t h, int64_t w, int64_t k, int64_t r,
+                             int64_t s, int32_t sh, int32_t sw, int32_t ph, int32_t pw,
+                             bool packed, ConvGeom &g)
 {
-    if (!x || !wts || !y) return fail(DS_ERR_NULL_POINTER, "x, weights and y must not be NULL");
     if (n <= 0 || c <= 0 || h <= 0 || w <= 0 || k <= 0 || r <= 0 || s <= 0)
         return fail(DS_ERR_INVALID_SHAPE, "all sizes must be > 0");
     if (sh < 1 || sw < 1) return fail(DS_ERR_INVALID_ARG, "stride must be >= 1");
     if (ph < 0 || pw < 0) return fail(DS_ERR_INVALID_ARG, "padding must be >= 0");
-    if (frac_bits < 0 || frac_bits > 31) return fail(DS_ERR_INVALID_ARG, "frac_bits must be in [0, 31]");
-    if (flags != 0) return fail(DS_ERR_INVALID_ARG, "flags must be 0");
     if (h + 2 * int64_t(ph) < r || w + 2 * int64_t(pw) < s)
         return fail(DS_ERR_INVALID_SHAPE, "kernel larger than the padded input");
     const int64_t oh = (h + 2 * int64_t(ph) - r) / sh + 1;
@@ -44,15 +40,32 @@ static ds_status check_conv(const void *x, const void *wts, const void *bias, co
     if (crs < 0 || xe < 0 || ye < 0 || we < 0 || crs > kMaxElems || xe > kMaxElems ||
         ye > kMaxElems || we > kMaxElems || prod({k, crs}) > kMaxElems)
         return fail(DS_ERR_UNSUPPORTED, "tensors with 2^31 or more elements are not supported");
-    const int64_t xb = 4 * xe, yb = 4 * ye, wb = 4 * we, bb = 4 * k;
+    g = ConvGeom{int(n), int(c), int(h), int(w), int(k), int(r), int(s), sh, sw, ph, pw,
+                 int(oh), int(ow), int(crs)};
+    return DS_SUCCESS;
+}
+
+// Validates a convolution problem (both operators) and fills `g`.
+static ds_status check_conv(const void *x, const void *wts, const void *bias, const void *y,
+                            int64_t n, int64_t c, int64_t h, int64_t w, int64_t k, int64_t r,
+                            int64_t s, int32_t sh, int32_t sw, int32_t ph, int32_t pw,
+                            int32_t frac_bits, uint32_t flags, bool packed, ConvGeom &g)
+{
+    if (!x || !wts || !y) return fail(DS_ERR_NULL_POINTER, "x, weights and y must not be NULL");
+    ds_status st = check_shape(n, c, h, w, k, r, s, sh, sw, ph, pw, packed, g);
+    if (st != DS_SUCCESS) return st;
+    if (frac_bits < 0 || frac_bits > 31) return fail(DS_ERR_INVALID_ARG, "frac_bits must be in [0, 31]");
+    if (flags != 0) return fail(DS_ERR_INVALID_ARG, "flags must be 0");
+    const int64_t xb = 4 * int64_t(g.n) * g.c * g.h * g.w;
+    const int64_t yb = 4 * int64_t(g.n) * g.k * g.oh * g.ow;
+    const int64_t wb = 4 * (packed ? int64_t(g.k) * row_words(g.crs) : int64_t(g.k) * g.crs);
+    const int64_t bb = 4 * int64_t(g.k);
     if (overlap(y, yb, x, xb) || overlap(y, yb, wts, wb) || overlap(y, yb, bias, bb))
         return fail(DS_ERR_INVALID_ARG, "y overlaps an input");
     if (!device_range_ok(x, xb)) return fail(DS_ERR_INVALID_ARG, "x is not a device buffer of %lld bytes", (long long)xb);
     if (!device_range_ok(wts, wb)) return fail(DS_ERR_INVALID_ARG, "weights are not a device buffer of %lld bytes", (long long)wb);
     if (!device_range_ok(y, yb)) return fail(DS_ERR_INVALID_ARG, "y is not a device buffer of %lld bytes", (long long)yb);
     if (bias && !device_range_ok(bias, bb)) return fail(DS_ERR_INVALID_ARG, "bias is not a device buffer of %lld bytes", (long long)bb);
-    g = ConvGeom{int(n), int(c), int(h), int(w), int(k), int(r), int(s), sh, sw, ph, pw,
-                 int(oh), int(ow), int(crs)};
     return DS_SUCCESS;
 }
 
@@ -93,6 +106,20 @@ extern "C" ds_status ds_linear_shift(const int32_t *x, const uint32_t *w_packed,
     return hip_status(run_conv(g, x, w_packed, nullptr, bias, y, Inner::Shift,
                                static_cast<hipStream_t>(stream)),
                       "ds_linear_shift");
+}
+
+extern "C" ds_status ds_conv2d_shift_describe(int64_t n, int64_t c, int64_t h, int64_t w,
+                                              int64_t k, int64_t r, int64_t s, int32_t stride_h,
+                                              int32_t stride_w, int32_t pad_h, int32_t pad_w,
+                                              char *buf, int64_t len)
+{
+    if (!buf) return fail(DS_ERR_NULL_POINTER, "buf must not be NULL");
+    if (len < 1) return fail(DS_ERR_BUFFER_TOO_SMALL, "len must be >= 1");
+    ConvGeom g;
+    const ds_status st = check_shape(n, c, h, w, k, r, s, stride_h, stride_w, pad_h, pad_w, true, g);
+    if (st != DS_SUCCESS) return st;
+    describe_conv(g, buf, size_t(len));
+    return ok();
 }
 
 extern "C" ds_status ds_conv2d_mul_i32(const int32_t *x, const int32_t *wts, const int32_t *bias,

@@ -11,7 +11,7 @@ import torch
 
 from ._native import DeepShiftError, call, lib
 
-__all__ = ["DeepShiftError", "packed_row_words", "pack_shift_weights", "unpack_shift_weights",
+__all__ = ["DeepShiftError", "describe_conv2d", "packed_row_words", "pack_shift_weights", "unpack_shift_weights",
            "linear_shift", "conv2d_shift", "linear_mul_i32", "conv2d_mul_i32", "out_size"]
 
 
@@ -36,6 +36,18 @@ def unpack_shift_weights(packed, cols: int) -> np.ndarray:
     out = np.empty((rows, cols), dtype=np.uint8)
     call("ds_unpack_shift_weights", packed.ctypes.data, rows, cols, out.ctypes.data, out.size)
     return out
+
+
+def describe_conv2d(n, c, h, w, k, kernel_size, stride=1, padding=0) -> str:
+    """Name of the kernel the library runs for this ConvShift shape (LinearShift:
+    a 1x1 convolution with h = w = 1)."""
+    r, s = _pair(kernel_size)
+    sh, sw = _pair(stride)
+    ph, pw = _pair(padding)
+    import ctypes
+    buf = ctypes.create_string_buffer(128)
+    call("ds_conv2d_shift_describe", n, c, h, w, k, r, s, sh, sw, ph, pw, buf, len(buf))
+    return buf.value.decode()
 
 
 def _dev_i32(t: torch.Tensor, name: str) -> torch.Tensor:

@@ -143,3 +143,17 @@ def test_host_pointers_rejected_without_gpu_access():
                                         2, 4, 3, 16, 0, None)
     assert st in (ARG, HIP)
     assert np.all(y == 7)
+
+
+def test_describe_names_a_kernel_without_a_gpu():
+    assert ops.describe_conv2d(128, 64, 56, 56, 256, 1).startswith("tiled point")
+    assert ops.describe_conv2d(128, 64, 56, 56, 64, 3, 1, 1).startswith("tiled window")
+    assert ops.describe_conv2d(2, 3, 224, 224, 64, 7, 2, 3).startswith("tiled window")
+    assert ops.describe_conv2d(1, 3, 9, 9, 5, 4, 1, 1) == "direct"
+    lib = _native.lib()
+    import ctypes
+    buf = ctypes.create_string_buffer(4)
+    assert lib.ds_conv2d_shift_describe(1, 1, 1, 1, 1, 1, 1, 1, 1, 0, 0, buf, 4) == OK
+    assert len(buf.value) <= 3
+    assert lib.ds_conv2d_shift_describe(0, 1, 1, 1, 1, 1, 1, 1, 1, 0, 0, buf, 4) == SHAPE
+    assert lib.ds_conv2d_shift_describe(1, 1, 1, 1, 1, 1, 1, 1, 1, 0, 0, None, 4) == NULLP
