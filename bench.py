@@ -63,11 +63,32 @@ def parse():
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-mul", action="store_true")
     ap.add_argument("--layers-out", default=None, help="write per-layer timings (JSON) here")
+    ap.add_argument("--copy-only", type=int, default=0, metavar="BYTES",
+                    help="only run a device-to-device copy of BYTES (HBM counter calibration)")
     return ap.parse_args()
+
+
+def copy_only(nbytes: int) -> None:
+    """A plain device-to-device copy of a known size, three times: what the HBM
+    traffic counters read for it calibrates them."""
+    import torch
+    dev = torch.device("cuda:0")
+    n = nbytes // 4
+    src = torch.arange(n, dtype=torch.int32, device=dev)
+    dst = torch.empty_like(src)
+    torch.cuda.synchronize()
+    for _ in range(3):
+        dst.copy_(src)
+    torch.cuda.synchronize()
+    assert torch.equal(dst, src)
+    print(json.dumps({"copy_bytes": 4 * n, "repeats": 3}), flush=True)
 
 
 def main():
     args = parse()
+    if args.copy_only:
+        copy_only(args.copy_only)
+        return
     if args.gpus != 1:
         print(f"bench.py runs on one GPU only (asked for {args.gpus}); the shift operators need "
               "no cross-GPU exchange for a layer, see the design notes for how they shard.",

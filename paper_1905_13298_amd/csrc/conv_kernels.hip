@@ -28,10 +28,10 @@
 #include <hip/hip_runtime.h>
 
 #include <algorithm>
-#include <cmath>
 #include <cstdio>
 #include <cstdlib>
 #include <mutex>
+#include <type_traits>
 
 #include "conv_plan.hpp"
 
@@ -147,43 +147,43 @@ conv_direct_kernel(const int32_t *__restrict__ x, const uint32_t *__restrict__ w
 // ---------------------------------------------------------------------------
 // Preparation: decoded weights wd[kg][j][TN] (k = kg*TN + t) and init[k].
 // Rows k >= K and taps j >= C*R*S (the padding up to whole chunks) become
-// zero weights.
+// zero weights. init[k] adds back the one that each negative weight's
+// complement (x >> s) ^ -1 = -(x >> s) - 1 leaves out.
 
+// One launch, two roles: blocks [0, wblocks) decode weights (grid-stride over
+// wd), the remaining blocks compute init, one wave per row k.
 template <Inner OP, int TN>
 __global__ void __launch_bounds__(256)
-prep_weights_kernel(const uint32_t *__restrict__ wp, const int32_t *__restrict__ wi, int K,
-                    int CRS, int wpr, int Jpad, int Kpad, int32_t *__restrict__ wd)
+prep_kernel(const uint32_t *__restrict__ wp, const int32_t *__restrict__ wi,
+            const int32_t *__restrict__ bias, int K, int CRS, int wpr, int Jpad, int Kpad,
+            int wblocks, int32_t *__restrict__ wd, int32_t *__restrict__ init)
 {
-    const int64_t total = int64_t(Kpad) * Jpad;
-    for (int64_t idx = int64_t(blockIdx.x) * blockDim.x + threadIdx.x; idx < total;
-         idx += int64_t(gridDim.x) * blockDim.x) {
-        const int t = int(idx % TN);
-        const int64_t rest = idx / TN;
-        const int j = int(rest % Jpad);
-        const int k = int(rest / Jpad) * TN + t;
-        int32_t v;
-        if (k < K && j < CRS) {
-            if constexpr (OP == Inner::Shift) {
-                const uint32_t code = (wp[int64_t(k) * wpr + j / 6] >> (5 * (j % 6))) & 31u;
-                const uint32_t sh = code & 15u;
-                v = sh == 15u ? 31 : int32_t(sh | ((code >> 4) << 31));
+    if (int(blockIdx.x) < wblocks) {
+        const int64_t total = int64_t(Kpad) * Jpad;
+        for (int64_t idx = int64_t(blockIdx.x) * blockDim.x + threadIdx.x; idx < total;
+             idx += int64_t(wblocks) * blockDim.x) {
+            const int t = int(idx % TN);
+            const int64_t rest = idx / TN;
+            const int j = int(rest % Jpad);
+            const int k = int(rest / Jpad) * TN + t;
+            int32_t v;
+            if (k < K && j < CRS) {
+                if constexpr (OP == Inner::Shift) {
+                    const uint32_t code = (wp[int64_t(k) * wpr + j / 6] >> (5 * (j % 6))) & 31u;
+                    const uint32_t sh = code & 15u;
+                    v = sh == 15u ? 31 : int32_t(sh | ((code >> 4) << 31));
+                } else {
+                    v = wi[int64_t(k) * CRS + j];
+                }
             } else {
-                v = wi[int64_t(k) * CRS + j];
+                v = OP == Inner::Shift ? 31 : 0;
             }
-        } else {
-            v = OP == Inner::Shift ? 31 : 0;
+            wd[idx] = v;
         }
-        wd[idx] = v;
+        return;
     }
-}
-
-// init[k] = bias[k] + negcount[k] (shift) or bias[k] (multiply); one wave per row.
-template <Inner OP>
-__global__ void __launch_bounds__(256)
-prep_init_kernel(const uint32_t *__restrict__ wp, const int32_t *__restrict__ bias, int K,
-                 int CRS, int wpr, int Kpad, int32_t *__restrict__ init)
-{
-    const int k = blockIdx.x * 4 + int(threadIdx.x >> 6);
+    // init[k] = bias[k] + negcount[k] (shift) or bias[k] (multiply)
+    const int k = (int(blockIdx.x) - wblocks) * 4 + int(threadIdx.x >> 6);
     const int lane = threadIdx.x & 63;
     if (k >= Kpad) return;
     uint32_t cnt = 0;
@@ -429,9 +429,11 @@ tiled_kernel(const int32_t *__restrict__ x, const int32_t *__restrict__ wd,
             }
         }
     };
-    // Wait for this wave's copies into buffer `bf`, then publish the OR of their signs.
-    auto check = [&](int bf) {
+    // Wait for this wave's copies into buffer `bf`; with `publish`, also tell the
+    // other waves whether any word it brought in is negative.
+    auto land = [&](int bf, bool publish) {
         asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
+        if (!publish) return;
         const int32_t *src = lds + bf * BUF;
         int32_t o = 0;
         if constexpr (MODE == MODE_WINDOW) {
@@ -457,33 +459,45 @@ tiled_kernel(const int32_t *__restrict__ x, const int32_t *__restrict__ wd,
 #pragma unroll
         for (int t = 0; t < TN; ++t) acc[i][t] = 0u;
 
-    const int ch_begin = z * p.chunks_per_split;
-    const int ch_end = min(p.nchunks, ch_begin + p.chunks_per_split);
-
-    issue(ch_begin, 0);
-    check(0);
-    __syncthreads();
-    for (int ch = ch_begin; ch < ch_end; ++ch) {
-        const int bf = (ch - ch_begin) & 1;
-        const bool more = ch + 1 < ch_end;
-        if (more) issue(ch + 1, bf ^ 1);
-        const bool sgn = OP == Inner::Shift &&
-                         (neg_flag[bf][0] | neg_flag[bf][1] | neg_flag[bf][2] | neg_flag[bf][3]);
+    auto compute = [&](auto signed_tag, int ch, int bf) {
+        constexpr bool SG = decltype(signed_tag)::value;
         const int32_t *buf = lds + bf * BUF;
         const int32_t *__restrict__ wk =
             wrow + size_t(ch * CC) * (MODE == MODE_WINDOW ? p.R * SK : 1) * TN;
-        if constexpr (MODE == MODE_WINDOW) {
-            if (sgn)
-                compute_window<OP, true, TM, TN, CC, SK>(acc, buf, base, wk, p.R, p.PLANE, p.IWP);
-            else
-                compute_window<OP, false, TM, TN, CC, SK>(acc, buf, base, wk, p.R, p.PLANE, p.IWP);
-        } else {
-            if (sgn)
-                compute_point<OP, true, TM, TN, CC>(acc, buf, lane, wk);
-            else
-                compute_point<OP, false, TM, TN, CC>(acc, buf, lane, wk);
+        if constexpr (MODE == MODE_WINDOW)
+            compute_window<OP, SG, TM, TN, CC, SK>(acc, buf, base, wk, p.R, p.PLANE, p.IWP);
+        else
+            compute_point<OP, SG, TM, TN, CC>(acc, buf, lane, wk);
+    };
+
+    const int ch_begin = z * p.chunks_per_split;
+    const int ch_end = min(p.nchunks, ch_begin + p.chunks_per_split);
+    constexpr bool SHIFT = OP == Inner::Shift;
+
+    // Two phases, so that neither chunk loop chooses between compute paths:
+    // chunks take the two-instruction form until one holds a negative input,
+    // and every chunk from there on takes the three-instruction form.
+    issue(ch_begin, 0);
+    land(0, SHIFT);
+    __syncthreads();
+    int ch = ch_begin;
+    if constexpr (SHIFT) {
+        for (; ch < ch_end; ++ch) {
+            const int bf = (ch - ch_begin) & 1;
+            if (neg_flag[bf][0] | neg_flag[bf][1] | neg_flag[bf][2] | neg_flag[bf][3]) break;
+            const bool more = ch + 1 < ch_end;
+            if (more) issue(ch + 1, bf ^ 1);
+            compute(std::false_type{}, ch, bf);
+            if (more) land(bf ^ 1, true);
+            __syncthreads();
         }
-        if (more) check(bf ^ 1);
+    }
+    for (; ch < ch_end; ++ch) {
+        const int bf = (ch - ch_begin) & 1;
+        const bool more = ch + 1 < ch_end;
+        if (more) issue(ch + 1, bf ^ 1);
+        compute(std::integral_constant<bool, SHIFT>{}, ch, bf);
+        if (more) land(bf ^ 1, false);
         __syncthreads();
     }
 
@@ -510,8 +524,8 @@ tiled_kernel(const int32_t *__restrict__ x, const int32_t *__restrict__ wd,
 
 constexpr int kTN = 8;              // output channels per wave (scalar weights per tap)
 constexpr int kLdsLimit = 64 * 1024;
-constexpr int kCUs = 256;           // compute units of an MI355X
-constexpr int kMinBlocks = 1024;    // four workgroups (16 waves) per CU
+constexpr int kFullGrid = 3000;     // workgroups that keep 256 CUs busy without a split
+constexpr int kSplitGrid = 4096;    // workgroups to aim for when splitting (16 per CU)
 
 struct Variant {
     int mode, tm, cc, sk, gw;
@@ -647,18 +661,15 @@ static void plan_splits(const ConvGeom &g, const Variant &v, int &tiles_p, int &
     tiles_k = (g.k + 4 * kTN - 1) / (4 * kTN);
     const int64_t NQ = int64_t(g.n) * g.oh * g.ow;
     tiles_p = int((NQ + P - 1) / P);
-    // Split the reduction when the tiles alone leave CUs idle: take the smallest
-    // split that gives at least kMinBlocks workgroups and spreads them over the
-    // CUs with at least 90 % balance (mean over maximum workgroups per CU),
-    // keeping at least two chunks per split.
+    // Split the reduction when the tiles alone are too few to keep every CU at
+    // full residency for most of the kernel (measured on MI355X: grids of
+    // fewer than ~3000 workgroups lose 10-30 %; about 16 workgroups per CU
+    // recovers it), keeping at least four chunks per split.
     const int64_t g0 = int64_t(tiles_p) * tiles_k;
     splits = 1;
-    for (int s = 1; s <= 16 && s <= std::max(1, nchunks / 2); ++s) {
-        const int64_t wgs = g0 * s;
-        const double per_cu = double(wgs) / kCUs;
-        const double balance = per_cu / std::ceil(per_cu);
-        splits = s;
-        if (wgs >= kMinBlocks && balance >= 0.9) break;
+    if (g0 < kFullGrid) {
+        const int64_t want = (kSplitGrid + g0 - 1) / g0;
+        splits = int(std::max<int64_t>(1, std::min<int64_t>(want, nchunks / 4)));
     }
     cps = (nchunks + splits - 1) / splits;
     splits = (nchunks + cps - 1) / cps;
@@ -730,18 +741,14 @@ hipError_t run_conv(const ConvGeom &g, const int32_t *x, const uint32_t *wp, con
     const int wpr = (g.crs + 5) / 6;
 
     const int64_t pw_total = int64_t(Kpad) * Jpad;
-    const int pgrid = int(std::min<int64_t>((pw_total + 255) / 256, 8192));
-    if (op == Inner::Shift) {
-        hipLaunchKernelGGL((prep_weights_kernel<Inner::Shift, kTN>), dim3(pgrid), dim3(256), 0, st,
-                           wp, wi, g.k, g.crs, wpr, Jpad, Kpad, wd);
-        hipLaunchKernelGGL(prep_init_kernel<Inner::Shift>, dim3((Kpad + 3) / 4), dim3(256), 0, st,
-                           wp, bias, g.k, g.crs, wpr, Kpad, init);
-    } else {
-        hipLaunchKernelGGL((prep_weights_kernel<Inner::Mul, kTN>), dim3(pgrid), dim3(256), 0, st,
-                           wp, wi, g.k, g.crs, wpr, Jpad, Kpad, wd);
-        hipLaunchKernelGGL(prep_init_kernel<Inner::Mul>, dim3((Kpad + 3) / 4), dim3(256), 0, st,
-                           wp, bias, g.k, g.crs, wpr, Kpad, init);
-    }
+    const int wblocks = int(std::min<int64_t>((pw_total + 255) / 256, 4096));
+    const int pgrid = wblocks + (Kpad + 3) / 4;
+    if (op == Inner::Shift)
+        hipLaunchKernelGGL((prep_kernel<Inner::Shift, kTN>), dim3(pgrid), dim3(256), 0, st, wp, wi,
+                           bias, g.k, g.crs, wpr, Jpad, Kpad, wblocks, wd, init);
+    else
+        hipLaunchKernelGGL((prep_kernel<Inner::Mul, kTN>), dim3(pgrid), dim3(256), 0, st, wp, wi,
+                           bias, g.k, g.crs, wpr, Jpad, Kpad, wblocks, wd, init);
     e = hipGetLastError();
     if (e == hipSuccess && p.atomic_out) {
         const int64_t total = int64_t(g.n) * g.k * p.OHOW;
