@@ -65,7 +65,77 @@ def parse():
     ap.add_argument("--layers-out", default=None, help="write per-layer timings (JSON) here")
     ap.add_argument("--copy-only", type=int, default=0, metavar="BYTES",
                     help="only run a device-to-device copy of BYTES (HBM counter calibration)")
+    ap.add_argument("--pmc-summary", nargs=4, metavar=("COPY_FETCH", "COPY_WRITE", "FETCH", "WRITE"),
+                    help="turn rocprofv3 --pmc CSV directories into the HBM traffic record")
+    ap.add_argument("--pmc-copy-bytes", type=int, default=1 << 30)
+    ap.add_argument("--pmc-out", default=TRAFFIC_FILE)
     return ap.parse_args()
+
+
+KERNEL_SOURCE = os.path.join(ROOT, "paper_1905_13298_amd", "csrc", "conv_kernels.hip")
+TRAFFIC_FILE = os.path.join(ROOT, "profiles", "hbm_traffic_resnet50_n128.json")
+
+
+def kernel_source_hash() -> str:
+    import hashlib
+    with open(KERNEL_SOURCE, "rb") as f:
+        return hashlib.sha256(f.read()).hexdigest()[:16]
+
+
+def _pmc_rows(directory: str):
+    """Per-dispatch counter sums from a rocprofv3 --pmc CSV directory."""
+    import csv
+    import glob
+    (path,) = glob.glob(os.path.join(directory, "*counter_collection.csv"))
+    rows = {}
+    for r in csv.DictReader(open(path)):
+        e = rows.setdefault(int(r["Dispatch_Id"]), {"name": r["Kernel_Name"], "ctr": {}})
+        e["ctr"][r["Counter_Name"]] = e["ctr"].get(r["Counter_Name"], 0.0) + float(r["Counter_Value"])
+    return [rows[k] for k in sorted(rows)]
+
+
+def pmc_summary(copy_fetch, copy_write, fetch, write, copy_bytes, workload, out):
+    """HBM traffic of the tiled kernels from FETCH_SIZE/WRITE_SIZE runs (KiB per
+    dispatch), each scaled by what the same counter reads for a plain copy of
+    copy_bytes (the largest copy dispatch in the calibration runs)."""
+    from paper_1905_13298_amd import workloads as W
+    cf = max(r["ctr"]["FETCH_SIZE"] for r in _pmc_rows(copy_fetch) if "copyBuffer" in r["name"])
+    cw = max(r["ctr"]["WRITE_SIZE"] for r in _pmc_rows(copy_write) if "copyBuffer" in r["name"])
+    fetch_scale = copy_bytes / (cf * 1024.0)
+    write_scale = copy_bytes / (cw * 1024.0)
+    layers = W.config_layers(WORKLOADS[workload])
+    f_rows = [r for r in _pmc_rows(fetch) if "tiled_kernel" in r["name"]][-len(layers):]
+    w_rows = [r for r in _pmc_rows(write) if "tiled_kernel" in r["name"]][-len(layers):]
+    per_kernel = {}
+    for L, fr, wr in zip(layers, f_rows, w_rows):
+        name = kernel_variant(L).rsplit(" splits", 1)[0]
+        k = per_kernel.setdefault(name, {"launches": 0, "fetch_bytes": 0.0, "write_bytes": 0.0,
+                                          "algorithmic_bytes": 0})
+        k["launches"] += 1
+        k["fetch_bytes"] += fr["ctr"]["FETCH_SIZE"] * 1024.0 * fetch_scale
+        k["write_bytes"] += wr["ctr"]["WRITE_SIZE"] * 1024.0 * write_scale
+        k["algorithmic_bytes"] += algorithmic_bytes(L)
+    rec = {"workload": W.CONFIG_NAMES[WORKLOADS[workload]], "kernel_source_sha256_16": kernel_source_hash(),
+           "copy_bytes": copy_bytes, "fetch_scale": round(fetch_scale, 4),
+           "write_scale": round(write_scale, 4), "kernels": per_kernel}
+    with open(out, "w") as f:
+        json.dump(rec, f, indent=1)
+    print(json.dumps(rec))
+
+
+def measured_traffic(kernel: str):
+    """HBM bytes per launch of `kernel` from the committed counter record, or None
+    when there is none or the kernel source changed since it was taken."""
+    try:
+        rec = json.load(open(TRAFFIC_FILE))
+    except (OSError, ValueError):
+        return None
+    if rec.get("kernel_source_sha256_16") != kernel_source_hash():
+        return None
+    k = rec["kernels"].get(kernel)
+    if not k:
+        return None
+    return (k["fetch_bytes"] + k["write_bytes"]) / k["launches"]
 
 
 def copy_only(nbytes: int) -> None:
@@ -88,6 +158,9 @@ def main():
     args = parse()
     if args.copy_only:
         copy_only(args.copy_only)
+        return
+    if args.pmc_summary:
+        pmc_summary(*args.pmc_summary, args.pmc_copy_bytes, args.workload, args.pmc_out)
         return
     if args.gpus != 1:
         print(f"bench.py runs on one GPU only (asked for {args.gpus}); the shift operators need "
@@ -177,9 +250,13 @@ def main():
         g["bytes"] += algorithmic_bytes(L)
     dom_name, dom = max(groups.items(), key=lambda kv: kv[1]["ms"])
     achieved = dom["sac"] / (dom["ms"] * 1e-3) / 1e12
+    traffic = measured_traffic(dom_name)
     roofline = {
         "bound": "alu", "achieved": round(achieved, 4), "peak": round(SAC_PEAK_T, 4),
-        "unit": "TSAC/s", "frac": round(achieved / SAC_PEAK_T, 4), "traffic": None,
+        "unit": "TSAC/s", "frac": round(achieved / SAC_PEAK_T, 4),
+        "traffic": None if traffic is None else int(traffic),
+        "traffic_unit": "HBM bytes per launch (FETCH_SIZE + WRITE_SIZE, copy-calibrated)",
+        "algorithmic_bytes_per_launch": dom["bytes"] // dom["launches"],
         "kernel": dom_name, "launches_per_step": dom["launches"],
         "avg_launch_ms": round(dom["ms"] / dom["launches"], 5),
         "sac_per_launch_avg": dom["sac"] // dom["launches"],
