@@ -212,6 +212,26 @@ fill_init_kernel(const int32_t *__restrict__ init, int32_t *__restrict__ y, int6
         y[idx] = init[(idx / OHOW) % K];
 }
 
+// xt[c][b] = x[b][c] for a row-major x [rows][cols]: 64 x 64 tiles through LDS,
+// so that both the reads and the writes are coalesced.
+__global__ void __launch_bounds__(256)
+transpose_kernel(const int32_t *__restrict__ x, int32_t *__restrict__ xt, int rows, int cols)
+{
+    __shared__ int32_t tile[64][65];
+    const int tiles_c = (cols + 63) / 64;
+    const int c0 = int(blockIdx.x % tiles_c) * 64, r0 = int(blockIdx.x / tiles_c) * 64;
+    const int tx = threadIdx.x & 63, ty = threadIdx.x >> 6;
+    for (int i = ty; i < 64; i += 4) {
+        const int r = r0 + i, c = c0 + tx;
+        if (r < rows && c < cols) tile[i][tx] = x[int64_t(r) * cols + c];
+    }
+    __syncthreads();
+    for (int i = ty; i < 64; i += 4) {
+        const int c = c0 + i, r = r0 + tx;
+        if (c < cols && r < rows) xt[int64_t(c) * rows + r] = tile[tx][i];
+    }
+}
+
 // ---------------------------------------------------------------------------
 // Tiled kernel.
 //
@@ -664,12 +684,14 @@ static void plan_splits(const ConvGeom &g, const Variant &v, int &tiles_p, int &
     // Split the reduction when the tiles alone are too few to keep every CU at
     // full residency for most of the kernel (measured on MI355X: grids of
     // fewer than ~3000 workgroups lose 10-30 %; about 16 workgroups per CU
-    // recovers it), keeping at least four chunks per split.
+    // recovers it), keeping at least four chunks per split unless the grid is
+    // so small that latency, not throughput, decides.
     const int64_t g0 = int64_t(tiles_p) * tiles_k;
     splits = 1;
     if (g0 < kFullGrid) {
         const int64_t want = (kSplitGrid + g0 - 1) / g0;
-        splits = int(std::max<int64_t>(1, std::min<int64_t>(want, nchunks / 4)));
+        const int64_t cap = g0 >= 64 ? nchunks / 4 : nchunks;  // tiny grids: any split
+        splits = int(std::max<int64_t>(1, std::min<int64_t>(want, cap)));
     }
     cps = (nchunks + splits - 1) / splits;
     splits = (nchunks + cps - 1) / cps;
@@ -681,8 +703,28 @@ static bool use_direct(const ConvGeom &g, const Variant &v)
     return v.mode < 0 || x_bytes >= (int64_t(1) << 31) || forced_variant() == 0;
 }
 
-void describe_conv(const ConvGeom &g, char *buf, size_t len)
+// A problem on 1 x 1 inputs with 1 x 1 taps (LinearShift, x [n][c]) runs on the
+// transposed input x^T [c][n] as one image of width n, so that the copies into
+// LDS read consecutive words, and produces y^T [k][n], whose stores (and
+// split-K atomics) are consecutive too; a transpose then gives y [n][k].
+static ConvGeom tiled_geometry(const ConvGeom &g, bool &rowmajor)
 {
+    rowmajor = g.h == 1 && g.w == 1 && g.r == 1 && g.s == 1 && g.ph == 0 && g.pw == 0;
+    if (!rowmajor) return g;
+    ConvGeom t = g;
+    t.n = 1;
+    t.h = 1;
+    t.w = g.n;
+    t.sh = t.sw = 1;
+    t.oh = 1;
+    t.ow = g.n;
+    return t;
+}
+
+void describe_conv(const ConvGeom &g0, char *buf, size_t len)
+{
+    bool rowmajor = false;
+    const ConvGeom g = tiled_geometry(g0, rowmajor);
     int plane = 0;
     size_t lds = 0;
     const Variant v = choose_variant(g, plane, lds);
@@ -693,20 +735,23 @@ void describe_conv(const ConvGeom &g, char *buf, size_t len)
     int tiles_p, tiles_k, nchunks, splits, cps;
     plan_splits(g, v, tiles_p, tiles_k, nchunks, splits, cps);
     if (v.mode == MODE_POINT)
-        snprintf(buf, len, "tiled point tm%d cc%d splits%d", v.tm, v.cc, splits);
+        snprintf(buf, len, "tiled point%s tm%d cc%d splits%d", rowmajor ? " transposed" : "", v.tm,
+                 v.cc, splits);
     else
         snprintf(buf, len, "tiled window tm%d cc%d s%d gw%d splits%d", v.tm, v.cc, v.sk, v.gw,
                  splits);
 }
 
-hipError_t run_conv(const ConvGeom &g, const int32_t *x, const uint32_t *wp, const int32_t *wi,
+hipError_t run_conv(const ConvGeom &g0, const int32_t *x, const uint32_t *wp, const int32_t *wi,
                     const int32_t *bias, int32_t *y, Inner op, hipStream_t st)
 {
+    bool rowmajor = false;
+    const ConvGeom g = tiled_geometry(g0, rowmajor);
     const int64_t x_bytes = int64_t(g.n) * g.c * g.h * g.w * 4;
     int plane = 0;
     size_t lds = 0;
     const Variant v = choose_variant(g, plane, lds);
-    if (use_direct(g, v)) return run_direct(g, x, wp, wi, bias, y, op, st);
+    if (use_direct(g, v)) return run_direct(g0, x, wp, wi, bias, y, op, st);
 
     const int RS = g.r * g.s;
     int tiles_p, tiles_k, nchunks, splits, cps;
@@ -730,14 +775,28 @@ hipError_t run_conv(const ConvGeom &g, const int32_t *x, const uint32_t *wp, con
     p.div_vh = make_fastdiv(uint32_t(p.VH));
     p.div_iwp = make_fastdiv(uint32_t(p.IWP));
 
-    // Scratch: init[Kpad] then wd[Kpad][Jpad].
+    // Scratch: init[Kpad], wd[Kpad][Jpad], and x^T for row-major inputs.
     const size_t init_bytes = (size_t(Kpad) * 4 + 255) & ~size_t(255);
-    const size_t bytes = init_bytes + size_t(Kpad) * Jpad * 4;
+    const size_t wd_bytes = (size_t(Kpad) * Jpad * 4 + 255) & ~size_t(255);
+    const size_t xt_bytes = rowmajor ? (size_t(x_bytes) + 255) & ~size_t(255) : 0;
+    const size_t yt_bytes = rowmajor ? size_t(g0.n) * g0.k * 4 : 0;
+    const size_t bytes = init_bytes + wd_bytes + xt_bytes + yt_bytes;
     void *scratch = nullptr;
     hipError_t e = scratch_alloc(&scratch, bytes, st);
     if (e != hipSuccess) return e;
     int32_t *init = static_cast<int32_t *>(scratch);
     int32_t *wd = reinterpret_cast<int32_t *>(static_cast<char *>(scratch) + init_bytes);
+    const int32_t *xin = x;
+    int32_t *yout = y;
+    if (rowmajor) {
+        yout = reinterpret_cast<int32_t *>(static_cast<char *>(scratch) + init_bytes + wd_bytes +
+                                           xt_bytes);
+        int32_t *xt = reinterpret_cast<int32_t *>(static_cast<char *>(scratch) + init_bytes + wd_bytes);
+        const int64_t tiles = int64_t((g0.c + 63) / 64) * ((g0.n + 63) / 64);
+        hipLaunchKernelGGL(transpose_kernel, dim3(unsigned(tiles)), dim3(256), 0, st, x, xt, g0.n,
+                           g0.c);
+        xin = xt;
+    }
     const int wpr = (g.crs + 5) / 6;
 
     const int64_t pw_total = int64_t(Kpad) * Jpad;
@@ -753,14 +812,20 @@ hipError_t run_conv(const ConvGeom &g, const int32_t *x, const uint32_t *wp, con
     if (e == hipSuccess && p.atomic_out) {
         const int64_t total = int64_t(g.n) * g.k * p.OHOW;
         const int fgrid = int(std::min<int64_t>((total + 255) / 256, 8192));
-        hipLaunchKernelGGL(fill_init_kernel, dim3(fgrid), dim3(256), 0, st, init, y, total, g.k,
+        hipLaunchKernelGGL(fill_init_kernel, dim3(fgrid), dim3(256), 0, st, init, yout, total, g.k,
                            p.OHOW);
         e = hipGetLastError();
     }
     if (e == hipSuccess) {
         e = op == Inner::Shift
-                ? dispatch_tiled<Inner::Shift>(v, p, int(grid), lds, x, wd, init, y, st)
-                : dispatch_tiled<Inner::Mul>(v, p, int(grid), lds, x, wd, init, y, st);
+                ? dispatch_tiled<Inner::Shift>(v, p, int(grid), lds, xin, wd, init, yout, st)
+                : dispatch_tiled<Inner::Mul>(v, p, int(grid), lds, xin, wd, init, yout, st);
+    }
+    if (e == hipSuccess && rowmajor) {
+        const int64_t tiles = int64_t((g0.n + 63) / 64) * ((g0.k + 63) / 64);
+        hipLaunchKernelGGL(transpose_kernel, dim3(unsigned(tiles)), dim3(256), 0, st, yout, y, g0.k,
+                           g0.n);
+        e = hipGetLastError();
     }
     const hipError_t ef = hipFreeAsync(scratch, st);
     return e != hipSuccess ? e : ef;
