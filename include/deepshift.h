@@ -114,6 +114,45 @@ ds_status ds_conv2d_shift(const int32_t *x, const uint32_t *w_packed, const int3
                           int32_t stride_h, int32_t stride_w, int32_t pad_h, int32_t pad_w,
                           int32_t frac_bits, uint32_t flags, void *stream);
 
+/* DeepShift-Q weight conversion (Section 3, Eqs. 4-5; range of Section 4):
+ * float weights w -> packed codes of flip(2^p, s) with
+ *     s = sign(w),  p = round(log2|w|) clipped to -max_shift .. 0.
+ * round(log2|w|) is evaluated exactly (no float log): it has no ties for a
+ * float w. w = +-0 and NaN give the zero weight (code 15); +-inf gives p = 0.
+ * w        device float32 [rows][cols] (a weight row per output channel, as
+ *          the compute entry points expect: cols = in_features or c*r*s)
+ * max_shift in [0, 14]: 14 is the 5-bit format; smaller values give the
+ *          shorter shift ranges of Section 4
+ * w_packed device uint32 [rows][ds_packed_row_words(cols)], written
+ * flags    reserved, must be 0; stream as for ds_linear_shift.
+ * Errors: NULL pointer, rows/cols <= 0, max_shift out of range, output
+ * overlapping the input, buffers that are not device allocations of the
+ * required size, 2^31 or more elements. */
+ds_status ds_quantize_shift_weights_q(const float *w, int64_t rows, int64_t cols,
+                                      int32_t max_shift, uint32_t *w_packed,
+                                      uint32_t flags, void *stream);
+
+/* DeepShift-PS weight conversion (Section 3): from the shift parameters P and
+ * the sign parameters S (device float32, both [rows][cols]):
+ *     p = round(P) clipped to -max_shift .. 0,
+ *     s = -1 if S <= -0.5, 0 if -0.5 < S < 0.5, +1 if S >= 0.5.
+ * round() takes halves away from zero, the tie rule the sign thresholds state.
+ * A NaN in P or S gives the zero weight. Other arguments and errors as for
+ * ds_quantize_shift_weights_q. */
+ds_status ds_quantize_shift_weights_ps(const float *p, const float *s, int64_t rows,
+                                       int64_t cols, int32_t max_shift, uint32_t *w_packed,
+                                       uint32_t flags, void *stream);
+
+/* Fixed-point rounding of activations and bias (Section 4: 32-bit words with
+ * 16 fractional bits):
+ *     y[i] = round(x[i] * 2^frac_bits)
+ * halves away from zero, saturated to [-2^31, 2^31 - 1]; NaN gives 0.
+ * x device float32 [n]; y device int32 [n], written; y == x (in place) is
+ * allowed, any other overlap is an error. frac_bits in [0, 31]; flags must be
+ * 0; stream as for ds_linear_shift. */
+ds_status ds_to_fixed_point(const float *x, int64_t n, int32_t frac_bits, int32_t *y,
+                            uint32_t flags, void *stream);
+
 /* Multiplication-based comparison operators. Not part of DeepShift: they run
  * the same tiling as the shift operators with a 32-bit integer multiply in
  * place of the shift, so that the two inner loops can be timed side by side

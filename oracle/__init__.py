@@ -49,6 +49,9 @@ def _load():
         lib.oracle_conv2d_mul.argtypes = [_P, _P, _P, _P] + [_I] * 11
         lib.oracle_pack_codes.argtypes = [_P, _I, _I, _P]
         lib.oracle_unpack_codes.argtypes = [_P, _I, _I, _P]
+        lib.oracle_quantize_q.argtypes = [_P, _I, ctypes.c_int, _P]
+        lib.oracle_quantize_ps.argtypes = [_P, _P, _I, ctypes.c_int, _P]
+        lib.oracle_to_fixed.argtypes = [_P, _I, ctypes.c_int, _P]
         _lib = lib
     return _lib
 
@@ -175,4 +178,31 @@ def unpack_codes(packed, cols):
     rows = packed.shape[0]
     out = np.empty((rows, cols), np.uint8)
     _load().oracle_unpack_codes(_ptr(packed), rows, cols, _ptr(out))
+    return out
+
+
+def quantize_q(w, max_shift=14):
+    """DeepShift-Q codes of float32 weights (any shape): sign(w), round(log2|w|) clipped
+    to -max_shift .. 0."""
+    w = np.ascontiguousarray(w, dtype=np.float32)
+    out = np.empty(w.shape, np.uint8)
+    _load().oracle_quantize_q(_ptr(w), w.size, int(max_shift), _ptr(out))
+    return out
+
+
+def quantize_ps(P, S, max_shift=14):
+    """DeepShift-PS codes from float32 shift and sign parameters of the same shape."""
+    P = np.ascontiguousarray(P, dtype=np.float32)
+    S = np.ascontiguousarray(S, dtype=np.float32)
+    assert P.shape == S.shape
+    out = np.empty(P.shape, np.uint8)
+    _load().oracle_quantize_ps(_ptr(P), _ptr(S), P.size, int(max_shift), _ptr(out))
+    return out
+
+
+def to_fixed(x, frac_bits=16):
+    """round(x * 2**F), halves away from zero, saturated to int32 (NaN -> 0)."""
+    x = np.ascontiguousarray(x, dtype=np.float32)
+    out = np.empty(x.shape, np.int32)
+    _load().oracle_to_fixed(_ptr(x), x.size, int(frac_bits), _ptr(out))
     return out

@@ -38,10 +38,14 @@
  * (brute force with exact rationals, the closed form against a float64
  * library convolution on inputs divisible by 2^15, a library arithmetic
  * shift, the one-sided rounding bound, zero-code and sign-flip invariants,
- * and hand-derived packed words).
+ * and hand-derived packed words). The converter functions at the end are
+ * pinned against numpy's float64 log2/round, exact rational rounding, the
+ * paper's second form of the ternary sign (sign of round(S)), the
+ * nearest-power property, and hand-derived examples.
  */
 #include <stdint.h>
 #include <stddef.h>
+#include <math.h>
 
 /* floor(x / 2^c) for 0 <= c <= 14, by integer division (Eq. 1, reading: floor). */
 static int64_t floor_div_pow2(int64_t x, int c)
@@ -215,4 +219,83 @@ void oracle_unpack_codes(const uint32_t *packed, int64_t rows, int64_t cols, uin
         for (int64_t col = 0; col < cols; ++col)
             codes[r * cols + col] =
                 (uint8_t)((packed[r * wpr + col / 6] >> (5 * (col % 6))) & 31u);
+}
+
+/* ------------------------------------------------------------------------
+ * Float -> weight code converter and fixed-point conversion.
+ *
+ * DeepShift-Q (Section 3, Eqs. 4-5): s = sign(w), p = round(log2|w|).
+ * DeepShift-PS (Section 3): p = round(P), s = -1 if S <= -0.5, 0 if
+ * -0.5 < S < 0.5, +1 if S >= 0.5.
+ * Both clip p to the supported range -max_shift .. 0 (Section 4; 14 for the
+ * 5-bit format). Inputs and bias are rounded to fixed point with F fractional
+ * bits (Section 4, 16.16).
+ *
+ * Readings where the paper is silent:
+ *   - The only tie rule the paper states is the one for the sign (+-0.5 go to
+ *     +-1, i.e. halves away from zero); round(P) and the fixed-point rounding
+ *     use the same rule. round(log2|w|) has no ties for a float w (log2|w| =
+ *     p + 1/2 would need |w| = 2^p * sqrt(2), which is irrational).
+ *   - w = +-0 has sign 0, i.e. the zero weight. A NaN (w, P or S) also gives
+ *     the zero weight; w = +-inf gives p = 0 after clipping.
+ *   - Fixed point saturates to the int32 range; NaN gives 0.
+ */
+
+/* round(log2|w|) for finite w != 0, evaluated exactly: with p = floor(log2|w|),
+ * |w| lies in [2^p, 2^(p+1)) and rounds up iff |w| >= 2^(p + 1/2), i.e. iff
+ * w^2 >= 2^(2p+1). Both sides are exact in double for a float w. */
+static int round_log2_abs(float w)
+{
+    int e;
+    (void)frexp(fabs((double)w), &e);        /* |w| = m * 2^e with m in [0.5, 1) */
+    const int p = e - 1;                     /* floor(log2|w|) */
+    const double w2 = (double)w * (double)w;
+    return (w2 >= ldexp(1.0, 2 * p + 1)) ? p + 1 : p;
+}
+
+/* Code of flip(2^p, s) with p clipped to -max_shift .. 0; s = 0 -> code 15. */
+static uint8_t code_of(int p, int s, int max_shift)
+{
+    if (s == 0) return 15;
+    if (p > 0) p = 0;
+    if (p < -max_shift) p = -max_shift;
+    return (uint8_t)((s < 0 ? 16 : 0) | (-p));
+}
+
+/* DeepShift-Q codes of n float weights (any layout; one code per weight). */
+void oracle_quantize_q(const float *w, int64_t n, int max_shift, uint8_t *codes)
+{
+    for (int64_t i = 0; i < n; ++i) {
+        const float v = w[i];
+        int s = (v > 0.0f) - (v < 0.0f);     /* sign(w); NaN -> 0 */
+        int p = (s == 0 || isinf(v)) ? 0 : round_log2_abs(v);
+        codes[i] = code_of(p, s, max_shift);
+    }
+}
+
+/* DeepShift-PS codes from the shift parameters P and sign parameters S. */
+void oracle_quantize_ps(const float *P, const float *S, int64_t n, int max_shift, uint8_t *codes)
+{
+    for (int64_t i = 0; i < n; ++i) {
+        const float sv = S[i];
+        int s = sv <= -0.5f ? -1 : (sv >= 0.5f ? 1 : 0);   /* NaN -> 0 */
+        const double r = round((double)P[i]);              /* halves away from zero */
+        if (isnan(r)) s = 0;
+        int p = (r > 0.0) ? 0 : (r < -64.0 ? -64 : (int)r);
+        codes[i] = code_of(p, s, max_shift);
+    }
+}
+
+/* Fixed point with F fractional bits: round(x * 2^F), halves away from zero,
+ * saturated to int32; NaN -> 0. */
+void oracle_to_fixed(const float *x, int64_t n, int frac_bits, int32_t *out)
+{
+    for (int64_t i = 0; i < n; ++i) {
+        const double v = (double)x[i];
+        if (isnan(v)) { out[i] = 0; continue; }
+        const double t = round(ldexp(v, frac_bits));
+        if (t >= 2147483647.0) out[i] = 2147483647;
+        else if (t <= -2147483648.0) out[i] = -2147483647 - 1;
+        else out[i] = (int32_t)t;
+    }
 }

@@ -12,7 +12,8 @@ import torch
 from ._native import DeepShiftError, call, lib
 
 __all__ = ["DeepShiftError", "describe_conv2d", "packed_row_words", "pack_shift_weights", "unpack_shift_weights",
-           "linear_shift", "conv2d_shift", "linear_mul_i32", "conv2d_mul_i32", "out_size"]
+           "linear_shift", "conv2d_shift", "linear_mul_i32", "conv2d_mul_i32", "out_size",
+           "quantize_shift_weights_q", "quantize_shift_weights_ps", "to_fixed_point"]
 
 
 def packed_row_words(cols: int) -> int:
@@ -55,6 +56,16 @@ def _dev_i32(t: torch.Tensor, name: str) -> torch.Tensor:
         raise TypeError(f"{name} must be a device tensor")
     if t.dtype not in (torch.int32, torch.uint32):
         raise TypeError(f"{name} must be int32, got {t.dtype}")
+    if not t.is_contiguous():
+        raise ValueError(f"{name} must be contiguous")
+    return t
+
+
+def _dev_f32(t: torch.Tensor, name: str) -> torch.Tensor:
+    if not isinstance(t, torch.Tensor) or not t.is_cuda:
+        raise TypeError(f"{name} must be a device tensor")
+    if t.dtype != torch.float32:
+        raise TypeError(f"{name} must be float32, got {t.dtype}")
     if not t.is_contiguous():
         raise ValueError(f"{name} must be contiguous")
     return t
@@ -139,4 +150,50 @@ def conv2d_mul_i32(x, w, bias, kernel_size, stride=1, padding=0, out=None):
     with torch.cuda.device(x.device):
         call("ds_conv2d_mul_i32", _ptr(x), _ptr(w), _ptr(bias), _ptr(y), n, c, h, wd, k, r, s,
              sh, sw, ph, pw, 0, _stream(x.device))
+    return y
+
+
+def _weight_rows(t: torch.Tensor):
+    rows = t.shape[0]
+    return rows, (t.numel() // rows if rows else 0)
+
+
+def quantize_shift_weights_q(w: torch.Tensor, max_shift: int = 14,
+                             out: torch.Tensor | None = None) -> torch.Tensor:
+    """DeepShift-Q: float32 weights [rows, ...] -> packed codes [rows, words] (int32 bits)."""
+    _dev_f32(w, "w")
+    rows, cols = _weight_rows(w)
+    y = out if out is not None else torch.empty((rows, max(packed_row_words(cols), 0)),
+                                                dtype=torch.int32, device=w.device)
+    _dev_i32(y, "out")
+    with torch.cuda.device(w.device):
+        call("ds_quantize_shift_weights_q", _ptr(w), rows, cols, max_shift, _ptr(y), 0,
+             _stream(w.device))
+    return y
+
+
+def quantize_shift_weights_ps(p: torch.Tensor, s: torch.Tensor, max_shift: int = 14,
+                              out: torch.Tensor | None = None) -> torch.Tensor:
+    """DeepShift-PS: shift and sign parameters [rows, ...] -> packed codes [rows, words]."""
+    _dev_f32(p, "p"); _dev_f32(s, "s")
+    if p.shape != s.shape:
+        raise ValueError("p and s must have the same shape")
+    rows, cols = _weight_rows(p)
+    y = out if out is not None else torch.empty((rows, max(packed_row_words(cols), 0)),
+                                                dtype=torch.int32, device=p.device)
+    _dev_i32(y, "out")
+    with torch.cuda.device(p.device):
+        call("ds_quantize_shift_weights_ps", _ptr(p), _ptr(s), rows, cols, max_shift, _ptr(y), 0,
+             _stream(p.device))
+    return y
+
+
+def to_fixed_point(x: torch.Tensor, frac_bits: int = 16,
+                   out: torch.Tensor | None = None) -> torch.Tensor:
+    """round(x * 2**frac_bits), halves away from zero, saturated to int32."""
+    _dev_f32(x, "x")
+    y = out if out is not None else torch.empty(x.shape, dtype=torch.int32, device=x.device)
+    _dev_i32(y, "out")
+    with torch.cuda.device(x.device):
+        call("ds_to_fixed_point", _ptr(x), x.numel(), frac_bits, _ptr(y), 0, _stream(x.device))
     return y

@@ -262,3 +262,25 @@ def random_codes(rng: np.random.Generator, shape, zero_frac: float = 0.1,
     shift = rng.integers(0, max_shift + 1, size=shape, dtype=np.uint8)
     shift[rng.random(shape) < zero_frac] = 15
     return (sign << 4 | shift).astype(np.uint8)
+
+
+def gen_float_weights(rows: int, cols: int, seed: int) -> np.ndarray:
+    """Float32 weights [rows, cols] with Kaiming-normal scale sqrt(2 / cols) (the
+    initialisation the paper uses for DeepShift-Q weights; fan-in = cols)."""
+    rng = np.random.default_rng(seed)
+    return (rng.standard_normal((rows, cols), dtype=np.float32) * np.float32(np.sqrt(2.0 / cols)))
+
+
+def gen_ps_params(rows: int, cols: int, seed: int, p_range=(-14.0, 0.0), s_range=(-1.0, 1.0)):
+    """DeepShift-PS parameters (P, S) [rows, cols], each uniform over its range (the
+    paper initialises both uniformly; the ranges are this project's choice)."""
+    rng = np.random.default_rng(seed)
+    p = rng.uniform(*p_range, (rows, cols)).astype(np.float32)
+    s = rng.uniform(*s_range, (rows, cols)).astype(np.float32)
+    return p, s
+
+
+def gen_float_acts(n: int, seed: int, scale: float = 4.0) -> np.ndarray:
+    """Float32 activations [n], normal with standard deviation ``scale``."""
+    rng = np.random.default_rng(seed)
+    return rng.standard_normal(n, dtype=np.float32) * np.float32(scale)

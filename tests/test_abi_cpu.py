@@ -157,3 +157,38 @@ def test_describe_names_a_kernel_without_a_gpu():
     assert len(buf.value) <= 3
     assert lib.ds_conv2d_shift_describe(0, 1, 1, 1, 1, 1, 1, 1, 1, 0, 0, buf, 4) == SHAPE
     assert lib.ds_conv2d_shift_describe(1, 1, 1, 1, 1, 1, 1, 1, 1, 0, 0, None, 4) == NULLP
+
+
+def test_converter_validation_codes():
+    lib = _native.lib()
+    q, ps, fx = lib.ds_quantize_shift_weights_q, lib.ds_quantize_shift_weights_ps, lib.ds_to_fixed_point
+    assert q(None, 2, 6, 14, FAKE * 4, 0, None) == NULLP
+    assert q(FAKE, 2, 6, 14, None, 0, None) == NULLP
+    assert q(FAKE, 0, 6, 14, FAKE * 4, 0, None) == SHAPE
+    assert q(FAKE, 2, -1, 14, FAKE * 4, 0, None) == SHAPE
+    assert q(FAKE, 2, 6, 15, FAKE * 4, 0, None) == ARG
+    assert q(FAKE, 2, 6, -1, FAKE * 4, 0, None) == ARG
+    assert q(FAKE, 2, 6, 14, FAKE * 4, 1, None) == ARG
+    assert q(FAKE, 1 << 16, 1 << 15, 14, FAKE * 4, 0, None) == UNSUP
+    assert q(FAKE, 2, 6, 14, FAKE + 8, 0, None) == ARG     # output overlaps w
+    assert "overlap" in lib.ds_last_error_message().decode()
+    assert ps(FAKE, None, 2, 6, 14, FAKE * 4, 0, None) == NULLP
+    assert ps(FAKE, FAKE * 2, 2, 6, 14, FAKE * 2 + 4, 0, None) == ARG   # overlaps s
+    assert ps(FAKE, FAKE * 2, 2, 0, 14, FAKE * 4, 0, None) == SHAPE
+    assert fx(None, 4, 16, FAKE * 4, 0, None) == NULLP
+    assert fx(FAKE, 0, 16, FAKE * 4, 0, None) == SHAPE
+    assert fx(FAKE, 4, 32, FAKE * 4, 0, None) == ARG
+    assert fx(FAKE, 4, -1, FAKE * 4, 0, None) == ARG
+    assert fx(FAKE, 4, 16, FAKE * 4, 3, None) == ARG
+    assert fx(FAKE, 1 << 31, 16, FAKE * 4, 0, None) == UNSUP
+    assert fx(FAKE, 4, 16, FAKE + 4, 0, None) == ARG       # partial overlap
+
+
+def test_converter_rejects_host_buffers():
+    lib = _native.lib()
+    w = np.ones((2, 6), np.float32)
+    out = np.full((2, 1), 7, np.uint32)
+    assert lib.ds_quantize_shift_weights_q(w.ctypes.data, 2, 6, 14, out.ctypes.data, 0, None) in (ARG, HIP)
+    y = np.full(12, 7, np.int32)
+    assert lib.ds_to_fixed_point(w.ctypes.data, 12, 16, y.ctypes.data, 0, None) in (ARG, HIP)
+    assert np.all(out == 7) and np.all(y == 7)

@@ -10,6 +10,7 @@ import shutil
 
 import pytest
 
+import tests.test_oracle_convert_pins as cpins
 import tests.test_oracle_pins as pins
 
 ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
@@ -37,7 +38,32 @@ MUTATIONS = {
     "pack_bit_offset": ("word |= (code & 31u) << (5 * j);", "word |= (code & 31u) << (5 * (5 - j));"),
     "drop_last_term": ("for (int64_t s = 0; s < S; ++s) {\n                int64_t ih",
                        "for (int64_t s = 0; s < S - (c == C - 1 && r == R - 1); ++s) {\n                int64_t ih"),
+    # float -> code converter and fixed point
+    "q_floor_instead_of_round": ("return (w2 >= ldexp(1.0, 2 * p + 1)) ? p + 1 : p;", "return p;"),
+    "q_boundary_one_off": ("ldexp(1.0, 2 * p + 1)", "ldexp(1.0, 2 * p + 2)"),
+    "q_sign_dropped": ("return (uint8_t)((s < 0 ? 16 : 0) | (-p));", "return (uint8_t)(-p);"),
+    "clip_below_to_zero_code": ("if (p < -max_shift) p = -max_shift;", "if (p < -max_shift) return 15;"),
+    "clip_range_ignored": ("if (p < -max_shift) p = -max_shift;", "if (p < -14) p = -14;"),
+    "zero_weight_as_shift_0": ("if (s == 0) return 15;", "if (s == 0) return 0;"),
+    "ps_strict_threshold": ("int s = sv <= -0.5f ? -1 : (sv >= 0.5f ? 1 : 0);",
+                            "int s = sv < -0.5f ? -1 : (sv > 0.5f ? 1 : 0);"),
+    "ps_round_half_even": ("const double r = round((double)P[i]);", "const double r = nearbyint((double)P[i]);"),
+    "fixed_truncate": ("const double t = round(ldexp(v, frac_bits));", "const double t = trunc(ldexp(v, frac_bits));"),
+    "fixed_half_even": ("const double t = round(ldexp(v, frac_bits));", "const double t = nearbyint(ldexp(v, frac_bits));"),
+    "fixed_no_saturation": ("if (t >= 2147483647.0) out[i] = 2147483647;", "if (0) out[i] = 0;"),
 }
+
+CONVERT_CHECKS = [
+    *[(cpins.test_q_matches_library_log2_round, (m,)) for m in (14, 3)],
+    (cpins.test_q_boundary_neighbours_round_up_and_down, ()),
+    (cpins.test_q_nearest_power_property_exact, ()),
+    (cpins.test_q_special_values, ()),
+    (cpins.test_ps_sign_threshold_equals_sign_of_round, ()),
+    (cpins.test_ps_round_p_halves_away_and_clips, ()),
+    (cpins.test_ps_nan_gives_zero_weight, ()),
+    *[(cpins.test_fixed_matches_exact_rounding, (f,)) for f in (16, 31)],
+    (cpins.test_golden_examples, ()),
+]
 
 CHECKS = [
     (pins.test_term_matches_exact_rational_floor, ()),
@@ -77,8 +103,9 @@ def load_mutant(tmp_path, name):
 def test_pins_catch_mutation(tmp_path, monkeypatch, name):
     mod = load_mutant(tmp_path, name)
     monkeypatch.setattr(pins, "oracle", mod)
+    monkeypatch.setattr(cpins, "oracle", mod)
     failed = []
-    for fn, args in CHECKS:
+    for fn, args in CHECKS + CONVERT_CHECKS:
         try:
             fn(*args)
         except AssertionError:
@@ -96,5 +123,6 @@ def test_unmutated_copy_passes(tmp_path, monkeypatch):
     spec.loader.exec_module(mod)
     mod.build(force=True)
     monkeypatch.setattr(pins, "oracle", mod)
-    for fn, args in CHECKS:
+    monkeypatch.setattr(cpins, "oracle", mod)
+    for fn, args in CHECKS + CONVERT_CHECKS:
         fn(*args)
