@@ -97,7 +97,7 @@ def _pmc_rows(directory: str):
 
 
 def pmc_summary(copy_fetch, copy_write, fetch, write, copy_bytes, workload, out):
-    """HBM traffic of the tiled kernels from FETCH_SIZE/WRITE_SIZE runs (KiB per
+    """HBM traffic of the main (tiled or direct) kernels from FETCH_SIZE/WRITE_SIZE runs (KiB per
     dispatch), each scaled by what the same counter reads for a plain copy of
     copy_bytes (the largest copy dispatch in the calibration runs)."""
     from paper_1905_13298_amd import workloads as W
@@ -106,8 +106,9 @@ def pmc_summary(copy_fetch, copy_write, fetch, write, copy_bytes, workload, out)
     fetch_scale = copy_bytes / (cf * 1024.0)
     write_scale = copy_bytes / (cw * 1024.0)
     layers = W.config_layers(WORKLOADS[workload])
-    f_rows = [r for r in _pmc_rows(fetch) if "tiled_kernel" in r["name"]][-len(layers):]
-    w_rows = [r for r in _pmc_rows(write) if "tiled_kernel" in r["name"]][-len(layers):]
+    main = ("tiled_kernel", "conv_direct_kernel")
+    f_rows = [r for r in _pmc_rows(fetch) if any(m in r["name"] for m in main)][-len(layers):]
+    w_rows = [r for r in _pmc_rows(write) if any(m in r["name"] for m in main)][-len(layers):]
     per_kernel = {}
     for L, fr, wr in zip(layers, f_rows, w_rows):
         name = kernel_variant(L).rsplit(" splits", 1)[0]
@@ -240,7 +241,7 @@ def main():
             "hbm_gbs": algorithmic_bytes(L) / (med * 1e-3) / 1e9,
         })
 
-    # ---- dominant kernel: the tiled-kernel instance with the most time per step
+    # ---- dominant kernel: the main-kernel instance with the most time per step
     groups = {}
     for li, (L, *_rest) in enumerate(res):
         name = kernel_variant(L).rsplit(" splits", 1)[0]   # one kernel instance
@@ -264,7 +265,7 @@ def main():
         "sac_per_launch_avg": dom["sac"] // dom["launches"],
         "int32_ops_frac": round(2 * achieved / INT32_OPS_PEAK_T, 4),
         "hbm_gbs_algorithmic": round(dom["bytes"] / (dom["ms"] * 1e-3) / 1e9, 1),
-        "timed_span": "library call (weight decode + tiled kernel) per launch",
+        "timed_span": "library call (weight decode + main kernel) per launch",
     }
 
     # ---- multiplication-based comparison kernel, same tiling, same layers

@@ -39,12 +39,9 @@ namespace ds {
 
 int forced_variant()
 {
-    static const int v = [] {
-        const char *e = std::getenv("DS_FORCE_VARIANT");
-        if (!e || !*e) return -1;
-        return std::atoi(e);
-    }();
-    return v;
+    const char *e = std::getenv("DS_FORCE_VARIANT");  // read per call: tests switch it
+    if (!e || !*e) return -1;
+    return std::atoi(e);
 }
 
 // ---------------------------------------------------------------------------

@@ -29,7 +29,7 @@ hipError_t run_conv(const ConvGeom &g, const int32_t *x, const uint32_t *wpacked
 void describe_conv(const ConvGeom &g, char *buf, size_t len);
 
 // Kernel variant forced for testing and tuning, from the environment variable
-// DS_FORCE_VARIANT (read once): unset or -1 = automatic choice, 0 = the
+// DS_FORCE_VARIANT (read at every call): unset or -1 = automatic choice, 0 = the
 // one-thread-per-output kernel, 8 = tiled kernels with 8 pixels per lane
 // where an instance exists (the default is 4).
 int forced_variant();

@@ -293,3 +293,26 @@ def test_mul_comparison_exact(shape):
     yl = ops.linear_mul_i32(to_dev(xl), to_dev(wl)).cpu().numpy()
     want = oracle.conv2d_mul(xl.reshape(33, 70, 1, 1), wl, None, r=1).reshape(33, 45)
     np.testing.assert_array_equal(yl, want)
+
+
+# Every output compared, at the full batch of the workload, for one layer of each
+# kernel family and shape class (the stem's 7 x 7 taps, 3 x 3 with and without
+# stride, 1 x 1 with and without stride, LinearShift), and run twice: the two
+# runs must agree bit for bit as well.
+FULL_LAYERS = [(3, "conv1"), (3, "layer1.0.conv1"), (4, "layer1.0.downsample"),
+               (4, "layer2.0.conv2"), (3, "layer2.0.downsample"), (2, "fc6")]
+
+
+@pytest.mark.parametrize("cfg,name", FULL_LAYERS)
+def test_full_size_every_output(cfg, name):
+    layers = W.config_layers(cfg)
+    li = [L.name for L in layers].index(name)
+    layer = layers[li]
+    x, codes, bias = W.gen_layer(layer, W.CONFIG_SEEDS[cfg], li)
+    say(f"cfg{cfg} {name} every output, batch {layer.n}")
+    y1 = gpu_layer(layer, x, codes, bias).cpu().numpy()
+    y2 = gpu_layer(layer, x, codes, bias).cpu().numpy()
+    want = oracle_layer(layer, x, codes, bias)
+    bad = np.flatnonzero(y1.ravel() != want.ravel())
+    assert bad.size == 0, f"{bad.size} of {want.size} outputs differ, first at {bad[:5]}"
+    np.testing.assert_array_equal(y1, y2)
