@@ -28,6 +28,9 @@ ROOT = os.path.dirname(os.path.abspath(__file__))
 sys.path.insert(0, ROOT)
 
 WORKLOADS = {"linear_small": 0, "conv_single": 1, "linear_fc6": 2, "resnet18": 3, "resnet50": 4}
+# The step upstream of the operators: float weights -> packed codes (DeepShift-Q)
+# and the float input batch -> fixed point, for every layer of ResNet-50 at N = 128.
+CONVERT_WORKLOADS = {"convert_resnet50": 4}
 
 # MI355X: 256 CUs, 4 SIMD16 per CU -> 64 int32 lane-ops per clock per CU, 2.4 GHz peak clock.
 CUS, LANES_PER_CU, CLOCK_GHZ = 256, 64, 2.4
@@ -57,7 +60,7 @@ def parse():
     ap.add_argument("--gpus", type=int, default=1)
     ap.add_argument("--steps", type=int, default=5)
     ap.add_argument("--warmup", type=int, default=2)
-    ap.add_argument("--workload", default="resnet50", choices=sorted(WORKLOADS))
+    ap.add_argument("--workload", default="resnet50", choices=sorted(WORKLOADS) + sorted(CONVERT_WORKLOADS))
     ap.add_argument("--cpu-batch", type=int, default=None,
                     help="batch of the oracle sample (default: sized for ~10-30 s)")
     ap.add_argument("--cpu-seconds", type=float, default=10.0,
@@ -157,6 +160,100 @@ def copy_only(nbytes: int) -> None:
     print(json.dumps({"copy_bytes": 4 * n, "repeats": 3}), flush=True)
 
 
+def bench_convert(args):
+    """One step = DeepShift-Q conversion of every weight tensor of the network plus the
+    fixed-point rounding of its input batch; HBM-bound, so reported in GB/s."""
+    import torch
+    from paper_1905_13298_amd import ops
+    from paper_1905_13298_amd import workloads as W
+
+    cfg = CONVERT_WORKLOADS[args.workload]
+    layers = W.config_layers(cfg)
+    dev = torch.device("cuda:0")
+    torch.cuda.set_device(dev)
+    ws = [torch.from_numpy(W.gen_float_weights(L.k, L.crs, seed=1000 + i)).to(dev)
+          for i, L in enumerate(layers)]
+    outs = [torch.empty((L.k, ops.packed_row_words(L.crs)), dtype=torch.int32, device=dev)
+            for L in layers]
+    stem = layers[0]
+    nx = int(np.prod(stem.x_shape))
+    xf = torch.from_numpy(W.gen_float_acts(nx, seed=5)).to(dev)
+    xq = torch.empty(nx, dtype=torch.int32, device=dev)
+    w_bytes = sum(4 * w.numel() + 4 * o.numel() for w, o in zip(ws, outs))
+    x_bytes = 8 * nx
+    # One library call converts all weight tensors (launches of up to 64 tensors each).
+    calls = [("quantize_q_many", ws, outs), ("to_fixed", xf, xq)]
+
+    def run(call):
+        kind, a, o = call
+        if kind == "quantize_q_many":
+            ops.quantize_shift_weights_q_many(a, outs=o)
+        else:
+            ops.to_fixed_point(a, out=o)
+
+    for _ in range(args.warmup):
+        for c in calls:
+            run(c)
+    stream = torch.cuda.current_stream(dev)
+    ev = [[(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True))
+           for _ in calls] for _ in range(args.steps)]
+    t0, t1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    torch.cuda.synchronize()
+    t0.record(stream)
+    for s in range(args.steps):
+        for i, c in enumerate(calls):
+            ev[s][i][0].record(stream)
+            run(c)
+            ev[s][i][1].record(stream)
+    t1.record(stream)
+    torch.cuda.synchronize()
+    ms_per_step = t0.elapsed_time(t1) / args.steps
+    step_bytes = w_bytes + x_bytes
+    q_ms = sum(ev[s][0][0].elapsed_time(ev[s][0][1]) for s in range(args.steps)) / args.steps
+    f_ms = sum(ev[s][1][0].elapsed_time(ev[s][1][1]) for s in range(args.steps)) / args.steps
+    q_launches = (len(layers) + 63) // 64
+    kernels = {"quantize_kernel<Q>": (q_ms, w_bytes, q_launches),
+               "to_fixed_kernel": (f_ms, x_bytes, 1)}
+    name, (k_ms, k_bytes, k_launches) = max(kernels.items(), key=lambda kv: kv[1][0])
+    achieved = k_bytes / (k_ms * 1e-3) / 1e9
+    roofline = {"bound": "hbm", "achieved": round(achieved, 1), "peak": HBM_PEAK_GBS,
+                "unit": "GB/s", "frac": round(achieved / HBM_PEAK_GBS, 4), "traffic": None,
+                "kernel": name, "launches_per_step": k_launches,
+                "avg_launch_ms": round(k_ms / k_launches, 5),
+                "algorithmic_bytes_per_launch": k_bytes // k_launches,
+                "per_kernel_gbs": {k: round(b / (m * 1e-3) / 1e9, 1) for k, (m, b, _) in kernels.items()},
+                "timed_span": "library call per launch (one kernel each)"}
+    cpu = None
+    if not args.no_cpu_baseline:
+        import oracle
+        wn = [W.gen_float_weights(L.k, L.crs, seed=1000 + i) for i, L in enumerate(layers)]
+        xn = W.gen_float_acts(nx, seed=5)
+        t = time.perf_counter()
+        passes = 0
+        while True:
+            for w in wn:
+                oracle.pack_codes(oracle.quantize_q(w))
+            oracle.to_fixed(xn)
+            passes += 1
+            if time.perf_counter() - t > args.cpu_seconds / 2:
+                break
+        dt = time.perf_counter() - t
+        cpu = {"value": round(passes * step_bytes / dt / 1e9, 3), "unit": "GB/s", "cores": 1,
+               "kind": "oracle", "sample": f"{passes} whole step(s) ({dt:.1f} s)"}
+    out = {
+        "metric": "GB/s of float-to-code conversion (weights) and fixed-point rounding (input)",
+        "value": round(step_bytes / (ms_per_step * 1e-3) / 1e9, 1), "unit": "GB/s", "n_gpus": 1,
+        "steps": args.steps, "warmup": args.warmup, "ms_per_step": round(ms_per_step, 4),
+        "higher_is_better": True, "scaling": "weak", "vs_baseline": None, "dtype": "f32->u5/i32",
+        "data": "synthetic",
+        "config": {"workload": "resnet50_weights_and_input_n128", "weight_tensors": len(layers),
+                   "weights": sum(L.k * L.crs for L in layers), "input_elements": nx,
+                   "bytes_per_step": step_bytes, "parallelism": "single GPU"},
+        "roofline": roofline, "cpu_baseline": cpu,
+    }
+    print(json.dumps(out), flush=True)
+
+
 def main():
     args = parse()
     if args.copy_only:
@@ -170,6 +267,10 @@ def main():
               "no cross-GPU exchange for a layer, see the design notes for how they shard.",
               file=sys.stderr)
         sys.exit(2)
+
+    if args.workload in CONVERT_WORKLOADS:
+        bench_convert(args)
+        return
 
     import torch
     from paper_1905_13298_amd import ops

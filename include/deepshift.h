@@ -132,6 +132,18 @@ ds_status ds_quantize_shift_weights_q(const float *w, int64_t rows, int64_t cols
                                       int32_t max_shift, uint32_t *w_packed,
                                       uint32_t flags, void *stream);
 
+/* ds_quantize_shift_weights_q for `count` tensors in as few launches as
+ * possible (one per 64 tensors): converting a whole network is then bound by
+ * HBM bandwidth instead of per-launch latency. w, rows, cols and w_packed are
+ * host arrays of `count` entries; w[i] and w_packed[i] are device pointers
+ * with the layouts of ds_quantize_shift_weights_q. Every tensor is validated
+ * before anything is launched (an error names the tensor), and no output may
+ * overlap an input or another output. */
+ds_status ds_quantize_shift_weights_q_many(int64_t count, const float *const *w,
+                                           const int64_t *rows, const int64_t *cols,
+                                           int32_t max_shift, uint32_t *const *w_packed,
+                                           uint32_t flags, void *stream);
+
 /* DeepShift-PS weight conversion (Section 3): from the shift parameters P and
  * the sign parameters S (device float32, both [rows][cols]):
  *     p = round(P) clipped to -max_shift .. 0,

@@ -34,6 +34,7 @@
 #include <type_traits>
 
 #include "conv_plan.hpp"
+#include "fastdiv.hpp"
 
 namespace ds {
 
@@ -42,27 +43,6 @@ int forced_variant()
     const char *e = std::getenv("DS_FORCE_VARIANT");  // read per call: tests switch it
     if (!e || !*e) return -1;
     return std::atoi(e);
-}
-
-// ---------------------------------------------------------------------------
-// Division by a launch-constant divisor for dividends below 2^31
-// (round-up multiplier method of Granlund and Montgomery, 1994).
-
-struct FastDiv {
-    uint32_t d, m, l;
-};
-
-static FastDiv make_fastdiv(uint32_t d)
-{
-    uint32_t l = 0;
-    while ((uint64_t(1) << l) < d) ++l;
-    const uint64_t m = ((uint64_t(1) << 32) * ((uint64_t(1) << l) - d)) / d + 1;
-    return FastDiv{d, uint32_t(m), l};
-}
-
-__device__ __forceinline__ int fdiv(int n, const FastDiv &f)
-{
-    return int((__umulhi(uint32_t(n), f.m) + uint32_t(n)) >> f.l);
 }
 
 // ---------------------------------------------------------------------------

@@ -15,9 +15,12 @@
 // stores the word (coalesced).
 #include <hip/hip_runtime.h>
 
+#include <algorithm>
 #include <cmath>
+#include <string>
 
 #include "common.hpp"
+#include "fastdiv.hpp"
 
 namespace ds {
 
@@ -66,47 +69,89 @@ __device__ __forceinline__ uint32_t code_ps(float pv, float sv, int max_shift)
 }
 
 struct WordRange {
-    int64_t first_float;  // flat index of the first float of word t
-    int ncodes;           // codes of word t that come from the row (1..6)
+    int first_float;  // flat index (within the tensor) of the first float of word t
+    int ncodes;       // codes of word t that come from the row (1..6)
 };
 
-__device__ __forceinline__ WordRange word_range(int64_t t, int64_t cols, int64_t wpr)
+// Word t of a tensor with `cols` floats and `wpr` words per row (all indexes
+// below 2^31: the entry points reject larger tensors).
+__device__ __forceinline__ WordRange word_range(int t, int cols, const FastDiv &wpr)
 {
-    const int64_t row = t / wpr, j = t - row * wpr;
-    const int64_t col = j * kCodesPerWord;
+    const int row = fdiv(t, wpr), j = t - row * int(wpr.d);
+    const int col = j * kCodesPerWord;
     WordRange r;
     r.first_float = row * cols + col;
-    r.ncodes = int(min<int64_t>(kCodesPerWord, cols - col));
+    r.ncodes = min(kCodesPerWord, cols - col);
     return r;
 }
 
+// One weight tensor of a launch: its inputs, its packed output, and the first
+// block of the launch that works on it.
+struct Segment {
+    const float *a;     // w (DeepShift-Q) or P (DeepShift-PS)
+    const float *b;     // S (DeepShift-PS), unused otherwise
+    uint32_t *out;
+    int cols, nwords, rows;
+    int block0;         // first block of the launch that works on this tensor
+    FastDiv wpr;        // words per row
+};
+
+// Up to kMaxSegments tensors per launch, passed by value in the kernel
+// arguments (about 3.5 KB, under the 4 KB limit), so a launch needs no device
+// table.
+constexpr int kMaxSegments = 64;
+struct SegmentTable {
+    int count;
+    int max_shift;
+    Segment seg[kMaxSegments];
+};
+
 template <bool PS>
-__global__ __launch_bounds__(kWordsPerBlock) void quantize_kernel(
-    const float *__restrict__ w, const float *__restrict__ sgn, int64_t cols, int64_t wpr,
-    int64_t nwords, int max_shift, uint32_t *__restrict__ out)
+__global__ __launch_bounds__(kWordsPerBlock) void quantize_kernel(const SegmentTable tab)
 {
     __shared__ uint8_t codes[kWordsPerBlock * kCodesPerWord];
-    const int64_t t0 = int64_t(blockIdx.x) * kWordsPerBlock;
-    const int64_t t1 = min<int64_t>(t0 + kWordsPerBlock, nwords);
+    // This block's tensor: the last segment whose first block is <= blockIdx.x.
+    int lo = 0, hi = tab.count - 1;
+    while (lo < hi) {
+        const int mid = (lo + hi + 1) >> 1;
+        if (tab.seg[mid].block0 <= int(blockIdx.x)) lo = mid; else hi = mid - 1;
+    }
+    const Segment &sg = tab.seg[lo];
+    const int cols = sg.cols, nwords = sg.nwords;
+    const int t0 = (int(blockIdx.x) - sg.block0) * kWordsPerBlock;
+    const int t1 = min(t0 + kWordsPerBlock, nwords);
     // Floats covered by words [t0, t1): [f0, f1). Word t1 (or the end) starts at f1.
-    const int64_t f0 = word_range(t0, cols, wpr).first_float;
-    const int64_t f1 = t1 == nwords ? (nwords / wpr) * cols : word_range(t1, cols, wpr).first_float;
-    const int nf = int(f1 - f0);  // <= 6 * 256
-    for (int i = threadIdx.x; i < nf; i += kWordsPerBlock) {
-        const float v = w[f0 + i];
-        codes[i] = uint8_t(PS ? code_ps(v, sgn[f0 + i], max_shift) : code_q(v, max_shift));
+    const int f0 = word_range(t0, cols, sg.wpr).first_float;
+    const int f1 = t1 == nwords ? sg.rows * cols : word_range(t1, cols, sg.wpr).first_float;
+    const int nf = f1 - f0;  // <= 6 * 256
+    const float *__restrict__ a = sg.a + f0;
+    const float *__restrict__ b = PS ? sg.b + f0 : nullptr;
+    // Six independent loads per thread in flight, then the codes into LDS.
+    float va[kCodesPerWord], vb[kCodesPerWord];
+#pragma unroll
+    for (int r = 0; r < kCodesPerWord; ++r) {
+        const int i = int(threadIdx.x) + r * kWordsPerBlock;
+        va[r] = i < nf ? a[i] : 0.0f;
+        vb[r] = PS && i < nf ? b[i] : 0.0f;
+    }
+#pragma unroll
+    for (int r = 0; r < kCodesPerWord; ++r) {
+        const int i = int(threadIdx.x) + r * kWordsPerBlock;
+        if (i < nf)
+            codes[i] = uint8_t(PS ? code_ps(va[r], vb[r], tab.max_shift) : code_q(va[r], tab.max_shift));
     }
     __syncthreads();
-    const int64_t t = t0 + threadIdx.x;
+    const int t = t0 + int(threadIdx.x);
     if (t >= t1) return;
-    const WordRange r = word_range(t, cols, wpr);
+    const WordRange r = word_range(t, cols, sg.wpr);
     const int base = int(r.first_float - f0);
     uint32_t word = 0;
+#pragma unroll
     for (int i = 0; i < kCodesPerWord; ++i) {
         const uint32_t c = i < r.ncodes ? uint32_t(codes[base + i]) : kZeroCode;
         word |= c << (5 * i);
     }
-    out[t] = word;
+    sg.out[t] = word;
 }
 
 // round(x * 2^F) with halves away from zero, saturated to int32; NaN -> 0.
@@ -152,6 +197,7 @@ ds_status hip_result(hipError_t e, const char *what)
     return fail(DS_ERR_HIP, "%s: %s", what, hipGetErrorString(e));
 }
 
+// Argument checks of one tensor that need no device access.
 ds_status check_quantize(const float *a, const float *b, bool need_b, int64_t rows, int64_t cols,
                          int32_t max_shift, const uint32_t *out, uint32_t flags, int64_t &nwords)
 {
@@ -166,6 +212,14 @@ ds_status check_quantize(const float *a, const float *b, bool need_b, int64_t ro
     const int64_t ib = 4 * ne, ob = 4 * nwords;
     if (overlap(out, ob, a, ib) || (need_b && overlap(out, ob, b, ib)))
         return fail(DS_ERR_INVALID_ARG, "output overlaps an input");
+    return DS_SUCCESS;
+}
+
+// The buffers of one tensor must be device allocations of the required size.
+ds_status check_quantize_buffers(const float *a, const float *b, bool need_b, int64_t rows,
+                                 int64_t cols, const uint32_t *out)
+{
+    const int64_t ib = 4 * rows * cols, ob = 4 * rows * row_words(cols);
     if (!device_range_ok(a, ib) || (need_b && !device_range_ok(b, ib)))
         return fail(DS_ERR_INVALID_ARG, "inputs are not device buffers of %lld bytes", (long long)ib);
     if (!device_range_ok(out, ob))
@@ -173,15 +227,65 @@ ds_status check_quantize(const float *a, const float *b, bool need_b, int64_t ro
     return DS_SUCCESS;
 }
 
+// Validates every tensor first (nothing is launched on an error), then
+// launches once per kMaxSegments tensors.
 template <bool PS>
-ds_status launch_quantize(const float *a, const float *b, int64_t cols, int64_t nwords,
-                          int32_t max_shift, uint32_t *out, void *stream, const char *name)
+ds_status quantize_many(int64_t count, const float *const *a, const float *const *b,
+                        const int64_t *rows, const int64_t *cols, uint32_t *const *out,
+                        int32_t max_shift, uint32_t flags, void *stream, const char *name)
 {
-    const int64_t blocks = (nwords + kWordsPerBlock - 1) / kWordsPerBlock;
-    hipLaunchKernelGGL(quantize_kernel<PS>, dim3(unsigned(blocks)), dim3(kWordsPerBlock), 0,
-                       static_cast<hipStream_t>(stream), a, b, cols, row_words(cols), nwords,
-                       int(max_shift), out);
-    return hip_result(hipGetLastError(), name);
+    if (count <= 0) return fail(DS_ERR_INVALID_SHAPE, "count must be > 0");
+    if (!a || (PS && !b) || !rows || !cols || !out)
+        return fail(DS_ERR_NULL_POINTER, "the arrays must not be NULL");
+    auto named = [&](ds_status st, int64_t i) {
+        if (count == 1) return st;
+        const std::string msg = last_error();
+        return fail(st, "tensor %lld: %s", (long long)i, msg.c_str());
+    };
+    // Arguments of every tensor first, then the device buffers.
+    for (int64_t i = 0; i < count; ++i) {
+        int64_t nwords = 0;
+        const ds_status st = check_quantize(a[i], PS ? b[i] : nullptr, PS, rows[i], cols[i],
+                                            max_shift, out[i], flags, nwords);
+        if (st != DS_SUCCESS) return named(st, i);
+        for (int64_t j = 0; j < i; ++j)
+            if (overlap(out[i], 4 * nwords, out[j], 4 * rows[j] * row_words(cols[j])) ||
+                overlap(out[i], 4 * nwords, a[j], 4 * rows[j] * cols[j]) ||
+                overlap(out[j], 4 * rows[j] * row_words(cols[j]), a[i], 4 * rows[i] * cols[i]))
+                return fail(DS_ERR_INVALID_ARG, "tensors %lld and %lld overlap (an output over "
+                            "an input or another output)", (long long)j, (long long)i);
+    }
+    for (int64_t i = 0; i < count; ++i) {
+        const ds_status st = check_quantize_buffers(a[i], PS ? b[i] : nullptr, PS, rows[i], cols[i],
+                                                    out[i]);
+        if (st != DS_SUCCESS) return named(st, i);
+    }
+    for (int64_t first = 0; first < count; first += kMaxSegments) {
+        SegmentTable tab;
+        tab.count = int(std::min<int64_t>(kMaxSegments, count - first));
+        tab.max_shift = max_shift;
+        int64_t blocks = 0;
+        for (int i = 0; i < tab.count; ++i) {
+            const int64_t k = first + i;
+            Segment &sg = tab.seg[i];
+            sg.a = a[k];
+            sg.b = PS ? b[k] : nullptr;
+            sg.out = out[k];
+            sg.cols = int(cols[k]);
+            sg.rows = int(rows[k]);
+            sg.wpr = make_fastdiv(uint32_t(row_words(cols[k])));
+            sg.nwords = int(rows[k] * row_words(cols[k]));
+            if (blocks > INT32_MAX) return fail(DS_ERR_UNSUPPORTED, "too many weights in one call");
+            sg.block0 = int(blocks);
+            blocks += (sg.nwords + kWordsPerBlock - 1) / kWordsPerBlock;
+        }
+        if (blocks > INT32_MAX) return fail(DS_ERR_UNSUPPORTED, "too many weights in one call");
+        hipLaunchKernelGGL(quantize_kernel<PS>, dim3(unsigned(blocks)), dim3(kWordsPerBlock), 0,
+                           static_cast<hipStream_t>(stream), tab);
+        const ds_status st = hip_result(hipGetLastError(), name);
+        if (st != DS_SUCCESS) return st;
+    }
+    return ok();
 }
 
 }  // namespace
@@ -194,22 +298,27 @@ extern "C" ds_status ds_quantize_shift_weights_q(const float *w, int64_t rows, i
                                                  int32_t max_shift, uint32_t *w_packed,
                                                  uint32_t flags, void *stream)
 {
-    int64_t nwords = 0;
-    const ds_status st = check_quantize(w, nullptr, false, rows, cols, max_shift, w_packed, flags, nwords);
-    if (st != DS_SUCCESS) return st;
-    return launch_quantize<false>(w, nullptr, cols, nwords, max_shift, w_packed, stream,
-                                  "ds_quantize_shift_weights_q");
+    if (!w || !w_packed) return fail(DS_ERR_NULL_POINTER, "inputs and output must not be NULL");
+    return quantize_many<false>(1, &w, nullptr, &rows, &cols, &w_packed, max_shift, flags, stream,
+                                "ds_quantize_shift_weights_q");
 }
 
 extern "C" ds_status ds_quantize_shift_weights_ps(const float *p, const float *s, int64_t rows,
                                                   int64_t cols, int32_t max_shift,
                                                   uint32_t *w_packed, uint32_t flags, void *stream)
 {
-    int64_t nwords = 0;
-    const ds_status st = check_quantize(p, s, true, rows, cols, max_shift, w_packed, flags, nwords);
-    if (st != DS_SUCCESS) return st;
-    return launch_quantize<true>(p, s, cols, nwords, max_shift, w_packed, stream,
-                                 "ds_quantize_shift_weights_ps");
+    if (!p || !s || !w_packed) return fail(DS_ERR_NULL_POINTER, "inputs and output must not be NULL");
+    return quantize_many<true>(1, &p, &s, &rows, &cols, &w_packed, max_shift, flags, stream,
+                               "ds_quantize_shift_weights_ps");
+}
+
+extern "C" ds_status ds_quantize_shift_weights_q_many(int64_t count, const float *const *w,
+                                                      const int64_t *rows, const int64_t *cols,
+                                                      int32_t max_shift, uint32_t *const *w_packed,
+                                                      uint32_t flags, void *stream)
+{
+    return quantize_many<false>(count, w, nullptr, rows, cols, w_packed, max_shift, flags, stream,
+                                "ds_quantize_shift_weights_q_many");
 }
 
 extern "C" ds_status ds_to_fixed_point(const float *x, int64_t n, int32_t frac_bits, int32_t *y,

@@ -13,7 +13,8 @@ from ._native import DeepShiftError, call, lib
 
 __all__ = ["DeepShiftError", "describe_conv2d", "packed_row_words", "pack_shift_weights", "unpack_shift_weights",
            "linear_shift", "conv2d_shift", "linear_mul_i32", "conv2d_mul_i32", "out_size",
-           "quantize_shift_weights_q", "quantize_shift_weights_ps", "to_fixed_point"]
+           "quantize_shift_weights_q", "quantize_shift_weights_q_many", "quantize_shift_weights_ps",
+           "to_fixed_point"]
 
 
 def packed_row_words(cols: int) -> int:
@@ -170,6 +171,30 @@ def quantize_shift_weights_q(w: torch.Tensor, max_shift: int = 14,
         call("ds_quantize_shift_weights_q", _ptr(w), rows, cols, max_shift, _ptr(y), 0,
              _stream(w.device))
     return y
+
+
+def quantize_shift_weights_q_many(ws, max_shift: int = 14, outs=None) -> list:
+    """DeepShift-Q for a list of float32 weight tensors in one library call."""
+    import ctypes
+    if not ws:
+        raise ValueError("no tensors")
+    for i, w in enumerate(ws):
+        _dev_f32(w, f"ws[{i}]")
+    shapes = [_weight_rows(w) for w in ws]
+    if outs is None:
+        outs = [torch.empty((r, max(packed_row_words(c), 0)), dtype=torch.int32, device=w.device)
+                for w, (r, c) in zip(ws, shapes)]
+    for i, o in enumerate(outs):
+        _dev_i32(o, f"outs[{i}]")
+    n = len(ws)
+    wp = (ctypes.c_void_p * n)(*[w.data_ptr() for w in ws])
+    op = (ctypes.c_void_p * n)(*[o.data_ptr() for o in outs])
+    rows = (ctypes.c_int64 * n)(*[r for r, _ in shapes])
+    cols = (ctypes.c_int64 * n)(*[c for _, c in shapes])
+    dev = ws[0].device
+    with torch.cuda.device(dev):
+        call("ds_quantize_shift_weights_q_many", n, wp, rows, cols, max_shift, op, 0, _stream(dev))
+    return outs
 
 
 def quantize_shift_weights_ps(p: torch.Tensor, s: torch.Tensor, max_shift: int = 14,

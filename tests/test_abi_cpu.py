@@ -192,3 +192,21 @@ def test_converter_rejects_host_buffers():
     y = np.full(12, 7, np.int32)
     assert lib.ds_to_fixed_point(w.ctypes.data, 12, 16, y.ctypes.data, 0, None) in (ARG, HIP)
     assert np.all(out == 7) and np.all(y == 7)
+
+
+def test_converter_many_validation_codes():
+    lib = _native.lib()
+    many = lib.ds_quantize_shift_weights_q_many
+    P2 = ctypes.c_void_p * 2
+    I2 = ctypes.c_int64 * 2
+    w = P2(FAKE, FAKE * 2)
+    out = P2(FAKE * 4, FAKE * 8)
+    assert many(0, w, I2(2, 2), I2(6, 6), 14, out, 0, None) == SHAPE
+    assert many(2, None, I2(2, 2), I2(6, 6), 14, out, 0, None) == NULLP
+    assert many(2, w, None, I2(6, 6), 14, out, 0, None) == NULLP
+    assert many(2, w, I2(2, 0), I2(6, 6), 14, out, 0, None) == SHAPE
+    assert "tensor 1" in lib.ds_last_error_message().decode()
+    assert many(2, P2(FAKE, None), I2(2, 2), I2(6, 6), 14, out, 0, None) == NULLP
+    assert many(2, w, I2(2, 2), I2(6, 6), 15, out, 0, None) == ARG
+    # two outputs on top of each other
+    assert many(2, w, I2(2, 2), I2(6, 6), 14, P2(FAKE * 4, FAKE * 4), 0, None) in (ARG,)

@@ -146,3 +146,21 @@ def test_float_layer_end_to_end():
     want = oracle.conv2d_shift(oracle.to_fixed(xf), oracle.quantize_q(wf), oracle.to_fixed(bf),
                                r=layer.r, s=layer.s, stride=layer.stride, pad=layer.pad)
     np.testing.assert_array_equal(y, want)
+
+
+def test_quantize_many_matches_oracle():
+    """One call for 70 tensors (two launches: 64 + 6), ragged and tiny shapes included,
+    and one call for every weight tensor of ResNet-50."""
+    rng = np.random.default_rng(9)
+    shapes = [(int(rng.integers(1, 40)), int(rng.integers(1, 300))) for _ in range(68)] + [(1, 1), (513, 4609)]
+    ws = [splice(W.gen_float_weights(r, c, seed=i), q_specials(), rng) for i, (r, c) in enumerate(shapes)]
+    say(f"quantize_q_many {len(ws)} tensors")
+    outs = ops.quantize_shift_weights_q_many([to_dev(w) for w in ws], max_shift=9)
+    for i, (w, o) in enumerate(zip(ws, outs)):
+        np.testing.assert_array_equal(o.cpu().numpy().view(np.uint32), want_q(w, 9), err_msg=f"tensor {i}")
+    layers = W.resnet50_layers()
+    ws = [W.gen_float_weights(L.k, L.crs, seed=2000 + i) for i, L in enumerate(layers)]
+    say(f"quantize_q_many resnet50 {len(ws)} tensors")
+    outs = ops.quantize_shift_weights_q_many([to_dev(w) for w in ws])
+    for L, w, o in zip(layers, ws, outs):
+        np.testing.assert_array_equal(o.cpu().numpy().view(np.uint32), want_q(w), err_msg=L.name)
