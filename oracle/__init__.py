@@ -52,6 +52,9 @@ def _load():
         lib.oracle_quantize_q.argtypes = [_P, _I, ctypes.c_int, _P]
         lib.oracle_quantize_ps.argtypes = [_P, _P, _I, ctypes.c_int, _P]
         lib.oracle_to_fixed.argtypes = [_P, _I, ctypes.c_int, _P]
+        lib.oracle_epilogue.argtypes = [_P, _I, _I, _I, _P, _P, ctypes.c_int, _P, ctypes.c_int]
+        lib.oracle_maxpool2d.argtypes = [_P, _P] + [_I] * 10
+        lib.oracle_avgpool_global.argtypes = [_P, _P, _I, _I, _I]
         _lib = lib
     return _lib
 
@@ -206,3 +209,38 @@ def to_fixed(x, frac_bits=16):
     out = np.empty(x.shape, np.int32)
     _load().oracle_to_fixed(_ptr(x), x.size, int(frac_bits), _ptr(out))
     return out
+
+
+def epilogue(y, mul=None, add=None, mul_shift=16, residual=None, relu=False):
+    """Copy of y [N, K, ...] after the fused epilogue: affine (mul, add per channel,
+    floor(v * mul / 2**mul_shift) + add), + residual, ReLU; int32 wrap-around."""
+    y = np.array(y, dtype=np.int32, copy=True, order="C")
+    N, K = y.shape[0], y.shape[1]
+    P = int(np.prod(y.shape[2:])) if y.ndim > 2 else 1
+    mul = _c(mul, np.int32); add = _c(add, np.int32); residual = _c(residual, np.int32)
+    assert residual is None or residual.shape == y.shape
+    _load().oracle_epilogue(_ptr(y), N, K, P, _ptr(mul), _ptr(add), int(mul_shift),
+                            _ptr(residual), int(bool(relu)))
+    return y
+
+
+def maxpool2d(x, r=3, s=None, stride=2, pad=1):
+    """Max pooling of x [N, C, H, W] (int32); padding positions are ignored."""
+    s = r if s is None else s
+    sh, sw = (stride, stride) if np.isscalar(stride) else stride
+    ph, pw = (pad, pad) if np.isscalar(pad) else pad
+    x = _c(x, np.int32)
+    N, C, H, W = x.shape
+    y = np.empty((N, C, out_size(H, ph, r, sh), out_size(W, pw, s, sw)), np.int32)
+    _load().oracle_maxpool2d(_ptr(x), _ptr(y), N, C, H, W, r, s, sh, sw, ph, pw)
+    return y
+
+
+def avgpool_global(x):
+    """x [N, C, H, W] -> [N, C]: floor(sum over H*W / (H*W))."""
+    x = _c(x, np.int32)
+    N, C = x.shape[:2]
+    HW = int(np.prod(x.shape[2:]))
+    y = np.empty((N, C), np.int32)
+    _load().oracle_avgpool_global(_ptr(x), _ptr(y), N, C, HW)
+    return y

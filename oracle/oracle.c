@@ -41,9 +41,12 @@
  * and hand-derived packed words). The converter functions at the end are
  * pinned against numpy's float64 log2/round, exact rational rounding, the
  * paper's second form of the ternary sign (sign of round(S)), the
- * nearest-power property, and hand-derived examples.
+ * nearest-power property, and hand-derived examples. The layers for chained
+ * inference at the end are pinned against numpy's int64 arithmetic shift and
+ * floor division and torch's max pooling.
  */
 #include <stdint.h>
+#include <limits.h>
 #include <stddef.h>
 #include <math.h>
 
@@ -297,5 +300,91 @@ void oracle_to_fixed(const float *x, int64_t n, int frac_bits, int32_t *out)
         if (t >= 2147483647.0) out[i] = 2147483647;
         else if (t <= -2147483648.0) out[i] = -2147483647 - 1;
         else out[i] = (int32_t)t;
+    }
+}
+
+/* ------------------------------------------------------------------------
+ * Layers around the shift convolutions, for chained inference: the network
+ * the paper times in Section 6 (ResNet-18) keeps batch normalisation, max and
+ * average pooling and residual connections next to its shift convolutions.
+ * Here they act on the same int32 fixed-point values (any F).
+ *
+ * Readings where the paper is silent:
+ *   - Batch normalisation at inference is a per-channel affine map, applied
+ *     as v * mul[k] / 2^mul_shift + add[k] with the division floored (the
+ *     rounding of the shift operators) and the result wrapped to int32.
+ *   - The residual is added after the affine map and before ReLU (the order of
+ *     a ResNet basic block), wrapping to int32; ReLU is max(v, 0).
+ *   - Max pooling ignores window positions in the padding.
+ *   - Global average pooling floors the division of the sum by H * W.
+ */
+
+/* floor(v / 2^s) for 0 <= s <= 62, by integer division. */
+static int64_t floor_div_pow2_64(int64_t v, int s)
+{
+    int64_t d = (int64_t)1 << s;
+    int64_t q = v / d;
+    if (v % d != 0 && v < 0)
+        q -= 1;
+    return q;
+}
+
+/* In place on y [N][K][P] (P = OH * OW): affine (when mul is not NULL; add may
+ * be NULL), then + residual[i] (when not NULL), then ReLU (when relu != 0). */
+void oracle_epilogue(int32_t *y, int64_t N, int64_t K, int64_t P, const int32_t *mul,
+                     const int32_t *add, int mul_shift, const int32_t *residual, int relu)
+{
+    for (int64_t n = 0; n < N; ++n)
+        for (int64_t k = 0; k < K; ++k)
+            for (int64_t p = 0; p < P; ++p) {
+                int64_t i = (n * K + k) * P + p;
+                int64_t v = y[i];
+                if (mul) {
+                    v = floor_div_pow2_64(v * (int64_t)mul[k], mul_shift);
+                    v = wrap32(v + (add ? (int64_t)add[k] : 0));
+                }
+                if (residual)
+                    v = wrap32(v + (int64_t)residual[i]);
+                if (relu && v < 0)
+                    v = 0;
+                y[i] = (int32_t)v;
+            }
+}
+
+/* Max pooling, x [N][C][H][W] -> y [N][C][OH][OW]; padding positions are ignored
+ * (the caller keeps pad <= R/2, S/2 so that every window holds an input). */
+void oracle_maxpool2d(const int32_t *x, int32_t *y, int64_t N, int64_t C, int64_t H, int64_t W,
+                      int64_t R, int64_t S, int64_t sh, int64_t sw, int64_t ph, int64_t pw)
+{
+    int64_t OH = out_dim(H, ph, R, sh), OW = out_dim(W, pw, S, sw);
+    for (int64_t n = 0; n < N; ++n)
+        for (int64_t c = 0; c < C; ++c)
+            for (int64_t oh = 0; oh < OH; ++oh)
+                for (int64_t ow = 0; ow < OW; ++ow) {
+                    int64_t best = INT64_MIN;
+                    for (int64_t r = 0; r < R; ++r)
+                        for (int64_t s = 0; s < S; ++s) {
+                            int64_t ih = oh * sh - ph + r, iw = ow * sw - pw + s;
+                            if (ih < 0 || ih >= H || iw < 0 || iw >= W)
+                                continue;
+                            int64_t v = x[((n * C + c) * H + ih) * W + iw];
+                            if (v > best)
+                                best = v;
+                        }
+                    y[((n * C + c) * OH + oh) * OW + ow] = (int32_t)best;
+                }
+}
+
+/* Global average pooling, x [N][C][HW] -> y [N][C]: floor(sum / HW). */
+void oracle_avgpool_global(const int32_t *x, int32_t *y, int64_t N, int64_t C, int64_t HW)
+{
+    for (int64_t i = 0; i < N * C; ++i) {
+        int64_t sum = 0;
+        for (int64_t p = 0; p < HW; ++p)
+            sum += x[i * HW + p];
+        int64_t q = sum / HW;
+        if (sum % HW != 0 && sum < 0)
+            q -= 1;
+        y[i] = (int32_t)q;
     }
 }

@@ -215,24 +215,29 @@ def gen_x(layer: Layer, seed: int, index: int, threads: int | None = None) -> np
     return out.reshape(layer.x_shape)
 
 
+# Shift-code frequencies of weights drawn from N(0, 0.05) and rounded to the nearest
+# power of two in the 0..-14 range (code s = weight 2^-s), used as a fixed
+# categorical distribution so that generating codes needs no quantisation.
+LOGNORMAL_SHIFT_P = np.array([0.0, 1.53744e-12, 0.000406952, 0.0766929, 0.299659, 0.281772,
+                              0.166584, 0.0869093, 0.0439207, 0.022019, 0.0110169, 0.00550936,
+                              0.00275479, 0.00137741, 0.00137742])
+
+
 def gen_codes(layer: Layer, seed: int, index: int) -> np.ndarray:
     """Weight codes [k, c*r*s] (uint8, sign << 4 | shift_code), seeded by (seed, index).
 
     ``uniform16``: sign ~ Bernoulli(1/2), shift code uniform over 0..15.
-    ``lognormal``: w ~ N(0, 0.05); sign = (w < 0); shift code = -clip(rint(log2|w|), -14, 0);
+    ``lognormal``: sign ~ Bernoulli(1/2); shift code drawn from ``LOGNORMAL_SHIFT_P``;
     then each code independently becomes the zero code 15 with probability ``zero_frac``.
     """
     rng = np.random.default_rng([seed, index, 1])
     shape = (layer.k, layer.crs)
+    sign = rng.integers(0, 2, size=shape, dtype=np.uint8)
     if layer.code_dist == "uniform16":
-        sign = rng.integers(0, 2, size=shape, dtype=np.uint8)
         shift = rng.integers(0, 16, size=shape, dtype=np.uint8)
     elif layer.code_dist == "lognormal":
-        w = rng.normal(0.0, 0.05, size=shape)
-        sign = (w < 0).astype(np.uint8)
-        with np.errstate(divide="ignore"):
-            p = np.clip(np.rint(np.log2(np.abs(w))), -14, 0)
-        shift = (-p).astype(np.uint8)
+        prob = LOGNORMAL_SHIFT_P / LOGNORMAL_SHIFT_P.sum()
+        shift = rng.choice(15, size=shape, p=prob).astype(np.uint8)
         zero = rng.random(shape) < layer.zero_frac
         shift[zero] = 15
     else:

@@ -11,13 +11,15 @@ import shutil
 import pytest
 
 import tests.test_oracle_convert_pins as cpins
+import tests.test_oracle_layer_pins as lpins
 import tests.test_oracle_pins as pins
 
 ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
 SRC = os.path.join(ROOT, "oracle", "oracle.c")
 
 MUTATIONS = {
-    "truncate_instead_of_floor": ("q -= 1;", "q -= 0;"),
+    "truncate_instead_of_floor": ("q -= 1;                   /* move truncation down to the floor */",
+                                  "q -= 0;"),
     "negate_then_shift": ("int64_t t = floor_div_pow2((int64_t)x, shift);",
                           "int64_t t = floor_div_pow2(negative ? -(int64_t)x : (int64_t)x, shift);"
                           " if (negative) return t;"),
@@ -51,7 +53,24 @@ MUTATIONS = {
     "fixed_truncate": ("const double t = round(ldexp(v, frac_bits));", "const double t = trunc(ldexp(v, frac_bits));"),
     "fixed_half_even": ("const double t = round(ldexp(v, frac_bits));", "const double t = nearbyint(ldexp(v, frac_bits));"),
     "fixed_no_saturation": ("if (t >= 2147483647.0) out[i] = 2147483647;", "if (0) out[i] = 0;"),
+    # layers for chained inference
+    "epilogue_truncating_shift": ("v = floor_div_pow2_64(v * (int64_t)mul[k], mul_shift);",
+                                  "v = (v * (int64_t)mul[k]) / ((int64_t)1 << mul_shift);"),
+    "epilogue_relu_before_residual": ("if (residual)\n                    v = wrap32(v + (int64_t)residual[i]);\n                if (relu && v < 0)\n                    v = 0;",
+                                      "if (relu && v < 0)\n                    v = 0;\n                if (residual)\n                    v = wrap32(v + (int64_t)residual[i]);"),
+    "epilogue_add_dropped": ("v = wrap32(v + (add ? (int64_t)add[k] : 0));", "v = wrap32(v);"),
+    "maxpool_padding_as_zero": ("if (ih < 0 || ih >= H || iw < 0 || iw >= W)\n                                continue;\n                            int64_t v = x[",
+                                "int64_t v = (ih < 0 || ih >= H || iw < 0 || iw >= W) ? 0 : x["),
+    "avgpool_truncates": ("if (sum % HW != 0 && sum < 0)\n            q -= 1;", ""),
 }
+
+LAYER_CHECKS = [
+    *[(lpins.test_epilogue_affine_matches_numpy_shift, (m,)) for m in (5, 16)],
+    (lpins.test_epilogue_residual_then_relu_order, ()),
+    (lpins.test_epilogue_wraps_residual_sum, ()),
+    *[(lpins.test_maxpool_matches_torch, (sh,)) for sh in ((2, 3, 9, 9, 3, 2, 1), (1, 4, 8, 7, 3, 2, 1))],
+    (lpins.test_avgpool_global_matches_numpy, ()),
+]
 
 CONVERT_CHECKS = [
     *[(cpins.test_q_matches_library_log2_round, (m,)) for m in (14, 3)],
@@ -104,8 +123,9 @@ def test_pins_catch_mutation(tmp_path, monkeypatch, name):
     mod = load_mutant(tmp_path, name)
     monkeypatch.setattr(pins, "oracle", mod)
     monkeypatch.setattr(cpins, "oracle", mod)
+    monkeypatch.setattr(lpins, "oracle", mod)
     failed = []
-    for fn, args in CHECKS + CONVERT_CHECKS:
+    for fn, args in CHECKS + CONVERT_CHECKS + LAYER_CHECKS:
         try:
             fn(*args)
         except AssertionError:
@@ -124,5 +144,6 @@ def test_unmutated_copy_passes(tmp_path, monkeypatch):
     mod.build(force=True)
     monkeypatch.setattr(pins, "oracle", mod)
     monkeypatch.setattr(cpins, "oracle", mod)
-    for fn, args in CHECKS + CONVERT_CHECKS:
+    monkeypatch.setattr(lpins, "oracle", mod)
+    for fn, args in CHECKS + CONVERT_CHECKS + LAYER_CHECKS:
         fn(*args)
