@@ -31,6 +31,9 @@ WORKLOADS = {"linear_small": 0, "conv_single": 1, "linear_fc6": 2, "resnet18": 3
 # The step upstream of the operators: float weights -> packed codes (DeepShift-Q)
 # and the float input batch -> fixed point, for every layer of ResNet-50 at N = 128.
 CONVERT_WORKLOADS = {"convert_resnet50": 4}
+# Chained inference: a ResNet-18 forward pass with shift convolutions (batch
+# normalisation, residual and ReLU fused into each convolution), N = 32.
+NETWORK_WORKLOADS = {"resnet18_infer": 32}
 
 # MI355X: 256 CUs, 4 SIMD16 per CU -> 64 int32 lane-ops per clock per CU, 2.4 GHz peak clock.
 CUS, LANES_PER_CU, CLOCK_GHZ = 256, 64, 2.4
@@ -60,7 +63,7 @@ def parse():
     ap.add_argument("--gpus", type=int, default=1)
     ap.add_argument("--steps", type=int, default=5)
     ap.add_argument("--warmup", type=int, default=2)
-    ap.add_argument("--workload", default="resnet50", choices=sorted(WORKLOADS) + sorted(CONVERT_WORKLOADS))
+    ap.add_argument("--workload", default="resnet50", choices=sorted(WORKLOADS) + sorted(CONVERT_WORKLOADS) + sorted(NETWORK_WORKLOADS))
     ap.add_argument("--cpu-batch", type=int, default=None,
                     help="batch of the oracle sample (default: sized for ~10-30 s)")
     ap.add_argument("--cpu-seconds", type=float, default=10.0,
@@ -254,6 +257,79 @@ def bench_convert(args):
     print(json.dumps(out), flush=True)
 
 
+def bench_network(args):
+    """One step = one forward pass of the network over the batch (every op on the GPU,
+    input resident in HBM); reported in images/s, with the shift convolutions'
+    SAC rate against the VALU roofline."""
+    import torch
+    from paper_1905_13298_amd import ops
+    from paper_1905_13298_amd import workloads as W
+    from paper_1905_13298_amd.network import ShiftNetwork
+
+    n = NETWORK_WORKLOADS[args.workload]
+    dev = torch.device("cuda:0")
+    torch.cuda.set_device(dev)
+    graph, params = W.resnet18_graph(n), W.resnet18_params(n)
+    net = ShiftNetwork(graph, params, device=dev)
+    x = torch.from_numpy(W.gen_images(n)).to(dev)
+    for _ in range(args.warmup):
+        net.forward(x)
+    stream = torch.cuda.current_stream(dev)
+    ev = [[(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True))
+           for _ in graph] for _ in range(args.steps)]
+    t0, t1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    torch.cuda.synchronize()
+    t0.record(stream)
+    for s in range(args.steps):
+        buf = {"x": x}
+        for i, op in enumerate(graph):
+            ev[s][i][0].record(stream)
+            net.run_op(op, buf)
+            ev[s][i][1].record(stream)
+    t1.record(stream)
+    torch.cuda.synchronize()
+    ms_per_step = t0.elapsed_time(t1) / args.steps
+    op_ms = [sum(ev[s][i][0].elapsed_time(ev[s][i][1]) for s in range(args.steps)) / args.steps
+             for i in range(len(graph))]
+    conv_idx = [i for i, op in enumerate(graph) if op["op"] in ("conv", "linear")]
+    sac = sum(graph[i]["layer"].sac for i in conv_idx)
+    conv_ms = sum(op_ms[i] for i in conv_idx)
+    per_kind = {}
+    for i, op in enumerate(graph):
+        per_kind[op["op"]] = round(per_kind.get(op["op"], 0.0) + op_ms[i], 4)
+    achieved = sac / (conv_ms * 1e-3) / 1e12
+    roofline = {"bound": "alu", "achieved": round(achieved, 4), "peak": SAC_PEAK_T,
+                "unit": "TSAC/s", "frac": round(achieved / SAC_PEAK_T, 4), "traffic": None,
+                "kernel": "shift convolutions with fused epilogue (all 21 layers)",
+                "launches_per_step": len(conv_idx), "avg_launch_ms": round(conv_ms / len(conv_idx), 5),
+                "sac_per_launch_avg": sac // len(conv_idx),
+                "timed_span": "library call per layer (weight decode + conv + fused epilogue)"}
+    cpu = None
+    if not args.no_cpu_baseline:
+        import oracle
+        nc = 8
+        xs = W.gen_images(nc)
+        pc = W.resnet18_params(nc)
+        gc = W.resnet18_graph(nc)
+        t = time.perf_counter()
+        oracle.network_forward(gc, pc, xs)
+        dt = time.perf_counter() - t
+        cpu = {"value": round(nc / dt, 3), "unit": "images/s", "cores": oracle.max_threads(),
+               "kind": "oracle", "sample": f"one forward pass over {nc} images ({dt:.1f} s)"}
+    ips = n / (ms_per_step * 1e-3)
+    out = {
+        "metric": "images/s of a ResNet-18 forward pass with shift convolutions (chained, fused epilogues)",
+        "value": round(ips, 1), "unit": "images/s", "n_gpus": 1, "steps": args.steps,
+        "warmup": args.warmup, "ms_per_step": round(ms_per_step, 4), "ms_per_image": round(ms_per_step / n, 5),
+        "higher_is_better": True, "scaling": "weak", "vs_baseline": None, "dtype": "i32",
+        "data": "synthetic",
+        "config": {"workload": f"resnet18_forward_n{n}_224", "batch": n, "ops": len(graph),
+                   "sac_per_step": sac, "frac_bits": W.FRAC_BITS, "parallelism": "single GPU"},
+        "ms_by_op": per_kind, "roofline": roofline, "cpu_baseline": cpu,
+    }
+    print(json.dumps(out), flush=True)
+
+
 def main():
     args = parse()
     if args.copy_only:
@@ -270,6 +346,9 @@ def main():
 
     if args.workload in CONVERT_WORKLOADS:
         bench_convert(args)
+        return
+    if args.workload in NETWORK_WORKLOADS:
+        bench_network(args)
         return
 
     import torch

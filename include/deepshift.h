@@ -54,6 +54,10 @@
 extern "C" {
 #endif
 
+/* flags bit of the shift operators: replace every output v by max(v, 0)
+ * (ReLU fused into the operator, as Section 6 suggests). */
+#define DS_RELU 1u
+
 typedef enum ds_status {
     DS_SUCCESS = 0,
     DS_ERR_NULL_POINTER = 1,     /* a required pointer is NULL */
@@ -90,7 +94,7 @@ ds_status ds_unpack_shift_weights(const uint32_t *packed, int64_t rows, int64_t 
  * bias     device int32 [out_features] with the same F, or NULL for none
  * y        device int32 [batch][out_features], written (not accumulated)
  * frac_bits in [0, 31]: the F of x, bias and y (validated, not used by the math)
- * flags    reserved, must be 0
+ * flags    0, or DS_RELU: y = max(y, 0) after the sum (fused)
  * stream   hipStream_t to enqueue on (NULL = default stream) */
 ds_status ds_linear_shift(const int32_t *x, const uint32_t *w_packed, const int32_t *bias,
                           int32_t *y, int64_t batch, int64_t in_features, int64_t out_features,
@@ -164,6 +168,39 @@ ds_status ds_quantize_shift_weights_ps(const float *p, const float *s, int64_t r
  * 0; stream as for ds_linear_shift. */
 ds_status ds_to_fixed_point(const float *x, int64_t n, int32_t frac_bits, int32_t *y,
                             uint32_t flags, void *stream);
+
+/* ConvShift followed, in the same call, by what a ResNet block applies to a
+ * convolution's output (batch normalisation, residual add, ReLU; fusing them
+ * into the convolution is the optimisation Section 6 proposes). For each
+ * output v = the ds_conv2d_shift result for channel k at flat index i:
+ *     v = floor(v * mul[k] / 2^mul_shift) + add[k]     when mul != NULL
+ *     v = v + residual[i]                              when residual != NULL
+ *     v = max(v, 0)                                    when flags & DS_RELU
+ * all in int32 with wrap-around (the product is formed in 64 bits). mul holds
+ * a per-channel scale with mul_shift fractional bits (batch normalisation at
+ * inference folds into it and add); add may be NULL (0) but needs mul.
+ * mul, add: device int32 [k] or NULL; residual: device int32 with y's shape
+ * [n][k][oh][ow] or NULL, and must not overlap y; mul_shift in [0, 31].
+ * Other arguments and errors as for ds_conv2d_shift. */
+ds_status ds_conv2d_shift_fused(const int32_t *x, const uint32_t *w_packed, const int32_t *bias,
+                                const int32_t *mul, const int32_t *add, int32_t mul_shift,
+                                const int32_t *residual, int32_t *y, int64_t n, int64_t c,
+                                int64_t h, int64_t w, int64_t k, int64_t r, int64_t s,
+                                int32_t stride_h, int32_t stride_w, int32_t pad_h, int32_t pad_w,
+                                int32_t frac_bits, uint32_t flags, void *stream);
+
+/* Max pooling of int32 x [n][c][h][w] into y [n][c][oh][ow] (oh, ow as for
+ * ConvShift); window positions in the padding are ignored, so pad_h <= r/2 and
+ * pad_w <= s/2 are required (every window then holds an input). The max pool
+ * of the ResNet stem is r = s = 3, stride 2, pad 1. flags must be 0. */
+ds_status ds_maxpool2d(const int32_t *x, int32_t *y, int64_t n, int64_t c, int64_t h, int64_t w,
+                       int64_t r, int64_t s, int32_t stride_h, int32_t stride_w, int32_t pad_h,
+                       int32_t pad_w, uint32_t flags, void *stream);
+
+/* Global average pooling: y[n][c] = floor(sum over h*w of x[n][c] / (h*w)),
+ * x device int32 [n][c][h][w], y device int32 [n][c]. flags must be 0. */
+ds_status ds_avgpool2d_global(const int32_t *x, int32_t *y, int64_t n, int64_t c, int64_t h,
+                              int64_t w, uint32_t flags, void *stream);
 
 /* Multiplication-based comparison operators. Not part of DeepShift: they run
  * the same tiling as the shift operators with a 32-bit integer multiply in

@@ -33,6 +33,9 @@ SIGNATURES = {
     "ds_quantize_shift_weights_ps": (ctypes.c_int, [_P, _P, _I64, _I64, _I32, _P, _U32, _P]),
     "ds_quantize_shift_weights_q_many": (ctypes.c_int, [_I64, _P, _P, _P, _I32, _P, _U32, _P]),
     "ds_to_fixed_point": (ctypes.c_int, [_P, _I64, _I32, _P, _U32, _P]),
+    "ds_conv2d_shift_fused": (ctypes.c_int, [_P, _P, _P, _P, _P, _I32, _P, _P] + [_I64] * 7 + [_I32] * 4 + [_I32, _U32, _P]),
+    "ds_maxpool2d": (ctypes.c_int, [_P, _P] + [_I64] * 6 + [_I32] * 4 + [_U32, _P]),
+    "ds_avgpool2d_global": (ctypes.c_int, [_P, _P] + [_I64] * 4 + [_U32, _P]),
     "ds_status_string": (ctypes.c_char_p, [ctypes.c_int]),
     "ds_last_error_message": (ctypes.c_char_p, []),
 }

@@ -189,6 +189,31 @@ fill_init_kernel(const int32_t *__restrict__ init, int32_t *__restrict__ y, int6
         y[idx] = init[(idx / OHOW) % K];
 }
 
+// The epilogue on one output value v of channel k at flat index o.
+__device__ __forceinline__ uint32_t apply_epilogue(uint32_t v, int k, int64_t o, const Epilogue &e)
+{
+    if (e.mul) {
+        const int64_t t = (int64_t(int32_t(v)) * e.mul[k]) >> e.mul_shift;  // arithmetic: floor
+        v = uint32_t(t) + (e.add ? uint32_t(e.add[k]) : 0u);
+    }
+    if (e.res) v += uint32_t(e.res[o]);
+    if (e.relu && int32_t(v) < 0) v = 0u;
+    return v;
+}
+
+// The epilogue as a pass of its own over y [N][K][P], where it cannot run in the
+// producing kernel's registers (split-K partial sums, transposed outputs, the
+// one-thread-per-output kernel).
+__global__ void __launch_bounds__(256)
+epilogue_kernel(int32_t *__restrict__ y, int64_t total, int K, int P, const Epilogue e)
+{
+    for (int64_t idx = int64_t(blockIdx.x) * blockDim.x + threadIdx.x; idx < total;
+         idx += int64_t(gridDim.x) * blockDim.x) {
+        const int k = int((idx / P) % K);
+        y[idx] = int32_t(apply_epilogue(uint32_t(y[idx]), k, idx, e));
+    }
+}
+
 // xt[c][b] = x[b][c] for a row-major x [rows][cols]: 64 x 64 tiles through LDS,
 // so that both the reads and the writes are coalesced.
 __global__ void __launch_bounds__(256)
@@ -241,6 +266,8 @@ struct TiledParams {
     int PLANE;          // LDS words per channel per chunk (window mode, multiple of 64)
     int tiles_p, tiles_k, chunks_per_split, nchunks;
     int atomic_out;     // split-K: add partial sums atomically into y
+    int fuse_epi;       // apply the epilogue in the kernel (not split, not transposed)
+    Epilogue epi;
     int x_bytes;        // size of x in bytes (< 2^31)
     FastDiv div_ohow, div_ow, div_vh, div_iwp;
 };
@@ -510,6 +537,8 @@ tiled_kernel(const int32_t *__restrict__ x, const int32_t *__restrict__ wd,
             const int o = yoff[i] + k * p.OHOW;
             if (p.atomic_out)
                 atomicAdd(reinterpret_cast<unsigned int *>(y) + o, acc[i][t]);
+            else if (p.fuse_epi)
+                y[o] = int32_t(apply_epilogue(acc[i][t] + ini, k, o, p.epi));
             else
                 y[o] = int32_t(acc[i][t] + ini);
         }
@@ -719,8 +748,18 @@ void describe_conv(const ConvGeom &g0, char *buf, size_t len)
                  splits);
 }
 
+// The epilogue as its own pass over y (see epilogue_kernel).
+static hipError_t run_epilogue(const ConvGeom &g, int32_t *y, const Epilogue &epi, hipStream_t st)
+{
+    const int64_t total = int64_t(g.n) * g.k * g.oh * g.ow;
+    const int grid = int(std::min<int64_t>((total + 255) / 256, 8192));
+    hipLaunchKernelGGL(epilogue_kernel, dim3(grid), dim3(256), 0, st, y, total, g.k, g.oh * g.ow,
+                       epi);
+    return hipGetLastError();
+}
+
 hipError_t run_conv(const ConvGeom &g0, const int32_t *x, const uint32_t *wp, const int32_t *wi,
-                    const int32_t *bias, int32_t *y, Inner op, hipStream_t st)
+                    const int32_t *bias, int32_t *y, Inner op, hipStream_t st, const Epilogue &epi)
 {
     bool rowmajor = false;
     const ConvGeom g = tiled_geometry(g0, rowmajor);
@@ -728,7 +767,10 @@ hipError_t run_conv(const ConvGeom &g0, const int32_t *x, const uint32_t *wp, co
     int plane = 0;
     size_t lds = 0;
     const Variant v = choose_variant(g, plane, lds);
-    if (use_direct(g, v)) return run_direct(g0, x, wp, wi, bias, y, op, st);
+    if (use_direct(g, v)) {
+        const hipError_t e = run_direct(g0, x, wp, wi, bias, y, op, st);
+        return e == hipSuccess && epi.any() ? run_epilogue(g0, y, epi, st) : e;
+    }
 
     const int RS = g.r * g.s;
     int tiles_p, tiles_k, nchunks, splits, cps;
@@ -746,6 +788,8 @@ hipError_t run_conv(const ConvGeom &g0, const int32_t *x, const uint32_t *wp, co
     p.Jpad = Jpad; p.VH = g.h + 2 * g.ph; p.IWP = g.w + 2 * g.pw; p.PLANE = plane;
     p.tiles_p = tiles_p; p.tiles_k = tiles_k; p.chunks_per_split = cps; p.nchunks = nchunks;
     p.atomic_out = splits > 1;
+    p.fuse_epi = epi.any() && !p.atomic_out && !rowmajor;
+    p.epi = epi;
     p.x_bytes = int(x_bytes);
     p.div_ohow = make_fastdiv(uint32_t(p.OHOW));
     p.div_ow = make_fastdiv(uint32_t(g.ow));
@@ -804,6 +848,7 @@ hipError_t run_conv(const ConvGeom &g0, const int32_t *x, const uint32_t *wp, co
                            g0.n);
         e = hipGetLastError();
     }
+    if (e == hipSuccess && epi.any() && !p.fuse_epi) e = run_epilogue(g0, y, epi, st);
     const hipError_t ef = hipFreeAsync(scratch, st);
     return e != hipSuccess ? e : ef;
 }

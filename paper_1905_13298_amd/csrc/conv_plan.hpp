@@ -19,11 +19,23 @@ struct ConvGeom {
 // multiplication-based comparison (int32 multiply-add).
 enum class Inner { Shift, Mul };
 
+// What follows the convolution on each output y[n][k][p] (all optional):
+//   v = floor(v * mul[k] / 2^mul_shift) + add[k]   (when mul; add may be NULL)
+//   v = v + res[n][k][p]                           (when res)
+//   v = max(v, 0)                                  (when relu)
+// with int32 wrap-around, as in the accumulation.
+struct Epilogue {
+    const int32_t *mul = nullptr, *add = nullptr, *res = nullptr;
+    int mul_shift = 0;
+    bool relu = false;
+    bool any() const { return mul || res || relu; }
+};
+
 // Enqueue the whole computation of y on `stream`. Exactly one of `wpacked`
 // (Shift) and `wint` (Mul) is used.
 hipError_t run_conv(const ConvGeom &g, const int32_t *x, const uint32_t *wpacked,
                     const int32_t *wint, const int32_t *bias, int32_t *y, Inner op,
-                    hipStream_t stream);
+                    hipStream_t stream, const Epilogue &epi = Epilogue());
 
 // Short name of the kernel run_conv would launch for g (see ds_conv2d_shift_describe).
 void describe_conv(const ConvGeom &g, char *buf, size_t len);

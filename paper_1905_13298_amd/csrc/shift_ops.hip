@@ -49,13 +49,14 @@ static ds_status check_shape(int64_t n, int64_t c, int64_t h, int64_t w, int64_t
 static ds_status check_conv(const void *x, const void *wts, const void *bias, const void *y,
                             int64_t n, int64_t c, int64_t h, int64_t w, int64_t k, int64_t r,
                             int64_t s, int32_t sh, int32_t sw, int32_t ph, int32_t pw,
-                            int32_t frac_bits, uint32_t flags, bool packed, ConvGeom &g)
+                            int32_t frac_bits, uint32_t flags, bool packed, ConvGeom &g,
+                            uint32_t allowed_flags)
 {
     if (!x || !wts || !y) return fail(DS_ERR_NULL_POINTER, "x, weights and y must not be NULL");
     ds_status st = check_shape(n, c, h, w, k, r, s, sh, sw, ph, pw, packed, g);
     if (st != DS_SUCCESS) return st;
     if (frac_bits < 0 || frac_bits > 31) return fail(DS_ERR_INVALID_ARG, "frac_bits must be in [0, 31]");
-    if (flags != 0) return fail(DS_ERR_INVALID_ARG, "flags must be 0");
+    if (flags & ~allowed_flags) return fail(DS_ERR_INVALID_ARG, "unknown flags 0x%x", flags);
     const int64_t xb = 4 * int64_t(g.n) * g.c * g.h * g.w;
     const int64_t yb = 4 * int64_t(g.n) * g.k * g.oh * g.ow;
     const int64_t wb = 4 * (packed ? int64_t(g.k) * row_words(g.crs) : int64_t(g.k) * g.crs);
@@ -87,11 +88,54 @@ extern "C" ds_status ds_conv2d_shift(const int32_t *x, const uint32_t *w_packed,
 {
     ConvGeom g;
     ds_status st = check_conv(x, w_packed, bias, y, n, c, h, w, k, r, s, stride_h, stride_w,
-                              pad_h, pad_w, frac_bits, flags, true, g);
+                              pad_h, pad_w, frac_bits, flags, true, g, DS_RELU);
     if (st != DS_SUCCESS) return st;
+    Epilogue epi;
+    epi.relu = (flags & DS_RELU) != 0;
     return hip_status(run_conv(g, x, w_packed, nullptr, bias, y, Inner::Shift,
-                               static_cast<hipStream_t>(stream)),
+                               static_cast<hipStream_t>(stream), epi),
                       "ds_conv2d_shift");
+}
+
+extern "C" ds_status ds_conv2d_shift_fused(const int32_t *x, const uint32_t *w_packed,
+                                           const int32_t *bias, const int32_t *mul,
+                                           const int32_t *add, int32_t mul_shift,
+                                           const int32_t *residual, int32_t *y, int64_t n,
+                                           int64_t c, int64_t h, int64_t w, int64_t k, int64_t r,
+                                           int64_t s, int32_t stride_h, int32_t stride_w,
+                                           int32_t pad_h, int32_t pad_w, int32_t frac_bits,
+                                           uint32_t flags, void *stream)
+{
+    ConvGeom g;
+    // Arguments first (no device access), then the buffers.
+    if (x && w_packed && y) {
+        ds_status st = check_shape(n, c, h, w, k, r, s, stride_h, stride_w, pad_h, pad_w, true, g);
+        if (st != DS_SUCCESS) return st;
+        if (add && !mul) return fail(DS_ERR_INVALID_ARG, "add needs mul");
+        if (mul_shift < 0 || mul_shift > 31) return fail(DS_ERR_INVALID_ARG, "mul_shift must be in [0, 31]");
+        const int64_t kb = 4 * int64_t(g.k);
+        const int64_t yb = 4 * int64_t(g.n) * g.k * g.oh * g.ow;
+        if (overlap(y, yb, mul, kb) || overlap(y, yb, add, kb) || overlap(y, yb, residual, yb))
+            return fail(DS_ERR_INVALID_ARG, "y overlaps an input");
+    }
+    ds_status st = check_conv(x, w_packed, bias, y, n, c, h, w, k, r, s, stride_h, stride_w,
+                              pad_h, pad_w, frac_bits, flags, true, g, DS_RELU);
+    if (st != DS_SUCCESS) return st;
+    const int64_t kb = 4 * int64_t(g.k);
+    const int64_t yb = 4 * int64_t(g.n) * g.k * g.oh * g.ow;
+    if (mul && !device_range_ok(mul, kb)) return fail(DS_ERR_INVALID_ARG, "mul is not a device buffer of %lld bytes", (long long)kb);
+    if (add && !device_range_ok(add, kb)) return fail(DS_ERR_INVALID_ARG, "add is not a device buffer of %lld bytes", (long long)kb);
+    if (residual && !device_range_ok(residual, yb))
+        return fail(DS_ERR_INVALID_ARG, "residual is not a device buffer of %lld bytes", (long long)yb);
+    Epilogue epi;
+    epi.mul = mul;
+    epi.add = add;
+    epi.mul_shift = mul_shift;
+    epi.res = residual;
+    epi.relu = (flags & DS_RELU) != 0;
+    return hip_status(run_conv(g, x, w_packed, nullptr, bias, y, Inner::Shift,
+                               static_cast<hipStream_t>(stream), epi),
+                      "ds_conv2d_shift_fused");
 }
 
 extern "C" ds_status ds_linear_shift(const int32_t *x, const uint32_t *w_packed, const int32_t *bias,
@@ -101,10 +145,12 @@ extern "C" ds_status ds_linear_shift(const int32_t *x, const uint32_t *w_packed,
 {
     ConvGeom g;
     ds_status st = check_conv(x, w_packed, bias, y, batch, in_features, 1, 1, out_features, 1, 1,
-                              1, 1, 0, 0, frac_bits, flags, true, g);
+                              1, 1, 0, 0, frac_bits, flags, true, g, DS_RELU);
     if (st != DS_SUCCESS) return st;
+    Epilogue epi;
+    epi.relu = (flags & DS_RELU) != 0;
     return hip_status(run_conv(g, x, w_packed, nullptr, bias, y, Inner::Shift,
-                               static_cast<hipStream_t>(stream)),
+                               static_cast<hipStream_t>(stream), epi),
                       "ds_linear_shift");
 }
 
@@ -130,7 +176,7 @@ extern "C" ds_status ds_conv2d_mul_i32(const int32_t *x, const int32_t *wts, con
 {
     ConvGeom g;
     ds_status st = check_conv(x, wts, bias, y, n, c, h, w, k, r, s, stride_h, stride_w, pad_h,
-                              pad_w, 0, flags, false, g);
+                              pad_w, 0, flags, false, g, 0);
     if (st != DS_SUCCESS) return st;
     return hip_status(run_conv(g, x, nullptr, wts, bias, y, Inner::Mul,
                                static_cast<hipStream_t>(stream)),
@@ -143,7 +189,7 @@ extern "C" ds_status ds_linear_mul_i32(const int32_t *x, const int32_t *wts, con
 {
     ConvGeom g;
     ds_status st = check_conv(x, wts, bias, y, batch, in_features, 1, 1, out_features, 1, 1, 1,
-                              1, 0, 0, 0, flags, false, g);
+                              1, 0, 0, 0, flags, false, g, 0);
     if (st != DS_SUCCESS) return st;
     return hip_status(run_conv(g, x, nullptr, wts, bias, y, Inner::Mul,
                                static_cast<hipStream_t>(stream)),

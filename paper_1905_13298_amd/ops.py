@@ -14,7 +14,9 @@ from ._native import DeepShiftError, call, lib
 __all__ = ["DeepShiftError", "describe_conv2d", "packed_row_words", "pack_shift_weights", "unpack_shift_weights",
            "linear_shift", "conv2d_shift", "linear_mul_i32", "conv2d_mul_i32", "out_size",
            "quantize_shift_weights_q", "quantize_shift_weights_q_many", "quantize_shift_weights_ps",
-           "to_fixed_point"]
+           "to_fixed_point", "conv2d_shift_fused", "maxpool2d", "avgpool2d_global", "DS_RELU"]
+
+DS_RELU = 1
 
 
 def packed_row_words(cols: int) -> int:
@@ -89,8 +91,9 @@ def _pair(v):
 
 
 def linear_shift(x: torch.Tensor, w_packed: torch.Tensor, bias: torch.Tensor | None = None,
-                 frac_bits: int = 16, out: torch.Tensor | None = None) -> torch.Tensor:
-    """LinearShift: y[b, o] = bias[o] + sum_i term(x[b, i], code[o, i]) (int32, mod 2^32)."""
+                 frac_bits: int = 16, out: torch.Tensor | None = None, relu: bool = False) -> torch.Tensor:
+    """LinearShift: y[b, o] = bias[o] + sum_i term(x[b, i], code[o, i]) (int32, mod 2^32),
+    then max(y, 0) when relu."""
     _dev_i32(x, "x"); _dev_i32(w_packed, "w_packed")
     if bias is not None:
         _dev_i32(bias, "bias")
@@ -100,14 +103,15 @@ def linear_shift(x: torch.Tensor, w_packed: torch.Tensor, bias: torch.Tensor | N
     _dev_i32(y, "out")
     with torch.cuda.device(x.device):
         call("ds_linear_shift", _ptr(x), _ptr(w_packed), _ptr(bias), _ptr(y), batch, fin, fout,
-             frac_bits, 0, _stream(x.device))
+             frac_bits, DS_RELU if relu else 0, _stream(x.device))
     return y
 
 
 def conv2d_shift(x: torch.Tensor, w_packed: torch.Tensor, bias: torch.Tensor | None,
                  kernel_size, stride=1, padding=0, frac_bits: int = 16,
-                 out: torch.Tensor | None = None) -> torch.Tensor:
-    """ConvShift (NCHW): y[n, k, oh, ow] = bias[k] + sum_{c,r,s} term(x[...], code[k, c, r, s])."""
+                 out: torch.Tensor | None = None, relu: bool = False) -> torch.Tensor:
+    """ConvShift (NCHW): y[n, k, oh, ow] = bias[k] + sum_{c,r,s} term(x[...], code[k, c, r, s]),
+    then max(y, 0) when relu."""
     _dev_i32(x, "x"); _dev_i32(w_packed, "w_packed")
     if bias is not None:
         _dev_i32(bias, "bias")
@@ -122,7 +126,7 @@ def conv2d_shift(x: torch.Tensor, w_packed: torch.Tensor, bias: torch.Tensor | N
     _dev_i32(y, "out")
     with torch.cuda.device(x.device):
         call("ds_conv2d_shift", _ptr(x), _ptr(w_packed), _ptr(bias), _ptr(y), n, c, h, w, k, r, s,
-             sh, sw, ph, pw, frac_bits, 0, _stream(x.device))
+             sh, sw, ph, pw, frac_bits, DS_RELU if relu else 0, _stream(x.device))
     return y
 
 
@@ -221,4 +225,55 @@ def to_fixed_point(x: torch.Tensor, frac_bits: int = 16,
     _dev_i32(y, "out")
     with torch.cuda.device(x.device):
         call("ds_to_fixed_point", _ptr(x), x.numel(), frac_bits, _ptr(y), 0, _stream(x.device))
+    return y
+
+
+def conv2d_shift_fused(x: torch.Tensor, w_packed: torch.Tensor, bias, kernel_size, stride=1,
+                       padding=0, mul=None, add=None, mul_shift: int = 16, residual=None,
+                       relu: bool = False, frac_bits: int = 16, out=None) -> torch.Tensor:
+    """ConvShift, then per channel floor(v * mul / 2**mul_shift) + add, + residual, ReLU."""
+    _dev_i32(x, "x"); _dev_i32(w_packed, "w_packed")
+    for t, name in ((bias, "bias"), (mul, "mul"), (add, "add"), (residual, "residual")):
+        if t is not None:
+            _dev_i32(t, name)
+    r, s = _pair(kernel_size)
+    sh, sw = _pair(stride)
+    ph, pw = _pair(padding)
+    n, c, h, w = x.shape
+    k = w_packed.shape[0]
+    oh, ow = out_size(h, ph, r, sh), out_size(w, pw, s, sw)
+    y = out if out is not None else torch.empty((n, k, max(oh, 0), max(ow, 0)), dtype=torch.int32,
+                                                device=x.device)
+    _dev_i32(y, "out")
+    with torch.cuda.device(x.device):
+        call("ds_conv2d_shift_fused", _ptr(x), _ptr(w_packed), _ptr(bias), _ptr(mul), _ptr(add),
+             mul_shift, _ptr(residual), _ptr(y), n, c, h, w, k, r, s, sh, sw, ph, pw, frac_bits,
+             DS_RELU if relu else 0, _stream(x.device))
+    return y
+
+
+def maxpool2d(x: torch.Tensor, kernel_size=3, stride=2, padding=1, out=None) -> torch.Tensor:
+    """Max pooling (int32 NCHW); padding positions are ignored."""
+    _dev_i32(x, "x")
+    r, s = _pair(kernel_size)
+    sh, sw = _pair(stride)
+    ph, pw = _pair(padding)
+    n, c, h, w = x.shape
+    oh, ow = out_size(h, ph, r, sh), out_size(w, pw, s, sw)
+    y = out if out is not None else torch.empty((n, c, max(oh, 0), max(ow, 0)), dtype=torch.int32,
+                                                device=x.device)
+    _dev_i32(y, "out")
+    with torch.cuda.device(x.device):
+        call("ds_maxpool2d", _ptr(x), _ptr(y), n, c, h, w, r, s, sh, sw, ph, pw, 0, _stream(x.device))
+    return y
+
+
+def avgpool2d_global(x: torch.Tensor, out=None) -> torch.Tensor:
+    """x [n, c, h, w] -> [n, c]: floor of the mean over h*w."""
+    _dev_i32(x, "x")
+    n, c, h, w = x.shape
+    y = out if out is not None else torch.empty((n, c), dtype=torch.int32, device=x.device)
+    _dev_i32(y, "out")
+    with torch.cuda.device(x.device):
+        call("ds_avgpool2d_global", _ptr(x), _ptr(y), n, c, h, w, 0, _stream(x.device))
     return y

@@ -289,3 +289,75 @@ def gen_float_acts(n: int, seed: int, scale: float = 4.0) -> np.ndarray:
     """Float32 activations [n], normal with standard deviation ``scale``."""
     rng = np.random.default_rng(seed)
     return rng.standard_normal(n, dtype=np.float32) * np.float32(scale)
+
+
+# ---------------------------------------------------------------------------
+# ResNet-18 with shift convolutions, chained (the network of the paper's
+# Section 6 inference timing). Topology and seeded synthetic parameters only.
+
+BN_SHIFT = 16  # fractional bits of the per-channel batch-normalisation multiplier
+
+
+def resnet18_graph(n: int = 32) -> list:
+    """The forward pass as a list of ops over named int32 buffers (input "x").
+
+    ``conv``: a ResNet-18 convolution layer (``layer``), then batch normalisation,
+    the optional residual buffer ``res`` and ReLU when ``relu``: src -> dst.
+    ``maxpool``: 3x3, stride 2, pad 1. ``avgpool``: global, [n, c, h, w] -> [n, c].
+    ``linear``: the classifier with its bias.
+    """
+    layers = {L.name: L for L in resnet18_layers(n)}
+    g = [{"op": "conv", "layer": layers["conv1"], "src": "x", "dst": "stem", "res": None, "relu": True},
+         {"op": "maxpool", "src": "stem", "dst": "b0", "r": 3, "stride": 2, "pad": 1}]
+    cur = "b0"
+    for stage in (1, 2, 3, 4):
+        for b in (0, 1):
+            pre = f"layer{stage}.{b}"
+            res = cur
+            if stage > 1 and b == 0:
+                g.append({"op": "conv", "layer": layers[pre + ".downsample"], "src": cur,
+                          "dst": pre + ".ds", "res": None, "relu": False})
+                res = pre + ".ds"
+            g.append({"op": "conv", "layer": layers[pre + ".conv1"], "src": cur, "dst": pre + ".t",
+                      "res": None, "relu": True})
+            g.append({"op": "conv", "layer": layers[pre + ".conv2"], "src": pre + ".t",
+                      "dst": pre + ".out", "res": res, "relu": True})
+            cur = pre + ".out"
+    g.append({"op": "avgpool", "src": cur, "dst": "pool"})
+    g.append({"op": "linear", "layer": layers["fc"], "src": "pool", "dst": "logits"})
+    return g
+
+
+def gen_bn(layer: Layer, seed: int, index: int):
+    """Batch-normalisation parameters of a conv layer as (mul [k], add [k]) int32:
+    mul = scale * 2**BN_SHIFT with scale = U[0.8, 1.2] / sqrt(C*R*S * E[w^2]) (E[w^2]
+    the second moment of the synthetic weight distribution, so that activations
+    keep their magnitude from layer to layer), add = N(0, 0.1) * 2**16."""
+    rng = np.random.default_rng([seed, index, 3])
+    p = LOGNORMAL_SHIFT_P / LOGNORMAL_SHIFT_P.sum()
+    ew2 = (1.0 - layer.zero_frac) * float(np.sum(p * 4.0 ** -np.arange(15)))
+    scale = rng.uniform(0.8, 1.2, layer.k) / np.sqrt(layer.crs * ew2)
+    mul = np.rint(scale * float(1 << BN_SHIFT)).astype(np.int32)
+    add = np.rint(rng.normal(0.0, 0.1, layer.k) * float(1 << FRAC_BITS)).astype(np.int32)
+    return mul, add
+
+
+def resnet18_params(n: int = 32, seed: int = 18) -> dict:
+    """Seeded synthetic parameters of every layer of ``resnet18_graph(n)``, by layer
+    name: codes [k, c*r*s] (uint8), and bn (mul, add) for convs or bias for the fc."""
+    params = {}
+    for i, L in enumerate(resnet18_layers(n)):
+        entry = {"codes": gen_codes(L, seed, i)}
+        if L.kind == "conv":
+            entry["bn"] = gen_bn(L, seed, i)
+        else:
+            entry["bias"] = gen_bias(L, seed, i)
+        params[L.name] = entry
+    return params
+
+
+def gen_images(n: int, seed: int = 18) -> np.ndarray:
+    """Input batch [n, 3, 224, 224] int32 F=16: normalised pixels, N(0, 1) clipped to +-3."""
+    rng = np.random.default_rng([seed, 99])
+    a = np.clip(rng.standard_normal((n, 3, 224, 224), dtype=np.float32), -3.0, 3.0)
+    return np.rint(a * float(1 << FRAC_BITS)).astype(np.int32)

@@ -115,7 +115,7 @@ def test_conv_validation_codes():
     assert conv(sh=0) == ARG and conv(sw=-1) == ARG
     assert conv(ph=-1) == ARG
     assert conv(f=-1) == ARG and conv(f=32) == ARG
-    assert conv(flags=1) == ARG
+    assert conv(flags=2) == ARG and conv(flags=0x80000000) == ARG
     assert conv(n=1 << 20, c=1 << 12, h=1, wd=1) == UNSUP
     assert conv(k=1 << 17, c=1 << 14, r=1, s=1, ph=0, pw=0) == UNSUP
     # y overlapping x
@@ -210,3 +210,33 @@ def test_converter_many_validation_codes():
     assert many(2, w, I2(2, 2), I2(6, 6), 15, out, 0, None) == ARG
     # two outputs on top of each other
     assert many(2, w, I2(2, 2), I2(6, 6), 14, P2(FAKE * 4, FAKE * 4), 0, None) in (ARG,)
+
+
+def test_fused_and_pool_validation_codes():
+    lib = _native.lib()
+    fused = lib.ds_conv2d_shift_fused
+
+    def fz(**kw):
+        a = dict(x=FAKE, w=FAKE + 4096, b=None, mul=FAKE + 6000, add=None, ms=16, res=None,
+                 y=FAKE + 8192, flags=0)
+        a.update(kw)
+        return fused(a["x"], a["w"], a["b"], a["mul"], a["add"], a["ms"], a["res"], a["y"],
+                     1, 2, 5, 5, 3, 3, 3, 1, 1, 1, 1, 16, a["flags"], None)
+    assert fz(x=None) == NULLP
+    assert fz(flags=2) == ARG
+    assert fz(mul=None, add=FAKE + 7000) == ARG
+    assert "add needs mul" in lib.ds_last_error_message().decode()
+    assert fz(ms=32) == ARG and fz(ms=-1) == ARG
+    assert fz(res=FAKE + 8192 + 8) == ARG          # residual overlapping y
+    assert "overlap" in lib.ds_last_error_message().decode()
+    mp = lib.ds_maxpool2d
+    assert mp(None, FAKE, 1, 1, 8, 8, 3, 3, 2, 2, 1, 1, 0, None) == NULLP
+    assert mp(FAKE, FAKE * 4, 0, 1, 8, 8, 3, 3, 2, 2, 1, 1, 0, None) == SHAPE
+    assert mp(FAKE, FAKE * 4, 1, 1, 8, 8, 3, 3, 2, 2, 2, 1, 0, None) == ARG   # pad > r/2
+    assert mp(FAKE, FAKE * 4, 1, 1, 8, 8, 3, 3, 0, 2, 1, 1, 0, None) == ARG   # stride 0
+    assert mp(FAKE, FAKE * 4, 1, 1, 8, 8, 3, 3, 2, 2, 1, 1, 1, None) == ARG   # flags
+    assert mp(FAKE, FAKE + 4, 1, 1, 8, 8, 3, 3, 2, 2, 1, 1, 0, None) == ARG   # overlap
+    ap = lib.ds_avgpool2d_global
+    assert ap(FAKE, None, 1, 1, 7, 7, 0, None) == NULLP
+    assert ap(FAKE, FAKE * 4, 1, 0, 7, 7, 0, None) == SHAPE
+    assert ap(FAKE, FAKE * 4, 1, 1, 7, 7, 4, None) == ARG
