@@ -75,6 +75,8 @@ def parse():
                     help="only run a device-to-device copy of BYTES (HBM counter calibration)")
     ap.add_argument("--pmc-summary", nargs=4, metavar=("COPY_FETCH", "COPY_WRITE", "FETCH", "WRITE"),
                     help="turn rocprofv3 --pmc CSV directories into the HBM traffic record")
+    ap.add_argument("--sq-summary", metavar="DIR",
+                    help="summarise a rocprofv3 --pmc run with SQ instruction counters per kernel")
     ap.add_argument("--pmc-copy-bytes", type=int, default=1 << 30)
     ap.add_argument("--pmc-out", default=TRAFFIC_FILE)
     return ap.parse_args()
@@ -97,7 +99,8 @@ def _pmc_rows(directory: str):
     (path,) = glob.glob(os.path.join(directory, "*counter_collection.csv"))
     rows = {}
     for r in csv.DictReader(open(path)):
-        e = rows.setdefault(int(r["Dispatch_Id"]), {"name": r["Kernel_Name"], "ctr": {}})
+        e = rows.setdefault(int(r["Dispatch_Id"]), {"name": r["Kernel_Name"], "ctr": {},
+                                                     "ns": int(r["End_Timestamp"]) - int(r["Start_Timestamp"])})
         e["ctr"][r["Counter_Name"]] = e["ctr"].get(r["Counter_Name"], 0.0) + float(r["Counter_Value"])
     return [rows[k] for k in sorted(rows)]
 
@@ -130,6 +133,47 @@ def pmc_summary(copy_fetch, copy_write, fetch, write, copy_bytes, workload, out)
     with open(out, "w") as f:
         json.dump(rec, f, indent=1)
     print(json.dumps(rec))
+
+
+def sq_summary(directory, workload):
+    """VALU evidence per kernel variant from one rocprofv3 --pmc run of the bench
+    (one timed step, no warm-up) with SQ_WAVES SQ_INSTS_VALU SQ_INSTS_SALU
+    SQ_INSTS_SMEM SQ_INSTS_LDS SQ_WAVE_CYCLES SQ_BUSY_CYCLES SQ_WAIT_INST_ANY and
+    GRBM_GUI_ACTIVE: VALU instructions per shift-accumulate, VALU issue rate per
+    SIMD per clock, and int32 lane-operations per second against the peak."""
+    from paper_1905_13298_amd import workloads as W
+    layers = W.config_layers(WORKLOADS[workload])
+    main = ("tiled_kernel", "conv_direct_kernel")
+    rows = [r for r in _pmc_rows(directory) if any(m in r["name"] for m in main)][-len(layers):]
+    per = {}
+    for L, r in zip(layers, rows):
+        name = kernel_variant(L).rsplit(" splits", 1)[0]
+        k = per.setdefault(name, {"launches": 0, "sac": 0, "ns": 0})
+        k["launches"] += 1
+        k["sac"] += L.sac
+        k["ns"] += r["ns"]
+        for c, v in r["ctr"].items():
+            k[c] = k.get(c, 0.0) + v
+    out = {}
+    for name, k in per.items():
+        clk = k["GRBM_GUI_ACTIVE"] / 8.0          # GPU clocks, summed over the 8 XCDs
+        valu = k["SQ_INSTS_VALU"]
+        out[name] = {
+            "launches": k["launches"], "ms": round(k["ns"] / 1e6, 3),
+            "tsac_s": round(k["sac"] / k["ns"] / 1e3, 3),
+            "clock_ghz": round(clk / k["ns"], 3),
+            "valu_insts_per_sac": round(valu * 64 / k["sac"], 3),
+            "valu_issue_per_simd_clk": round(valu / (CUS * 4) / clk, 4),
+            "int32_lane_ops_t": round(valu * 64 / k["ns"] / 1e3, 2),
+            "frac_of_int32_peak": round(valu * 64 / k["ns"] / 1e3 / INT32_OPS_PEAK_T, 4),
+            "salu_per_valu": round(k["SQ_INSTS_SALU"] / valu, 3),
+            "smem_per_valu": round(k["SQ_INSTS_SMEM"] / valu, 4),
+            "lds_per_valu": round(k["SQ_INSTS_LDS"] / valu, 4),
+            "wait_inst_any_per_wave_cycle": round(k["SQ_WAIT_INST_ANY"] / k["SQ_WAVE_CYCLES"], 3),
+        }
+    rec = {"workload": W.CONFIG_NAMES[WORKLOADS[workload]], "kernel_source_sha256_16": kernel_source_hash(),
+           "kernels": out}
+    print(json.dumps(rec, indent=1))
 
 
 def measured_traffic(kernel: str):
@@ -337,6 +381,9 @@ def main():
         return
     if args.pmc_summary:
         pmc_summary(*args.pmc_summary, args.pmc_copy_bytes, args.workload, args.pmc_out)
+        return
+    if args.sq_summary:
+        sq_summary(args.sq_summary, args.workload)
         return
     if args.gpus != 1:
         print(f"bench.py runs on one GPU only (asked for {args.gpus}); the shift operators need "

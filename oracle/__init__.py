@@ -244,3 +244,34 @@ def avgpool_global(x):
     y = np.empty((N, C), np.int32)
     _load().oracle_avgpool_global(_ptr(x), _ptr(y), N, C, HW)
     return y
+
+
+def network_forward(graph, params, x, mul_shift=16, keep=False):
+    """Runs a graph of ops (see ``workloads.resnet18_graph``) on x with the oracle:
+    conv -> ConvShift, then the epilogue with the layer's batch normalisation
+    (mul, add), the residual buffer and ReLU; maxpool; global avgpool; linear ->
+    LinearShift with bias. Returns the last op's output (all buffers if keep)."""
+    buf = {"x": np.ascontiguousarray(x, dtype=np.int32)}
+    out = None
+    for op in graph:
+        kind = op["op"]
+        src = buf[op["src"]]
+        if kind == "conv":
+            L = op["layer"]
+            p = params[L.name]
+            y = conv2d_shift(src, p["codes"], None, r=L.r, s=L.s, stride=L.stride, pad=L.pad)
+            mul, add = p["bn"]
+            res = buf[op["res"]] if op["res"] else None
+            out = epilogue(y, mul, add, mul_shift, residual=res, relu=op["relu"])
+        elif kind == "maxpool":
+            out = maxpool2d(src, r=op["r"], stride=op["stride"], pad=op["pad"])
+        elif kind == "avgpool":
+            out = avgpool_global(src)
+        elif kind == "linear":
+            L = op["layer"]
+            p = params[L.name]
+            out = linear_shift(src, p["codes"], p["bias"])
+        else:
+            raise ValueError(kind)
+        buf[op["dst"]] = out
+    return buf if keep else out
