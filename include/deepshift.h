@@ -58,6 +58,10 @@ extern "C" {
  * (ReLU fused into the operator, as Section 6 suggests). */
 #define DS_RELU 1u
 
+/* flags bit of ds_jit_conv_create: ds_jit_conv_run adds a residual tensor
+ * (shape of y) after the affine map and before ReLU. */
+#define DS_JIT_RESIDUAL 2u
+
 typedef enum ds_status {
     DS_SUCCESS = 0,
     DS_ERR_NULL_POINTER = 1,     /* a required pointer is NULL */
@@ -227,6 +231,65 @@ ds_status ds_linear_mul_i32(const int32_t *x, const int32_t *w, const int32_t *b
 ds_status ds_conv2d_shift_describe(int64_t n, int64_t c, int64_t h, int64_t w, int64_t k,
                                    int64_t r, int64_t s, int32_t stride_h, int32_t stride_w,
                                    int32_t pad_h, int32_t pad_w, char *buf, int64_t len);
+
+/* ---- Weight-specialised ConvShift (run-time code generation) --------------
+ *
+ * Section 6 of the paper proposes compiling the shift kernels for the weights
+ * at hand. A plan is such a kernel: made once for fixed weights and a fixed
+ * problem shape, it holds machine code in which every non-zero weight is one
+ * integer add or subtract of a register that holds x >> shift, and zero
+ * weights cost nothing. Run, it computes the same y as ds_conv2d_shift_fused
+ * with the same bias, affine map, residual and ReLU, bit for bit:
+ *     v = bias[k] + sum of term(x, code)                      (modulo 2^32)
+ *     v = floor(v * mul[k] / 2^mul_shift) + add[k]            (when mul)
+ *     v = v + residual[n][k][p]                               (DS_JIT_RESIDUAL)
+ *     v = max(v, 0)                                           (DS_RELU)
+ * Supported: kernels up to 3 x 3 (r, s <= 3), any stride and padding; a
+ * LinearShift is the case h = w = r = s = 1.
+ *
+ * ds_jit_conv_create: w_packed is HOST memory, [k][ds_packed_row_words(c*r*s)]
+ * words as for ds_conv2d_shift; bias, mul and add are HOST int32 [k] or NULL
+ * (add needs mul; mul_shift in [0, 31] when mul is given). The plan copies
+ * what it keeps; the caller's buffers may be freed on return. n, c, h, w and
+ * the window fix the shape of every ds_jit_conv_run of the plan. splits: 0
+ * chooses the split of the reduction over input channels (partial sums added
+ * atomically into y); a positive value forces that many parts (at most c).
+ * The plan's code is loaded on the current device with hipModuleLoadData and
+ * lives until ds_jit_conv_destroy. Errors: as ds_conv2d_shift_fused for
+ * arguments, DS_ERR_UNSUPPORTED for r or s > 3, DS_ERR_HIP when loading fails.
+ * Making a plan synchronises the device (module load, uploads).
+ *
+ * ds_jit_conv_run: x [n][c][h][w], residual and y [n][k][oh][ow], device
+ * memory on the plan's device; residual must be non-NULL exactly when the
+ * plan was made with DS_JIT_RESIDUAL. Asynchronous on `stream`. y must not
+ * overlap x or residual.
+ *
+ * ds_jit_conv_image: the code object ds_jit_conv_create would load, written
+ * to host memory `image` of `capacity` bytes (*size = bytes needed;
+ * DS_ERR_BUFFER_TOO_SMALL when capacity is short). Touches no device; for
+ * inspection and tests.
+ *
+ * ds_jit_conv_query: size of the generated code in bytes, number of code
+ * segments (64 output channels x one part of the input channels each), and
+ * the number of parts the reduction is split into. Any output may be NULL. */
+typedef struct ds_jit_conv ds_jit_conv;
+
+ds_status ds_jit_conv_create(const uint32_t *w_packed, const int32_t *bias, const int32_t *mul,
+                             const int32_t *add, int32_t mul_shift, int64_t n, int64_t c,
+                             int64_t h, int64_t w, int64_t k, int64_t r, int64_t s,
+                             int32_t stride_h, int32_t stride_w, int32_t pad_h, int32_t pad_w,
+                             uint32_t flags, int32_t splits, ds_jit_conv **plan);
+ds_status ds_jit_conv_run(const ds_jit_conv *plan, const int32_t *x, const int32_t *residual,
+                          int32_t *y, void *stream);
+ds_status ds_jit_conv_destroy(ds_jit_conv *plan);
+ds_status ds_jit_conv_image(const uint32_t *w_packed, const int32_t *bias, const int32_t *mul,
+                            const int32_t *add, int32_t mul_shift, int64_t n, int64_t c,
+                            int64_t h, int64_t w, int64_t k, int64_t r, int64_t s,
+                            int32_t stride_h, int32_t stride_w, int32_t pad_h, int32_t pad_w,
+                            uint32_t flags, int32_t splits, void *image, int64_t capacity,
+                            int64_t *size);
+ds_status ds_jit_conv_query(const ds_jit_conv *plan, int64_t *code_bytes, int32_t *segments,
+                            int32_t *splits);
 
 /* Static text for a status code. */
 const char *ds_status_string(ds_status status);

@@ -36,6 +36,11 @@ SIGNATURES = {
     "ds_conv2d_shift_fused": (ctypes.c_int, [_P, _P, _P, _P, _P, _I32, _P, _P] + [_I64] * 7 + [_I32] * 4 + [_I32, _U32, _P]),
     "ds_maxpool2d": (ctypes.c_int, [_P, _P] + [_I64] * 6 + [_I32] * 4 + [_U32, _P]),
     "ds_avgpool2d_global": (ctypes.c_int, [_P, _P] + [_I64] * 4 + [_U32, _P]),
+    "ds_jit_conv_create": (ctypes.c_int, [_P, _P, _P, _P, _I32] + [_I64] * 7 + [_I32] * 4 + [_U32, _I32, _P]),
+    "ds_jit_conv_run": (ctypes.c_int, [_P, _P, _P, _P, _P]),
+    "ds_jit_conv_destroy": (ctypes.c_int, [_P]),
+    "ds_jit_conv_image": (ctypes.c_int, [_P, _P, _P, _P, _I32] + [_I64] * 7 + [_I32] * 4 + [_U32, _I32, _P, _I64, _P]),
+    "ds_jit_conv_query": (ctypes.c_int, [_P, _P, _P, _P]),
     "ds_status_string": (ctypes.c_char_p, [ctypes.c_int]),
     "ds_last_error_message": (ctypes.c_char_p, []),
 }

@@ -24,8 +24,29 @@ HIP_FLAGS = ["-O3", "-std=c++17", f"--offload-arch={ARCH}", "-fPIC", "-Wall",
              "-I", INCLUDE, "-I", CSRC]
 CXX_FLAGS = ["-O2", "-std=c++17", "-fPIC", "-Wall", "-Wextra", "-I", INCLUDE, "-I", CSRC]
 
-HIP_SOURCES = ["shift_ops.hip", "conv_kernels.hip", "convert.hip", "pool.hip"]
+HIP_SOURCES = ["shift_ops.hip", "conv_kernels.hip", "convert.hip", "pool.hip", "jit.hip"]
 CXX_SOURCES = ["pack.cpp"]
+LLVM = "/opt/rocm/llvm/bin"
+
+# The weight-specialised kernel template (jit_template.hip) is compiled to
+# gfx950 assembly; its JITBODY marker becomes a jump through a table at the
+# start of section .jitbody, indexed by the segment number in s19 (stubs of 20
+# bytes each). The table and the segments' code are generated at run time.
+JIT_JUMP = """s_getpc_b64 s[28:29]
+	s_add_u32 s28, s28, ds_jit_body@rel32@lo+4
+	s_addc_u32 s29, s29, ds_jit_body@rel32@hi+12
+	s_mul_i32 s30, s19, 20
+	s_add_u32 s28, s28, s30
+	s_addc_u32 s29, s29, 0
+	s_setpc_b64 s[28:29]"""
+JIT_BODY_SECTION = """
+	.section .jitbody,"ax",@progbits
+	.p2align 8
+	.hidden ds_jit_body
+	.globl ds_jit_body
+ds_jit_body:
+	.fill 64, 4, 0xbf810000
+"""
 
 
 def _compile(src: str) -> str:
@@ -41,12 +62,57 @@ def _compile(src: str) -> str:
     return obj
 
 
+def _run(cmd):
+    res = subprocess.run(cmd, capture_output=True, text=True)
+    if res.returncode != 0:
+        raise RuntimeError(f"failed: {' '.join(cmd)}\n{res.stdout}\n{res.stderr}")
+
+
+def _jit_template() -> str:
+    """Build the template code object and an x86 object that embeds it
+    (symbols ds_jit_template_image / ds_jit_template_image_end)."""
+    src = os.path.join(CSRC, "jit_template.hip")
+    asm = os.path.join(OBJDIR, "jit_template.s")
+    _run([HIPCC, *HIP_FLAGS, "--cuda-device-only", "-S", src, "-o", asm])
+    text = open(asm).read()
+    marker = "; JITBODY"
+    if text.count(marker) != 1:
+        raise RuntimeError("jit_template.s: expected one JITBODY marker")
+    text = text.replace(marker, JIT_JUMP) + JIT_BODY_SECTION
+    spliced = os.path.join(OBJDIR, "jit_template_spliced.s")
+    with open(spliced, "w") as f:
+        f.write(text)
+    obj = os.path.join(OBJDIR, "jit_template_dev.o")
+    hsaco = os.path.join(OBJDIR, "jit_template.hsaco")
+    _run([os.path.join(LLVM, "clang"), "-target", "amdgcn-amd-amdhsa", f"-mcpu={ARCH}",
+          "-c", spliced, "-o", obj])
+    _run([os.path.join(LLVM, "ld.lld"), "-shared", obj, "-T",
+          os.path.join(CSRC, "jit_template.ld"), "-o", hsaco])
+    embed = os.path.join(OBJDIR, "jit_image.S")
+    with open(embed, "w") as f:
+        f.write(f"""\t.section .rodata
+\t.balign 64
+\t.globl ds_jit_template_image
+\t.hidden ds_jit_template_image
+ds_jit_template_image:
+\t.incbin "{hsaco}"
+\t.globl ds_jit_template_image_end
+\t.hidden ds_jit_template_image_end
+ds_jit_template_image_end:
+\t.section .note.GNU-stack,"",@progbits
+""")
+    out = os.path.join(OBJDIR, "jit_image.o")
+    _run(["gcc", "-c", embed, "-o", out])
+    return out
+
+
 def build(verbose: bool = False) -> str:
     """Compile every source and link the library; returns its path."""
     os.makedirs(OBJDIR, exist_ok=True)
     srcs = HIP_SOURCES + CXX_SOURCES
-    with ThreadPoolExecutor(len(srcs)) as ex:
-        objs = list(ex.map(_compile, srcs))
+    with ThreadPoolExecutor(len(srcs) + 1) as ex:
+        jit = ex.submit(_jit_template)
+        objs = list(ex.map(_compile, srcs)) + [jit.result()]
     tmp = LIB + f".tmp{os.getpid()}"
     cmd = [HIPCC, "-shared", "-fPIC", f"--offload-arch={ARCH}", "-o", tmp, *objs]
     res = subprocess.run(cmd, capture_output=True, text=True)
@@ -59,7 +125,7 @@ def build(verbose: bool = False) -> str:
 
 
 def sources() -> list:
-    return [os.path.join(CSRC, s) for s in HIP_SOURCES + CXX_SOURCES] + \
+    return [os.path.join(CSRC, s) for s in HIP_SOURCES + CXX_SOURCES + ["jit_template.hip", "jit_template.ld"]] + \
         [os.path.join(CSRC, f) for f in os.listdir(CSRC) if f.endswith((".hpp", ".h"))] + \
         [os.path.join(INCLUDE, "deepshift.h")]
 

@@ -749,7 +749,16 @@ void describe_conv(const ConvGeom &g0, char *buf, size_t len)
 }
 
 // The epilogue as its own pass over y (see epilogue_kernel).
-static hipError_t run_epilogue(const ConvGeom &g, int32_t *y, const Epilogue &epi, hipStream_t st)
+hipError_t run_fill_init(const ConvGeom &g, const int32_t *init, int32_t *y, hipStream_t st)
+{
+    const int64_t total = int64_t(g.n) * g.k * g.oh * g.ow;
+    const int grid = int(std::min<int64_t>((total + 255) / 256, 8192));
+    hipLaunchKernelGGL(fill_init_kernel, dim3(grid), dim3(256), 0, st, init, y, total, g.k,
+                       g.oh * g.ow);
+    return hipGetLastError();
+}
+
+hipError_t run_epilogue(const ConvGeom &g, int32_t *y, const Epilogue &epi, hipStream_t st)
 {
     const int64_t total = int64_t(g.n) * g.k * g.oh * g.ow;
     const int grid = int(std::min<int64_t>((total + 255) / 256, 8192));

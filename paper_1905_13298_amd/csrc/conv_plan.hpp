@@ -37,6 +37,11 @@ hipError_t run_conv(const ConvGeom &g, const int32_t *x, const uint32_t *wpacked
                     const int32_t *wint, const int32_t *bias, int32_t *y, Inner op,
                     hipStream_t stream, const Epilogue &epi = Epilogue());
 
+// y[n][k][p] = init[k] (the start of split-K accumulation), and the epilogue as
+// a pass of its own over y, both enqueued on `stream`.
+hipError_t run_fill_init(const ConvGeom &g, const int32_t *init, int32_t *y, hipStream_t stream);
+hipError_t run_epilogue(const ConvGeom &g, int32_t *y, const Epilogue &epi, hipStream_t stream);
+
 // Short name of the kernel run_conv would launch for g (see ds_conv2d_shift_describe).
 void describe_conv(const ConvGeom &g, char *buf, size_t len);
 

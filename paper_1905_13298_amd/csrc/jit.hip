@@ -1,0 +1,595 @@
+// Weight-specialised ConvShift kernels (the run-time compilation the paper
+// suggests in Section 6): code generation, code object assembly and launch.
+//
+// With the weight codes known when the plan is made, the inner loop needs no
+// weight loads, no decode and no work for zero weights. For each reduction
+// element (input channel c, tap (r, s)) a lane loads its input x, forms the
+// right shifts x >> s that the 64 output channels of the segment use at that
+// element, and adds or subtracts each one into its channel's accumulator: one
+// v_add_u32 / v_sub_u32 per non-zero weight, with the register of the shift
+// and the sign fixed in the instruction. The term of a weight with sign bit set
+// is -(x >> shift) (Eq. 1 with the sign applied after the shift), so the
+// results equal those of ds_conv2d_shift bit for bit.
+//
+// Code layout. A plan is one code object: the template kernel built with the
+// library (jit_template.hip), whose last loadable segment `.jitbody` is
+// replaced by the generated code: a table of `nseg` jump stubs, then one block
+// of straight-line code per segment (64 output channels x a range of input
+// channels). The template computes the lane's tap and output offsets and jumps
+// through the table; each segment ends the wave. Segments are spliced into
+// the template image in memory (no assembler or linker runs at plan time) and
+// the result is loaded with hipModuleLoadData.
+#include <hip/hip_runtime.h>
+
+#include <elf.h>
+
+#include <algorithm>
+#include <cstdlib>
+#include <cstring>
+#include <new>
+#include <vector>
+
+#include "common.hpp"
+#include "conv_plan.hpp"
+#include "jit.hpp"
+
+// The template code object, embedded by the build (see build.py).
+extern "C" const unsigned char ds_jit_template_image[];
+extern "C" const unsigned char ds_jit_template_image_end[];
+
+namespace ds {
+namespace {
+
+// Register contract with the template (see the JITBODY marker there).
+constexpr int kTap0 = 4;     // v4..v12: byte offset in x of tap (r, s) = v[4 + 3r + s], channel 0
+constexpr int kYoff = 13;    // v13: byte offset in y of the lane's output pixel, channel 0
+constexpr int kTmpLo = 14, kTmpHi = 15;
+constexpr int kTab = 16;     // v[16 + s] = x >> s for s = 1..14 (x itself stays in its load slot)
+constexpr int kAcc = 32;     // v32..v95: accumulators of the segment's 64 output channels
+constexpr int kSlot = 96;    // v96..v103: loads in flight
+constexpr int kSlots = 8;
+constexpr int kXrsrc = 20, kYrsrc = 24, kRrsrc = 36;  // buffer resources (SGPR quads)
+constexpr int kSy = 28, kSx = 29, kSmul = 30;         // scalar scratch of the generated code
+constexpr int kTN = 64;      // output channels per segment
+constexpr int kBlockPixels = 256;
+constexpr int kStubWords = 5;
+constexpr int kMaxTaps = 3;  // R, S <= 3: the template computes a 3 x 3 window of taps
+
+// gfx950 instruction encodings used by the generator (VOP2, VOP1, VOP3, MUBUF,
+// SOP1/SOP2/SOPP words; see the CDNA ISA reference).
+constexpr uint32_t kOpAshr = 0x11, kOpMax = 0x0d, kOpAdd = 0x34, kOpSub = 0x35;  // VOP2
+constexpr uint32_t kOpMulLo = 0x285, kOpMulHi = 0x287, kOpAlignbit = 0x1ce;     // VOP3
+constexpr uint32_t kLoad = 0xe0501000u, kStore = 0xe0701000u, kAtomicAdd = 0xe1081000u;
+constexpr uint32_t kEndpgm = 0xbf810000u, kNop = 0xbf800000u;
+constexpr uint32_t kLiteral = 255;
+
+class Emitter {
+public:
+    std::vector<uint32_t> w;
+
+    static uint32_t vgpr(int r) { return 256u + uint32_t(r); }
+    static bool is_inline(int32_t v) { return v >= -16 && v <= 64; }
+    static uint32_t inline_int(int32_t v) { return v >= 0 ? 128u + uint32_t(v) : 192u + uint32_t(-v); }
+
+    void vop2(uint32_t op, int vdst, uint32_t src0, int vsrc1)
+    {
+        w.push_back((op << 25) | (uint32_t(vdst) << 17) | (uint32_t(vsrc1) << 9) | src0);
+    }
+    // vdst = op(imm, vsrc1), the constant inline when it fits, else a literal word.
+    void vop2_imm(uint32_t op, int vdst, int32_t imm, int vsrc1)
+    {
+        if (is_inline(imm)) {
+            vop2(op, vdst, inline_int(imm), vsrc1);
+        } else {
+            vop2(op, vdst, kLiteral, vsrc1);
+            w.push_back(uint32_t(imm));
+        }
+    }
+    void mov_imm(int vdst, int32_t imm)
+    {
+        const uint32_t base = 0x7e000200u | (uint32_t(vdst) << 17);  // v_mov_b32
+        if (is_inline(imm)) {
+            w.push_back(base | inline_int(imm));
+        } else {
+            w.push_back(base | kLiteral);
+            w.push_back(uint32_t(imm));
+        }
+    }
+    void vop3(uint32_t op, int vdst, uint32_t s0, uint32_t s1, uint32_t s2)
+    {
+        w.push_back(0xd0000000u | (op << 16) | uint32_t(vdst));
+        w.push_back(s0 | (s1 << 9) | (s2 << 18));
+    }
+    void wait_vm(int n)  // s_waitcnt vmcnt(n), other counters not waited on
+    {
+        w.push_back(0xbf8c0f70u | uint32_t(n & 15) | (uint32_t(n >> 4) << 14));
+    }
+    void mubuf(uint32_t word0, int vdata, int vaddr, int srsrc, int soff)
+    {
+        w.push_back(word0);
+        w.push_back((uint32_t(soff) << 24) | (uint32_t(srsrc / 4) << 16) |
+                    (uint32_t(vdata) << 8) | uint32_t(vaddr));
+    }
+    void s_mov_imm(int sdst, uint32_t imm)
+    {
+        w.push_back(0xbe8000ffu | (uint32_t(sdst) << 16));
+        w.push_back(imm);
+    }
+    void s_add_imm(int sdst, uint32_t imm)  // s_add_u32 sdst, sdst, imm
+    {
+        w.push_back(0x8000ff00u | (uint32_t(sdst) << 16) | uint32_t(sdst));
+        w.push_back(imm);
+    }
+};
+
+struct Spec {
+    ConvGeom g;
+    const uint32_t *wp;  // host packed codes [k][row_words(crs)]
+    int64_t rw;
+    const int32_t *bias, *mul, *add;
+    int mul_shift;
+    bool relu, residual;
+    int nsplit, kgroups, nseg, tiles_p;
+};
+
+inline int code_at(const Spec &sp, int k, int j)
+{
+    return int((sp.wp[int64_t(k) * sp.rw + j / 6] >> (5 * (j % 6))) & 31u);
+}
+
+// Straight-line code of segment (kg, part): output channels [64 kg, 64 kg + 64)
+// and input channels [c0, c1), all taps. `split` = the partial sums of several
+// segments meet in y through atomic adds (y holds the bias beforehand and the
+// epilogue runs afterwards, as separate passes).
+void emit_segment(Emitter &e, const Spec &sp, int kg, int c0, int c1, bool split)
+{
+    const ConvGeom &g = sp.g;
+    const int kbase = kg * kTN, jn = std::min(kTN, g.k - kbase);
+    const int RS = g.r * g.s, E = (c1 - c0) * RS;
+    const uint32_t cstride = uint32_t(g.h) * uint32_t(g.w) * 4u;
+    const uint32_t kstride = uint32_t(g.oh) * uint32_t(g.ow) * 4u;
+
+    for (int j = 0; j < jn; ++j)
+        e.mov_imm(kAcc + j, (!split && sp.bias) ? sp.bias[kbase + j] : 0);
+
+    // Element i = (c0 + i / RS, tap i % RS); its load goes to slot i % kSlots and
+    // reads x at v[tap] + s29, where s29 = c * H * W * 4 for the channel of the
+    // most recently issued load.
+    const int D = std::min(kSlots, E);
+    int cur_c = c0;
+    e.s_mov_imm(kSx, uint32_t(c0) * cstride);
+    auto issue = [&](int i) {
+        const int c = c0 + i / RS, t = i % RS;
+        if (c != cur_c) {
+            e.s_add_imm(kSx, uint32_t(c - cur_c) * cstride);
+            cur_c = c;
+        }
+        const int tap = kTap0 + (t / g.s) * 3 + (t % g.s);
+        e.mubuf(kLoad, kSlot + i % kSlots, tap, kXrsrc, kSx);
+    };
+    for (int i = 0; i < D; ++i) issue(i);
+
+    for (int i = 0; i < E; ++i) {
+        const int issued = std::min(E, i + D);
+        e.wait_vm(issued - i - 1);
+        const int slot = kSlot + i % kSlots;
+        const int jw = (c0 + i / RS) * RS + i % RS;
+        uint32_t need = 0;
+        for (int j = 0; j < jn; ++j) {
+            const int sh = code_at(sp, kbase + j, jw) & 15;
+            if (sh != 15 && sh != 0) need |= 1u << sh;
+        }
+        for (int s = 1; s <= 14; ++s)
+            if (need >> s & 1u) e.vop2(kOpAshr, kTab + s, Emitter::inline_int(s), slot);
+        for (int j = 0; j < jn; ++j) {
+            const int code = code_at(sp, kbase + j, jw);
+            const int sh = code & 15;
+            if (sh == 15) continue;
+            const int src = sh == 0 ? slot : kTab + sh;
+            if (code & 16)
+                e.vop2(kOpSub, kAcc + j, Emitter::vgpr(kAcc + j), src);  // acc - term
+            else
+                e.vop2(kOpAdd, kAcc + j, Emitter::vgpr(src), kAcc + j);  // term + acc
+        }
+        if (i + D < E) issue(i + D);
+    }
+
+    if (!split) {
+        if (sp.mul) {
+            for (int j = 0; j < jn; ++j) {
+                // floor(acc * mul / 2^mul_shift): the low word of the 64-bit product
+                // shifted right, taken from its two halves.
+                e.s_mov_imm(kSmul, uint32_t(sp.mul[kbase + j]));
+                e.vop3(kOpMulLo, kTmpLo, uint32_t(kSmul), Emitter::vgpr(kAcc + j), 0);
+                e.vop3(kOpMulHi, kTmpHi, uint32_t(kSmul), Emitter::vgpr(kAcc + j), 0);
+                e.vop3(kOpAlignbit, kAcc + j, Emitter::vgpr(kTmpHi), Emitter::vgpr(kTmpLo),
+                       Emitter::inline_int(sp.mul_shift));
+                const int32_t a = sp.add ? sp.add[kbase + j] : 0;
+                if (a != 0) e.vop2_imm(kOpAdd, kAcc + j, a, kAcc + j);
+            }
+        }
+        if (sp.residual) {
+            for (int j0 = 0; j0 < jn; j0 += kSlots) {
+                const int nb = std::min(kSlots, jn - j0);
+                e.s_mov_imm(kSy, uint32_t(kbase + j0) * kstride);
+                for (int b = 0; b < nb; ++b) {
+                    e.mubuf(kLoad, kSlot + b, kYoff, kRrsrc, kSy);
+                    if (b + 1 < nb) e.s_add_imm(kSy, kstride);
+                }
+                e.wait_vm(0);
+                for (int b = 0; b < nb; ++b)
+                    e.vop2(kOpAdd, kAcc + j0 + b, Emitter::vgpr(kSlot + b), kAcc + j0 + b);
+            }
+        }
+        if (sp.relu)
+            for (int j = 0; j < jn; ++j) e.vop2(kOpMax, kAcc + j, Emitter::inline_int(0), kAcc + j);
+    }
+    e.s_mov_imm(kSy, uint32_t(kbase) * kstride);
+    for (int j = 0; j < jn; ++j) {
+        e.mubuf(split ? kAtomicAdd : kStore, kAcc + j, kYoff, kYrsrc, kSy);
+        if (j + 1 < jn) e.s_add_imm(kSy, kstride);
+    }
+    e.w.push_back(kEndpgm);
+}
+
+// Body of `.jitbody`: the jump stubs, then the segments (each 64-byte aligned),
+// then a tail of s_endpgm words so that instruction prefetch past the last
+// segment stays inside the loaded image.
+std::vector<uint32_t> generate_body(const Spec &sp)
+{
+    Emitter e;
+    e.w.resize(size_t(sp.nseg) * kStubWords, kNop);
+    std::vector<size_t> start(sp.nseg);
+    int seg = 0;
+    for (int kg = 0; kg < sp.kgroups; ++kg) {
+        for (int part = 0; part < sp.nsplit; ++part, ++seg) {
+            while (e.w.size() % 16) e.w.push_back(kNop);
+            start[seg] = e.w.size();
+            const int c0 = int(int64_t(part) * sp.g.c / sp.nsplit);
+            const int c1 = int(int64_t(part + 1) * sp.g.c / sp.nsplit);
+            emit_segment(e, sp, kg, c0, c1, sp.nsplit > 1);
+        }
+    }
+    for (int i = 0; i < 64; ++i) e.w.push_back(kEndpgm);
+    for (int s = 0; s < sp.nseg; ++s) {
+        // s_getpc_b64 s[28:29] (= address of the next word); s_add_u32 s28, s28,
+        // delta; s_addc_u32 s29, s29, 0; s_setpc_b64 s[28:29]
+        uint32_t *stub = &e.w[size_t(s) * kStubWords];
+        const uint64_t delta = (start[s] - (size_t(s) * kStubWords + 1)) * 4;
+        stub[0] = 0xbe9c1c00u;
+        stub[1] = 0x801cff1cu;
+        stub[2] = uint32_t(delta);
+        stub[3] = 0x821d801du;
+        stub[4] = 0xbe801d1cu;
+    }
+    return e.w;
+}
+
+// The template image with `.jitbody` replaced by `body`: the body is appended
+// at the end of the file, and the section header and the program header of the
+// last loadable segment (which holds `.jitbody` alone) are pointed at it.
+ds_status splice_body(const std::vector<uint32_t> &body, std::vector<uint8_t> &out)
+{
+    const size_t n = size_t(ds_jit_template_image_end - ds_jit_template_image);
+    out.assign(ds_jit_template_image, ds_jit_template_image + n);
+    Elf64_Ehdr eh;
+    if (n < sizeof eh) return fail(DS_ERR_HIP, "template code object missing");
+    std::memcpy(&eh, out.data(), sizeof eh);
+    if (std::memcmp(eh.e_ident, ELFMAG, SELFMAG) != 0 || eh.e_ident[EI_CLASS] != ELFCLASS64 ||
+        eh.e_shentsize != sizeof(Elf64_Shdr) || eh.e_phentsize != sizeof(Elf64_Phdr) ||
+        eh.e_shoff + uint64_t(eh.e_shnum) * sizeof(Elf64_Shdr) > n ||
+        eh.e_phoff + uint64_t(eh.e_phnum) * sizeof(Elf64_Phdr) > n || eh.e_shstrndx >= eh.e_shnum)
+        return fail(DS_ERR_HIP, "template code object malformed");
+    auto shdr = [&](int i) {
+        Elf64_Shdr s;
+        std::memcpy(&s, out.data() + eh.e_shoff + size_t(i) * sizeof s, sizeof s);
+        return s;
+    };
+    auto phdr = [&](int i) {
+        Elf64_Phdr p;
+        std::memcpy(&p, out.data() + eh.e_phoff + size_t(i) * sizeof p, sizeof p);
+        return p;
+    };
+    const Elf64_Shdr strtab = shdr(eh.e_shstrndx);
+    int js = -1;
+    for (int i = 0; i < eh.e_shnum; ++i) {
+        const Elf64_Shdr s = shdr(i);
+        if (strtab.sh_offset + s.sh_name + 9 <= n &&
+            std::memcmp(out.data() + strtab.sh_offset + s.sh_name, ".jitbody", 9) == 0)
+            js = i;
+    }
+    if (js < 0) return fail(DS_ERR_HIP, "template code object has no .jitbody section");
+    Elf64_Shdr sec = shdr(js);
+    int jp = -1;
+    uint64_t top = 0;
+    for (int i = 0; i < eh.e_phnum; ++i) {
+        const Elf64_Phdr p = phdr(i);
+        if (p.p_type != PT_LOAD) continue;
+        if (p.p_vaddr == sec.sh_addr) jp = i;
+        top = std::max(top, p.p_vaddr);
+    }
+    if (jp < 0 || phdr(jp).p_vaddr != top || phdr(jp).p_filesz != sec.sh_size)
+        return fail(DS_ERR_HIP, ".jitbody is not alone in the last loadable segment");
+    Elf64_Phdr seg = phdr(jp);
+    const uint64_t align = std::max<uint64_t>(seg.p_align, 256);
+    const uint64_t off = (out.size() + align - 1) / align * align + seg.p_vaddr % align;
+    const uint64_t bytes = uint64_t(body.size()) * 4;
+    out.resize(off + bytes);
+    std::memcpy(out.data() + off, body.data(), bytes);
+    seg.p_offset = off;
+    seg.p_filesz = seg.p_memsz = bytes;
+    sec.sh_offset = off;
+    sec.sh_size = bytes;
+    std::memcpy(out.data() + eh.e_phoff + size_t(jp) * sizeof seg, &seg, sizeof seg);
+    std::memcpy(out.data() + eh.e_shoff + size_t(js) * sizeof sec, &sec, sizeof sec);
+    return ok();
+}
+
+int env_int(const char *name, int dflt)
+{
+    const char *v = std::getenv(name);
+    return v && *v ? std::atoi(v) : dflt;
+}
+
+struct CreateArgs {
+    const uint32_t *wp;
+    const int32_t *bias, *mul, *add;
+    int mul_shift;
+    int64_t n, c, h, w, k, r, s;
+    int sh, sw, ph, pw;
+    uint32_t flags;
+    int splits;
+};
+
+// Validation and planning shared by ds_jit_conv_create and ds_jit_conv_image.
+ds_status plan_spec(const CreateArgs &a, Spec &sp)
+{
+    if (!a.wp) return fail(DS_ERR_NULL_POINTER, "w_packed must not be NULL");
+    if (a.n <= 0 || a.c <= 0 || a.h <= 0 || a.w <= 0 || a.k <= 0 || a.r <= 0 || a.s <= 0)
+        return fail(DS_ERR_INVALID_SHAPE, "all sizes must be > 0");
+    if (a.sh < 1 || a.sw < 1 || a.ph < 0 || a.pw < 0)
+        return fail(DS_ERR_INVALID_ARG, "stride must be >= 1 and padding >= 0");
+    if (a.flags & ~(DS_RELU | DS_JIT_RESIDUAL)) return fail(DS_ERR_INVALID_ARG, "unknown flags");
+    if (a.add && !a.mul) return fail(DS_ERR_INVALID_ARG, "add needs mul");
+    if (a.mul && (a.mul_shift < 0 || a.mul_shift > 31))
+        return fail(DS_ERR_INVALID_ARG, "mul_shift must be in [0, 31]");
+    if (a.splits < 0) return fail(DS_ERR_INVALID_ARG, "splits must be >= 0");
+    if (a.r > kMaxTaps || a.s > kMaxTaps)
+        return fail(DS_ERR_UNSUPPORTED, "kernels larger than 3 x 3 are not supported");
+    const int64_t oh = a.h + 2 * int64_t(a.ph) - a.r, ow = a.w + 2 * int64_t(a.pw) - a.s;
+    if (oh < 0 || ow < 0) return fail(DS_ERR_INVALID_SHAPE, "kernel larger than the padded input");
+    ConvGeom &g = sp.g;
+    g.oh = int(oh / a.sh + 1);
+    g.ow = int(ow / a.sw + 1);
+    const int64_t xe = prod({a.n, a.c, a.h, a.w}), ye = prod({a.n, a.k, int64_t(g.oh), int64_t(g.ow)});
+    const int64_t crs = prod({a.c, a.r, a.s});
+    if (xe < 0 || ye < 0 || xe > kMaxElems || ye > kMaxElems || crs > kMaxElems ||
+        a.h + 2 * int64_t(a.ph) > kMaxElems || a.w + 2 * int64_t(a.pw) > kMaxElems)
+        return fail(DS_ERR_UNSUPPORTED, "tensors with 2^31 or more elements are not supported");
+    g.n = int(a.n); g.c = int(a.c); g.h = int(a.h); g.w = int(a.w); g.k = int(a.k);
+    g.r = int(a.r); g.s = int(a.s); g.sh = a.sh; g.sw = a.sw; g.ph = a.ph; g.pw = a.pw;
+    g.crs = int(crs);
+    sp.wp = a.wp;
+    sp.rw = row_words(crs);
+    for (int64_t i = 0; i < a.k * sp.rw; ++i)
+        if (a.wp[i] >> 30) return fail(DS_ERR_INVALID_CODE, "bits 30-31 of packed word %lld are not 0", (long long)i);
+    sp.bias = a.bias; sp.mul = a.mul; sp.add = a.add; sp.mul_shift = a.mul ? a.mul_shift : 0;
+    sp.relu = a.flags & DS_RELU;
+    sp.residual = a.flags & DS_JIT_RESIDUAL;
+    const int64_t nq = int64_t(g.n) * g.oh * g.ow;
+    sp.tiles_p = int((nq + kBlockPixels - 1) / kBlockPixels);
+    sp.kgroups = (g.k + kTN - 1) / kTN;
+    // Enough blocks to keep every compute unit busy through the tail (about 8 per
+    // CU); each part keeps at least 64 reduction elements.
+    int ns = a.splits;
+    if (ns == 0) {
+        const int64_t base = int64_t(sp.tiles_p) * sp.kgroups;
+        const int64_t want = (2048 + base - 1) / base;
+        const int64_t cap = std::max<int64_t>(1, crs / 64);
+        ns = int(std::max<int64_t>(1, std::min(want, cap)));
+    }
+    sp.nsplit = std::min(ns, g.c);
+    const int64_t nseg = int64_t(sp.kgroups) * sp.nsplit;
+    if (nseg * sp.tiles_p > INT32_MAX) return fail(DS_ERR_UNSUPPORTED, "grid too large");
+    sp.nseg = int(nseg);
+    return ok();
+}
+
+}  // namespace
+}  // namespace ds
+
+using namespace ds;
+
+struct ds_jit_conv {
+    int device = -1;
+    hipModule_t module = nullptr;
+    hipFunction_t fn = nullptr;
+    Spec sp;
+    int group_tiles = 64;
+    int64_t code_bytes = 0;
+    int32_t *init = nullptr;        // [k] bias or zeros: y's start for split-K
+    int32_t *mul = nullptr, *add = nullptr;
+};
+
+static ds_status destroy_plan(ds_jit_conv *p)
+{
+    if (!p) return ok();
+    hipError_t e = hipSuccess;
+    if (p->module) e = hipModuleUnload(p->module);
+    for (int32_t *q : {p->init, p->mul, p->add})
+        if (q) {
+            const hipError_t f = hipFree(q);
+            if (e == hipSuccess) e = f;
+        }
+    delete p;
+    if (e != hipSuccess) return fail(DS_ERR_HIP, "ds_jit_conv_destroy: %s", hipGetErrorString(e));
+    return ok();
+}
+
+static ds_status upload(int32_t **dst, const int32_t *src, int k, bool zeros)
+{
+    if (hipMalloc(dst, size_t(k) * 4) != hipSuccess) return fail(DS_ERR_HIP, "hipMalloc failed");
+    hipError_t e = zeros ? hipMemset(*dst, 0, size_t(k) * 4)
+                         : hipMemcpy(*dst, src, size_t(k) * 4, hipMemcpyHostToDevice);
+    if (e != hipSuccess) return fail(DS_ERR_HIP, "upload: %s", hipGetErrorString(e));
+    return ok();
+}
+
+extern "C" ds_status ds_jit_conv_image(const uint32_t *w_packed, const int32_t *bias,
+                                       const int32_t *mul, const int32_t *add, int32_t mul_shift,
+                                       int64_t n, int64_t c, int64_t h, int64_t w, int64_t k,
+                                       int64_t r, int64_t s, int32_t stride_h, int32_t stride_w,
+                                       int32_t pad_h, int32_t pad_w, uint32_t flags,
+                                       int32_t splits, void *image, int64_t capacity,
+                                       int64_t *size)
+{
+    try {
+        if (!size) return fail(DS_ERR_NULL_POINTER, "size must not be NULL");
+        Spec sp;
+        const CreateArgs a{w_packed, bias, mul, add, mul_shift, n, c, h, w, k, r, s,
+                           stride_h, stride_w, pad_h, pad_w, flags, splits};
+        ds_status st = plan_spec(a, sp);
+        if (st != DS_SUCCESS) return st;
+        std::vector<uint8_t> img;
+        st = splice_body(generate_body(sp), img);
+        if (st != DS_SUCCESS) return st;
+        *size = int64_t(img.size());
+        if (!image || capacity < int64_t(img.size()))
+            return fail(DS_ERR_BUFFER_TOO_SMALL, "the code object needs %lld bytes", (long long)img.size());
+        std::memcpy(image, img.data(), img.size());
+        return ok();
+    } catch (const std::bad_alloc &) {
+        return fail(DS_ERR_HIP, "out of host memory");
+    }
+}
+
+extern "C" ds_status ds_jit_conv_create(const uint32_t *w_packed, const int32_t *bias,
+                                        const int32_t *mul, const int32_t *add, int32_t mul_shift,
+                                        int64_t n, int64_t c, int64_t h, int64_t w, int64_t k,
+                                        int64_t r, int64_t s, int32_t stride_h, int32_t stride_w,
+                                        int32_t pad_h, int32_t pad_w, uint32_t flags,
+                                        int32_t splits, ds_jit_conv **plan)
+{
+    if (!plan) return fail(DS_ERR_NULL_POINTER, "plan must not be NULL");
+    *plan = nullptr;
+    ds_jit_conv *p = nullptr;
+    try {
+        p = new ds_jit_conv;
+        const CreateArgs a{w_packed, bias, mul, add, mul_shift, n, c, h, w, k, r, s,
+                           stride_h, stride_w, pad_h, pad_w, flags, splits};
+        ds_status st = plan_spec(a, p->sp);
+        if (st != DS_SUCCESS) {
+            delete p;
+            return st;
+        }
+        std::vector<uint8_t> img;
+        const std::vector<uint32_t> body = generate_body(p->sp);
+        p->code_bytes = int64_t(body.size()) * 4;
+        st = splice_body(body, img);
+        if (st != DS_SUCCESS) {
+            delete p;
+            return st;
+        }
+        if (hipGetDevice(&p->device) != hipSuccess) {
+            delete p;
+            return fail(DS_ERR_HIP, "no HIP device");
+        }
+        hipError_t e = hipModuleLoadData(&p->module, img.data());
+        if (e == hipSuccess) e = hipModuleGetFunction(&p->fn, p->module, "ds_jit_conv_template");
+        if (e != hipSuccess) {
+            destroy_plan(p);
+            return fail(DS_ERR_HIP, "loading the generated code: %s", hipGetErrorString(e));
+        }
+        const int K = p->sp.g.k;
+        // The bias, mul and add pointers are host memory and not kept: what the
+        // separate split-K passes need is copied to the device here.
+        if (p->sp.nsplit > 1) {
+            st = upload(&p->init, bias, K, !bias);
+            if (st == DS_SUCCESS && mul) st = upload(&p->mul, mul, K, false);
+            if (st == DS_SUCCESS && add) st = upload(&p->add, add, K, false);
+            if (st != DS_SUCCESS) {
+                const std::string msg = last_error();
+                destroy_plan(p);
+                return fail(st, "%s", msg.c_str());
+            }
+        }
+        p->sp.bias = p->sp.mul = p->sp.add = nullptr;
+        p->sp.wp = nullptr;
+        p->group_tiles = std::max(1, env_int("DS_JIT_GROUP_TILES", 64));
+        *plan = p;
+        return ok();
+    } catch (const std::bad_alloc &) {
+        if (p) destroy_plan(p);
+        return fail(DS_ERR_HIP, "out of host memory");
+    }
+}
+
+extern "C" ds_status ds_jit_conv_run(const ds_jit_conv *plan, const int32_t *x,
+                                     const int32_t *residual, int32_t *y, void *stream)
+{
+    if (!plan || !x || !y) return fail(DS_ERR_NULL_POINTER, "plan, x and y must not be NULL");
+    const Spec &sp = plan->sp;
+    const ConvGeom &g = sp.g;
+    if (sp.residual != (residual != nullptr))
+        return fail(DS_ERR_INVALID_ARG, sp.residual ? "the plan adds a residual: residual must not be NULL"
+                                                    : "the plan adds no residual: residual must be NULL");
+    int dev = -1;
+    if (hipGetDevice(&dev) != hipSuccess || dev != plan->device)
+        return fail(DS_ERR_INVALID_ARG, "the plan was made on device %d, the current device is %d", plan->device, dev);
+    const int64_t xb = int64_t(g.n) * g.c * g.h * g.w * 4;
+    const int64_t yb = int64_t(g.n) * g.k * g.oh * g.ow * 4;
+    if (overlap(x, xb, y, yb)) return fail(DS_ERR_INVALID_ARG, "y overlaps x");
+    if (residual && overlap(residual, yb, y, yb)) return fail(DS_ERR_INVALID_ARG, "y overlaps residual");
+    if (!device_range_ok(x, xb)) return fail(DS_ERR_INVALID_ARG, "x is not a device buffer of %lld bytes", (long long)xb);
+    if (!device_range_ok(y, yb)) return fail(DS_ERR_INVALID_ARG, "y is not a device buffer of %lld bytes", (long long)yb);
+    if (residual && !device_range_ok(residual, yb))
+        return fail(DS_ERR_INVALID_ARG, "residual is not a device buffer of %lld bytes", (long long)yb);
+
+    hipStream_t st = static_cast<hipStream_t>(stream);
+    const bool split = sp.nsplit > 1;
+    hipError_t e = hipSuccess;
+    if (split) e = run_fill_init(g, plan->init, y, st);
+    if (e == hipSuccess) {
+        JitArgs a;
+        a.x = x;
+        a.y = y;
+        a.residual = split ? nullptr : residual;
+        a.x_bytes = int(xb);
+        a.y_bytes = int(yb);
+        a.OHOW = g.oh * g.ow;
+        a.NQ = g.n * a.OHOW;
+        a.OW = g.ow; a.H = g.h; a.W = g.w; a.C = g.c; a.K = g.k; a.HW = g.h * g.w;
+        a.sh = g.sh; a.sw = g.sw; a.ph = g.ph; a.pw = g.pw;
+        a.tiles_p = sp.tiles_p;
+        a.group_tiles = std::min(plan->group_tiles, sp.tiles_p);
+        a.nseg = sp.nseg;
+        a.div_ohow = make_fastdiv(uint32_t(a.OHOW));
+        a.div_ow = make_fastdiv(uint32_t(a.OW));
+        void *args[] = {&a};
+        e = hipModuleLaunchKernel(plan->fn, unsigned(int64_t(sp.tiles_p) * sp.nseg), 1, 1,
+                                  kBlockPixels, 1, 1, 0, st, args, nullptr);
+    }
+    if (e == hipSuccess && split) {
+        Epilogue epi;
+        epi.mul = plan->mul;
+        epi.add = plan->add;
+        epi.res = residual;
+        epi.mul_shift = sp.mul_shift;
+        epi.relu = sp.relu;
+        if (epi.any()) e = run_epilogue(g, y, epi, st);
+    }
+    if (e != hipSuccess) return fail(DS_ERR_HIP, "ds_jit_conv_run: %s", hipGetErrorString(e));
+    return ok();
+}
+
+extern "C" ds_status ds_jit_conv_destroy(ds_jit_conv *plan) { return destroy_plan(plan); }
+
+extern "C" ds_status ds_jit_conv_query(const ds_jit_conv *plan, int64_t *code_bytes,
+                                       int32_t *segments, int32_t *splits)
+{
+    if (!plan) return fail(DS_ERR_NULL_POINTER, "plan must not be NULL");
+    if (code_bytes) *code_bytes = plan->code_bytes;
+    if (segments) *segments = plan->sp.nseg;
+    if (splits) *splits = plan->sp.nsplit;
+    return ok();
+}

@@ -1,0 +1,24 @@
+// Kernel arguments shared by the weight-specialised kernel template and its
+// launcher. The generated code itself reads none of them: the template's
+// prologue turns them into per-lane offsets in fixed registers.
+#pragma once
+
+#include <cstdint>
+
+#include "fastdiv.hpp"
+
+namespace ds {
+
+struct JitArgs {
+    const int32_t *x;
+    int32_t *y;
+    const int32_t *residual;  // NULL when the layer adds none
+    int x_bytes, y_bytes;
+    int NQ, OHOW, OW, H, W, C, K, HW, sh, sw, ph, pw;
+    int tiles_p;              // workgroups (4 waves x 64 pixels) per segment
+    int group_tiles;          // pixel tiles that run all segments before the next tiles
+    int nseg;
+    FastDiv div_ohow, div_ow;
+};
+
+}  // namespace ds

@@ -1,0 +1,86 @@
+// Template of the weight-specialised ConvShift kernels.
+//
+// The paper (Section 6) proposes compiling the shift kernels at run time. With
+// the weights known, every shift amount and sign becomes part of the
+// instruction stream: for each reduction element j (input channel, tap) a
+// lane holds its input value x and the 14 right shifts x >> 1 .. x >> 14 in
+// registers, and each non-zero weight of the 64 output channels of a segment
+// is one v_add_u32 or v_sub_u32 of the right register into that channel's
+// accumulator; zero weights cost nothing.
+//
+// This file is compiled to assembly when the library is built. The kernel
+// below computes, per lane, what the generated code needs (the byte offsets of
+// the lane's taps in x, or an offset past the end of x for taps in the
+// padding; the byte offset of its output pixel in y) and hands them over in
+// fixed registers at the JITBODY marker. At run time the generator replaces
+// the marker with a jump, through a table, to the code of this workgroup's
+// segment (64 output channels and a range of input channels), assembled from
+// generated machine words; each segment ends the wave itself. Register use of
+// the generated code (the clobbers below): v14..v111 (v16..v30 the shifted
+// values, v32..v95 the accumulators, v96..v103 the loads in flight), s28..s31.
+#include <hip/hip_runtime.h>
+
+#include <cstdint>
+
+#include "jit.hpp"
+
+using ds::JitArgs;
+
+extern "C" __global__ void __launch_bounds__(256) ds_jit_conv_template(const JitArgs p)
+{
+    const int lane = threadIdx.x & 63;
+    const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+    // Block order: groups of `group_tiles` pixel tiles (the last group may be
+    // smaller); within a group, the segments one after the other, and within a
+    // segment the group's tiles, so that the waves running at the same time
+    // share one segment's code and the inputs of a few pixel tiles stay in L2
+    // while the segments go by. The grid is exactly tiles_p * nseg blocks.
+    const int b = blockIdx.x;
+    const int per_group = p.group_tiles * p.nseg;
+    const int grp = b / per_group, r = b - grp * per_group;
+    const int gsize = min(p.group_tiles, p.tiles_p - grp * p.group_tiles);
+    const int seg = __builtin_amdgcn_readfirstlane(r / gsize);
+    const int tile = grp * p.group_tiles + (r - (r / gsize) * gsize);
+    const int q = tile * 256 + wave * 64 + lane;
+    const int kOOB = int(0x80000000u);
+    int yoff = kOOB;
+    int t0 = kOOB, t1 = kOOB, t2 = kOOB, t3 = kOOB, t4 = kOOB, t5 = kOOB, t6 = kOOB, t7 = kOOB,
+        t8 = kOOB;
+    if (tile < p.tiles_p && q < p.NQ) {
+        const int n = ds::fdiv(q, p.div_ohow);
+        const int pix = q - n * p.OHOW;
+        const int oh = ds::fdiv(pix, p.div_ow);
+        const int ow = pix - oh * p.OW;
+        yoff = (n * p.K * p.OHOW + pix) * 4;
+        const int ih0 = oh * p.sh - p.ph, iw0 = ow * p.sw - p.pw, base = n * p.C * p.HW;
+        // Taps of a 3 x 3 window (r, s) = (t / 3, t % 3); a 1 x 1 layer uses t0 only.
+        auto off = [&](int rr, int ss) {
+            const int ih = ih0 + rr, iw = iw0 + ss;
+            return (ih >= 0 && ih < p.H && iw >= 0 && iw < p.W) ? (base + ih * p.W + iw) * 4 : kOOB;
+        };
+        t0 = off(0, 0); t1 = off(0, 1); t2 = off(0, 2);
+        t3 = off(1, 0); t4 = off(1, 1); t5 = off(1, 2);
+        t6 = off(2, 0); t7 = off(2, 1); t8 = off(2, 2);
+    }
+    const __amdgpu_buffer_rsrc_t xr = __builtin_amdgcn_make_buffer_rsrc(
+        const_cast<int32_t *>(p.x), short(0), p.x_bytes, 0x00020000);
+    const __amdgpu_buffer_rsrc_t yr = __builtin_amdgcn_make_buffer_rsrc(p.y, short(0), p.y_bytes,
+                                                                        0x00020000);
+    const __amdgpu_buffer_rsrc_t rr = __builtin_amdgcn_make_buffer_rsrc(
+        const_cast<int32_t *>(p.residual), short(0), p.residual ? p.y_bytes : 0, 0x00020000);
+    asm volatile("; JITBODY"
+                 :
+                 : "{s[20:23]}"(xr), "{s[24:27]}"(yr), "{s[36:39]}"(rr), "{s19}"(seg),
+                   "{v4}"(t0), "{v5}"(t1), "{v6}"(t2), "{v7}"(t3), "{v8}"(t4), "{v9}"(t5),
+                   "{v10}"(t6), "{v11}"(t7), "{v12}"(t8), "{v13}"(yoff)
+                 : "memory", "v14", "v15", "v16", "v17", "v18", "v19", "v20", "v21", "v22", "v23",
+                   "v24", "v25", "v26", "v27", "v28", "v29", "v30", "v31", "v32", "v33", "v34",
+                   "v35", "v36", "v37", "v38", "v39", "v40", "v41", "v42", "v43", "v44", "v45",
+                   "v46", "v47", "v48", "v49", "v50", "v51", "v52", "v53", "v54", "v55", "v56",
+                   "v57", "v58", "v59", "v60", "v61", "v62", "v63", "v64", "v65", "v66", "v67",
+                   "v68", "v69", "v70", "v71", "v72", "v73", "v74", "v75", "v76", "v77", "v78",
+                   "v79", "v80", "v81", "v82", "v83", "v84", "v85", "v86", "v87", "v88", "v89",
+                   "v90", "v91", "v92", "v93", "v94", "v95", "v96", "v97", "v98", "v99", "v100",
+                   "v101", "v102", "v103", "v104", "v105", "v106", "v107", "v108", "v109",
+                   "v110", "v111", "s28", "s29", "s30", "s31");
+}

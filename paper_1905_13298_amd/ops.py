@@ -6,6 +6,8 @@ weights are int32 tensors holding the uint32 words bit for bit.
 """
 from __future__ import annotations
 
+import ctypes
+
 import numpy as np
 import torch
 
@@ -14,7 +16,8 @@ from ._native import DeepShiftError, call, lib
 __all__ = ["DeepShiftError", "describe_conv2d", "packed_row_words", "pack_shift_weights", "unpack_shift_weights",
            "linear_shift", "conv2d_shift", "linear_mul_i32", "conv2d_mul_i32", "out_size",
            "quantize_shift_weights_q", "quantize_shift_weights_q_many", "quantize_shift_weights_ps",
-           "to_fixed_point", "conv2d_shift_fused", "maxpool2d", "avgpool2d_global", "DS_RELU"]
+           "to_fixed_point", "conv2d_shift_fused", "maxpool2d", "avgpool2d_global", "DS_RELU",
+           "DS_JIT_RESIDUAL", "JitConv", "jit_conv_image"]
 
 DS_RELU = 1
 
@@ -277,3 +280,103 @@ def avgpool2d_global(x: torch.Tensor, out=None) -> torch.Tensor:
     with torch.cuda.device(x.device):
         call("ds_avgpool2d_global", _ptr(x), _ptr(y), n, c, h, w, 0, _stream(x.device))
     return y
+
+
+DS_JIT_RESIDUAL = 2
+
+
+def _host_i32(a, k, name):
+    if a is None:
+        return None
+    a = np.ascontiguousarray(a.cpu().numpy() if isinstance(a, torch.Tensor) else a)
+    if a.dtype != np.int32 or a.size != k:
+        raise ValueError(f"{name} must be {k} int32 values")
+    return a
+
+
+def _jit_args(w_packed, k, bias, mul, add):
+    wp = np.ascontiguousarray(w_packed.cpu().numpy() if isinstance(w_packed, torch.Tensor) else w_packed)
+    wp = wp.view(np.uint32) if wp.dtype in (np.int32, np.uint32) else wp
+    if wp.dtype != np.uint32 or wp.ndim != 2 or wp.shape[0] != k:
+        raise ValueError("w_packed must be packed words [k][row_words]")
+    return wp, _host_i32(bias, k, "bias"), _host_i32(mul, k, "mul"), _host_i32(add, k, "add")
+
+
+def _np_ptr(a):
+    return None if a is None else a.ctypes.data
+
+
+def jit_conv_image(w_packed, x_shape, kernel_size, stride=1, padding=0, bias=None, mul=None,
+                   add=None, mul_shift: int = 16, residual: bool = False, relu: bool = False,
+                   splits: int = 0) -> bytes:
+    """The code object a JitConv with these arguments would load (host only)."""
+    k = int(w_packed.shape[0])
+    wp, b, m, a = _jit_args(w_packed, k, bias, mul, add)
+    n, c, h, w = x_shape
+    r, s = _pair(kernel_size)
+    sh, sw = _pair(stride)
+    ph, pw = _pair(padding)
+    flags = (DS_RELU if relu else 0) | (DS_JIT_RESIDUAL if residual else 0)
+    size = ctypes.c_int64(0)
+    args = [_np_ptr(wp), _np_ptr(b), _np_ptr(m), _np_ptr(a), mul_shift, n, c, h, w, k, r, s, sh, sw,
+            ph, pw, flags, splits]
+    st = lib().ds_jit_conv_image(*args, None, 0, ctypes.byref(size))
+    if st not in (0, 4):
+        call("ds_jit_conv_image", *args, None, 0, ctypes.byref(size))
+    buf = ctypes.create_string_buffer(size.value)
+    call("ds_jit_conv_image", *args, buf, size.value, ctypes.byref(size))
+    return buf.raw[:size.value]
+
+
+class JitConv:
+    """A weight-specialised ConvShift (``ds_jit_conv_*``): machine code generated
+    for fixed weights and a fixed input shape, loaded on the current device.
+
+    ``w_packed``, ``bias``, ``mul`` and ``add`` may be host arrays or tensors (they
+    are read on the host while the code is generated)."""
+
+    def __init__(self, w_packed, x_shape, kernel_size, stride=1, padding=0, bias=None, mul=None,
+                 add=None, mul_shift: int = 16, residual: bool = False, relu: bool = False,
+                 splits: int = 0, device="cuda:0"):
+        self.k = int(w_packed.shape[0])
+        wp, b, m, a = _jit_args(w_packed, self.k, bias, mul, add)
+        self.x_shape = tuple(int(v) for v in x_shape)
+        n, c, h, w = self.x_shape
+        r, s = _pair(kernel_size)
+        sh, sw = _pair(stride)
+        ph, pw = _pair(padding)
+        self.y_shape = (n, self.k, out_size(h, ph, r, sh), out_size(w, pw, s, sw))
+        self.device = torch.device(device)
+        self.residual = residual
+        flags = (DS_RELU if relu else 0) | (DS_JIT_RESIDUAL if residual else 0)
+        handle = ctypes.c_void_p()
+        with torch.cuda.device(self.device):
+            call("ds_jit_conv_create", _np_ptr(wp), _np_ptr(b), _np_ptr(m), _np_ptr(a), mul_shift,
+                 n, c, h, w, self.k, r, s, sh, sw, ph, pw, flags, splits, ctypes.byref(handle))
+        self._h = handle
+        cb, seg, sp = ctypes.c_int64(), ctypes.c_int32(), ctypes.c_int32()
+        call("ds_jit_conv_query", self._h, ctypes.byref(cb), ctypes.byref(seg), ctypes.byref(sp))
+        self.code_bytes, self.segments, self.splits = cb.value, seg.value, sp.value
+
+    def __call__(self, x: torch.Tensor, residual: torch.Tensor | None = None, out=None):
+        _dev_i32(x, "x")
+        if tuple(x.shape) != self.x_shape:
+            raise ValueError(f"x must have shape {self.x_shape}")
+        if residual is not None:
+            _dev_i32(residual, "residual")
+        y = out if out is not None else torch.empty(self.y_shape, dtype=torch.int32, device=x.device)
+        _dev_i32(y, "out")
+        with torch.cuda.device(x.device):
+            call("ds_jit_conv_run", self._h, _ptr(x), _ptr(residual), _ptr(y), _stream(x.device))
+        return y
+
+    def close(self):
+        if getattr(self, "_h", None) is not None and self._h.value:
+            lib().ds_jit_conv_destroy(self._h)
+            self._h = None
+
+    def __del__(self):
+        try:
+            self.close()
+        except Exception:
+            pass

@@ -1,0 +1,168 @@
+"""GPU parity of the weight-specialised ConvShift plans (``ds_jit_conv_*``).
+
+Each plan's output is compared with the oracle element by element on seeded
+inputs: edge shapes (ragged channels, pixels and output channels; strides,
+padding, rectangular windows; LinearShift as 1 x 1 on 1 x 1 images), each with
+the reduction whole, split automatically and split by force (the split-K path
+adds partial sums atomically and runs the epilogue as a pass of its own); the
+fused epilogue (affine map, residual, ReLU) against the oracle's; the single-
+layer workloads in full; and every ResNet-50 layer up to 3 x 3 at batch 128 in
+full against the production kernel, plus sampled outputs against the oracle.
+"""
+import zlib
+
+import numpy as np
+import pytest
+import torch
+
+import oracle
+from paper_1905_13298_amd import ops
+from paper_1905_13298_amd import workloads as W
+
+pytestmark = pytest.mark.gpu
+DEV = torch.device("cuda:0")
+
+
+def say(*a):
+    print(*a, flush=True)
+
+
+def to_dev(a):
+    return None if a is None else torch.from_numpy(np.ascontiguousarray(a)).to(DEV)
+
+
+def rand_case(seed, n, c, h, w, k, r, s, small_x=False):
+    rng = np.random.default_rng(seed)
+    sign = rng.integers(0, 2, (k, c * r * s))
+    shift = rng.integers(0, 16, (k, c * r * s))
+    codes = (sign << 4 | shift).astype(np.uint8)
+    lim = 2 ** 18 if small_x else 2 ** 31
+    x = rng.integers(-lim, lim, (n, c, h, w), dtype=np.int64).astype(np.int32)
+    bias = rng.integers(-(2 ** 31), 2 ** 31, k, dtype=np.int64).astype(np.int32)
+    return codes, x, bias, rng
+
+
+EDGE = [
+    # name, n, c, h, w, k, r, s, stride, pad
+    ("ragged_k_c_pix", 3, 13, 9, 11, 37, 3, 3, 1, 1),
+    ("1x1_s2", 3, 20, 15, 15, 33, 1, 1, 2, 0),
+    ("1x1_s1_odd", 2, 9, 7, 5, 70, 1, 1, 1, 0),
+    ("1x1_pad", 1, 5, 6, 6, 9, 1, 1, 1, 1),
+    ("3x3_s2_odd", 2, 11, 13, 9, 17, 3, 3, 2, 1),
+    ("3x3_s3_pad2", 1, 6, 17, 17, 8, 3, 3, 3, 2),
+    ("rect_2x3", 2, 5, 10, 12, 6, 2, 3, 1, 1),
+    ("7x7_images", 5, 16, 7, 7, 40, 3, 3, 1, 1),
+    ("linear_like", 70, 300, 1, 1, 130, 1, 1, 1, 0),
+    ("tiny", 1, 1, 1, 1, 1, 1, 1, 1, 0),
+    ("big_c_small_k", 1, 300, 6, 6, 3, 3, 3, 1, 1),
+    ("many_tiles", 4, 64, 20, 20, 128, 3, 3, 1, 1),
+]
+
+
+@pytest.mark.parametrize("splits", [1, 0, 3])
+@pytest.mark.parametrize("spec", EDGE, ids=[e[0] for e in EDGE])
+def test_edge_shapes_match_oracle(spec, splits):
+    name, n, c, h, w, k, r, s, st, pd = spec
+    codes, x, bias, _ = rand_case(zlib.crc32(name.encode()) + splits, n, c, h, w, k, r, s)
+    plan = ops.JitConv(ops.pack_shift_weights(codes), x.shape, (r, s), st, pd, bias=bias,
+                       splits=splits)
+    say(f"jit {name} splits={splits} -> {plan.splits} parts, {plan.segments} segments, "
+        f"{plan.code_bytes} code bytes")
+    y = plan(to_dev(x)).cpu().numpy()
+    want = oracle.conv2d_shift(x, codes, bias, r=r, s=s, stride=st, pad=pd)
+    bad = np.flatnonzero(y.ravel() != want.ravel())
+    assert bad.size == 0, f"{bad.size} of {want.size} outputs differ, first at {bad[:5]}"
+
+
+@pytest.mark.parametrize("splits", [1, 2])
+@pytest.mark.parametrize("parts", ["mul", "mul_add_relu", "residual_relu", "all", "relu"])
+def test_epilogue_matches_oracle(parts, splits):
+    n, c, h, w, k, r, s, st, pd = 2, 24, 11, 11, 70, 3, 3, 1, 1
+    codes, x, bias, rng = rand_case(zlib.crc32(parts.encode()) + splits, n, c, h, w, k, r, s,
+                                    small_x=True)
+    mul = add = res = None
+    if "mul" in parts or parts == "all":
+        mul = rng.integers(-(2 ** 17), 2 ** 17, k).astype(np.int32)
+    if "add" in parts or parts == "all":
+        add = rng.integers(-(2 ** 20), 2 ** 20, k).astype(np.int32)
+    if "residual" in parts or parts == "all":
+        res = rng.integers(-(2 ** 24), 2 ** 24, (n, k, h, w)).astype(np.int32)
+    relu = "relu" in parts or parts == "all"
+    say(f"jit epilogue {parts} splits={splits}")
+    plan = ops.JitConv(ops.pack_shift_weights(codes), x.shape, 3, st, pd, bias=bias, mul=mul,
+                       add=add, mul_shift=16, residual=res is not None, relu=relu, splits=splits)
+    y = plan(to_dev(x), residual=to_dev(res)).cpu().numpy()
+    conv = oracle.conv2d_shift(x, codes, bias, r=r, s=s, stride=st, pad=pd)
+    want = oracle.epilogue(conv, mul, add, 16, residual=res, relu=relu)
+    np.testing.assert_array_equal(y, want)
+
+
+@pytest.mark.parametrize("cfg", [0, 1, 2])
+def test_single_layer_configs_exact(cfg):
+    (layer,) = W.config_layers(cfg)
+    x, codes, bias = W.gen_layer(layer, W.CONFIG_SEEDS[cfg], 0)
+    lin = layer.kind == "linear"
+    shape = (layer.n, layer.c, 1, 1) if lin else x.shape
+    say(f"jit cfg{cfg} {layer.name}")
+    plan = ops.JitConv(ops.pack_shift_weights(codes), shape, (1, 1) if lin else (layer.r, layer.s),
+                       1 if lin else layer.stride, 0 if lin else layer.pad, bias=bias)
+    y = plan(to_dev(x.reshape(shape))).cpu().numpy()
+    if lin:
+        want = oracle.linear_shift(x, codes, bias)
+        y = y.reshape(want.shape)
+    else:
+        want = oracle.conv2d_shift(x, codes, bias, r=layer.r, s=layer.s, stride=layer.stride,
+                                   pad=layer.pad)
+    bad = np.flatnonzero(y.ravel() != want.ravel())
+    assert bad.size == 0, f"{bad.size} of {want.size} outputs differ, first at {bad[:5]}"
+
+
+def test_resnet50_full_batch_against_production_kernel_and_oracle():
+    """Every ResNet-50 layer with a window up to 3 x 3, batch 128: all outputs equal
+    those of ds_conv2d_shift (itself pinned to the oracle), 400 sampled outputs
+    per layer equal the oracle's."""
+    rng = np.random.default_rng(50)
+    layers = W.config_layers(4)
+    for li, L in enumerate(layers):
+        if L.kind != "conv" or L.r > 3 or L.s > 3:
+            continue
+        x, codes, bias = W.gen_layer(L, W.CONFIG_SEEDS[4], li)
+        wp = ops.pack_shift_weights(codes)
+        plan = ops.JitConv(wp, x.shape, (L.r, L.s), L.stride, L.pad, bias=bias)
+        say(f"jit resnet50 {L.name}: {plan.splits} parts, {plan.code_bytes / 2 ** 20:.1f} MiB code")
+        xd = to_dev(x)
+        y = plan(xd)
+        ref = ops.conv2d_shift(xd, to_dev(wp.view(np.int32)), to_dev(bias), (L.r, L.s), L.stride, L.pad)
+        diff = int((y != ref).sum())
+        assert diff == 0, f"{L.name}: {diff} outputs differ from ds_conv2d_shift"
+        total = int(np.prod(L.y_shape))
+        idx = np.unique(np.concatenate([rng.choice(total, 400, replace=False), [0, total - 1]]))
+        got = y.reshape(-1)[torch.from_numpy(idx).to(DEV)].cpu().numpy()
+        want = oracle.conv2d_shift_points(x, codes, bias, idx, r=L.r, s=L.s, stride=L.stride,
+                                          pad=L.pad)
+        np.testing.assert_array_equal(got, want, err_msg=L.name)
+        plan.close()
+        del y, ref, xd
+
+
+def test_plan_is_reusable_and_checks_its_arguments():
+    n, c, h, w, k = 2, 10, 6, 6, 8
+    codes, x, bias, rng = rand_case(5, n, c, h, w, k, 3, 3)
+    plan = ops.JitConv(ops.pack_shift_weights(codes), x.shape, 3, 1, 1, bias=bias)
+    for i in range(3):
+        xi = rng.integers(-(2 ** 31), 2 ** 31, x.shape, dtype=np.int64).astype(np.int32)
+        y = plan(to_dev(xi)).cpu().numpy()
+        np.testing.assert_array_equal(y, oracle.conv2d_shift(xi, codes, bias, r=3, stride=1, pad=1))
+    xd = to_dev(x)
+    with pytest.raises(ops.DeepShiftError, match="residual must be NULL"):
+        plan(xd, residual=torch.zeros((n, k, h, w), dtype=torch.int32, device=DEV))
+    with pytest.raises(ops.DeepShiftError, match="overlaps"):
+        plan(xd, out=xd.view(-1)[: n * k * h * w].view(n, k, h, w))
+    rplan = ops.JitConv(ops.pack_shift_weights(codes), x.shape, 3, 1, 1, residual=True)
+    with pytest.raises(ops.DeepShiftError, match="residual must not be NULL"):
+        rplan(xd)
+    res = torch.zeros((n, k, h, w), dtype=torch.int32, device=DEV)
+    with pytest.raises(ops.DeepShiftError, match="overlaps residual"):
+        rplan(xd, residual=res, out=res)
+    plan.close()
+    rplan.close()

@@ -1,0 +1,300 @@
+"""CPU checks of the weight-specialised ConvShift code generator.
+
+``ds_jit_conv_image`` returns the code object a plan would load; no GPU is
+needed. The tests
+
+* check the ELF structure: the generated code is the last loadable segment and
+  lies past every other one;
+* disassemble it with llvm-objdump (an encoder mistake shows up as an unknown or
+  different instruction) and run it in a small interpreter of the dozen gfx950
+  instructions the generator emits, over every lane of every pixel tile at
+  once. The lane inputs (tap and output offsets) follow the template kernel's
+  index arithmetic. The interpreter checks that every in-range buffer access
+  stays inside its buffer (with the range check taken either with or without
+  the scalar offset), that no register is read before the s_waitcnt that
+  covers its load, and that each lane stores each output once. The result is
+  compared with the oracle's convolution and epilogue.
+"""
+import collections
+import zlib
+import os
+import re
+import subprocess
+
+import numpy as np
+import pytest
+
+import oracle
+from paper_1905_13298_amd import ops
+
+LLVM = "/opt/rocm/llvm/bin"
+OOB = 0x80000000
+M32 = 0xFFFFFFFF
+
+
+def gen_layer(seed, n, c, h, w, k, r, s, zero_frac=0.1):
+    rng = np.random.default_rng(seed)
+    sign = rng.integers(0, 2, (k, c * r * s))
+    shift = rng.integers(0, 15, (k, c * r * s))
+    shift[rng.random(shift.shape) < zero_frac] = 15
+    codes = (sign << 4 | shift).astype(np.uint8)
+    x = rng.integers(-(2 ** 31), 2 ** 31, (n, c, h, w), dtype=np.int64).astype(np.int32)
+    return codes, x, rng
+
+
+def disassemble(img, tmp_path):
+    path = os.path.join(tmp_path, "plan.hsaco")
+    with open(path, "wb") as f:
+        f.write(img)
+    out = subprocess.run([f"{LLVM}/llvm-objdump", "-d", "--mcpu=gfx950", path], capture_output=True,
+                         text=True, check=True).stdout
+    insts, body = {}, False
+    for line in out.splitlines():
+        if line.startswith("Disassembly of section"):
+            body = ".jitbody" in line
+            continue
+        if not body or "//" not in line:
+            continue
+        code, comment = line.split("//", 1)
+        addr, words = comment.strip().split(":", 1)
+        parts = code.replace(",", " ").split()
+        insts[int(addr, 16)] = (parts[0], parts[1:], int(addr, 16) + 4 * len(words.split()))
+    return insts
+
+
+def elf_layout(img):
+    rd = subprocess.run([f"{LLVM}/llvm-readelf", "-lS", "-W", "/dev/stdin"], input=img,
+                        capture_output=True, check=True).stdout.decode()
+    loads = [ln.split() for ln in rd.splitlines() if ln.strip().startswith("LOAD")]
+    sec = [ln for ln in rd.splitlines() if ".jitbody" in ln and "PROGBITS" in ln][0].split()
+    i = sec.index("PROGBITS")
+    return loads, int(sec[i + 1], 16), int(sec[i + 2], 16), int(sec[i + 3], 16)
+
+
+def lane_inputs(n, c, h, w, k, r, s, st, pd):
+    """Per lane (pixel q of every 256-pixel tile): tap byte offsets v4..v12 of
+    the 3 x 3 window at channel 0 and the output byte offset v13, as the
+    template kernel computes them (past-the-end marker for padding and for
+    lanes beyond the last pixel)."""
+    oh, ow = (h + 2 * pd - r) // st + 1, (w + 2 * pd - s) // st + 1
+    nq = n * oh * ow
+    lanes = -(-nq // 256) * 256
+    q = np.arange(lanes)
+    valid = q < nq
+    nn, pix = q // (oh * ow), q % (oh * ow)
+    ohh, oww = pix // ow, pix % ow
+    regs = {}
+    for rr in range(3):
+        for ss in range(3):
+            ih, iw = ohh * st - pd + rr, oww * st - pd + ss
+            ok = valid & (ih >= 0) & (ih < h) & (iw >= 0) & (iw < w)
+            regs[4 + rr * 3 + ss] = np.where(ok, (nn * c * h * w + ih * w + iw) * 4, OOB).astype(np.int64)
+    regs[13] = np.where(valid, (nn * k * oh * ow + pix) * 4, OOB).astype(np.int64)
+    return regs, (oh, ow)
+
+
+class Interp:
+    """The generated code, run for all lanes of one segment."""
+
+    def __init__(self, insts, bufs):
+        self.insts, self.bufs = insts, bufs   # bufs: sgpr base -> (uint32 array, num_records)
+
+    @staticmethod
+    def reg(tok):
+        m = re.fullmatch(r"([vs])(\d+)", tok)
+        return (m.group(1), int(m.group(2))) if m else None
+
+    def run(self, start, seg, lanes, y, atomic_ok):
+        V = {i: a.copy() for i, a in lanes.items()}
+        S = {19: seg}
+        pending = collections.OrderedDict()   # vgpr -> value, in issue order
+        stored = collections.Counter()
+        pc = start
+        steps = 0
+
+        def val(tok):
+            rg = self.reg(tok)
+            if rg is None:
+                return int(tok, 0) & M32
+            kind, i = rg
+            if kind == "s":
+                return S[i] & M32
+            assert i not in pending, f"v{i} read before its load completed (pc {pc:#x})"
+            return V[i]
+
+        def sq(tok):
+            return int(re.fullmatch(r"s\[(\d+):\d+\]", tok).group(1))
+
+        def access(ops):
+            base = sq(ops[2])
+            arr, nrec = self.bufs[base]
+            voff = V[int(ops[1][1:])].astype(np.int64)
+            soff = S[int(ops[3][1:])] & M32
+            tot = voff + soff
+            inr = voff < nrec
+            assert not np.any(inr & (tot + 4 > nrec)), f"out-of-range access at pc {pc:#x}"
+            assert not np.any(inr & (tot % 4 != 0))
+            return arr, inr, tot // 4
+
+        while True:
+            steps += 1
+            assert steps < 50_000_000
+            op, ops, nxt = self.insts[pc]
+            if op == "s_getpc_b64":
+                S[28], S[29] = nxt & M32, nxt >> 32
+            elif op in ("s_add_u32", "s_addc_u32"):
+                d = int(ops[0][1:])
+                t = val(ops[1]) + val(ops[2]) + (S.get("scc", 0) if op == "s_addc_u32" else 0)
+                S[d], S["scc"] = t & M32, t >> 32
+            elif op == "s_setpc_b64":
+                nxt = S[28] | (S[29] << 32)
+            elif op == "s_mov_b32":
+                S[int(ops[0][1:])] = val(ops[1])
+            elif op == "s_waitcnt":
+                m = re.fullmatch(r"vmcnt\((\d+)\)", ops[0])
+                keep = int(m.group(1))
+                while len(pending) > keep:
+                    i, v = pending.popitem(last=False)
+                    V[i] = v
+            elif op == "buffer_load_dword":
+                arr, inr, idx = access(ops)
+                d = int(ops[0][1:])
+                assert d not in pending
+                pending[d] = np.where(inr, arr[np.where(inr, idx, 0)], 0).astype(np.int64) & M32
+            elif op in ("buffer_store_dword", "buffer_atomic_add"):
+                assert not pending, "store with loads in flight"
+                arr, inr, idx = access(ops)
+                assert arr is y
+                v = val(ops[0]).astype(np.int64)
+                if op == "buffer_store_dword":
+                    assert not atomic_ok
+                    y[idx[inr]] = v[inr]
+                else:
+                    assert atomic_ok
+                    np.add.at(y, idx[inr], v[inr])
+                    y &= M32
+                for t in idx[inr]:
+                    stored[int(t)] += 1
+            elif op == "v_mov_b32_e32":
+                V[int(ops[0][1:])] = np.broadcast_to(val(ops[1]), V[4].shape).astype(np.int64)
+            elif op in ("v_add_u32_e32", "v_sub_u32_e32"):
+                a, b = np.int64(0) + val(ops[1]), np.int64(0) + val(ops[2])
+                V[int(ops[0][1:])] = ((a + b) if op == "v_add_u32_e32" else (a - b)) & M32
+            elif op == "v_ashrrev_i32_e32":
+                x = val(ops[2]).astype(np.int64)
+                x = np.where(x >= 2 ** 31, x - 2 ** 32, x)
+                V[int(ops[0][1:])] = (x >> int(ops[1], 0)) & M32
+            elif op == "v_max_i32_e32":
+                a = val(ops[2]).astype(np.int64)
+                sa = np.where(a >= 2 ** 31, a - 2 ** 32, a)
+                V[int(ops[0][1:])] = np.maximum(sa, int(ops[1], 0)) & M32
+            elif op in ("v_mul_lo_u32", "v_mul_hi_i32"):
+                a = val(ops[1])
+                sa = a - 2 ** 32 if a >= 2 ** 31 else a
+                b = val(ops[2]).astype(np.int64)
+                sb = np.where(b >= 2 ** 31, b - 2 ** 32, b).astype(object)
+                p = sb * sa
+                V[int(ops[0][1:])] = np.array(((p & M32) if op == "v_mul_lo_u32" else ((p >> 32) & M32)),
+                                              dtype=np.int64)
+            elif op == "v_alignbit_b32":
+                hi, lo = val(ops[1]).astype(object), val(ops[2]).astype(object)
+                sh = int(ops[3], 0)
+                V[int(ops[0][1:])] = np.array((((hi << 32) | lo) >> sh) & M32, dtype=np.int64)
+            elif op == "s_endpgm":
+                return stored
+            elif op == "s_nop":
+                pass
+            else:
+                raise AssertionError(f"unexpected instruction {op} at {pc:#x}")
+            pc = nxt
+
+
+def to_i32(a):
+    a = np.asarray(a, dtype=np.int64) & M32
+    return np.where(a >= 2 ** 31, a - 2 ** 32, a).astype(np.int32)
+
+
+CASES = [
+    # n, c, h, w, k, r, s, stride, pad, splits, epilogue
+    (2, 5, 9, 9, 70, 3, 3, 1, 1, 1, "full"),
+    (2, 5, 9, 9, 70, 3, 3, 2, 1, 2, "none"),
+    (3, 7, 12, 12, 64, 1, 1, 1, 0, 1, "relu"),
+    (1, 6, 7, 8, 20, 2, 3, 1, 1, 3, "full"),
+    (1, 3, 10, 10, 5, 3, 3, 2, 0, 1, "mul"),
+    (33, 40, 1, 1, 17, 1, 1, 1, 0, 1, "full"),     # a LinearShift [33 x 40] -> 17
+    (2, 64, 4, 4, 3, 3, 3, 1, 1, 4, "full"),
+]
+
+
+@pytest.mark.parametrize("case", CASES, ids=[str(i) for i in range(len(CASES))])
+def test_generated_code_matches_oracle(case, tmp_path):
+    n, c, h, w, k, r, s, st, pd, splits, epi = case
+    codes, x, rng = gen_layer(zlib.crc32(str(case).encode()), n, c, h, w, k, r, s)
+    bias = rng.integers(-(2 ** 31), 2 ** 31, k, dtype=np.int64).astype(np.int32)
+    mul = add = res = None
+    relu = epi in ("full", "relu")
+    if epi in ("full", "mul"):
+        mul = rng.integers(-(2 ** 20), 2 ** 20, k).astype(np.int32)
+        add = rng.integers(-(2 ** 31), 2 ** 31, k, dtype=np.int64).astype(np.int32)
+        add[0] = 0
+    wp = ops.pack_shift_weights(codes)
+    lanes, (oh, ow) = lane_inputs(n, c, h, w, k, r, s, st, pd)
+    if epi == "full":
+        res = rng.integers(-(2 ** 31), 2 ** 31, (n, k, oh, ow), dtype=np.int64).astype(np.int32)
+    img = ops.jit_conv_image(wp, (n, c, h, w), (r, s), st, pd, bias=bias, mul=mul, add=add,
+                             mul_shift=13, residual=res is not None, relu=relu, splits=splits)
+
+    loads, addr, off, size = elf_layout(img)
+    assert max(int(ld[2], 16) for ld in loads) == addr          # highest loadable segment
+    assert [ld for ld in loads if int(ld[2], 16) == addr][0][1] == f"0x{off:06x}"
+    assert off + size == len(img)
+
+    insts = disassemble(img, str(tmp_path))
+    body = min(insts)
+    conv = oracle.conv2d_shift(x, codes, bias, r=r, s=s, stride=st, pad=pd)
+    xb = x.reshape(-1).view(np.uint32).astype(np.int64)
+    y = np.full(n * k * oh * ow, 0xDEADBEEF, dtype=np.int64)
+    bufs = {20: (xb, xb.size * 4), 24: (y, y.size * 4)}
+    bufs[36] = (res.reshape(-1).view(np.uint32).astype(np.int64), y.size * 4) if res is not None else (y, 0)
+    nsplit = min(splits, c)
+    kgroups = -(-k // 64)
+    split = nsplit > 1
+    if split:
+        y[:] = np.repeat(np.tile(bias.view(np.uint32).astype(np.int64), n), oh * ow)
+    interp = Interp(insts, bufs)
+    total = collections.Counter()
+    for seg in range(kgroups * nsplit):
+        total.update(interp.run(body + 20 * seg, seg, lanes, y, split))
+    assert len(total) == y.size and set(total.values()) == {nsplit}
+    got = to_i32(y).reshape(n, k, oh, ow)
+    if split:
+        np.testing.assert_array_equal(got, conv)
+    else:
+        want = oracle.epilogue(conv, mul, add, 13, residual=res, relu=relu)
+        np.testing.assert_array_equal(got, want)
+
+
+def test_image_rejects_bad_arguments():
+    codes = np.full((4, 9), 15, np.uint8)
+    wp = ops.pack_shift_weights(codes)
+    with pytest.raises(ops.DeepShiftError, match="UNSUPPORTED"):
+        ops.jit_conv_image(ops.pack_shift_weights(np.full((4, 25), 15, np.uint8)), (1, 1, 8, 8), 5)
+    with pytest.raises(ops.DeepShiftError, match="INVALID_SHAPE"):
+        ops.jit_conv_image(wp, (1, 1, 2, 2), 3)
+    with pytest.raises(ops.DeepShiftError, match="INVALID_ARG"):
+        ops.jit_conv_image(wp, (1, 1, 8, 8), 3, add=np.zeros(4, np.int32))
+    with pytest.raises(ops.DeepShiftError, match="INVALID_ARG"):
+        ops.jit_conv_image(wp, (1, 1, 8, 8), 3, mul=np.ones(4, np.int32), mul_shift=32)
+    bad = wp.copy()
+    bad[0, 0] |= 1 << 30
+    with pytest.raises(ops.DeepShiftError, match="INVALID_CODE"):
+        ops.jit_conv_image(bad, (1, 1, 8, 8), 3)
+
+
+def test_zero_weights_emit_no_arithmetic(tmp_path):
+    """A segment whose weights are all zero is bias, loads and stores only."""
+    codes = np.full((8, 4), 15 | 16, np.uint8)
+    img = ops.jit_conv_image(ops.pack_shift_weights(codes), (1, 4, 3, 3), 1, splits=1)
+    names = collections.Counter(op for op, _, _ in disassemble(img, str(tmp_path)).values())
+    assert names["v_add_u32_e32"] == names["v_sub_u32_e32"] == names["v_ashrrev_i32_e32"] == 0
+    assert names["buffer_store_dword"] == 8
