@@ -2,17 +2,27 @@
 
 A step is one pass of every layer of the workload (each layer's ConvShift or
 LinearShift call on its own seeded input, all inputs resident in HBM).
+Two paths compute the same outputs bit for bit (checked before timing):
+  jit      (default) a weight-specialised plan per layer, its code generated
+           at setup from the fixed weights (Section 6's run-time compilation);
+           layers it does not cover (windows over 3 x 3) run the runtime kernel
+  runtime  ds_conv2d_shift / ds_linear_shift with the packed weights as data
 Prints ONE JSON line:
   value       whole-step throughput in G shift-accumulates/s (dense SAC =
               output elements x reduction terms, zero weights included)
-  roofline    the dominant kernel against the int32 VALU roofline
-              (2 VALU instructions per shift-accumulate)
+  roofline    the dominant kernel against the int32 VALU roofline: the runtime
+              kernel at 2 VALU instructions per dense shift-accumulate (one of
+              them three-operand, 64 lanes per CU per clock); the generated
+              kernel at one two-operand add/sub per non-zero weight term (128
+              lanes per CU per clock)
+  runtime_weights  the runtime path timed on the same inputs (path jit)
   cpu_baseline the oracle on the host cores, on a prefix (small batch) of
               the same seeded inputs
-  mul_i32     the multiplication-based comparison kernel (same tiling) on the
-              same layers
+  mul_i32     the multiplication-based comparison kernel (tiling of the
+              runtime kernel) on the same layers
 
 Usage: python bench.py [--gpus 1] [--steps K] [--warmup W] [--workload resnet50]
+                       [--path jit|runtime]
 """
 from __future__ import annotations
 
@@ -35,9 +45,13 @@ CONVERT_WORKLOADS = {"convert_resnet50": 4}
 # normalisation, residual and ReLU fused into each convolution), N = 32.
 NETWORK_WORKLOADS = {"resnet18_infer": 32}
 
-# MI355X: 256 CUs, 4 SIMD16 per CU -> 64 int32 lane-ops per clock per CU, 2.4 GHz peak clock.
+# MI355X: 256 CUs at 2.4 GHz. Three-operand (VOP3) integer instructions such as
+# v_xad_u32 run 64 lanes per CU per clock; two-operand (VOP2) ones such as
+# v_add_u32 / v_sub_u32 / v_ashrrev_i32 run up to 128, the lane rate of the
+# published fp32 vector peak (157.3 TFLOP/s = 256 x 128 FMA x 2 x 2.4 GHz).
 CUS, LANES_PER_CU, CLOCK_GHZ = 256, 64, 2.4
-INT32_OPS_PEAK_T = CUS * LANES_PER_CU * CLOCK_GHZ / 1000.0        # 39.32 T int32 ops/s
+INT32_OPS_PEAK_T = CUS * LANES_PER_CU * CLOCK_GHZ / 1000.0        # 39.32 T int32 ops/s (VOP3)
+VOP2_OPS_PEAK_T = 2 * INT32_OPS_PEAK_T                              # 78.64 T int32 ops/s (VOP2)
 SAC_PEAK_T = INT32_OPS_PEAK_T / 2.0                                  # 19.66 T SAC/s
 HBM_PEAK_GBS = 8000.0
 
@@ -78,18 +92,35 @@ def parse():
     ap.add_argument("--sq-summary", metavar="DIR",
                     help="summarise a rocprofv3 --pmc run with SQ instruction counters per kernel")
     ap.add_argument("--pmc-copy-bytes", type=int, default=1 << 30)
-    ap.add_argument("--pmc-out", default=TRAFFIC_FILE)
+    ap.add_argument("--pmc-out", default=None,
+                    help="traffic record to write (default: the committed one of --path)")
+    ap.add_argument("--path", default="jit", choices=["jit", "runtime"],
+                    help="jit: weight-specialised plans made at setup (layers they do not cover "
+                         "run the runtime kernel); runtime: ds_conv2d_shift / ds_linear_shift")
+    ap.add_argument("--no-runtime", action="store_true",
+                    help="with --path jit, skip timing the runtime-weights path as well")
     return ap.parse_args()
 
 
-KERNEL_SOURCE = os.path.join(ROOT, "paper_1905_13298_amd", "csrc", "conv_kernels.hip")
-TRAFFIC_FILE = os.path.join(ROOT, "profiles", "hbm_traffic_resnet50_n128.json")
+CSRC = os.path.join(ROOT, "paper_1905_13298_amd", "csrc")
+# The generated weight-specialised kernel (one name for every plan).
+JIT_KERNEL = "ds_jit_conv_template"
+# Per kernel family: the sources its code comes from, and the committed HBM
+# traffic record of its counters on the ResNet-50 workload.
+FAMILIES = {
+    "runtime": (["conv_kernels.hip"], os.path.join(ROOT, "profiles", "hbm_traffic_resnet50_n128.json")),
+    "jit": (["jit.hip", "jit_template.hip"],
+            os.path.join(ROOT, "profiles", "hbm_traffic_jit_resnet50_n128.json")),
+}
 
 
-def kernel_source_hash() -> str:
+def kernel_source_hash(family: str = "runtime") -> str:
     import hashlib
-    with open(KERNEL_SOURCE, "rb") as f:
-        return hashlib.sha256(f.read()).hexdigest()[:16]
+    h = hashlib.sha256()
+    for src in FAMILIES[family][0]:
+        with open(os.path.join(CSRC, src), "rb") as f:
+            h.update(f.read())
+    return h.hexdigest()[:16]
 
 
 def _pmc_rows(directory: str):
@@ -105,9 +136,17 @@ def _pmc_rows(directory: str):
     return [rows[k] for k in sorted(rows)]
 
 
-def pmc_summary(copy_fetch, copy_write, fetch, write, copy_bytes, workload, out):
-    """HBM traffic of the main (tiled or direct) kernels from FETCH_SIZE/WRITE_SIZE runs (KiB per
-    dispatch), each scaled by what the same counter reads for a plain copy of
+MAIN_KERNELS = ("tiled_kernel", "conv_direct_kernel", "ds_jit_conv_template")
+
+
+def _main_rows(rows, layers):
+    """The last len(layers) dispatches of a main kernel: one per layer of the last step."""
+    return [r for r in rows if any(m in r["name"] for m in MAIN_KERNELS)][-len(layers):]
+
+
+def pmc_summary(copy_fetch, copy_write, fetch, write, copy_bytes, workload, path, out):
+    """HBM traffic of the main (tiled, direct or generated) kernels from FETCH_SIZE/WRITE_SIZE
+    runs (KiB per dispatch), each scaled by what the same counter reads for a plain copy of
     copy_bytes (the largest copy dispatch in the calibration runs)."""
     from paper_1905_13298_amd import workloads as W
     cf = max(r["ctr"]["FETCH_SIZE"] for r in _pmc_rows(copy_fetch) if "copyBuffer" in r["name"])
@@ -115,42 +154,45 @@ def pmc_summary(copy_fetch, copy_write, fetch, write, copy_bytes, workload, out)
     fetch_scale = copy_bytes / (cf * 1024.0)
     write_scale = copy_bytes / (cw * 1024.0)
     layers = W.config_layers(WORKLOADS[workload])
-    main = ("tiled_kernel", "conv_direct_kernel")
-    f_rows = [r for r in _pmc_rows(fetch) if any(m in r["name"] for m in main)][-len(layers):]
-    w_rows = [r for r in _pmc_rows(write) if any(m in r["name"] for m in main)][-len(layers):]
+    f_rows = _main_rows(_pmc_rows(fetch), layers)
+    w_rows = _main_rows(_pmc_rows(write), layers)
     per_kernel = {}
     for L, fr, wr in zip(layers, f_rows, w_rows):
-        name = kernel_variant(L).rsplit(" splits", 1)[0]
+        name = group_name(L, path, JIT_KERNEL in fr["name"])
         k = per_kernel.setdefault(name, {"launches": 0, "fetch_bytes": 0.0, "write_bytes": 0.0,
                                           "algorithmic_bytes": 0})
         k["launches"] += 1
         k["fetch_bytes"] += fr["ctr"]["FETCH_SIZE"] * 1024.0 * fetch_scale
         k["write_bytes"] += wr["ctr"]["WRITE_SIZE"] * 1024.0 * write_scale
         k["algorithmic_bytes"] += algorithmic_bytes(L)
-    rec = {"workload": W.CONFIG_NAMES[WORKLOADS[workload]], "kernel_source_sha256_16": kernel_source_hash(),
+    rec = {"workload": W.CONFIG_NAMES[WORKLOADS[workload]], "path": path,
+           "kernel_source_sha256_16": kernel_source_hash(path),
            "copy_bytes": copy_bytes, "fetch_scale": round(fetch_scale, 4),
            "write_scale": round(write_scale, 4), "kernels": per_kernel}
-    with open(out, "w") as f:
+    with open(out or FAMILIES[path][1], "w") as f:
         json.dump(rec, f, indent=1)
     print(json.dumps(rec))
 
 
-def sq_summary(directory, workload):
-    """VALU evidence per kernel variant from one rocprofv3 --pmc run of the bench
+def sq_summary(directory, workload, path):
+    """VALU evidence per kernel from one rocprofv3 --pmc run of the bench
     (one timed step, no warm-up) with SQ_WAVES SQ_INSTS_VALU SQ_INSTS_SALU
     SQ_INSTS_SMEM SQ_INSTS_LDS SQ_WAVE_CYCLES SQ_BUSY_CYCLES SQ_WAIT_INST_ANY and
-    GRBM_GUI_ACTIVE: VALU instructions per shift-accumulate, VALU issue rate per
-    SIMD per clock, and int32 lane-operations per second against the peak."""
+    GRBM_GUI_ACTIVE: VALU instructions per shift-accumulate (dense and non-zero),
+    VALU issue rate per SIMD per clock, and int32 lane-operations per second
+    against the peak."""
     from paper_1905_13298_amd import workloads as W
-    layers = W.config_layers(WORKLOADS[workload])
-    main = ("tiled_kernel", "conv_direct_kernel")
-    rows = [r for r in _pmc_rows(directory) if any(m in r["name"] for m in main)][-len(layers):]
+    cfg = WORKLOADS[workload]
+    layers = W.config_layers(cfg)
+    rows = _main_rows(_pmc_rows(directory), layers)
     per = {}
-    for L, r in zip(layers, rows):
-        name = kernel_variant(L).rsplit(" splits", 1)[0]
-        k = per.setdefault(name, {"launches": 0, "sac": 0, "ns": 0})
+    for li, (L, r) in enumerate(zip(layers, rows)):
+        codes = W.gen_codes(L, W.CONFIG_SEEDS[cfg], li)
+        name = group_name(L, path, JIT_KERNEL in r["name"])
+        k = per.setdefault(name, {"launches": 0, "sac": 0, "nz": 0.0, "ns": 0})
         k["launches"] += 1
         k["sac"] += L.sac
+        k["nz"] += L.sac * float(np.mean((codes & 15) != 15))
         k["ns"] += r["ns"]
         for c, v in r["ctr"].items():
             k[c] = k.get(c, 0.0) + v
@@ -163,27 +205,29 @@ def sq_summary(directory, workload):
             "tsac_s": round(k["sac"] / k["ns"] / 1e3, 3),
             "clock_ghz": round(clk / k["ns"], 3),
             "valu_insts_per_sac": round(valu * 64 / k["sac"], 3),
+            "valu_insts_per_nonzero_sac": round(valu * 64 / k["nz"], 3),
             "valu_issue_per_simd_clk": round(valu / (CUS * 4) / clk, 4),
             "int32_lane_ops_t": round(valu * 64 / k["ns"] / 1e3, 2),
-            "frac_of_int32_peak": round(valu * 64 / k["ns"] / 1e3 / INT32_OPS_PEAK_T, 4),
+            "frac_of_vop3_lane_rate": round(valu * 64 / k["ns"] / 1e3 / INT32_OPS_PEAK_T, 4),
+            "frac_of_vop2_lane_rate": round(valu * 64 / k["ns"] / 1e3 / VOP2_OPS_PEAK_T, 4),
             "salu_per_valu": round(k["SQ_INSTS_SALU"] / valu, 3),
             "smem_per_valu": round(k["SQ_INSTS_SMEM"] / valu, 4),
             "lds_per_valu": round(k["SQ_INSTS_LDS"] / valu, 4),
             "wait_inst_any_per_wave_cycle": round(k["SQ_WAIT_INST_ANY"] / k["SQ_WAVE_CYCLES"], 3),
         }
-    rec = {"workload": W.CONFIG_NAMES[WORKLOADS[workload]], "kernel_source_sha256_16": kernel_source_hash(),
-           "kernels": out}
+    rec = {"workload": W.CONFIG_NAMES[cfg], "path": path,
+           "kernel_source_sha256_16": kernel_source_hash(path), "kernels": out}
     print(json.dumps(rec, indent=1))
 
 
-def measured_traffic(kernel: str):
+def measured_traffic(kernel: str, family: str):
     """HBM bytes per launch of `kernel` from the committed counter record, or None
     when there is none or the kernel source changed since it was taken."""
     try:
-        rec = json.load(open(TRAFFIC_FILE))
+        rec = json.load(open(FAMILIES[family][1]))
     except (OSError, ValueError):
         return None
-    if rec.get("kernel_source_sha256_16") != kernel_source_hash():
+    if rec.get("kernel_source_sha256_16") != kernel_source_hash(family):
         return None
     k = rec["kernels"].get(kernel)
     if not k:
@@ -304,9 +348,8 @@ def bench_convert(args):
 def bench_network(args):
     """One step = one forward pass of the network over the batch (every op on the GPU,
     input resident in HBM); reported in images/s, with the shift convolutions'
-    SAC rate against the VALU roofline."""
+    rate against the VALU roofline."""
     import torch
-    from paper_1905_13298_amd import ops
     from paper_1905_13298_amd import workloads as W
     from paper_1905_13298_amd.network import ShiftNetwork
 
@@ -314,40 +357,58 @@ def bench_network(args):
     dev = torch.device("cuda:0")
     torch.cuda.set_device(dev)
     graph, params = W.resnet18_graph(n), W.resnet18_params(n)
-    net = ShiftNetwork(graph, params, device=dev)
     x = torch.from_numpy(W.gen_images(n)).to(dev)
-    for _ in range(args.warmup):
-        net.forward(x)
     stream = torch.cuda.current_stream(dev)
-    ev = [[(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True))
-           for _ in graph] for _ in range(args.steps)]
-    t0, t1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
-    torch.cuda.synchronize()
-    t0.record(stream)
-    for s in range(args.steps):
-        buf = {"x": x}
-        for i, op in enumerate(graph):
-            ev[s][i][0].record(stream)
-            net.run_op(op, buf)
-            ev[s][i][1].record(stream)
-    t1.record(stream)
-    torch.cuda.synchronize()
-    ms_per_step = t0.elapsed_time(t1) / args.steps
-    op_ms = [sum(ev[s][i][0].elapsed_time(ev[s][i][1]) for s in range(args.steps)) / args.steps
-             for i in range(len(graph))]
     conv_idx = [i for i, op in enumerate(graph) if op["op"] in ("conv", "linear")]
     sac = sum(graph[i]["layer"].sac for i in conv_idx)
-    conv_ms = sum(op_ms[i] for i in conv_idx)
+    nz = sum(graph[i]["layer"].sac * float(np.mean((params[graph[i]["layer"].name]["codes"] & 15) != 15))
+             for i in conv_idx)
+
+    def timed(net):
+        calls = []
+        buf = {"x": x}
+        for op in graph:
+            calls.append(lambda op=op: net.run_op(op, buf))
+        return time_layers(calls, args.steps, args.warmup, stream)
+
+    nets = {"runtime": ShiftNetwork(graph, params, device=dev)}
+    if args.path == "jit":
+        nets["jit"] = ShiftNetwork(graph, params, device=dev, jit=True)
+        a_out = nets["runtime"].forward(x, keep=True)
+        b_out = nets["jit"].forward(x, keep=True)
+        for op in graph:
+            if not torch.equal(a_out[op["dst"]], b_out[op["dst"]]):
+                raise SystemExit(f"{op['dst']}: weight-specialised and runtime outputs differ")
+        del a_out, b_out
+    results = {p: timed(net) for p, net in nets.items()}
+    ms_per_step, d = results[args.path]
+    op_ms = d.mean(axis=0)
+    conv_ms = float(sum(op_ms[i] for i in conv_idx))
     per_kind = {}
     for i, op in enumerate(graph):
-        per_kind[op["op"]] = round(per_kind.get(op["op"], 0.0) + op_ms[i], 4)
-    achieved = sac / (conv_ms * 1e-3) / 1e12
-    roofline = {"bound": "alu", "achieved": round(achieved, 4), "peak": SAC_PEAK_T,
-                "unit": "TSAC/s", "frac": round(achieved / SAC_PEAK_T, 4), "traffic": None,
-                "kernel": "shift convolutions with fused epilogue (all 21 layers)",
-                "launches_per_step": len(conv_idx), "avg_launch_ms": round(conv_ms / len(conv_idx), 5),
-                "sac_per_launch_avg": sac // len(conv_idx),
-                "timed_span": "library call per layer (weight decode + conv + fused epilogue)"}
+        per_kind[op["op"]] = round(per_kind.get(op["op"], 0.0) + float(op_ms[i]), 4)
+    common = {"traffic": None, "launches_per_step": len(conv_idx),
+              "avg_launch_ms": round(conv_ms / len(conv_idx), 5), "sac_per_launch_avg": sac // len(conv_idx),
+              "dense_tsac_s": round(sac / (conv_ms * 1e-3) / 1e12, 4)}
+    if args.path == "jit":
+        achieved = nz / (conv_ms * 1e-3) / 1e12
+        roofline = {"bound": "alu", "achieved": round(achieved, 4), "peak": round(VOP2_OPS_PEAK_T, 4),
+                    "unit": "T int32 ops/s", "frac": round(achieved / VOP2_OPS_PEAK_T, 4), **common,
+                    "work_unit": "one int32 VOP2 add/sub per non-zero weight term",
+                    "kernel": "weight-specialised convolutions with fused epilogue (stem on the runtime kernel)",
+                    "timed_span": "library call per layer"}
+    else:
+        achieved = sac / (conv_ms * 1e-3) / 1e12
+        roofline = {"bound": "alu", "achieved": round(achieved, 4), "peak": SAC_PEAK_T,
+                    "unit": "TSAC/s", "frac": round(achieved / SAC_PEAK_T, 4), **common,
+                    "work_unit": "dense shift-accumulate, 2 int32 VALU ops each",
+                    "kernel": "shift convolutions with fused epilogue (all 21 layers)",
+                    "timed_span": "library call per layer (weight decode + conv + fused epilogue)"}
+    runtime = None
+    if args.path == "jit":
+        rt_ms = results["runtime"][0]
+        runtime = {"ms_per_step": round(rt_ms, 4), "value": round(n / (rt_ms * 1e-3), 1),
+                   "unit": "images/s"}
     cpu = None
     if not args.no_cpu_baseline:
         import oracle
@@ -366,10 +427,11 @@ def bench_network(args):
         "value": round(ips, 1), "unit": "images/s", "n_gpus": 1, "steps": args.steps,
         "warmup": args.warmup, "ms_per_step": round(ms_per_step, 4), "ms_per_image": round(ms_per_step / n, 5),
         "higher_is_better": True, "scaling": "weak", "vs_baseline": None, "dtype": "i32",
-        "data": "synthetic",
+        "data": "synthetic", "path": args.path,
         "config": {"workload": f"resnet18_forward_n{n}_224", "batch": n, "ops": len(graph),
-                   "sac_per_step": sac, "frac_bits": W.FRAC_BITS, "parallelism": "single GPU"},
-        "ms_by_op": per_kind, "roofline": roofline, "cpu_baseline": cpu,
+                   "sac_per_step": sac, "nonzero_sac_per_step": int(nz), "frac_bits": W.FRAC_BITS,
+                   "parallelism": "single GPU"},
+        "ms_by_op": per_kind, "roofline": roofline, "runtime_weights": runtime, "cpu_baseline": cpu,
     }
     print(json.dumps(out), flush=True)
 
@@ -380,10 +442,10 @@ def main():
         copy_only(args.copy_only)
         return
     if args.pmc_summary:
-        pmc_summary(*args.pmc_summary, args.pmc_copy_bytes, args.workload, args.pmc_out)
+        pmc_summary(*args.pmc_summary, args.pmc_copy_bytes, args.workload, args.path, args.pmc_out)
         return
     if args.sq_summary:
-        sq_summary(args.sq_summary, args.workload)
+        sq_summary(args.sq_summary, args.workload, args.path)
         return
     if args.gpus != 1:
         print(f"bench.py runs on one GPU only (asked for {args.gpus}); the shift operators need "
@@ -398,6 +460,91 @@ def main():
         bench_network(args)
         return
 
+    bench_layers(args)
+
+
+def jit_supported(L) -> bool:
+    """Layers a weight-specialised plan covers: windows up to 3 x 3 and LinearShift."""
+    return L.kind == "linear" or (L.r <= 3 and L.s <= 3)
+
+
+def group_name(L, path: str, planned: bool | None = None) -> str:
+    """The kernel a layer's call is accounted to (one kernel instance). `planned`:
+    whether the layer runs a weight-specialised plan (default: whenever one covers it)."""
+    if path == "jit" and (jit_supported(L) if planned is None else planned):
+        return JIT_KERNEL
+    return kernel_variant(L).rsplit(" splits", 1)[0]
+
+
+def time_layers(calls, steps, warmup, stream):
+    """Run every call `warmup` times untimed, then `steps` timed passes with
+    HIP events around each call on `stream`. Returns (ms per step, per-call
+    durations [steps][calls] in ms)."""
+    import torch
+    for _ in range(warmup):
+        for c in calls:
+            c()
+    torch.cuda.synchronize()
+    ev = [[(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True))
+           for _ in calls] for _ in range(steps)]
+    t_start = torch.cuda.Event(enable_timing=True)
+    t_end = torch.cuda.Event(enable_timing=True)
+    torch.cuda.synchronize()
+    t_start.record(stream)
+    for s in range(steps):
+        for i, c in enumerate(calls):
+            ev[s][i][0].record(stream)
+            c()
+            ev[s][i][1].record(stream)
+    t_end.record(stream)
+    torch.cuda.synchronize()
+    d = np.array([[a.elapsed_time(b) for a, b in row] for row in ev])
+    return t_start.elapsed_time(t_end) / steps, d
+
+
+def roofline_of(layers, d, path, nonzero, planned=None):
+    """Roofline record of the kernel with the most time per step, from the
+    per-call durations `d` [steps][layers]; planned[i]: layer i runs a plan."""
+    groups = {}
+    for li, L in enumerate(layers):
+        g = groups.setdefault(group_name(L, path, None if planned is None else planned[li]), {"sac": 0, "nz": 0.0, "ms": 0.0, "launches": 0,
+                                                    "bytes": 0})
+        g["sac"] += L.sac
+        g["nz"] += L.sac * nonzero[li]
+        g["ms"] += float(d[:, li].mean())
+        g["launches"] += 1
+        g["bytes"] += algorithmic_bytes(L)
+    name, g = max(groups.items(), key=lambda kv: kv[1]["ms"])
+    traffic = measured_traffic(name, "jit" if name == JIT_KERNEL else "runtime")
+    common = {
+        "traffic": None if traffic is None else int(traffic),
+        "traffic_unit": "HBM bytes per launch (FETCH_SIZE + WRITE_SIZE, copy-calibrated)",
+        "algorithmic_bytes_per_launch": g["bytes"] // g["launches"],
+        "kernel": name, "launches_per_step": g["launches"],
+        "avg_launch_ms": round(g["ms"] / g["launches"], 5),
+        "sac_per_launch_avg": g["sac"] // g["launches"],
+        "hbm_gbs_algorithmic": round(g["bytes"] / (g["ms"] * 1e-3) / 1e9, 1),
+    }
+    dense = g["sac"] / (g["ms"] * 1e-3) / 1e12
+    if name == JIT_KERNEL:
+        # Weight-specialised code: one VOP2 add or subtract per non-zero weight term
+        # is the floor (the shifts are shared by 64 output channels, zero weights cost
+        # nothing), so the roofline counts non-zero terms against the VOP2 lane-op peak.
+        nz = g["nz"] / (g["ms"] * 1e-3) / 1e12
+        return {"bound": "alu", "achieved": round(nz, 4), "peak": round(VOP2_OPS_PEAK_T, 4),
+                "unit": "T int32 ops/s", "frac": round(nz / VOP2_OPS_PEAK_T, 4), **common,
+                "work_unit": "one int32 VOP2 add/sub per non-zero weight term",
+                "nonzero_sac_per_launch_avg": int(g["nz"] // g["launches"]),
+                "dense_tsac_s": round(dense, 4),
+                "timed_span": "library call per launch (split-K fill pass + generated kernel)"}
+    return {"bound": "alu", "achieved": round(dense, 4), "peak": round(SAC_PEAK_T, 4),
+            "unit": "TSAC/s", "frac": round(dense / SAC_PEAK_T, 4), **common,
+            "work_unit": "dense shift-accumulate, 2 int32 VALU ops each",
+            "int32_ops_frac": round(2 * dense / INT32_OPS_PEAK_T, 4),
+            "timed_span": "library call (weight decode + main kernel) per launch"}
+
+
+def bench_layers(args):
     import torch
     from paper_1905_13298_amd import ops
     from paper_1905_13298_amd import workloads as W
@@ -407,185 +554,195 @@ def main():
     layers = W.config_layers(cfg)
     dev = torch.device("cuda:0")
     torch.cuda.set_device(dev)
+    stream = torch.cuda.current_stream(dev)
 
-    # ---- inputs, resident in HBM before timing
+    # ---- inputs resident in HBM before timing; weight-specialised plans are made
+    # here too (host code generation, once per layer, like packing the weights)
     t0 = time.time()
-    res = []
+    res, plans, nonzero = [], [], []
+    plan_s = 0.0
     for li, L in enumerate(layers):
         x, codes, bias = W.gen_layer(L, seed, li)
-        wp = ops.pack_shift_weights(codes).view(np.int32)
+        nonzero.append(float(np.mean((codes & 15) != 15)))
+        wp = ops.pack_shift_weights(codes)
         xt = torch.from_numpy(x).to(dev)
-        wt = torch.from_numpy(wp).to(dev)
+        wt = torch.from_numpy(wp.view(np.int32)).to(dev)
         bt = None if bias is None else torch.from_numpy(bias).to(dev)
         yt = torch.empty(L.y_shape, dtype=torch.int32, device=dev)
         res.append((L, xt, wt, bt, yt))
+        plan = None
+        if args.path == "jit" and jit_supported(L):
+            tp = time.time()
+            if L.kind == "linear":
+                plan = ops.JitConv(wp, (L.n, L.c, 1, 1), 1, 1, 0, bias=bias)
+            else:
+                plan = ops.JitConv(wp, L.x_shape, (L.r, L.s), L.stride, L.pad, bias=bias)
+            plan_s += time.time() - tp
+            if not plan.preferred:
+                plan.close()
+                plan = None
+        plans.append(plan)
         del x, codes, bias
     torch.cuda.synchronize()
-    print(f"# inputs ready in {time.time() - t0:.1f} s", file=sys.stderr, flush=True)
+    print(f"# inputs ready in {time.time() - t0:.1f} s (plans {plan_s:.1f} s)", file=sys.stderr, flush=True)
 
-    def run_layer(L, xt, wt, bt, yt):
+    def runtime_call(L, xt, wt, bt, yt):
         if L.kind == "linear":
-            ops.linear_shift(xt, wt, bt, out=yt)
-        else:
-            ops.conv2d_shift(xt, wt, bt, (L.r, L.s), L.stride, L.pad, out=yt)
+            return lambda: ops.linear_shift(xt, wt, bt, out=yt)
+        return lambda: ops.conv2d_shift(xt, wt, bt, (L.r, L.s), L.stride, L.pad, out=yt)
 
-    for _ in range(args.warmup):
-        for r in res:
-            run_layer(*r)
-    torch.cuda.synchronize()
+    def jit_call(plan, L, xt, wt, bt, yt):
+        if plan is None:
+            return runtime_call(L, xt, wt, bt, yt)
+        if L.kind == "linear":
+            x4, y4 = xt.view(L.n, L.c, 1, 1), yt.view(L.n, L.k, 1, 1)
+            return lambda: plan(x4, out=y4)
+        return lambda: plan(xt, out=yt)
 
-    stream = torch.cuda.current_stream(dev)
-    ev = [[(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True))
-           for _ in res] for _ in range(args.steps)]
-    t_start = torch.cuda.Event(enable_timing=True)
-    t_end = torch.cuda.Event(enable_timing=True)
-    torch.cuda.synchronize()
-    t_start.record(stream)
-    for s in range(args.steps):
-        for li, r in enumerate(res):
-            ev[s][li][0].record(stream)
-            run_layer(*r)
-            ev[s][li][1].record(stream)
-    t_end.record(stream)
-    torch.cuda.synchronize()
-    total_ms = t_start.elapsed_time(t_end)
-    ms_per_step = total_ms / args.steps
-
+    runtime_calls = [runtime_call(*r) for r in res]
     sac_step = sum(L.sac for L in layers)
+    nz_step = sum(L.sac * f for L, f in zip(layers, nonzero))
+
+    if args.path == "jit":
+        jit_calls = [jit_call(p, *r) for p, r in zip(plans, res)]
+        # Both paths must agree on every output before either is timed.
+        for c in jit_calls:
+            c()
+        jit_out = [r[4].clone() for r in res]
+        for c in runtime_calls:
+            c()
+        torch.cuda.synchronize()
+        for (L, *_r, yt), yj in zip(res, jit_out):
+            if not torch.equal(yt, yj):
+                raise SystemExit(f"{L.name}: weight-specialised and runtime outputs differ")
+        del jit_out
+        ms_per_step, d = time_layers(jit_calls, args.steps, args.warmup, stream)
+    else:
+        ms_per_step, d = time_layers(runtime_calls, args.steps, args.warmup, stream)
     value = sac_step / (ms_per_step * 1e-3) / 1e9
+    planned = [p is not None for p in plans]
+    roofline = roofline_of(layers, d, args.path, nonzero, planned)
+
+    runtime = None
+    d_rt = d
+    if args.path == "jit" and not args.no_runtime:
+        rt_ms, d_rt = time_layers(runtime_calls, args.steps, args.warmup, stream)
+        rt_value = sac_step / (rt_ms * 1e-3) / 1e9
+        runtime = {"ms_per_step": round(rt_ms, 4), "value": round(rt_value, 2), "unit": "GSAC/s",
+                   "frac_sac_peak": round(rt_value / 1000.0 / SAC_PEAK_T, 4),
+                   "roofline": roofline_of(layers, d_rt, "runtime", nonzero)}
 
     per_layer = []
     for li, L in enumerate(layers):
-        d = np.array([ev[s][li][0].elapsed_time(ev[s][li][1]) for s in range(args.steps)])
-        med = float(np.median(d))
-        per_layer.append({
-            "layer": L.name, "kind": L.kind, "variant": kernel_variant(L),
+        med = float(np.median(d[:, li]))
+        row = {
+            "layer": L.name, "kind": L.kind, "kernel": group_name(L, args.path, planned[li]),
+            "variant": kernel_variant(L),
             "shape": {"n": L.n, "c": L.c, "h": L.h, "w": L.w, "k": L.k, "r": L.r, "s": L.s,
                       "stride": L.stride, "pad": L.pad},
-            "sac": L.sac, "ms_median": med, "ms_mean": float(d.mean()), "ms_min": float(d.min()),
+            "sac": L.sac, "nonzero_frac": round(nonzero[li], 4), "ms_median": med,
+            "ms_mean": float(d[:, li].mean()), "ms_min": float(d[:, li].min()),
             "gsac_s": L.sac / (med * 1e-3) / 1e9,
             "frac_sac_peak": L.sac / (med * 1e-3) / 1e12 / SAC_PEAK_T,
+            "frac_vop2_peak_nonzero": L.sac * nonzero[li] / (med * 1e-3) / 1e12 / VOP2_OPS_PEAK_T,
             "hbm_gbs": algorithmic_bytes(L) / (med * 1e-3) / 1e9,
-        })
+        }
+        if runtime is not None:
+            row["runtime_ms_median"] = float(np.median(d_rt[:, li]))
+        per_layer.append(row)
 
-    # ---- dominant kernel: the main-kernel instance with the most time per step
-    groups = {}
-    for li, (L, *_rest) in enumerate(res):
-        name = kernel_variant(L).rsplit(" splits", 1)[0]   # one kernel instance
-        g = groups.setdefault(name, {"sac": 0, "ms": 0.0, "launches": 0, "bytes": 0})
-        g["sac"] += L.sac
-        g["ms"] += float(np.mean([ev[s][li][0].elapsed_time(ev[s][li][1])
-                                  for s in range(args.steps)]))
-        g["launches"] += 1
-        g["bytes"] += algorithmic_bytes(L)
-    dom_name, dom = max(groups.items(), key=lambda kv: kv[1]["ms"])
-    achieved = dom["sac"] / (dom["ms"] * 1e-3) / 1e12
-    traffic = measured_traffic(dom_name)
-    roofline = {
-        "bound": "alu", "achieved": round(achieved, 4), "peak": round(SAC_PEAK_T, 4),
-        "unit": "TSAC/s", "frac": round(achieved / SAC_PEAK_T, 4),
-        "traffic": None if traffic is None else int(traffic),
-        "traffic_unit": "HBM bytes per launch (FETCH_SIZE + WRITE_SIZE, copy-calibrated)",
-        "algorithmic_bytes_per_launch": dom["bytes"] // dom["launches"],
-        "kernel": dom_name, "launches_per_step": dom["launches"],
-        "avg_launch_ms": round(dom["ms"] / dom["launches"], 5),
-        "sac_per_launch_avg": dom["sac"] // dom["launches"],
-        "int32_ops_frac": round(2 * achieved / INT32_OPS_PEAK_T, 4),
-        "hbm_gbs_algorithmic": round(dom["bytes"] / (dom["ms"] * 1e-3) / 1e9, 1),
-        "timed_span": "library call (weight decode + main kernel) per launch",
-    }
-
-    # ---- multiplication-based comparison kernel, same tiling, same layers
+    # ---- multiplication-based comparison kernel, same tiling as the runtime kernel
     mul = None
     if not args.no_mul:
-        mres = []
         g = torch.Generator(device=dev)
         g.manual_seed(seed)
+        mul_calls = []
         for (L, xt, wt, bt, yt) in res:
             wm = torch.randint(-(1 << 15), 1 << 15, (L.k, L.crs), dtype=torch.int32, device=dev,
                                generator=g)
-            mres.append((L, xt, wm, bt, yt))
-
-        def run_mul(L, xt, wm, bt, yt):
             if L.kind == "linear":
-                ops.linear_mul_i32(xt, wm, bt, out=yt)
+                mul_calls.append(lambda xt=xt, wm=wm, bt=bt, yt=yt: ops.linear_mul_i32(xt, wm, bt, out=yt))
             else:
-                ops.conv2d_mul_i32(xt, wm, bt, (L.r, L.s), L.stride, L.pad, out=yt)
-
-        for r in mres:
-            run_mul(*r)
-        torch.cuda.synchronize()
-        a = torch.cuda.Event(enable_timing=True)
-        b = torch.cuda.Event(enable_timing=True)
-        a.record(stream)
-        for _ in range(args.steps):
-            for r in mres:
-                run_mul(*r)
-        b.record(stream)
-        torch.cuda.synchronize()
-        mul_ms = a.elapsed_time(b) / args.steps
+                mul_calls.append(lambda L=L, xt=xt, wm=wm, bt=bt, yt=yt:
+                                 ops.conv2d_mul_i32(xt, wm, bt, (L.r, L.s), L.stride, L.pad, out=yt))
+        mul_ms, _ = time_layers(mul_calls, args.steps, 1, stream)
         mul = {"ms_per_step": round(mul_ms, 4), "gmac_s": round(sac_step / (mul_ms * 1e-3) / 1e9, 1),
                "shift_speedup": round(mul_ms / ms_per_step, 3),
-               "inner_op": "v_mul_lo_u32 + v_add_u32 (int32, mod 2^32)"}
-        del mres
+               "inner_op": "v_mul_lo_u32 + v_add_u32 (int32, mod 2^32), tiling of the runtime kernel"}
+        del mul_calls
 
     # ---- CPU baseline: the oracle on the host cores, same layers at a small batch
     cpu = None
     if not args.no_cpu_baseline:
-        import oracle
-        del res
+        del res, plans, runtime_calls
+        if args.path == "jit":
+            del jit_calls
         torch.cuda.empty_cache()
-        nthreads = oracle.max_threads()
-        cpu_batch = args.cpu_batch
-        if cpu_batch is None:
-            cpu_batch = {0: 8, 1: 1, 2: 256, 3: 8, 4: 8}[cfg]
-        sample = [L.with_batch(min(cpu_batch, L.n)) for L in layers]
-        cache_inputs = sum(4 * int(np.prod(L.x_shape)) for L in sample) < (2 << 30)
-        cached = {}
-        sample_sac = 0
-        cpu_total = 0.0
-        passes = 0
-        wall0 = time.perf_counter()
-        # Whole passes over the sample until about args.cpu_seconds of oracle time.
-        while True:
-            for li, Ls in enumerate(sample):
-                if li in cached:
-                    x, codes, bias = cached[li]
-                else:
-                    x, codes, bias = W.gen_layer(Ls, seed, li)
-                    if cache_inputs:
-                        cached[li] = (x, codes, bias)
-                t1 = time.perf_counter()
-                if Ls.kind == "linear":
-                    oracle.linear_shift(x, codes, bias)
-                else:
-                    oracle.conv2d_shift(x, codes, bias, r=Ls.r, s=Ls.s, stride=Ls.stride, pad=Ls.pad)
-                cpu_total += time.perf_counter() - t1
-                sample_sac += Ls.sac
-            passes += 1
-            if cpu_total >= args.cpu_seconds or time.perf_counter() - wall0 > 3 * args.cpu_seconds:
-                break
-        cached.clear()
-        cpu = {"value": round(sample_sac / cpu_total / 1e9, 3), "unit": "GSAC/s",
-               "cores": nthreads, "kind": "oracle",
-               "sample": f"{passes} pass(es) over every layer of the workload at batch {cpu_batch} "
-                         f"({sample_sac / 1e9:.2f} G SAC, {cpu_total:.1f} s)"}
+        cpu = cpu_baseline(args, cfg, seed, layers)
 
+    path_desc = ("weight-specialised plans (code generated per layer at setup; windows up to 3x3 "
+                 "and LinearShift), other layers on the runtime kernel"
+                 if args.path == "jit" else "runtime weights (ds_conv2d_shift / ds_linear_shift)")
     out = {
         "metric": "G shift-accumulates/s per layer and % of int32 VALU peak on one MI355X",
         "value": round(value, 2), "unit": "GSAC/s", "n_gpus": 1, "steps": args.steps,
         "warmup": args.warmup, "ms_per_step": round(ms_per_step, 4), "higher_is_better": True,
         "scaling": "weak", "vs_baseline": None, "dtype": "i32", "data": "synthetic",
-        "frac_sac_peak": round(value / 1000.0 / SAC_PEAK_T, 4),
+        **({"frac_vop2_peak_nonzero": round(nz_step / (ms_per_step * 1e-3) / 1e12 / VOP2_OPS_PEAK_T, 4)}
+           if args.path == "jit" else {"frac_sac_peak": round(value / 1000.0 / SAC_PEAK_T, 4)}),
+        "path": path_desc,
         "config": {"workload": W.CONFIG_NAMES[cfg], "layers": len(layers),
                    "batch": layers[0].n, "frac_bits": W.FRAC_BITS,
-                   "sac_per_step": sac_step, "parallelism": "single GPU"},
-        "roofline": roofline, "cpu_baseline": cpu, "mul_i32": mul,
+                   "sac_per_step": sac_step, "nonzero_sac_per_step": int(nz_step),
+                   "parallelism": "single GPU"},
+        "roofline": roofline, "runtime_weights": runtime, "cpu_baseline": cpu, "mul_i32": mul,
     }
     if args.layers_out:
         with open(args.layers_out, "w") as f:
-            json.dump({"workload": W.CONFIG_NAMES[cfg], "layers": per_layer}, f, indent=1)
+            json.dump({"workload": W.CONFIG_NAMES[cfg], "path": args.path, "layers": per_layer}, f,
+                      indent=1)
     print(json.dumps(out), flush=True)
+
+
+def cpu_baseline(args, cfg, seed, layers):
+    """The oracle on the host's cores over whole passes of every layer at a small
+    batch, for about args.cpu_seconds of oracle time."""
+    import oracle
+    from paper_1905_13298_amd import workloads as W
+    nthreads = oracle.max_threads()
+    cpu_batch = args.cpu_batch
+    if cpu_batch is None:
+        cpu_batch = {0: 8, 1: 1, 2: 256, 3: 8, 4: 8}[cfg]
+    sample = [L.with_batch(min(cpu_batch, L.n)) for L in layers]
+    cache_inputs = sum(4 * int(np.prod(L.x_shape)) for L in sample) < (2 << 30)
+    cached = {}
+    sample_sac = 0
+    cpu_total = 0.0
+    passes = 0
+    wall0 = time.perf_counter()
+    while True:
+        for li, Ls in enumerate(sample):
+            if li in cached:
+                x, codes, bias = cached[li]
+            else:
+                x, codes, bias = W.gen_layer(Ls, seed, li)
+                if cache_inputs:
+                    cached[li] = (x, codes, bias)
+            t1 = time.perf_counter()
+            if Ls.kind == "linear":
+                oracle.linear_shift(x, codes, bias)
+            else:
+                oracle.conv2d_shift(x, codes, bias, r=Ls.r, s=Ls.s, stride=Ls.stride, pad=Ls.pad)
+            cpu_total += time.perf_counter() - t1
+            sample_sac += Ls.sac
+        passes += 1
+        if cpu_total >= args.cpu_seconds or time.perf_counter() - wall0 > 3 * args.cpu_seconds:
+            break
+    cached.clear()
+    return {"value": round(sample_sac / cpu_total / 1e9, 3), "unit": "GSAC/s",
+            "cores": nthreads, "kind": "oracle",
+            "sample": f"{passes} pass(es) over every layer of the workload at batch {cpu_batch} "
+                      f"({sample_sac / 1e9:.2f} G SAC, {cpu_total:.1f} s)"}
 
 
 if __name__ == "__main__":

@@ -47,6 +47,9 @@ def _load():
         lib.oracle_conv2d_shift_points.argtypes = [_P, _P, _P] + [_I] * 11 + [_P, _I, _P]
         lib.oracle_linear_shift_points.argtypes = [_P, _P, _P, _I, _I, _I, _P, _I, _P]
         lib.oracle_conv2d_mul.argtypes = [_P, _P, _P, _P] + [_I] * 11
+        lib.oracle_linear_shift_backward_data.argtypes = [_P, _P, _P, _I, _I, _I]
+        lib.oracle_conv2d_shift_backward_data.argtypes = [_P, _P, _P] + [_I] * 11
+        lib.oracle_conv2d_shift_backward_data_points.argtypes = [_P, _P] + [_I] * 11 + [_P, _I, _P]
         lib.oracle_pack_codes.argtypes = [_P, _I, _I, _P]
         lib.oracle_unpack_codes.argtypes = [_P, _I, _I, _P]
         lib.oracle_quantize_q.argtypes = [_P, _I, ctypes.c_int, _P]
@@ -149,6 +152,49 @@ def linear_shift_points(x, codes, bias, idx):
     out = np.empty(idx.shape, np.int32)
     _load().oracle_linear_shift_points(_ptr(x), _ptr(codes), _ptr(bias), batch, fin,
                                        codes.shape[0], _ptr(idx), idx.size, _ptr(out))
+    return out
+
+
+def linear_shift_backward_data(dy, codes):
+    """Input gradient of LinearShift: dy [batch, out] int32, codes [out, in] uint8 ->
+    dx [batch, in] = sum_o term(dy[b, o], code[o, i])."""
+    dy = _c(dy, np.int32); codes = _c(codes, np.uint8)
+    batch, fout = dy.shape
+    fout2, fin = codes.shape
+    assert fout == fout2
+    dx = np.empty((batch, fin), np.int32)
+    _load().oracle_linear_shift_backward_data(_ptr(dy), _ptr(codes), _ptr(dx), batch, fin, fout)
+    return dx
+
+
+def conv2d_shift_backward_data(dy, codes, x_shape, r=3, s=None, stride=1, pad=0):
+    """Input gradient of ConvShift: dy [N, K, OH, OW] int32, codes [K, C*R*S] ->
+    dx of the forward input's shape x_shape = (N, C, H, W)."""
+    s = r if s is None else s
+    sh, sw = (stride, stride) if np.isscalar(stride) else stride
+    ph, pw = (pad, pad) if np.isscalar(pad) else pad
+    dy = _c(dy, np.int32); codes = _c(codes, np.uint8)
+    N, C, H, W = x_shape
+    K = codes.shape[0]
+    assert dy.shape == (N, K, out_size(H, ph, r, sh), out_size(W, pw, s, sw))
+    assert codes.size == K * C * r * s
+    dx = np.empty((N, C, H, W), np.int32)
+    _load().oracle_conv2d_shift_backward_data(_ptr(dy), _ptr(codes), _ptr(dx), N, C, H, W, K, r, s,
+                                              sh, sw, ph, pw)
+    return dx
+
+
+def conv2d_shift_backward_data_points(dy, codes, x_shape, idx, r=3, s=None, stride=1, pad=0):
+    """Selected elements dx.flat[idx] of ``conv2d_shift_backward_data``, each gathered alone."""
+    s = r if s is None else s
+    sh, sw = (stride, stride) if np.isscalar(stride) else stride
+    ph, pw = (pad, pad) if np.isscalar(pad) else pad
+    dy = _c(dy, np.int32); codes = _c(codes, np.uint8); idx = _c(idx, np.int64)
+    N, C, H, W = x_shape
+    K = codes.shape[0]
+    out = np.empty(idx.shape, np.int32)
+    _load().oracle_conv2d_shift_backward_data_points(_ptr(dy), _ptr(codes), N, C, H, W, K, r, s,
+                                                     sh, sw, ph, pw, _ptr(idx), idx.size, _ptr(out))
     return out
 
 

@@ -31,6 +31,10 @@
  *     bits [5j, 5j+5), bits 30-31 zero; each weight row starts a new word and
  *     its last word is filled with code 15.
  *
+ * Input gradients (Section 3, backward pass): the same terms applied to the
+ * output gradient and summed over the forward connections (the adjoint), see
+ * oracle_conv2d_shift_backward_data.
+ *
  * The floor is computed by integer division, not by the shift operator, so
  * the oracle does not rely on how C shifts negative numbers.
  *
@@ -43,12 +47,18 @@
  * paper's second form of the ternary sign (sign of round(S)), the
  * nearest-power property, and hand-derived examples. The layers for chained
  * inference at the end are pinned against numpy's int64 arithmetic shift and
- * floor division and torch's max pooling.
+ * floor division and torch's max pooling. The input gradients are pinned
+ * against torch's float64 conv2d input gradient on inputs divisible by 2^15
+ * (closed form), the adjoint identity <W x, g> = <x, W^T g> with exact
+ * integers, a brute-force gather loop in Python, the transposed-codes forward
+ * pass for LinearShift and for stride-1 convolutions, and the one-sided
+ * rounding bound.
  */
 #include <stdint.h>
 #include <limits.h>
 #include <stddef.h>
 #include <math.h>
+#include <stdlib.h>
 
 /* floor(x / 2^c) for 0 <= c <= 14, by integer division (Eq. 1, reading: floor). */
 static int64_t floor_div_pow2(int64_t x, int c)
@@ -168,6 +178,102 @@ void oracle_linear_shift_points(const int32_t *x, const uint8_t *codes, const in
         int64_t acc = bias ? (int64_t)bias[o] : 0;
         for (int64_t j = 0; j < in; ++j)
             acc += oracle_term(x[b * in + j], codes[o * in + j]);
+        out[i] = wrap32(acc);
+    }
+}
+
+/* ---- Input gradients (the data half of the backward pass) ------------------
+ *
+ * Section 3 (DeepShift-Q backward pass, with its footnote): the gradient of the
+ * loss with respect to the operator input is the output gradient multiplied by
+ * the same quantised weights: dX = dY W~ for LinearShift (W~ transposed, in
+ * the footnote's words), and the convolution of dY with W~ rotated by 180
+ * degrees for ConvShift, i.e. the adjoint of the forward convolution. In shift
+ * form each product of an output-gradient value g (fixed point) with a weight
+ * is the same term(g, code) as in the forward pass (floor shift, then the
+ * sign); sums are exact and wrapped once.
+ *
+ * The definition used here is the adjoint written as a scatter: every forward
+ * connection (output (n, k, oh, ow), tap (c, r, s), input (ih, iw)) sends
+ * term(dy[n][k][oh][ow], code[k][c][r][s]) back to dx[n][c][ih][iw]. */
+
+/* dx [batch][in] = sum_o term(dy[b][o], code[o][i]); dy [batch][out]. */
+void oracle_linear_shift_backward_data(const int32_t *dy, const uint8_t *codes, int32_t *dx,
+                                       int64_t batch, int64_t in, int64_t out)
+{
+    #pragma omp parallel for schedule(dynamic, 1)
+    for (int64_t b = 0; b < batch; ++b)
+        for (int64_t i = 0; i < in; ++i) {
+            int64_t acc = 0;
+            for (int64_t o = 0; o < out; ++o)
+                acc += oracle_term(dy[b * out + o], codes[o * in + i]);
+            dx[b * in + i] = wrap32(acc);
+        }
+}
+
+/* dx [N][C][H][W] from dy [N][K][OH][OW] (OH, OW of the forward pass). */
+void oracle_conv2d_shift_backward_data(const int32_t *dy, const uint8_t *codes, int32_t *dx,
+                                       int64_t N, int64_t C, int64_t H, int64_t W, int64_t K,
+                                       int64_t R, int64_t S, int64_t sh, int64_t sw,
+                                       int64_t ph, int64_t pw)
+{
+    int64_t OH = out_dim(H, ph, R, sh), OW = out_dim(W, pw, S, sw);
+    #pragma omp parallel for collapse(2) schedule(dynamic, 1)
+    for (int64_t n = 0; n < N; ++n)
+        for (int64_t c = 0; c < C; ++c) {
+            /* each (n, c) plane of dx is written by this iteration only */
+            int64_t *acc = (int64_t *)calloc((size_t)(H * W), sizeof(int64_t));
+            for (int64_t k = 0; k < K; ++k)
+                for (int64_t oh = 0; oh < OH; ++oh)
+                    for (int64_t ow = 0; ow < OW; ++ow) {
+                        int32_t g = dy[((n * K + k) * OH + oh) * OW + ow];
+                        for (int64_t r = 0; r < R; ++r)
+                            for (int64_t s = 0; s < S; ++s) {
+                                int64_t ih = oh * sh - ph + r, iw = ow * sw - pw + s;
+                                if (ih < 0 || ih >= H || iw < 0 || iw >= W)
+                                    continue;  /* the forward pass read padding here */
+                                acc[ih * W + iw] +=
+                                    oracle_term(g, codes[((k * C + c) * R + r) * S + s]);
+                            }
+                    }
+            for (int64_t i = 0; i < H * W; ++i)
+                dx[(n * C + c) * H * W + i] = wrap32(acc[i]);
+            free(acc);
+        }
+}
+
+/* Selected elements dx.flat[idx[i]] of the input gradient, each gathered on its
+ * own: the taps (r, s) and outputs (oh, ow) with oh*sh - ph + r == ih and
+ * ow*sw - pw + s == iw. */
+void oracle_conv2d_shift_backward_data_points(const int32_t *dy, const uint8_t *codes,
+                                              int64_t N, int64_t C, int64_t H, int64_t W,
+                                              int64_t K, int64_t R, int64_t S, int64_t sh,
+                                              int64_t sw, int64_t ph, int64_t pw,
+                                              const int64_t *idx, int64_t npts, int32_t *out)
+{
+    int64_t OH = out_dim(H, ph, R, sh), OW = out_dim(W, pw, S, sw);
+    (void)N;
+    #pragma omp parallel for schedule(dynamic, 16)
+    for (int64_t i = 0; i < npts; ++i) {
+        int64_t t = idx[i];
+        int64_t iw = t % W; t /= W;
+        int64_t ih = t % H; t /= H;
+        int64_t c = t % C;  t /= C;
+        int64_t n = t;
+        int64_t acc = 0;
+        for (int64_t k = 0; k < K; ++k)
+            for (int64_t r = 0; r < R; ++r) {
+                int64_t a = ih + ph - r;           /* = oh * sh */
+                if (a < 0 || a % sh != 0 || a / sh >= OH)
+                    continue;
+                for (int64_t s = 0; s < S; ++s) {
+                    int64_t b = iw + pw - s;       /* = ow * sw */
+                    if (b < 0 || b % sw != 0 || b / sw >= OW)
+                        continue;
+                    acc += oracle_term(dy[((n * K + k) * OH + a / sh) * OW + b / sw],
+                                       codes[((k * C + c) * R + r) * S + s]);
+                }
+            }
         out[i] = wrap32(acc);
     }
 }

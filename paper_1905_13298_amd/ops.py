@@ -357,6 +357,19 @@ class JitConv:
         cb, seg, sp = ctypes.c_int64(), ctypes.c_int32(), ctypes.c_int32()
         call("ds_jit_conv_query", self._h, ctypes.byref(cb), ctypes.byref(seg), ctypes.byref(sp))
         self.code_bytes, self.segments, self.splits = cb.value, seg.value, sp.value
+        # Workgroups of 256 output pixels that run each code segment.
+        self.pixel_tiles = -(-(n * self.y_shape[2] * self.y_shape[3]) // 256)
+
+    @property
+    def preferred(self) -> bool:
+        """Whether this plan is expected to beat the runtime kernel. Each code
+        segment is straight-line code that a workgroup streams through the
+        instruction cache once; when only one or two pixel tiles share a segment
+        (a LinearShift at small batch) most of that code comes from HBM with no
+        reuse, and on MI355X such plans ran 2.7-5.4x slower than the runtime
+        kernel once the code passed a few MiB, while plans with 4 or more pixel
+        tiles per segment, or under 4 MiB of code, were faster."""
+        return self.pixel_tiles >= 4 or self.code_bytes <= (4 << 20)
 
     def __call__(self, x: torch.Tensor, residual: torch.Tensor | None = None, out=None):
         _dev_i32(x, "x")

@@ -111,13 +111,16 @@ def test_avgpool_matches_oracle(shape):
     np.testing.assert_array_equal(y, oracle.avgpool_global(x))
 
 
-def test_resnet18_forward_matches_oracle():
-    """Every intermediate buffer of a ResNet-18 forward pass (batch 2), bit for bit."""
+@pytest.mark.parametrize("jit", [False, "all"], ids=["runtime", "jit"])
+def test_resnet18_forward_matches_oracle(jit):
+    """Every intermediate buffer of a ResNet-18 forward pass (batch 2), bit for bit,
+    with the runtime kernels and with weight-specialised plans."""
     n = 2
     graph, params = W.resnet18_graph(n), W.resnet18_params(n)
     x = W.gen_images(n)
-    say("resnet18 forward n=2")
-    net = ShiftNetwork(graph, params)
+    say(f"resnet18 forward n=2 jit={jit}")
+    net = ShiftNetwork(graph, params, jit=jit)
+    assert len(net.plans) == (20 if jit else 0)   # every conv but the 7 x 7 stem, and the fc
     got = net.forward(to_dev(x), keep=True)
     want = oracle.network_forward(graph, params, x, keep=True)
     for op in graph:
@@ -126,3 +129,16 @@ def test_resnet18_forward_matches_oracle():
     # a second pass on the same buffers gives the same logits
     again = net.forward(to_dev(x)).cpu().numpy()
     np.testing.assert_array_equal(again, want["logits"])
+
+
+def test_resnet18_forward_jit_full_batch_equals_runtime():
+    """Batch 32 (the benchmark's): the logits and every block output of the plans'
+    forward pass equal the runtime kernels' bit for bit."""
+    n = 32
+    graph, params = W.resnet18_graph(n), W.resnet18_params(n)
+    x = to_dev(W.gen_images(n))
+    say("resnet18 forward n=32 jit vs runtime")
+    a = ShiftNetwork(graph, params).forward(x, keep=True)
+    b = ShiftNetwork(graph, params, jit=True).forward(x, keep=True)
+    for op in graph:
+        assert torch.equal(a[op["dst"]], b[op["dst"]]), op["dst"]

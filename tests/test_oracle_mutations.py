@@ -10,6 +10,7 @@ import shutil
 
 import pytest
 
+import tests.test_oracle_backward_pins as bpins
 import tests.test_oracle_convert_pins as cpins
 import tests.test_oracle_layer_pins as lpins
 import tests.test_oracle_pins as pins
@@ -27,7 +28,8 @@ MUTATIONS = {
     "sign_ignored": ("return negative ? -t : t;", "return t;"),
     "conv_bias_dropped": ("int64_t acc = bias ? (int64_t)bias[k] : 0;\n    for (int64_t c = 0; c < C; ++c)\n        for (int64_t r",
                           "int64_t acc = 0;\n    for (int64_t c = 0; c < C; ++c)\n        for (int64_t r"),
-    "kernel_r_s_transposed": ("codes[((k * C + c) * R + r) * S + s]", "codes[((k * C + c) * S + s) * R + r]"),
+    "kernel_r_s_transposed": ("uint8_t code = codes[((k * C + c) * R + r) * S + s];",
+                              "uint8_t code = codes[((k * C + c) * S + s) * R + r];"),
     "input_h_w_transposed": ("int32_t xv = x[((n * C + c) * H + ih) * W + iw];",
                              "int32_t xv = x[((n * C + c) * W + iw) * H + ih];"),
     "stride_h_w_swapped": ("int64_t ih = oh * sh - ph + r;", "int64_t ih = oh * sw - ph + r;"),
@@ -62,6 +64,20 @@ MUTATIONS = {
     "maxpool_padding_as_zero": ("if (ih < 0 || ih >= H || iw < 0 || iw >= W)\n                                continue;\n                            int64_t v = x[",
                                 "int64_t v = (ih < 0 || ih >= H || iw < 0 || iw >= W) ? 0 : x["),
     "avgpool_truncates": ("if (sum % HW != 0 && sum < 0)\n            q -= 1;", ""),
+    # input gradients
+    "bwd_window_not_rotated": ("int64_t ih = oh * sh - ph + r, iw = ow * sw - pw + s;\n                                if (ih < 0 || ih >= H || iw < 0 || iw >= W)\n                                    continue;  /* the forward pass read padding here */",
+                               "int64_t ih = oh * sh - ph + (R - 1 - r), iw = ow * sw - pw + (S - 1 - s);\n                                if (ih < 0 || ih >= H || iw < 0 || iw >= W)\n                                    continue;  /* the forward pass read padding here */"),
+    "bwd_channels_transposed": ("oracle_term(g, codes[((k * C + c) * R + r) * S + s]);",
+                                "oracle_term(g, codes[(((c * K + k) % (K * C)) * R + r) * S + s]);"),
+    "bwd_stride_ignored": ("int64_t ih = oh * sh - ph + r, iw = ow * sw - pw + s;\n                                if (ih < 0 || ih >= H || iw < 0 || iw >= W)\n                                    continue;  /* the forward pass read padding here */",
+                           "int64_t ih = oh - ph + r, iw = ow - pw + s;\n                                if (ih < 0 || ih >= H || iw < 0 || iw >= W)\n                                    continue;  /* the forward pass read padding here */"),
+    "bwd_pad_sign": ("int64_t ih = oh * sh - ph + r, iw = ow * sw - pw + s;\n                                if (ih < 0 || ih >= H || iw < 0 || iw >= W)\n                                    continue;  /* the forward pass read padding here */",
+                     "int64_t ih = oh * sh + ph - r, iw = ow * sw + pw - s;\n                                if (ih < 0 || ih >= H || iw < 0 || iw >= W)\n                                    continue;  /* the forward pass read padding here */"),
+    "bwd_last_output_row_dropped": ("for (int64_t oh = 0; oh < OH; ++oh)\n                    for (int64_t ow = 0; ow < OW; ++ow) {\n                        int32_t g",
+                                    "for (int64_t oh = 0; oh < OH - 1; ++oh)\n                    for (int64_t ow = 0; ow < OW; ++ow) {\n                        int32_t g"),
+    "bwd_linear_codes_not_transposed": ("acc += oracle_term(dy[b * out + o], codes[o * in + i]);",
+                                        "acc += oracle_term(dy[b * out + o], codes[(i * out + o) % (in * out)]);"),
+    "bwd_points_divisibility_ignored": ("if (a < 0 || a % sh != 0 || a / sh >= OH)", "if (a < 0 || a / sh >= OH)"),
 }
 
 LAYER_CHECKS = [
@@ -82,6 +98,14 @@ CONVERT_CHECKS = [
     (cpins.test_ps_nan_gives_zero_weight, ()),
     *[(cpins.test_fixed_matches_exact_rounding, (f,)) for f in (16, 31)],
     (cpins.test_golden_examples, ()),
+]
+
+BACKWARD_CHECKS = [
+    *[(bpins.test_closed_form_matches_torch_input_gradient, (s,)) for s in bpins.SHAPES],
+    (bpins.test_linear_closed_form_matches_matmul, ()),
+    (bpins.test_bruteforce_tiny, (0,)),
+    (bpins.test_linear_equals_forward_with_transposed_codes, ()),
+    (bpins.test_points_agree_with_full, ()),
 ]
 
 CHECKS = [
@@ -124,8 +148,9 @@ def test_pins_catch_mutation(tmp_path, monkeypatch, name):
     monkeypatch.setattr(pins, "oracle", mod)
     monkeypatch.setattr(cpins, "oracle", mod)
     monkeypatch.setattr(lpins, "oracle", mod)
+    monkeypatch.setattr(bpins, "oracle", mod)
     failed = []
-    for fn, args in CHECKS + CONVERT_CHECKS + LAYER_CHECKS:
+    for fn, args in CHECKS + CONVERT_CHECKS + LAYER_CHECKS + BACKWARD_CHECKS:
         try:
             fn(*args)
         except AssertionError:
@@ -145,5 +170,6 @@ def test_unmutated_copy_passes(tmp_path, monkeypatch):
     monkeypatch.setattr(pins, "oracle", mod)
     monkeypatch.setattr(cpins, "oracle", mod)
     monkeypatch.setattr(lpins, "oracle", mod)
-    for fn, args in CHECKS + CONVERT_CHECKS + LAYER_CHECKS:
+    monkeypatch.setattr(bpins, "oracle", mod)
+    for fn, args in CHECKS + CONVERT_CHECKS + LAYER_CHECKS + BACKWARD_CHECKS:
         fn(*args)
