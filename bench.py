@@ -44,6 +44,9 @@ CONVERT_WORKLOADS = {"convert_resnet50": 4}
 # Chained inference: a ResNet-18 forward pass with shift convolutions (batch
 # normalisation, residual and ReLU fused into each convolution), N = 32.
 NETWORK_WORKLOADS = {"resnet18_infer": 32}
+# Input gradients (the data half of the backward pass) of every layer of a
+# workload but the stem (the images need no gradient), on signed output gradients.
+BACKWARD_WORKLOADS = {"resnet50_bwd_data": 4, "resnet18_bwd_data": 3}
 
 # MI355X: 256 CUs at 2.4 GHz. Three-operand (VOP3) integer instructions such as
 # v_xad_u32 run 64 lanes per CU per clock; two-operand (VOP2) ones such as
@@ -77,7 +80,8 @@ def parse():
     ap.add_argument("--gpus", type=int, default=1)
     ap.add_argument("--steps", type=int, default=5)
     ap.add_argument("--warmup", type=int, default=2)
-    ap.add_argument("--workload", default="resnet50", choices=sorted(WORKLOADS) + sorted(CONVERT_WORKLOADS) + sorted(NETWORK_WORKLOADS))
+    ap.add_argument("--workload", default="resnet50", choices=sorted(WORKLOADS) + sorted(CONVERT_WORKLOADS) + sorted(NETWORK_WORKLOADS)
+                    + sorted(BACKWARD_WORKLOADS))
     ap.add_argument("--cpu-batch", type=int, default=None,
                     help="batch of the oracle sample (default: sized for ~10-30 s)")
     ap.add_argument("--cpu-seconds", type=float, default=10.0,
@@ -436,6 +440,107 @@ def bench_network(args):
     print(json.dumps(out), flush=True)
 
 
+def gen_grad(L, seed: int, index: int) -> np.ndarray:
+    """Signed output gradient of a layer: rint(N(0, 1) * 2^16), int32 (F = 16)."""
+    rng = np.random.default_rng([seed, index, 7])
+    return np.rint(rng.standard_normal(L.y_shape, dtype=np.float32) * 65536.0).astype(np.int32)
+
+
+def bench_backward(args):
+    """One step = the input gradient of every layer (the stem aside) on its own
+    seeded output gradient, all resident in HBM; dense shift-accumulates as for the
+    forward pass (one term per forward connection)."""
+    import torch
+    from paper_1905_13298_amd import ops
+    from paper_1905_13298_amd import workloads as W
+
+    cfg = BACKWARD_WORKLOADS[args.workload]
+    seed = W.CONFIG_SEEDS[cfg]
+    layers = [(li, L) for li, L in enumerate(W.config_layers(cfg)) if L.name != "conv1"]
+    dev = torch.device("cuda:0")
+    torch.cuda.set_device(dev)
+    stream = torch.cuda.current_stream(dev)
+    calls, plans = [], []
+    for li, L in layers:
+        codes = W.gen_codes(L, seed, li)
+        wp = torch.from_numpy(ops.pack_shift_weights(codes).view(np.int32)).to(dev)
+        dy = torch.from_numpy(gen_grad(L, seed, li)).to(dev)
+        dx = torch.empty(L.x_shape, dtype=torch.int32, device=dev)
+        if L.kind == "linear":
+            calls.append(lambda dy=dy, wp=wp, dx=dx, L=L: ops.linear_shift_backward_data(dy, wp, L.c, out=dx))
+            plans.append(ops.describe_conv2d_backward_data(L.n, L.c, 1, 1, L.k, 1))
+        else:
+            calls.append(lambda dy=dy, wp=wp, dx=dx, L=L: ops.conv2d_shift_backward_data(
+                dy, wp, L.x_shape, (L.r, L.s), L.stride, L.pad, out=dx))
+            plans.append(ops.describe_conv2d_backward_data(*L.x_shape, L.k, (L.r, L.s), L.stride, L.pad))
+    torch.cuda.synchronize()
+    ms_per_step, d = time_layers(calls, args.steps, args.warmup, stream)
+    sac_step = sum(L.sac for _, L in layers)
+    value = sac_step / (ms_per_step * 1e-3) / 1e9
+    groups = {}
+    for i, (li, L) in enumerate(layers):
+        g = groups.setdefault(plans[i], {"sac": 0, "ms": 0.0, "launches": 0, "bytes": 0})
+        g["sac"] += L.sac
+        g["ms"] += float(d[:, i].mean())
+        g["launches"] += 1
+        g["bytes"] += algorithmic_bytes(L)
+    name, g = max(groups.items(), key=lambda kv: kv[1]["ms"])
+    achieved = g["sac"] / (g["ms"] * 1e-3) / 1e12
+    roofline = {"bound": "alu", "achieved": round(achieved, 4), "peak": round(SAC_PEAK_T, 4),
+                "unit": "TSAC/s", "frac": round(achieved / SAC_PEAK_T, 4), "traffic": None,
+                "kernel": name, "launches_per_step": g["launches"],
+                "avg_launch_ms": round(g["ms"] / g["launches"], 5),
+                "sac_per_launch_avg": g["sac"] // g["launches"],
+                "algorithmic_bytes_per_launch": g["bytes"] // g["launches"],
+                "work_unit": "dense shift-accumulate, 2 int32 VALU ops each (3 on chunks holding a negative value)",
+                "timed_span": "library call per layer (code re-pack, weight decode, fill, phase kernels)"}
+    per_layer = [{"layer": L.name, "plan": plans[i], "sac": L.sac,
+                  "ms_median": float(np.median(d[:, i])),
+                  "gsac_s": L.sac / (float(np.median(d[:, i])) * 1e-3) / 1e9}
+                 for i, (li, L) in enumerate(layers)]
+    cpu = None
+    if not args.no_cpu_baseline:
+        import oracle
+        del calls
+        torch.cuda.empty_cache()
+        nb = 2
+        t_total, s_total, passes = 0.0, 0, 0
+        while True:
+            for li, L in layers:
+                Ls = L.with_batch(min(nb, L.n))
+                codes = W.gen_codes(L, seed, li)
+                dy = gen_grad(Ls, seed, li)
+                t = time.perf_counter()
+                if L.kind == "linear":
+                    oracle.linear_shift_backward_data(dy, codes)
+                else:
+                    oracle.conv2d_shift_backward_data(dy, codes, Ls.x_shape, r=L.r, s=L.s,
+                                                      stride=L.stride, pad=L.pad)
+                t_total += time.perf_counter() - t
+                s_total += Ls.sac
+            passes += 1
+            if t_total >= args.cpu_seconds:
+                break
+        cpu = {"value": round(s_total / t_total / 1e9, 3), "unit": "GSAC/s", "cores": oracle.max_threads(),
+               "kind": "oracle", "sample": f"{passes} pass(es) over the layers at batch {nb} "
+                                           f"({s_total / 1e9:.2f} G SAC, {t_total:.1f} s)"}
+    out = {
+        "metric": "G shift-accumulates/s of the input gradient (backward data) per layer on one MI355X",
+        "value": round(value, 2), "unit": "GSAC/s", "n_gpus": 1, "steps": args.steps,
+        "warmup": args.warmup, "ms_per_step": round(ms_per_step, 4), "higher_is_better": True,
+        "scaling": "weak", "vs_baseline": None, "dtype": "i32", "data": "synthetic",
+        "frac_sac_peak": round(value / 1000.0 / SAC_PEAK_T, 4),
+        "config": {"workload": W.CONFIG_NAMES[cfg] + "_backward_data", "layers": len(layers),
+                   "batch": layers[0][1].n, "frac_bits": W.FRAC_BITS, "sac_per_step": sac_step,
+                   "grad": "rint(N(0,1) * 2^16), signed", "parallelism": "single GPU"},
+        "roofline": roofline, "cpu_baseline": cpu,
+    }
+    if args.layers_out:
+        with open(args.layers_out, "w") as f:
+            json.dump({"workload": args.workload, "layers": per_layer}, f, indent=1)
+    print(json.dumps(out), flush=True)
+
+
 def main():
     args = parse()
     if args.copy_only:
@@ -458,6 +563,9 @@ def main():
         return
     if args.workload in NETWORK_WORKLOADS:
         bench_network(args)
+        return
+    if args.workload in BACKWARD_WORKLOADS:
+        bench_backward(args)
         return
 
     bench_layers(args)

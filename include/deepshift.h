@@ -206,6 +206,52 @@ ds_status ds_maxpool2d(const int32_t *x, int32_t *y, int64_t n, int64_t c, int64
 ds_status ds_avgpool2d_global(const int32_t *x, int32_t *y, int64_t n, int64_t c, int64_t h,
                               int64_t w, uint32_t flags, void *stream);
 
+/* Input gradients (Section 3, the DeepShift backward pass): the gradient of
+ * the loss with respect to an operator's input is the output gradient times
+ * the same quantised weights -- transposed for LinearShift, and for ConvShift
+ * the convolution of dY with the weights rotated by 180 degrees (the adjoint
+ * of the forward convolution). In shift form every product of an output
+ * gradient value g with a weight is term(g, code) as in the forward pass, so
+ * the result is exact integer arithmetic like the forward one:
+ *     dx[n][c][ih][iw] = sum over k, oh, ow, r, s with oh*stride_h - pad_h + r == ih
+ *                        and ow*stride_w - pad_w + s == iw of
+ *                        term(dy[n][k][oh][ow], code[k][c][r][s])      (mod 2^32)
+ * dy and dx carry the same F (frac_bits, validated and not used by the math).
+ *
+ * ds_conv2d_shift_backward_data: the arguments describe the FORWARD layer
+ * (n, c, h, w, k, r, s, stride, padding as for ds_conv2d_shift).
+ * dy       device int32 [n][k][oh][ow] (oh, ow of the forward pass)
+ * w_packed device uint32, the forward layer's packed weights [k][ds_packed_row_words(c*r*s)]
+ * dx       device int32 [n][c][h][w], written (not accumulated); must not overlap dy or w_packed
+ * flags    must be 0; stream as for ds_linear_shift.
+ * Device scratch (re-packed codes per stride phase, decoded weights) comes from
+ * the library's stream-ordered pool, as for the forward operators.
+ * Errors as for ds_conv2d_shift. */
+ds_status ds_conv2d_shift_backward_data(const int32_t *dy, const uint32_t *w_packed, int32_t *dx,
+                                        int64_t n, int64_t c, int64_t h, int64_t w, int64_t k,
+                                        int64_t r, int64_t s, int32_t stride_h, int32_t stride_w,
+                                        int32_t pad_h, int32_t pad_w, int32_t frac_bits,
+                                        uint32_t flags, void *stream);
+
+/* LinearShift input gradient: dx[b][i] = sum_o term(dy[b][o], code[o][i]) (mod 2^32).
+ * dy device int32 [batch][out_features]; w_packed the forward layer's
+ * [out_features][ds_packed_row_words(in_features)]; dx device int32
+ * [batch][in_features], written. Other arguments and errors as above. */
+ds_status ds_linear_shift_backward_data(const int32_t *dy, const uint32_t *w_packed, int32_t *dx,
+                                        int64_t batch, int64_t in_features, int64_t out_features,
+                                        int32_t frac_bits, uint32_t flags, void *stream);
+
+/* Names, without launching anything, what ds_conv2d_shift_backward_data runs
+ * for a forward layer of this shape: "direct" (one thread per dx element), or
+ * "phases<P>" followed by each stride phase's window and kernel (a phase whose
+ * rows or columns no tap reaches is "zero"). Arguments as for
+ * ds_conv2d_shift_describe. For profiling and tests. */
+ds_status ds_conv2d_shift_backward_data_describe(int64_t n, int64_t c, int64_t h, int64_t w,
+                                                 int64_t k, int64_t r, int64_t s,
+                                                 int32_t stride_h, int32_t stride_w,
+                                                 int32_t pad_h, int32_t pad_w, char *buf,
+                                                 int64_t len);
+
 /* Multiplication-based comparison operators. Not part of DeepShift: they run
  * the same tiling as the shift operators with a 32-bit integer multiply in
  * place of the shift, so that the two inner loops can be timed side by side

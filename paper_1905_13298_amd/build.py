@@ -24,7 +24,7 @@ HIP_FLAGS = ["-O3", "-std=c++17", f"--offload-arch={ARCH}", "-fPIC", "-Wall",
              "-I", INCLUDE, "-I", CSRC]
 CXX_FLAGS = ["-O2", "-std=c++17", "-fPIC", "-Wall", "-Wextra", "-I", INCLUDE, "-I", CSRC]
 
-HIP_SOURCES = ["shift_ops.hip", "conv_kernels.hip", "convert.hip", "pool.hip", "jit.hip"]
+HIP_SOURCES = ["shift_ops.hip", "conv_kernels.hip", "convert.hip", "pool.hip", "jit.hip", "backward.hip"]
 CXX_SOURCES = ["pack.cpp"]
 LLVM = "/opt/rocm/llvm/bin"
 

@@ -49,7 +49,7 @@ int forced_variant()
 // Scratch memory: stream-ordered allocations from one pool per device that
 // keeps freed memory for reuse.
 
-static hipError_t scratch_alloc(void **p, size_t bytes, hipStream_t st)
+hipError_t scratch_alloc(void **p, size_t bytes, hipStream_t st)
 {
     static std::mutex mu;
     static hipMemPool_t pools[64] = {};
@@ -189,6 +189,24 @@ fill_init_kernel(const int32_t *__restrict__ init, int32_t *__restrict__ y, int6
         y[idx] = init[(idx / OHOW) % K];
 }
 
+// y[map(n, k, oh, ow)] = init[k] (0 without init) over a problem's output grid.
+__global__ void __launch_bounds__(256)
+fill_mapped_kernel(const int32_t *__restrict__ init, int32_t *__restrict__ y, int64_t total, int K,
+                   int OH, int OW, OutMap m)
+{
+    for (int64_t idx = int64_t(blockIdx.x) * blockDim.x + threadIdx.x; idx < total;
+         idx += int64_t(gridDim.x) * blockDim.x) {
+        const int ow = int(idx % OW);
+        int64_t t = idx / OW;
+        const int oh = int(t % OH);
+        t /= OH;
+        const int k = int(t % K);
+        const int64_t n = t / K;
+        y[m.base + n * m.nstride + int64_t(k) * m.kstride + int64_t(oh) * m.rstride +
+          int64_t(ow) * m.cstride] = init ? init[k] : 0;
+    }
+}
+
 // The epilogue on one output value v of channel k at flat index o.
 __device__ __forceinline__ uint32_t apply_epilogue(uint32_t v, int k, int64_t o, const Epilogue &e)
 {
@@ -267,6 +285,8 @@ struct TiledParams {
     int tiles_p, tiles_k, chunks_per_split, nchunks;
     int atomic_out;     // split-K: add partial sums atomically into y
     int fuse_epi;       // apply the epilogue in the kernel (not split, not transposed)
+    // Output placement: y[ybase + n*ynst + k*ykst + oh*yrst + ow*ycst] (see OutMap).
+    int ybase, ynst, ykst, yrst, ycst;
     Epilogue epi;
     int x_bytes;        // size of x in bytes (< 2^31)
     FastDiv div_ohow, div_ow, div_vh, div_iwp;
@@ -419,7 +439,7 @@ tiled_kernel(const int32_t *__restrict__ x, const int32_t *__restrict__ wd,
             const int pix = q - n * p.OHOW;
             const int oh = fdiv(pix, p.div_ow);
             const int ow = pix - oh * p.OW;
-            yoff[i] = n * p.K * p.OHOW + pix;
+            yoff[i] = p.ybase + n * p.ynst + oh * p.yrst + ow * p.ycst;
             if constexpr (MODE == MODE_WINDOW)
                 base[i] = (n * p.VH + oh * p.sh - vbase) * p.IWP + ow * p.sw;
             if constexpr (MODE == MODE_POINT)
@@ -534,7 +554,7 @@ tiled_kernel(const int32_t *__restrict__ x, const int32_t *__restrict__ wd,
 #pragma unroll
         for (int i = 0; i < TM; ++i) {
             if (yoff[i] < 0) continue;
-            const int o = yoff[i] + k * p.OHOW;
+            const int o = yoff[i] + k * p.ykst;
             if (p.atomic_out)
                 atomicAdd(reinterpret_cast<unsigned int *>(y) + o, acc[i][t]);
             else if (p.fuse_epi)
@@ -633,11 +653,23 @@ static hipError_t run_direct(const ConvGeom &g, const int32_t *x, const uint32_t
     return hipGetLastError();
 }
 
+// Padded input extents of the window mode for g.
+static void padded_dims(const ConvGeom &g, const Padded &pad, int &VH, int &IWP)
+{
+    VH = pad.vh > 0 ? pad.vh : g.h + 2 * g.ph;
+    IWP = pad.iwp > 0 ? pad.iwp : g.w + 2 * g.pw;
+}
+
 // Picks the tiled instance for a problem: v.mode < 0 when none fits.
-static Variant choose_variant(const ConvGeom &g, int &plane, size_t &lds)
+static Variant choose_variant(const ConvGeom &g, const Padded &pad, int &plane, size_t &lds)
 {
     const int64_t NQ = int64_t(g.n) * g.oh * g.ow;
-    const bool point = g.r == 1 && g.s == 1 && g.ph == 0 && g.pw == 0;
+    // Pointwise staging reads input pixel (oh*sh, ow*sw) with no bounds check of its
+    // own, so the output grid must stay inside the input (always so for a 1x1
+    // window without padding and the usual output size).
+    const bool point = g.r == 1 && g.s == 1 && g.ph == 0 && g.pw == 0 &&
+                       g.oh <= (g.h - 1) / g.sh + 1 && g.ow <= (g.w - 1) / g.sw + 1 &&
+                       pad.vh <= 0 && pad.iwp <= 0;
     plane = 0;
     lds = 0;
     const int fv = forced_variant();
@@ -646,7 +678,8 @@ static Variant choose_variant(const ConvGeom &g, int &plane, size_t &lds)
         lds = size_t(2) * 8 * 64 * tm * 4;
         return Variant{MODE_POINT, tm, 8, 1, 0};
     }
-    const int VH = g.h + 2 * g.ph, IWP = g.w + 2 * g.pw;
+    int VH = 0, IWP = 0;
+    padded_dims(g, pad, VH, IWP);
     const int order[2][2] = {{4, 8}, {8, 4}};
     for (int tm : order[fv == 8 ? 1 : 0]) {
         const int rows = window_rows_max(g, 64 * tm, VH);
@@ -709,6 +742,14 @@ static bool use_direct(const ConvGeom &g, const Variant &v)
     return v.mode < 0 || x_bytes >= (int64_t(1) << 31) || forced_variant() == 0;
 }
 
+bool tiled_fits(const ConvGeom &g, const Padded &pad)
+{
+    int plane = 0;
+    size_t lds = 0;
+    const Variant v = choose_variant(g, pad, plane, lds);
+    return !use_direct(g, v);
+}
+
 // A problem on 1 x 1 inputs with 1 x 1 taps (LinearShift, x [n][c]) runs on the
 // transposed input x^T [c][n] as one image of width n, so that the copies into
 // LDS read consecutive words, and produces y^T [k][n], whose stores (and
@@ -733,7 +774,7 @@ void describe_conv(const ConvGeom &g0, char *buf, size_t len)
     const ConvGeom g = tiled_geometry(g0, rowmajor);
     int plane = 0;
     size_t lds = 0;
-    const Variant v = choose_variant(g, plane, lds);
+    const Variant v = choose_variant(g, Padded(), plane, lds);
     if (use_direct(g, v)) {
         snprintf(buf, len, "direct");
         return;
@@ -758,6 +799,24 @@ hipError_t run_fill_init(const ConvGeom &g, const int32_t *init, int32_t *y, hip
     return hipGetLastError();
 }
 
+hipError_t run_fill_mapped(const ConvGeom &g, const int32_t *init, int32_t *y, const OutMap &map,
+                           hipStream_t st)
+{
+    if (map.dense() && init) return run_fill_init(g, init, y, st);
+    OutMap m = map;
+    if (m.dense()) {
+        m.kstride = g.oh * g.ow;
+        m.nstride = g.k * m.kstride;
+        m.rstride = g.ow;
+        m.cstride = 1;
+    }
+    const int64_t total = int64_t(g.n) * g.k * g.oh * g.ow;
+    const int grid = int(std::min<int64_t>((total + 255) / 256, 8192));
+    hipLaunchKernelGGL(fill_mapped_kernel, dim3(grid), dim3(256), 0, st, init, y, total, g.k, g.oh,
+                       g.ow, m);
+    return hipGetLastError();
+}
+
 hipError_t run_epilogue(const ConvGeom &g, int32_t *y, const Epilogue &epi, hipStream_t st)
 {
     const int64_t total = int64_t(g.n) * g.k * g.oh * g.ow;
@@ -768,18 +827,24 @@ hipError_t run_epilogue(const ConvGeom &g, int32_t *y, const Epilogue &epi, hipS
 }
 
 hipError_t run_conv(const ConvGeom &g0, const int32_t *x, const uint32_t *wp, const int32_t *wi,
-                    const int32_t *bias, int32_t *y, Inner op, hipStream_t st, const Epilogue &epi)
+                    const int32_t *bias, int32_t *y, Inner op, hipStream_t st, const Epilogue &epi,
+                    const OutMap &map, const Padded &pad)
 {
+    // A strided output map or custom padded extents come only from the
+    // input-gradient phases: tiled kernel, no epilogue, no transposition.
+    const bool mapped = !map.dense() || pad.vh > 0 || pad.iwp > 0;
     bool rowmajor = false;
-    const ConvGeom g = tiled_geometry(g0, rowmajor);
+    const ConvGeom g = mapped ? g0 : tiled_geometry(g0, rowmajor);
     const int64_t x_bytes = int64_t(g.n) * g.c * g.h * g.w * 4;
     int plane = 0;
     size_t lds = 0;
-    const Variant v = choose_variant(g, plane, lds);
+    const Variant v = choose_variant(g, pad, plane, lds);
     if (use_direct(g, v)) {
+        if (mapped) return hipErrorInvalidValue;
         const hipError_t e = run_direct(g0, x, wp, wi, bias, y, op, st);
         return e == hipSuccess && epi.any() ? run_epilogue(g0, y, epi, st) : e;
     }
+    if (mapped && epi.any()) return hipErrorInvalidValue;
 
     const int RS = g.r * g.s;
     int tiles_p, tiles_k, nchunks, splits, cps;
@@ -794,7 +859,10 @@ hipError_t run_conv(const ConvGeom &g0, const int32_t *x, const uint32_t *wp, co
     p.N = g.n; p.C = g.c; p.H = g.h; p.W = g.w; p.K = g.k; p.R = g.r; p.S = g.s;
     p.sh = g.sh; p.sw = g.sw; p.ph = g.ph; p.pw = g.pw; p.OH = g.oh; p.OW = g.ow;
     p.OHOW = g.oh * g.ow; p.NQ = int(NQ); p.HW = g.h * g.w;
-    p.Jpad = Jpad; p.VH = g.h + 2 * g.ph; p.IWP = g.w + 2 * g.pw; p.PLANE = plane;
+    p.Jpad = Jpad; p.PLANE = plane;
+    padded_dims(g, pad, p.VH, p.IWP);
+    const OutMap m = map.dense() ? OutMap{0, g.k * g.oh * g.ow, g.oh * g.ow, g.ow, 1} : map;
+    p.ybase = int(m.base); p.ynst = m.nstride; p.ykst = m.kstride; p.yrst = m.rstride; p.ycst = m.cstride;
     p.tiles_p = tiles_p; p.tiles_k = tiles_k; p.chunks_per_split = cps; p.nchunks = nchunks;
     p.atomic_out = splits > 1;
     p.fuse_epi = epi.any() && !p.atomic_out && !rowmajor;
@@ -839,13 +907,7 @@ hipError_t run_conv(const ConvGeom &g0, const int32_t *x, const uint32_t *wp, co
         hipLaunchKernelGGL((prep_kernel<Inner::Mul, kTN>), dim3(pgrid), dim3(256), 0, st, wp, wi,
                            bias, g.k, g.crs, wpr, Jpad, Kpad, wblocks, wd, init);
     e = hipGetLastError();
-    if (e == hipSuccess && p.atomic_out) {
-        const int64_t total = int64_t(g.n) * g.k * p.OHOW;
-        const int fgrid = int(std::min<int64_t>((total + 255) / 256, 8192));
-        hipLaunchKernelGGL(fill_init_kernel, dim3(fgrid), dim3(256), 0, st, init, yout, total, g.k,
-                           p.OHOW);
-        e = hipGetLastError();
-    }
+    if (e == hipSuccess && p.atomic_out) e = run_fill_mapped(g, init, yout, map, st);
     if (e == hipSuccess) {
         e = op == Inner::Shift
                 ? dispatch_tiled<Inner::Shift>(v, p, int(grid), lds, xin, wd, init, yout, st)

@@ -31,15 +31,45 @@ struct Epilogue {
     bool any() const { return mul || res || relu; }
 };
 
+// Where output (n, k, oh, ow) of a problem lands in y:
+//     y[base + n * nstride + k * kstride + oh * rstride + ow * cstride]
+// The default (all zero) is the dense NCHW layout of the problem's own output.
+// A strided map lets one problem fill a regular sub-grid of a larger tensor
+// (the stride phases of an input gradient).
+struct OutMap {
+    int64_t base = 0;
+    int nstride = 0, kstride = 0, rstride = 0, cstride = 0;
+    bool dense() const { return nstride == 0; }
+};
+
+// Padded extents of the input in the window staging mode: `vh` rows (top
+// padding ph, then h rows, then whatever bottom padding reaches vh) and `iwp`
+// columns per row. Zero means the symmetric default h + 2 ph, w + 2 pw.
+struct Padded {
+    int vh = 0, iwp = 0;
+};
+
 // Enqueue the whole computation of y on `stream`. Exactly one of `wpacked`
-// (Shift) and `wint` (Mul) is used.
+// (Shift) and `wint` (Mul) is used. g.oh and g.ow give the output grid; with
+// the defaults of `map` and `pad` they must be the usual output sizes.
 hipError_t run_conv(const ConvGeom &g, const int32_t *x, const uint32_t *wpacked,
                     const int32_t *wint, const int32_t *bias, int32_t *y, Inner op,
-                    hipStream_t stream, const Epilogue &epi = Epilogue());
+                    hipStream_t stream, const Epilogue &epi = Epilogue(),
+                    const OutMap &map = OutMap(), const Padded &pad = Padded());
+
+// Whether run_conv runs g (with `pad`) on the tiled kernel rather than the
+// one-thread-per-output kernel.
+bool tiled_fits(const ConvGeom &g, const Padded &pad);
+
+// Stream-ordered device scratch from the library's memory pool.
+hipError_t scratch_alloc(void **p, size_t bytes, hipStream_t stream);
 
 // y[n][k][p] = init[k] (the start of split-K accumulation), and the epilogue as
 // a pass of its own over y, both enqueued on `stream`.
 hipError_t run_fill_init(const ConvGeom &g, const int32_t *init, int32_t *y, hipStream_t stream);
+// The same through a map; init == NULL writes zeros.
+hipError_t run_fill_mapped(const ConvGeom &g, const int32_t *init, int32_t *y, const OutMap &map,
+                           hipStream_t stream);
 hipError_t run_epilogue(const ConvGeom &g, int32_t *y, const Epilogue &epi, hipStream_t stream);
 
 // Short name of the kernel run_conv would launch for g (see ds_conv2d_shift_describe).

@@ -17,7 +17,8 @@ __all__ = ["DeepShiftError", "describe_conv2d", "packed_row_words", "pack_shift_
            "linear_shift", "conv2d_shift", "linear_mul_i32", "conv2d_mul_i32", "out_size",
            "quantize_shift_weights_q", "quantize_shift_weights_q_many", "quantize_shift_weights_ps",
            "to_fixed_point", "conv2d_shift_fused", "maxpool2d", "avgpool2d_global", "DS_RELU",
-           "DS_JIT_RESIDUAL", "JitConv", "jit_conv_image"]
+           "DS_JIT_RESIDUAL", "JitConv", "jit_conv_image", "conv2d_shift_backward_data",
+           "linear_shift_backward_data", "describe_conv2d_backward_data"]
 
 DS_RELU = 1
 
@@ -54,6 +55,17 @@ def describe_conv2d(n, c, h, w, k, kernel_size, stride=1, padding=0) -> str:
     import ctypes
     buf = ctypes.create_string_buffer(128)
     call("ds_conv2d_shift_describe", n, c, h, w, k, r, s, sh, sw, ph, pw, buf, len(buf))
+    return buf.value.decode()
+
+
+def describe_conv2d_backward_data(n, c, h, w, k, kernel_size, stride=1, padding=0) -> str:
+    """What the library runs for the input gradient of this forward ConvShift shape."""
+    r, s = _pair(kernel_size)
+    sh, sw = _pair(stride)
+    ph, pw = _pair(padding)
+    import ctypes
+    buf = ctypes.create_string_buffer(512)
+    call("ds_conv2d_shift_backward_data_describe", n, c, h, w, k, r, s, sh, sw, ph, pw, buf, len(buf))
     return buf.value.decode()
 
 
@@ -131,6 +143,39 @@ def conv2d_shift(x: torch.Tensor, w_packed: torch.Tensor, bias: torch.Tensor | N
         call("ds_conv2d_shift", _ptr(x), _ptr(w_packed), _ptr(bias), _ptr(y), n, c, h, w, k, r, s,
              sh, sw, ph, pw, frac_bits, DS_RELU if relu else 0, _stream(x.device))
     return y
+
+
+def conv2d_shift_backward_data(dy: torch.Tensor, w_packed: torch.Tensor, x_shape, kernel_size,
+                               stride=1, padding=0, frac_bits: int = 16,
+                               out: torch.Tensor | None = None) -> torch.Tensor:
+    """Input gradient of a ConvShift layer (NCHW): dx[n, c, ih, iw] = sum of
+    term(dy[n, k, oh, ow], code[k, c, r, s]) over the forward connections. x_shape =
+    (n, c, h, w) of the forward input; dy has the forward output's shape."""
+    _dev_i32(dy, "dy"); _dev_i32(w_packed, "w_packed")
+    r, s = _pair(kernel_size)
+    sh, sw = _pair(stride)
+    ph, pw = _pair(padding)
+    n, c, h, w = (int(v) for v in x_shape)
+    k = w_packed.shape[0]
+    dx = out if out is not None else torch.empty((n, c, h, w), dtype=torch.int32, device=dy.device)
+    _dev_i32(dx, "out")
+    with torch.cuda.device(dy.device):
+        call("ds_conv2d_shift_backward_data", _ptr(dy), _ptr(w_packed), _ptr(dx), n, c, h, w, k, r, s,
+             sh, sw, ph, pw, frac_bits, 0, _stream(dy.device))
+    return dx
+
+
+def linear_shift_backward_data(dy: torch.Tensor, w_packed: torch.Tensor, in_features: int,
+                               frac_bits: int = 16, out: torch.Tensor | None = None) -> torch.Tensor:
+    """Input gradient of a LinearShift layer: dx[b, i] = sum_o term(dy[b, o], code[o, i])."""
+    _dev_i32(dy, "dy"); _dev_i32(w_packed, "w_packed")
+    batch, fout = dy.shape
+    dx = out if out is not None else torch.empty((batch, in_features), dtype=torch.int32, device=dy.device)
+    _dev_i32(dx, "out")
+    with torch.cuda.device(dy.device):
+        call("ds_linear_shift_backward_data", _ptr(dy), _ptr(w_packed), _ptr(dx), batch, in_features,
+             fout, frac_bits, 0, _stream(dy.device))
+    return dx
 
 
 def linear_mul_i32(x, w, bias=None, out=None):

@@ -240,3 +240,49 @@ def test_fused_and_pool_validation_codes():
     assert ap(FAKE, None, 1, 1, 7, 7, 0, None) == NULLP
     assert ap(FAKE, FAKE * 4, 1, 0, 7, 7, 0, None) == SHAPE
     assert ap(FAKE, FAKE * 4, 1, 1, 7, 7, 4, None) == ARG
+
+
+def test_backward_validation_codes():
+    lib = _native.lib()
+    a = [FAKE, FAKE * 2, FAKE * 4, 1, 2, 6, 6, 3, 3, 3, 1, 1, 1, 1, 16, 0, None]
+
+    def bwd(**kw):
+        v = list(a)
+        keys = ["dy", "w", "dx", "n", "c", "h", "wd", "k", "r", "s", "sh", "sw", "ph", "pw", "f", "flags"]
+        for key, val in kw.items():
+            v[keys.index(key)] = val
+        return lib.ds_conv2d_shift_backward_data(*v)
+
+    assert bwd(dy=None) == NULLP and bwd(w=None) == NULLP and bwd(dx=None) == NULLP
+    for key in ("n", "c", "h", "wd", "k", "r", "s"):
+        assert bwd(**{key: 0}) == SHAPE, key
+    assert bwd(r=9) == SHAPE
+    assert bwd(sh=0) == ARG and bwd(pw=-1) == ARG
+    assert bwd(f=32) == ARG and bwd(flags=1) == ARG
+    assert bwd(n=1 << 20, c=1 << 12, h=1, wd=1, r=1, s=1, ph=0, pw=0) == UNSUP
+    assert bwd(dx=FAKE + 4) == ARG                       # dx overlapping dy
+    assert "overlap" in lib.ds_last_error_message().decode()
+    assert lib.ds_linear_shift_backward_data(None, FAKE, FAKE * 4, 2, 3, 4, 16, 0, None) == NULLP
+    assert lib.ds_linear_shift_backward_data(FAKE, FAKE * 2, FAKE * 4, 0, 3, 4, 16, 0, None) == SHAPE
+    assert lib.ds_linear_shift_backward_data(FAKE, FAKE * 2, FAKE * 4, 2, 3, 4, 16, 4, None) == ARG
+    # host buffers are not device buffers; nothing is written
+    dy = np.zeros((2, 4), np.int32)
+    w = ops.pack_shift_weights(random_codes(np.random.default_rng(0), (4, 3)))
+    dx = np.full((2, 3), 7, np.int32)
+    st = lib.ds_linear_shift_backward_data(dy.ctypes.data, w.ctypes.data, dx.ctypes.data, 2, 3, 4,
+                                           16, 0, None)
+    assert st in (ARG, HIP) and np.all(dx == 7)
+
+
+def test_backward_describe_plans_phases_without_a_gpu():
+    d = ops.describe_conv2d_backward_data
+    s2 = d(128, 64, 56, 56, 128, 3, 2, 1)
+    assert s2.startswith("phases4") and s2.count("tiled") == 4
+    assert d(128, 64, 56, 56, 64, 3, 1, 1).startswith("phases1; 3x3 tiled window")
+    ds = d(128, 1024, 14, 14, 2048, 1, 2, 0)
+    assert ds.startswith("phases4; 1x1 tiled point") and ds.count("zero") == 3
+    assert d(256, 4096, 1, 1, 4096, 1).startswith("phases1; 1x1 tiled point transposed")
+    assert d(2, 3, 224, 224, 64, 7, 2, 3) == "direct"          # tap width 4 has no instance
+    assert d(1, 3, 6, 6, 2, 1, 1, 1) == "direct"               # padding beyond the window
+    with pytest.raises(ops.DeepShiftError, match="INVALID_SHAPE"):
+        d(1, 1, 2, 2, 1, 3, 1, 0)

@@ -1,0 +1,173 @@
+"""GPU parity of the input gradients (``ds_conv2d_shift_backward_data``,
+``ds_linear_shift_backward_data``) with the oracle, bit for bit.
+
+Edge shapes cover every path of the stride-phase decomposition: stride 1 (one
+phase), strides 2 and 3 with padding (phases with 1 and 2 taps per axis,
+pointwise and window staging, split and unsplit), phases no tap reaches (zero
+fill), rectangular windows and strides, and shapes that go to the gather
+kernel (a phase with padding beyond its window; a window width without a
+tiled instance); the gather kernel is also forced on its own. Gradients are
+signed int32 over the whole range. At full size, the input gradient of every
+ResNet-50 convolution (batch 128) equals the gather kernel element by element,
+and 400 sampled elements per layer equal the oracle's.
+"""
+import zlib
+
+import numpy as np
+import pytest
+import torch
+
+import oracle
+from paper_1905_13298_amd import ops
+from paper_1905_13298_amd import workloads as W
+from paper_1905_13298_amd.workloads import random_codes
+
+pytestmark = pytest.mark.gpu
+DEV = torch.device("cuda:0")
+
+
+def say(*a):
+    print(*a, flush=True)
+
+
+def to_dev(a):
+    return torch.from_numpy(np.ascontiguousarray(a)).to(DEV)
+
+
+def oh_of(h, pad, r, stride):
+    return (h + 2 * pad - r) // stride + 1
+
+
+def pair(v):
+    return (v, v) if np.isscalar(v) else tuple(v)
+
+
+# name, n, c, h, w, k, r, s, stride, pad
+EDGE = [
+    ("s1_3x3", 2, 13, 9, 11, 37, 3, 3, 1, 1),
+    ("s1_3x3_pad0", 2, 6, 8, 8, 9, 3, 3, 1, 0),
+    ("s1_3x3_pad2", 1, 5, 7, 7, 6, 3, 3, 1, 2),
+    ("s2_3x3_even", 3, 20, 16, 16, 33, 3, 3, 2, 1),
+    ("s2_3x3_odd", 2, 11, 13, 9, 17, 3, 3, 2, 1),
+    ("s2_3x3_pad0", 2, 7, 11, 11, 10, 3, 3, 2, 0),
+    ("s3_3x3_pad1", 1, 6, 17, 17, 8, 3, 3, 3, 1),
+    ("s2_1x1", 3, 20, 15, 15, 33, 1, 1, 2, 0),
+    ("s2_1x1_even", 2, 64, 14, 14, 70, 1, 1, 2, 0),
+    ("s1_1x1", 2, 9, 7, 5, 70, 1, 1, 1, 0),
+    ("rect_2x3", 2, 5, 10, 12, 6, (2, 3), (2, 3), 1, 1),
+    ("rect_stride", 2, 5, 9, 8, 3, (2, 3), (2, 3), (2, 1), (1, 0)),   # negative-pad phase: gather
+    ("s2_7x7_stem", 2, 3, 30, 30, 16, 7, 7, 2, 3),                    # tap width 4: gather
+    ("pad_beyond_1x1", 1, 3, 6, 6, 2, 1, 1, 1, 1),                    # gather
+    ("big_k_small_c", 2, 3, 12, 12, 300, 3, 3, 2, 1),
+    ("many_tiles", 4, 64, 20, 20, 128, 3, 3, 1, 1),
+    ("tiny", 1, 1, 1, 1, 1, 1, 1, 1, 0),
+]
+
+
+def make(seed, n, c, h, w, k, r, s, st, pd, lim=2 ** 31):
+    r, s = pair(r) if not np.isscalar(r) else (r, s)
+    sh, sw = pair(st)
+    ph, pw = pair(pd)
+    rng = np.random.default_rng(seed)
+    oh, ow = oh_of(h, ph, r, sh), oh_of(w, pw, s, sw)
+    dy = rng.integers(-lim, lim, (n, k, oh, ow), dtype=np.int64).astype(np.int32)
+    codes = rng.integers(0, 32, (k, c * r * s)).astype(np.uint8)
+    return dy, codes, (r, s)
+
+
+@pytest.mark.parametrize("direct", [False, True], ids=["auto", "gather"])
+@pytest.mark.parametrize("spec", EDGE, ids=[e[0] for e in EDGE])
+def test_edge_shapes_match_oracle(spec, direct, monkeypatch):
+    name, n, c, h, w, k, r, s, st, pd = spec
+    if direct:
+        monkeypatch.setenv("DS_FORCE_VARIANT", "0")
+    rr = r if np.isscalar(r) else r[0]
+    ss = s if np.isscalar(s) else s[1]
+    dy, codes, _ = make(zlib.crc32(name.encode()), n, c, h, w, k, rr, ss, st, pd)
+    plan = ops.describe_conv2d_backward_data(n, c, h, w, k, (rr, ss), st, pd)
+    say(f"backward {name} direct={direct}: {plan}")
+    wp = to_dev(ops.pack_shift_weights(codes).view(np.int32))
+    dx = ops.conv2d_shift_backward_data(to_dev(dy), wp, (n, c, h, w), (rr, ss), st, pd).cpu().numpy()
+    want = oracle.conv2d_shift_backward_data(dy, codes, (n, c, h, w), r=rr, s=ss, stride=st, pad=pd)
+    bad = np.flatnonzero(dx.ravel() != want.ravel())
+    assert bad.size == 0, f"{bad.size} of {want.size} differ, first at {bad[:5]}"
+
+
+def test_plans_cover_the_expected_paths():
+    d = ops.describe_conv2d_backward_data
+    assert d(2, 64, 56, 56, 128, 3, 2, 1).startswith("phases4")
+    assert d(2, 64, 56, 56, 64, 3, 1, 1).startswith("phases1")
+    assert "zero" in d(8, 64, 14, 14, 70, 1, 2, 0)
+    assert d(2, 5, 9, 8, 3, (2, 3), (2, 1), (1, 0)) == "direct"
+    assert d(2, 3, 30, 30, 16, 7, 2, 3) == "direct"
+
+
+@pytest.mark.parametrize("shape", [(8, 256, 128), (33, 300, 70), (256, 4096, 4096), (1, 1, 1)])
+def test_linear_matches_oracle(shape):
+    batch, fin, fout = shape
+    rng = np.random.default_rng(fin + fout)
+    dy = rng.integers(-(2 ** 31), 2 ** 31, (batch, fout), dtype=np.int64).astype(np.int32)
+    codes = random_codes(rng, (fout, fin), zero_frac=0.1)
+    wp = to_dev(ops.pack_shift_weights(codes).view(np.int32))
+    say(f"linear backward {shape}")
+    dx = ops.linear_shift_backward_data(to_dev(dy), wp, fin).cpu().numpy()
+    np.testing.assert_array_equal(dx, oracle.linear_shift_backward_data(dy, codes))
+
+
+def test_output_fully_overwritten_and_repeatable():
+    """dx starts as garbage; every element is written, and a second call gives the same."""
+    n, c, h, w, k = 2, 16, 14, 14, 24
+    dy, codes, _ = make(77, n, c, h, w, k, 3, 3, 2, 1)
+    wp = to_dev(ops.pack_shift_weights(codes).view(np.int32))
+    want = oracle.conv2d_shift_backward_data(dy, codes, (n, c, h, w), r=3, stride=2, pad=1)
+    out = torch.full((n, c, h, w), -123456, dtype=torch.int32, device=DEV)
+    for _ in range(2):
+        ops.conv2d_shift_backward_data(to_dev(dy), wp, (n, c, h, w), 3, 2, 1, out=out)
+        np.testing.assert_array_equal(out.cpu().numpy(), want)
+
+
+def test_errors_write_nothing():
+    n, c, h, w, k = 1, 4, 6, 6, 5
+    dy = torch.zeros((n, k, 6, 6), dtype=torch.int32, device=DEV)
+    wp = to_dev(ops.pack_shift_weights(np.zeros((k, c * 9), np.uint8)).view(np.int32))
+    dx = torch.full((n, c, h, w), 7, dtype=torch.int32, device=DEV)
+    with pytest.raises(ops.DeepShiftError, match="INVALID_ARG"):
+        ops.call("ds_conv2d_shift_backward_data", dy.data_ptr(), wp.data_ptr(), dx.data_ptr(),
+                 n, c, h, w, k, 3, 3, 1, 1, 1, 1, 16, 1, None)                     # flags
+    with pytest.raises(ops.DeepShiftError, match="INVALID_ARG"):
+        ops.conv2d_shift_backward_data(dy, wp, (n, c, h, w), 3, 1, 1,
+                                       out=dy.view(-1)[: n * c * h * w].view(n, c, h, w))  # overlap
+    with pytest.raises(ops.DeepShiftError, match="INVALID_SHAPE"):
+        ops.conv2d_shift_backward_data(dy, wp, (n, c, 2, 2), 3, 1, 0, out=dx[:, :, :2, :2].contiguous())
+    assert torch.all(dx == 7)
+
+
+def test_resnet50_full_batch_against_gather_kernel_and_oracle(monkeypatch):
+    """Every ResNet-50 convolution at batch 128 (the stem aside: an input gradient of
+    the images is not needed): all elements equal the gather kernel's, 400 sampled
+    elements per layer equal the oracle's."""
+    rng = np.random.default_rng(51)
+    layers = W.config_layers(4)
+    for li, L in enumerate(layers):
+        if L.kind != "conv" or L.name == "conv1":
+            continue
+        codes = W.gen_codes(L, W.CONFIG_SEEDS[4], li)
+        g = np.random.default_rng([4, li, 7])
+        dy = np.rint(g.standard_normal(L.y_shape, dtype=np.float32) * 2 ** 16).astype(np.int32)
+        wp = to_dev(ops.pack_shift_weights(codes).view(np.int32))
+        dyd = to_dev(dy)
+        x_shape = L.x_shape
+        say(f"backward resnet50 {L.name}: {ops.describe_conv2d_backward_data(*x_shape, L.k, (L.r, L.s), L.stride, L.pad)}")
+        dx = ops.conv2d_shift_backward_data(dyd, wp, x_shape, (L.r, L.s), L.stride, L.pad)
+        monkeypatch.setenv("DS_FORCE_VARIANT", "0")
+        ref = ops.conv2d_shift_backward_data(dyd, wp, x_shape, (L.r, L.s), L.stride, L.pad)
+        monkeypatch.delenv("DS_FORCE_VARIANT")
+        diff = int((dx != ref).sum())
+        assert diff == 0, f"{L.name}: {diff} elements differ from the gather kernel"
+        total = int(np.prod(x_shape))
+        idx = np.unique(np.concatenate([rng.choice(total, 400, replace=False), [0, total - 1]]))
+        got = dx.reshape(-1)[torch.from_numpy(idx).to(DEV)].cpu().numpy()
+        want = oracle.conv2d_shift_backward_data_points(dy, codes, x_shape, idx, r=L.r, s=L.s,
+                                                        stride=L.stride, pad=L.pad)
+        np.testing.assert_array_equal(got, want, err_msg=L.name)
+        del dx, ref, dyd
