@@ -62,6 +62,18 @@ extern "C" {
  * (shape of y) after the affine map and before ReLU. */
 #define DS_JIT_RESIDUAL 2u
 
+/* flags field (bits 8-11) of every entry point that reads packed weights: the
+ * width b of the packed codes, 2..5 (0 = 5). Section 4 keeps the weights in 5
+ * bits (1 sign bit, a 4-bit shift) and Section 5 trains with fewer bits by
+ * limiting the shifts to shorter ranges. A b-bit code holds the sign in its top
+ * bit and a (b-1)-bit shift code below it, all ones meaning a zero weight, so
+ * the shifts are 0 .. -(2^(b-1) - 2): 4 bits reach -6, 3 bits -2, and 2 bits
+ * give the ternary weights {-1, 0, +1}. A row of `cols` codes takes
+ * ds_packed_row_words_bits(cols, b) words, floor(32 / b) codes per word, code j
+ * of a word in bits [b*j, b*j + b), unused top bits zero, the last word filled
+ * with the zero code. For b = 5 this is the default layout described above. */
+#define DS_CODE_BITS(b) ((uint32_t)(b) << 8)
+
 typedef enum ds_status {
     DS_SUCCESS = 0,
     DS_ERR_NULL_POINTER = 1,     /* a required pointer is NULL */
@@ -91,6 +103,19 @@ ds_status ds_pack_shift_weights(const uint8_t *codes, int64_t rows, int64_t cols
 ds_status ds_unpack_shift_weights(const uint32_t *packed, int64_t rows, int64_t cols,
                                   uint8_t *codes, int64_t codes_len);
 
+/* The b-bit packed format of DS_CODE_BITS (host memory), b in 2..5. The codes
+ * are given and returned in the unpacked 5-bit form above; packing fails with
+ * DS_ERR_INVALID_CODE (nothing written) when a code is >= 32 or its shift does
+ * not fit b bits (a shift code above 2^(b-1) - 2 other than 15). Unpacking
+ * returns canonical codes (a zero weight as shift code 15, its sign bit kept)
+ * and fails when a word's unused top bits are set. ds_packed_row_words_bits
+ * returns -1 for cols <= 0 or b outside 2..5. */
+int64_t ds_packed_row_words_bits(int64_t cols, int32_t bits);
+ds_status ds_pack_shift_weights_bits(const uint8_t *codes, int64_t rows, int64_t cols,
+                                     int32_t bits, uint32_t *packed, int64_t packed_words);
+ds_status ds_unpack_shift_weights_bits(const uint32_t *packed, int64_t rows, int64_t cols,
+                                       int32_t bits, uint8_t *codes, int64_t codes_len);
+
 /* LinearShift forward (Section 3, Y = W~ X + b with W~ = flip(2^P, S), Eq. 3):
  *     y[b][o] = bias[o] + sum_i term(x[b][i], code[o][i])    (mod 2^32)
  * x        device int32 [batch][in_features], fixed point with frac_bits F
@@ -98,7 +123,9 @@ ds_status ds_unpack_shift_weights(const uint32_t *packed, int64_t rows, int64_t 
  * bias     device int32 [out_features] with the same F, or NULL for none
  * y        device int32 [batch][out_features], written (not accumulated)
  * frac_bits in [0, 31]: the F of x, bias and y (validated, not used by the math)
- * flags    0, or DS_RELU: y = max(y, 0) after the sum (fused)
+ * flags    0, or DS_RELU: y = max(y, 0) after the sum (fused); with
+ *          DS_CODE_BITS(b), w_packed holds b-bit codes (rows of
+ *          ds_packed_row_words_bits(in_features, b) words)
  * stream   hipStream_t to enqueue on (NULL = default stream) */
 ds_status ds_linear_shift(const int32_t *x, const uint32_t *w_packed, const int32_t *bias,
                           int32_t *y, int64_t batch, int64_t in_features, int64_t out_features,
@@ -132,7 +159,9 @@ ds_status ds_conv2d_shift(const int32_t *x, const uint32_t *w_packed, const int3
  * max_shift in [0, 14]: 14 is the 5-bit format; smaller values give the
  *          shorter shift ranges of Section 4
  * w_packed device uint32 [rows][ds_packed_row_words(cols)], written
- * flags    reserved, must be 0; stream as for ds_linear_shift.
+ *          ([rows][ds_packed_row_words_bits(cols, b)] with DS_CODE_BITS(b))
+ * flags    0, or DS_CODE_BITS(b) to write b-bit codes, b in 2..5; then max_shift
+ *          must be at most 2^(b-1) - 2; stream as for ds_linear_shift.
  * Errors: NULL pointer, rows/cols <= 0, max_shift out of range, output
  * overlapping the input, buffers that are not device allocations of the
  * required size, 2^31 or more elements. */
@@ -223,7 +252,7 @@ ds_status ds_avgpool2d_global(const int32_t *x, int32_t *y, int64_t n, int64_t c
  * dy       device int32 [n][k][oh][ow] (oh, ow of the forward pass)
  * w_packed device uint32, the forward layer's packed weights [k][ds_packed_row_words(c*r*s)]
  * dx       device int32 [n][c][h][w], written (not accumulated); must not overlap dy or w_packed
- * flags    must be 0; stream as for ds_linear_shift.
+ * flags    0, or DS_CODE_BITS(b) for b-bit packed codes; stream as for ds_linear_shift.
  * Device scratch (re-packed codes per stride phase, decoded weights) comes from
  * the library's stream-ordered pool, as for the forward operators.
  * Errors as for ds_conv2d_shift. */
@@ -294,7 +323,7 @@ ds_status ds_conv2d_shift_describe(int64_t n, int64_t c, int64_t h, int64_t w, i
  * LinearShift is the case h = w = r = s = 1.
  *
  * ds_jit_conv_create: w_packed is HOST memory, [k][ds_packed_row_words(c*r*s)]
- * words as for ds_conv2d_shift; bias, mul and add are HOST int32 [k] or NULL
+ * words as for ds_conv2d_shift (b-bit codes with DS_CODE_BITS(b) in flags); bias, mul and add are HOST int32 [k] or NULL
  * (add needs mul; mul_shift in [0, 31] when mul is given). The plan copies
  * what it keeps; the caller's buffers may be freed on return. n, c, h, w and
  * the window fix the shape of every ds_jit_conv_run of the plan. splits: 0

@@ -52,6 +52,9 @@ def _load():
         lib.oracle_conv2d_shift_backward_data_points.argtypes = [_P, _P] + [_I] * 11 + [_P, _I, _P]
         lib.oracle_pack_codes.argtypes = [_P, _I, _I, _P]
         lib.oracle_unpack_codes.argtypes = [_P, _I, _I, _P]
+        lib.oracle_pack_codes_bits.argtypes = [_P, _I, _I, ctypes.c_int, _P]
+        lib.oracle_pack_codes_bits.restype = ctypes.c_int
+        lib.oracle_unpack_codes_bits.argtypes = [_P, _I, _I, ctypes.c_int, _P]
         lib.oracle_quantize_q.argtypes = [_P, _I, ctypes.c_int, _P]
         lib.oracle_quantize_ps.argtypes = [_P, _P, _I, ctypes.c_int, _P]
         lib.oracle_to_fixed.argtypes = [_P, _I, ctypes.c_int, _P]
@@ -227,6 +230,26 @@ def unpack_codes(packed, cols):
     rows = packed.shape[0]
     out = np.empty((rows, cols), np.uint8)
     _load().oracle_unpack_codes(_ptr(packed), rows, cols, _ptr(out))
+    return out
+
+
+def pack_codes_bits(codes, bits):
+    """codes [rows, cols] uint8 (5-bit form) -> words of `bits`-bit codes, floor(32 / bits)
+    per word; None when a shift does not fit."""
+    codes = _c(codes, np.uint8)
+    rows, cols = codes.shape
+    per = 32 // bits
+    out = np.zeros((rows, (cols + per - 1) // per), np.uint32)
+    if _load().oracle_pack_codes_bits(_ptr(codes), rows, cols, int(bits), _ptr(out)) != 0:
+        return None
+    return out
+
+
+def unpack_codes_bits(packed, cols, bits):
+    packed = _c(packed, np.uint32)
+    rows = packed.shape[0]
+    out = np.empty((rows, cols), np.uint8)
+    _load().oracle_unpack_codes_bits(_ptr(packed), rows, cols, int(bits), _ptr(out))
     return out
 
 

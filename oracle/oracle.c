@@ -330,6 +330,55 @@ void oracle_unpack_codes(const uint32_t *packed, int64_t rows, int64_t cols, uin
                 (uint8_t)((packed[r * wpr + col / 6] >> (5 * (col % 6))) & 31u);
 }
 
+/* Weight codes in fewer bits (Section 5 trains with shift values limited to
+ * shorter ranges). Reading: a b-bit code (b = 2..5) keeps the sign in its top
+ * bit and the shift code in the b-1 bits below it; the all-ones shift code is
+ * the zero weight, so shifts run 0 .. -(2^(b-1) - 2) (b = 5 gives the 0 .. -14
+ * and code 15 of the 5-bit format). floor(32 / b) codes fill a word from bit 0
+ * up, rows start on a new word, the last word is padded with the zero weight.
+ * Codes are given and returned in the 5-bit form (sign << 4 | shift code).
+ * Returns -1 (and writes nothing) when a code's shift does not fit b bits. */
+int oracle_pack_codes_bits(const uint8_t *codes, int64_t rows, int64_t cols, int bits,
+                           uint32_t *packed)
+{
+    int64_t per = 32 / bits, wpr = (cols + per - 1) / per;
+    uint32_t ones = (1u << (bits - 1)) - 1u;
+    for (int64_t i = 0; i < rows * cols; ++i) {
+        uint32_t shift = codes[i] & 15u;
+        if (shift != 15u && shift >= ones)
+            return -1;
+    }
+    for (int64_t r = 0; r < rows; ++r)
+        for (int64_t w = 0; w < wpr; ++w) {
+            uint32_t word = 0;
+            for (int64_t j = 0; j < per; ++j) {
+                int64_t col = w * per + j;
+                uint32_t field = ones, sign = 0;
+                if (col < cols) {
+                    uint32_t code = codes[r * cols + col];
+                    sign = (code >> 4) & 1u;
+                    field = (code & 15u) == 15u ? ones : (code & 15u);
+                }
+                word |= ((sign << (bits - 1)) | field) << (bits * j);
+            }
+            packed[r * wpr + w] = word;
+        }
+    return 0;
+}
+
+void oracle_unpack_codes_bits(const uint32_t *packed, int64_t rows, int64_t cols, int bits,
+                              uint8_t *codes)
+{
+    int64_t per = 32 / bits, wpr = (cols + per - 1) / per;
+    uint32_t ones = (1u << (bits - 1)) - 1u;
+    for (int64_t r = 0; r < rows; ++r)
+        for (int64_t col = 0; col < cols; ++col) {
+            uint32_t raw = (packed[r * wpr + col / per] >> (bits * (col % per))) & ((1u << bits) - 1u);
+            uint32_t field = raw & ones, sign = raw >> (bits - 1);
+            codes[r * cols + col] = (uint8_t)((sign << 4) | (field == ones ? 15u : field));
+        }
+}
+
 /* ------------------------------------------------------------------------
  * Float -> weight code converter and fixed-point conversion.
  *

@@ -24,6 +24,9 @@ SIGNATURES = {
     "ds_packed_row_words": (_I64, [_I64]),
     "ds_pack_shift_weights": (ctypes.c_int, [_P, _I64, _I64, _P, _I64]),
     "ds_unpack_shift_weights": (ctypes.c_int, [_P, _I64, _I64, _P, _I64]),
+    "ds_packed_row_words_bits": (_I64, [_I64, _I32]),
+    "ds_pack_shift_weights_bits": (ctypes.c_int, [_P, _I64, _I64, _I32, _P, _I64]),
+    "ds_unpack_shift_weights_bits": (ctypes.c_int, [_P, _I64, _I64, _I32, _P, _I64]),
     "ds_linear_shift": (ctypes.c_int, [_P, _P, _P, _P, _I64, _I64, _I64, _I32, _U32, _P]),
     "ds_conv2d_shift": (ctypes.c_int, [_P, _P, _P, _P] + [_I64] * 7 + [_I32] * 4 + [_I32, _U32, _P]),
     "ds_conv2d_mul_i32": (ctypes.c_int, [_P, _P, _P, _P] + [_I64] * 7 + [_I32] * 4 + [_U32, _P]),

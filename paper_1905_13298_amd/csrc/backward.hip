@@ -57,8 +57,8 @@ Axis phase_axis(int in, int out_fwd, int R, int stride, int pad, int a)
 // code[k][c][r0 + sh*(Ta-1-t)][s0 + sw*(Tb-1-u)] of the forward weights; the
 // row is padded with code 15 to whole words.
 __global__ void __launch_bounds__(256)
-repack_phase_kernel(const uint32_t *__restrict__ wp, int K, int C, int R, int S, int wpr, int r0,
-                    int s0, int sh, int sw, int Ta, int Tb, int wpr_out,
+repack_phase_kernel(const uint32_t *__restrict__ wp, CodeFmt fmt, int K, int C, int R, int S,
+                    int wpr, int r0, int s0, int sh, int sw, int Ta, int Tb, int wpr_out,
                     uint32_t *__restrict__ out)
 {
     const int64_t total = int64_t(C) * wpr_out;
@@ -76,7 +76,7 @@ repack_phase_kernel(const uint32_t *__restrict__ wp, int K, int C, int R, int S,
                 const int t = rem / Tb, u = rem - t * Tb;
                 const int r = r0 + sh * (Ta - 1 - t), s = s0 + sw * (Tb - 1 - u);
                 const int col = (c * R + r) * S + s;
-                code = (wp[int64_t(k) * wpr + col / 6] >> (5 * (col % 6))) & 31u;
+                code = fmt.at(wp + int64_t(k) * wpr, col);
             }
             word |= code << (5 * j);
         }
@@ -87,7 +87,7 @@ repack_phase_kernel(const uint32_t *__restrict__ wp, int K, int C, int R, int S,
 // One thread per dx element: every (k, r, s) whose forward output covers it.
 __global__ void __launch_bounds__(256)
 bwd_direct_kernel(const int32_t *__restrict__ dy, const uint32_t *__restrict__ wp,
-                  int32_t *__restrict__ dx, ConvGeom g, int wpr)
+                  int32_t *__restrict__ dx, ConvGeom g, int wpr, CodeFmt fmt)
 {
     const int64_t total = int64_t(g.n) * g.c * g.h * g.w;
     for (int64_t idx = int64_t(blockIdx.x) * blockDim.x + threadIdx.x; idx < total;
@@ -109,7 +109,7 @@ bwd_direct_kernel(const int32_t *__restrict__ dy, const uint32_t *__restrict__ w
                     if (b < 0 || b % g.sw != 0 || b / g.sw >= g.ow) continue;
                     const int32_t gv = dy[((int64_t(n) * g.k + k) * g.oh + oh) * g.ow + b / g.sw];
                     const int j = (c * g.r + r) * g.s + s;
-                    const uint32_t code = (wp[int64_t(k) * wpr + j / 6] >> (5 * (j % 6))) & 31u;
+                    const uint32_t code = fmt.at(wp + int64_t(k) * wpr, j);
                     const int sh = int(code & 15u);
                     if (sh == 15) continue;
                     const uint32_t tv = uint32_t(gv >> sh);
@@ -180,11 +180,12 @@ hipError_t run_backward_data(const ConvGeom &g, const int32_t *dy, const uint32_
 {
     std::vector<PhasePlan> phases;
     size_t words = 0;
-    const int wpr = int(row_words(g.crs));
+    const int wpr = int(row_words_bits(g.crs, g.bits));
+    const CodeFmt fmt = code_fmt(g.bits);
     if (!plan_phases(g, phases, words) || forced_variant() == 0) {
         const int64_t total = int64_t(g.n) * g.c * g.h * g.w;
         const int grid = int(std::min<int64_t>((total + 255) / 256, 1 << 20));
-        hipLaunchKernelGGL(bwd_direct_kernel, dim3(grid), dim3(256), 0, st, dy, wp, dx, g, wpr);
+        hipLaunchKernelGGL(bwd_direct_kernel, dim3(grid), dim3(256), 0, st, dy, wp, dx, g, wpr, fmt);
         return hipGetLastError();
     }
     void *scratch = nullptr;
@@ -200,7 +201,7 @@ hipError_t run_backward_data(const ConvGeom &g, const int32_t *dy, const uint32_
         uint32_t *pw = packed + p.word_offset;
         const int64_t total = int64_t(p.g.k) * p.wpr;
         const int grid = int(std::min<int64_t>((total + 255) / 256, 4096));
-        hipLaunchKernelGGL(repack_phase_kernel, dim3(grid), dim3(256), 0, st, wp, g.k, g.c, g.r,
+        hipLaunchKernelGGL(repack_phase_kernel, dim3(grid), dim3(256), 0, st, wp, fmt, g.k, g.c, g.r,
                            g.s, wpr, p.ah.first, p.aw.first, g.sh, g.sw, p.g.r, p.g.s, p.wpr, pw);
         e = hipGetLastError();
         if (e == hipSuccess)
@@ -246,17 +247,19 @@ ds_status check_backward(const void *dy, const void *wp, const void *dx, int64_t
     if (h + 2 * int64_t(ph) < r || w + 2 * int64_t(pw) < s)
         return fail(DS_ERR_INVALID_SHAPE, "kernel larger than the padded input");
     if (frac_bits < 0 || frac_bits > 31) return fail(DS_ERR_INVALID_ARG, "frac_bits must be in [0, 31]");
-    if (flags != 0) return fail(DS_ERR_INVALID_ARG, "flags must be 0");
+    const int bits = flags_code_bits(flags);
+    if ((flags & ~0xF00u) != 0 || bits < 0)
+        return fail(DS_ERR_INVALID_ARG, "flags must be 0 apart from DS_CODE_BITS(2..5)");
     const int64_t oh = (h + 2 * int64_t(ph) - r) / sh + 1;
     const int64_t ow = (w + 2 * int64_t(pw) - s) / sw + 1;
     const int64_t crs = prod({c, r, s});
     const int64_t xe = prod({n, c, h, w}), ye = prod({n, k, oh, ow});
-    const int64_t we = prod({k, row_words(crs)});
+    const int64_t we = prod({k, row_words_bits(crs, bits)});
     if (crs < 0 || xe < 0 || ye < 0 || we < 0 || crs > kMaxElems || xe > kMaxElems ||
         ye > kMaxElems || we > kMaxElems || prod({k, crs}) > kMaxElems)
         return fail(DS_ERR_UNSUPPORTED, "tensors with 2^31 or more elements are not supported");
     g = ConvGeom{int(n), int(c), int(h), int(w), int(k), int(r), int(s), sh, sw, ph, pw,
-                 int(oh), int(ow), int(crs)};
+                 int(oh), int(ow), int(crs), bits};
     const int64_t dyb = 4 * ye, dxb = 4 * xe, wb = 4 * we;
     if (overlap(dx, dxb, dy, dyb) || overlap(dx, dxb, wp, wb))
         return fail(DS_ERR_INVALID_ARG, "dx overlaps an input");

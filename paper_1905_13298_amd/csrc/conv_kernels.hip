@@ -85,7 +85,7 @@ template <Inner OP>
 __global__ void __launch_bounds__(256)
 conv_direct_kernel(const int32_t *__restrict__ x, const uint32_t *__restrict__ wp,
                    const int32_t *__restrict__ wi, const int32_t *__restrict__ bias,
-                   int32_t *__restrict__ y, ConvGeom g, int wpr)
+                   int32_t *__restrict__ y, ConvGeom g, int wpr, CodeFmt fmt)
 {
     const int64_t total = int64_t(g.n) * g.k * g.oh * g.ow;
     for (int64_t idx = int64_t(blockIdx.x) * blockDim.x + threadIdx.x; idx < total;
@@ -107,7 +107,7 @@ conv_direct_kernel(const int32_t *__restrict__ x, const uint32_t *__restrict__ w
                     const int32_t xv = x[(int64_t(n * g.c + c) * g.h + ih) * g.w + iw];
                     const int j = (c * g.r + r) * g.s + s;
                     if constexpr (OP == Inner::Shift) {
-                        const uint32_t code = (wp[int64_t(k) * wpr + j / 6] >> (5 * (j % 6))) & 31u;
+                        const uint32_t code = fmt.at(wp + int64_t(k) * wpr, j);
                         const int sh = int(code & 15u);
                         if (sh == 15) continue;
                         const uint32_t tv = uint32_t(xv >> sh);
@@ -133,7 +133,7 @@ template <Inner OP, int TN>
 __global__ void __launch_bounds__(256)
 prep_kernel(const uint32_t *__restrict__ wp, const int32_t *__restrict__ wi,
             const int32_t *__restrict__ bias, int K, int CRS, int wpr, int Jpad, int Kpad,
-            int wblocks, int32_t *__restrict__ wd, int32_t *__restrict__ init)
+            int wblocks, int32_t *__restrict__ wd, int32_t *__restrict__ init, CodeFmt fmt)
 {
     if (int(blockIdx.x) < wblocks) {
         const int64_t total = int64_t(Kpad) * Jpad;
@@ -146,7 +146,7 @@ prep_kernel(const uint32_t *__restrict__ wp, const int32_t *__restrict__ wi,
             int32_t v;
             if (k < K && j < CRS) {
                 if constexpr (OP == Inner::Shift) {
-                    const uint32_t code = (wp[int64_t(k) * wpr + j / 6] >> (5 * (j % 6))) & 31u;
+                    const uint32_t code = fmt.at(wp + int64_t(k) * wpr, j);
                     const uint32_t sh = code & 15u;
                     v = sh == 15u ? 31 : int32_t(sh | ((code >> 4) << 31));
                 } else {
@@ -165,12 +165,13 @@ prep_kernel(const uint32_t *__restrict__ wp, const int32_t *__restrict__ wi,
     if (k >= Kpad) return;
     uint32_t cnt = 0;
     if (OP == Inner::Shift && k < K) {
+        const uint32_t *row = wp + int64_t(k) * wpr;
         for (int wdx = lane; wdx < wpr; wdx += 64) {
-            const uint32_t word = wp[int64_t(k) * wpr + wdx];
-            for (int j = 0; j < 6; ++j) {
-                const uint32_t code = (word >> (5 * j)) & 31u;
-                const bool live = wdx * 6 + j < CRS;
-                cnt += (live && (code & 16u) && (code & 15u) != 15u) ? 1u : 0u;
+            for (int j = 0; j < fmt.per_word; ++j) {
+                const int col = wdx * fmt.per_word + j;
+                if (col >= CRS) break;
+                const uint32_t code = fmt.at(row, col);
+                cnt += ((code & 16u) && (code & 15u) != 15u) ? 1u : 0u;
             }
         }
     }
@@ -643,13 +644,13 @@ static hipError_t run_direct(const ConvGeom &g, const int32_t *x, const uint32_t
 {
     const int64_t total = int64_t(g.n) * g.k * g.oh * g.ow;
     const int grid = int(std::min<int64_t>((total + 255) / 256, 1 << 20));
-    const int wpr = (g.crs + 5) / 6;
+    const int wpr = int(row_words_bits(g.crs, g.bits));
     if (op == Inner::Shift)
         hipLaunchKernelGGL(conv_direct_kernel<Inner::Shift>, dim3(grid), dim3(256), 0, st, x, wp,
-                           wi, bias, y, g, wpr);
+                           wi, bias, y, g, wpr, code_fmt(g.bits));
     else
         hipLaunchKernelGGL(conv_direct_kernel<Inner::Mul>, dim3(grid), dim3(256), 0, st, x, wp,
-                           wi, bias, y, g, wpr);
+                           wi, bias, y, g, wpr, code_fmt(g.bits));
     return hipGetLastError();
 }
 
@@ -895,17 +896,17 @@ hipError_t run_conv(const ConvGeom &g0, const int32_t *x, const uint32_t *wp, co
                            g0.c);
         xin = xt;
     }
-    const int wpr = (g.crs + 5) / 6;
+    const int wpr = int(row_words_bits(g.crs, g.bits));
 
     const int64_t pw_total = int64_t(Kpad) * Jpad;
     const int wblocks = int(std::min<int64_t>((pw_total + 255) / 256, 4096));
     const int pgrid = wblocks + (Kpad + 3) / 4;
     if (op == Inner::Shift)
         hipLaunchKernelGGL((prep_kernel<Inner::Shift, kTN>), dim3(pgrid), dim3(256), 0, st, wp, wi,
-                           bias, g.k, g.crs, wpr, Jpad, Kpad, wblocks, wd, init);
+                           bias, g.k, g.crs, wpr, Jpad, Kpad, wblocks, wd, init, code_fmt(g.bits));
     else
         hipLaunchKernelGGL((prep_kernel<Inner::Mul, kTN>), dim3(pgrid), dim3(256), 0, st, wp, wi,
-                           bias, g.k, g.crs, wpr, Jpad, Kpad, wblocks, wd, init);
+                           bias, g.k, g.crs, wpr, Jpad, Kpad, wblocks, wd, init, code_fmt(g.bits));
     e = hipGetLastError();
     if (e == hipSuccess && p.atomic_out) e = run_fill_mapped(g, init, yout, map, st);
     if (e == hipSuccess) {

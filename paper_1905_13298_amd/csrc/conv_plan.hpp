@@ -5,6 +5,8 @@
 
 #include <cstdint>
 
+#include "common.hpp"
+
 namespace ds {
 
 // One convolution problem (LinearShift is the case h = w = r = s = 1).
@@ -13,6 +15,7 @@ struct ConvGeom {
     int sh, sw, ph, pw;
     int oh, ow;
     int crs;
+    int bits = 5;  // width of the packed weight codes
 };
 
 // Inner operation of the reduction: the DeepShift shift-accumulate, or the

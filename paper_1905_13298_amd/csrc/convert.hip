@@ -5,14 +5,15 @@
 //   * the power is clipped to -max_shift .. 0 (Section 4, 14 for 5-bit codes);
 //   * inputs and bias rounded to fixed point with F fractional bits
 //     (Section 4, 16.16).
-// The weight converters write the packed 5-bit format directly.
+// The weight converters write the packed format directly: 5-bit codes, or the
+// shorter b-bit codes of DS_CODE_BITS (Section 5's shorter shift ranges).
 //
 // Both are streaming kernels bound by HBM bandwidth. A weight block owns 256
 // consecutive packed words. The floats those words cover form one contiguous
 // range (rows are stored back to back), so the block reads that range with
 // coalesced loads, turns every float into its code once, keeps the codes as
-// bytes in LDS, and then each thread gathers the six codes of its word and
-// stores the word (coalesced).
+// bytes in LDS, and then each thread gathers the codes of its word (six for
+// 5-bit codes, floor(32 / b) for b bits) and stores the word (coalesced).
 #include <hip/hip_runtime.h>
 
 #include <algorithm>
@@ -27,7 +28,6 @@ namespace ds {
 namespace {
 
 constexpr int kWordsPerBlock = 256;
-constexpr int kCodesPerWord = 6;
 constexpr uint32_t kZeroCode = 15;
 
 // Code of flip(2^p, s) for p already clipped to -max_shift .. 0.
@@ -70,19 +70,30 @@ __device__ __forceinline__ uint32_t code_ps(float pv, float sv, int max_shift)
 
 struct WordRange {
     int first_float;  // flat index (within the tensor) of the first float of word t
-    int ncodes;       // codes of word t that come from the row (1..6)
+    int ncodes;       // codes of word t that come from the row (1..PER)
 };
 
-// Word t of a tensor with `cols` floats and `wpr` words per row (all indexes
-// below 2^31: the entry points reject larger tensors).
+// Word t of a tensor with `cols` floats and `wpr` words per row, PER codes per
+// word (all indexes below 2^31: the entry points reject larger tensors).
+template <int PER>
 __device__ __forceinline__ WordRange word_range(int t, int cols, const FastDiv &wpr)
 {
     const int row = fdiv(t, wpr), j = t - row * int(wpr.d);
-    const int col = j * kCodesPerWord;
+    const int col = j * PER;
     WordRange r;
     r.first_float = row * cols + col;
-    r.ncodes = min(kCodesPerWord, cols - col);
+    r.ncodes = min(PER, cols - col);
     return r;
+}
+
+// A 5-bit code in the BITS-bit layout: the sign on top, the shift code below,
+// all ones for a zero weight (the entry points keep max_shift inside the range).
+template <int BITS>
+__device__ __forceinline__ uint32_t narrow(uint32_t code)
+{
+    constexpr uint32_t ones = (1u << (BITS - 1)) - 1u;
+    const uint32_t sh = code & 15u;
+    return ((code >> 4) << (BITS - 1)) | (sh == 15u ? ones : sh);
 }
 
 // One weight tensor of a launch: its inputs, its packed output, and the first
@@ -106,10 +117,11 @@ struct SegmentTable {
     Segment seg[kMaxSegments];
 };
 
-template <bool PS>
+template <bool PS, int BITS>
 __global__ __launch_bounds__(kWordsPerBlock) void quantize_kernel(const SegmentTable tab)
 {
-    __shared__ uint8_t codes[kWordsPerBlock * kCodesPerWord];
+    constexpr int PER = 32 / BITS;
+    __shared__ uint8_t codes[kWordsPerBlock * PER];
     // This block's tensor: the last segment whose first block is <= blockIdx.x.
     int lo = 0, hi = tab.count - 1;
     while (lo < hi) {
@@ -121,21 +133,21 @@ __global__ __launch_bounds__(kWordsPerBlock) void quantize_kernel(const SegmentT
     const int t0 = (int(blockIdx.x) - sg.block0) * kWordsPerBlock;
     const int t1 = min(t0 + kWordsPerBlock, nwords);
     // Floats covered by words [t0, t1): [f0, f1). Word t1 (or the end) starts at f1.
-    const int f0 = word_range(t0, cols, sg.wpr).first_float;
-    const int f1 = t1 == nwords ? sg.rows * cols : word_range(t1, cols, sg.wpr).first_float;
-    const int nf = f1 - f0;  // <= 6 * 256
+    const int f0 = word_range<PER>(t0, cols, sg.wpr).first_float;
+    const int f1 = t1 == nwords ? sg.rows * cols : word_range<PER>(t1, cols, sg.wpr).first_float;
+    const int nf = f1 - f0;  // <= PER * 256
     const float *__restrict__ a = sg.a + f0;
     const float *__restrict__ b = PS ? sg.b + f0 : nullptr;
-    // Six independent loads per thread in flight, then the codes into LDS.
-    float va[kCodesPerWord], vb[kCodesPerWord];
+    // PER independent loads per thread in flight, then the codes into LDS.
+    float va[PER], vb[PER];
 #pragma unroll
-    for (int r = 0; r < kCodesPerWord; ++r) {
+    for (int r = 0; r < PER; ++r) {
         const int i = int(threadIdx.x) + r * kWordsPerBlock;
         va[r] = i < nf ? a[i] : 0.0f;
         vb[r] = PS && i < nf ? b[i] : 0.0f;
     }
 #pragma unroll
-    for (int r = 0; r < kCodesPerWord; ++r) {
+    for (int r = 0; r < PER; ++r) {
         const int i = int(threadIdx.x) + r * kWordsPerBlock;
         if (i < nf)
             codes[i] = uint8_t(PS ? code_ps(va[r], vb[r], tab.max_shift) : code_q(va[r], tab.max_shift));
@@ -143,13 +155,13 @@ __global__ __launch_bounds__(kWordsPerBlock) void quantize_kernel(const SegmentT
     __syncthreads();
     const int t = t0 + int(threadIdx.x);
     if (t >= t1) return;
-    const WordRange r = word_range(t, cols, sg.wpr);
+    const WordRange r = word_range<PER>(t, cols, sg.wpr);
     const int base = int(r.first_float - f0);
     uint32_t word = 0;
 #pragma unroll
-    for (int i = 0; i < kCodesPerWord; ++i) {
+    for (int i = 0; i < PER; ++i) {
         const uint32_t c = i < r.ncodes ? uint32_t(codes[base + i]) : kZeroCode;
-        word |= c << (5 * i);
+        word |= narrow<BITS>(c) << (BITS * i);
     }
     sg.out[t] = word;
 }
@@ -204,9 +216,14 @@ ds_status check_quantize(const float *a, const float *b, bool need_b, int64_t ro
     if (!a || (need_b && !b) || !out) return fail(DS_ERR_NULL_POINTER, "inputs and output must not be NULL");
     if (rows <= 0 || cols <= 0) return fail(DS_ERR_INVALID_SHAPE, "rows and cols must be > 0");
     if (max_shift < 0 || max_shift > 14) return fail(DS_ERR_INVALID_ARG, "max_shift must be in [0, 14]");
-    if (flags != 0) return fail(DS_ERR_INVALID_ARG, "flags must be 0");
+    const int bits = flags_code_bits(flags);
+    if ((flags & ~0xF00u) != 0 || bits < 0)
+        return fail(DS_ERR_INVALID_ARG, "flags must be 0 apart from DS_CODE_BITS(2..5)");
+    if (max_shift > (1 << (bits - 1)) - 2)
+        return fail(DS_ERR_INVALID_ARG, "max_shift %d does not fit %d-bit codes (at most %d)",
+                    int(max_shift), bits, (1 << (bits - 1)) - 2);
     const int64_t ne = prod({rows, cols});
-    nwords = prod({rows, row_words(cols)});
+    nwords = prod({rows, row_words_bits(cols, bits)});
     if (ne < 0 || ne > kMaxElems || nwords < 0 || nwords > kMaxElems)
         return fail(DS_ERR_UNSUPPORTED, "tensors with 2^31 or more elements are not supported");
     const int64_t ib = 4 * ne, ob = 4 * nwords;
@@ -217,9 +234,9 @@ ds_status check_quantize(const float *a, const float *b, bool need_b, int64_t ro
 
 // The buffers of one tensor must be device allocations of the required size.
 ds_status check_quantize_buffers(const float *a, const float *b, bool need_b, int64_t rows,
-                                 int64_t cols, const uint32_t *out)
+                                 int64_t cols, const uint32_t *out, int bits)
 {
-    const int64_t ib = 4 * rows * cols, ob = 4 * rows * row_words(cols);
+    const int64_t ib = 4 * rows * cols, ob = 4 * rows * row_words_bits(cols, bits);
     if (!device_range_ok(a, ib) || (need_b && !device_range_ok(b, ib)))
         return fail(DS_ERR_INVALID_ARG, "inputs are not device buffers of %lld bytes", (long long)ib);
     if (!device_range_ok(out, ob))
@@ -242,6 +259,7 @@ ds_status quantize_many(int64_t count, const float *const *a, const float *const
         const std::string msg = last_error();
         return fail(st, "tensor %lld: %s", (long long)i, msg.c_str());
     };
+    const int bits = flags_code_bits(flags);
     // Arguments of every tensor first, then the device buffers.
     for (int64_t i = 0; i < count; ++i) {
         int64_t nwords = 0;
@@ -249,15 +267,15 @@ ds_status quantize_many(int64_t count, const float *const *a, const float *const
                                             max_shift, out[i], flags, nwords);
         if (st != DS_SUCCESS) return named(st, i);
         for (int64_t j = 0; j < i; ++j)
-            if (overlap(out[i], 4 * nwords, out[j], 4 * rows[j] * row_words(cols[j])) ||
+            if (overlap(out[i], 4 * nwords, out[j], 4 * rows[j] * row_words_bits(cols[j], bits)) ||
                 overlap(out[i], 4 * nwords, a[j], 4 * rows[j] * cols[j]) ||
-                overlap(out[j], 4 * rows[j] * row_words(cols[j]), a[i], 4 * rows[i] * cols[i]))
+                overlap(out[j], 4 * rows[j] * row_words_bits(cols[j], bits), a[i], 4 * rows[i] * cols[i]))
                 return fail(DS_ERR_INVALID_ARG, "tensors %lld and %lld overlap (an output over "
                             "an input or another output)", (long long)j, (long long)i);
     }
     for (int64_t i = 0; i < count; ++i) {
         const ds_status st = check_quantize_buffers(a[i], PS ? b[i] : nullptr, PS, rows[i], cols[i],
-                                                    out[i]);
+                                                    out[i], bits);
         if (st != DS_SUCCESS) return named(st, i);
     }
     for (int64_t first = 0; first < count; first += kMaxSegments) {
@@ -273,15 +291,21 @@ ds_status quantize_many(int64_t count, const float *const *a, const float *const
             sg.out = out[k];
             sg.cols = int(cols[k]);
             sg.rows = int(rows[k]);
-            sg.wpr = make_fastdiv(uint32_t(row_words(cols[k])));
-            sg.nwords = int(rows[k] * row_words(cols[k]));
+            sg.wpr = make_fastdiv(uint32_t(row_words_bits(cols[k], bits)));
+            sg.nwords = int(rows[k] * row_words_bits(cols[k], bits));
             if (blocks > INT32_MAX) return fail(DS_ERR_UNSUPPORTED, "too many weights in one call");
             sg.block0 = int(blocks);
             blocks += (sg.nwords + kWordsPerBlock - 1) / kWordsPerBlock;
         }
         if (blocks > INT32_MAX) return fail(DS_ERR_UNSUPPORTED, "too many weights in one call");
-        hipLaunchKernelGGL(quantize_kernel<PS>, dim3(unsigned(blocks)), dim3(kWordsPerBlock), 0,
-                           static_cast<hipStream_t>(stream), tab);
+        const hipStream_t st_ = static_cast<hipStream_t>(stream);
+        const dim3 grid{unsigned(blocks)}, block{unsigned(kWordsPerBlock)};
+        switch (bits) {
+        case 2: hipLaunchKernelGGL((quantize_kernel<PS, 2>), grid, block, 0, st_, tab); break;
+        case 3: hipLaunchKernelGGL((quantize_kernel<PS, 3>), grid, block, 0, st_, tab); break;
+        case 4: hipLaunchKernelGGL((quantize_kernel<PS, 4>), grid, block, 0, st_, tab); break;
+        default: hipLaunchKernelGGL((quantize_kernel<PS, 5>), grid, block, 0, st_, tab); break;
+        }
         const ds_status st = hip_result(hipGetLastError(), name);
         if (st != DS_SUCCESS) return st;
     }

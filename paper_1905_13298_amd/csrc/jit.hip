@@ -124,8 +124,9 @@ public:
 
 struct Spec {
     ConvGeom g;
-    const uint32_t *wp;  // host packed codes [k][row_words(crs)]
+    const uint32_t *wp;  // host packed codes [k][rw], codes of fmt.bits bits
     int64_t rw;
+    CodeFmt fmt;
     const int32_t *bias, *mul, *add;
     int mul_shift;
     bool relu, residual;
@@ -134,7 +135,7 @@ struct Spec {
 
 inline int code_at(const Spec &sp, int k, int j)
 {
-    return int((sp.wp[int64_t(k) * sp.rw + j / 6] >> (5 * (j % 6))) & 31u);
+    return int(sp.fmt.at(sp.wp + int64_t(k) * sp.rw, j));
 }
 
 // Straight-line code of segment (kg, part): output channels [64 kg, 64 kg + 64)
@@ -349,7 +350,9 @@ ds_status plan_spec(const CreateArgs &a, Spec &sp)
         return fail(DS_ERR_INVALID_SHAPE, "all sizes must be > 0");
     if (a.sh < 1 || a.sw < 1 || a.ph < 0 || a.pw < 0)
         return fail(DS_ERR_INVALID_ARG, "stride must be >= 1 and padding >= 0");
-    if (a.flags & ~(DS_RELU | DS_JIT_RESIDUAL)) return fail(DS_ERR_INVALID_ARG, "unknown flags");
+    if (a.flags & ~(DS_RELU | DS_JIT_RESIDUAL | 0xF00u)) return fail(DS_ERR_INVALID_ARG, "unknown flags");
+    const int bits = flags_code_bits(a.flags);
+    if (bits < 0) return fail(DS_ERR_INVALID_ARG, "DS_CODE_BITS must be 2..5 (or 0 for 5)");
     if (a.add && !a.mul) return fail(DS_ERR_INVALID_ARG, "add needs mul");
     if (a.mul && (a.mul_shift < 0 || a.mul_shift > 31))
         return fail(DS_ERR_INVALID_ARG, "mul_shift must be in [0, 31]");
@@ -370,9 +373,12 @@ ds_status plan_spec(const CreateArgs &a, Spec &sp)
     g.r = int(a.r); g.s = int(a.s); g.sh = a.sh; g.sw = a.sw; g.ph = a.ph; g.pw = a.pw;
     g.crs = int(crs);
     sp.wp = a.wp;
-    sp.rw = row_words(crs);
-    for (int64_t i = 0; i < a.k * sp.rw; ++i)
-        if (a.wp[i] >> 30) return fail(DS_ERR_INVALID_CODE, "bits 30-31 of packed word %lld are not 0", (long long)i);
+    sp.fmt = code_fmt(bits);
+    sp.rw = row_words_bits(crs, bits);
+    const int used = sp.fmt.per_word * bits;
+    for (int64_t i = 0; used < 32 && i < a.k * sp.rw; ++i)
+        if (a.wp[i] >> used)
+            return fail(DS_ERR_INVALID_CODE, "bits %d-31 of packed word %lld are not 0", used, (long long)i);
     sp.bias = a.bias; sp.mul = a.mul; sp.add = a.add; sp.mul_shift = a.mul ? a.mul_shift : 0;
     sp.relu = a.flags & DS_RELU;
     sp.residual = a.flags & DS_JIT_RESIDUAL;

@@ -24,7 +24,7 @@ bool device_range_ok(const void *p, int64_t bytes)
 // Validates the sizes of a convolution problem and fills `g` (no pointers).
 static ds_status check_shape(int64_t n, int64_t c, int64_t h, int64_t w, int64_t k, int64_t r,
                              int64_t s, int32_t sh, int32_t sw, int32_t ph, int32_t pw,
-                             bool packed, ConvGeom &g)
+                             bool packed, ConvGeom &g, int bits = 5)
 {
     if (n <= 0 || c <= 0 || h <= 0 || w <= 0 || k <= 0 || r <= 0 || s <= 0)
         return fail(DS_ERR_INVALID_SHAPE, "all sizes must be > 0");
@@ -36,12 +36,12 @@ static ds_status check_shape(int64_t n, int64_t c, int64_t h, int64_t w, int64_t
     const int64_t ow = (w + 2 * int64_t(pw) - s) / sw + 1;
     const int64_t crs = prod({c, r, s});
     const int64_t xe = prod({n, c, h, w}), ye = prod({n, k, oh, ow});
-    const int64_t we = packed ? prod({k, row_words(crs)}) : prod({k, crs});
+    const int64_t we = packed ? prod({k, row_words_bits(crs, bits)}) : prod({k, crs});
     if (crs < 0 || xe < 0 || ye < 0 || we < 0 || crs > kMaxElems || xe > kMaxElems ||
         ye > kMaxElems || we > kMaxElems || prod({k, crs}) > kMaxElems)
         return fail(DS_ERR_UNSUPPORTED, "tensors with 2^31 or more elements are not supported");
     g = ConvGeom{int(n), int(c), int(h), int(w), int(k), int(r), int(s), sh, sw, ph, pw,
-                 int(oh), int(ow), int(crs)};
+                 int(oh), int(ow), int(crs), bits};
     return DS_SUCCESS;
 }
 
@@ -53,13 +53,16 @@ static ds_status check_conv(const void *x, const void *wts, const void *bias, co
                             uint32_t allowed_flags)
 {
     if (!x || !wts || !y) return fail(DS_ERR_NULL_POINTER, "x, weights and y must not be NULL");
-    ds_status st = check_shape(n, c, h, w, k, r, s, sh, sw, ph, pw, packed, g);
+    if (packed) allowed_flags |= 0xF00u;                 // DS_CODE_BITS field
+    const int bits = packed ? flags_code_bits(flags) : 5;
+    ds_status st = check_shape(n, c, h, w, k, r, s, sh, sw, ph, pw, packed, g, bits < 0 ? 5 : bits);
     if (st != DS_SUCCESS) return st;
     if (frac_bits < 0 || frac_bits > 31) return fail(DS_ERR_INVALID_ARG, "frac_bits must be in [0, 31]");
     if (flags & ~allowed_flags) return fail(DS_ERR_INVALID_ARG, "unknown flags 0x%x", flags);
+    if (bits < 0) return fail(DS_ERR_INVALID_ARG, "DS_CODE_BITS must be 2..5 (or 0 for 5)");
     const int64_t xb = 4 * int64_t(g.n) * g.c * g.h * g.w;
     const int64_t yb = 4 * int64_t(g.n) * g.k * g.oh * g.ow;
-    const int64_t wb = 4 * (packed ? int64_t(g.k) * row_words(g.crs) : int64_t(g.k) * g.crs);
+    const int64_t wb = 4 * (packed ? int64_t(g.k) * row_words_bits(g.crs, g.bits) : int64_t(g.k) * g.crs);
     const int64_t bb = 4 * int64_t(g.k);
     if (overlap(y, yb, x, xb) || overlap(y, yb, wts, wb) || overlap(y, yb, bias, bb))
         return fail(DS_ERR_INVALID_ARG, "y overlaps an input");
@@ -109,7 +112,9 @@ extern "C" ds_status ds_conv2d_shift_fused(const int32_t *x, const uint32_t *w_p
     ConvGeom g;
     // Arguments first (no device access), then the buffers.
     if (x && w_packed && y) {
-        ds_status st = check_shape(n, c, h, w, k, r, s, stride_h, stride_w, pad_h, pad_w, true, g);
+        const int bits = flags_code_bits(flags);
+        ds_status st = check_shape(n, c, h, w, k, r, s, stride_h, stride_w, pad_h, pad_w, true, g,
+                                   bits < 0 ? 5 : bits);
         if (st != DS_SUCCESS) return st;
         if (add && !mul) return fail(DS_ERR_INVALID_ARG, "add needs mul");
         if (mul_shift < 0 || mul_shift > 31) return fail(DS_ERR_INVALID_ARG, "mul_shift must be in [0, 31]");

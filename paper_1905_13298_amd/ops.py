@@ -13,7 +13,7 @@ import torch
 
 from ._native import DeepShiftError, call, lib
 
-__all__ = ["DeepShiftError", "describe_conv2d", "packed_row_words", "pack_shift_weights", "unpack_shift_weights",
+__all__ = ["DeepShiftError", "code_bits_flag", "describe_conv2d", "packed_row_words", "pack_shift_weights", "unpack_shift_weights",
            "linear_shift", "conv2d_shift", "linear_mul_i32", "conv2d_mul_i32", "out_size",
            "quantize_shift_weights_q", "quantize_shift_weights_q_many", "quantize_shift_weights_ps",
            "to_fixed_point", "conv2d_shift_fused", "maxpool2d", "avgpool2d_global", "DS_RELU",
@@ -23,26 +23,34 @@ __all__ = ["DeepShiftError", "describe_conv2d", "packed_row_words", "pack_shift_
 DS_RELU = 1
 
 
-def packed_row_words(cols: int) -> int:
-    return int(lib().ds_packed_row_words(int(cols)))
+def code_bits_flag(bits: int) -> int:
+    """The DS_CODE_BITS flags field for packed codes of `bits` bits (0 for the default 5)."""
+    if bits not in (2, 3, 4, 5):
+        raise ValueError("code bits must be 2..5")
+    return 0 if bits == 5 else bits << 8
 
 
-def pack_shift_weights(codes) -> np.ndarray:
-    """Host codes [rows, cols] (uint8, sign << 4 | shift) -> packed words [rows, ceil(cols/6)]."""
+def packed_row_words(cols: int, bits: int = 5) -> int:
+    return int(lib().ds_packed_row_words_bits(int(cols), int(bits)))
+
+
+def pack_shift_weights(codes, bits: int = 5) -> np.ndarray:
+    """Host codes [rows, cols] (uint8, sign << 4 | shift) -> packed words
+    [rows, ceil(cols / floor(32 / bits))] of `bits`-bit codes (5: six per word)."""
     codes = np.ascontiguousarray(codes, dtype=np.uint8)
     if codes.ndim != 2:
         codes = codes.reshape(codes.shape[0], -1)
     rows, cols = codes.shape
-    out = np.empty((rows, max(packed_row_words(cols), 0)), dtype=np.uint32)
-    call("ds_pack_shift_weights", codes.ctypes.data, rows, cols, out.ctypes.data, out.size)
+    out = np.empty((rows, max(packed_row_words(cols, bits), 0)), dtype=np.uint32)
+    call("ds_pack_shift_weights_bits", codes.ctypes.data, rows, cols, bits, out.ctypes.data, out.size)
     return out
 
 
-def unpack_shift_weights(packed, cols: int) -> np.ndarray:
+def unpack_shift_weights(packed, cols: int, bits: int = 5) -> np.ndarray:
     packed = np.ascontiguousarray(packed, dtype=np.uint32)
     rows = packed.shape[0]
     out = np.empty((rows, cols), dtype=np.uint8)
-    call("ds_unpack_shift_weights", packed.ctypes.data, rows, cols, out.ctypes.data, out.size)
+    call("ds_unpack_shift_weights_bits", packed.ctypes.data, rows, cols, bits, out.ctypes.data, out.size)
     return out
 
 
@@ -106,7 +114,8 @@ def _pair(v):
 
 
 def linear_shift(x: torch.Tensor, w_packed: torch.Tensor, bias: torch.Tensor | None = None,
-                 frac_bits: int = 16, out: torch.Tensor | None = None, relu: bool = False) -> torch.Tensor:
+                 frac_bits: int = 16, out: torch.Tensor | None = None, relu: bool = False,
+                 code_bits: int = 5) -> torch.Tensor:
     """LinearShift: y[b, o] = bias[o] + sum_i term(x[b, i], code[o, i]) (int32, mod 2^32),
     then max(y, 0) when relu."""
     _dev_i32(x, "x"); _dev_i32(w_packed, "w_packed")
@@ -118,13 +127,14 @@ def linear_shift(x: torch.Tensor, w_packed: torch.Tensor, bias: torch.Tensor | N
     _dev_i32(y, "out")
     with torch.cuda.device(x.device):
         call("ds_linear_shift", _ptr(x), _ptr(w_packed), _ptr(bias), _ptr(y), batch, fin, fout,
-             frac_bits, DS_RELU if relu else 0, _stream(x.device))
+             frac_bits, (DS_RELU if relu else 0) | code_bits_flag(code_bits), _stream(x.device))
     return y
 
 
 def conv2d_shift(x: torch.Tensor, w_packed: torch.Tensor, bias: torch.Tensor | None,
                  kernel_size, stride=1, padding=0, frac_bits: int = 16,
-                 out: torch.Tensor | None = None, relu: bool = False) -> torch.Tensor:
+                 out: torch.Tensor | None = None, relu: bool = False,
+                 code_bits: int = 5) -> torch.Tensor:
     """ConvShift (NCHW): y[n, k, oh, ow] = bias[k] + sum_{c,r,s} term(x[...], code[k, c, r, s]),
     then max(y, 0) when relu."""
     _dev_i32(x, "x"); _dev_i32(w_packed, "w_packed")
@@ -141,13 +151,14 @@ def conv2d_shift(x: torch.Tensor, w_packed: torch.Tensor, bias: torch.Tensor | N
     _dev_i32(y, "out")
     with torch.cuda.device(x.device):
         call("ds_conv2d_shift", _ptr(x), _ptr(w_packed), _ptr(bias), _ptr(y), n, c, h, w, k, r, s,
-             sh, sw, ph, pw, frac_bits, DS_RELU if relu else 0, _stream(x.device))
+             sh, sw, ph, pw, frac_bits, (DS_RELU if relu else 0) | code_bits_flag(code_bits),
+             _stream(x.device))
     return y
 
 
 def conv2d_shift_backward_data(dy: torch.Tensor, w_packed: torch.Tensor, x_shape, kernel_size,
                                stride=1, padding=0, frac_bits: int = 16,
-                               out: torch.Tensor | None = None) -> torch.Tensor:
+                               out: torch.Tensor | None = None, code_bits: int = 5) -> torch.Tensor:
     """Input gradient of a ConvShift layer (NCHW): dx[n, c, ih, iw] = sum of
     term(dy[n, k, oh, ow], code[k, c, r, s]) over the forward connections. x_shape =
     (n, c, h, w) of the forward input; dy has the forward output's shape."""
@@ -161,12 +172,13 @@ def conv2d_shift_backward_data(dy: torch.Tensor, w_packed: torch.Tensor, x_shape
     _dev_i32(dx, "out")
     with torch.cuda.device(dy.device):
         call("ds_conv2d_shift_backward_data", _ptr(dy), _ptr(w_packed), _ptr(dx), n, c, h, w, k, r, s,
-             sh, sw, ph, pw, frac_bits, 0, _stream(dy.device))
+             sh, sw, ph, pw, frac_bits, code_bits_flag(code_bits), _stream(dy.device))
     return dx
 
 
 def linear_shift_backward_data(dy: torch.Tensor, w_packed: torch.Tensor, in_features: int,
-                               frac_bits: int = 16, out: torch.Tensor | None = None) -> torch.Tensor:
+                               frac_bits: int = 16, out: torch.Tensor | None = None,
+                               code_bits: int = 5) -> torch.Tensor:
     """Input gradient of a LinearShift layer: dx[b, i] = sum_o term(dy[b, o], code[o, i])."""
     _dev_i32(dy, "dy"); _dev_i32(w_packed, "w_packed")
     batch, fout = dy.shape
@@ -174,7 +186,7 @@ def linear_shift_backward_data(dy: torch.Tensor, w_packed: torch.Tensor, in_feat
     _dev_i32(dx, "out")
     with torch.cuda.device(dy.device):
         call("ds_linear_shift_backward_data", _ptr(dy), _ptr(w_packed), _ptr(dx), batch, in_features,
-             fout, frac_bits, 0, _stream(dy.device))
+             fout, frac_bits, code_bits_flag(code_bits), _stream(dy.device))
     return dx
 
 
@@ -212,20 +224,21 @@ def _weight_rows(t: torch.Tensor):
 
 
 def quantize_shift_weights_q(w: torch.Tensor, max_shift: int = 14,
-                             out: torch.Tensor | None = None) -> torch.Tensor:
-    """DeepShift-Q: float32 weights [rows, ...] -> packed codes [rows, words] (int32 bits)."""
+                             out: torch.Tensor | None = None, code_bits: int = 5) -> torch.Tensor:
+    """DeepShift-Q: float32 weights [rows, ...] -> packed codes [rows, words] (int32 bits),
+    `code_bits`-bit codes (max_shift at most 2^(code_bits-1) - 2)."""
     _dev_f32(w, "w")
     rows, cols = _weight_rows(w)
-    y = out if out is not None else torch.empty((rows, max(packed_row_words(cols), 0)),
+    y = out if out is not None else torch.empty((rows, max(packed_row_words(cols, code_bits), 0)),
                                                 dtype=torch.int32, device=w.device)
     _dev_i32(y, "out")
     with torch.cuda.device(w.device):
-        call("ds_quantize_shift_weights_q", _ptr(w), rows, cols, max_shift, _ptr(y), 0,
-             _stream(w.device))
+        call("ds_quantize_shift_weights_q", _ptr(w), rows, cols, max_shift, _ptr(y),
+             code_bits_flag(code_bits), _stream(w.device))
     return y
 
 
-def quantize_shift_weights_q_many(ws, max_shift: int = 14, outs=None) -> list:
+def quantize_shift_weights_q_many(ws, max_shift: int = 14, outs=None, code_bits: int = 5) -> list:
     """DeepShift-Q for a list of float32 weight tensors in one library call."""
     import ctypes
     if not ws:
@@ -234,7 +247,7 @@ def quantize_shift_weights_q_many(ws, max_shift: int = 14, outs=None) -> list:
         _dev_f32(w, f"ws[{i}]")
     shapes = [_weight_rows(w) for w in ws]
     if outs is None:
-        outs = [torch.empty((r, max(packed_row_words(c), 0)), dtype=torch.int32, device=w.device)
+        outs = [torch.empty((r, max(packed_row_words(c, code_bits), 0)), dtype=torch.int32, device=w.device)
                 for w, (r, c) in zip(ws, shapes)]
     for i, o in enumerate(outs):
         _dev_i32(o, f"outs[{i}]")
@@ -245,23 +258,24 @@ def quantize_shift_weights_q_many(ws, max_shift: int = 14, outs=None) -> list:
     cols = (ctypes.c_int64 * n)(*[c for _, c in shapes])
     dev = ws[0].device
     with torch.cuda.device(dev):
-        call("ds_quantize_shift_weights_q_many", n, wp, rows, cols, max_shift, op, 0, _stream(dev))
+        call("ds_quantize_shift_weights_q_many", n, wp, rows, cols, max_shift, op,
+             code_bits_flag(code_bits), _stream(dev))
     return outs
 
 
 def quantize_shift_weights_ps(p: torch.Tensor, s: torch.Tensor, max_shift: int = 14,
-                              out: torch.Tensor | None = None) -> torch.Tensor:
+                              out: torch.Tensor | None = None, code_bits: int = 5) -> torch.Tensor:
     """DeepShift-PS: shift and sign parameters [rows, ...] -> packed codes [rows, words]."""
     _dev_f32(p, "p"); _dev_f32(s, "s")
     if p.shape != s.shape:
         raise ValueError("p and s must have the same shape")
     rows, cols = _weight_rows(p)
-    y = out if out is not None else torch.empty((rows, max(packed_row_words(cols), 0)),
+    y = out if out is not None else torch.empty((rows, max(packed_row_words(cols, code_bits), 0)),
                                                 dtype=torch.int32, device=p.device)
     _dev_i32(y, "out")
     with torch.cuda.device(p.device):
-        call("ds_quantize_shift_weights_ps", _ptr(p), _ptr(s), rows, cols, max_shift, _ptr(y), 0,
-             _stream(p.device))
+        call("ds_quantize_shift_weights_ps", _ptr(p), _ptr(s), rows, cols, max_shift, _ptr(y),
+             code_bits_flag(code_bits), _stream(p.device))
     return y
 
 
@@ -278,7 +292,8 @@ def to_fixed_point(x: torch.Tensor, frac_bits: int = 16,
 
 def conv2d_shift_fused(x: torch.Tensor, w_packed: torch.Tensor, bias, kernel_size, stride=1,
                        padding=0, mul=None, add=None, mul_shift: int = 16, residual=None,
-                       relu: bool = False, frac_bits: int = 16, out=None) -> torch.Tensor:
+                       relu: bool = False, frac_bits: int = 16, out=None,
+                       code_bits: int = 5) -> torch.Tensor:
     """ConvShift, then per channel floor(v * mul / 2**mul_shift) + add, + residual, ReLU."""
     _dev_i32(x, "x"); _dev_i32(w_packed, "w_packed")
     for t, name in ((bias, "bias"), (mul, "mul"), (add, "add"), (residual, "residual")):
@@ -296,7 +311,7 @@ def conv2d_shift_fused(x: torch.Tensor, w_packed: torch.Tensor, bias, kernel_siz
     with torch.cuda.device(x.device):
         call("ds_conv2d_shift_fused", _ptr(x), _ptr(w_packed), _ptr(bias), _ptr(mul), _ptr(add),
              mul_shift, _ptr(residual), _ptr(y), n, c, h, w, k, r, s, sh, sw, ph, pw, frac_bits,
-             DS_RELU if relu else 0, _stream(x.device))
+             (DS_RELU if relu else 0) | code_bits_flag(code_bits), _stream(x.device))
     return y
 
 
@@ -353,7 +368,7 @@ def _np_ptr(a):
 
 def jit_conv_image(w_packed, x_shape, kernel_size, stride=1, padding=0, bias=None, mul=None,
                    add=None, mul_shift: int = 16, residual: bool = False, relu: bool = False,
-                   splits: int = 0) -> bytes:
+                   splits: int = 0, code_bits: int = 5) -> bytes:
     """The code object a JitConv with these arguments would load (host only)."""
     k = int(w_packed.shape[0])
     wp, b, m, a = _jit_args(w_packed, k, bias, mul, add)
@@ -361,7 +376,7 @@ def jit_conv_image(w_packed, x_shape, kernel_size, stride=1, padding=0, bias=Non
     r, s = _pair(kernel_size)
     sh, sw = _pair(stride)
     ph, pw = _pair(padding)
-    flags = (DS_RELU if relu else 0) | (DS_JIT_RESIDUAL if residual else 0)
+    flags = (DS_RELU if relu else 0) | (DS_JIT_RESIDUAL if residual else 0) | code_bits_flag(code_bits)
     size = ctypes.c_int64(0)
     args = [_np_ptr(wp), _np_ptr(b), _np_ptr(m), _np_ptr(a), mul_shift, n, c, h, w, k, r, s, sh, sw,
             ph, pw, flags, splits]
@@ -382,7 +397,7 @@ class JitConv:
 
     def __init__(self, w_packed, x_shape, kernel_size, stride=1, padding=0, bias=None, mul=None,
                  add=None, mul_shift: int = 16, residual: bool = False, relu: bool = False,
-                 splits: int = 0, device="cuda:0"):
+                 splits: int = 0, device="cuda:0", code_bits: int = 5):
         self.k = int(w_packed.shape[0])
         wp, b, m, a = _jit_args(w_packed, self.k, bias, mul, add)
         self.x_shape = tuple(int(v) for v in x_shape)
@@ -393,7 +408,7 @@ class JitConv:
         self.y_shape = (n, self.k, out_size(h, ph, r, sh), out_size(w, pw, s, sw))
         self.device = torch.device(device)
         self.residual = residual
-        flags = (DS_RELU if relu else 0) | (DS_JIT_RESIDUAL if residual else 0)
+        flags = (DS_RELU if relu else 0) | (DS_JIT_RESIDUAL if residual else 0) | code_bits_flag(code_bits)
         handle = ctypes.c_void_p()
         with torch.cuda.device(self.device):
             call("ds_jit_conv_create", _np_ptr(wp), _np_ptr(b), _np_ptr(m), _np_ptr(a), mul_shift,

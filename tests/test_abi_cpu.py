@@ -169,6 +169,9 @@ def test_converter_validation_codes():
     assert q(FAKE, 2, 6, 15, FAKE * 4, 0, None) == ARG
     assert q(FAKE, 2, 6, -1, FAKE * 4, 0, None) == ARG
     assert q(FAKE, 2, 6, 14, FAKE * 4, 1, None) == ARG
+    assert q(FAKE, 2, 6, 14, FAKE * 4, 3 << 8, None) == ARG    # shifts to -14 need 5 bits
+    assert "does not fit" in lib.ds_last_error_message().decode()
+    assert q(FAKE, 2, 6, 2, FAKE * 4, 7 << 8, None) == ARG     # no 7-bit codes
     assert q(FAKE, 1 << 16, 1 << 15, 14, FAKE * 4, 0, None) == UNSUP
     assert q(FAKE, 2, 6, 14, FAKE + 8, 0, None) == ARG     # output overlaps w
     assert "overlap" in lib.ds_last_error_message().decode()

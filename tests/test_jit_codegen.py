@@ -298,3 +298,19 @@ def test_zero_weights_emit_no_arithmetic(tmp_path):
     names = collections.Counter(op for op, _, _ in disassemble(img, str(tmp_path)).values())
     assert names["v_add_u32_e32"] == names["v_sub_u32_e32"] == names["v_ashrrev_i32_e32"] == 0
     assert names["buffer_store_dword"] == 8
+
+
+@pytest.mark.parametrize("bits", [2, 3, 4])
+def test_code_width_does_not_change_the_generated_code(bits):
+    """The generated code depends on the weights only: b-bit packed codes give the
+    same code object as the same weights in the 5-bit format."""
+    rng = np.random.default_rng(bits)
+    ones = (1 << (bits - 1)) - 1
+    shift = rng.integers(0, ones, (70, 5 * 9))
+    shift[rng.random(shift.shape) < 0.2] = 15
+    codes = (rng.integers(0, 2, shift.shape) << 4 | shift).astype(np.uint8)
+    bias = rng.integers(-1000, 1000, 70).astype(np.int32)
+    a = ops.jit_conv_image(ops.pack_shift_weights(codes), (2, 5, 9, 9), 3, 1, 1, bias=bias)
+    b = ops.jit_conv_image(ops.pack_shift_weights(codes, bits=bits), (2, 5, 9, 9), 3, 1, 1, bias=bias,
+                           code_bits=bits)
+    assert a == b

@@ -11,6 +11,7 @@ import shutil
 import pytest
 
 import tests.test_oracle_backward_pins as bpins
+import tests.test_oracle_bits_pins as kpins
 import tests.test_oracle_convert_pins as cpins
 import tests.test_oracle_layer_pins as lpins
 import tests.test_oracle_pins as pins
@@ -77,6 +78,13 @@ MUTATIONS = {
                                     "for (int64_t oh = 0; oh < OH - 1; ++oh)\n                    for (int64_t ow = 0; ow < OW; ++ow) {\n                        int32_t g"),
     "bwd_linear_codes_not_transposed": ("acc += oracle_term(dy[b * out + o], codes[o * in + i]);",
                                         "acc += oracle_term(dy[b * out + o], codes[(i * out + o) % (in * out)]);"),
+    # b-bit packed codes
+    "bits_padding_as_plus_one": ("uint32_t field = ones, sign = 0;", "uint32_t field = 0, sign = 0;"),
+    "bits_sign_one_too_high": ("word |= ((sign << (bits - 1)) | field) << (bits * j);",
+                               "word |= ((sign << bits) | field) << (bits * j);"),
+    "bits_codes_per_word_off": ("int64_t per = 32 / bits, wpr = (cols + per - 1) / per;\n    uint32_t ones = (1u << (bits - 1)) - 1u;\n    for (int64_t i",
+                                "int64_t per = 32 / bits - (bits == 3), wpr = (cols + per - 1) / per;\n    uint32_t ones = (1u << (bits - 1)) - 1u;\n    for (int64_t i"),
+    "bits_range_check_off_by_one": ("if (shift != 15u && shift >= ones)", "if (shift != 15u && shift > ones)"),
     "bwd_points_divisibility_ignored": ("if (a < 0 || a % sh != 0 || a / sh >= OH)", "if (a < 0 || a / sh >= OH)"),
 }
 
@@ -98,6 +106,12 @@ CONVERT_CHECKS = [
     (cpins.test_ps_nan_gives_zero_weight, ()),
     *[(cpins.test_fixed_matches_exact_rounding, (f,)) for f in (16, 31)],
     (cpins.test_golden_examples, ()),
+]
+
+BITS_CHECKS = [
+    *[(kpins.test_pack_matches_bitstream, (b,)) for b in kpins.BITS],
+    (kpins.test_pack_literal_words, ()),
+    *[(kpins.test_round_trip_and_range, (b,)) for b in kpins.BITS],
 ]
 
 BACKWARD_CHECKS = [
@@ -149,8 +163,9 @@ def test_pins_catch_mutation(tmp_path, monkeypatch, name):
     monkeypatch.setattr(cpins, "oracle", mod)
     monkeypatch.setattr(lpins, "oracle", mod)
     monkeypatch.setattr(bpins, "oracle", mod)
+    monkeypatch.setattr(kpins, "oracle", mod)
     failed = []
-    for fn, args in CHECKS + CONVERT_CHECKS + LAYER_CHECKS + BACKWARD_CHECKS:
+    for fn, args in CHECKS + CONVERT_CHECKS + LAYER_CHECKS + BACKWARD_CHECKS + BITS_CHECKS:
         try:
             fn(*args)
         except AssertionError:
@@ -171,5 +186,6 @@ def test_unmutated_copy_passes(tmp_path, monkeypatch):
     monkeypatch.setattr(cpins, "oracle", mod)
     monkeypatch.setattr(lpins, "oracle", mod)
     monkeypatch.setattr(bpins, "oracle", mod)
-    for fn, args in CHECKS + CONVERT_CHECKS + LAYER_CHECKS + BACKWARD_CHECKS:
+    monkeypatch.setattr(kpins, "oracle", mod)
+    for fn, args in CHECKS + CONVERT_CHECKS + LAYER_CHECKS + BACKWARD_CHECKS + BITS_CHECKS:
         fn(*args)
