@@ -3,11 +3,12 @@
 //
 // With the weight codes known when the plan is made, the inner loop needs no
 // weight loads, no decode and no work for zero weights. For each reduction
-// element (input channel c, tap (r, s)) a lane loads its input x, forms the
-// right shifts x >> s that the 64 output channels of the segment use at that
-// element, and adds or subtracts each one into its channel's accumulator: one
-// v_add_u32 / v_sub_u32 per non-zero weight, with the register of the shift
-// and the sign fixed in the instruction. The term of a weight with sign bit set
+// element (input channel c, tap (r, s)) a lane loads its input x, forms each
+// right shift x >> s that the 64 output channels of the segment use at that
+// element (once, into one of two registers in turn), and adds or subtracts it
+// into the accumulators of the channels with that shift: one v_add_u32 /
+// v_sub_u32 per non-zero weight, with the register and the sign fixed in the
+// instruction. The term of a weight with sign bit set
 // is -(x >> shift) (Eq. 1 with the sign applied after the shift), so the
 // results equal those of ds_conv2d_shift bit for bit.
 //
@@ -44,10 +45,11 @@ namespace {
 constexpr int kTap0 = 4;     // v4..v12: byte offset in x of tap (r, s) = v[4 + 3r + s], channel 0
 constexpr int kYoff = 13;    // v13: byte offset in y of the lane's output pixel, channel 0
 constexpr int kTmpLo = 14, kTmpHi = 15;
-constexpr int kTab = 16;     // v[16 + s] = x >> s for s = 1..14 (x itself stays in its load slot)
-constexpr int kAcc = 32;     // v32..v95: accumulators of the segment's 64 output channels
-constexpr int kSlot = 96;    // v96..v103: loads in flight
-constexpr int kSlots = 8;
+constexpr int kTab = 16;     // v16, v17: x >> s, alternately (x itself stays in its load slot)
+constexpr int kAcc = 18;     // v18..v81: accumulators of the segment's 64 output channels
+constexpr int kSlot = 82;    // v82..: loads in flight (at most 14: v82..v95)
+constexpr int kMaxSlots = 14;
+// v0..v95 in all: 96 VGPRs leave room for 5 waves per SIMD.
 constexpr int kXrsrc = 20, kYrsrc = 24, kRrsrc = 36;  // buffer resources (SGPR quads)
 constexpr int kSy = 28, kSx = 29, kSmul = 30;         // scalar scratch of the generated code
 constexpr int kTN = 64;      // output channels per segment
@@ -131,6 +133,7 @@ struct Spec {
     int mul_shift;
     bool relu, residual;
     int nsplit, kgroups, nseg, tiles_p;
+    int slots = 8;       // loads in flight per wave
 };
 
 inline int code_at(const Spec &sp, int k, int j)
@@ -156,6 +159,7 @@ void emit_segment(Emitter &e, const Spec &sp, int kg, int c0, int c1, bool split
     // Element i = (c0 + i / RS, tap i % RS); its load goes to slot i % kSlots and
     // reads x at v[tap] + s29, where s29 = c * H * W * 4 for the channel of the
     // most recently issued load.
+    const int kSlots = sp.slots;
     const int D = std::min(kSlots, E);
     int cur_c = c0;
     e.s_mov_imm(kSx, uint32_t(c0) * cstride);
@@ -175,22 +179,28 @@ void emit_segment(Emitter &e, const Spec &sp, int kg, int c0, int c1, bool split
         e.wait_vm(issued - i - 1);
         const int slot = kSlot + i % kSlots;
         const int jw = (c0 + i / RS) * RS + i % RS;
-        uint32_t need = 0;
-        for (int j = 0; j < jn; ++j) {
-            const int sh = code_at(sp, kbase + j, jw) & 15;
-            if (sh != 15 && sh != 0) need |= 1u << sh;
-        }
-        for (int s = 1; s <= 14; ++s)
-            if (need >> s & 1u) e.vop2(kOpAshr, kTab + s, Emitter::inline_int(s), slot);
+        // The element's non-zero weights grouped by shift; each shift is formed
+        // once, into one of two registers in turn, right before the adds that use it.
+        int by_shift[15][kTN], count[15] = {};
         for (int j = 0; j < jn; ++j) {
             const int code = code_at(sp, kbase + j, jw);
-            const int sh = code & 15;
-            if (sh == 15) continue;
-            const int src = sh == 0 ? slot : kTab + sh;
-            if (code & 16)
-                e.vop2(kOpSub, kAcc + j, Emitter::vgpr(kAcc + j), src);  // acc - term
-            else
-                e.vop2(kOpAdd, kAcc + j, Emitter::vgpr(src), kAcc + j);  // term + acc
+            if ((code & 15) != 15) by_shift[code & 15][count[code & 15]++] = code & 16 ? -1 - j : j;
+        }
+        int formed = 0;
+        for (int sh = 0; sh <= 14; ++sh) {
+            if (count[sh] == 0) continue;
+            int src = slot;
+            if (sh > 0) {
+                src = kTab + (formed++ & 1);
+                e.vop2(kOpAshr, src, Emitter::inline_int(sh), slot);
+            }
+            for (int q = 0; q < count[sh]; ++q) {
+                const int v = by_shift[sh][q];
+                if (v < 0)
+                    e.vop2(kOpSub, kAcc - 1 - v, Emitter::vgpr(kAcc - 1 - v), src);  // acc - term
+                else
+                    e.vop2(kOpAdd, kAcc + v, Emitter::vgpr(src), kAcc + v);          // term + acc
+            }
         }
         if (i + D < E) issue(i + D);
     }
@@ -398,6 +408,10 @@ ds_status plan_spec(const CreateArgs &a, Spec &sp)
     const int64_t nseg = int64_t(sp.kgroups) * sp.nsplit;
     if (nseg * sp.tiles_p > INT32_MAX) return fail(DS_ERR_UNSUPPORTED, "grid too large");
     sp.nseg = int(nseg);
+    // Loads in flight: 14 (the most the register budget holds) on large pixel grids,
+    // where a sweep of every ResNet-50 and ResNet-18 layer on MI355X showed the load
+    // latency exposed at 8; 8 elsewhere.
+    sp.slots = std::min(kMaxSlots, std::max(1, env_int("DS_JIT_SLOTS", sp.tiles_p >= 1568 ? 14 : 8)));
     return ok();
 }
 
@@ -411,7 +425,7 @@ struct ds_jit_conv {
     hipModule_t module = nullptr;
     hipFunction_t fn = nullptr;
     Spec sp;
-    int group_tiles = 64;
+    int group_tiles = 16;
     int64_t code_bytes = 0;
     int32_t *init = nullptr;        // [k] bias or zeros: y's start for split-K
     int32_t *mul = nullptr, *add = nullptr;
@@ -521,7 +535,10 @@ extern "C" ds_status ds_jit_conv_create(const uint32_t *w_packed, const int32_t 
         }
         p->sp.bias = p->sp.mul = p->sp.add = nullptr;
         p->sp.wp = nullptr;
-        p->group_tiles = std::max(1, env_int("DS_JIT_GROUP_TILES", 64));
+        // 16 pixel tiles per group: their inputs stay in L2 while the group's segments
+        // go by (the same sweep: 64 was up to 1.6x slower on layers with many output
+        // channels; 4, 8 and 16 within a few percent of each other, 16 the best).
+        p->group_tiles = std::max(1, env_int("DS_JIT_GROUP_TILES", 16));
         *plan = p;
         return ok();
     } catch (const std::bad_alloc &) {

@@ -3,10 +3,10 @@
 // The paper (Section 6) proposes compiling the shift kernels at run time. With
 // the weights known, every shift amount and sign becomes part of the
 // instruction stream: for each reduction element j (input channel, tap) a
-// lane holds its input value x and the 14 right shifts x >> 1 .. x >> 14 in
-// registers, and each non-zero weight of the 64 output channels of a segment
-// is one v_add_u32 or v_sub_u32 of the right register into that channel's
-// accumulator; zero weights cost nothing.
+// lane loads its input value x, forms each right shift x >> s that the 64
+// output channels of a segment use there once, and each non-zero weight is one
+// v_add_u32 or v_sub_u32 of that shifted value into its channel's accumulator;
+// zero weights cost nothing.
 //
 // This file is compiled to assembly when the library is built. The kernel
 // below computes, per lane, what the generated code needs (the byte offsets of
@@ -16,8 +16,9 @@
 // the marker with a jump, through a table, to the code of this workgroup's
 // segment (64 output channels and a range of input channels), assembled from
 // generated machine words; each segment ends the wave itself. Register use of
-// the generated code (the clobbers below): v14..v111 (v16..v30 the shifted
-// values, v32..v95 the accumulators, v96..v103 the loads in flight), s28..s31.
+// the generated code (the clobbers below): v14..v95 (v16, v17 the shifted
+// values, v18..v81 the accumulators, v82..v95 the loads in flight), s28..s31;
+// 96 VGPRs in all, so that 5 waves fit on a SIMD.
 #include <hip/hip_runtime.h>
 
 #include <cstdint>
@@ -80,7 +81,5 @@ extern "C" __global__ void __launch_bounds__(256) ds_jit_conv_template(const Jit
                    "v57", "v58", "v59", "v60", "v61", "v62", "v63", "v64", "v65", "v66", "v67",
                    "v68", "v69", "v70", "v71", "v72", "v73", "v74", "v75", "v76", "v77", "v78",
                    "v79", "v80", "v81", "v82", "v83", "v84", "v85", "v86", "v87", "v88", "v89",
-                   "v90", "v91", "v92", "v93", "v94", "v95", "v96", "v97", "v98", "v99", "v100",
-                   "v101", "v102", "v103", "v104", "v105", "v106", "v107", "v108", "v109",
-                   "v110", "v111", "s28", "s29", "s30", "s31");
+                   "v90", "v91", "v92", "v93", "v94", "v95", "s28", "s29", "s30", "s31");
 }
