@@ -449,7 +449,9 @@ def gen_grad(L, seed: int, index: int) -> np.ndarray:
 def bench_backward(args):
     """One step = the input gradient of every layer (the stem aside) on its own
     seeded output gradient, all resident in HBM; dense shift-accumulates as for the
-    forward pass (one term per forward connection)."""
+    forward pass (one term per forward connection). Path jit: a weight-specialised
+    plan per layer (made at setup, stride phases as generated kernels) where one is
+    preferred; path runtime: ds_conv2d_shift_backward_data / ds_linear_shift_backward_data."""
     import torch
     from paper_1905_13298_amd import ops
     from paper_1905_13298_amd import workloads as W
@@ -460,48 +462,95 @@ def bench_backward(args):
     dev = torch.device("cuda:0")
     torch.cuda.set_device(dev)
     stream = torch.cuda.current_stream(dev)
-    calls, plans = [], []
+    rt_calls, calls, plans, names, nonzero, keep = [], [], [], [], [], []
     for li, L in layers:
         codes = W.gen_codes(L, seed, li)
-        wp = torch.from_numpy(ops.pack_shift_weights(codes).view(np.int32)).to(dev)
+        nonzero.append(float(np.mean((codes & 15) != 15)))
+        wph = ops.pack_shift_weights(codes)
+        wp = torch.from_numpy(wph.view(np.int32)).to(dev)
         dy = torch.from_numpy(gen_grad(L, seed, li)).to(dev)
         dx = torch.empty(L.x_shape, dtype=torch.int32, device=dev)
         if L.kind == "linear":
-            calls.append(lambda dy=dy, wp=wp, dx=dx, L=L: ops.linear_shift_backward_data(dy, wp, L.c, out=dx))
-            plans.append(ops.describe_conv2d_backward_data(L.n, L.c, 1, 1, L.k, 1))
+            rt = lambda dy=dy, wp=wp, dx=dx, L=L: ops.linear_shift_backward_data(dy, wp, L.c, out=dx)
+            names.append(ops.describe_conv2d_backward_data(L.n, L.c, 1, 1, L.k, 1))
+            fx, kern, st_, pd_, dy4 = (L.n, L.c, 1, 1), 1, 1, 0, dy.view(L.n, L.k, 1, 1)
         else:
-            calls.append(lambda dy=dy, wp=wp, dx=dx, L=L: ops.conv2d_shift_backward_data(
-                dy, wp, L.x_shape, (L.r, L.s), L.stride, L.pad, out=dx))
-            plans.append(ops.describe_conv2d_backward_data(*L.x_shape, L.k, (L.r, L.s), L.stride, L.pad))
+            rt = lambda dy=dy, wp=wp, dx=dx, L=L: ops.conv2d_shift_backward_data(
+                dy, wp, L.x_shape, (L.r, L.s), L.stride, L.pad, out=dx)
+            names.append(ops.describe_conv2d_backward_data(*L.x_shape, L.k, (L.r, L.s), L.stride, L.pad))
+            fx, kern, st_, pd_, dy4 = L.x_shape, (L.r, L.s), L.stride, L.pad, dy
+        rt_calls.append(rt)
+        plan = None
+        if args.path == "jit":
+            try:
+                plan = ops.JitConvBackwardData(wph, fx, kern, st_, pd_)
+            except ops.DeepShiftError:
+                plan = None
+            if plan is not None and not plan.preferred:
+                plan.close()
+                plan = None
+        plans.append(plan)
+        if plan is None:
+            calls.append(rt)
+        else:
+            calls.append(lambda plan=plan, dy4=dy4, dx=dx: plan(dy4, out=dx.view(plan.y_shape)))
+        keep.append((dy, wp, dx))
     torch.cuda.synchronize()
+    if args.path == "jit":
+        for i, (c_, r_) in enumerate(zip(calls, rt_calls)):
+            c_()
+            a_ = keep[i][2].clone()
+            r_()
+            if not torch.equal(a_, keep[i][2]):
+                raise SystemExit(f"{layers[i][1].name}: plan and runtime input gradients differ")
+        torch.cuda.synchronize()
     ms_per_step, d = time_layers(calls, args.steps, args.warmup, stream)
     sac_step = sum(L.sac for _, L in layers)
+    nz_step = sum(L.sac * f for (_, L), f in zip(layers, nonzero))
     value = sac_step / (ms_per_step * 1e-3) / 1e9
     groups = {}
     for i, (li, L) in enumerate(layers):
-        g = groups.setdefault(plans[i], {"sac": 0, "ms": 0.0, "launches": 0, "bytes": 0})
+        gname = JIT_KERNEL if plans[i] is not None else names[i]
+        g = groups.setdefault(gname, {"sac": 0, "nz": 0.0, "ms": 0.0, "launches": 0, "bytes": 0})
         g["sac"] += L.sac
+        g["nz"] += L.sac * nonzero[i]
         g["ms"] += float(d[:, i].mean())
         g["launches"] += 1
         g["bytes"] += algorithmic_bytes(L)
     name, g = max(groups.items(), key=lambda kv: kv[1]["ms"])
-    achieved = g["sac"] / (g["ms"] * 1e-3) / 1e12
-    roofline = {"bound": "alu", "achieved": round(achieved, 4), "peak": round(SAC_PEAK_T, 4),
-                "unit": "TSAC/s", "frac": round(achieved / SAC_PEAK_T, 4), "traffic": None,
-                "kernel": name, "launches_per_step": g["launches"],
-                "avg_launch_ms": round(g["ms"] / g["launches"], 5),
-                "sac_per_launch_avg": g["sac"] // g["launches"],
-                "algorithmic_bytes_per_launch": g["bytes"] // g["launches"],
-                "work_unit": "dense shift-accumulate, 2 int32 VALU ops each (3 on chunks holding a negative value)",
-                "timed_span": "library call per layer (code re-pack, weight decode, fill, phase kernels)"}
-    per_layer = [{"layer": L.name, "plan": plans[i], "sac": L.sac,
+    common = {"traffic": None, "kernel": name, "launches_per_step": g["launches"],
+              "avg_launch_ms": round(g["ms"] / g["launches"], 5),
+              "sac_per_launch_avg": g["sac"] // g["launches"],
+              "algorithmic_bytes_per_launch": g["bytes"] // g["launches"]}
+    if name == JIT_KERNEL:
+        nz = g["nz"] / (g["ms"] * 1e-3) / 1e12
+        roofline = {"bound": "alu", "achieved": round(nz, 4), "peak": round(VOP2_OPS_PEAK_T, 4),
+                    "unit": "T int32 ops/s", "frac": round(nz / VOP2_OPS_PEAK_T, 4), **common,
+                    "work_unit": "one int32 VOP2 add/sub per non-zero weight term",
+                    "dense_tsac_s": round(g["sac"] / (g["ms"] * 1e-3) / 1e12, 4),
+                    "timed_span": "library call per layer (zero fills, the phases' generated kernels)"}
+    else:
+        achieved = g["sac"] / (g["ms"] * 1e-3) / 1e12
+        roofline = {"bound": "alu", "achieved": round(achieved, 4), "peak": round(SAC_PEAK_T, 4),
+                    "unit": "TSAC/s", "frac": round(achieved / SAC_PEAK_T, 4), **common,
+                    "work_unit": "dense shift-accumulate, 2 int32 VALU ops each (3 on chunks holding a negative value)",
+                    "timed_span": "library call per layer (code re-pack, weight decode, fill, phase kernels)"}
+    runtime = None
+    if args.path == "jit" and not args.no_runtime:
+        rt_ms, _ = time_layers(rt_calls, args.steps, args.warmup, stream)
+        runtime = {"ms_per_step": round(rt_ms, 4), "value": round(sac_step / (rt_ms * 1e-3) / 1e9, 2),
+                   "unit": "GSAC/s"}
+    per_layer = [{"layer": L.name, "plan": names[i], "jit": plans[i] is not None, "sac": L.sac,
                   "ms_median": float(np.median(d[:, i])),
                   "gsac_s": L.sac / (float(np.median(d[:, i])) * 1e-3) / 1e9}
                  for i, (li, L) in enumerate(layers)]
     cpu = None
     if not args.no_cpu_baseline:
         import oracle
-        del calls
+        del calls, rt_calls, keep
+        for p in plans:
+            if p is not None:
+                p.close()
         torch.cuda.empty_cache()
         nb = 2
         t_total, s_total, passes = 0.0, 0, 0
@@ -529,11 +578,13 @@ def bench_backward(args):
         "value": round(value, 2), "unit": "GSAC/s", "n_gpus": 1, "steps": args.steps,
         "warmup": args.warmup, "ms_per_step": round(ms_per_step, 4), "higher_is_better": True,
         "scaling": "weak", "vs_baseline": None, "dtype": "i32", "data": "synthetic",
-        "frac_sac_peak": round(value / 1000.0 / SAC_PEAK_T, 4),
+        **({"frac_vop2_peak_nonzero": round(nz_step / (ms_per_step * 1e-3) / 1e12 / VOP2_OPS_PEAK_T, 4)}
+           if args.path == "jit" else {"frac_sac_peak": round(value / 1000.0 / SAC_PEAK_T, 4)}),
+        "path": args.path,
         "config": {"workload": W.CONFIG_NAMES[cfg] + "_backward_data", "layers": len(layers),
                    "batch": layers[0][1].n, "frac_bits": W.FRAC_BITS, "sac_per_step": sac_step,
                    "grad": "rint(N(0,1) * 2^16), signed", "parallelism": "single GPU"},
-        "roofline": roofline, "cpu_baseline": cpu,
+        "roofline": roofline, "runtime_weights": runtime, "cpu_baseline": cpu,
     }
     if args.layers_out:
         with open(args.layers_out, "w") as f:

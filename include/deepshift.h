@@ -366,6 +366,23 @@ ds_status ds_jit_conv_image(const uint32_t *w_packed, const int32_t *bias, const
 ds_status ds_jit_conv_query(const ds_jit_conv *plan, int64_t *code_bytes, int32_t *segments,
                             int32_t *splits);
 
+/* A plan for the input gradient of a ConvShift layer (the result of
+ * ds_conv2d_shift_backward_data, bit for bit), with the weights baked into
+ * the code as for ds_jit_conv_create. The arguments describe the FORWARD layer;
+ * w_packed is HOST memory (b-bit codes with DS_CODE_BITS(b), the only flag).
+ * The plan splits dx into the stride phases of the layer, each a generated
+ * kernel writing its own rows and columns of dx; ds_jit_conv_run(plan, dy,
+ * NULL, dx, stream) then takes dy [n][k][oh][ow] and writes all of dx
+ * [n][c][h][w] (residual must be NULL). A LinearShift is the case
+ * h = w = r = s = 1. DS_ERR_UNSUPPORTED when a phase's window exceeds 3 x 3
+ * (r or s above 3 at stride 1, above 6 at stride 2). ds_jit_conv_query reports
+ * the code of all phases. Other errors as for ds_jit_conv_create. */
+ds_status ds_jit_conv_backward_data_create(const uint32_t *w_packed, int64_t n, int64_t c,
+                                           int64_t h, int64_t w, int64_t k, int64_t r, int64_t s,
+                                           int32_t stride_h, int32_t stride_w, int32_t pad_h,
+                                           int32_t pad_w, uint32_t flags, int32_t splits,
+                                           ds_jit_conv **plan);
+
 /* Static text for a status code. */
 const char *ds_status_string(ds_status status);
 

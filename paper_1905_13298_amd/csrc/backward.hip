@@ -53,6 +53,44 @@ Axis phase_axis(int in, int out_fwd, int R, int stride, int pad, int a)
     return ax;
 }
 
+}  // namespace
+
+std::vector<GradPhase> grad_phases(const ConvGeom &g)
+{
+    std::vector<GradPhase> out;
+    const bool single = g.sh == 1 && g.sw == 1;
+    for (int a = 0; a < g.sh; ++a)
+        for (int b = 0; b < g.sw; ++b) {
+            const Axis ah = phase_axis(g.h, g.oh, g.r, g.sh, g.ph, a);
+            const Axis aw = phase_axis(g.w, g.ow, g.s, g.sw, g.pw, b);
+            if (ah.out == 0 || aw.out == 0) continue;  // no dx positions
+            GradPhase p;
+            p.a = a;
+            p.b = b;
+            p.r0 = ah.first;
+            p.s0 = aw.first;
+            p.ext_h = ah.ext;
+            p.ext_w = aw.ext;
+            ConvGeom &q = p.g;
+            q.n = g.n; q.c = g.k; q.h = g.oh; q.w = g.ow; q.k = g.c;
+            q.r = ah.taps; q.s = aw.taps; q.sh = 1; q.sw = 1;
+            q.ph = ah.pad; q.pw = aw.pad; q.oh = ah.out; q.ow = aw.out;
+            q.crs = g.k * q.r * q.s;
+            q.bits = 5;
+            if (!single) {
+                p.map.base = int64_t(a) * g.w + b;
+                p.map.nstride = g.c * g.h * g.w;
+                p.map.kstride = g.h * g.w;
+                p.map.rstride = g.sh * g.w;
+                p.map.cstride = g.sw;
+            }
+            out.push_back(p);
+        }
+    return out;
+}
+
+namespace {
+
 // Packed codes of one phase: row c, column j = (k * Ta + t) * Tb + u holds
 // code[k][c][r0 + sh*(Ta-1-t)][s0 + sw*(Tb-1-u)] of the forward weights; the
 // row is padded with code 15 to whole words.
@@ -121,57 +159,38 @@ bwd_direct_kernel(const int32_t *__restrict__ dy, const uint32_t *__restrict__ w
 }
 
 struct PhasePlan {
-    ConvGeom g;       // the phase's stride-1 problem on dy
-    OutMap map;
+    GradPhase ph;
     Padded pad;
-    Axis ah, aw;
-    int a, b;
     size_t word_offset;  // its re-packed codes in the scratch buffer
     int wpr;
 };
 
-// Phases of the input gradient of forward geometry g; false when one of them
-// does not fit the tiled kernel.
+// Phases of the input gradient of forward geometry g for the tiled kernel;
+// false when one of them does not fit it.
 bool plan_phases(const ConvGeom &g, std::vector<PhasePlan> &out, size_t &words)
 {
     out.clear();
     words = 0;
     const bool single = g.sh == 1 && g.sw == 1;
-    for (int a = 0; a < g.sh; ++a)
-        for (int b = 0; b < g.sw; ++b) {
-            PhasePlan p;
-            p.a = a;
-            p.b = b;
-            p.ah = phase_axis(g.h, g.oh, g.r, g.sh, g.ph, a);
-            p.aw = phase_axis(g.w, g.ow, g.s, g.sw, g.pw, b);
-            if (p.ah.out == 0 || p.aw.out == 0) continue;  // no dx positions
-            ConvGeom &q = p.g;
-            q.n = g.n; q.c = g.k; q.h = g.oh; q.w = g.ow; q.k = g.c;
-            q.r = p.ah.taps; q.s = p.aw.taps; q.sh = 1; q.sw = 1;
-            q.ph = p.ah.pad; q.pw = p.aw.pad; q.oh = p.ah.out; q.ow = p.aw.out;
-            q.crs = g.k * q.r * q.s;
-            if (!single) {
-                p.map.base = int64_t(a) * g.w + b;
-                p.map.nstride = g.c * g.h * g.w;
-                p.map.kstride = g.h * g.w;
-                p.map.rstride = g.sh * g.w;
-                p.map.cstride = g.sw;
+    for (const GradPhase &ph : grad_phases(g)) {
+        PhasePlan p;
+        p.ph = ph;
+        p.wpr = 0;
+        const ConvGeom &q = ph.g;
+        if (q.r > 0 && q.s > 0) {
+            if (q.ph < 0 || q.pw < 0) return false;
+            if (ph.ext_h != q.h + 2 * q.ph || ph.ext_w != q.w + 2 * q.pw) {
+                if (single) return false;   // keeps the single phase on the dense path
+                p.pad.vh = ph.ext_h;
+                p.pad.iwp = ph.ext_w;
             }
-            p.wpr = 0;
-            if (q.r > 0 && q.s > 0) {
-                if (q.ph < 0 || q.pw < 0) return false;
-                if (p.ah.ext != q.h + 2 * q.ph || p.aw.ext != q.w + 2 * q.pw) {
-                    if (single) return false;   // keeps the single phase on the dense path
-                    p.pad.vh = p.ah.ext;
-                    p.pad.iwp = p.aw.ext;
-                }
-                if (!tiled_fits(q, p.pad)) return false;
-                p.wpr = int(row_words(q.crs));
-                p.word_offset = words;
-                words += (size_t(q.k) * p.wpr + 63) / 64 * 64;
-            }
-            out.push_back(p);
+            if (!tiled_fits(q, p.pad)) return false;
+            p.wpr = int(row_words(q.crs));
+            p.word_offset = words;
+            words += (size_t(q.k) * p.wpr + 63) / 64 * 64;
         }
+        out.push_back(p);
+    }
     return true;
 }
 
@@ -192,21 +211,22 @@ hipError_t run_backward_data(const ConvGeom &g, const int32_t *dy, const uint32_
     hipError_t e = words ? scratch_alloc(&scratch, words * 4, st) : hipSuccess;
     if (e != hipSuccess) return e;
     uint32_t *packed = static_cast<uint32_t *>(scratch);
-    for (const PhasePlan &p : phases) {
+    for (const PhasePlan &pp : phases) {
         if (e != hipSuccess) break;
+        const GradPhase &p = pp.ph;
         if (p.g.r == 0 || p.g.s == 0) {  // no taps reach these rows or columns
             e = run_fill_mapped(p.g, nullptr, dx, p.map, st);
             continue;
         }
-        uint32_t *pw = packed + p.word_offset;
-        const int64_t total = int64_t(p.g.k) * p.wpr;
+        uint32_t *pw = packed + pp.word_offset;
+        const int64_t total = int64_t(p.g.k) * pp.wpr;
         const int grid = int(std::min<int64_t>((total + 255) / 256, 4096));
         hipLaunchKernelGGL(repack_phase_kernel, dim3(grid), dim3(256), 0, st, wp, fmt, g.k, g.c, g.r,
-                           g.s, wpr, p.ah.first, p.aw.first, g.sh, g.sw, p.g.r, p.g.s, p.wpr, pw);
+                           g.s, wpr, p.r0, p.s0, g.sh, g.sw, p.g.r, p.g.s, pp.wpr, pw);
         e = hipGetLastError();
         if (e == hipSuccess)
             e = run_conv(p.g, dy, pw, nullptr, nullptr, dx, Inner::Shift, st, Epilogue(), p.map,
-                         p.pad);
+                         pp.pad);
     }
     const hipError_t ef = scratch ? hipFreeAsync(scratch, st) : hipSuccess;
     return e != hipSuccess ? e : ef;
@@ -221,15 +241,16 @@ void describe_backward(const ConvGeom &g, char *buf, size_t len)
         return;
     }
     size_t used = size_t(snprintf(buf, len, "phases%zu", phases.size()));
-    for (const PhasePlan &p : phases) {
+    for (const PhasePlan &pp : phases) {
         if (used >= len) break;
+        const ConvGeom &q = pp.ph.g;
         char sub[96];
-        if (p.g.r == 0 || p.g.s == 0)
+        if (q.r == 0 || q.s == 0)
             snprintf(sub, sizeof sub, "zero");
         else
-            describe_conv(p.g, sub, sizeof sub);
-        used += size_t(snprintf(buf + used, len - used, "%s%dx%d %s", used ? "; " : "", p.g.r,
-                                p.g.s, sub));
+            describe_conv(q, sub, sizeof sub);
+        used += size_t(snprintf(buf + used, len - used, "%s%dx%d %s", used ? "; " : "", q.r,
+                                q.s, sub));
     }
 }
 

@@ -190,20 +190,17 @@ fill_init_kernel(const int32_t *__restrict__ init, int32_t *__restrict__ y, int6
         y[idx] = init[(idx / OHOW) % K];
 }
 
-// y[map(n, k, oh, ow)] = init[k] (0 without init) over a problem's output grid.
+// y[map(n, k, oh, ow)] = init[k] (0 without init) over a problem's output grid
+// (fewer than 2^31 elements; flat index split with multiply-shift division).
 __global__ void __launch_bounds__(256)
-fill_mapped_kernel(const int32_t *__restrict__ init, int32_t *__restrict__ y, int64_t total, int K,
-                   int OH, int OW, OutMap m)
+fill_mapped_kernel(const int32_t *__restrict__ init, int32_t *__restrict__ y, int total,
+                   FastDiv div_ow, FastDiv div_oh, FastDiv div_k, OutMap m)
 {
-    for (int64_t idx = int64_t(blockIdx.x) * blockDim.x + threadIdx.x; idx < total;
-         idx += int64_t(gridDim.x) * blockDim.x) {
-        const int ow = int(idx % OW);
-        int64_t t = idx / OW;
-        const int oh = int(t % OH);
-        t /= OH;
-        const int k = int(t % K);
-        const int64_t n = t / K;
-        y[m.base + n * m.nstride + int64_t(k) * m.kstride + int64_t(oh) * m.rstride +
+    for (int idx = int(blockIdx.x) * 256 + int(threadIdx.x); idx < total; idx += int(gridDim.x) * 256) {
+        const int t = fdiv(idx, div_ow), ow = idx - t * int(div_ow.d);
+        const int u = fdiv(t, div_oh), oh = t - u * int(div_oh.d);
+        const int n = fdiv(u, div_k), k = u - n * int(div_k.d);
+        y[m.base + int64_t(n) * m.nstride + int64_t(k) * m.kstride + int64_t(oh) * m.rstride +
           int64_t(ow) * m.cstride] = init ? init[k] : 0;
     }
 }
@@ -812,9 +809,12 @@ hipError_t run_fill_mapped(const ConvGeom &g, const int32_t *init, int32_t *y, c
         m.cstride = 1;
     }
     const int64_t total = int64_t(g.n) * g.k * g.oh * g.ow;
+    if (total <= 0) return hipSuccess;
+    if (total > INT32_MAX) return hipErrorInvalidValue;
     const int grid = int(std::min<int64_t>((total + 255) / 256, 8192));
-    hipLaunchKernelGGL(fill_mapped_kernel, dim3(grid), dim3(256), 0, st, init, y, total, g.k, g.oh,
-                       g.ow, m);
+    hipLaunchKernelGGL(fill_mapped_kernel, dim3(grid), dim3(256), 0, st, init, y, int(total),
+                       make_fastdiv(uint32_t(g.ow)), make_fastdiv(uint32_t(g.oh)),
+                       make_fastdiv(uint32_t(g.k)), m);
     return hipGetLastError();
 }
 

@@ -4,6 +4,7 @@
 #include <hip/hip_runtime.h>
 
 #include <cstdint>
+#include <vector>
 
 #include "common.hpp"
 
@@ -59,6 +60,22 @@ hipError_t run_conv(const ConvGeom &g, const int32_t *x, const uint32_t *wpacked
                     const int32_t *wint, const int32_t *bias, int32_t *y, Inner op,
                     hipStream_t stream, const Epilogue &epi = Epilogue(),
                     const OutMap &map = OutMap(), const Padded &pad = Padded());
+
+// One stride phase of the input gradient of a forward layer (backward.hip): the
+// stride-1 correlation of dy that produces the dx rows a + sh*i and columns
+// b + sw*j, with the phase's taps in reverse order.
+struct GradPhase {
+    ConvGeom g;        // the phase's problem: input dy [n][k][oh][ow], output channels c
+    OutMap map;        // its place in dx (the dense default for a stride-1 layer)
+    int a, b;          // row and column residues
+    int r0, s0;        // first forward tap row and column of the phase
+    int ext_h, ext_w;  // padded extents the phase's window staging needs
+};
+
+// The phases of the input gradient of forward layer g, in (a, b) order, leaving
+// out residues with no dx positions; a phase that no tap reaches has g.r == 0
+// or g.s == 0 (its dx positions are zero).
+std::vector<GradPhase> grad_phases(const ConvGeom &g);
 
 // Whether run_conv runs g (with `pad`) on the tiled kernel rather than the
 // one-thread-per-output kernel.

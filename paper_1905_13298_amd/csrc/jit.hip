@@ -125,16 +125,29 @@ public:
 };
 
 struct Spec {
-    ConvGeom g;
-    const uint32_t *wp;  // host packed codes [k][rw], codes of fmt.bits bits
-    int64_t rw;
+    ConvGeom g{};
+    const uint32_t *wp = nullptr;  // host packed codes [k][rw], codes of fmt.bits bits
+    int64_t rw = 0;
     CodeFmt fmt;
-    const int32_t *bias, *mul, *add;
-    int mul_shift;
-    bool relu, residual;
-    int nsplit, kgroups, nseg, tiles_p;
+    const int32_t *bias = nullptr, *mul = nullptr, *add = nullptr;  // host, [k] or NULL
+    int mul_shift = 0;
+    bool relu = false, residual = false;
+    int nsplit = 1, kgroups = 0, nseg = 0, tiles_p = 0;
     int slots = 8;       // loads in flight per wave
+    OutMap map;          // where output (n, k, oh, ow) goes in y (dense by default)
 };
+
+// Element strides of the output map of a spec (the dense layout when unset).
+inline OutMap full_map(const Spec &sp)
+{
+    if (!sp.map.dense()) return sp.map;
+    OutMap m;
+    m.kstride = sp.g.oh * sp.g.ow;
+    m.nstride = sp.g.k * m.kstride;
+    m.rstride = sp.g.ow;
+    m.cstride = 1;
+    return m;
+}
 
 inline int code_at(const Spec &sp, int k, int j)
 {
@@ -151,7 +164,7 @@ void emit_segment(Emitter &e, const Spec &sp, int kg, int c0, int c1, bool split
     const int kbase = kg * kTN, jn = std::min(kTN, g.k - kbase);
     const int RS = g.r * g.s, E = (c1 - c0) * RS;
     const uint32_t cstride = uint32_t(g.h) * uint32_t(g.w) * 4u;
-    const uint32_t kstride = uint32_t(g.oh) * uint32_t(g.ow) * 4u;
+    const uint32_t kstride = uint32_t(full_map(sp).kstride) * 4u;
 
     for (int j = 0; j < jn; ++j)
         e.mov_imm(kAcc + j, (!split && sp.bias) ? sp.bias[kbase + j] : 0);
@@ -352,56 +365,27 @@ struct CreateArgs {
     int splits;
 };
 
-// Validation and planning shared by ds_jit_conv_create and ds_jit_conv_image.
-ds_status plan_spec(const CreateArgs &a, Spec &sp)
+// Planning of a spec whose geometry, codes and epilogue are set: code width
+// checks, pixel tiles, segments and the split of the reduction.
+ds_status finish_spec(Spec &sp, int bits, int splits)
 {
-    if (!a.wp) return fail(DS_ERR_NULL_POINTER, "w_packed must not be NULL");
-    if (a.n <= 0 || a.c <= 0 || a.h <= 0 || a.w <= 0 || a.k <= 0 || a.r <= 0 || a.s <= 0)
-        return fail(DS_ERR_INVALID_SHAPE, "all sizes must be > 0");
-    if (a.sh < 1 || a.sw < 1 || a.ph < 0 || a.pw < 0)
-        return fail(DS_ERR_INVALID_ARG, "stride must be >= 1 and padding >= 0");
-    if (a.flags & ~(DS_RELU | DS_JIT_RESIDUAL | 0xF00u)) return fail(DS_ERR_INVALID_ARG, "unknown flags");
-    const int bits = flags_code_bits(a.flags);
-    if (bits < 0) return fail(DS_ERR_INVALID_ARG, "DS_CODE_BITS must be 2..5 (or 0 for 5)");
-    if (a.add && !a.mul) return fail(DS_ERR_INVALID_ARG, "add needs mul");
-    if (a.mul && (a.mul_shift < 0 || a.mul_shift > 31))
-        return fail(DS_ERR_INVALID_ARG, "mul_shift must be in [0, 31]");
-    if (a.splits < 0) return fail(DS_ERR_INVALID_ARG, "splits must be >= 0");
-    if (a.r > kMaxTaps || a.s > kMaxTaps)
-        return fail(DS_ERR_UNSUPPORTED, "kernels larger than 3 x 3 are not supported");
-    const int64_t oh = a.h + 2 * int64_t(a.ph) - a.r, ow = a.w + 2 * int64_t(a.pw) - a.s;
-    if (oh < 0 || ow < 0) return fail(DS_ERR_INVALID_SHAPE, "kernel larger than the padded input");
-    ConvGeom &g = sp.g;
-    g.oh = int(oh / a.sh + 1);
-    g.ow = int(ow / a.sw + 1);
-    const int64_t xe = prod({a.n, a.c, a.h, a.w}), ye = prod({a.n, a.k, int64_t(g.oh), int64_t(g.ow)});
-    const int64_t crs = prod({a.c, a.r, a.s});
-    if (xe < 0 || ye < 0 || xe > kMaxElems || ye > kMaxElems || crs > kMaxElems ||
-        a.h + 2 * int64_t(a.ph) > kMaxElems || a.w + 2 * int64_t(a.pw) > kMaxElems)
-        return fail(DS_ERR_UNSUPPORTED, "tensors with 2^31 or more elements are not supported");
-    g.n = int(a.n); g.c = int(a.c); g.h = int(a.h); g.w = int(a.w); g.k = int(a.k);
-    g.r = int(a.r); g.s = int(a.s); g.sh = a.sh; g.sw = a.sw; g.ph = a.ph; g.pw = a.pw;
-    g.crs = int(crs);
-    sp.wp = a.wp;
+    const ConvGeom &g = sp.g;
     sp.fmt = code_fmt(bits);
-    sp.rw = row_words_bits(crs, bits);
+    sp.rw = row_words_bits(g.crs, bits);
     const int used = sp.fmt.per_word * bits;
-    for (int64_t i = 0; used < 32 && i < a.k * sp.rw; ++i)
-        if (a.wp[i] >> used)
+    for (int64_t i = 0; used < 32 && i < int64_t(g.k) * sp.rw; ++i)
+        if (sp.wp[i] >> used)
             return fail(DS_ERR_INVALID_CODE, "bits %d-31 of packed word %lld are not 0", used, (long long)i);
-    sp.bias = a.bias; sp.mul = a.mul; sp.add = a.add; sp.mul_shift = a.mul ? a.mul_shift : 0;
-    sp.relu = a.flags & DS_RELU;
-    sp.residual = a.flags & DS_JIT_RESIDUAL;
     const int64_t nq = int64_t(g.n) * g.oh * g.ow;
     sp.tiles_p = int((nq + kBlockPixels - 1) / kBlockPixels);
     sp.kgroups = (g.k + kTN - 1) / kTN;
     // Enough blocks to keep every compute unit busy through the tail (about 8 per
     // CU); each part keeps at least 64 reduction elements.
-    int ns = a.splits;
+    int ns = splits;
     if (ns == 0) {
         const int64_t base = int64_t(sp.tiles_p) * sp.kgroups;
         const int64_t want = (2048 + base - 1) / base;
-        const int64_t cap = std::max<int64_t>(1, crs / 64);
+        const int64_t cap = std::max<int64_t>(1, g.crs / 64);
         ns = int(std::max<int64_t>(1, std::min(want, cap)));
     }
     sp.nsplit = std::min(ns, g.c);
@@ -415,11 +399,84 @@ ds_status plan_spec(const CreateArgs &a, Spec &sp)
     return ok();
 }
 
+// Shape checks of a forward layer given by its sizes (no pointers); fills g.
+ds_status check_layer(int64_t n, int64_t c, int64_t h, int64_t w, int64_t k, int64_t r, int64_t s,
+                      int sh, int sw, int ph, int pw, int bits, ConvGeom &g)
+{
+    if (n <= 0 || c <= 0 || h <= 0 || w <= 0 || k <= 0 || r <= 0 || s <= 0)
+        return fail(DS_ERR_INVALID_SHAPE, "all sizes must be > 0");
+    if (sh < 1 || sw < 1 || ph < 0 || pw < 0)
+        return fail(DS_ERR_INVALID_ARG, "stride must be >= 1 and padding >= 0");
+    const int64_t oh = h + 2 * int64_t(ph) - r, ow = w + 2 * int64_t(pw) - s;
+    if (oh < 0 || ow < 0) return fail(DS_ERR_INVALID_SHAPE, "kernel larger than the padded input");
+    const int64_t xe = prod({n, c, h, w}), ye = prod({n, k, oh / sh + 1, ow / sw + 1});
+    const int64_t crs = prod({c, r, s});
+    // x and y are addressed through buffer resources: their sizes in bytes stay below 2^31.
+    if (xe < 0 || ye < 0 || xe > kMaxElems / 4 || ye > kMaxElems / 4 || crs > kMaxElems ||
+        h + 2 * int64_t(ph) > kMaxElems || w + 2 * int64_t(pw) > kMaxElems)
+        return fail(DS_ERR_UNSUPPORTED, "tensors of 2^31 or more bytes are not supported");
+    g = ConvGeom{int(n), int(c), int(h), int(w), int(k), int(r), int(s), sh, sw, ph, pw,
+                 int(oh / sh + 1), int(ow / sw + 1), int(crs), bits};
+    return DS_SUCCESS;
+}
+
+// Validation and planning shared by ds_jit_conv_create and ds_jit_conv_image.
+ds_status plan_spec(const CreateArgs &a, Spec &sp)
+{
+    if (!a.wp) return fail(DS_ERR_NULL_POINTER, "w_packed must not be NULL");
+    if (a.flags & ~(DS_RELU | DS_JIT_RESIDUAL | 0xF00u)) return fail(DS_ERR_INVALID_ARG, "unknown flags");
+    const int bits = flags_code_bits(a.flags);
+    if (bits < 0) return fail(DS_ERR_INVALID_ARG, "DS_CODE_BITS must be 2..5 (or 0 for 5)");
+    if (a.add && !a.mul) return fail(DS_ERR_INVALID_ARG, "add needs mul");
+    if (a.mul && (a.mul_shift < 0 || a.mul_shift > 31))
+        return fail(DS_ERR_INVALID_ARG, "mul_shift must be in [0, 31]");
+    if (a.splits < 0) return fail(DS_ERR_INVALID_ARG, "splits must be >= 0");
+    if (a.r > kMaxTaps || a.s > kMaxTaps)
+        return fail(DS_ERR_UNSUPPORTED, "kernels larger than 3 x 3 are not supported");
+    ds_status st = check_layer(a.n, a.c, a.h, a.w, a.k, a.r, a.s, a.sh, a.sw, a.ph, a.pw, bits, sp.g);
+    if (st != DS_SUCCESS) return st;
+    sp.wp = a.wp;
+    sp.bias = a.bias; sp.mul = a.mul; sp.add = a.add; sp.mul_shift = a.mul ? a.mul_shift : 0;
+    sp.relu = a.flags & DS_RELU;
+    sp.residual = a.flags & DS_JIT_RESIDUAL;
+    return finish_spec(sp, bits, a.splits);
+}
+
+// Host re-pack of the codes of one input-gradient phase (5-bit format): row c,
+// column (k * Ta + t) * Tb + u holds code[k][c][r0 + sh*(Ta-1-t)][s0 + sw*(Tb-1-u)].
+std::vector<uint32_t> repack_phase(const uint32_t *wp, const ConvGeom &fwd, const GradPhase &ph)
+{
+    const CodeFmt src = code_fmt(fwd.bits);
+    const int64_t wpr_in = row_words_bits(fwd.crs, fwd.bits);
+    const int Ta = ph.g.r, Tb = ph.g.s, cols = ph.g.crs;
+    const int64_t wpr = row_words(cols);
+    std::vector<uint32_t> out(size_t(ph.g.k) * size_t(wpr), 0u);
+    for (int c = 0; c < fwd.c; ++c)
+        for (int64_t wd = 0; wd < wpr; ++wd) {
+            uint32_t word = 0;
+            for (int j = 0; j < 6; ++j) {
+                const int64_t jp = wd * 6 + j;
+                uint32_t code = 15u;
+                if (jp < cols) {
+                    const int k = int(jp / (Ta * Tb)), rem = int(jp % (Ta * Tb));
+                    const int t = rem / Tb, u = rem % Tb;
+                    const int r = ph.r0 + fwd.sh * (Ta - 1 - t), s = ph.s0 + fwd.sw * (Tb - 1 - u);
+                    code = src.at(wp + int64_t(k) * wpr_in, (c * fwd.r + r) * fwd.s + s);
+                }
+                word |= code << (5 * j);
+            }
+            out[size_t(c) * size_t(wpr) + size_t(wd)] = word;
+        }
+    return out;
+}
+
 }  // namespace
 }  // namespace ds
 
 using namespace ds;
 
+// A plan: one generated kernel (forward), or the phases of an input gradient,
+// each a plan of its own writing its part of dx, plus the parts no tap reaches.
 struct ds_jit_conv {
     int device = -1;
     hipModule_t module = nullptr;
@@ -429,12 +486,21 @@ struct ds_jit_conv {
     int64_t code_bytes = 0;
     int32_t *init = nullptr;        // [k] bias or zeros: y's start for split-K
     int32_t *mul = nullptr, *add = nullptr;
+    bool backward = false;
+    ConvGeom fwd;                   // backward: the forward layer
+    std::vector<ds_jit_conv *> parts;
+    std::vector<GradPhase> zeros;   // backward: phases whose dx positions are 0
 };
 
 static ds_status destroy_plan(ds_jit_conv *p)
 {
     if (!p) return ok();
     hipError_t e = hipSuccess;
+    ds_status st = DS_SUCCESS;
+    for (ds_jit_conv *q : p->parts) {
+        const ds_status sq = destroy_plan(q);
+        if (st == DS_SUCCESS) st = sq;
+    }
     if (p->module) e = hipModuleUnload(p->module);
     for (int32_t *q : {p->init, p->mul, p->add})
         if (q) {
@@ -443,6 +509,7 @@ static ds_status destroy_plan(ds_jit_conv *p)
         }
     delete p;
     if (e != hipSuccess) return fail(DS_ERR_HIP, "ds_jit_conv_destroy: %s", hipGetErrorString(e));
+    if (st != DS_SUCCESS) return st;
     return ok();
 }
 
@@ -452,6 +519,50 @@ static ds_status upload(int32_t **dst, const int32_t *src, int k, bool zeros)
     hipError_t e = zeros ? hipMemset(*dst, 0, size_t(k) * 4)
                          : hipMemcpy(*dst, src, size_t(k) * 4, hipMemcpyHostToDevice);
     if (e != hipSuccess) return fail(DS_ERR_HIP, "upload: %s", hipGetErrorString(e));
+    return ok();
+}
+
+// Generates, loads and completes the plan of one planned spec (host bias, mul
+// and add as in the spec; they are not kept).
+static ds_status build_plan(const Spec &spec, ds_jit_conv **out)
+{
+    *out = nullptr;
+    ds_jit_conv *p = new ds_jit_conv;
+    p->sp = spec;
+    std::vector<uint8_t> img;
+    const std::vector<uint32_t> body = generate_body(p->sp);
+    p->code_bytes = int64_t(body.size()) * 4;
+    ds_status st = splice_body(body, img);
+    if (st != DS_SUCCESS) {
+        delete p;
+        return st;
+    }
+    if (hipGetDevice(&p->device) != hipSuccess) {
+        delete p;
+        return fail(DS_ERR_HIP, "no HIP device");
+    }
+    hipError_t e = hipModuleLoadData(&p->module, img.data());
+    if (e == hipSuccess) e = hipModuleGetFunction(&p->fn, p->module, "ds_jit_conv_template");
+    if (e != hipSuccess) {
+        destroy_plan(p);
+        return fail(DS_ERR_HIP, "loading the generated code: %s", hipGetErrorString(e));
+    }
+    const int K = p->sp.g.k;
+    // What the separate split-K passes need is copied to the device here.
+    if (p->sp.nsplit > 1) {
+        st = upload(&p->init, spec.bias, K, !spec.bias);
+        if (st == DS_SUCCESS && spec.mul) st = upload(&p->mul, spec.mul, K, false);
+        if (st == DS_SUCCESS && spec.add) st = upload(&p->add, spec.add, K, false);
+        if (st != DS_SUCCESS) {
+            const std::string msg = last_error();
+            destroy_plan(p);
+            return fail(st, "%s", msg.c_str());
+        }
+    }
+    p->sp.bias = p->sp.mul = p->sp.add = nullptr;
+    p->sp.wp = nullptr;
+    p->group_tiles = std::max(1, env_int("DS_JIT_GROUP_TILES", 16));
+    *out = p;
     return ok();
 }
 
@@ -492,53 +603,75 @@ extern "C" ds_status ds_jit_conv_create(const uint32_t *w_packed, const int32_t 
 {
     if (!plan) return fail(DS_ERR_NULL_POINTER, "plan must not be NULL");
     *plan = nullptr;
-    ds_jit_conv *p = nullptr;
     try {
-        p = new ds_jit_conv;
+        Spec sp;
         const CreateArgs a{w_packed, bias, mul, add, mul_shift, n, c, h, w, k, r, s,
                            stride_h, stride_w, pad_h, pad_w, flags, splits};
-        ds_status st = plan_spec(a, p->sp);
-        if (st != DS_SUCCESS) {
-            delete p;
-            return st;
-        }
-        std::vector<uint8_t> img;
-        const std::vector<uint32_t> body = generate_body(p->sp);
-        p->code_bytes = int64_t(body.size()) * 4;
-        st = splice_body(body, img);
-        if (st != DS_SUCCESS) {
-            delete p;
-            return st;
-        }
+        ds_status st = plan_spec(a, sp);
+        if (st != DS_SUCCESS) return st;
+        return build_plan(sp, plan);
+    } catch (const std::bad_alloc &) {
+        return fail(DS_ERR_HIP, "out of host memory");
+    }
+}
+
+extern "C" ds_status ds_jit_conv_backward_data_create(const uint32_t *w_packed, int64_t n,
+                                                      int64_t c, int64_t h, int64_t w, int64_t k,
+                                                      int64_t r, int64_t s, int32_t stride_h,
+                                                      int32_t stride_w, int32_t pad_h,
+                                                      int32_t pad_w, uint32_t flags,
+                                                      int32_t splits, ds_jit_conv **plan)
+{
+    if (!plan) return fail(DS_ERR_NULL_POINTER, "plan must not be NULL");
+    *plan = nullptr;
+    if (!w_packed) return fail(DS_ERR_NULL_POINTER, "w_packed must not be NULL");
+    const int bits = flags_code_bits(flags);
+    if ((flags & ~0xF00u) != 0 || bits < 0)
+        return fail(DS_ERR_INVALID_ARG, "flags must be 0 apart from DS_CODE_BITS(2..5)");
+    if (splits < 0) return fail(DS_ERR_INVALID_ARG, "splits must be >= 0");
+    ds_jit_conv *p = nullptr;
+    try {
+        ConvGeom g;
+        ds_status st = check_layer(n, c, h, w, k, r, s, stride_h, stride_w, pad_h, pad_w, bits, g);
+        if (st != DS_SUCCESS) return st;
+        const std::vector<GradPhase> phases = grad_phases(g);
+        for (const GradPhase &ph : phases)
+            if (ph.g.r > kMaxTaps || ph.g.s > kMaxTaps)
+                return fail(DS_ERR_UNSUPPORTED, "a stride phase has a window larger than 3 x 3");
+        const CodeFmt fmt = code_fmt(bits);
+        const int64_t rw = row_words_bits(g.crs, bits);
+        const int used = fmt.per_word * bits;
+        for (int64_t i = 0; used < 32 && i < int64_t(g.k) * rw; ++i)
+            if (w_packed[i] >> used)
+                return fail(DS_ERR_INVALID_CODE, "bits %d-31 of packed word %lld are not 0", used, (long long)i);
+        p = new ds_jit_conv;
+        p->backward = true;
+        p->fwd = g;
         if (hipGetDevice(&p->device) != hipSuccess) {
             delete p;
             return fail(DS_ERR_HIP, "no HIP device");
         }
-        hipError_t e = hipModuleLoadData(&p->module, img.data());
-        if (e == hipSuccess) e = hipModuleGetFunction(&p->fn, p->module, "ds_jit_conv_template");
-        if (e != hipSuccess) {
-            destroy_plan(p);
-            return fail(DS_ERR_HIP, "loading the generated code: %s", hipGetErrorString(e));
-        }
-        const int K = p->sp.g.k;
-        // The bias, mul and add pointers are host memory and not kept: what the
-        // separate split-K passes need is copied to the device here.
-        if (p->sp.nsplit > 1) {
-            st = upload(&p->init, bias, K, !bias);
-            if (st == DS_SUCCESS && mul) st = upload(&p->mul, mul, K, false);
-            if (st == DS_SUCCESS && add) st = upload(&p->add, add, K, false);
+        for (const GradPhase &ph : phases) {
+            if (ph.g.r == 0 || ph.g.s == 0) {
+                p->zeros.push_back(ph);
+                continue;
+            }
+            const std::vector<uint32_t> codes = repack_phase(w_packed, g, ph);
+            Spec sp;
+            sp.g = ph.g;
+            sp.wp = codes.data();
+            sp.map = ph.map;
+            st = finish_spec(sp, 5, splits);
+            ds_jit_conv *part = nullptr;
+            if (st == DS_SUCCESS) st = build_plan(sp, &part);
             if (st != DS_SUCCESS) {
                 const std::string msg = last_error();
                 destroy_plan(p);
                 return fail(st, "%s", msg.c_str());
             }
+            p->code_bytes += part->code_bytes;
+            p->parts.push_back(part);
         }
-        p->sp.bias = p->sp.mul = p->sp.add = nullptr;
-        p->sp.wp = nullptr;
-        // 16 pixel tiles per group: their inputs stay in L2 while the group's segments
-        // go by (the same sweep: 64 was up to 1.6x slower on layers with many output
-        // channels; 4, 8 and 16 within a few percent of each other, 16 the best).
-        p->group_tiles = std::max(1, env_int("DS_JIT_GROUP_TILES", 16));
         *plan = p;
         return ok();
     } catch (const std::bad_alloc &) {
@@ -547,42 +680,28 @@ extern "C" ds_status ds_jit_conv_create(const uint32_t *w_packed, const int32_t 
     }
 }
 
-extern "C" ds_status ds_jit_conv_run(const ds_jit_conv *plan, const int32_t *x,
-                                     const int32_t *residual, int32_t *y, void *stream)
+// Enqueues one generated kernel (with its split-K fill and epilogue passes).
+static hipError_t run_part(const ds_jit_conv *plan, const int32_t *x, const int32_t *residual,
+                           int32_t *y, int64_t x_bytes, int64_t y_bytes, hipStream_t st)
 {
-    if (!plan || !x || !y) return fail(DS_ERR_NULL_POINTER, "plan, x and y must not be NULL");
     const Spec &sp = plan->sp;
     const ConvGeom &g = sp.g;
-    if (sp.residual != (residual != nullptr))
-        return fail(DS_ERR_INVALID_ARG, sp.residual ? "the plan adds a residual: residual must not be NULL"
-                                                    : "the plan adds no residual: residual must be NULL");
-    int dev = -1;
-    if (hipGetDevice(&dev) != hipSuccess || dev != plan->device)
-        return fail(DS_ERR_INVALID_ARG, "the plan was made on device %d, the current device is %d", plan->device, dev);
-    const int64_t xb = int64_t(g.n) * g.c * g.h * g.w * 4;
-    const int64_t yb = int64_t(g.n) * g.k * g.oh * g.ow * 4;
-    if (overlap(x, xb, y, yb)) return fail(DS_ERR_INVALID_ARG, "y overlaps x");
-    if (residual && overlap(residual, yb, y, yb)) return fail(DS_ERR_INVALID_ARG, "y overlaps residual");
-    if (!device_range_ok(x, xb)) return fail(DS_ERR_INVALID_ARG, "x is not a device buffer of %lld bytes", (long long)xb);
-    if (!device_range_ok(y, yb)) return fail(DS_ERR_INVALID_ARG, "y is not a device buffer of %lld bytes", (long long)yb);
-    if (residual && !device_range_ok(residual, yb))
-        return fail(DS_ERR_INVALID_ARG, "residual is not a device buffer of %lld bytes", (long long)yb);
-
-    hipStream_t st = static_cast<hipStream_t>(stream);
+    const OutMap m = full_map(sp);
     const bool split = sp.nsplit > 1;
     hipError_t e = hipSuccess;
-    if (split) e = run_fill_init(g, plan->init, y, st);
+    if (split) e = run_fill_mapped(g, plan->init, y, sp.map, st);
     if (e == hipSuccess) {
         JitArgs a;
         a.x = x;
         a.y = y;
         a.residual = split ? nullptr : residual;
-        a.x_bytes = int(xb);
-        a.y_bytes = int(yb);
+        a.x_bytes = int(x_bytes);
+        a.y_bytes = int(y_bytes);
         a.OHOW = g.oh * g.ow;
         a.NQ = g.n * a.OHOW;
         a.OW = g.ow; a.H = g.h; a.W = g.w; a.C = g.c; a.K = g.k; a.HW = g.h * g.w;
         a.sh = g.sh; a.sw = g.sw; a.ph = g.ph; a.pw = g.pw;
+        a.ybase = int(m.base); a.ynst = m.nstride; a.yrst = m.rstride; a.ycst = m.cstride;
         a.tiles_p = sp.tiles_p;
         a.group_tiles = std::min(plan->group_tiles, sp.tiles_p);
         a.nseg = sp.nseg;
@@ -601,6 +720,42 @@ extern "C" ds_status ds_jit_conv_run(const ds_jit_conv *plan, const int32_t *x,
         epi.relu = sp.relu;
         if (epi.any()) e = run_epilogue(g, y, epi, st);
     }
+    return e;
+}
+
+extern "C" ds_status ds_jit_conv_run(const ds_jit_conv *plan, const int32_t *x,
+                                     const int32_t *residual, int32_t *y, void *stream)
+{
+    if (!plan || !x || !y) return fail(DS_ERR_NULL_POINTER, "plan, x and y must not be NULL");
+    const bool res_wanted = !plan->backward && plan->sp.residual;
+    if (res_wanted != (residual != nullptr))
+        return fail(DS_ERR_INVALID_ARG, res_wanted ? "the plan adds a residual: residual must not be NULL"
+                                                   : "the plan adds no residual: residual must be NULL");
+    int dev = -1;
+    if (hipGetDevice(&dev) != hipSuccess || dev != plan->device)
+        return fail(DS_ERR_INVALID_ARG, "the plan was made on device %d, the current device is %d", plan->device, dev);
+    // Forward: x [n][c][h][w] -> y [n][k][oh][ow]; input gradient: dy -> dx of the forward layer.
+    const ConvGeom &g = plan->backward ? plan->fwd : plan->sp.g;
+    const int64_t fx = int64_t(g.n) * g.c * g.h * g.w * 4, fy = int64_t(g.n) * g.k * g.oh * g.ow * 4;
+    const int64_t xb = plan->backward ? fy : fx, yb = plan->backward ? fx : fy;
+    const char *xn = plan->backward ? "dy" : "x", *yn = plan->backward ? "dx" : "y";
+    if (overlap(x, xb, y, yb)) return fail(DS_ERR_INVALID_ARG, "%s overlaps %s", yn, xn);
+    if (residual && overlap(residual, yb, y, yb)) return fail(DS_ERR_INVALID_ARG, "y overlaps residual");
+    if (!device_range_ok(x, xb)) return fail(DS_ERR_INVALID_ARG, "%s is not a device buffer of %lld bytes", xn, (long long)xb);
+    if (!device_range_ok(y, yb)) return fail(DS_ERR_INVALID_ARG, "%s is not a device buffer of %lld bytes", yn, (long long)yb);
+    if (residual && !device_range_ok(residual, yb))
+        return fail(DS_ERR_INVALID_ARG, "residual is not a device buffer of %lld bytes", (long long)yb);
+
+    hipStream_t st = static_cast<hipStream_t>(stream);
+    hipError_t e = hipSuccess;
+    if (!plan->backward) {
+        e = run_part(plan, x, residual, y, xb, yb, st);
+    } else {
+        for (const GradPhase &z : plan->zeros)
+            if (e == hipSuccess) e = run_fill_mapped(z.g, nullptr, y, z.map, st);
+        for (const ds_jit_conv *part : plan->parts)
+            if (e == hipSuccess) e = run_part(part, x, nullptr, y, xb, yb, st);
+    }
     if (e != hipSuccess) return fail(DS_ERR_HIP, "ds_jit_conv_run: %s", hipGetErrorString(e));
     return ok();
 }
@@ -611,8 +766,13 @@ extern "C" ds_status ds_jit_conv_query(const ds_jit_conv *plan, int64_t *code_by
                                        int32_t *segments, int32_t *splits)
 {
     if (!plan) return fail(DS_ERR_NULL_POINTER, "plan must not be NULL");
+    int32_t seg = plan->backward ? 0 : plan->sp.nseg, sp = plan->backward ? 0 : plan->sp.nsplit;
+    for (const ds_jit_conv *q : plan->parts) {
+        seg += q->sp.nseg;
+        sp = std::max(sp, q->sp.nsplit);
+    }
     if (code_bytes) *code_bytes = plan->code_bytes;
-    if (segments) *segments = plan->sp.nseg;
-    if (splits) *splits = plan->sp.nsplit;
+    if (segments) *segments = seg;
+    if (splits) *splits = sp;
     return ok();
 }

@@ -15,6 +15,7 @@ struct JitArgs {
     const int32_t *residual;  // NULL when the layer adds none
     int x_bytes, y_bytes;
     int NQ, OHOW, OW, H, W, C, K, HW, sh, sw, ph, pw;
+    int ybase, ynst, yrst, ycst;  // output (n, oh, ow) of channel 0 at y[ybase + n*ynst + oh*yrst + ow*ycst]
     int tiles_p;              // workgroups (4 waves x 64 pixels) per segment
     int group_tiles;          // pixel tiles that run all segments before the next tiles
     int nseg;

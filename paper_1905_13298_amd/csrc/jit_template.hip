@@ -52,7 +52,7 @@ extern "C" __global__ void __launch_bounds__(256) ds_jit_conv_template(const Jit
         const int pix = q - n * p.OHOW;
         const int oh = ds::fdiv(pix, p.div_ow);
         const int ow = pix - oh * p.OW;
-        yoff = (n * p.K * p.OHOW + pix) * 4;
+        yoff = (p.ybase + n * p.ynst + oh * p.yrst + ow * p.ycst) * 4;
         const int ih0 = oh * p.sh - p.ph, iw0 = ow * p.sw - p.pw, base = n * p.C * p.HW;
         // Taps of a 3 x 3 window (r, s) = (t / 3, t % 3); a 1 x 1 layer uses t0 only.
         auto off = [&](int rr, int ss) {

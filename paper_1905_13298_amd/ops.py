@@ -18,7 +18,7 @@ __all__ = ["DeepShiftError", "code_bits_flag", "describe_conv2d", "packed_row_wo
            "quantize_shift_weights_q", "quantize_shift_weights_q_many", "quantize_shift_weights_ps",
            "to_fixed_point", "conv2d_shift_fused", "maxpool2d", "avgpool2d_global", "DS_RELU",
            "DS_JIT_RESIDUAL", "JitConv", "jit_conv_image", "conv2d_shift_backward_data",
-           "linear_shift_backward_data", "describe_conv2d_backward_data"]
+           "linear_shift_backward_data", "describe_conv2d_backward_data", "JitConvBackwardData"]
 
 DS_RELU = 1
 
@@ -453,3 +453,31 @@ class JitConv:
             self.close()
         except Exception:
             pass
+
+
+class JitConvBackwardData(JitConv):
+    """A weight-specialised plan for the input gradient of a ConvShift layer
+    (``ds_jit_conv_backward_data_create``): ``plan(dy)`` returns dx. The arguments
+    describe the forward layer (x_shape = its input)."""
+
+    def __init__(self, w_packed, x_shape, kernel_size, stride=1, padding=0, splits: int = 0,
+                 device="cuda:0", code_bits: int = 5):
+        self.k = int(w_packed.shape[0])
+        wp, _, _, _ = _jit_args(w_packed, self.k, None, None, None)
+        n, c, h, w = (int(v) for v in x_shape)
+        r, s = _pair(kernel_size)
+        sh, sw = _pair(stride)
+        ph, pw = _pair(padding)
+        self.x_shape = (n, self.k, out_size(h, ph, r, sh), out_size(w, pw, s, sw))   # dy
+        self.y_shape = (n, c, h, w)                                                  # dx
+        self.device = torch.device(device)
+        self.residual = False
+        handle = ctypes.c_void_p()
+        with torch.cuda.device(self.device):
+            call("ds_jit_conv_backward_data_create", _np_ptr(wp), n, c, h, w, self.k, r, s, sh, sw,
+                 ph, pw, code_bits_flag(code_bits), splits, ctypes.byref(handle))
+        self._h = handle
+        cb, seg, sp = ctypes.c_int64(), ctypes.c_int32(), ctypes.c_int32()
+        call("ds_jit_conv_query", self._h, ctypes.byref(cb), ctypes.byref(seg), ctypes.byref(sp))
+        self.code_bytes, self.segments, self.splits = cb.value, seg.value, sp.value
+        self.pixel_tiles = -(-(n * h * w) // 256)

@@ -171,3 +171,73 @@ def test_resnet50_full_batch_against_gather_kernel_and_oracle(monkeypatch):
                                                         stride=L.stride, pad=L.pad)
         np.testing.assert_array_equal(got, want, err_msg=L.name)
         del dx, ref, dyd
+
+
+JIT_EDGE = [e for e in EDGE if e[0] != "s2_7x7_stem"]
+
+
+@pytest.mark.parametrize("splits", [0, 1, 3])
+@pytest.mark.parametrize("spec", JIT_EDGE, ids=[e[0] for e in JIT_EDGE])
+def test_weight_specialised_plans_match_oracle(spec, splits):
+    """Input-gradient plans (one generated kernel per stride phase, writing its rows
+    and columns of dx through an output map) against the oracle."""
+    name, n, c, h, w, k, r, s, st, pd = spec
+    rr = r if np.isscalar(r) else r[0]
+    ss = s if np.isscalar(s) else s[1]
+    dy, codes, _ = make(zlib.crc32(name.encode()) + 7, n, c, h, w, k, rr, ss, st, pd)
+    plan = ops.JitConvBackwardData(ops.pack_shift_weights(codes), (n, c, h, w), (rr, ss), st, pd,
+                                   splits=splits)
+    say(f"jit backward {name} splits={splits}: {plan.segments} segments, {plan.code_bytes} code bytes")
+    out = torch.full((n, c, h, w), 0x5A5A5A5A, dtype=torch.int32, device=DEV)   # every element written
+    dx = plan(to_dev(dy), out=out).cpu().numpy()
+    want = oracle.conv2d_shift_backward_data(dy, codes, (n, c, h, w), r=rr, s=ss, stride=st, pad=pd)
+    bad = np.flatnonzero(dx.ravel() != want.ravel())
+    assert bad.size == 0, f"{bad.size} of {want.size} differ, first at {bad[:5]}"
+    plan.close()
+
+
+def test_weight_specialised_plan_limits_and_arguments():
+    codes = np.zeros((16, 3 * 49), np.uint8)
+    with pytest.raises(ops.DeepShiftError, match="UNSUPPORTED"):
+        ops.JitConvBackwardData(ops.pack_shift_weights(codes), (2, 3, 30, 30), 7, 2, 3)
+    codes = random_codes(np.random.default_rng(3), (8, 4 * 9))
+    plan = ops.JitConvBackwardData(ops.pack_shift_weights(codes), (2, 4, 8, 8), 3, 2, 1)
+    dy = torch.zeros(plan.x_shape, dtype=torch.int32, device=DEV)
+    with pytest.raises(ops.DeepShiftError, match="residual must be NULL"):
+        plan(dy, residual=torch.zeros(plan.y_shape, dtype=torch.int32, device=DEV))
+    with pytest.raises(ops.DeepShiftError, match="overlaps"):
+        big = torch.zeros(4 * 8 * 8 * 2 + 64, dtype=torch.int32, device=DEV)
+        plan(big[: dy.numel()].view(plan.x_shape), out=big[:2 * 4 * 8 * 8].view(plan.y_shape))
+    plan.close()
+
+
+def test_linear_plan_matches_oracle():
+    rng = np.random.default_rng(61)
+    dy = rng.integers(-(2 ** 31), 2 ** 31, (33, 70), dtype=np.int64).astype(np.int32)
+    codes = random_codes(rng, (70, 300))
+    plan = ops.JitConvBackwardData(ops.pack_shift_weights(codes), (33, 300, 1, 1), 1)
+    dx = plan(to_dev(dy.reshape(33, 70, 1, 1))).cpu().numpy().reshape(33, 300)
+    np.testing.assert_array_equal(dx, oracle.linear_shift_backward_data(dy, codes))
+    plan.close()
+
+
+def test_resnet50_full_batch_plans_equal_runtime_kernel():
+    """Every ResNet-50 convolution but the stem at batch 128: the plans' input
+    gradient equals ds_conv2d_shift_backward_data's on every element."""
+    layers = W.config_layers(4)
+    for li, L in enumerate(layers):
+        if L.kind != "conv" or L.name == "conv1":
+            continue
+        codes = W.gen_codes(L, W.CONFIG_SEEDS[4], li)
+        g = np.random.default_rng([4, li, 7])
+        dy = to_dev(np.rint(g.standard_normal(L.y_shape, dtype=np.float32) * 2 ** 16).astype(np.int32))
+        wp = ops.pack_shift_weights(codes)
+        plan = ops.JitConvBackwardData(wp, L.x_shape, (L.r, L.s), L.stride, L.pad)
+        say(f"jit backward resnet50 {L.name}: {plan.segments} segments, {plan.code_bytes / 2 ** 20:.1f} MiB")
+        got = plan(dy)
+        ref = ops.conv2d_shift_backward_data(dy, to_dev(wp.view(np.int32)), L.x_shape, (L.r, L.s),
+                                             L.stride, L.pad)
+        diff = int((got != ref).sum())
+        assert diff == 0, f"{L.name}: {diff} elements differ"
+        plan.close()
+        del got, ref, dy
