@@ -205,6 +205,21 @@ fill_mapped_kernel(const int32_t *__restrict__ init, int32_t *__restrict__ y, in
     }
 }
 
+// y[map(n, k, oh, ow)] = src[((n * K + k) * OH + oh) * OW + ow]: a dense result
+// scattered into its place (fewer than 2^31 elements).
+__global__ void __launch_bounds__(256)
+copy_mapped_kernel(const int32_t *__restrict__ src, int32_t *__restrict__ y, int total,
+                   FastDiv div_ow, FastDiv div_oh, FastDiv div_k, OutMap m)
+{
+    for (int idx = int(blockIdx.x) * 256 + int(threadIdx.x); idx < total; idx += int(gridDim.x) * 256) {
+        const int t = fdiv(idx, div_ow), ow = idx - t * int(div_ow.d);
+        const int u = fdiv(t, div_oh), oh = t - u * int(div_oh.d);
+        const int n = fdiv(u, div_k), k = u - n * int(div_k.d);
+        y[m.base + int64_t(n) * m.nstride + int64_t(k) * m.kstride + int64_t(oh) * m.rstride +
+          int64_t(ow) * m.cstride] = src[idx];
+    }
+}
+
 // The epilogue on one output value v of channel k at flat index o.
 __device__ __forceinline__ uint32_t apply_epilogue(uint32_t v, int k, int64_t o, const Epilogue &e)
 {
@@ -818,6 +833,19 @@ hipError_t run_fill_mapped(const ConvGeom &g, const int32_t *init, int32_t *y, c
     return hipGetLastError();
 }
 
+hipError_t run_copy_mapped(const ConvGeom &g, const int32_t *src, int32_t *y, const OutMap &map,
+                           hipStream_t st)
+{
+    const int64_t total = int64_t(g.n) * g.k * g.oh * g.ow;
+    if (total <= 0) return hipSuccess;
+    if (total > INT32_MAX || map.dense()) return hipErrorInvalidValue;
+    const int grid = int(std::min<int64_t>((total + 255) / 256, 8192));
+    hipLaunchKernelGGL(copy_mapped_kernel, dim3(grid), dim3(256), 0, st, src, y, int(total),
+                       make_fastdiv(uint32_t(g.ow)), make_fastdiv(uint32_t(g.oh)),
+                       make_fastdiv(uint32_t(g.k)), map);
+    return hipGetLastError();
+}
+
 hipError_t run_epilogue(const ConvGeom &g, int32_t *y, const Epilogue &epi, hipStream_t st)
 {
     const int64_t total = int64_t(g.n) * g.k * g.oh * g.ow;
@@ -874,11 +902,21 @@ hipError_t run_conv(const ConvGeom &g0, const int32_t *x, const uint32_t *wp, co
     p.div_vh = make_fastdiv(uint32_t(p.VH));
     p.div_iwp = make_fastdiv(uint32_t(p.IWP));
 
-    // Scratch: init[Kpad], wd[Kpad][Jpad], and x^T for row-major inputs.
+    // Split partial sums meet through int32 atomics; through a strided output map
+    // those land on scattered addresses, so a split mapped problem accumulates into
+    // a dense buffer that is scattered into place afterwards.
+    const bool via_dense = mapped && splits > 1;
+    if (via_dense) {
+        const OutMap d{0, g.k * g.oh * g.ow, g.oh * g.ow, g.ow, 1};
+        p.ybase = 0; p.ynst = d.nstride; p.ykst = d.kstride; p.yrst = d.rstride; p.ycst = d.cstride;
+    }
+    // Scratch: init[Kpad], wd[Kpad][Jpad], x^T for row-major inputs, y^T (row-major) or
+    // the dense partial sums (split mapped problems).
     const size_t init_bytes = (size_t(Kpad) * 4 + 255) & ~size_t(255);
     const size_t wd_bytes = (size_t(Kpad) * Jpad * 4 + 255) & ~size_t(255);
     const size_t xt_bytes = rowmajor ? (size_t(x_bytes) + 255) & ~size_t(255) : 0;
-    const size_t yt_bytes = rowmajor ? size_t(g0.n) * g0.k * 4 : 0;
+    const size_t yt_bytes = rowmajor ? size_t(g0.n) * g0.k * 4
+                          : via_dense ? size_t(g.n) * g.k * g.oh * g.ow * 4 : 0;
     const size_t bytes = init_bytes + wd_bytes + xt_bytes + yt_bytes;
     void *scratch = nullptr;
     hipError_t e = scratch_alloc(&scratch, bytes, st);
@@ -887,6 +925,8 @@ hipError_t run_conv(const ConvGeom &g0, const int32_t *x, const uint32_t *wp, co
     int32_t *wd = reinterpret_cast<int32_t *>(static_cast<char *>(scratch) + init_bytes);
     const int32_t *xin = x;
     int32_t *yout = y;
+    if (via_dense)
+        yout = reinterpret_cast<int32_t *>(static_cast<char *>(scratch) + init_bytes + wd_bytes);
     if (rowmajor) {
         yout = reinterpret_cast<int32_t *>(static_cast<char *>(scratch) + init_bytes + wd_bytes +
                                            xt_bytes);
@@ -908,12 +948,13 @@ hipError_t run_conv(const ConvGeom &g0, const int32_t *x, const uint32_t *wp, co
         hipLaunchKernelGGL((prep_kernel<Inner::Mul, kTN>), dim3(pgrid), dim3(256), 0, st, wp, wi,
                            bias, g.k, g.crs, wpr, Jpad, Kpad, wblocks, wd, init, code_fmt(g.bits));
     e = hipGetLastError();
-    if (e == hipSuccess && p.atomic_out) e = run_fill_mapped(g, init, yout, map, st);
+    if (e == hipSuccess && p.atomic_out) e = run_fill_mapped(g, init, yout, via_dense ? OutMap() : map, st);
     if (e == hipSuccess) {
         e = op == Inner::Shift
                 ? dispatch_tiled<Inner::Shift>(v, p, int(grid), lds, xin, wd, init, yout, st)
                 : dispatch_tiled<Inner::Mul>(v, p, int(grid), lds, xin, wd, init, yout, st);
     }
+    if (e == hipSuccess && via_dense) e = run_copy_mapped(g, yout, y, map, st);
     if (e == hipSuccess && rowmajor) {
         const int64_t tiles = int64_t((g0.n + 63) / 64) * ((g0.k + 63) / 64);
         hipLaunchKernelGGL(transpose_kernel, dim3(unsigned(tiles)), dim3(256), 0, st, yout, y, g0.k,

@@ -90,6 +90,9 @@ hipError_t run_fill_init(const ConvGeom &g, const int32_t *init, int32_t *y, hip
 // The same through a map; init == NULL writes zeros.
 hipError_t run_fill_mapped(const ConvGeom &g, const int32_t *init, int32_t *y, const OutMap &map,
                            hipStream_t stream);
+// y[map(n, k, oh, ow)] = src (dense [n][k][oh][ow]) for a strided map.
+hipError_t run_copy_mapped(const ConvGeom &g, const int32_t *src, int32_t *y, const OutMap &map,
+                           hipStream_t stream);
 hipError_t run_epilogue(const ConvGeom &g, int32_t *y, const Epilogue &epi, hipStream_t stream);
 
 // Short name of the kernel run_conv would launch for g (see ds_conv2d_shift_describe).

@@ -367,7 +367,7 @@ struct CreateArgs {
 
 // Planning of a spec whose geometry, codes and epilogue are set: code width
 // checks, pixel tiles, segments and the split of the reduction.
-ds_status finish_spec(Spec &sp, int bits, int splits)
+ds_status finish_spec(Spec &sp, int bits, int splits, int target_blocks = 2048)
 {
     const ConvGeom &g = sp.g;
     sp.fmt = code_fmt(bits);
@@ -380,11 +380,11 @@ ds_status finish_spec(Spec &sp, int bits, int splits)
     sp.tiles_p = int((nq + kBlockPixels - 1) / kBlockPixels);
     sp.kgroups = (g.k + kTN - 1) / kTN;
     // Enough blocks to keep every compute unit busy through the tail (about 8 per
-    // CU); each part keeps at least 64 reduction elements.
+    // CU by default); each part keeps at least 64 reduction elements.
     int ns = splits;
     if (ns == 0) {
         const int64_t base = int64_t(sp.tiles_p) * sp.kgroups;
-        const int64_t want = (2048 + base - 1) / base;
+        const int64_t want = (target_blocks + base - 1) / base;
         const int64_t cap = std::max<int64_t>(1, g.crs / 64);
         ns = int(std::max<int64_t>(1, std::min(want, cap)));
     }
@@ -488,6 +488,8 @@ struct ds_jit_conv {
     int32_t *mul = nullptr, *add = nullptr;
     bool backward = false;
     ConvGeom fwd;                   // backward: the forward layer
+    int32_t *dense = nullptr;       // split phase: its partial sums, dense [n][k][oh][ow]
+    OutMap scatter;                 // ... and where they go in dx
     std::vector<ds_jit_conv *> parts;
     std::vector<GradPhase> zeros;   // backward: phases whose dx positions are 0
 };
@@ -502,7 +504,7 @@ static ds_status destroy_plan(ds_jit_conv *p)
         if (st == DS_SUCCESS) st = sq;
     }
     if (p->module) e = hipModuleUnload(p->module);
-    for (int32_t *q : {p->init, p->mul, p->add})
+    for (int32_t *q : {p->init, p->mul, p->add, p->dense})
         if (q) {
             const hipError_t f = hipFree(q);
             if (e == hipSuccess) e = f;
@@ -661,9 +663,27 @@ extern "C" ds_status ds_jit_conv_backward_data_create(const uint32_t *w_packed, 
             sp.g = ph.g;
             sp.wp = codes.data();
             sp.map = ph.map;
-            st = finish_spec(sp, 5, splits);
+            // A strided phase that splits pays a dense buffer's round trip (below), so
+            // it splits only toward 2 blocks per CU (MI355X: a 3x3 stride-2 layer's phases
+            // ran 1.8x faster unsplit at 784 blocks, and 1.3x faster at 2-4 parts than at
+            // 11 on a 200-block grid).
+            st = finish_spec(sp, 5, splits, ph.map.dense() ? 2048 : 512);
+            // Split partial sums meet through int32 atomics, which on a strided map land
+            // on scattered addresses: such a phase accumulates densely into a buffer of
+            // its own and is scattered into dx afterwards.
+            const bool via_dense = st == DS_SUCCESS && sp.nsplit > 1 && !ph.map.dense();
+            if (via_dense) sp.map = OutMap();
             ds_jit_conv *part = nullptr;
             if (st == DS_SUCCESS) st = build_plan(sp, &part);
+            if (st == DS_SUCCESS && via_dense) {
+                part->scatter = ph.map;
+                const size_t bytes = size_t(ph.g.n) * ph.g.k * ph.g.oh * ph.g.ow * 4;
+                if (hipMalloc(&part->dense, bytes) != hipSuccess) {
+                    destroy_plan(part);
+                    part = nullptr;
+                    st = fail(DS_ERR_HIP, "hipMalloc of %zu bytes failed", bytes);
+                }
+            }
             if (st != DS_SUCCESS) {
                 const std::string msg = last_error();
                 destroy_plan(p);
@@ -688,6 +708,11 @@ static hipError_t run_part(const ds_jit_conv *plan, const int32_t *x, const int3
     const ConvGeom &g = sp.g;
     const OutMap m = full_map(sp);
     const bool split = sp.nsplit > 1;
+    int32_t *const dst = y;
+    if (plan->dense) {  // accumulate densely, scatter below
+        y = plan->dense;
+        y_bytes = int64_t(g.n) * g.k * g.oh * g.ow * 4;
+    }
     hipError_t e = hipSuccess;
     if (split) e = run_fill_mapped(g, plan->init, y, sp.map, st);
     if (e == hipSuccess) {
@@ -720,6 +745,7 @@ static hipError_t run_part(const ds_jit_conv *plan, const int32_t *x, const int3
         epi.relu = sp.relu;
         if (epi.any()) e = run_epilogue(g, y, epi, st);
     }
+    if (e == hipSuccess && plan->dense) e = run_copy_mapped(g, plan->dense, dst, plan->scatter, st);
     return e;
 }
 
