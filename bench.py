@@ -5,7 +5,8 @@ LinearShift call on its own seeded input, all inputs resident in HBM).
 Two paths compute the same outputs bit for bit (checked before timing):
   jit      (default) a weight-specialised plan per layer, its code generated
            at setup from the fixed weights (Section 6's run-time compilation);
-           layers it does not cover (windows over 3 x 3) run the runtime kernel
+           the classifier, whose plan would be slower at this batch
+           (JitConv.preferred), runs the runtime kernel
   runtime  ds_conv2d_shift / ds_linear_shift with the packed weights as data
 Prints ONE JSON line:
   value       whole-step throughput in G shift-accumulates/s (dense SAC =
@@ -623,8 +624,9 @@ def main():
 
 
 def jit_supported(L) -> bool:
-    """Layers a weight-specialised plan covers: windows up to 3 x 3 and LinearShift."""
-    return L.kind == "linear" or (L.r <= 3 and L.s <= 3)
+    """Layers a weight-specialised plan covers: every ConvShift (windows over 3 x 3
+    through a zero-padded copy of x) and LinearShift."""
+    return L.kind in ("conv", "linear")
 
 
 def group_name(L, path: str, planned: bool | None = None) -> str:
@@ -839,8 +841,8 @@ def bench_layers(args):
         torch.cuda.empty_cache()
         cpu = cpu_baseline(args, cfg, seed, layers)
 
-    path_desc = ("weight-specialised plans (code generated per layer at setup; windows up to 3x3 "
-                 "and LinearShift), other layers on the runtime kernel"
+    path_desc = ("weight-specialised plans (code generated per layer at setup), the runtime "
+                 "kernel where a plan is not preferred"
                  if args.path == "jit" else "runtime weights (ds_conv2d_shift / ds_linear_shift)")
     out = {
         "metric": "G shift-accumulates/s per layer and % of int32 VALU peak on one MI355X",

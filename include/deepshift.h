@@ -319,8 +319,11 @@ ds_status ds_conv2d_shift_describe(int64_t n, int64_t c, int64_t h, int64_t w, i
  *     v = floor(v * mul[k] / 2^mul_shift) + add[k]            (when mul)
  *     v = v + residual[n][k][p]                               (DS_JIT_RESIDUAL)
  *     v = max(v, 0)                                           (DS_RELU)
- * Supported: kernels up to 3 x 3 (r, s <= 3), any stride and padding; a
- * LinearShift is the case h = w = r = s = 1.
+ * Supported: any window up to 1023 columns wide, any stride and padding; a
+ * LinearShift is the case h = w = r = s = 1. Windows over 3 x 3 read a
+ * zero-padded copy of x, [n][c][xh][xw] with xh = (oh - 1) * stride_h + r and
+ * xw = (ow - 1) * stride_w + s, that each run writes first into device memory
+ * the plan holds (from create to destroy).
  *
  * ds_jit_conv_create: w_packed is HOST memory, [k][ds_packed_row_words(c*r*s)]
  * words as for ds_conv2d_shift (b-bit codes with DS_CODE_BITS(b) in flags); bias, mul and add are HOST int32 [k] or NULL
@@ -331,13 +334,17 @@ ds_status ds_conv2d_shift_describe(int64_t n, int64_t c, int64_t h, int64_t w, i
  * atomically into y); a positive value forces that many parts (at most c).
  * The plan's code is loaded on the current device with hipModuleLoadData and
  * lives until ds_jit_conv_destroy. Errors: as ds_conv2d_shift_fused for
- * arguments, DS_ERR_UNSUPPORTED for r or s > 3, DS_ERR_HIP when loading fails.
- * Making a plan synchronises the device (module load, uploads).
+ * arguments, DS_ERR_UNSUPPORTED for s > 1023 or a padded copy of 2^31 bytes or
+ * more, DS_ERR_HIP when loading fails or device memory runs out. Making a plan
+ * synchronises the device (module load, uploads).
  *
  * ds_jit_conv_run: x [n][c][h][w], residual and y [n][k][oh][ow], device
  * memory on the plan's device; residual must be non-NULL exactly when the
  * plan was made with DS_JIT_RESIDUAL. Asynchronous on `stream`. y must not
- * overlap x or residual.
+ * overlap x or residual. A plan may hold device scratch (the padded copy of x;
+ * the partial sums of split strided phases of an input-gradient plan), so runs
+ * of one plan must not overlap in time: issue them on one stream, or order
+ * them with events.
  *
  * ds_jit_conv_image: the code object ds_jit_conv_create would load, written
  * to host memory `image` of `capacity` bytes (*size = bytes needed;
@@ -374,9 +381,10 @@ ds_status ds_jit_conv_query(const ds_jit_conv *plan, int64_t *code_bytes, int32_
  * kernel writing its own rows and columns of dx; ds_jit_conv_run(plan, dy,
  * NULL, dx, stream) then takes dy [n][k][oh][ow] and writes all of dx
  * [n][c][h][w] (residual must be NULL). A LinearShift is the case
- * h = w = r = s = 1. DS_ERR_UNSUPPORTED when a phase's window exceeds 3 x 3
- * (r or s above 3 at stride 1, above 6 at stride 2). ds_jit_conv_query reports
- * the code of all phases. Other errors as for ds_jit_conv_create. */
+ * h = w = r = s = 1. Phases with windows over 3 x 3 read a padded copy of dy
+ * as forward plans do. DS_ERR_UNSUPPORTED when a phase is wider than 1023
+ * columns. ds_jit_conv_query reports the code of all phases. Other errors as
+ * for ds_jit_conv_create. */
 ds_status ds_jit_conv_backward_data_create(const uint32_t *w_packed, int64_t n, int64_t c,
                                            int64_t h, int64_t w, int64_t k, int64_t r, int64_t s,
                                            int32_t stride_h, int32_t stride_w, int32_t pad_h,

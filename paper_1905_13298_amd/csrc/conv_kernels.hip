@@ -220,6 +220,22 @@ copy_mapped_kernel(const int32_t *__restrict__ src, int32_t *__restrict__ y, int
     }
 }
 
+// xp[p][i][j] = x[p][i - ph][j - pw] where that lies inside x, else 0: planes of
+// h x w copied into zero-padded planes of xh x xw (which may also crop).
+__global__ void __launch_bounds__(256)
+pad_planes_kernel(const int32_t *__restrict__ x, int32_t *__restrict__ xp, int total, int h,
+                  int w, int ph, int pw, FastDiv div_xw, FastDiv div_xh)
+{
+    for (int idx = int(blockIdx.x) * 256 + int(threadIdx.x); idx < total; idx += int(gridDim.x) * 256) {
+        const int t = fdiv(idx, div_xw), j = idx - t * int(div_xw.d);
+        const int pl = fdiv(t, div_xh), i = t - pl * int(div_xh.d);
+        const int ii = i - ph, jj = j - pw;
+        xp[idx] = (unsigned(ii) < unsigned(h) && unsigned(jj) < unsigned(w))
+                      ? x[(int64_t(pl) * h + ii) * w + jj]
+                      : 0;
+    }
+}
+
 // The epilogue on one output value v of channel k at flat index o.
 __device__ __forceinline__ uint32_t apply_epilogue(uint32_t v, int k, int64_t o, const Epilogue &e)
 {
@@ -843,6 +859,18 @@ hipError_t run_copy_mapped(const ConvGeom &g, const int32_t *src, int32_t *y, co
     hipLaunchKernelGGL(copy_mapped_kernel, dim3(grid), dim3(256), 0, st, src, y, int(total),
                        make_fastdiv(uint32_t(g.ow)), make_fastdiv(uint32_t(g.oh)),
                        make_fastdiv(uint32_t(g.k)), map);
+    return hipGetLastError();
+}
+
+hipError_t run_pad_planes(const int32_t *x, int32_t *xp, int64_t planes, int h, int w, int ph,
+                          int pw, int xh, int xw, hipStream_t st)
+{
+    const int64_t total = planes * xh * xw;
+    if (total <= 0) return hipSuccess;
+    if (total > INT32_MAX || h <= 0 || w <= 0) return hipErrorInvalidValue;
+    const int grid = int(std::min<int64_t>((total + 255) / 256, 8192));
+    hipLaunchKernelGGL(pad_planes_kernel, dim3(grid), dim3(256), 0, st, x, xp, int(total), h, w,
+                       ph, pw, make_fastdiv(uint32_t(xw)), make_fastdiv(uint32_t(xh)));
     return hipGetLastError();
 }
 

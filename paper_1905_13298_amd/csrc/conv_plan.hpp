@@ -94,6 +94,11 @@ hipError_t run_fill_mapped(const ConvGeom &g, const int32_t *init, int32_t *y, c
 hipError_t run_copy_mapped(const ConvGeom &g, const int32_t *src, int32_t *y, const OutMap &map,
                            hipStream_t stream);
 hipError_t run_epilogue(const ConvGeom &g, int32_t *y, const Epilogue &epi, hipStream_t stream);
+// xp [planes][xh][xw] = x [planes][h][w] shifted down by ph rows and right by pw
+// columns, zeros elsewhere (rows and columns past xh, xw are dropped).
+hipError_t run_pad_planes(const int32_t *x, int32_t *xp, int64_t planes, int h, int w, int ph,
+                          int pw, int xh, int xw, hipStream_t stream);
+
 
 // Short name of the kernel run_conv would launch for g (see ds_conv2d_shift_describe).
 void describe_conv(const ConvGeom &g, char *buf, size_t len);

@@ -56,6 +56,7 @@ constexpr int kTN = 64;      // output channels per segment
 constexpr int kBlockPixels = 256;
 constexpr int kStubWords = 5;
 constexpr int kMaxTaps = 3;  // R, S <= 3: the template computes a 3 x 3 window of taps
+constexpr int kMaxPaddedS = 1023;  // wider windows: tap column s at immediate offset 4 s < 4096
 
 // gfx950 instruction encodings used by the generator (VOP2, VOP1, VOP3, MUBUF,
 // SOP1/SOP2/SOPP words; see the CDNA ISA reference).
@@ -106,9 +107,9 @@ public:
     {
         w.push_back(0xbf8c0f70u | uint32_t(n & 15) | (uint32_t(n >> 4) << 14));
     }
-    void mubuf(uint32_t word0, int vdata, int vaddr, int srsrc, int soff)
+    void mubuf(uint32_t word0, int vdata, int vaddr, int srsrc, int soff, uint32_t imm = 0)
     {
-        w.push_back(word0);
+        w.push_back(word0 | (imm & 0xfffu));  // 12-bit immediate byte offset
         w.push_back((uint32_t(soff) << 24) | (uint32_t(srsrc / 4) << 16) |
                     (uint32_t(vdata) << 8) | uint32_t(vaddr));
     }
@@ -135,6 +136,11 @@ struct Spec {
     int nsplit = 1, kgroups = 0, nseg = 0, tiles_p = 0;
     int slots = 8;       // loads in flight per wave
     OutMap map;          // where output (n, k, oh, ow) goes in y (dense by default)
+    // Windows over 3 x 3: the kernel reads a zero-padded copy of x, [n][c][xh][xw]
+    // with the padding included, that the plan makes before each run; a lane's
+    // window then starts at one offset and every tap sits at a uniform distance
+    // from it. Zero: x itself, with per-tap offsets from the template.
+    int xh = 0, xw = 0;
 };
 
 // Element strides of the output map of a spec (the dense layout when unset).
@@ -163,7 +169,10 @@ void emit_segment(Emitter &e, const Spec &sp, int kg, int c0, int c1, bool split
     const ConvGeom &g = sp.g;
     const int kbase = kg * kTN, jn = std::min(kTN, g.k - kbase);
     const int RS = g.r * g.s, E = (c1 - c0) * RS;
-    const uint32_t cstride = uint32_t(g.h) * uint32_t(g.w) * 4u;
+    const bool padded = sp.xh > 0;
+    const uint32_t cstride = padded ? uint32_t(sp.xh) * uint32_t(sp.xw) * 4u
+                                    : uint32_t(g.h) * uint32_t(g.w) * 4u;
+    const uint32_t rstride = uint32_t(sp.xw) * 4u;
     const uint32_t kstride = uint32_t(full_map(sp).kstride) * 4u;
 
     for (int j = 0; j < jn; ++j)
@@ -171,19 +180,23 @@ void emit_segment(Emitter &e, const Spec &sp, int kg, int c0, int c1, bool split
 
     // Element i = (c0 + i / RS, tap i % RS); its load goes to slot i % kSlots and
     // reads x at v[tap] + s29, where s29 = c * H * W * 4 for the channel of the
-    // most recently issued load.
+    // most recently issued load. From a padded copy: at v4 + s29 + 4 s, where
+    // s29 = (c * xh * xw + r * xw) * 4 for the channel and tap row of that load.
     const int kSlots = sp.slots;
     const int D = std::min(kSlots, E);
-    int cur_c = c0;
-    e.s_mov_imm(kSx, uint32_t(c0) * cstride);
+    uint32_t cur = uint32_t(c0) * cstride;
+    e.s_mov_imm(kSx, cur);
     auto issue = [&](int i) {
-        const int c = c0 + i / RS, t = i % RS;
-        if (c != cur_c) {
-            e.s_add_imm(kSx, uint32_t(c - cur_c) * cstride);
-            cur_c = c;
+        const int c = c0 + i / RS, t = i % RS, tr = t / g.s, ts = t % g.s;
+        const uint32_t soff = uint32_t(c) * cstride + (padded ? uint32_t(tr) * rstride : 0u);
+        if (soff != cur) {
+            e.s_add_imm(kSx, soff - cur);  // modulo 2^32
+            cur = soff;
         }
-        const int tap = kTap0 + (t / g.s) * 3 + (t % g.s);
-        e.mubuf(kLoad, kSlot + i % kSlots, tap, kXrsrc, kSx);
+        if (padded)
+            e.mubuf(kLoad, kSlot + i % kSlots, kTap0, kXrsrc, kSx, uint32_t(ts) * 4u);
+        else
+            e.mubuf(kLoad, kSlot + i % kSlots, kTap0 + tr * 3 + ts, kXrsrc, kSx);
     };
     for (int i = 0; i < D; ++i) issue(i);
 
@@ -376,6 +389,16 @@ ds_status finish_spec(Spec &sp, int bits, int splits, int deep_blocks = 2048)
     for (int64_t i = 0; used < 32 && i < int64_t(g.k) * sp.rw; ++i)
         if (sp.wp[i] >> used)
             return fail(DS_ERR_INVALID_CODE, "bits %d-31 of packed word %lld are not 0", used, (long long)i);
+    if (g.r > kMaxTaps || g.s > kMaxTaps) {
+        if (g.s > kMaxPaddedS)
+            return fail(DS_ERR_UNSUPPORTED, "kernels wider than %d columns are not supported", kMaxPaddedS);
+        const int64_t xh = int64_t(g.oh - 1) * g.sh + g.r, xw = int64_t(g.ow - 1) * g.sw + g.s;
+        const int64_t xe = prod({g.n, g.c, xh, xw});
+        if (xe < 0 || xe > kMaxElems / 4)
+            return fail(DS_ERR_UNSUPPORTED, "the padded input would take 2^31 bytes or more");
+        sp.xh = int(xh);
+        sp.xw = int(xw);
+    }
     const int64_t nq = int64_t(g.n) * g.oh * g.ow;
     sp.tiles_p = int((nq + kBlockPixels - 1) / kBlockPixels);
     sp.kgroups = (g.k + kTN - 1) / kTN;
@@ -440,8 +463,8 @@ ds_status plan_spec(const CreateArgs &a, Spec &sp)
     if (a.mul && (a.mul_shift < 0 || a.mul_shift > 31))
         return fail(DS_ERR_INVALID_ARG, "mul_shift must be in [0, 31]");
     if (a.splits < 0) return fail(DS_ERR_INVALID_ARG, "splits must be >= 0");
-    if (a.r > kMaxTaps || a.s > kMaxTaps)
-        return fail(DS_ERR_UNSUPPORTED, "kernels larger than 3 x 3 are not supported");
+    if (a.s > kMaxPaddedS)
+        return fail(DS_ERR_UNSUPPORTED, "kernels wider than %d columns are not supported", kMaxPaddedS);
     ds_status st = check_layer(a.n, a.c, a.h, a.w, a.k, a.r, a.s, a.sh, a.sw, a.ph, a.pw, bits, sp.g);
     if (st != DS_SUCCESS) return st;
     sp.wp = a.wp;
@@ -497,6 +520,7 @@ struct ds_jit_conv {
     int32_t *mul = nullptr, *add = nullptr;
     bool backward = false;
     ConvGeom fwd;                   // backward: the forward layer
+    int32_t *xpad = nullptr;        // windows over 3 x 3: the zero-padded input [n][c][xh][xw]
     int32_t *dense = nullptr;       // split phase: its partial sums, dense [n][k][oh][ow]
     OutMap scatter;                 // ... and where they go in dx
     std::vector<ds_jit_conv *> parts;
@@ -513,7 +537,7 @@ static ds_status destroy_plan(ds_jit_conv *p)
         if (st == DS_SUCCESS) st = sq;
     }
     if (p->module) e = hipModuleUnload(p->module);
-    for (int32_t *q : {p->init, p->mul, p->add, p->dense})
+    for (int32_t *q : {p->init, p->mul, p->add, p->dense, p->xpad})
         if (q) {
             const hipError_t f = hipFree(q);
             if (e == hipSuccess) e = f;
@@ -568,6 +592,13 @@ static ds_status build_plan(const Spec &spec, ds_jit_conv **out)
             const std::string msg = last_error();
             destroy_plan(p);
             return fail(st, "%s", msg.c_str());
+        }
+    }
+    if (p->sp.xh > 0) {
+        const size_t bytes = size_t(p->sp.g.n) * p->sp.g.c * p->sp.xh * p->sp.xw * 4;
+        if (hipMalloc(&p->xpad, bytes) != hipSuccess) {
+            destroy_plan(p);
+            return fail(DS_ERR_HIP, "hipMalloc of %zu bytes (padded input) failed", bytes);
         }
     }
     p->sp.bias = p->sp.mul = p->sp.add = nullptr;
@@ -647,8 +678,8 @@ extern "C" ds_status ds_jit_conv_backward_data_create(const uint32_t *w_packed, 
         if (st != DS_SUCCESS) return st;
         const std::vector<GradPhase> phases = grad_phases(g);
         for (const GradPhase &ph : phases)
-            if (ph.g.r > kMaxTaps || ph.g.s > kMaxTaps)
-                return fail(DS_ERR_UNSUPPORTED, "a stride phase has a window larger than 3 x 3");
+            if (ph.g.s > kMaxPaddedS)
+                return fail(DS_ERR_UNSUPPORTED, "a stride phase is wider than %d columns", kMaxPaddedS);
         const CodeFmt fmt = code_fmt(bits);
         const int64_t rw = row_words_bits(g.crs, bits);
         const int used = fmt.per_word * bits;
@@ -723,7 +754,15 @@ static hipError_t run_part(const ds_jit_conv *plan, const int32_t *x, const int3
         y_bytes = int64_t(g.n) * g.k * g.oh * g.ow * 4;
     }
     hipError_t e = hipSuccess;
-    if (split) e = run_fill_mapped(g, plan->init, y, sp.map, st);
+    // Padded input: the template sees the copy as x with no padding, and its tap
+    // (0, 0) offset is where each lane's window starts.
+    const bool padded = plan->xpad != nullptr;
+    if (padded) {
+        e = run_pad_planes(x, plan->xpad, int64_t(g.n) * g.c, g.h, g.w, g.ph, g.pw, sp.xh, sp.xw, st);
+        x = plan->xpad;
+        x_bytes = int64_t(g.n) * g.c * sp.xh * sp.xw * 4;
+    }
+    if (e == hipSuccess && split) e = run_fill_mapped(g, plan->init, y, sp.map, st);
     if (e == hipSuccess) {
         JitArgs a;
         a.x = x;
@@ -733,8 +772,13 @@ static hipError_t run_part(const ds_jit_conv *plan, const int32_t *x, const int3
         a.y_bytes = int(y_bytes);
         a.OHOW = g.oh * g.ow;
         a.NQ = g.n * a.OHOW;
-        a.OW = g.ow; a.H = g.h; a.W = g.w; a.C = g.c; a.K = g.k; a.HW = g.h * g.w;
-        a.sh = g.sh; a.sw = g.sw; a.ph = g.ph; a.pw = g.pw;
+        a.OW = g.ow; a.C = g.c; a.K = g.k;
+        a.H = padded ? sp.xh : g.h;
+        a.W = padded ? sp.xw : g.w;
+        a.HW = a.H * a.W;
+        a.sh = g.sh; a.sw = g.sw;
+        a.ph = padded ? 0 : g.ph;
+        a.pw = padded ? 0 : g.pw;
         a.ybase = int(m.base); a.ynst = m.nstride; a.yrst = m.rstride; a.ycst = m.cstride;
         a.tiles_p = sp.tiles_p;
         a.group_tiles = std::min(plan->group_tiles, sp.tiles_p);

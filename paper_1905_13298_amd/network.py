@@ -7,12 +7,11 @@ residual add and ReLU in one kernel), pooling is ``ds_maxpool2d`` /
 ``ds_avgpool2d_global``, the classifier is ``ds_linear_shift``. Parameters are
 uploaded once; activation buffers are allocated once per batch size and reused.
 
-With ``jit=True`` the convolutions with windows up to 3 x 3 and the classifier
-run weight-specialised plans (``ds_jit_conv_*``, made once here for the graph's
-batch size) with the same fused epilogue where a plan is expected to be faster
-(``JitConv.preferred``); ``jit="all"`` uses a plan wherever one covers the
-layer. The results are the same bit for bit. Calls at another batch size, and
-larger windows, take the runtime kernels.
+With ``jit=True`` the convolutions and the classifier run weight-specialised
+plans (``ds_jit_conv_*``, made once here for the graph's batch size) with the
+same fused epilogue where a plan is expected to be faster
+(``JitConv.preferred``); ``jit="all"`` uses a plan for every layer. The results
+are the same bit for bit. Calls at another batch size take the runtime kernels.
 """
 from __future__ import annotations
 
@@ -54,13 +53,11 @@ class ShiftNetwork:
         wp = ops.pack_shift_weights(p["codes"])
         if op["op"] == "linear":
             plan = ops.JitConv(wp, (L.n, L.c, 1, 1), 1, 1, 0, bias=p.get("bias"), device=self.dev)
-        elif L.r <= 3 and L.s <= 3:
+        else:
             mul, add = p["bn"]
             plan = ops.JitConv(wp, L.x_shape, (L.r, L.s), L.stride, L.pad, mul=mul, add=add,
                                mul_shift=self.mul_shift, residual=op["res"] is not None,
                                relu=op["relu"], device=self.dev)
-        else:
-            return
         if plan.preferred or self.jit == "all":
             self.plans[L.name] = plan
         else:

@@ -56,7 +56,7 @@ EDGE = [
     ("s1_1x1", 2, 9, 7, 5, 70, 1, 1, 1, 0),
     ("rect_2x3", 2, 5, 10, 12, 6, (2, 3), (2, 3), 1, 1),
     ("rect_stride", 2, 5, 9, 8, 3, (2, 3), (2, 3), (2, 1), (1, 0)),   # negative-pad phase: gather
-    ("s2_7x7_stem", 2, 3, 30, 30, 16, 7, 7, 2, 3),                    # tap width 4: gather
+    ("s2_7x7_stem", 2, 3, 30, 30, 16, 7, 7, 2, 3),                    # tap width 4: gather; plans: padded
     ("pad_beyond_1x1", 1, 3, 6, 6, 2, 1, 1, 1, 1),                    # gather
     ("big_k_small_c", 2, 3, 12, 12, 300, 3, 3, 2, 1),
     ("many_tiles", 4, 64, 20, 20, 128, 3, 3, 1, 1),
@@ -173,7 +173,7 @@ def test_resnet50_full_batch_against_gather_kernel_and_oracle(monkeypatch):
         del dx, ref, dyd
 
 
-JIT_EDGE = [e for e in EDGE if e[0] != "s2_7x7_stem"]
+JIT_EDGE = EDGE
 
 
 @pytest.mark.parametrize("splits", [0, 1, 3])
@@ -197,9 +197,9 @@ def test_weight_specialised_plans_match_oracle(spec, splits):
 
 
 def test_weight_specialised_plan_limits_and_arguments():
-    codes = np.zeros((16, 3 * 49), np.uint8)
+    codes = np.zeros((16, 1024), np.uint8)      # a phase window 1024 columns wide
     with pytest.raises(ops.DeepShiftError, match="UNSUPPORTED"):
-        ops.JitConvBackwardData(ops.pack_shift_weights(codes), (2, 3, 30, 30), 7, 2, 3)
+        ops.JitConvBackwardData(ops.pack_shift_weights(codes), (2, 1, 4, 1030), (1, 1024), 1, 0)
     codes = random_codes(np.random.default_rng(3), (8, 4 * 9))
     plan = ops.JitConvBackwardData(ops.pack_shift_weights(codes), (2, 4, 8, 8), 3, 2, 1)
     dy = torch.zeros(plan.x_shape, dtype=torch.int32, device=DEV)

@@ -6,8 +6,9 @@ padding, rectangular windows; LinearShift as 1 x 1 on 1 x 1 images), each with
 the reduction whole, split automatically and split by force (the split-K path
 adds partial sums atomically and runs the epilogue as a pass of its own); the
 fused epilogue (affine map, residual, ReLU) against the oracle's; the single-
-layer workloads in full; and every ResNet-50 layer up to 3 x 3 at batch 128 in
-full against the production kernel, plus sampled outputs against the oracle.
+layer workloads in full; and every ResNet-50 convolution (the 7 x 7 stem through
+a padded copy of x) at batch 128 in full against the production kernel, plus
+sampled outputs against the oracle.
 """
 import zlib
 
@@ -56,6 +57,11 @@ EDGE = [
     ("tiny", 1, 1, 1, 1, 1, 1, 1, 1, 0),
     ("big_c_small_k", 1, 300, 6, 6, 3, 3, 3, 1, 1),
     ("many_tiles", 4, 64, 20, 20, 128, 3, 3, 1, 1),
+    # windows over 3 x 3 read a zero-padded copy of x
+    ("7x7_s2_stem_like", 2, 3, 23, 21, 70, 7, 7, 2, 3),
+    ("5x5_pad2", 2, 9, 12, 10, 40, 5, 5, 1, 2),
+    ("4x6_s3_cropped", 1, 6, 14, 17, 20, 4, 6, 3, 0),
+    ("1x7_pad3", 2, 5, 9, 16, 33, 1, 7, 1, 3),
 ]
 
 
@@ -118,13 +124,13 @@ def test_single_layer_configs_exact(cfg):
 
 
 def test_resnet50_full_batch_against_production_kernel_and_oracle():
-    """Every ResNet-50 layer with a window up to 3 x 3, batch 128: all outputs equal
+    """Every ResNet-50 convolution, batch 128: all outputs equal
     those of ds_conv2d_shift (itself pinned to the oracle), 400 sampled outputs
     per layer equal the oracle's."""
     rng = np.random.default_rng(50)
     layers = W.config_layers(4)
     for li, L in enumerate(layers):
-        if L.kind != "conv" or L.r > 3 or L.s > 3:
+        if L.kind != "conv":
             continue
         x, codes, bias = W.gen_layer(L, W.CONFIG_SEEDS[4], li)
         wp = ops.pack_shift_weights(codes)

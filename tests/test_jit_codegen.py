@@ -71,12 +71,32 @@ def elf_layout(img):
     return loads, int(sec[i + 1], 16), int(sec[i + 2], 16), int(sec[i + 3], 16)
 
 
+def padded_extents(h, w, r, s, st, pd):
+    """Windows over 3 x 3 read a zero-padded copy of x with the extents the
+    windows reach; None for smaller windows."""
+    if r <= 3 and s <= 3:
+        return None
+    oh, ow = (h + 2 * pd - r) // st + 1, (w + 2 * pd - s) // st + 1
+    return (oh - 1) * st + r, (ow - 1) * st + s
+
+
+def pad_input(x, pd, xh, xw):
+    n, c, h, w = x.shape
+    xp = np.zeros((n, c, xh + h + pd, xw + w + pd), x.dtype)
+    xp[:, :, pd:pd + h, pd:pd + w] = x
+    return xp[:, :, :xh, :xw]
+
+
 def lane_inputs(n, c, h, w, k, r, s, st, pd):
     """Per lane (pixel q of every 256-pixel tile): tap byte offsets v4..v12 of
     the 3 x 3 window at channel 0 and the output byte offset v13, as the
     template kernel computes them (past-the-end marker for padding and for
-    lanes beyond the last pixel)."""
+    lanes beyond the last pixel). For a window over 3 x 3 the template sees
+    the padded copy of x as an unpadded input."""
     oh, ow = (h + 2 * pd - r) // st + 1, (w + 2 * pd - s) // st + 1
+    ext = padded_extents(h, w, r, s, st, pd)
+    if ext is not None:
+        h, w, pd = ext[0], ext[1], 0
     nq = n * oh * ow
     lanes = -(-nq // 256) * 256
     q = np.arange(lanes)
@@ -130,7 +150,8 @@ class Interp:
             arr, nrec = self.bufs[base]
             voff = V[int(ops[1][1:])].astype(np.int64)
             soff = S[int(ops[3][1:])] & M32
-            tot = voff + soff
+            imm = [int(t.split(":")[1]) for t in ops[4:] if t.startswith("offset:")]
+            tot = voff + soff + (imm[0] if imm else 0)
             inr = voff < nrec
             assert not np.any(inr & (tot + 4 > nrec)), f"out-of-range access at pc {pc:#x}"
             assert not np.any(inr & (tot % 4 != 0))
@@ -223,6 +244,9 @@ CASES = [
     (1, 3, 10, 10, 5, 3, 3, 2, 0, 1, "mul"),
     (33, 40, 1, 1, 17, 1, 1, 1, 0, 1, "full"),     # a LinearShift [33 x 40] -> 17
     (2, 64, 4, 4, 3, 3, 3, 1, 1, 4, "full"),
+    (2, 3, 13, 11, 70, 7, 7, 2, 3, 1, "full"),     # a padded copy of x (windows over 3 x 3)
+    (1, 4, 9, 10, 20, 5, 4, 1, 2, 2, "none"),
+    (1, 2, 12, 12, 9, 4, 6, 3, 0, 1, "relu"),      # stride leaves the last rows unread
 ]
 
 
@@ -252,7 +276,9 @@ def test_generated_code_matches_oracle(case, tmp_path):
     insts = disassemble(img, str(tmp_path))
     body = min(insts)
     conv = oracle.conv2d_shift(x, codes, bias, r=r, s=s, stride=st, pad=pd)
-    xb = x.reshape(-1).view(np.uint32).astype(np.int64)
+    ext = padded_extents(h, w, r, s, st, pd)
+    xr = x if ext is None else pad_input(x, pd, *ext)
+    xb = np.ascontiguousarray(xr).reshape(-1).view(np.uint32).astype(np.int64)
     y = np.full(n * k * oh * ow, 0xDEADBEEF, dtype=np.int64)
     bufs = {20: (xb, xb.size * 4), 24: (y, y.size * 4)}
     bufs[36] = (res.reshape(-1).view(np.uint32).astype(np.int64), y.size * 4) if res is not None else (y, 0)
@@ -278,7 +304,8 @@ def test_image_rejects_bad_arguments():
     codes = np.full((4, 9), 15, np.uint8)
     wp = ops.pack_shift_weights(codes)
     with pytest.raises(ops.DeepShiftError, match="UNSUPPORTED"):
-        ops.jit_conv_image(ops.pack_shift_weights(np.full((4, 25), 15, np.uint8)), (1, 1, 8, 8), 5)
+        ops.jit_conv_image(ops.pack_shift_weights(np.full((4, 1024), 15, np.uint8)), (1, 1, 1, 1100),
+                           (1, 1024))
     with pytest.raises(ops.DeepShiftError, match="INVALID_SHAPE"):
         ops.jit_conv_image(wp, (1, 1, 2, 2), 3)
     with pytest.raises(ops.DeepShiftError, match="INVALID_ARG"):
