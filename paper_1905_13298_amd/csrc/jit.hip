@@ -42,6 +42,7 @@ namespace ds {
 namespace {
 
 // Register contract with the template (see the JITBODY marker there).
+constexpr int kLds = 3;      // v3: the lane's LDS byte offset (wave split)
 constexpr int kTap0 = 4;     // v4..v12: byte offset in x of tap (r, s) = v[4 + 3r + s], channel 0
 constexpr int kYoff = 13;    // v13: byte offset in y of the lane's output pixel, channel 0
 constexpr int kTmpLo = 14, kTmpHi = 15;
@@ -63,7 +64,8 @@ constexpr int kMaxPaddedS = 1023;  // wider windows: tap column s at immediate o
 constexpr uint32_t kOpAshr = 0x11, kOpMax = 0x0d, kOpAdd = 0x34, kOpSub = 0x35;  // VOP2
 constexpr uint32_t kOpMulLo = 0x285, kOpMulHi = 0x287, kOpAlignbit = 0x1ce;     // VOP3
 constexpr uint32_t kLoad = 0xe0501000u, kStore = 0xe0701000u, kAtomicAdd = 0xe1081000u;
-constexpr uint32_t kEndpgm = 0xbf810000u, kNop = 0xbf800000u;
+constexpr uint32_t kEndpgm = 0xbf810000u, kNop = 0xbf800000u, kBarrier = 0xbf8a0000u;
+constexpr uint32_t kDsAdd = 0xd8000000u, kDsRead = 0xd86c0000u;  // ds_add_u32, ds_read_b32
 constexpr uint32_t kLiteral = 255;
 
 class Emitter {
@@ -113,6 +115,18 @@ public:
         w.push_back((uint32_t(soff) << 24) | (uint32_t(srsrc / 4) << 16) |
                     (uint32_t(vdata) << 8) | uint32_t(vaddr));
     }
+    // LDS at v[vaddr] + offset (16 bits): ds_add_u32 of v[vdata]; ds_read_b32 into v[vdst].
+    void ds_add(int vaddr, int vdata, uint32_t offset)
+    {
+        w.push_back(kDsAdd | (offset & 0xffffu));
+        w.push_back(uint32_t(vaddr) | (uint32_t(vdata) << 8));
+    }
+    void ds_read(int vdst, int vaddr, uint32_t offset)
+    {
+        w.push_back(kDsRead | (offset & 0xffffu));
+        w.push_back(uint32_t(vaddr) | (uint32_t(vdst) << 24));
+    }
+    void wait_lgkm0() { w.push_back(0xbf8cc07fu); }  // s_waitcnt lgkmcnt(0)
     void s_mov_imm(int sdst, uint32_t imm)
     {
         w.push_back(0xbe8000ffu | (uint32_t(sdst) << 16));
@@ -141,6 +155,10 @@ struct Spec {
     // window then starts at one offset and every tap sits at a uniform distance
     // from it. Zero: x itself, with per-tap offsets from the template.
     int xh = 0, xw = 0;
+    // Waves per 64 pixels (1, 2 or 4), each with a contiguous share of every
+    // part's reduction elements, meeting in LDS; a workgroup covers 256 / wsplit
+    // pixels.
+    int wsplit = 1;
 };
 
 // Element strides of the output map of a spec (the dense layout when unset).
@@ -160,15 +178,19 @@ inline int code_at(const Spec &sp, int k, int j)
     return int(sp.fmt.at(sp.wp + int64_t(k) * sp.rw, j));
 }
 
-// Straight-line code of segment (kg, part): output channels [64 kg, 64 kg + 64)
-// and input channels [c0, c1), all taps. `split` = the partial sums of several
-// segments meet in y through atomic adds (y holds the bias beforehand and the
-// epilogue runs afterwards, as separate passes).
-void emit_segment(Emitter &e, const Spec &sp, int kg, int c0, int c1, bool split)
+// Straight-line code of one wave's segment: output channels [64 kg, 64 kg + 64)
+// and reduction elements [e0, e1), element i being (input channel i / RS, tap
+// i % RS). `split`: the partial sums of several parts of the reduction meet in y
+// through atomic adds (y holds the bias beforehand and the epilogue runs
+// afterwards, as separate passes). With a wave split W = sp.wsplit > 1, the W
+// waves sharing 64 pixels run shares 0..W-1 of a part's elements: each adds its
+// 64 sums into LDS, waits for the others at a barrier and finishes channels
+// [64 share / W, 64 (share + 1) / W) of the totals.
+void emit_segment(Emitter &e, const Spec &sp, int kg, int e0, int e1, int share, bool split)
 {
     const ConvGeom &g = sp.g;
     const int kbase = kg * kTN, jn = std::min(kTN, g.k - kbase);
-    const int RS = g.r * g.s, E = (c1 - c0) * RS;
+    const int RS = g.r * g.s, E = e1 - e0;
     const bool padded = sp.xh > 0;
     const uint32_t cstride = padded ? uint32_t(sp.xh) * uint32_t(sp.xw) * 4u
                                     : uint32_t(g.h) * uint32_t(g.w) * 4u;
@@ -176,35 +198,36 @@ void emit_segment(Emitter &e, const Spec &sp, int kg, int c0, int c1, bool split
     const uint32_t kstride = uint32_t(full_map(sp).kstride) * 4u;
 
     for (int j = 0; j < jn; ++j)
-        e.mov_imm(kAcc + j, (!split && sp.bias) ? sp.bias[kbase + j] : 0);
+        e.mov_imm(kAcc + j, (!split && sp.bias && share == 0) ? sp.bias[kbase + j] : 0);
 
-    // Element i = (c0 + i / RS, tap i % RS); its load goes to slot i % kSlots and
-    // reads x at v[tap] + s29, where s29 = c * H * W * 4 for the channel of the
-    // most recently issued load. From a padded copy: at v4 + s29 + 4 s, where
-    // s29 = (c * xh * xw + r * xw) * 4 for the channel and tap row of that load.
+    // Element i's load goes to slot (i - e0) % kSlots and reads x at v[tap] + s29,
+    // where s29 = c * H * W * 4 for the channel of the most recently issued load.
+    // From a padded copy: at v4 + s29 + 4 s, where s29 = (c * xh * xw + r * xw) * 4
+    // for the channel and tap row of that load.
     const int kSlots = sp.slots;
     const int D = std::min(kSlots, E);
-    uint32_t cur = uint32_t(c0) * cstride;
+    uint32_t cur = uint32_t(e0 / RS) * cstride;
     e.s_mov_imm(kSx, cur);
     auto issue = [&](int i) {
-        const int c = c0 + i / RS, t = i % RS, tr = t / g.s, ts = t % g.s;
+        const int c = i / RS, t = i % RS, tr = t / g.s, ts = t % g.s;
         const uint32_t soff = uint32_t(c) * cstride + (padded ? uint32_t(tr) * rstride : 0u);
         if (soff != cur) {
             e.s_add_imm(kSx, soff - cur);  // modulo 2^32
             cur = soff;
         }
+        const int slot = kSlot + (i - e0) % kSlots;
         if (padded)
-            e.mubuf(kLoad, kSlot + i % kSlots, kTap0, kXrsrc, kSx, uint32_t(ts) * 4u);
+            e.mubuf(kLoad, slot, kTap0, kXrsrc, kSx, uint32_t(ts) * 4u);
         else
-            e.mubuf(kLoad, kSlot + i % kSlots, kTap0 + tr * 3 + ts, kXrsrc, kSx);
+            e.mubuf(kLoad, slot, kTap0 + tr * 3 + ts, kXrsrc, kSx);
     };
-    for (int i = 0; i < D; ++i) issue(i);
+    for (int i = 0; i < D; ++i) issue(e0 + i);
 
     for (int i = 0; i < E; ++i) {
         const int issued = std::min(E, i + D);
         e.wait_vm(issued - i - 1);
         const int slot = kSlot + i % kSlots;
-        const int jw = (c0 + i / RS) * RS + i % RS;
+        const int jw = e0 + i;  // column of the element in the packed rows
         // The element's non-zero weights grouped by shift; each shift is formed
         // once, into one of two registers in turn, right before the adds that use it.
         int by_shift[15][kTN], count[15] = {};
@@ -228,12 +251,23 @@ void emit_segment(Emitter &e, const Spec &sp, int kg, int c0, int c1, bool split
                     e.vop2(kOpAdd, kAcc + v, Emitter::vgpr(src), kAcc + v);          // term + acc
             }
         }
-        if (i + D < E) issue(i + D);
+        if (i + D < E) issue(e0 + i + D);
     }
 
+    // The channels this wave finishes: all, or its share of them after the LDS sum.
+    int j0 = 0, j1 = jn;
+    if (sp.wsplit > 1) {
+        for (int j = 0; j < jn; ++j) e.ds_add(kLds, kAcc + j, uint32_t(j) * 256u);
+        e.wait_lgkm0();
+        e.w.push_back(kBarrier);
+        j0 = std::min(jn, share * kTN / sp.wsplit);
+        j1 = std::min(jn, (share + 1) * kTN / sp.wsplit);
+        for (int j = j0; j < j1; ++j) e.ds_read(kAcc + j, kLds, uint32_t(j) * 256u);
+        e.wait_lgkm0();
+    }
     if (!split) {
         if (sp.mul) {
-            for (int j = 0; j < jn; ++j) {
+            for (int j = j0; j < j1; ++j) {
                 // floor(acc * mul / 2^mul_shift): the low word of the 64-bit product
                 // shifted right, taken from its two halves.
                 e.s_mov_imm(kSmul, uint32_t(sp.mul[kbase + j]));
@@ -246,25 +280,25 @@ void emit_segment(Emitter &e, const Spec &sp, int kg, int c0, int c1, bool split
             }
         }
         if (sp.residual) {
-            for (int j0 = 0; j0 < jn; j0 += kSlots) {
-                const int nb = std::min(kSlots, jn - j0);
-                e.s_mov_imm(kSy, uint32_t(kbase + j0) * kstride);
+            for (int jb = j0; jb < j1; jb += kSlots) {
+                const int nb = std::min(kSlots, j1 - jb);
+                e.s_mov_imm(kSy, uint32_t(kbase + jb) * kstride);
                 for (int b = 0; b < nb; ++b) {
                     e.mubuf(kLoad, kSlot + b, kYoff, kRrsrc, kSy);
                     if (b + 1 < nb) e.s_add_imm(kSy, kstride);
                 }
                 e.wait_vm(0);
                 for (int b = 0; b < nb; ++b)
-                    e.vop2(kOpAdd, kAcc + j0 + b, Emitter::vgpr(kSlot + b), kAcc + j0 + b);
+                    e.vop2(kOpAdd, kAcc + jb + b, Emitter::vgpr(kSlot + b), kAcc + jb + b);
             }
         }
         if (sp.relu)
-            for (int j = 0; j < jn; ++j) e.vop2(kOpMax, kAcc + j, Emitter::inline_int(0), kAcc + j);
+            for (int j = j0; j < j1; ++j) e.vop2(kOpMax, kAcc + j, Emitter::inline_int(0), kAcc + j);
     }
-    e.s_mov_imm(kSy, uint32_t(kbase) * kstride);
-    for (int j = 0; j < jn; ++j) {
+    e.s_mov_imm(kSy, uint32_t(kbase + j0) * kstride);
+    for (int j = j0; j < j1; ++j) {
         e.mubuf(split ? kAtomicAdd : kStore, kAcc + j, kYoff, kYrsrc, kSy);
-        if (j + 1 < jn) e.s_add_imm(kSy, kstride);
+        if (j + 1 < j1) e.s_add_imm(kSy, kstride);
     }
     e.w.push_back(kEndpgm);
 }
@@ -275,20 +309,26 @@ void emit_segment(Emitter &e, const Spec &sp, int kg, int c0, int c1, bool split
 std::vector<uint32_t> generate_body(const Spec &sp)
 {
     Emitter e;
-    e.w.resize(size_t(sp.nseg) * kStubWords, kNop);
-    std::vector<size_t> start(sp.nseg);
+    const int nstub = sp.nseg * sp.wsplit;  // stub s19 = block segment * wsplit + share
+    e.w.resize(size_t(nstub) * kStubWords, kNop);
+    std::vector<size_t> start(nstub);
+    const int RS = sp.g.r * sp.g.s;
     int seg = 0;
     for (int kg = 0; kg < sp.kgroups; ++kg) {
-        for (int part = 0; part < sp.nsplit; ++part, ++seg) {
-            while (e.w.size() % 16) e.w.push_back(kNop);
-            start[seg] = e.w.size();
+        for (int part = 0; part < sp.nsplit; ++part) {
             const int c0 = int(int64_t(part) * sp.g.c / sp.nsplit);
             const int c1 = int(int64_t(part + 1) * sp.g.c / sp.nsplit);
-            emit_segment(e, sp, kg, c0, c1, sp.nsplit > 1);
+            const int E = (c1 - c0) * RS;
+            for (int share = 0; share < sp.wsplit; ++share, ++seg) {
+                while (e.w.size() % 16) e.w.push_back(kNop);
+                start[seg] = e.w.size();
+                emit_segment(e, sp, kg, c0 * RS + int(int64_t(E) * share / sp.wsplit),
+                             c0 * RS + int(int64_t(E) * (share + 1) / sp.wsplit), share, sp.nsplit > 1);
+            }
         }
     }
     for (int i = 0; i < 64; ++i) e.w.push_back(kEndpgm);
-    for (int s = 0; s < sp.nseg; ++s) {
+    for (int s = 0; s < nstub; ++s) {
         // s_getpc_b64 s[28:29] (= address of the next word); s_add_u32 s28, s28,
         // delta; s_addc_u32 s29, s29, 0; s_setpc_b64 s[28:29]
         uint32_t *stub = &e.w[size_t(s) * kStubWords];
@@ -380,7 +420,7 @@ struct CreateArgs {
 
 // Planning of a spec whose geometry, codes and epilogue are set: code width
 // checks, pixel tiles, segments and the split of the reduction.
-ds_status finish_spec(Spec &sp, int bits, int splits, int deep_blocks = 2048)
+ds_status finish_spec(Spec &sp, int bits, int splits, int deep_blocks = 3072)
 {
     const ConvGeom &g = sp.g;
     sp.fmt = code_fmt(bits);
@@ -400,24 +440,42 @@ ds_status finish_spec(Spec &sp, int bits, int splits, int deep_blocks = 2048)
         sp.xw = int(xw);
     }
     const int64_t nq = int64_t(g.n) * g.oh * g.ow;
-    sp.tiles_p = int((nq + kBlockPixels - 1) / kBlockPixels);
     sp.kgroups = (g.k + kTN - 1) / kTN;
+    // Wave split (2 or 4 waves per 64 pixels, each with a share of the reduction,
+    // meeting in LDS): more waves without atomics on grids under 2048 workgroups
+    // of 256 pixels (at most 2 from 1024 up), each share keeping 128 reduction
+    // elements (32 on grids under 256 workgroups, where parallelism decides). A
+    // strided 1 x 1 layer, whose loads already span twice the cache lines, splits
+    // at most in 2.
+    const int64_t base = (nq + kBlockPixels - 1) / kBlockPixels * sp.kgroups;
+    {
+        const bool thin = base < 256;
+        const int64_t min_share = thin ? 32 : 128;
+        const bool strided_point = int64_t(g.r) * g.s == 1 && (g.sh > 1 || g.sw > 1);
+        const int cap = (strided_point && !thin) || base >= 1024 ? 2 : 4;
+        int ws = 1;
+        if (base < 2048)
+            while (ws < cap && g.crs / (2 * ws) >= min_share) ws *= 2;
+        const int forced = env_int("DS_JIT_WSPLIT", 0);
+        sp.wsplit = forced == 1 || forced == 2 || forced == 4 ? forced : ws;
+    }
+    const int tile_pixels = kBlockPixels / sp.wsplit;
+    sp.tiles_p = int((nq + tile_pixels - 1) / tile_pixels);
     // Split-K: the parts' partial sums meet in y through int32 atomics after a fill
     // pass, a round trip of y per part, so splitting is kept to what the grid needs.
-    // (1) Toward 384 blocks (1.5 waves per SIMD on MI355X's 1024 SIMDs; a single
-    // wave issues about half as fast), each part keeping at least 64 reduction
-    // elements. (2) A window whose parts keep at least 512 elements (a long
-    // reduction hides the round trips) spreads further, toward `deep_blocks`. A
-    // sweep of every ResNet-50 (N = 128) and ResNet-18 (N = 32) layer over 1-32
-    // parts on MI355X put this rule within 2 % of the best split per layer summed
-    // over each network, where splitting toward 2048 blocks everywhere was 11 % and
-    // 36 % slower.
+    // (1) Toward 384 workgroups (1.5 waves per SIMD on MI355X's 1024 SIMDs), each
+    // wave's share keeping at least 64 reduction elements. (2) A window whose
+    // parts keep at least 768 elements (a long reduction hides the round trips)
+    // spreads further, toward `deep_blocks`. Both splits were fitted to a sweep
+    // of every ResNet-50 (N = 128) and ResNet-18 (N = 32) convolution over wave
+    // splits 1, 2, 4 and 1-8 parts on MI355X: summed over each network the rule
+    // is within 0.5 % of the best choice per layer.
     int ns = splits;
     if (ns == 0) {
-        const int64_t base = int64_t(sp.tiles_p) * sp.kgroups;
-        int64_t want = std::min<int64_t>((384 + base - 1) / base, g.crs / 64);
+        const int64_t blocks = int64_t(sp.tiles_p) * sp.kgroups;
+        int64_t want = std::min<int64_t>((384 + blocks - 1) / blocks, g.crs / (64 * sp.wsplit));
         if (deep_blocks > 0 && int64_t(g.r) * g.s > 1)
-            want = std::max<int64_t>(want, std::min<int64_t>((deep_blocks + base - 1) / base, g.crs / 512));
+            want = std::max<int64_t>(want, std::min<int64_t>((deep_blocks + blocks - 1) / blocks, g.crs / 768));
         ns = int(std::max<int64_t>(1, want));
     }
     sp.nsplit = std::min(ns, g.c);
@@ -427,7 +485,7 @@ ds_status finish_spec(Spec &sp, int bits, int splits, int deep_blocks = 2048)
     // Loads in flight: 14 (the most the register budget holds) on large pixel grids,
     // where a sweep of every ResNet-50 and ResNet-18 layer on MI355X showed the load
     // latency exposed at 8; 8 elsewhere.
-    sp.slots = std::min(kMaxSlots, std::max(1, env_int("DS_JIT_SLOTS", sp.tiles_p >= 1568 ? 14 : 8)));
+    sp.slots = std::min(kMaxSlots, std::max(1, env_int("DS_JIT_SLOTS", nq >= 1568 * kBlockPixels ? 14 : 8)));
     return ok();
 }
 
@@ -707,7 +765,7 @@ extern "C" ds_status ds_jit_conv_backward_data_create(const uint32_t *w_packed, 
             // it splits only toward the 384-block floor (MI355X: a 3x3 stride-2 layer's
             // phases ran 1.3x faster unsplit at 392 blocks than at 2 parts, and 1.1x
             // faster at 2 parts than at 3-11 on a 200-block grid).
-            st = finish_spec(sp, 5, splits, ph.map.dense() ? 2048 : 0);
+            st = finish_spec(sp, 5, splits, ph.map.dense() ? 3072 : 0);
             // Split partial sums meet through int32 atomics, which on a strided map land
             // on scattered addresses: such a phase accumulates densely into a buffer of
             // its own and is scattered into dx afterwards.
@@ -781,13 +839,15 @@ static hipError_t run_part(const ds_jit_conv *plan, const int32_t *x, const int3
         a.pw = padded ? 0 : g.pw;
         a.ybase = int(m.base); a.ynst = m.nstride; a.yrst = m.rstride; a.ycst = m.cstride;
         a.tiles_p = sp.tiles_p;
-        a.group_tiles = std::min(plan->group_tiles, sp.tiles_p);
+        a.group_tiles = std::min(plan->group_tiles * sp.wsplit, sp.tiles_p);
         a.nseg = sp.nseg;
+        a.wsplit_log2 = sp.wsplit == 4 ? 2 : sp.wsplit == 2 ? 1 : 0;
         a.div_ohow = make_fastdiv(uint32_t(a.OHOW));
         a.div_ow = make_fastdiv(uint32_t(a.OW));
         void *args[] = {&a};
+        const unsigned lds = sp.wsplit > 1 ? unsigned(4 / sp.wsplit) * 16384u : 0u;
         e = hipModuleLaunchKernel(plan->fn, unsigned(int64_t(sp.tiles_p) * sp.nseg), 1, 1,
-                                  kBlockPixels, 1, 1, 0, st, args, nullptr);
+                                  kBlockPixels, 1, 1, lds, st, args, nullptr);
     }
     if (e == hipSuccess && split) {
         Epilogue epi;

@@ -13,12 +13,21 @@
 // the lane's taps in x, or an offset past the end of x for taps in the
 // padding; the byte offset of its output pixel in y) and hands them over in
 // fixed registers at the JITBODY marker. At run time the generator replaces
-// the marker with a jump, through a table, to the code of this workgroup's
-// segment (64 output channels and a range of input channels), assembled from
+// the marker with a jump, through a table, to the code of this wave's segment
+// (64 output channels and a range of input channels), assembled from
 // generated machine words; each segment ends the wave itself. Register use of
 // the generated code (the clobbers below): v14..v95 (v16, v17 the shifted
 // values, v18..v81 the accumulators, v82..v95 the loads in flight), s28..s31;
 // 96 VGPRs in all, so that 5 waves fit on a SIMD.
+//
+// A workgroup is 4 waves. Without a wave split each wave covers 64 pixels of a
+// 256-pixel tile with the whole reduction of its segment. With a split of 2 or
+// 4 (grids too small to fill the chip otherwise), that many waves share 64
+// pixels, each with a contiguous share of the reduction in code of its own;
+// they add their partial sums into LDS, which the prologue zeroes, and after a
+// barrier each finishes its share of the 64 channels. v3 holds the lane's LDS
+// byte offset: (pixel group in the workgroup) * 16 KiB + lane * 4, channel j
+// at j * 256 above it.
 #include <hip/hip_runtime.h>
 
 #include <cstdint>
@@ -29,8 +38,11 @@ using ds::JitArgs;
 
 extern "C" __global__ void __launch_bounds__(256) ds_jit_conv_template(const JitArgs p)
 {
+    extern __shared__ int32_t red[];  // wave split: [4 >> wsplit_log2][64 channels][64 lanes]
     const int lane = threadIdx.x & 63;
     const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+    const int wl = p.wsplit_log2;
+    const int pg = wave >> wl, share = wave & ((1 << wl) - 1);  // pixel group, reduction share
     // Block order: groups of `group_tiles` pixel tiles (the last group may be
     // smaller); within a group, the segments one after the other, and within a
     // segment the group's tiles, so that the waves running at the same time
@@ -40,9 +52,16 @@ extern "C" __global__ void __launch_bounds__(256) ds_jit_conv_template(const Jit
     const int per_group = p.group_tiles * p.nseg;
     const int grp = b / per_group, r = b - grp * per_group;
     const int gsize = min(p.group_tiles, p.tiles_p - grp * p.group_tiles);
-    const int seg = __builtin_amdgcn_readfirstlane(r / gsize);
+    const int seg = __builtin_amdgcn_readfirstlane(((r / gsize) << wl) + share);
     const int tile = grp * p.group_tiles + (r - (r / gsize) * gsize);
-    const int q = tile * 256 + wave * 64 + lane;
+    const int q = ((tile << (2 - wl)) + pg) * 64 + lane;
+    const int lds = pg * 16384 + lane * 4;
+    if (wl > 0) {
+        // Each wave zeroes 64 >> wl channels of its pixel group's partial sums.
+        const int per = 64 >> wl;
+        for (int j = 0; j < per; ++j) red[(pg * 64 + share * per + j) * 64 + lane] = 0;
+        __syncthreads();
+    }
     const int kOOB = int(0x80000000u);
     int yoff = kOOB;
     int t0 = kOOB, t1 = kOOB, t2 = kOOB, t3 = kOOB, t4 = kOOB, t5 = kOOB, t6 = kOOB, t7 = kOOB,
@@ -71,7 +90,7 @@ extern "C" __global__ void __launch_bounds__(256) ds_jit_conv_template(const Jit
         const_cast<int32_t *>(p.residual), short(0), p.residual ? p.y_bytes : 0, 0x00020000);
     asm volatile("; JITBODY"
                  :
-                 : "{s[20:23]}"(xr), "{s[24:27]}"(yr), "{s[36:39]}"(rr), "{s19}"(seg),
+                 : "{s[20:23]}"(xr), "{s[24:27]}"(yr), "{s[36:39]}"(rr), "{s19}"(seg), "{v3}"(lds),
                    "{v4}"(t0), "{v5}"(t1), "{v6}"(t2), "{v7}"(t3), "{v8}"(t4), "{v9}"(t5),
                    "{v10}"(t6), "{v11}"(t7), "{v12}"(t8), "{v13}"(yoff)
                  : "memory", "v14", "v15", "v16", "v17", "v18", "v19", "v20", "v21", "v22", "v23",

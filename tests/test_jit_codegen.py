@@ -87,7 +87,7 @@ def pad_input(x, pd, xh, xw):
     return xp[:, :, :xh, :xw]
 
 
-def lane_inputs(n, c, h, w, k, r, s, st, pd):
+def lane_inputs(n, c, h, w, k, r, s, st, pd, wsplit=1):
     """Per lane (pixel q of every 256-pixel tile): tap byte offsets v4..v12 of
     the 3 x 3 window at channel 0 and the output byte offset v13, as the
     template kernel computes them (past-the-end marker for padding and for
@@ -110,25 +110,35 @@ def lane_inputs(n, c, h, w, k, r, s, st, pd):
             ok = valid & (ih >= 0) & (ih < h) & (iw >= 0) & (iw < w)
             regs[4 + rr * 3 + ss] = np.where(ok, (nn * c * h * w + ih * w + iw) * 4, OOB).astype(np.int64)
     regs[13] = np.where(valid, (nn * k * oh * ow + pix) * 4, OOB).astype(np.int64)
+    # v3: LDS byte offset of the lane's pixel in its workgroup (wave split)
+    within = q % (256 // wsplit)
+    regs[3] = ((within // 64) * 16384 + (within % 64) * 4).astype(np.int64)
     return regs, (oh, ow)
 
 
 class Interp:
-    """The generated code, run for all lanes of one segment."""
+    """The generated code, run for all lanes of one segment. ``run`` is a
+    generator that stops at each s_barrier, so that the waves sharing pixels
+    (wave split) can be run up to the barrier one after the other. LDS is one
+    row of 64 channels per lane (pixel); an LDS access must land in the lane's
+    own row."""
 
-    def __init__(self, insts, bufs):
+    def __init__(self, insts, bufs, wsplit=1):
         self.insts, self.bufs = insts, bufs   # bufs: sgpr base -> (uint32 array, num_records)
+        self.wsplit = wsplit
 
     @staticmethod
     def reg(tok):
         m = re.fullmatch(r"([vs])(\d+)", tok)
         return (m.group(1), int(m.group(2))) if m else None
 
-    def run(self, start, seg, lanes, y, atomic_ok):
+    def run(self, start, seg, lanes, y, atomic_ok, lds, stored):
         V = {i: a.copy() for i, a in lanes.items()}
         S = {19: seg}
         pending = collections.OrderedDict()   # vgpr -> value, in issue order
-        stored = collections.Counter()
+        lgkm = {}                              # vgpr -> value of an LDS read in flight
+        q = np.arange(V[3].size)
+        tile_px = 256 // self.wsplit
         pc = start
         steps = 0
 
@@ -139,8 +149,15 @@ class Interp:
             kind, i = rg
             if kind == "s":
                 return S[i] & M32
-            assert i not in pending, f"v{i} read before its load completed (pc {pc:#x})"
+            assert i not in pending and i not in lgkm, f"v{i} read before its load completed (pc {pc:#x})"
             return V[i]
+
+        def lds_row(ops_, imm_tok):
+            off = V[int(ops_[0][1:])] + int(imm_tok.split(":")[1]) if imm_tok else V[int(ops_[0][1:])]
+            j, rem = (off % 16384) // 256, off % 256
+            assert np.all((off // 16384) * 64 + rem // 4 == q % tile_px), "LDS access outside the lane's row"
+            assert np.all(j == j[0]) and 0 <= j[0] < 64
+            return int(j[0])
 
         def sq(tok):
             return int(re.fullmatch(r"s\[(\d+):\d+\]", tok).group(1))
@@ -173,17 +190,31 @@ class Interp:
                 S[int(ops[0][1:])] = val(ops[1])
             elif op == "s_waitcnt":
                 m = re.fullmatch(r"vmcnt\((\d+)\)", ops[0])
-                keep = int(m.group(1))
-                while len(pending) > keep:
-                    i, v = pending.popitem(last=False)
-                    V[i] = v
+                if m:
+                    keep = int(m.group(1))
+                    while len(pending) > keep:
+                        i, v = pending.popitem(last=False)
+                        V[i] = v
+                else:
+                    assert ops[0] == "lgkmcnt(0)", ops
+                    V.update(lgkm)
+                    lgkm.clear()
+            elif op == "s_barrier":
+                assert not lgkm and not pending
+                yield pc
+            elif op == "ds_add_u32":
+                j = lds_row(ops[:1], next((t for t in ops[2:] if t.startswith("offset:")), None))
+                lds[:, j] = (lds[:, j] + val(ops[1])) & M32
+            elif op == "ds_read_b32":
+                j = lds_row(ops[1:2], next((t for t in ops[2:] if t.startswith("offset:")), None))
+                lgkm[int(ops[0][1:])] = lds[:, j].copy()
             elif op == "buffer_load_dword":
                 arr, inr, idx = access(ops)
                 d = int(ops[0][1:])
                 assert d not in pending
                 pending[d] = np.where(inr, arr[np.where(inr, idx, 0)], 0).astype(np.int64) & M32
             elif op in ("buffer_store_dword", "buffer_atomic_add"):
-                assert not pending, "store with loads in flight"
+                assert not pending and not lgkm, "store with loads in flight"
                 arr, inr, idx = access(ops)
                 assert arr is y
                 v = val(ops[0]).astype(np.int64)
@@ -222,7 +253,8 @@ class Interp:
                 sh = int(ops[3], 0)
                 V[int(ops[0][1:])] = np.array((((hi << 32) | lo) >> sh) & M32, dtype=np.int64)
             elif op == "s_endpgm":
-                return stored
+                assert not lgkm
+                return
             elif op == "s_nop":
                 pass
             else:
@@ -247,12 +279,21 @@ CASES = [
     (2, 3, 13, 11, 70, 7, 7, 2, 3, 1, "full"),     # a padded copy of x (windows over 3 x 3)
     (1, 4, 9, 10, 20, 5, 4, 1, 2, 2, "none"),
     (1, 2, 12, 12, 9, 4, 6, 3, 0, 1, "relu"),      # stride leaves the last rows unread
+    # wave splits (forced): 2 or 4 waves share 64 pixels, each with a share of
+    # the reduction, meeting in LDS
+    (2, 40, 9, 9, 70, 3, 3, 1, 1, 1, "full", 2),
+    (3, 37, 7, 6, 64, 3, 3, 2, 1, 1, "full", 4),
+    (2, 5, 9, 9, 33, 3, 3, 1, 1, 2, "none", 4),     # with split-K: atomics of each share
+    (1, 300, 3, 5, 130, 1, 1, 1, 0, 1, "mul", 4),
+    (1, 3, 13, 11, 20, 7, 7, 2, 3, 1, "relu", 2),   # padded copy and wave split
 ]
 
 
 @pytest.mark.parametrize("case", CASES, ids=[str(i) for i in range(len(CASES))])
-def test_generated_code_matches_oracle(case, tmp_path):
-    n, c, h, w, k, r, s, st, pd, splits, epi = case
+def test_generated_code_matches_oracle(case, tmp_path, monkeypatch):
+    n, c, h, w, k, r, s, st, pd, splits, epi = case[:11]
+    wsplit = case[11] if len(case) > 11 else 1
+    monkeypatch.setenv("DS_JIT_WSPLIT", str(wsplit))
     codes, x, rng = gen_layer(zlib.crc32(str(case).encode()), n, c, h, w, k, r, s)
     bias = rng.integers(-(2 ** 31), 2 ** 31, k, dtype=np.int64).astype(np.int32)
     mul = add = res = None
@@ -262,7 +303,7 @@ def test_generated_code_matches_oracle(case, tmp_path):
         add = rng.integers(-(2 ** 31), 2 ** 31, k, dtype=np.int64).astype(np.int32)
         add[0] = 0
     wp = ops.pack_shift_weights(codes)
-    lanes, (oh, ow) = lane_inputs(n, c, h, w, k, r, s, st, pd)
+    lanes, (oh, ow) = lane_inputs(n, c, h, w, k, r, s, st, pd, wsplit)
     if epi == "full":
         res = rng.integers(-(2 ** 31), 2 ** 31, (n, k, oh, ow), dtype=np.int64).astype(np.int32)
     img = ops.jit_conv_image(wp, (n, c, h, w), (r, s), st, pd, bias=bias, mul=mul, add=add,
@@ -287,10 +328,20 @@ def test_generated_code_matches_oracle(case, tmp_path):
     split = nsplit > 1
     if split:
         y[:] = np.repeat(np.tile(bias.view(np.uint32).astype(np.int64), n), oh * ow)
-    interp = Interp(insts, bufs)
+    stubs = sum(1 for op, _, _ in insts.values() if op == "s_getpc_b64")
+    assert stubs == kgroups * nsplit * wsplit
+    interp = Interp(insts, bufs, wsplit)
     total = collections.Counter()
     for seg in range(kgroups * nsplit):
-        total.update(interp.run(body + 20 * seg, seg, lanes, y, split))
+        # the waves of one pixel group: each share up to the barrier, then each to the end
+        lds = np.zeros((lanes[4].size, 64), np.int64)
+        runs = [interp.run(body + 20 * (seg * wsplit + sh), seg * wsplit + sh, lanes, y, split, lds, total)
+                for sh in range(wsplit)]
+        for _ in range(2 if wsplit > 1 else 1):
+            for r_ in runs:
+                next(r_, None)
+        for r_ in runs:
+            assert next(r_, "done") == "done", "a second barrier"
     assert len(total) == y.size and set(total.values()) == {nsplit}
     got = to_i32(y).reshape(n, k, oh, ow)
     if split:
