@@ -211,13 +211,18 @@ hipError_t run_backward_data(const ConvGeom &g, const int32_t *dy, const uint32_
     hipError_t e = words ? scratch_alloc(&scratch, words * 4, st) : hipSuccess;
     if (e != hipSuccess) return e;
     uint32_t *packed = static_cast<uint32_t *>(scratch);
+    // Rows or columns no tap reaches are zero: dx is cleared densely first (the
+    // phases then write their own positions), which is several times faster than
+    // filling the empty phases through their strided maps.
+    for (const PhasePlan &pp : phases)
+        if (e == hipSuccess && (pp.ph.g.r == 0 || pp.ph.g.s == 0)) {
+            e = run_fill_zero(dx, int64_t(g.n) * g.c * g.h * g.w, st);
+            break;
+        }
     for (const PhasePlan &pp : phases) {
         if (e != hipSuccess) break;
         const GradPhase &p = pp.ph;
-        if (p.g.r == 0 || p.g.s == 0) {  // no taps reach these rows or columns
-            e = run_fill_mapped(p.g, nullptr, dx, p.map, st);
-            continue;
-        }
+        if (p.g.r == 0 || p.g.s == 0) continue;
         uint32_t *pw = packed + pp.word_offset;
         const int64_t total = int64_t(p.g.k) * pp.wpr;
         const int grid = int(std::min<int64_t>((total + 255) / 256, 4096));

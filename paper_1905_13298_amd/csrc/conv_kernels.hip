@@ -220,6 +220,19 @@ copy_mapped_kernel(const int32_t *__restrict__ src, int32_t *__restrict__ y, int
     }
 }
 
+// y[0 .. count) = 0, 16 bytes per store (y 16-byte aligned, count a multiple of 4).
+__global__ void __launch_bounds__(256) fill_zero_kernel(int4 *__restrict__ y, int64_t count4)
+{
+    for (int64_t i = int64_t(blockIdx.x) * 256 + threadIdx.x; i < count4; i += int64_t(gridDim.x) * 256)
+        y[i] = make_int4(0, 0, 0, 0);
+}
+
+__global__ void __launch_bounds__(256) fill_zero_scalar_kernel(int32_t *__restrict__ y, int64_t count)
+{
+    for (int64_t i = int64_t(blockIdx.x) * 256 + threadIdx.x; i < count; i += int64_t(gridDim.x) * 256)
+        y[i] = 0;
+}
+
 // xp[p][i][j] = x[p][i - ph][j - pw] where that lies inside x, else 0: planes of
 // h x w copied into zero-padded planes of xh x xw (which may also crop).
 __global__ void __launch_bounds__(256)
@@ -859,6 +872,24 @@ hipError_t run_copy_mapped(const ConvGeom &g, const int32_t *src, int32_t *y, co
     hipLaunchKernelGGL(copy_mapped_kernel, dim3(grid), dim3(256), 0, st, src, y, int(total),
                        make_fastdiv(uint32_t(g.ow)), make_fastdiv(uint32_t(g.oh)),
                        make_fastdiv(uint32_t(g.k)), map);
+    return hipGetLastError();
+}
+
+hipError_t run_fill_zero(int32_t *y, int64_t count, hipStream_t st)
+{
+    if (count <= 0) return hipSuccess;
+    // The 16-byte-aligned body in vector stores, the few elements around it one by one.
+    const int64_t head = std::min<int64_t>(count, ((16 - int64_t(reinterpret_cast<uintptr_t>(y) & 15)) & 15) / 4);
+    const int64_t body4 = (count - head) / 4;
+    const int64_t tail = count - head - body4 * 4;
+    if (reinterpret_cast<uintptr_t>(y) & 3) return hipErrorInvalidValue;
+    if (head)
+        hipLaunchKernelGGL(fill_zero_scalar_kernel, dim3(1), dim3(256), 0, st, y, head);
+    if (body4)
+        hipLaunchKernelGGL(fill_zero_kernel, dim3(unsigned(std::min<int64_t>((body4 + 255) / 256, 8192))),
+                           dim3(256), 0, st, reinterpret_cast<int4 *>(y + head), body4);
+    if (tail)
+        hipLaunchKernelGGL(fill_zero_scalar_kernel, dim3(1), dim3(256), 0, st, y + head + body4 * 4, tail);
     return hipGetLastError();
 }
 

@@ -94,6 +94,8 @@ hipError_t run_fill_mapped(const ConvGeom &g, const int32_t *init, int32_t *y, c
 hipError_t run_copy_mapped(const ConvGeom &g, const int32_t *src, int32_t *y, const OutMap &map,
                            hipStream_t stream);
 hipError_t run_epilogue(const ConvGeom &g, int32_t *y, const Epilogue &epi, hipStream_t stream);
+// y[0 .. count) = 0 (a 4-byte-aligned y), in 16-byte stores where aligned.
+hipError_t run_fill_zero(int32_t *y, int64_t count, hipStream_t stream);
 // xp [planes][xh][xw] = x [planes][h][w] shifted down by ph rows and right by pw
 // columns, zeros elsewhere (rows and columns past xh, xw are dropped).
 hipError_t run_pad_planes(const int32_t *x, int32_t *xp, int64_t planes, int h, int w, int ph,

@@ -891,8 +891,9 @@ extern "C" ds_status ds_jit_conv_run(const ds_jit_conv *plan, const int32_t *x,
     if (!plan->backward) {
         e = run_part(plan, x, residual, y, xb, yb, st);
     } else {
-        for (const GradPhase &z : plan->zeros)
-            if (e == hipSuccess) e = run_fill_mapped(z.g, nullptr, y, z.map, st);
+        // Positions no tap reaches are zero: all of dx is cleared densely first.
+        if (!plan->zeros.empty())
+            e = run_fill_zero(y, int64_t(g.n) * g.c * g.h * g.w, st);
         for (const ds_jit_conv *part : plan->parts)
             if (e == hipSuccess) e = run_part(part, x, nullptr, y, xb, yb, st);
     }

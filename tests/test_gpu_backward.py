@@ -126,6 +126,32 @@ def test_output_fully_overwritten_and_repeatable():
         np.testing.assert_array_equal(out.cpu().numpy(), want)
 
 
+@pytest.mark.parametrize("offset", [0, 1, 2, 3])
+def test_cleared_positions_at_any_alignment(offset):
+    """A 1x1 stride-2 layer: dx is cleared densely (16-byte stores on the aligned
+    part, single stores around it) before the phase writes its positions; dx views
+    at every 4-byte offset, with guard elements around them left untouched, on
+    both paths."""
+    n, c, h, w, k = 3, 20, 15, 13, 33
+    dy, codes, _ = make(91 + offset, n, c, h, w, k, 1, 1, 2, 0)
+    wph = ops.pack_shift_weights(codes)
+    wp = to_dev(wph.view(np.int32))
+    want = oracle.conv2d_shift_backward_data(dy, codes, (n, c, h, w), r=1, stride=2, pad=0)
+    size = n * c * h * w
+    plan = ops.JitConvBackwardData(wph, (n, c, h, w), 1, 2, 0)
+    for run in ("runtime", "plan"):
+        big = torch.full((size + 8,), 0x5A5A5A5A, dtype=torch.int32, device=DEV)
+        out = big[offset:offset + size].view(n, c, h, w)
+        if run == "runtime":
+            ops.conv2d_shift_backward_data(to_dev(dy), wp, (n, c, h, w), 1, 2, 0, out=out)
+        else:
+            plan(to_dev(dy), out=out)
+        got = big.cpu().numpy()
+        np.testing.assert_array_equal(got[offset:offset + size].reshape(want.shape), want, err_msg=run)
+        assert np.all(got[:offset] == 0x5A5A5A5A) and np.all(got[offset + size:] == 0x5A5A5A5A), run
+    plan.close()
+
+
 def test_errors_write_nothing():
     n, c, h, w, k = 1, 4, 6, 6, 5
     dy = torch.zeros((n, k, 6, 6), dtype=torch.int32, device=DEV)
