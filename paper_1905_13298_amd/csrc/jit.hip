@@ -159,6 +159,11 @@ struct Spec {
     // part's reduction elements, meeting in LDS; a workgroup covers 256 / wsplit
     // pixels.
     int wsplit = 1;
+    // Fused stride phases of an input gradient: output-channel group kg stores
+    // its first channel at element kout[kg] + (pixel's map offset) and has kjn[kg]
+    // channels (empty: group kg stores channel 64 kg + j at its map offset).
+    std::vector<int64_t> kout;
+    std::vector<int> kjn;
 };
 
 // Element strides of the output map of a spec (the dense layout when unset).
@@ -189,18 +194,32 @@ inline int code_at(const Spec &sp, int k, int j)
 void emit_segment(Emitter &e, const Spec &sp, int kg, int e0, int e1, int share, bool split)
 {
     const ConvGeom &g = sp.g;
-    const int kbase = kg * kTN, jn = std::min(kTN, g.k - kbase);
-    const int RS = g.r * g.s, E = e1 - e0;
+    const int kbase = kg * kTN;
+    const int jn = sp.kjn.empty() ? std::min(kTN, g.k - kbase) : sp.kjn[size_t(kg)];
+    const int RS = g.r * g.s;
     const bool padded = sp.xh > 0;
     const uint32_t cstride = padded ? uint32_t(sp.xh) * uint32_t(sp.xw) * 4u
                                     : uint32_t(g.h) * uint32_t(g.w) * 4u;
     const uint32_t rstride = uint32_t(sp.xw) * 4u;
     const uint32_t kstride = uint32_t(full_map(sp).kstride) * 4u;
+    // Byte offset of the group's first output channel (added to the lane's v13).
+    const uint32_t out0 = sp.kout.empty() ? uint32_t(kbase) * kstride : uint32_t(sp.kout[size_t(kg)]) * 4u;
+    // The elements with at least one non-zero weight in the group; the others
+    // contribute nothing and are not even loaded.
+    std::vector<int> el;
+    el.reserve(size_t(e1 - e0));
+    for (int i = e0; i < e1; ++i)
+        for (int j = 0; j < jn; ++j)
+            if ((code_at(sp, kbase + j, i) & 15) != 15) {
+                el.push_back(i);
+                break;
+            }
+    const int E = int(el.size());
 
     for (int j = 0; j < jn; ++j)
         e.mov_imm(kAcc + j, (!split && sp.bias && share == 0) ? sp.bias[kbase + j] : 0);
 
-    // Element i's load goes to slot (i - e0) % kSlots and reads x at v[tap] + s29,
+    // Listed element n's load goes to slot n % kSlots and reads x at v[tap] + s29,
     // where s29 = c * H * W * 4 for the channel of the most recently issued load.
     // From a padded copy: at v4 + s29 + 4 s, where s29 = (c * xh * xw + r * xw) * 4
     // for the channel and tap row of that load.
@@ -208,26 +227,27 @@ void emit_segment(Emitter &e, const Spec &sp, int kg, int e0, int e1, int share,
     const int D = std::min(kSlots, E);
     uint32_t cur = uint32_t(e0 / RS) * cstride;
     e.s_mov_imm(kSx, cur);
-    auto issue = [&](int i) {
+    auto issue = [&](int n) {
+        const int i = el[size_t(n)];
         const int c = i / RS, t = i % RS, tr = t / g.s, ts = t % g.s;
         const uint32_t soff = uint32_t(c) * cstride + (padded ? uint32_t(tr) * rstride : 0u);
         if (soff != cur) {
             e.s_add_imm(kSx, soff - cur);  // modulo 2^32
             cur = soff;
         }
-        const int slot = kSlot + (i - e0) % kSlots;
+        const int slot = kSlot + n % kSlots;
         if (padded)
             e.mubuf(kLoad, slot, kTap0, kXrsrc, kSx, uint32_t(ts) * 4u);
         else
             e.mubuf(kLoad, slot, kTap0 + tr * 3 + ts, kXrsrc, kSx);
     };
-    for (int i = 0; i < D; ++i) issue(e0 + i);
+    for (int n = 0; n < D; ++n) issue(n);
 
     for (int i = 0; i < E; ++i) {
         const int issued = std::min(E, i + D);
         e.wait_vm(issued - i - 1);
         const int slot = kSlot + i % kSlots;
-        const int jw = e0 + i;  // column of the element in the packed rows
+        const int jw = el[size_t(i)];  // column of the element in the packed rows
         // The element's non-zero weights grouped by shift; each shift is formed
         // once, into one of two registers in turn, right before the adds that use it.
         int by_shift[15][kTN], count[15] = {};
@@ -251,7 +271,7 @@ void emit_segment(Emitter &e, const Spec &sp, int kg, int e0, int e1, int share,
                     e.vop2(kOpAdd, kAcc + v, Emitter::vgpr(src), kAcc + v);          // term + acc
             }
         }
-        if (i + D < E) issue(e0 + i + D);
+        if (i + D < E) issue(i + D);
     }
 
     // The channels this wave finishes: all, or its share of them after the LDS sum.
@@ -282,7 +302,7 @@ void emit_segment(Emitter &e, const Spec &sp, int kg, int e0, int e1, int share,
         if (sp.residual) {
             for (int jb = j0; jb < j1; jb += kSlots) {
                 const int nb = std::min(kSlots, j1 - jb);
-                e.s_mov_imm(kSy, uint32_t(kbase + jb) * kstride);
+                e.s_mov_imm(kSy, out0 + uint32_t(jb) * kstride);
                 for (int b = 0; b < nb; ++b) {
                     e.mubuf(kLoad, kSlot + b, kYoff, kRrsrc, kSy);
                     if (b + 1 < nb) e.s_add_imm(kSy, kstride);
@@ -295,7 +315,7 @@ void emit_segment(Emitter &e, const Spec &sp, int kg, int e0, int e1, int share,
         if (sp.relu)
             for (int j = j0; j < j1; ++j) e.vop2(kOpMax, kAcc + j, Emitter::inline_int(0), kAcc + j);
     }
-    e.s_mov_imm(kSy, uint32_t(kbase + j0) * kstride);
+    e.s_mov_imm(kSy, out0 + uint32_t(j0) * kstride);
     for (int j = j0; j < j1; ++j) {
         e.mubuf(split ? kAtomicAdd : kStore, kAcc + j, kYoff, kYrsrc, kSy);
         if (j + 1 < j1) e.s_add_imm(kSy, kstride);
@@ -560,6 +580,82 @@ std::vector<uint32_t> repack_phase(const uint32_t *wp, const ConvGeom &fwd, cons
     return out;
 }
 
+// The stride phases of an input gradient as one problem: output-channel group
+// (phase p, channels 64 q ..) of a stride-1 correlation of dy over the union of
+// the phases' windows, aligned at a common padding (the largest); a phase's tap
+// t sits at union tap t + (P - its padding), and the union taps outside its own
+// window carry zero weights, which generate no code. Possible when at least two
+// phases have taps and all of those share one output grid. Fills sp (geometry,
+// map, kout, kjn) and the codes it points to; false otherwise.
+bool fuse_phases(const uint32_t *wp, const ConvGeom &fwd, const std::vector<GradPhase> &phases,
+                 Spec &sp, std::vector<uint32_t> &codes)
+{
+    std::vector<const GradPhase *> act;
+    for (const GradPhase &ph : phases)
+        if (ph.g.r > 0 && ph.g.s > 0) act.push_back(&ph);
+    if (act.size() < 2) return false;
+    int P = act[0]->g.ph, Q = act[0]->g.pw;
+    for (const GradPhase *ph : act) {
+        if (ph->g.oh != act[0]->g.oh || ph->g.ow != act[0]->g.ow) return false;
+        P = std::max(P, ph->g.ph);
+        Q = std::max(Q, ph->g.pw);
+    }
+    int Tu = 0, Tv = 0;
+    for (const GradPhase *ph : act) {
+        Tu = std::max(Tu, ph->g.r + P - ph->g.ph);
+        Tv = std::max(Tv, ph->g.s + Q - ph->g.pw);
+    }
+    const int C = fwd.c, K = fwd.k, cpad = (C + kTN - 1) / kTN * kTN, groups = cpad / kTN;
+    ConvGeom &g = sp.g;
+    g = act[0]->g;
+    g.k = int(act.size()) * cpad;
+    g.r = Tu;
+    g.s = Tv;
+    g.ph = P;
+    g.pw = Q;
+    g.crs = K * Tu * Tv;
+    g.bits = 5;
+    sp.map = act[0]->map;
+    sp.map.base = 0;
+    const CodeFmt src = code_fmt(fwd.bits);
+    const int64_t wpr_in = row_words_bits(fwd.crs, fwd.bits);
+    const int64_t wpr = row_words(g.crs);
+    codes.assign(size_t(g.k) * size_t(wpr), 0u);
+    sp.kout.clear();
+    sp.kjn.clear();
+    for (size_t pi = 0; pi < act.size(); ++pi) {
+        const GradPhase &ph = *act[pi];
+        const int du = P - ph.g.ph, dv = Q - ph.g.pw;
+        for (int q = 0; q < groups; ++q) {
+            sp.kout.push_back(ph.map.base + int64_t(q) * kTN * ph.map.kstride);
+            sp.kjn.push_back(std::min(kTN, C - q * kTN));
+        }
+        for (int c = 0; c < cpad; ++c) {
+            uint32_t *row = codes.data() + (pi * size_t(cpad) + size_t(c)) * size_t(wpr);
+            for (int64_t wd = 0; wd < wpr; ++wd) {
+                uint32_t word = 0;
+                for (int j = 0; j < 6; ++j) {
+                    const int64_t jp = wd * 6 + j;
+                    uint32_t code = 15u;
+                    if (c < C && jp < g.crs) {
+                        const int k = int(jp / (Tu * Tv)), rem = int(jp % (Tu * Tv));
+                        const int t = rem / Tv - du, u = rem % Tv - dv;
+                        if (t >= 0 && t < ph.g.r && u >= 0 && u < ph.g.s) {
+                            const int r = ph.r0 + fwd.sh * (ph.g.r - 1 - t);
+                            const int s = ph.s0 + fwd.sw * (ph.g.s - 1 - u);
+                            code = src.at(wp + int64_t(k) * wpr_in, (c * fwd.r + r) * fwd.s + s);
+                        }
+                    }
+                    word |= code << (5 * j);
+                }
+                row[wd] = word;
+            }
+        }
+    }
+    sp.wp = codes.data();
+    return true;
+}
+
 }  // namespace
 }  // namespace ds
 
@@ -751,11 +847,30 @@ extern "C" ds_status ds_jit_conv_backward_data_create(const uint32_t *w_packed, 
             delete p;
             return fail(DS_ERR_HIP, "no HIP device");
         }
-        for (const GradPhase &ph : phases) {
-            if (ph.g.r == 0 || ph.g.s == 0) {
-                p->zeros.push_back(ph);
-                continue;
+        for (const GradPhase &ph : phases)
+            if (ph.g.r == 0 || ph.g.s == 0) p->zeros.push_back(ph);
+        // Stride phases fused into one kernel when they can be (no split of the
+        // reduction: the wave split supplies the parallelism); else one per phase.
+        {
+            Spec sp;
+            std::vector<uint32_t> codes;
+            if (splits <= 1 && fuse_phases(w_packed, g, phases, sp, codes)) {
+                st = finish_spec(sp, 5, 1, 0);
+                ds_jit_conv *part = nullptr;
+                if (st == DS_SUCCESS) st = build_plan(sp, &part);
+                if (st != DS_SUCCESS) {
+                    const std::string msg = last_error();
+                    destroy_plan(p);
+                    return fail(st, "%s", msg.c_str());
+                }
+                p->code_bytes += part->code_bytes;
+                p->parts.push_back(part);
+                *plan = p;
+                return ok();
             }
+        }
+        for (const GradPhase &ph : phases) {
+            if (ph.g.r == 0 || ph.g.s == 0) continue;
             const std::vector<uint32_t> codes = repack_phase(w_packed, g, ph);
             Spec sp;
             sp.g = ph.g;

@@ -370,12 +370,18 @@ def test_image_rejects_bad_arguments():
 
 
 def test_zero_weights_emit_no_arithmetic(tmp_path):
-    """A segment whose weights are all zero is bias, loads and stores only."""
+    """A segment whose weights are all zero is bias and stores only: elements with
+    no non-zero weight in a segment are not even loaded."""
     codes = np.full((8, 4), 15 | 16, np.uint8)
     img = ops.jit_conv_image(ops.pack_shift_weights(codes), (1, 4, 3, 3), 1, splits=1)
     names = collections.Counter(op for op, _, _ in disassemble(img, str(tmp_path)).values())
     assert names["v_add_u32_e32"] == names["v_sub_u32_e32"] == names["v_ashrrev_i32_e32"] == 0
-    assert names["buffer_store_dword"] == 8
+    assert names["buffer_load_dword"] == 0 and names["buffer_store_dword"] == 8
+    codes[3, 2] = 16 | 4      # one non-zero weight: one load, one shift, one subtract
+    img = ops.jit_conv_image(ops.pack_shift_weights(codes), (1, 4, 3, 3), 1, splits=1)
+    names = collections.Counter(op for op, _, _ in disassemble(img, str(tmp_path)).values())
+    assert names["buffer_load_dword"] == 1 and names["v_ashrrev_i32_e32"] == 1
+    assert names["v_sub_u32_e32"] == 1 and names["v_add_u32_e32"] == 0
 
 
 @pytest.mark.parametrize("bits", [2, 3, 4])
