@@ -490,17 +490,29 @@ ds_status finish_spec(Spec &sp, int bits, int splits, int deep_blocks = 3072)
     // of every ResNet-50 (N = 128) and ResNet-18 (N = 32) convolution over wave
     // splits 1, 2, 4 and 1-8 parts on MI355X: summed over each network the rule
     // is within 0.5 % of the best choice per layer.
+    // (3) A 1 x 1 layer on a grid under 256 workgroups of 256 pixels (at least 4
+    // pixel tiles) whose wave shares keep at least 128 elements per part spreads
+    // toward 2400 workgroups (ResNet-50's 2048 -> 512 layer at 7 x 7: 3 parts ran
+    // 1.1x faster than 1 or 2).
     int ns = splits;
     if (ns == 0) {
         const int64_t blocks = int64_t(sp.tiles_p) * sp.kgroups;
         int64_t want = std::min<int64_t>((384 + blocks - 1) / blocks, g.crs / (64 * sp.wsplit));
         if (deep_blocks > 0 && int64_t(g.r) * g.s > 1)
             want = std::max<int64_t>(want, std::min<int64_t>((deep_blocks + blocks - 1) / blocks, g.crs / 768));
+        const int64_t tiles256 = (nq + kBlockPixels - 1) / kBlockPixels;
+        if (int64_t(g.r) * g.s == 1 && base < 256 && tiles256 >= 4)
+            want = std::max<int64_t>(want, std::min<int64_t>((2400 + blocks - 1) / blocks, g.crs / (128 * sp.wsplit)));
+        // (4) Fewer than 4 tiles of 256 pixels (a LinearShift at small batch): every
+        // code segment streams through the instruction cache for a few waves only,
+        // and more parts mean more code streams: at most 2 (2048 -> 1000 at batch
+        // 128: 62 us at 2 parts, 112 us at 8).
+        if (tiles256 < 4) want = std::min<int64_t>(want, 2);
         ns = int(std::max<int64_t>(1, want));
     }
     sp.nsplit = std::min(ns, g.c);
     const int64_t nseg = int64_t(sp.kgroups) * sp.nsplit;
-    if (nseg * 8 * ((sp.tiles_p + 7) / 8) > INT32_MAX) return fail(DS_ERR_UNSUPPORTED, "grid too large");
+    if (nseg * sp.tiles_p > INT32_MAX) return fail(DS_ERR_UNSUPPORTED, "grid too large");
     sp.nseg = int(nseg);
     // Loads in flight: 14, the most the register budget holds (a sweep of every
     // ResNet-50 convolution on MI355X: 1 % faster summed than 8, up to 4 % on the
@@ -668,7 +680,7 @@ struct ds_jit_conv {
     hipModule_t module = nullptr;
     hipFunction_t fn = nullptr;
     Spec sp;
-    int group_tiles = 2;            // per XCD, in 256-pixel tiles
+    int group_tiles = 16;           // in 256-pixel tiles
     int64_t code_bytes = 0;
     int32_t *init = nullptr;        // [k] bias or zeros: y's start for split-K
     int32_t *mul = nullptr, *add = nullptr;
@@ -757,7 +769,7 @@ static ds_status build_plan(const Spec &spec, ds_jit_conv **out)
     }
     p->sp.bias = p->sp.mul = p->sp.add = nullptr;
     p->sp.wp = nullptr;
-    p->group_tiles = std::max(1, env_int("DS_JIT_GROUP_TILES", 2));
+    p->group_tiles = std::max(1, env_int("DS_JIT_GROUP_TILES", 16));
     *out = p;
     return ok();
 }
@@ -954,15 +966,14 @@ static hipError_t run_part(const ds_jit_conv *plan, const int32_t *x, const int3
         a.pw = padded ? 0 : g.pw;
         a.ybase = int(m.base); a.ynst = m.nstride; a.yrst = m.rstride; a.ycst = m.cstride;
         a.tiles_p = sp.tiles_p;
-        a.tiles_x = (sp.tiles_p + 7) / 8;
-        a.group_tiles = std::min(plan->group_tiles * sp.wsplit, a.tiles_x);
+        a.group_tiles = std::min(plan->group_tiles * sp.wsplit, sp.tiles_p);
         a.nseg = sp.nseg;
         a.wsplit_log2 = sp.wsplit == 4 ? 2 : sp.wsplit == 2 ? 1 : 0;
         a.div_ohow = make_fastdiv(uint32_t(a.OHOW));
         a.div_ow = make_fastdiv(uint32_t(a.OW));
         void *args[] = {&a};
         const unsigned lds = sp.wsplit > 1 ? unsigned(4 / sp.wsplit) * 16384u : 0u;
-        e = hipModuleLaunchKernel(plan->fn, unsigned(int64_t(a.tiles_x) * 8 * sp.nseg), 1, 1,
+        e = hipModuleLaunchKernel(plan->fn, unsigned(int64_t(sp.tiles_p) * sp.nseg), 1, 1,
                                   kBlockPixels, 1, 1, lds, st, args, nullptr);
     }
     if (e == hipSuccess && split) {

@@ -17,8 +17,7 @@ struct JitArgs {
     int NQ, OHOW, OW, H, W, C, K, HW, sh, sw, ph, pw;
     int ybase, ynst, yrst, ycst;  // output (n, oh, ow) of channel 0 at y[ybase + n*ynst + oh*yrst + ow*ycst]
     int tiles_p;              // pixel tiles (workgroups) per segment
-    int tiles_x;              // pixel tiles per XCD: ceil(tiles_p / 8)
-    int group_tiles;          // tiles of one XCD that run all segments before its next tiles
+    int group_tiles;          // pixel tiles that run all segments before the next tiles
     int nseg;
     int wsplit_log2;          // waves per 64 pixels: 1, 2 or 4, each a share of the reduction
     FastDiv div_ohow, div_ow;

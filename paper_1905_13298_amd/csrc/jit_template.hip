@@ -43,23 +43,17 @@ extern "C" __global__ void __launch_bounds__(256) ds_jit_conv_template(const Jit
     const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
     const int wl = p.wsplit_log2;
     const int pg = wave >> wl, share = wave & ((1 << wl) - 1);  // pixel group, reduction share
-    // Block order, XCD-aware: workgroups are dealt to the 8 XCDs in turn (block b
-    // to XCD b % 8), and XCD x takes the pixel tiles t with t % 8 == x, so that all
-    // segments of a tile run on one XCD and find the tile's inputs in its L2.
-    // Within an XCD: groups of `group_tiles` of its tiles (the last group may be
-    // smaller); within a group the segments one after the other, and within a
-    // segment the group's tiles, so that the waves running at the same time share
-    // one segment's code while the group's inputs stay in L2. The grid is
-    // 8 * tiles_x * nseg blocks; those past the last tile end at once.
+    // Block order: groups of `group_tiles` pixel tiles (the last group may be
+    // smaller); within a group, the segments one after the other, and within a
+    // segment the group's tiles, so that the waves running at the same time
+    // share one segment's code and the inputs of a few pixel tiles stay in L2
+    // while the segments go by. The grid is exactly tiles_p * nseg blocks.
     const int b = blockIdx.x;
-    const int xcd = b & 7, i = b >> 3;
     const int per_group = p.group_tiles * p.nseg;
-    const int grp = i / per_group, r = i - grp * per_group;
-    const int gsize = min(p.group_tiles, p.tiles_x - grp * p.group_tiles);
-    const int sg = r / gsize;
-    const int tile = (grp * p.group_tiles + (r - sg * gsize)) * 8 + xcd;
-    if (tile >= p.tiles_p) return;
-    const int seg = __builtin_amdgcn_readfirstlane((sg << wl) + share);
+    const int grp = b / per_group, r = b - grp * per_group;
+    const int gsize = min(p.group_tiles, p.tiles_p - grp * p.group_tiles);
+    const int seg = __builtin_amdgcn_readfirstlane(((r / gsize) << wl) + share);
+    const int tile = grp * p.group_tiles + (r - (r / gsize) * gsize);
     const int q = ((tile << (2 - wl)) + pg) * 64 + lane;
     const int lds = pg * 16384 + lane * 4;
     if (wl > 0) {

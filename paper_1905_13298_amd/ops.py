@@ -423,13 +423,14 @@ class JitConv:
     @property
     def preferred(self) -> bool:
         """Whether this plan is expected to beat the runtime kernel. Each code
-        segment is straight-line code that a workgroup streams through the
-        instruction cache once; when only one or two pixel tiles share a segment
-        (a LinearShift at small batch) most of that code comes from HBM with no
-        reuse, and on MI355X such plans ran 2.7-5.4x slower than the runtime
-        kernel once the code passed a few MiB, while plans with 4 or more pixel
-        tiles per segment, or under 4 MiB of code, were faster."""
-        return self.pixel_tiles >= 4 or self.code_bytes <= (4 << 20)
+        segment is straight-line code that a few waves stream through the
+        instruction cache; when only one pixel tile shares a segment (a
+        LinearShift at small batch) most of that code comes from memory with no
+        reuse. On MI355X, plans with 4 or more pixel tiles per segment were
+        faster, and so were small-batch plans up to 16 MiB of code (2048 -> 1000
+        at batch 128, 8 MiB: 62 us against 83 us), but not beyond (4096 -> 4096
+        at batch 256, 71 MiB: 418 us against 362 us)."""
+        return self.pixel_tiles >= 4 or self.code_bytes <= (16 << 20)
 
     def __call__(self, x: torch.Tensor, residual: torch.Tensor | None = None, out=None):
         _dev_i32(x, "x")
