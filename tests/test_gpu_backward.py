@@ -222,6 +222,24 @@ def test_weight_specialised_plans_match_oracle(spec, splits):
     plan.close()
 
 
+def test_stride_phases_fuse_into_one_kernel():
+    """A 3x3 stride-2 layer's four phases become one kernel of 4 x ceil(c/64) output-
+    channel groups (no split); with odd extents (phase grids differ) or a forced split
+    each phase keeps a kernel of its own. Each plan is checked against the oracle."""
+    for (h, splits, segments) in ((16, 0, 4 * 2), (16, 3, 4 * 2 * 3), (15, 0, None)):
+        n, c, k = 2, 70, 33
+        dy, codes, _ = make(1234 + h + splits, n, c, h, h, k, 3, 3, 2, 1)
+        plan = ops.JitConvBackwardData(ops.pack_shift_weights(codes), (n, c, h, h), 3, 2, 1,
+                                       splits=splits)
+        say(f"fuse h={h} splits={splits}: {plan.segments} segments, {plan.splits} parts")
+        if segments is not None:
+            assert plan.segments == segments
+        dx = plan(to_dev(dy)).cpu().numpy()
+        plan.close()
+        want = oracle.conv2d_shift_backward_data(dy, codes, (n, c, h, h), r=3, stride=2, pad=1)
+        np.testing.assert_array_equal(dx, want)
+
+
 def test_weight_specialised_plan_limits_and_arguments():
     codes = np.zeros((16, 1024), np.uint8)      # a phase window 1024 columns wide
     with pytest.raises(ops.DeepShiftError, match="UNSUPPORTED"):
