@@ -190,6 +190,18 @@ fill_init_kernel(const int32_t *__restrict__ init, int32_t *__restrict__ y, int6
         y[idx] = init[(idx / OHOW) % K];
 }
 
+// The same for fewer than 2^31 elements: 32-bit multiply-shift division instead of
+// the 64-bit divide (which made the pass three times slower than its stores).
+__global__ void __launch_bounds__(256)
+fill_init32_kernel(const int32_t *__restrict__ init, int32_t *__restrict__ y, int total,
+                   FastDiv div_ohow, FastDiv div_k)
+{
+    for (int idx = int(blockIdx.x) * 256 + int(threadIdx.x); idx < total; idx += int(gridDim.x) * 256) {
+        const int plane = fdiv(idx, div_ohow);
+        y[idx] = init[plane - fdiv(plane, div_k) * int(div_k.d)];
+    }
+}
+
 // y[map(n, k, oh, ow)] = init[k] (0 without init) over a problem's output grid
 // (fewer than 2^31 elements; flat index split with multiply-shift division).
 __global__ void __launch_bounds__(256)
@@ -836,8 +848,13 @@ hipError_t run_fill_init(const ConvGeom &g, const int32_t *init, int32_t *y, hip
 {
     const int64_t total = int64_t(g.n) * g.k * g.oh * g.ow;
     const int grid = int(std::min<int64_t>((total + 255) / 256, 8192));
-    hipLaunchKernelGGL(fill_init_kernel, dim3(grid), dim3(256), 0, st, init, y, total, g.k,
-                       g.oh * g.ow);
+    if (total <= 0) return hipSuccess;
+    if (total <= INT32_MAX)
+        hipLaunchKernelGGL(fill_init32_kernel, dim3(grid), dim3(256), 0, st, init, y, int(total),
+                           make_fastdiv(uint32_t(g.oh * g.ow)), make_fastdiv(uint32_t(g.k)));
+    else
+        hipLaunchKernelGGL(fill_init_kernel, dim3(grid), dim3(256), 0, st, init, y, total, g.k,
+                           g.oh * g.ow);
     return hipGetLastError();
 }
 
