@@ -172,3 +172,62 @@ def test_plan_is_reusable_and_checks_its_arguments():
         rplan(xd, residual=res, out=res)
     plan.close()
     rplan.close()
+
+
+def test_plans_replay_in_a_captured_graph():
+    """Plans allocate nothing and launch only kernels when run (the padding, fill
+    and epilogue passes included), so a stream capture of several plans replays:
+    three replays, with the outputs overwritten eagerly between them, each equal
+    to the eager result, itself equal to the oracle."""
+    rng = np.random.default_rng(77)
+    cases = [  # n, c, h, w, k, r, s, stride, pad, splits: padded 5x5, wave split, split-K
+        (2, 3, 15, 13, 40, 5, 5, 2, 2, 0),
+        (2, 40, 9, 9, 70, 3, 3, 1, 1, 0),
+        (3, 300, 6, 6, 9, 1, 1, 1, 0, 3),
+    ]
+    runs, wants = [], []
+    for (n, c, h, w, k, r, s, st, pd, sp) in cases:
+        codes = random_codes_like(rng, k, c * r * s)
+        x = rng.integers(-(2 ** 31), 2 ** 31, (n, c, h, w), dtype=np.int64).astype(np.int32)
+        bias = rng.integers(-(2 ** 31), 2 ** 31, k, dtype=np.int64).astype(np.int32)
+        plan = ops.JitConv(ops.pack_shift_weights(codes), x.shape, (r, s), st, pd, bias=bias,
+                           splits=sp)
+        xd = to_dev(x)
+        y = torch.empty(plan.y_shape, dtype=torch.int32, device=DEV)
+        runs.append((plan, xd, y))
+        wants.append(oracle.conv2d_shift(x, codes, bias, r=r, s=s, stride=st, pad=pd))
+    for plan, xd, y in runs:
+        plan(xd, out=y)
+    torch.cuda.synchronize()
+    for (_, _, y), want in zip(runs, wants):
+        np.testing.assert_array_equal(y.cpu().numpy(), want)
+    graph = torch.cuda.CUDAGraph()
+    side = torch.cuda.Stream()
+    side.wait_stream(torch.cuda.current_stream())
+    with torch.cuda.stream(side):
+        for plan, xd, y in runs:
+            plan(xd, out=y)
+    torch.cuda.current_stream().wait_stream(side)
+    torch.cuda.synchronize()
+    with torch.cuda.graph(graph, capture_error_mode="thread_local"):
+        for plan, xd, y in runs:
+            plan(xd, out=y)
+    for rep in range(3):
+        for _, _, y in runs:
+            y.fill_(0x5A5A5A5A)
+        torch.cuda.synchronize()
+        graph.replay()
+        torch.cuda.synchronize()
+        for (_, _, y), want in zip(runs, wants):
+            np.testing.assert_array_equal(y.cpu().numpy(), want, err_msg=f"replay {rep}")
+    say("graph of 3 plans: 3 replays equal the oracle")
+    del graph
+    for plan, _, _ in runs:
+        plan.close()
+
+
+def random_codes_like(rng, k, cols, zero_frac=0.2):
+    sign = rng.integers(0, 2, (k, cols))
+    shift = rng.integers(0, 15, (k, cols))
+    shift[rng.random((k, cols)) < zero_frac] = 15
+    return (sign << 4 | shift).astype(np.uint8)
