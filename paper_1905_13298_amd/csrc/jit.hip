@@ -14,12 +14,19 @@
 //
 // Code layout. A plan is one code object: the template kernel built with the
 // library (jit_template.hip), whose last loadable segment `.jitbody` is
-// replaced by the generated code: a table of `nseg` jump stubs, then one block
-// of straight-line code per segment (64 output channels x a range of input
-// channels). The template computes the lane's tap and output offsets and jumps
-// through the table; each segment ends the wave. Segments are spliced into
-// the template image in memory (no assembler or linker runs at plan time) and
-// the result is loaded with hipModuleLoadData.
+// replaced by the generated code: a table of jump stubs, then one block of
+// straight-line code per segment (64 output channels x a range of reduction
+// elements; with a wave split, one per share of that range). The template
+// computes the lane's tap and output offsets and jumps through the table; each
+// segment ends the wave. Segments are spliced into the template image in
+// memory (no assembler or linker runs at plan time) and the result is loaded
+// with hipModuleLoadData.
+//
+// Variants of the same code: windows over 3 x 3 read a zero-padded copy of x
+// (uniform tap offsets); small grids split each 64 pixels' reduction over 2 or
+// 4 waves that meet in LDS, and long reductions over segments that meet in y
+// through atomics; the stride phases of an input gradient run as output-channel
+// groups of one problem (fuse_phases).
 #include <hip/hip_runtime.h>
 
 #include <elf.h>
