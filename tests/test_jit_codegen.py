@@ -293,8 +293,46 @@ CASES = [
 def test_generated_code_matches_oracle(case, tmp_path, monkeypatch):
     n, c, h, w, k, r, s, st, pd, splits, epi = case[:11]
     wsplit = case[11] if len(case) > 11 else 1
+    run_generated(case[:11] + (wsplit,), zlib.crc32(str(case).encode()), 0.1, tmp_path, monkeypatch)
+
+
+def random_cases(count, seed=1905):
+    """Seeded random shapes: windows 1-5 (over 3 x 3: padded copies), strides 1-3,
+    padding 0-2, ragged channel counts, forced splits and wave splits, every
+    epilogue, weight sparsity from none to 95 % (whole elements without a
+    non-zero weight, which are skipped)."""
+    rng = np.random.default_rng(seed)
+    out = []
+    while len(out) < count:
+        n, c, k = int(rng.integers(1, 4)), int(rng.integers(1, 80)), int(rng.integers(1, 150))
+        r, s = int(rng.integers(1, 6)), int(rng.integers(1, 6))
+        st, pd = int(rng.integers(1, 4)), int(rng.integers(0, 3))
+        h, w = int(rng.integers(max(1, r - 2 * pd), 12)), int(rng.integers(max(1, s - 2 * pd), 12))
+        if h + 2 * pd < r or w + 2 * pd < s:
+            continue
+        splits = int(rng.choice([1, 2, 3]))
+        wsplit = int(rng.choice([1, 2, 4]))
+        epi = str(rng.choice(["none", "relu", "mul", "full"]))
+        zero = float(rng.choice([0.0, 0.1, 0.5, 0.95]))
+        out.append(((n, c, h, w, k, r, s, st, pd, splits, epi, wsplit), zero))
+    return out
+
+
+RANDOM = random_cases(20)
+
+
+@pytest.mark.parametrize("case,zero", RANDOM, ids=[str(i) for i in range(len(RANDOM))])
+def test_generated_code_matches_oracle_random_shapes(case, zero, tmp_path, monkeypatch):
+    run_generated(case, zlib.crc32(repr((case, zero)).encode()), zero, tmp_path, monkeypatch)
+
+
+def run_generated(case, seed, zero_frac, tmp_path, monkeypatch):
+    """Generate a plan's code object for `case` (n, c, h, w, k, r, s, stride, pad,
+    splits, epilogue, wave split), run it in the interpreter over every lane, and
+    compare with the oracle."""
+    n, c, h, w, k, r, s, st, pd, splits, epi, wsplit = case
     monkeypatch.setenv("DS_JIT_WSPLIT", str(wsplit))
-    codes, x, rng = gen_layer(zlib.crc32(str(case).encode()), n, c, h, w, k, r, s)
+    codes, x, rng = gen_layer(seed, n, c, h, w, k, r, s, zero_frac)
     bias = rng.integers(-(2 ** 31), 2 ** 31, k, dtype=np.int64).astype(np.int32)
     mul = add = res = None
     relu = epi in ("full", "relu")
