@@ -285,3 +285,39 @@ def test_resnet50_full_batch_plans_equal_runtime_kernel():
         assert diff == 0, f"{L.name}: {diff} elements differ"
         plan.close()
         del got, ref, dy
+
+
+def _random_layers(count, seed):
+    rng = np.random.default_rng(seed)
+    out = []
+    while len(out) < count:
+        n, c, k = int(rng.integers(1, 4)), int(rng.integers(1, 150)), int(rng.integers(1, 150))
+        r, s = int(rng.integers(1, 8)), int(rng.integers(1, 8))
+        st, pd = int(rng.integers(1, 4)), int(rng.integers(0, 4))
+        h, w = int(rng.integers(1, 26)), int(rng.integers(1, 26))
+        if h + 2 * pd < r or w + 2 * pd < s:
+            continue
+        out.append((n, c, h, w, k, r, s, st, pd))
+    return out
+
+
+RANDOM_LAYERS = _random_layers(16, 1356)
+
+
+@pytest.mark.parametrize("spec", RANDOM_LAYERS, ids=[str(i) for i in range(len(RANDOM_LAYERS))])
+def test_random_shapes_both_paths_match_oracle(spec):
+    """Seeded random shapes: the runtime gradient and the plan (fused phases where
+    the phase grids agree, windows over 3 x 3 through padded copies) against the
+    oracle."""
+    n, c, h, w, k, r, s, st, pd = spec
+    dy, codes, _ = make(zlib.crc32(repr(spec).encode()), n, c, h, w, k, r, s, st, pd)
+    want = oracle.conv2d_shift_backward_data(dy, codes, (n, c, h, w), r=r, s=s, stride=st, pad=pd)
+    wph = ops.pack_shift_weights(codes)
+    dx = ops.conv2d_shift_backward_data(to_dev(dy), to_dev(wph.view(np.int32)), (n, c, h, w), (r, s),
+                                        st, pd).cpu().numpy()
+    np.testing.assert_array_equal(dx, want, err_msg="runtime")
+    plan = ops.JitConvBackwardData(wph, (n, c, h, w), (r, s), st, pd)
+    say(f"backward random {spec}: {plan.segments} segments, {plan.splits} parts")
+    dxp = plan(to_dev(dy)).cpu().numpy()
+    plan.close()
+    np.testing.assert_array_equal(dxp, want, err_msg="plan")

@@ -231,3 +231,35 @@ def random_codes_like(rng, k, cols, zero_frac=0.2):
     shift = rng.integers(0, 15, (k, cols))
     shift[rng.random((k, cols)) < zero_frac] = 15
     return (sign << 4 | shift).astype(np.uint8)
+
+
+def _random_layers(count, seed):
+    rng = np.random.default_rng(seed)
+    out = []
+    while len(out) < count:
+        n, c, k = int(rng.integers(1, 5)), int(rng.integers(1, 200)), int(rng.integers(1, 200))
+        r, s = int(rng.integers(1, 8)), int(rng.integers(1, 8))
+        st, pd = int(rng.integers(1, 4)), int(rng.integers(0, 4))
+        h, w = int(rng.integers(1, 30)), int(rng.integers(1, 30))
+        if h + 2 * pd < r or w + 2 * pd < s:
+            continue
+        out.append((n, c, h, w, k, r, s, st, pd))
+    return out
+
+
+RANDOM_LAYERS = _random_layers(16, 355)
+
+
+@pytest.mark.parametrize("spec", RANDOM_LAYERS, ids=[str(i) for i in range(len(RANDOM_LAYERS))])
+def test_random_shapes_match_oracle(spec):
+    """Seeded random shapes (windows up to 7 x 7, strides up to 3, padding up to 3)
+    with the planner's own choices of wave split and split-K."""
+    n, c, h, w, k, r, s, st, pd = spec
+    codes, x, bias, _ = rand_case(zlib.crc32(repr(spec).encode()), n, c, h, w, k, r, s)
+    plan = ops.JitConv(ops.pack_shift_weights(codes), x.shape, (r, s), st, pd, bias=bias)
+    say(f"jit random {spec}: {plan.splits} parts, {plan.segments} segments")
+    y = plan(to_dev(x)).cpu().numpy()
+    plan.close()
+    want = oracle.conv2d_shift(x, codes, bias, r=r, s=s, stride=st, pad=pd)
+    bad = np.flatnonzero(y.ravel() != want.ravel())
+    assert bad.size == 0, f"{bad.size} of {want.size} outputs differ, first at {bad[:5]}"
