@@ -20,6 +20,7 @@ struct JitArgs {
     int group_tiles;          // pixel tiles that run all segments before the next tiles
     int nseg;
     int wsplit_log2;          // waves per 64 pixels: 1, 2 or 4, each a share of the reduction
+    int tile_major;           // block order: all segments of a tile, then the next tile
     FastDiv div_ohow, div_ow;
 };
 

@@ -45,15 +45,24 @@ extern "C" __global__ void __launch_bounds__(256) ds_jit_conv_template(const Jit
     const int pg = wave >> wl, share = wave & ((1 << wl) - 1);  // pixel group, reduction share
     // Block order: groups of `group_tiles` pixel tiles (the last group may be
     // smaller); within a group, the segments one after the other, and within a
-    // segment the group's tiles, so that the waves running at the same time
-    // share one segment's code and the inputs of a few pixel tiles stay in L2
-    // while the segments go by. The grid is exactly tiles_p * nseg blocks.
+    // segment the group's tiles, so that the inputs of a few pixel tiles stay in
+    // L2 while the segments go by. Tile-major (small grids): all segments of a
+    // tile, then the next tile, so that the blocks resident on one CU (block b
+    // and b + 256 k at the start) run the same segment's code. The grid is
+    // exactly tiles_p * nseg blocks.
     const int b = blockIdx.x;
-    const int per_group = p.group_tiles * p.nseg;
-    const int grp = b / per_group, r = b - grp * per_group;
-    const int gsize = min(p.group_tiles, p.tiles_p - grp * p.group_tiles);
-    const int seg = __builtin_amdgcn_readfirstlane(((r / gsize) << wl) + share);
-    const int tile = grp * p.group_tiles + (r - (r / gsize) * gsize);
+    int sg, tile;
+    if (p.tile_major) {
+        tile = b / p.nseg;
+        sg = b - tile * p.nseg;
+    } else {
+        const int per_group = p.group_tiles * p.nseg;
+        const int grp = b / per_group, r = b - grp * per_group;
+        const int gsize = min(p.group_tiles, p.tiles_p - grp * p.group_tiles);
+        sg = r / gsize;
+        tile = grp * p.group_tiles + (r - sg * gsize);
+    }
+    const int seg = __builtin_amdgcn_readfirstlane((sg << wl) + share);
     const int q = ((tile << (2 - wl)) + pg) * 64 + lane;
     const int lds = pg * 16384 + lane * 4;
     if (wl > 0) {
