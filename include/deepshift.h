@@ -359,7 +359,8 @@ ds_status ds_conv2d_shift_describe(int64_t n, int64_t c, int64_t h, int64_t w, i
  * loads in flight, tile grouping) or run (block order); for measurements only:
  * DS_JIT_WSPLIT (1, 2 or 4 waves per 64 pixels), DS_JIT_SLOTS (1-14 loads in
  * flight), DS_JIT_GROUP_TILES (tiles per group), DS_JIT_ORDER (0 grouped, 1
- * tile-major). The results do not depend on them. */
+ * tile-major, 2 tile-major with each tile's workgroups on one XCD). The results
+ * do not depend on them. */
 typedef struct ds_jit_conv ds_jit_conv;
 
 ds_status ds_jit_conv_create(const uint32_t *w_packed, const int32_t *bias, const int32_t *mul,

@@ -173,7 +173,7 @@ struct Spec {
     std::vector<int> kjn;
     // Block order (see the template): all segments of one pixel tile after the
     // other, instead of groups of tiles passing through the segments one by one.
-    bool tile_major = false;
+    int tile_major = 0;         // 0 grouped, 1 tile-major, 2 XCD-local tile-major
 };
 
 // Element strides of the output map of a spec (the dense layout when unset).
@@ -532,10 +532,17 @@ ds_status finish_spec(Spec &sp, int bits, int splits, int deep_blocks = 3072)
     // cheap for small inputs only. A sweep of ResNet-50 at N = 128: its 14 x 14 and
     // 7 x 7 layers ran 1-12 % faster, while its 56 x 56 stride-2 1 x 1 layer (a
     // 411 MB input) ran 1.34x slower.
+    // A strided 1 x 1 layer (little code, an input read at scattered pixels) takes
+    // the XCD-local variant, which keeps each tile on one XCD: 4 % faster on
+    // ResNet-50's 1024 -> 2048 stride-2 layer at 14 x 14, 13-25 % on ResNet-18's
+    // three (N = 32). Layers with more code per input ran 5-25 % slower in it:
+    // every XCD's L2 then holds every segment's code.
     {
         const int64_t tiles256 = (nq + kBlockPixels - 1) / kBlockPixels;
         const int64_t xin = sp.xh > 0 ? prod({g.n, g.c, sp.xh, sp.xw}) : prod({g.n, g.c, g.h, g.w});
-        sp.tile_major = tiles256 <= 100 && xin * 4 <= (int64_t(128) << 20);
+        const bool strided_point = int64_t(g.r) * g.s == 1 && (g.sh > 1 || g.sw > 1);
+        const bool small = tiles256 <= 100 && xin * 4 <= (int64_t(128) << 20);
+        sp.tile_major = small ? (strided_point ? 2 : 1) : 0;
     }
     // Loads in flight: 14, the most the register budget holds (a sweep of every
     // ResNet-50 convolution on MI355X: 1 % faster summed than 8, up to 4 % on the
@@ -993,7 +1000,7 @@ static hipError_t run_part(const ds_jit_conv *plan, const int32_t *x, const int3
         a.nseg = sp.nseg;
         a.wsplit_log2 = sp.wsplit == 4 ? 2 : sp.wsplit == 2 ? 1 : 0;
         const int order = env_int("DS_JIT_ORDER", -1);
-        a.tile_major = order < 0 ? sp.tile_major : order == 1;
+        a.tile_major = order < 0 ? sp.tile_major : order >= 0 && order <= 2 ? order : 0;
         a.div_ohow = make_fastdiv(uint32_t(a.OHOW));
         a.div_ow = make_fastdiv(uint32_t(a.OW));
         void *args[] = {&a};

@@ -52,7 +52,17 @@ extern "C" __global__ void __launch_bounds__(256) ds_jit_conv_template(const Jit
     // exactly tiles_p * nseg blocks.
     const int b = blockIdx.x;
     int sg, tile;
-    if (p.tile_major) {
+    if (p.tile_major == 2 && b < (p.tiles_p >> 3) * 8 * p.nseg) {
+        // XCD-local tile-major: workgroups are dealt to the 8 XCDs in turn
+        // (block b to XCD b % 8), so whole rows of 8 tiles map tile 8 i + x to
+        // XCD x: every segment of a tile then runs on one XCD and reads the
+        // tile's input through that XCD's L2 only. The tiles of the last,
+        // partial row (the rest of the grid) take the plain tile-major order.
+        const int j = b >> 3;
+        const int row = j / p.nseg;
+        sg = j - row * p.nseg;
+        tile = row * 8 + (b & 7);
+    } else if (p.tile_major) {
         tile = b / p.nseg;
         sg = b - tile * p.nseg;
     } else {

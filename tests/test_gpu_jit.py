@@ -5,7 +5,8 @@ inputs: edge shapes (ragged channels, pixels and output channels; strides,
 padding, rectangular windows; LinearShift as 1 x 1 on 1 x 1 images), each with
 the reduction whole, split automatically and split by force (the split-K path
 adds partial sums atomically and runs the epilogue as a pass of its own); the
-fused epilogue (affine map, residual, ReLU) against the oracle's; the single-
+fused epilogue (affine map, residual, ReLU) against the oracle's; every block
+order of the grid; the single-
 layer workloads in full; and every ResNet-50 convolution (the 7 x 7 stem through
 a padded copy of x) at batch 128 in full against the production kernel, plus
 sampled outputs against the oracle.
@@ -245,6 +246,35 @@ def _random_layers(count, seed):
             continue
         out.append((n, c, h, w, k, r, s, st, pd))
     return out
+
+
+ORDER_CASES = [
+    # pixel tiles not a multiple of 8 (a partial last row of tiles), fewer than 8,
+    # and a strided 1 x 1 layer
+    ("ragged_rows", 2, 40, 28, 29, 130, 3, 3, 1, 1),
+    ("point_s2", 4, 64, 30, 30, 96, 1, 1, 2, 0),
+    ("many_tiles", 8, 32, 20, 20, 64, 3, 3, 1, 1),
+    ("few_tiles", 1, 24, 9, 9, 200, 3, 3, 1, 1),
+]
+
+
+@pytest.mark.parametrize("spec", ORDER_CASES, ids=[e[0] for e in ORDER_CASES])
+def test_block_orders_match_oracle(spec, monkeypatch):
+    """Every block order (grouped, tile-major, tile-major with a tile's workgroups
+    on one XCD) maps the grid onto all (tile, segment) pairs once: each gives the
+    oracle's output."""
+    _, n, c, h, w, k, r, s, st, pd = spec
+    codes, x, bias, _ = rand_case(zlib.crc32(repr(spec).encode()), n, c, h, w, k, r, s)
+    want = oracle.conv2d_shift(x, codes, bias, r=r, s=s, stride=st, pad=pd)
+    plan = ops.JitConv(ops.pack_shift_weights(codes), x.shape, (r, s), st, pd, bias=bias)
+    xd = to_dev(x)
+    for order in (0, 1, 2):
+        monkeypatch.setenv("DS_JIT_ORDER", str(order))
+        say(f"jit order {order} {spec[0]}: {plan.segments} segments, {plan.pixel_tiles} tiles")
+        y = plan(xd).cpu().numpy()
+        bad = np.flatnonzero(y.ravel() != want.ravel())
+        assert bad.size == 0, f"order {order}: {bad.size} of {want.size} outputs differ, first at {bad[:5]}"
+    plan.close()
 
 
 RANDOM_LAYERS = _random_layers(16, 355)
