@@ -108,8 +108,16 @@ def parse():
 
 
 CSRC = os.path.join(ROOT, "paper_1905_13298_amd", "csrc")
-# The generated weight-specialised kernel (one name for every plan).
+# The generated weight-specialised kernel: one code object per plan with two
+# entry points (up to 3 x 3 taps per element, 96 VGPRs; one tap, 80 VGPRs),
+# accounted together under the first one's name.
 JIT_KERNEL = "ds_jit_conv_template"
+JIT_ENTRY_POINTS = ("ds_jit_conv_template", "ds_jit_conv_one_tap_template")
+
+
+def is_jit_kernel(name: str) -> bool:
+    return any(e in name for e in JIT_ENTRY_POINTS)
+
 # Per kernel family: the sources its code comes from, and the committed HBM
 # traffic record of its counters on the ResNet-50 workload.
 FAMILIES = {
@@ -141,7 +149,7 @@ def _pmc_rows(directory: str):
     return [rows[k] for k in sorted(rows)]
 
 
-MAIN_KERNELS = ("tiled_kernel", "conv_direct_kernel", "ds_jit_conv_template")
+MAIN_KERNELS = ("tiled_kernel", "conv_direct_kernel") + JIT_ENTRY_POINTS
 
 
 def _main_rows(rows, layers):
@@ -163,7 +171,7 @@ def pmc_summary(copy_fetch, copy_write, fetch, write, copy_bytes, workload, path
     w_rows = _main_rows(_pmc_rows(write), layers)
     per_kernel = {}
     for L, fr, wr in zip(layers, f_rows, w_rows):
-        name = group_name(L, path, JIT_KERNEL in fr["name"])
+        name = group_name(L, path, is_jit_kernel(fr["name"]))
         k = per_kernel.setdefault(name, {"launches": 0, "fetch_bytes": 0.0, "write_bytes": 0.0,
                                           "algorithmic_bytes": 0})
         k["launches"] += 1
@@ -193,7 +201,7 @@ def sq_summary(directory, workload, path):
     per = {}
     for li, (L, r) in enumerate(zip(layers, rows)):
         codes = W.gen_codes(L, W.CONFIG_SEEDS[cfg], li)
-        name = group_name(L, path, JIT_KERNEL in r["name"])
+        name = group_name(L, path, is_jit_kernel(r["name"]))
         k = per.setdefault(name, {"launches": 0, "sac": 0, "nz": 0.0, "ns": 0})
         k["launches"] += 1
         k["sac"] += L.sac
@@ -400,6 +408,7 @@ def bench_network(args):
         roofline = {"bound": "alu", "achieved": round(achieved, 4), "peak": round(VOP2_OPS_PEAK_T, 4),
                     "unit": "T int32 ops/s", "frac": round(achieved / VOP2_OPS_PEAK_T, 4), **common,
                     "work_unit": "one int32 VOP2 add/sub per non-zero weight term",
+                    "entry_points": list(JIT_ENTRY_POINTS),
                     "kernel": "weight-specialised convolutions with fused epilogue",
                     "timed_span": "library call per layer"}
     else:
@@ -528,6 +537,7 @@ def bench_backward(args):
         roofline = {"bound": "alu", "achieved": round(nz, 4), "peak": round(VOP2_OPS_PEAK_T, 4),
                     "unit": "T int32 ops/s", "frac": round(nz / VOP2_OPS_PEAK_T, 4), **common,
                     "work_unit": "one int32 VOP2 add/sub per non-zero weight term",
+                    "entry_points": list(JIT_ENTRY_POINTS),
                     "dense_tsac_s": round(g["sac"] / (g["ms"] * 1e-3) / 1e12, 4),
                     "timed_span": "library call per layer (zero fills, the phases' generated kernels)"}
     else:
@@ -702,6 +712,7 @@ def roofline_of(layers, d, path, nonzero, planned=None):
         return {"bound": "alu", "achieved": round(nz, 4), "peak": round(VOP2_OPS_PEAK_T, 4),
                 "unit": "T int32 ops/s", "frac": round(nz / VOP2_OPS_PEAK_T, 4), **common,
                 "work_unit": "one int32 VOP2 add/sub per non-zero weight term",
+                "entry_points": list(JIT_ENTRY_POINTS),
                 "nonzero_sac_per_launch_avg": int(g["nz"] // g["launches"]),
                 "dense_tsac_s": round(dense, 4),
                 "timed_span": "library call per launch (split-K fill pass + generated kernel)"}

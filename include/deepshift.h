@@ -356,11 +356,13 @@ ds_status ds_conv2d_shift_describe(int64_t n, int64_t c, int64_t h, int64_t w, i
  * the number of parts the reduction is split into. Any output may be NULL.
  *
  * Tuning overrides, read from the environment when a plan is made (wave split,
- * loads in flight, tile grouping) or run (block order); for measurements only:
- * DS_JIT_WSPLIT (1, 2 or 4 waves per 64 pixels), DS_JIT_SLOTS (1-14 loads in
- * flight), DS_JIT_GROUP_TILES (tiles per group), DS_JIT_ORDER (0 grouped, 1
- * tile-major, 2 tile-major with each tile's workgroups on one XCD). The results
- * do not depend on them. */
+ * loads in flight, register map, tile grouping) or run (block order); for
+ * measurements only: DS_JIT_WSPLIT (1, 2 or 4 waves per 64 pixels),
+ * DS_JIT_SLOTS (loads in flight: 1-14, at most 8 in the 80-register code of
+ * layers with one tap per element), DS_JIT_MAP (96: the 96-register code for
+ * those layers too), DS_JIT_GROUP_TILES (tiles per group), DS_JIT_ORDER (0
+ * grouped, 1 tile-major, 2 tile-major with each tile's workgroups on one XCD).
+ * The results do not depend on them. */
 typedef struct ds_jit_conv ds_jit_conv;
 
 ds_status ds_jit_conv_create(const uint32_t *w_packed, const int32_t *bias, const int32_t *mul,

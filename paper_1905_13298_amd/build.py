@@ -29,9 +29,10 @@ CXX_SOURCES = ["pack.cpp"]
 LLVM = "/opt/rocm/llvm/bin"
 
 # The weight-specialised kernel template (jit_template.hip) is compiled to
-# gfx950 assembly; its JITBODY marker becomes a jump through a table at the
-# start of section .jitbody, indexed by the segment number in s19 (stubs of 20
-# bytes each). The table and the segments' code are generated at run time.
+# gfx950 assembly; the JITBODY marker of each of its two kernels becomes a jump
+# through a table at the start of section .jitbody, indexed by the segment
+# number in s19 (stubs of 20 bytes each). The table and the segments' code are
+# generated at run time.
 JIT_JUMP = """s_getpc_b64 s[28:29]
 	s_add_u32 s28, s28, ds_jit_body@rel32@lo+4
 	s_addc_u32 s29, s29, ds_jit_body@rel32@hi+12
@@ -76,8 +77,8 @@ def _jit_template() -> str:
     _run([HIPCC, *HIP_FLAGS, "--cuda-device-only", "-S", src, "-o", asm])
     text = open(asm).read()
     marker = "; JITBODY"
-    if text.count(marker) != 1:
-        raise RuntimeError("jit_template.s: expected one JITBODY marker")
+    if text.count(marker) != 2:
+        raise RuntimeError("jit_template.s: expected a JITBODY marker in each of its two kernels")
     text = text.replace(marker, JIT_JUMP) + JIT_BODY_SECTION
     spliced = os.path.join(OBJDIR, "jit_template_spliced.s")
     with open(spliced, "w") as f:

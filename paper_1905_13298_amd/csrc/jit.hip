@@ -48,16 +48,23 @@ extern "C" const unsigned char ds_jit_template_image_end[];
 namespace ds {
 namespace {
 
-// Register contract with the template (see the JITBODY marker there).
-constexpr int kLds = 3;      // v3: the lane's LDS byte offset (wave split)
-constexpr int kTap0 = 4;     // v4..v12: byte offset in x of tap (r, s) = v[4 + 3r + s], channel 0
-constexpr int kYoff = 13;    // v13: byte offset in y of the lane's output pixel, channel 0
-constexpr int kTmpLo = 14, kTmpHi = 15;
-constexpr int kTab = 16;     // v16, v17: x >> s, alternately (x itself stays in its load slot)
-constexpr int kAcc = 18;     // v18..v81: accumulators of the segment's 64 output channels
-constexpr int kSlot = 82;    // v82..: loads in flight (at most 14: v82..v95)
-constexpr int kMaxSlots = 14;
-// v0..v95 in all: 96 VGPRs leave room for 5 waves per SIMD.
+// Register contract with the template (see the JITBODY marker there), one map
+// per entry point. Up to 3 x 3 taps per element: v3 the lane's LDS byte offset
+// (wave split), v4..v12 the byte offset in x of tap (r, s) = v[4 + 3r + s] at
+// channel 0, v13 the byte offset in y of the lane's output pixel at channel 0,
+// v14, v15 the multiplier's temporaries, v16, v17 x >> s alternately (x itself
+// stays in its load slot), v18..v81 the accumulators of the segment's 64
+// output channels, v82..v95 up to 14 loads in flight: 96 VGPRs, 5 waves per
+// SIMD. One tap per element (1 x 1 windows, or the tap column as an offset in
+// the instruction): v4 the tap, v5..v12 up to 8 loads in flight (the
+// multiplier's temporaries share them, free by then), v14, v15 the shifted
+// values, v16..v79 the accumulators: 80 VGPRs, 6 waves per SIMD.
+struct RegMap {
+    int lds, tap0, yoff, tmp_lo, tmp_hi, tab, acc, slot, max_slots;
+    const char *kernel;
+};
+constexpr RegMap kMap96 = {3, 4, 13, 14, 15, 16, 18, 82, 14, "ds_jit_conv_template"};
+constexpr RegMap kMap80 = {3, 4, 13, 5, 6, 14, 16, 5, 8, "ds_jit_conv_one_tap_template"};
 constexpr int kXrsrc = 20, kYrsrc = 24, kRrsrc = 36;  // buffer resources (SGPR quads)
 constexpr int kSy = 28, kSx = 29, kSmul = 30;         // scalar scratch of the generated code
 constexpr int kTN = 64;      // output channels per segment
@@ -174,6 +181,7 @@ struct Spec {
     // Block order (see the template): all segments of one pixel tile after the
     // other, instead of groups of tiles passing through the segments one by one.
     int tile_major = 0;         // 0 grouped, 1 tile-major, 2 XCD-local tile-major
+    bool one_tap = false;       // the 80-VGPR entry point (one tap register)
 };
 
 // Element strides of the output map of a spec (the dense layout when unset).
@@ -226,15 +234,16 @@ void emit_segment(Emitter &e, const Spec &sp, int kg, int e0, int e1, int share,
             }
     const int E = int(el.size());
 
+    const RegMap &m = sp.one_tap ? kMap80 : kMap96;
     for (int j = 0; j < jn; ++j)
-        e.mov_imm(kAcc + j, (!split && sp.bias && share == 0) ? sp.bias[kbase + j] : 0);
+        e.mov_imm(m.acc + j, (!split && sp.bias && share == 0) ? sp.bias[kbase + j] : 0);
 
-    // Listed element n's load goes to slot n % kSlots and reads x at v[tap] + s29,
+    // Listed element n's load goes to slot n % nslots and reads x at v[tap] + s29,
     // where s29 = c * H * W * 4 for the channel of the most recently issued load.
     // From a padded copy: at v4 + s29 + 4 s, where s29 = (c * xh * xw + r * xw) * 4
     // for the channel and tap row of that load.
-    const int kSlots = sp.slots;
-    const int D = std::min(kSlots, E);
+    const int nslots = sp.slots;
+    const int D = std::min(nslots, E);
     uint32_t cur = uint32_t(e0 / RS) * cstride;
     e.s_mov_imm(kSx, cur);
     auto issue = [&](int n) {
@@ -245,18 +254,18 @@ void emit_segment(Emitter &e, const Spec &sp, int kg, int e0, int e1, int share,
             e.s_add_imm(kSx, soff - cur);  // modulo 2^32
             cur = soff;
         }
-        const int slot = kSlot + n % kSlots;
+        const int slot = m.slot + n % nslots;
         if (padded)
-            e.mubuf(kLoad, slot, kTap0, kXrsrc, kSx, uint32_t(ts) * 4u);
+            e.mubuf(kLoad, slot, m.tap0, kXrsrc, kSx, uint32_t(ts) * 4u);
         else
-            e.mubuf(kLoad, slot, kTap0 + tr * 3 + ts, kXrsrc, kSx);
+            e.mubuf(kLoad, slot, m.tap0 + tr * 3 + ts, kXrsrc, kSx);
     };
     for (int n = 0; n < D; ++n) issue(n);
 
     for (int i = 0; i < E; ++i) {
         const int issued = std::min(E, i + D);
         e.wait_vm(issued - i - 1);
-        const int slot = kSlot + i % kSlots;
+        const int slot = m.slot + i % nslots;
         const int jw = el[size_t(i)];  // column of the element in the packed rows
         // The element's non-zero weights grouped by shift; each shift is formed
         // once, into one of two registers in turn, right before the adds that use it.
@@ -270,15 +279,15 @@ void emit_segment(Emitter &e, const Spec &sp, int kg, int e0, int e1, int share,
             if (count[sh] == 0) continue;
             int src = slot;
             if (sh > 0) {
-                src = kTab + (formed++ & 1);
+                src = m.tab + (formed++ & 1);
                 e.vop2(kOpAshr, src, Emitter::inline_int(sh), slot);
             }
             for (int q = 0; q < count[sh]; ++q) {
                 const int v = by_shift[sh][q];
                 if (v < 0)
-                    e.vop2(kOpSub, kAcc - 1 - v, Emitter::vgpr(kAcc - 1 - v), src);  // acc - term
+                    e.vop2(kOpSub, m.acc - 1 - v, Emitter::vgpr(m.acc - 1 - v), src);  // acc - term
                 else
-                    e.vop2(kOpAdd, kAcc + v, Emitter::vgpr(src), kAcc + v);          // term + acc
+                    e.vop2(kOpAdd, m.acc + v, Emitter::vgpr(src), m.acc + v);          // term + acc
             }
         }
         if (i + D < E) issue(i + D);
@@ -287,12 +296,12 @@ void emit_segment(Emitter &e, const Spec &sp, int kg, int e0, int e1, int share,
     // The channels this wave finishes: all, or its share of them after the LDS sum.
     int j0 = 0, j1 = jn;
     if (sp.wsplit > 1) {
-        for (int j = 0; j < jn; ++j) e.ds_add(kLds, kAcc + j, uint32_t(j) * 256u);
+        for (int j = 0; j < jn; ++j) e.ds_add(m.lds, m.acc + j, uint32_t(j) * 256u);
         e.wait_lgkm0();
         e.w.push_back(kBarrier);
         j0 = std::min(jn, share * kTN / sp.wsplit);
         j1 = std::min(jn, (share + 1) * kTN / sp.wsplit);
-        for (int j = j0; j < j1; ++j) e.ds_read(kAcc + j, kLds, uint32_t(j) * 256u);
+        for (int j = j0; j < j1; ++j) e.ds_read(m.acc + j, m.lds, uint32_t(j) * 256u);
         e.wait_lgkm0();
     }
     if (!split) {
@@ -301,33 +310,33 @@ void emit_segment(Emitter &e, const Spec &sp, int kg, int e0, int e1, int share,
                 // floor(acc * mul / 2^mul_shift): the low word of the 64-bit product
                 // shifted right, taken from its two halves.
                 e.s_mov_imm(kSmul, uint32_t(sp.mul[kbase + j]));
-                e.vop3(kOpMulLo, kTmpLo, uint32_t(kSmul), Emitter::vgpr(kAcc + j), 0);
-                e.vop3(kOpMulHi, kTmpHi, uint32_t(kSmul), Emitter::vgpr(kAcc + j), 0);
-                e.vop3(kOpAlignbit, kAcc + j, Emitter::vgpr(kTmpHi), Emitter::vgpr(kTmpLo),
+                e.vop3(kOpMulLo, m.tmp_lo, uint32_t(kSmul), Emitter::vgpr(m.acc + j), 0);
+                e.vop3(kOpMulHi, m.tmp_hi, uint32_t(kSmul), Emitter::vgpr(m.acc + j), 0);
+                e.vop3(kOpAlignbit, m.acc + j, Emitter::vgpr(m.tmp_hi), Emitter::vgpr(m.tmp_lo),
                        Emitter::inline_int(sp.mul_shift));
                 const int32_t a = sp.add ? sp.add[kbase + j] : 0;
-                if (a != 0) e.vop2_imm(kOpAdd, kAcc + j, a, kAcc + j);
+                if (a != 0) e.vop2_imm(kOpAdd, m.acc + j, a, m.acc + j);
             }
         }
         if (sp.residual) {
-            for (int jb = j0; jb < j1; jb += kSlots) {
-                const int nb = std::min(kSlots, j1 - jb);
+            for (int jb = j0; jb < j1; jb += nslots) {
+                const int nb = std::min(nslots, j1 - jb);
                 e.s_mov_imm(kSy, out0 + uint32_t(jb) * kstride);
                 for (int b = 0; b < nb; ++b) {
-                    e.mubuf(kLoad, kSlot + b, kYoff, kRrsrc, kSy);
+                    e.mubuf(kLoad, m.slot + b, m.yoff, kRrsrc, kSy);
                     if (b + 1 < nb) e.s_add_imm(kSy, kstride);
                 }
                 e.wait_vm(0);
                 for (int b = 0; b < nb; ++b)
-                    e.vop2(kOpAdd, kAcc + jb + b, Emitter::vgpr(kSlot + b), kAcc + jb + b);
+                    e.vop2(kOpAdd, m.acc + jb + b, Emitter::vgpr(m.slot + b), m.acc + jb + b);
             }
         }
         if (sp.relu)
-            for (int j = j0; j < j1; ++j) e.vop2(kOpMax, kAcc + j, Emitter::inline_int(0), kAcc + j);
+            for (int j = j0; j < j1; ++j) e.vop2(kOpMax, m.acc + j, Emitter::inline_int(0), m.acc + j);
     }
     e.s_mov_imm(kSy, out0 + uint32_t(j0) * kstride);
     for (int j = j0; j < j1; ++j) {
-        e.mubuf(split ? kAtomicAdd : kStore, kAcc + j, kYoff, kYrsrc, kSy);
+        e.mubuf(split ? kAtomicAdd : kStore, m.acc + j, m.yoff, kYrsrc, kSy);
         if (j + 1 < j1) e.s_add_imm(kSy, kstride);
     }
     e.w.push_back(kEndpgm);
@@ -546,8 +555,14 @@ ds_status finish_spec(Spec &sp, int bits, int splits, int deep_blocks = 3072)
     }
     // Loads in flight: 14, the most the register budget holds (a sweep of every
     // ResNet-50 convolution on MI355X: 1 % faster summed than 8, up to 4 % on the
-    // largest pixel grids).
-    sp.slots = std::min(kMaxSlots, std::max(1, env_int("DS_JIT_SLOTS", kMaxSlots)));
+    // largest pixel grids). One tap per element (1 x 1 windows, or wider ones
+    // through the padded copy): the 80-VGPR entry point, 6 waves per SIMD with 8
+    // loads in flight; ResNet-50's 37 such layers (N = 128) ran 2.8 % faster
+    // summed than with 96 VGPRs (8 or 14 loads in flight alike), ResNet-18's four
+    // 3.6 %.
+    sp.one_tap = (int64_t(g.r) * g.s == 1 || sp.xh > 0) && env_int("DS_JIT_MAP", 0) != 96;
+    const RegMap &m = sp.one_tap ? kMap80 : kMap96;
+    sp.slots = std::min(m.max_slots, std::max(1, env_int("DS_JIT_SLOTS", m.max_slots)));
     return ok();
 }
 
@@ -773,7 +788,8 @@ static ds_status build_plan(const Spec &spec, ds_jit_conv **out)
         return fail(DS_ERR_HIP, "no HIP device");
     }
     hipError_t e = hipModuleLoadData(&p->module, img.data());
-    if (e == hipSuccess) e = hipModuleGetFunction(&p->fn, p->module, "ds_jit_conv_template");
+    if (e == hipSuccess)
+        e = hipModuleGetFunction(&p->fn, p->module, (p->sp.one_tap ? kMap80 : kMap96).kernel);
     if (e != hipSuccess) {
         destroy_plan(p);
         return fail(DS_ERR_HIP, "loading the generated code: %s", hipGetErrorString(e));

@@ -18,7 +18,12 @@
 // generated machine words; each segment ends the wave itself. Register use of
 // the generated code (the clobbers below): v14..v95 (v16, v17 the shifted
 // values, v18..v81 the accumulators, v82..v95 the loads in flight), s28..s31;
-// 96 VGPRs in all, so that 5 waves fit on a SIMD.
+// 96 VGPRs in all, so that 5 waves fit on a SIMD. Layers that read x at one
+// tap per element (1 x 1 windows, and wider windows through a zero-padded copy
+// of x, where the tap is an offset in the instruction) run the second entry
+// point, which hands over only the first tap: v5..v12 hold 8 loads in flight,
+// v14, v15 the shifted values and v16..v79 the accumulators; 80 VGPRs, 6
+// waves per SIMD.
 //
 // A workgroup is 4 waves. Without a wave split each wave covers 64 pixels of a
 // 256-pixel tile with the whole reduction of its segment. With a split of 2 or
@@ -36,7 +41,8 @@
 
 using ds::JitArgs;
 
-extern "C" __global__ void __launch_bounds__(256) ds_jit_conv_template(const JitArgs p)
+template <bool kOneTap>
+__device__ __forceinline__ void jit_conv(const JitArgs &p)
 {
     extern __shared__ int32_t red[];  // wave split: [4 >> wsplit_log2][64 channels][64 lanes]
     const int lane = threadIdx.x & 63;
@@ -97,9 +103,12 @@ extern "C" __global__ void __launch_bounds__(256) ds_jit_conv_template(const Jit
             const int ih = ih0 + rr, iw = iw0 + ss;
             return (ih >= 0 && ih < p.H && iw >= 0 && iw < p.W) ? (base + ih * p.W + iw) * 4 : kOOB;
         };
-        t0 = off(0, 0); t1 = off(0, 1); t2 = off(0, 2);
-        t3 = off(1, 0); t4 = off(1, 1); t5 = off(1, 2);
-        t6 = off(2, 0); t7 = off(2, 1); t8 = off(2, 2);
+        t0 = off(0, 0);
+        if (!kOneTap) {
+            t1 = off(0, 1); t2 = off(0, 2);
+            t3 = off(1, 0); t4 = off(1, 1); t5 = off(1, 2);
+            t6 = off(2, 0); t7 = off(2, 1); t8 = off(2, 2);
+        }
     }
     const __amdgpu_buffer_rsrc_t xr = __builtin_amdgcn_make_buffer_rsrc(
         const_cast<int32_t *>(p.x), short(0), p.x_bytes, 0x00020000);
@@ -107,17 +116,44 @@ extern "C" __global__ void __launch_bounds__(256) ds_jit_conv_template(const Jit
                                                                         0x00020000);
     const __amdgpu_buffer_rsrc_t rr = __builtin_amdgcn_make_buffer_rsrc(
         const_cast<int32_t *>(p.residual), short(0), p.residual ? p.y_bytes : 0, 0x00020000);
-    asm volatile("; JITBODY"
-                 :
-                 : "{s[20:23]}"(xr), "{s[24:27]}"(yr), "{s[36:39]}"(rr), "{s19}"(seg), "{v3}"(lds),
-                   "{v4}"(t0), "{v5}"(t1), "{v6}"(t2), "{v7}"(t3), "{v8}"(t4), "{v9}"(t5),
-                   "{v10}"(t6), "{v11}"(t7), "{v12}"(t8), "{v13}"(yoff)
-                 : "memory", "v14", "v15", "v16", "v17", "v18", "v19", "v20", "v21", "v22", "v23",
-                   "v24", "v25", "v26", "v27", "v28", "v29", "v30", "v31", "v32", "v33", "v34",
-                   "v35", "v36", "v37", "v38", "v39", "v40", "v41", "v42", "v43", "v44", "v45",
-                   "v46", "v47", "v48", "v49", "v50", "v51", "v52", "v53", "v54", "v55", "v56",
-                   "v57", "v58", "v59", "v60", "v61", "v62", "v63", "v64", "v65", "v66", "v67",
-                   "v68", "v69", "v70", "v71", "v72", "v73", "v74", "v75", "v76", "v77", "v78",
-                   "v79", "v80", "v81", "v82", "v83", "v84", "v85", "v86", "v87", "v88", "v89",
-                   "v90", "v91", "v92", "v93", "v94", "v95", "s28", "s29", "s30", "s31");
+    if constexpr (kOneTap) {
+        asm volatile("; JITBODY"
+                     :
+                     : "{s[20:23]}"(xr), "{s[24:27]}"(yr), "{s[36:39]}"(rr), "{s19}"(seg), "{v3}"(lds),
+                       "{v4}"(t0), "{v13}"(yoff)
+                     : "memory", "v5", "v6", "v7", "v8", "v9", "v10", "v11", "v12", "v14", "v15",
+                       "v16", "v17", "v18", "v19", "v20", "v21", "v22", "v23", "v24", "v25", "v26",
+                       "v27", "v28", "v29", "v30", "v31", "v32", "v33", "v34", "v35", "v36", "v37",
+                       "v38", "v39", "v40", "v41", "v42", "v43", "v44", "v45", "v46", "v47", "v48",
+                       "v49", "v50", "v51", "v52", "v53", "v54", "v55", "v56", "v57", "v58", "v59",
+                       "v60", "v61", "v62", "v63", "v64", "v65", "v66", "v67", "v68", "v69", "v70",
+                       "v71", "v72", "v73", "v74", "v75", "v76", "v77", "v78", "v79", "s28", "s29",
+                       "s30", "s31");
+    } else {
+        asm volatile("; JITBODY"
+                     :
+                     : "{s[20:23]}"(xr), "{s[24:27]}"(yr), "{s[36:39]}"(rr), "{s19}"(seg), "{v3}"(lds),
+                       "{v4}"(t0), "{v5}"(t1), "{v6}"(t2), "{v7}"(t3), "{v8}"(t4), "{v9}"(t5),
+                       "{v10}"(t6), "{v11}"(t7), "{v12}"(t8), "{v13}"(yoff)
+                     : "memory", "v14", "v15", "v16", "v17", "v18", "v19", "v20", "v21", "v22", "v23",
+                       "v24", "v25", "v26", "v27", "v28", "v29", "v30", "v31", "v32", "v33", "v34",
+                       "v35", "v36", "v37", "v38", "v39", "v40", "v41", "v42", "v43", "v44", "v45",
+                       "v46", "v47", "v48", "v49", "v50", "v51", "v52", "v53", "v54", "v55", "v56",
+                       "v57", "v58", "v59", "v60", "v61", "v62", "v63", "v64", "v65", "v66", "v67",
+                       "v68", "v69", "v70", "v71", "v72", "v73", "v74", "v75", "v76", "v77", "v78",
+                       "v79", "v80", "v81", "v82", "v83", "v84", "v85", "v86", "v87", "v88", "v89",
+                       "v90", "v91", "v92", "v93", "v94", "v95", "s28", "s29", "s30", "s31");
+    }
+}
+
+// Layers with up to 3 x 3 taps per element: 96 VGPRs, 5 waves per SIMD.
+extern "C" __global__ void __launch_bounds__(256) ds_jit_conv_template(const JitArgs p)
+{
+    jit_conv<false>(p);
+}
+
+// Layers with one tap per element: 80 VGPRs, 6 waves per SIMD.
+extern "C" __global__ void __launch_bounds__(256) ds_jit_conv_one_tap_template(const JitArgs p)
+{
+    jit_conv<true>(p);
 }
