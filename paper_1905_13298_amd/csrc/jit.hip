@@ -485,21 +485,21 @@ ds_status finish_spec(Spec &sp, int bits, int splits, int deep_blocks = 3072)
     sp.one_tap = (int64_t(g.r) * g.s == 1 || sp.xh > 0) && env_int("DS_JIT_MAP", 0) != 96;
     // Wave split (2 or 4 waves per 64 pixels, each with a share of the reduction,
     // meeting in LDS): more waves without atomics on grids under 2048 workgroups
-    // of 256 pixels (at most 2 from 1024 up), each share keeping 128 reduction
-    // elements (32 on grids under 256 workgroups, where parallelism decides). A
-    // strided 1 x 1 layer, whose loads already span twice the cache lines, splits
-    // at most in 2. Other one-tap layers split in 4 down to shares of 64 at any
-    // grid under 2048 workgroups: with 80 VGPRs a CU holds 6 workgroups of 16 KiB
-    // of LDS (a split of 4) but only 5 of 32 KiB (a split of 2). On MI355X this
-    // ran ResNet-50's 256 -> 64 layers at 56 x 56, 512 -> 256 at 28 x 28 and
-    // 256 -> 1024 at 14 x 14 (N = 128) 5-10 % faster than a split of 2.
+    // of 256 pixels, each share keeping 128 reduction elements (32 on grids under
+    // 256 workgroups, where parallelism decides). A strided 1 x 1 layer, whose
+    // loads already span twice the cache lines, splits at most in 2; other
+    // one-tap layers keep shares of 64: with 80 VGPRs a CU holds 6 workgroups of
+    // 16 KiB of LDS (a split of 4) but only 5 of 32 KiB (a split of 2). In a
+    // randomized A/B on MI355X a split of 4 against 2 ran ResNet-50's (N = 128)
+    // 256 -> 64 layers at 56 x 56, 512 -> 256 at 28 x 28 and 256 -> 1024 at
+    // 14 x 14 5-10 % faster, its 3 x 3 layers at 56 x 56 5 % faster.
     const int64_t base = (nq + kBlockPixels - 1) / kBlockPixels * sp.kgroups;
     {
         const bool thin = base < 256;
         const bool strided_point = int64_t(g.r) * g.s == 1 && (g.sh > 1 || g.sw > 1);
         const bool wide = sp.one_tap && !strided_point;
         const int64_t min_share = thin ? 32 : wide ? 64 : 128;
-        const int cap = (strided_point && !thin) || (base >= 1024 && !wide) ? 2 : 4;
+        const int cap = strided_point && !thin ? 2 : 4;
         int ws = 1;
         if (base < 2048)
             while (ws < cap && g.crs / (2 * ws) >= min_share) ws *= 2;
