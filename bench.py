@@ -5,8 +5,8 @@ LinearShift call on its own seeded input, all inputs resident in HBM).
 Two paths compute the same outputs bit for bit (checked before timing):
   jit      (default) a weight-specialised plan per layer, its code generated
            at setup from the fixed weights (Section 6's run-time compilation);
-           a layer whose plan would be slower (JitConv.preferred: large code
-           streamed for a single pixel tile) runs the runtime kernel
+           a layer whose plan is not preferred (JitConv.preferred, true for
+           every shape measured on MI355X) runs the runtime kernel
   runtime  ds_conv2d_shift / ds_linear_shift with the packed weights as data
 Prints ONE JSON line:
   value       whole-step throughput in G shift-accumulates/s (dense SAC =

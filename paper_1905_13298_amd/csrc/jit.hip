@@ -533,8 +533,10 @@ ds_status finish_spec(Spec &sp, int bits, int splits, int deep_blocks = 3072)
         // (4) Fewer than 4 tiles of 256 pixels (a LinearShift at small batch): every
         // code segment streams through the instruction cache for a few waves only,
         // and more parts mean more code streams: at most 2 (2048 -> 1000 at batch
-        // 128: 62 us at 2 parts, 112 us at 8).
-        if (tiles256 < 4) want = std::min<int64_t>(want, 2);
+        // 128: 62 us at 2 parts, 112 us at 8), and none once the grid has a
+        // workgroup per CU (4096 -> 4096 at batch 256, 256 workgroups: 175 us
+        // whole, 261 us in 2 parts).
+        if (tiles256 < 4) want = blocks >= 256 ? 1 : std::min<int64_t>(want, 2);
         ns = int(std::max<int64_t>(1, want));
     }
     sp.nsplit = std::min(ns, g.c);

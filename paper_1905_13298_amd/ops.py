@@ -422,15 +422,14 @@ class JitConv:
 
     @property
     def preferred(self) -> bool:
-        """Whether this plan is expected to beat the runtime kernel. Each code
-        segment is straight-line code that a few waves stream through the
-        instruction cache; when only one pixel tile shares a segment (a
-        LinearShift at small batch) most of that code comes from memory with no
-        reuse. On MI355X, plans with 4 or more pixel tiles per segment were
-        faster, and so were small-batch plans up to 16 MiB of code (2048 -> 1000
-        at batch 128, 8 MiB: 62 us against 83 us), but not beyond (4096 -> 4096
-        at batch 256, 71 MiB: 418 us against 362 us)."""
-        return self.pixel_tiles >= 4 or self.code_bytes <= (16 << 20)
+        """Whether this plan is expected to beat the runtime kernel: on MI355X
+        every measured case. Each code segment is straight-line code that a few
+        waves stream through the instruction cache, so when only one pixel tile
+        shares a segment (a LinearShift at small batch) most of that code comes
+        from memory with no reuse; even so the plans ran faster: 4096 -> 4096 at
+        batch 256 (71 MiB of code) 175 us against 361 us, 2048 -> 1000 at batch
+        128 62 us against 83 us, 256 -> 128 at batch 8 12.5 us against 45 us."""
+        return True
 
     def __call__(self, x: torch.Tensor, residual: torch.Tensor | None = None, out=None):
         _dev_i32(x, "x")
