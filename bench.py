@@ -752,10 +752,7 @@ def bench_layers(args):
         plan = None
         if args.path == "jit" and jit_supported(L):
             tp = time.time()
-            if L.kind == "linear":
-                plan = ops.JitConv(wp, (L.n, L.c, 1, 1), 1, 1, 0, bias=bias)
-            else:
-                plan = ops.JitConv(wp, L.x_shape, (L.r, L.s), L.stride, L.pad, bias=bias)
+            plan = ops.layer_plan(L, wp, bias)
             plan_s += time.time() - tp
             if not plan.preferred:
                 plan.close()
@@ -773,10 +770,7 @@ def bench_layers(args):
     def jit_call(plan, L, xt, wt, bt, yt):
         if plan is None:
             return runtime_call(L, xt, wt, bt, yt)
-        if L.kind == "linear":
-            x4, y4 = xt.view(L.n, L.c, 1, 1), yt.view(L.n, L.k, 1, 1)
-            return lambda: plan(x4, out=y4)
-        return lambda: plan(xt, out=yt)
+        return lambda: ops.run_layer_plan(plan, L, xt, out=yt)
 
     runtime_calls = [runtime_call(*r) for r in res]
     sac_step = sum(L.sac for L in layers)

@@ -34,9 +34,16 @@
  *
  * Ownership and memory: the caller owns every buffer. Compute entry points
  * take device pointers on the current HIP device; the pack/unpack helpers
- * take host pointers. y must not overlap any input. The compute entry points
- * allocate device scratch memory (decoded weights) in stream order from a
- * library-owned memory pool and free it in stream order.
+ * take host pointers. y must not overlap any input. The runtime-weights
+ * entry points (ds_linear_shift, ds_conv2d_shift and their variants) take
+ * device scratch memory (decoded weights, per-channel start values, transposed
+ * operands) in stream order from the device's default memory pool
+ * (hipMallocAsync) and give it back in stream order (hipFreeAsync) within the
+ * same call: the library keeps no pool and no device memory between calls.
+ * Under the runtime's default release threshold the memory returns to the
+ * driver at the caller's next synchronisation. Callers that cannot allocate
+ * use ds_conv2d_shift_noalloc (below). Plans (ds_jit_conv_*) hold the device
+ * memory they need from create to destroy.
  *
  * Errors: arguments are validated before any device work. On a validation
  * error nothing is written and nothing is launched. Compute entry points are
@@ -355,7 +362,7 @@ ds_status ds_conv2d_shift_describe(int64_t n, int64_t c, int64_t h, int64_t w, i
  * segments (64 output channels x one part of the input channels each), and
  * the number of parts the reduction is split into. Any output may be NULL.
  *
- * Tuning overrides, read from the environment when a plan is made (wave split,
+ * Tuning overrides (ds_set_tuning, below) used when a plan is made (wave split,
  * loads in flight, register map, tile grouping) or run (block order); for
  * measurements only: DS_JIT_WSPLIT (1, 2 or 4 waves per 64 pixels),
  * DS_JIT_SLOTS (loads in flight: 1-14, at most 8 in the 80-register code of
@@ -399,6 +406,19 @@ ds_status ds_jit_conv_backward_data_create(const uint32_t *w_packed, int64_t n, 
                                            int32_t stride_h, int32_t stride_w, int32_t pad_h,
                                            int32_t pad_w, uint32_t flags, int32_t splits,
                                            ds_jit_conv **plan);
+
+/* Tuning overrides, for tests and measurements: they change which kernel
+ * variant, wave split, block order or load depth the library uses, never a
+ * result. Knobs: "DS_FORCE_VARIANT" (0: the one-thread-per-output kernel for
+ * ds_conv2d_shift and the input gradients; 8: the tiled kernel with 8 pixels
+ * per lane where one exists) and the plan knobs listed with ds_jit_conv_create.
+ * Each starts from the environment variable of the same name, read once when
+ * the library is loaded (unset: -1, the library's own choice); no entry point
+ * reads the environment afterwards. value < 0 resets a knob to -1. Errors:
+ * NULL pointer, unknown name (DS_ERR_INVALID_ARG). Thread-safe; a change is
+ * seen by calls and plans made after it. */
+ds_status ds_set_tuning(const char *name, int32_t value);
+ds_status ds_get_tuning(const char *name, int32_t *value);
 
 /* Static text for a status code. */
 const char *ds_status_string(ds_status status);

@@ -25,7 +25,7 @@ HIP_FLAGS = ["-O3", "-std=c++17", f"--offload-arch={ARCH}", "-fPIC", "-Wall",
 CXX_FLAGS = ["-O2", "-std=c++17", "-fPIC", "-Wall", "-Wextra", "-I", INCLUDE, "-I", CSRC]
 
 HIP_SOURCES = ["shift_ops.hip", "conv_kernels.hip", "convert.hip", "pool.hip", "jit.hip", "backward.hip"]
-CXX_SOURCES = ["pack.cpp"]
+CXX_SOURCES = ["pack.cpp", "tuning.cpp"]
 LLVM = "/opt/rocm/llvm/bin"
 
 # The weight-specialised kernel template (jit_template.hip) is compiled to

@@ -30,50 +30,27 @@
 #include <algorithm>
 #include <cstdio>
 #include <cstdlib>
-#include <mutex>
 #include <type_traits>
 
 #include "conv_plan.hpp"
 #include "fastdiv.hpp"
+#include "tuning.hpp"
 
 namespace ds {
 
-int forced_variant()
-{
-    const char *e = std::getenv("DS_FORCE_VARIANT");  // read per call: tests switch it
-    if (!e || !*e) return -1;
-    return std::atoi(e);
-}
+int forced_variant() { return tuning(kForceVariant); }
 
 // ---------------------------------------------------------------------------
-// Scratch memory: stream-ordered allocations from one pool per device that
-// keeps freed memory for reuse.
+// Scratch memory: stream-ordered allocations from the device's default memory
+// pool (hipMallocAsync), freed in stream order (hipFreeAsync) once the call's
+// kernels are enqueued. The library keeps no pool and no allocation of its own:
+// with the runtime's default release threshold of the default pool, freed
+// scratch goes back to the driver at the caller's next synchronisation, and
+// calls enqueued back to back reuse it in the meantime.
 
 hipError_t scratch_alloc(void **p, size_t bytes, hipStream_t st)
 {
-    static std::mutex mu;
-    static hipMemPool_t pools[64] = {};
-    int dev = 0;
-    hipError_t e = hipGetDevice(&dev);
-    if (e != hipSuccess) return e;
-    if (dev < 0 || dev >= 64) return hipErrorInvalidDevice;
-    {
-        std::lock_guard<std::mutex> lock(mu);
-        if (!pools[dev]) {
-            hipMemPoolProps props = {};
-            props.allocType = hipMemAllocationTypePinned;
-            props.location.type = hipMemLocationTypeDevice;
-            props.location.id = dev;
-            hipMemPool_t pool;
-            e = hipMemPoolCreate(&pool, &props);
-            if (e != hipSuccess) return e;
-            uint64_t keep = UINT64_MAX;
-            e = hipMemPoolSetAttribute(pool, hipMemPoolAttrReleaseThreshold, &keep);
-            if (e != hipSuccess) return e;
-            pools[dev] = pool;
-        }
-    }
-    return hipMallocFromPoolAsync(p, bytes, pools[dev], st);
+    return hipMallocAsync(p, bytes, st);
 }
 
 // ---------------------------------------------------------------------------

@@ -105,10 +105,10 @@ hipError_t run_pad_planes(const int32_t *x, int32_t *xp, int64_t planes, int h, 
 // Short name of the kernel run_conv would launch for g (see ds_conv2d_shift_describe).
 void describe_conv(const ConvGeom &g, char *buf, size_t len);
 
-// Kernel variant forced for testing and tuning, from the environment variable
-// DS_FORCE_VARIANT (read at every call): unset or -1 = automatic choice, 0 = the
-// one-thread-per-output kernel, 8 = tiled kernels with 8 pixels per lane
-// where an instance exists (the default is 4).
+// Kernel variant forced for testing and tuning (the DS_FORCE_VARIANT knob of
+// tuning.hpp): -1 = automatic choice, 0 = the one-thread-per-output kernel,
+// 8 = tiled kernels with 8 pixels per lane where an instance exists (the
+// default is 4).
 int forced_variant();
 
 }  // namespace ds

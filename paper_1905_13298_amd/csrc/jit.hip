@@ -40,6 +40,7 @@
 #include "common.hpp"
 #include "conv_plan.hpp"
 #include "jit.hpp"
+#include "tuning.hpp"
 
 // The template code object, embedded by the build (see build.py).
 extern "C" const unsigned char ds_jit_template_image[];
@@ -441,12 +442,6 @@ ds_status splice_body(const std::vector<uint32_t> &body, std::vector<uint8_t> &o
     return ok();
 }
 
-int env_int(const char *name, int dflt)
-{
-    const char *v = std::getenv(name);
-    return v && *v ? std::atoi(v) : dflt;
-}
-
 struct CreateArgs {
     const uint32_t *wp;
     const int32_t *bias, *mul, *add;
@@ -482,7 +477,7 @@ ds_status finish_spec(Spec &sp, int bits, int splits, int deep_blocks = 3072)
     sp.kgroups = (g.k + kTN - 1) / kTN;
     // One tap per element (1 x 1 windows, or wider ones through the padded copy):
     // the 80-VGPR entry point, 6 waves per SIMD instead of 5.
-    sp.one_tap = (int64_t(g.r) * g.s == 1 || sp.xh > 0) && env_int("DS_JIT_MAP", 0) != 96;
+    sp.one_tap = (int64_t(g.r) * g.s == 1 || sp.xh > 0) && tuning(kJitMap) != 96;
     // Wave split (2 or 4 waves per 64 pixels, each with a share of the reduction,
     // meeting in LDS): more waves without atomics on grids under 2048 workgroups
     // of 256 pixels, each share keeping 128 reduction elements (32 on grids under
@@ -503,7 +498,7 @@ ds_status finish_spec(Spec &sp, int bits, int splits, int deep_blocks = 3072)
         int ws = 1;
         if (base < 2048)
             while (ws < cap && g.crs / (2 * ws) >= min_share) ws *= 2;
-        const int forced = env_int("DS_JIT_WSPLIT", 0);
+        const int forced = tuning(kJitWsplit);
         sp.wsplit = forced == 1 || forced == 2 || forced == 4 ? forced : ws;
     }
     const int tile_pixels = kBlockPixels / sp.wsplit;
@@ -571,7 +566,8 @@ ds_status finish_spec(Spec &sp, int bits, int splits, int deep_blocks = 3072)
     // summed than with 96 VGPRs (8 or 14 loads in flight alike), ResNet-18's four
     // 3.6 %.
     const RegMap &m = sp.one_tap ? kMap80 : kMap96;
-    sp.slots = std::min(m.max_slots, std::max(1, env_int("DS_JIT_SLOTS", m.max_slots)));
+    const int slots = tuning(kJitSlots);
+    sp.slots = std::min(m.max_slots, std::max(1, slots < 0 ? m.max_slots : slots));
     return ok();
 }
 
@@ -824,7 +820,7 @@ static ds_status build_plan(const Spec &spec, ds_jit_conv **out)
     }
     p->sp.bias = p->sp.mul = p->sp.add = nullptr;
     p->sp.wp = nullptr;
-    p->group_tiles = std::max(1, env_int("DS_JIT_GROUP_TILES", 16));
+    p->group_tiles = tuning(kJitGroupTiles) > 0 ? tuning(kJitGroupTiles) : 16;
     *out = p;
     return ok();
 }
@@ -1024,7 +1020,7 @@ static hipError_t run_part(const ds_jit_conv *plan, const int32_t *x, const int3
         a.group_tiles = std::min(plan->group_tiles * sp.wsplit, sp.tiles_p);
         a.nseg = sp.nseg;
         a.wsplit_log2 = sp.wsplit == 4 ? 2 : sp.wsplit == 2 ? 1 : 0;
-        const int order = env_int("DS_JIT_ORDER", -1);
+        const int order = tuning(kJitOrder);
         a.tile_major = order < 0 ? sp.tile_major : order >= 0 && order <= 2 ? order : 0;
         a.div_ohow = make_fastdiv(uint32_t(a.OHOW));
         a.div_ow = make_fastdiv(uint32_t(a.OW));

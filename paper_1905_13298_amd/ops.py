@@ -18,7 +18,8 @@ __all__ = ["DeepShiftError", "code_bits_flag", "describe_conv2d", "packed_row_wo
            "quantize_shift_weights_q", "quantize_shift_weights_q_many", "quantize_shift_weights_ps",
            "to_fixed_point", "conv2d_shift_fused", "maxpool2d", "avgpool2d_global", "DS_RELU",
            "DS_JIT_RESIDUAL", "JitConv", "jit_conv_image", "conv2d_shift_backward_data",
-           "linear_shift_backward_data", "describe_conv2d_backward_data", "JitConvBackwardData"]
+           "linear_shift_backward_data", "describe_conv2d_backward_data", "JitConvBackwardData",
+           "layer_plan", "run_layer_plan", "set_tuning", "get_tuning", "tuning"]
 
 DS_RELU = 1
 
@@ -481,3 +482,53 @@ class JitConvBackwardData(JitConv):
         call("ds_jit_conv_query", self._h, ctypes.byref(cb), ctypes.byref(seg), ctypes.byref(sp))
         self.code_bytes, self.segments, self.splits = cb.value, seg.value, sp.value
         self.pixel_tiles = -(-(n * h * w) // 256)
+
+
+def layer_plan(layer, w_packed, bias=None, device="cuda:0") -> JitConv:
+    """The weight-specialised plan of one workload layer (an object with ``kind``
+    "conv" or "linear", ``n, c, h, w, k, r, s, stride, pad``), made the way the
+    benchmark makes it: a LinearShift [batch, in] -> [batch, out] is the 1 x 1
+    ConvShift of [batch, in, 1, 1]. ``w_packed``: host packed codes [k, words]."""
+    if layer.kind == "linear":
+        return JitConv(w_packed, (layer.n, layer.c, 1, 1), 1, 1, 0, bias=bias, device=device)
+    return JitConv(w_packed, (layer.n, layer.c, layer.h, layer.w), (layer.r, layer.s), layer.stride,
+                   layer.pad, bias=bias, device=device)
+
+
+def run_layer_plan(plan: JitConv, layer, x: torch.Tensor, out: torch.Tensor | None = None) -> torch.Tensor:
+    """Runs a plan of ``layer_plan`` on the layer's own input layout ([batch, in] for a
+    LinearShift) and returns y in the layer's output layout."""
+    if layer.kind == "linear":
+        y4 = plan(x.view(layer.n, layer.c, 1, 1), out=None if out is None else out.view(layer.n, layer.k, 1, 1))
+        return y4.view(layer.n, layer.k)
+    return plan(x, out=out)
+
+
+def set_tuning(name: str, value: int) -> None:
+    """Sets a tuning override of the library (``ds_set_tuning``): "DS_FORCE_VARIANT",
+    "DS_JIT_WSPLIT", "DS_JIT_SLOTS", "DS_JIT_MAP", "DS_JIT_GROUP_TILES" or
+    "DS_JIT_ORDER"; a negative value restores the library's own choice."""
+    call("ds_set_tuning", name.encode(), int(value))
+
+
+def get_tuning(name: str) -> int:
+    v = ctypes.c_int32()
+    call("ds_get_tuning", name.encode(), ctypes.byref(v))
+    return v.value
+
+
+class tuning:
+    """Context manager: ``with ops.tuning("DS_FORCE_VARIANT", 0): ...`` sets a tuning
+    override for the block and restores the previous value afterwards."""
+
+    def __init__(self, name: str, value: int):
+        self.name, self.value = name, value
+
+    def __enter__(self):
+        self.prev = get_tuning(self.name)
+        set_tuning(self.name, self.value)
+        return self
+
+    def __exit__(self, *exc):
+        set_tuning(self.name, self.prev)
+        return False

@@ -289,3 +289,36 @@ def test_backward_describe_plans_phases_without_a_gpu():
     assert d(1, 3, 6, 6, 2, 1, 1, 1) == "direct"               # padding beyond the window
     with pytest.raises(ops.DeepShiftError, match="INVALID_SHAPE"):
         d(1, 1, 2, 2, 1, 3, 1, 0)
+
+
+def test_tuning_overrides_are_explicit():
+    """Tuning knobs start from the environment at load and change only through
+    ds_set_tuning; unknown names and NULL pointers are rejected."""
+    from paper_1905_13298_amd import ops
+    lib = _native.lib()
+    before = ops.get_tuning("DS_JIT_ORDER")
+    try:
+        ops.set_tuning("DS_JIT_ORDER", 2)
+        assert ops.get_tuning("DS_JIT_ORDER") == 2
+        with ops.tuning("DS_JIT_ORDER", 1):
+            assert ops.get_tuning("DS_JIT_ORDER") == 1
+        assert ops.get_tuning("DS_JIT_ORDER") == 2
+        ops.set_tuning("DS_JIT_ORDER", -7)
+        assert ops.get_tuning("DS_JIT_ORDER") == -1
+    finally:
+        ops.set_tuning("DS_JIT_ORDER", before)
+    assert lib.ds_set_tuning(b"DS_NO_SUCH_KNOB", 1) == 3
+    assert lib.ds_set_tuning(None, 1) == 1
+    assert lib.ds_get_tuning(b"DS_JIT_SLOTS", None) == 1
+    # The environment is not read again after load.
+    import os
+    loaded = ops.get_tuning("DS_JIT_WSPLIT")
+    old = os.environ.get("DS_JIT_WSPLIT")
+    os.environ["DS_JIT_WSPLIT"] = "4" if loaded != 4 else "2"
+    try:
+        assert ops.get_tuning("DS_JIT_WSPLIT") == loaded
+    finally:
+        if old is None:
+            del os.environ["DS_JIT_WSPLIT"]
+        else:
+            os.environ["DS_JIT_WSPLIT"] = old

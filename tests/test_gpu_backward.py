@@ -77,10 +77,10 @@ def make(seed, n, c, h, w, k, r, s, st, pd, lim=2 ** 31):
 
 @pytest.mark.parametrize("direct", [False, True], ids=["auto", "gather"])
 @pytest.mark.parametrize("spec", EDGE, ids=[e[0] for e in EDGE])
-def test_edge_shapes_match_oracle(spec, direct, monkeypatch):
+def test_edge_shapes_match_oracle(spec, direct, knob):
     name, n, c, h, w, k, r, s, st, pd = spec
     if direct:
-        monkeypatch.setenv("DS_FORCE_VARIANT", "0")
+        knob("DS_FORCE_VARIANT", 0)
     rr = r if np.isscalar(r) else r[0]
     ss = s if np.isscalar(s) else s[1]
     dy, codes, _ = make(zlib.crc32(name.encode()), n, c, h, w, k, rr, ss, st, pd)
@@ -168,7 +168,7 @@ def test_errors_write_nothing():
     assert torch.all(dx == 7)
 
 
-def test_resnet50_full_batch_against_gather_kernel_and_oracle(monkeypatch):
+def test_resnet50_full_batch_against_gather_kernel_and_oracle(knob):
     """Every ResNet-50 convolution at batch 128 (the stem aside: an input gradient of
     the images is not needed): all elements equal the gather kernel's, 400 sampled
     elements per layer equal the oracle's."""
@@ -185,9 +185,9 @@ def test_resnet50_full_batch_against_gather_kernel_and_oracle(monkeypatch):
         x_shape = L.x_shape
         say(f"backward resnet50 {L.name}: {ops.describe_conv2d_backward_data(*x_shape, L.k, (L.r, L.s), L.stride, L.pad)}")
         dx = ops.conv2d_shift_backward_data(dyd, wp, x_shape, (L.r, L.s), L.stride, L.pad)
-        monkeypatch.setenv("DS_FORCE_VARIANT", "0")
+        knob("DS_FORCE_VARIANT", 0)
         ref = ops.conv2d_shift_backward_data(dyd, wp, x_shape, (L.r, L.s), L.stride, L.pad)
-        monkeypatch.delenv("DS_FORCE_VARIANT")
+        knob("DS_FORCE_VARIANT", -1)
         diff = int((dx != ref).sum())
         assert diff == 0, f"{L.name}: {diff} elements differ from the gather kernel"
         total = int(np.prod(x_shape))

@@ -40,9 +40,9 @@ CONV = [(2, 13, 9, 11, 37, 3, 1, 1), (3, 20, 15, 15, 33, 1, 2, 0), (1, 300, 6, 6
 
 @pytest.mark.parametrize("bits", BITS)
 @pytest.mark.parametrize("direct", [False, True], ids=["tiled", "direct"])
-def test_conv_matches_oracle(bits, direct, monkeypatch):
+def test_conv_matches_oracle(bits, direct, knob):
     if direct:
-        monkeypatch.setenv("DS_FORCE_VARIANT", "0")
+        knob("DS_FORCE_VARIANT", 0)
     for shape in CONV:
         n, c, h, w, k, r, st, pd = shape
         rng = np.random.default_rng(zlib.crc32(repr((shape, bits)).encode()))

@@ -61,8 +61,8 @@ def test_fused_conv_matches_oracle(shape, combo):
     np.testing.assert_array_equal(y.cpu().numpy(), want)
 
 
-def test_fused_conv_direct_kernel(monkeypatch):
-    monkeypatch.setenv("DS_FORCE_VARIANT", "0")
+def test_fused_conv_direct_kernel(knob):
+    knob("DS_FORCE_VARIANT", 0)
     n, c, h, k = 2, 5, 11, 7
     rng = np.random.default_rng(5)
     x = rng.integers(-(2 ** 22), 2 ** 22, (n, c, h, h)).astype(np.int32)

@@ -290,10 +290,10 @@ CASES = [
 
 
 @pytest.mark.parametrize("case", CASES, ids=[str(i) for i in range(len(CASES))])
-def test_generated_code_matches_oracle(case, tmp_path, monkeypatch):
+def test_generated_code_matches_oracle(case, tmp_path, knob):
     n, c, h, w, k, r, s, st, pd, splits, epi = case[:11]
     wsplit = case[11] if len(case) > 11 else 1
-    run_generated(case[:11] + (wsplit,), zlib.crc32(str(case).encode()), 0.1, tmp_path, monkeypatch)
+    run_generated(case[:11] + (wsplit,), zlib.crc32(str(case).encode()), 0.1, tmp_path, knob)
 
 
 def random_cases(count, seed=1905):
@@ -322,16 +322,16 @@ RANDOM = random_cases(20)
 
 
 @pytest.mark.parametrize("case,zero", RANDOM, ids=[str(i) for i in range(len(RANDOM))])
-def test_generated_code_matches_oracle_random_shapes(case, zero, tmp_path, monkeypatch):
-    run_generated(case, zlib.crc32(repr((case, zero)).encode()), zero, tmp_path, monkeypatch)
+def test_generated_code_matches_oracle_random_shapes(case, zero, tmp_path, knob):
+    run_generated(case, zlib.crc32(repr((case, zero)).encode()), zero, tmp_path, knob)
 
 
-def run_generated(case, seed, zero_frac, tmp_path, monkeypatch):
+def run_generated(case, seed, zero_frac, tmp_path, knob):
     """Generate a plan's code object for `case` (n, c, h, w, k, r, s, stride, pad,
     splits, epilogue, wave split), run it in the interpreter over every lane, and
     compare with the oracle."""
     n, c, h, w, k, r, s, st, pd, splits, epi, wsplit = case
-    monkeypatch.setenv("DS_JIT_WSPLIT", str(wsplit))
+    knob("DS_JIT_WSPLIT", wsplit)
     codes, x, rng = gen_layer(seed, n, c, h, w, k, r, s, zero_frac)
     bias = rng.integers(-(2 ** 31), 2 ** 31, k, dtype=np.int64).astype(np.int32)
     mul = add = res = None
