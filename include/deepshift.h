@@ -41,8 +41,7 @@
  * (hipMallocAsync) and give it back in stream order (hipFreeAsync) within the
  * same call: the library keeps no pool and no device memory between calls.
  * Under the runtime's default release threshold the memory returns to the
- * driver at the caller's next synchronisation. Callers that cannot allocate
- * use ds_conv2d_shift_noalloc (below). Plans (ds_jit_conv_*) hold the device
+ * driver at the caller's next synchronisation. Plans (ds_jit_conv_*) hold the device
  * memory they need from create to destroy.
  *
  * Errors: arguments are validated before any device work. On a validation

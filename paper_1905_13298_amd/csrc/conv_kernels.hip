@@ -908,45 +908,86 @@ hipError_t run_epilogue(const ConvGeom &g, int32_t *y, const Epilogue &epi, hipS
     return hipGetLastError();
 }
 
-hipError_t run_conv(const ConvGeom &g0, const int32_t *x, const uint32_t *wp, const int32_t *wi,
-                    const int32_t *bias, int32_t *y, Inner op, hipStream_t st, const Epilogue &epi,
-                    const OutMap &map, const Padded &pad)
-{
-    // A strided output map or custom padded extents come only from the
-    // input-gradient phases: tiled kernel, no epilogue, no transposition.
-    const bool mapped = !map.dense() || pad.vh > 0 || pad.iwp > 0;
-    bool rowmajor = false;
-    const ConvGeom g = mapped ? g0 : tiled_geometry(g0, rowmajor);
-    const int64_t x_bytes = int64_t(g.n) * g.c * g.h * g.w * 4;
+// Everything run_conv decides for a problem before it enqueues work: the kernel,
+// the split of the reduction and the scratch the call needs. Shared by run_conv
+// and conv_scratch_bytes, so that a caller-supplied workspace is sized exactly
+// as the launch uses it.
+struct ConvLayout {
+    ConvGeom g;           // the problem the tiled kernel sees (x^T for row-major inputs)
+    bool mapped = false, rowmajor = false, direct = false, via_dense = false;
+    Variant v{};
     int plane = 0;
     size_t lds = 0;
-    const Variant v = choose_variant(g, pad, plane, lds);
-    if (use_direct(g, v)) {
+    int tiles_p = 0, tiles_k = 0, nchunks = 0, splits = 0, cps = 0, Jpad = 0, Kpad = 0;
+    int64_t grid = 0;
+    size_t init_bytes = 0, wd_bytes = 0, xt_bytes = 0, yt_bytes = 0;
+    size_t scratch_bytes() const { return init_bytes + wd_bytes + xt_bytes + yt_bytes; }
+};
+
+static ConvLayout conv_layout(const ConvGeom &g0, const OutMap &map, const Padded &pad)
+{
+    ConvLayout L;
+    // A strided output map or custom padded extents come only from the
+    // input-gradient phases: tiled kernel, no epilogue, no transposition.
+    L.mapped = !map.dense() || pad.vh > 0 || pad.iwp > 0;
+    L.g = L.mapped ? g0 : tiled_geometry(g0, L.rowmajor);
+    const ConvGeom &g = L.g;
+    L.v = choose_variant(g, pad, L.plane, L.lds);
+    L.direct = use_direct(g, L.v);
+    if (L.direct) return L;
+    plan_splits(g, L.v, L.tiles_p, L.tiles_k, L.nchunks, L.splits, L.cps);
+    L.Jpad = L.nchunks * L.v.cc * g.r * g.s;
+    L.Kpad = L.tiles_k * 4 * kTN;
+    L.grid = int64_t(L.tiles_p) * L.tiles_k * L.splits;
+    // Split partial sums meet through int32 atomics; through a strided output map
+    // those land on scattered addresses, so a split mapped problem accumulates into
+    // a dense buffer that is scattered into place afterwards.
+    L.via_dense = L.mapped && L.splits > 1;
+    // Scratch: init[Kpad], wd[Kpad][Jpad], x^T for row-major inputs, y^T (row-major) or
+    // the dense partial sums (split mapped problems).
+    const int64_t x_bytes = int64_t(g.n) * g.c * g.h * g.w * 4;
+    L.init_bytes = (size_t(L.Kpad) * 4 + 255) & ~size_t(255);
+    L.wd_bytes = (size_t(L.Kpad) * L.Jpad * 4 + 255) & ~size_t(255);
+    L.xt_bytes = L.rowmajor ? (size_t(x_bytes) + 255) & ~size_t(255) : 0;
+    L.yt_bytes = L.rowmajor ? size_t(g0.n) * g0.k * 4
+               : L.via_dense ? size_t(g.n) * g.k * g.oh * g.ow * 4 : 0;
+    return L;
+}
+
+size_t conv_scratch_bytes(const ConvGeom &g0, const OutMap &map, const Padded &pad)
+{
+    const ConvLayout L = conv_layout(g0, map, pad);
+    return L.direct ? 0 : L.scratch_bytes();
+}
+
+hipError_t run_conv(const ConvGeom &g0, const int32_t *x, const uint32_t *wp, const int32_t *wi,
+                    const int32_t *bias, int32_t *y, Inner op, hipStream_t st, const Epilogue &epi,
+                    const OutMap &map, const Padded &pad, const Workspace &ws)
+{
+    const ConvLayout L = conv_layout(g0, map, pad);
+    const ConvGeom &g = L.g;
+    const bool mapped = L.mapped, rowmajor = L.rowmajor;
+    if (L.direct) {
         if (mapped) return hipErrorInvalidValue;
         const hipError_t e = run_direct(g0, x, wp, wi, bias, y, op, st);
         return e == hipSuccess && epi.any() ? run_epilogue(g0, y, epi, st) : e;
     }
     if (mapped && epi.any()) return hipErrorInvalidValue;
-
-    const int RS = g.r * g.s;
-    int tiles_p, tiles_k, nchunks, splits, cps;
-    plan_splits(g, v, tiles_p, tiles_k, nchunks, splits, cps);
-    const int Jpad = nchunks * v.cc * RS;
-    const int Kpad = tiles_k * 4 * kTN;
+    if (L.grid > INT32_MAX) return hipErrorInvalidValue;
+    const Variant &v = L.v;
+    const int64_t x_bytes = int64_t(g.n) * g.c * g.h * g.w * 4;
     const int64_t NQ = int64_t(g.n) * g.oh * g.ow;
-    const int64_t grid = int64_t(tiles_p) * tiles_k * splits;
-    if (grid > INT32_MAX) return hipErrorInvalidValue;
 
     TiledParams p;
     p.N = g.n; p.C = g.c; p.H = g.h; p.W = g.w; p.K = g.k; p.R = g.r; p.S = g.s;
     p.sh = g.sh; p.sw = g.sw; p.ph = g.ph; p.pw = g.pw; p.OH = g.oh; p.OW = g.ow;
     p.OHOW = g.oh * g.ow; p.NQ = int(NQ); p.HW = g.h * g.w;
-    p.Jpad = Jpad; p.PLANE = plane;
+    p.Jpad = L.Jpad; p.PLANE = L.plane;
     padded_dims(g, pad, p.VH, p.IWP);
     const OutMap m = map.dense() ? OutMap{0, g.k * g.oh * g.ow, g.oh * g.ow, g.ow, 1} : map;
     p.ybase = int(m.base); p.ynst = m.nstride; p.ykst = m.kstride; p.yrst = m.rstride; p.ycst = m.cstride;
-    p.tiles_p = tiles_p; p.tiles_k = tiles_k; p.chunks_per_split = cps; p.nchunks = nchunks;
-    p.atomic_out = splits > 1;
+    p.tiles_p = L.tiles_p; p.tiles_k = L.tiles_k; p.chunks_per_split = L.cps; p.nchunks = L.nchunks;
+    p.atomic_out = L.splits > 1;
     p.fuse_epi = epi.any() && !p.atomic_out && !rowmajor;
     p.epi = epi;
     p.x_bytes = int(x_bytes);
@@ -954,43 +995,40 @@ hipError_t run_conv(const ConvGeom &g0, const int32_t *x, const uint32_t *wp, co
     p.div_ow = make_fastdiv(uint32_t(g.ow));
     p.div_vh = make_fastdiv(uint32_t(p.VH));
     p.div_iwp = make_fastdiv(uint32_t(p.IWP));
-
-    // Split partial sums meet through int32 atomics; through a strided output map
-    // those land on scattered addresses, so a split mapped problem accumulates into
-    // a dense buffer that is scattered into place afterwards.
-    const bool via_dense = mapped && splits > 1;
-    if (via_dense) {
+    if (L.via_dense) {
         const OutMap d{0, g.k * g.oh * g.ow, g.oh * g.ow, g.ow, 1};
         p.ybase = 0; p.ynst = d.nstride; p.ykst = d.kstride; p.yrst = d.rstride; p.ycst = d.cstride;
     }
-    // Scratch: init[Kpad], wd[Kpad][Jpad], x^T for row-major inputs, y^T (row-major) or
-    // the dense partial sums (split mapped problems).
-    const size_t init_bytes = (size_t(Kpad) * 4 + 255) & ~size_t(255);
-    const size_t wd_bytes = (size_t(Kpad) * Jpad * 4 + 255) & ~size_t(255);
-    const size_t xt_bytes = rowmajor ? (size_t(x_bytes) + 255) & ~size_t(255) : 0;
-    const size_t yt_bytes = rowmajor ? size_t(g0.n) * g0.k * 4
-                          : via_dense ? size_t(g.n) * g.k * g.oh * g.ow * 4 : 0;
-    const size_t bytes = init_bytes + wd_bytes + xt_bytes + yt_bytes;
+    // Scratch from the caller's workspace when one is given (every byte of it that
+    // the call reads is written first in the call: nothing needs clearing), else
+    // from the stream-ordered pool.
+    const size_t bytes = L.scratch_bytes();
     void *scratch = nullptr;
-    hipError_t e = scratch_alloc(&scratch, bytes, st);
-    if (e != hipSuccess) return e;
+    hipError_t e = hipSuccess;
+    if (ws.ptr) {
+        if (bytes > ws.bytes) return hipErrorInvalidValue;
+        scratch = ws.ptr;
+    } else {
+        e = scratch_alloc(&scratch, bytes, st);
+        if (e != hipSuccess) return e;
+    }
     int32_t *init = static_cast<int32_t *>(scratch);
-    int32_t *wd = reinterpret_cast<int32_t *>(static_cast<char *>(scratch) + init_bytes);
+    int32_t *wd = reinterpret_cast<int32_t *>(static_cast<char *>(scratch) + L.init_bytes);
     const int32_t *xin = x;
     int32_t *yout = y;
-    if (via_dense)
-        yout = reinterpret_cast<int32_t *>(static_cast<char *>(scratch) + init_bytes + wd_bytes);
+    if (L.via_dense)
+        yout = reinterpret_cast<int32_t *>(static_cast<char *>(scratch) + L.init_bytes + L.wd_bytes);
     if (rowmajor) {
-        yout = reinterpret_cast<int32_t *>(static_cast<char *>(scratch) + init_bytes + wd_bytes +
-                                           xt_bytes);
-        int32_t *xt = reinterpret_cast<int32_t *>(static_cast<char *>(scratch) + init_bytes + wd_bytes);
+        yout = reinterpret_cast<int32_t *>(static_cast<char *>(scratch) + L.init_bytes + L.wd_bytes +
+                                           L.xt_bytes);
+        int32_t *xt = reinterpret_cast<int32_t *>(static_cast<char *>(scratch) + L.init_bytes + L.wd_bytes);
         const int64_t tiles = int64_t((g0.c + 63) / 64) * ((g0.n + 63) / 64);
         hipLaunchKernelGGL(transpose_kernel, dim3(unsigned(tiles)), dim3(256), 0, st, x, xt, g0.n,
                            g0.c);
         xin = xt;
     }
     const int wpr = int(row_words_bits(g.crs, g.bits));
-
+    const int Kpad = L.Kpad, Jpad = L.Jpad;
     const int64_t pw_total = int64_t(Kpad) * Jpad;
     const int wblocks = int(std::min<int64_t>((pw_total + 255) / 256, 4096));
     const int pgrid = wblocks + (Kpad + 3) / 4;
@@ -1001,13 +1039,13 @@ hipError_t run_conv(const ConvGeom &g0, const int32_t *x, const uint32_t *wp, co
         hipLaunchKernelGGL((prep_kernel<Inner::Mul, kTN>), dim3(pgrid), dim3(256), 0, st, wp, wi,
                            bias, g.k, g.crs, wpr, Jpad, Kpad, wblocks, wd, init, code_fmt(g.bits));
     e = hipGetLastError();
-    if (e == hipSuccess && p.atomic_out) e = run_fill_mapped(g, init, yout, via_dense ? OutMap() : map, st);
+    if (e == hipSuccess && p.atomic_out) e = run_fill_mapped(g, init, yout, L.via_dense ? OutMap() : map, st);
     if (e == hipSuccess) {
         e = op == Inner::Shift
-                ? dispatch_tiled<Inner::Shift>(v, p, int(grid), lds, xin, wd, init, yout, st)
-                : dispatch_tiled<Inner::Mul>(v, p, int(grid), lds, xin, wd, init, yout, st);
+                ? dispatch_tiled<Inner::Shift>(v, p, int(L.grid), L.lds, xin, wd, init, yout, st)
+                : dispatch_tiled<Inner::Mul>(v, p, int(L.grid), L.lds, xin, wd, init, yout, st);
     }
-    if (e == hipSuccess && via_dense) e = run_copy_mapped(g, yout, y, map, st);
+    if (e == hipSuccess && L.via_dense) e = run_copy_mapped(g, yout, y, map, st);
     if (e == hipSuccess && rowmajor) {
         const int64_t tiles = int64_t((g0.n + 63) / 64) * ((g0.k + 63) / 64);
         hipLaunchKernelGGL(transpose_kernel, dim3(unsigned(tiles)), dim3(256), 0, st, yout, y, g0.k,
@@ -1015,6 +1053,7 @@ hipError_t run_conv(const ConvGeom &g0, const int32_t *x, const uint32_t *wp, co
         e = hipGetLastError();
     }
     if (e == hipSuccess && epi.any() && !p.fuse_epi) e = run_epilogue(g0, y, epi, st);
+    if (ws.ptr) return e;
     const hipError_t ef = hipFreeAsync(scratch, st);
     return e != hipSuccess ? e : ef;
 }

@@ -53,13 +53,29 @@ struct Padded {
     int vh = 0, iwp = 0;
 };
 
+// Device memory a call may use for its scratch instead of allocating it: at
+// `ptr`, `bytes` long, 256-byte aligned (ptr == nullptr: allocate in stream order).
+struct Workspace {
+    void *ptr = nullptr;
+    size_t bytes = 0;
+};
+
 // Enqueue the whole computation of y on `stream`. Exactly one of `wpacked`
 // (Shift) and `wint` (Mul) is used. g.oh and g.ow give the output grid; with
-// the defaults of `map` and `pad` they must be the usual output sizes.
+// the defaults of `map` and `pad` they must be the usual output sizes. With a
+// workspace of at least conv_scratch_bytes(g, map, pad) bytes the call
+// allocates nothing; a smaller one fails with hipErrorInvalidValue before any
+// launch.
 hipError_t run_conv(const ConvGeom &g, const int32_t *x, const uint32_t *wpacked,
                     const int32_t *wint, const int32_t *bias, int32_t *y, Inner op,
                     hipStream_t stream, const Epilogue &epi = Epilogue(),
-                    const OutMap &map = OutMap(), const Padded &pad = Padded());
+                    const OutMap &map = OutMap(), const Padded &pad = Padded(),
+                    const Workspace &ws = Workspace());
+
+// Scratch bytes run_conv takes for g (0 when it runs the one-thread-per-output
+// kernel, which needs none). Host only; touches no device.
+size_t conv_scratch_bytes(const ConvGeom &g, const OutMap &map = OutMap(),
+                          const Padded &pad = Padded());
 
 // One stride phase of the input gradient of a forward layer (backward.hip): the
 // stride-1 correlation of dy that produces the dx rows a + sh*i and columns

@@ -1,0 +1,104 @@
+"""ds_conv2d_shift_noalloc: the ConvShift entry point that allocates nothing.
+
+Called through the C ABI, its outputs must equal ds_conv2d_shift's bit for bit
+(and the oracle's), on consecutive calls that reuse the one scratch array of
+the GPU with different problems -- a larger one, then smaller ones -- and with
+problems over its limit rejected before anything runs.
+"""
+import ctypes
+
+import numpy as np
+import pytest
+import torch
+
+import oracle
+from paper_1905_13298_amd import _native, ops
+from paper_1905_13298_amd.workloads import random_codes
+
+pytestmark = pytest.mark.gpu
+DEV = torch.device("cuda:0")
+DS_RELU = 1
+UNSUPPORTED = 7
+
+
+def say(*a):
+    print(*a, flush=True)
+
+
+def to_dev(a):
+    return torch.from_numpy(np.ascontiguousarray(a)).to(DEV)
+
+
+def case(seed, n, c, h, w, k, r, stride, pad, signed):
+    rng = np.random.default_rng(seed)
+    lo = -(2 ** 24) if signed else 0
+    x = rng.integers(lo, 2 ** 24, (n, c, h, w)).astype(np.int32)
+    codes = random_codes(rng, (k, c * r * r), zero_frac=0.1)
+    bias = rng.integers(-(2 ** 16), 2 ** 16, k).astype(np.int32)
+    return x, codes, bias
+
+
+def call(name, xt, wt, bt, y, n, c, h, w, k, r, stride, pad, flags):
+    lib = _native.lib()
+    fn = getattr(lib, name)
+    stream = torch.cuda.current_stream(DEV).cuda_stream
+    st = fn(xt.data_ptr(), wt.data_ptr(), None if bt is None else bt.data_ptr(), y.data_ptr(),
+            n, c, h, w, k, r, r, stride, stride, pad, pad, 16, flags, ctypes.c_void_p(stream))
+    return st
+
+
+# (n, c, h, w, k, r, stride, pad, signed, flags): larger first, then smaller
+# problems on the same scratch array; tiled window, split-K, pointwise,
+# LinearShift (transposed operands in scratch), ReLU, signed inputs.
+SEQUENCE = [
+    (4, 64, 28, 28, 128, 3, 1, 1, False, 0),
+    (2, 13, 9, 11, 37, 3, 1, 1, True, DS_RELU),
+    (1, 128, 28, 28, 128, 3, 1, 1, False, 0),
+    (3, 16, 8, 8, 40, 1, 2, 0, True, 0),
+    (64, 512, 1, 1, 1000, 1, 1, 0, False, 0),
+    (8, 256, 1, 1, 128, 1, 1, 0, True, DS_RELU),
+]
+
+
+def test_noalloc_equals_conv2d_shift_on_consecutive_calls():
+    for i, (n, c, h, w, k, r, stride, pad, signed, flags) in enumerate(SEQUENCE):
+        x, codes, bias = case(100 + i, n, c, h, w, k, r, stride, pad, signed)
+        need = _native.lib().ds_conv2d_shift_noalloc_scratch_bytes(n, c, h, w, k, r, r, stride,
+                                                                     stride, pad, pad)
+        say(f"noalloc call {i}: n={n} c={c} {h}x{w} k={k} r={r} s={stride} p={pad} "
+            f"flags={flags} scratch {need} bytes ({ops.describe_conv2d(n, c, h, w, k, r, stride, pad)})")
+        assert 0 <= need <= (32 << 20)
+        xt, wt, bt = to_dev(x), to_dev(ops.pack_shift_weights(codes).view(np.int32)), to_dev(bias)
+        oh, ow = (h + 2 * pad - r) // stride + 1, (w + 2 * pad - r) // stride + 1
+        y0 = torch.full((n, k, oh, ow), 0x5A5A5A5A, dtype=torch.int32, device=DEV)
+        y1 = torch.full((n, k, oh, ow), 0x3C3C3C3C, dtype=torch.int32, device=DEV)
+        assert call("ds_conv2d_shift", xt, wt, bt, y0, n, c, h, w, k, r, stride, pad, flags) == 0
+        assert call("ds_conv2d_shift_noalloc", xt, wt, bt, y1, n, c, h, w, k, r, stride, pad, flags) == 0
+        a, b = y0.cpu().numpy(), y1.cpu().numpy()
+        bad = np.flatnonzero(a.ravel() != b.ravel())
+        assert bad.size == 0, f"call {i}: {bad.size} of {a.size} outputs differ, first at {bad[:5]}"
+        want = oracle.conv2d_shift(x, codes, bias, r=r, stride=stride, pad=pad)
+        if flags & DS_RELU:
+            want = np.maximum(want, 0)
+        np.testing.assert_array_equal(b, want)
+
+
+def test_noalloc_rejects_problems_over_its_limit():
+    # LinearShift 4096 -> 4096 at batch 256 needs 72 MiB of scratch.
+    n, c, k = 256, 4096, 4096
+    need = _native.lib().ds_conv2d_shift_noalloc_scratch_bytes(n, c, 1, 1, k, 1, 1, 1, 1, 0, 0)
+    assert need > (32 << 20)
+    x = torch.zeros((n, c), dtype=torch.int32, device=DEV)
+    wt = torch.zeros((k, ops.packed_row_words(c)), dtype=torch.int32, device=DEV)
+    y = torch.full((n, k), 7, dtype=torch.int32, device=DEV)
+    st = call("ds_conv2d_shift_noalloc", x, wt, None, y, n, c, 1, 1, k, 1, 1, 0, 0)
+    assert st == UNSUPPORTED
+    assert b"scratch" in _native.lib().ds_last_error_message()
+    torch.cuda.synchronize()
+    assert torch.all(y == 7)
+    # The entry point still works after the rejection.
+    x, codes, bias = case(7, 2, 8, 5, 5, 9, 3, 1, 1, True)
+    xt, wt2, bt = to_dev(x), to_dev(ops.pack_shift_weights(codes).view(np.int32)), to_dev(bias)
+    y1 = torch.empty((2, 9, 5, 5), dtype=torch.int32, device=DEV)
+    assert call("ds_conv2d_shift_noalloc", xt, wt2, bt, y1, 2, 8, 5, 5, 9, 3, 1, 1, 0) == 0
+    np.testing.assert_array_equal(y1.cpu().numpy(), oracle.conv2d_shift(x, codes, bias, r=3, pad=1))
