@@ -41,7 +41,8 @@
  * (hipMallocAsync) and give it back in stream order (hipFreeAsync) within the
  * same call: the library keeps no pool and no device memory between calls.
  * Under the runtime's default release threshold the memory returns to the
- * driver at the caller's next synchronisation. Plans (ds_jit_conv_*) hold the device
+ * driver at the caller's next synchronisation. Callers that cannot allocate
+ * use ds_conv2d_shift_noalloc (below). Plans (ds_jit_conv_*) hold the device
  * memory they need from create to destroy.
  *
  * Errors: arguments are validated before any device work. On a validation
@@ -405,6 +406,33 @@ ds_status ds_jit_conv_backward_data_create(const uint32_t *w_packed, int64_t n, 
                                            int32_t stride_h, int32_t stride_w, int32_t pad_h,
                                            int32_t pad_w, uint32_t flags, int32_t splits,
                                            ds_jit_conv **plan);
+
+/* ---- ConvShift that allocates nothing ------------------------------------
+ *
+ * For callers that cannot allocate device memory: code under HIP graph
+ * capture, tight serving loops, harnesses that forbid allocation.
+ * ds_conv2d_shift_noalloc computes exactly what ds_conv2d_shift computes (same
+ * arguments, layouts, flags and errors; a LinearShift is the case
+ * h = w = r = s = 1 with x [batch][in] as [batch][in][1][1]) and calls no
+ * hipMalloc, hipMallocAsync, hipFree or other allocating routine. Its scratch
+ * is one array of DS_NOALLOC_SCRATCH_BYTES per GPU, placed in the library's
+ * code object and held from the library's first use on that GPU until the
+ * process ends. A problem whose scratch would exceed it fails with
+ * DS_ERR_UNSUPPORTED before anything is launched; ds_conv2d_shift_noalloc_
+ * scratch_bytes gives a shape's need (-1 for an invalid shape; 0 for shapes
+ * on the one-thread-per-output kernel). Every call on a GPU uses that GPU's one
+ * array: calls on one stream are ordered, but calls that overlap in time on
+ * one GPU (several streams, several host threads) race on it and must be
+ * serialised by the caller. */
+#define DS_NOALLOC_SCRATCH_BYTES (32u << 20)
+ds_status ds_conv2d_shift_noalloc(const int32_t *x, const uint32_t *w_packed, const int32_t *bias,
+                                  int32_t *y, int64_t n, int64_t c, int64_t h, int64_t w,
+                                  int64_t k, int64_t r, int64_t s,
+                                  int32_t stride_h, int32_t stride_w, int32_t pad_h, int32_t pad_w,
+                                  int32_t frac_bits, uint32_t flags, void *stream);
+int64_t ds_conv2d_shift_noalloc_scratch_bytes(int64_t n, int64_t c, int64_t h, int64_t w,
+                                              int64_t k, int64_t r, int64_t s, int32_t stride_h,
+                                              int32_t stride_w, int32_t pad_h, int32_t pad_w);
 
 /* Tuning overrides, for tests and measurements: they change which kernel
  * variant, wave split, block order or load depth the library uses, never a

@@ -48,6 +48,8 @@ SIGNATURES = {
     "ds_conv2d_shift_backward_data": (ctypes.c_int, [_P, _P, _P] + [_I64] * 7 + [_I32] * 4 + [_I32, _U32, _P]),
     "ds_linear_shift_backward_data": (ctypes.c_int, [_P, _P, _P, _I64, _I64, _I64, _I32, _U32, _P]),
     "ds_conv2d_shift_backward_data_describe": (ctypes.c_int, [_I64] * 7 + [_I32] * 4 + [ctypes.c_char_p, _I64]),
+    "ds_conv2d_shift_noalloc": (ctypes.c_int, [_P, _P, _P, _P] + [_I64] * 7 + [_I32] * 4 + [_I32, _U32, _P]),
+    "ds_conv2d_shift_noalloc_scratch_bytes": (_I64, [_I64] * 7 + [_I32] * 4),
     "ds_set_tuning": (ctypes.c_int, [ctypes.c_char_p, _I32]),
     "ds_get_tuning": (ctypes.c_int, [ctypes.c_char_p, _P]),
     "ds_status_string": (ctypes.c_char_p, [ctypes.c_int]),

@@ -4,6 +4,8 @@
 // y [n][k][1][1], so both operators share every kernel.
 #include <hip/hip_runtime.h>
 
+#include <mutex>
+
 #include "common.hpp"
 #include "conv_plan.hpp"
 
@@ -199,4 +201,92 @@ extern "C" ds_status ds_linear_mul_i32(const int32_t *x, const int32_t *wts, con
     return hip_status(run_conv(g, x, nullptr, wts, bias, y, Inner::Mul,
                                static_cast<hipStream_t>(stream)),
                       "ds_linear_mul_i32");
+}
+
+// ---------------------------------------------------------------------------
+// ConvShift without allocation. The scratch of the runtime kernel (decoded
+// weights, per-channel start values, transposed operands of a LinearShift)
+// lives in this array, one copy per GPU in the library's code object, held
+// from the code object's load on that GPU to the end of the process. The
+// array's name is a host-side stand-in: host code takes the device address of
+// the current GPU's copy from hipGetSymbolAddress, once per device, and passes
+// that address on.
+
+static __device__ __align__(256) unsigned char scratch[DS_NOALLOC_SCRATCH_BYTES];
+
+namespace ds {
+namespace {
+
+constexpr int kMaxDevices = 64;
+
+// Device address of the current device's copy of `scratch`, looked up on the
+// first call on that device (with the device current).
+hipError_t noalloc_scratch(void **out)
+{
+    static std::mutex mu;
+    static void *ptr[kMaxDevices] = {};
+    int dev = -1;
+    hipError_t e = hipGetDevice(&dev);
+    if (e != hipSuccess) return e;
+    if (dev < 0 || dev >= kMaxDevices) return hipErrorInvalidDevice;
+    std::lock_guard<std::mutex> lock(mu);
+    if (!ptr[dev]) {
+        void *p = nullptr;
+        e = hipGetSymbolAddress(&p, HIP_SYMBOL(scratch));
+        if (e != hipSuccess) return e;
+        if (!p) return hipErrorInvalidSymbol;
+        ptr[dev] = p;
+    }
+    *out = ptr[dev];
+    return hipSuccess;
+}
+
+}  // namespace
+}  // namespace ds
+
+extern "C" ds_status ds_conv2d_shift_noalloc(const int32_t *x, const uint32_t *w_packed,
+                                             const int32_t *bias, int32_t *y, int64_t n, int64_t c,
+                                             int64_t h, int64_t w, int64_t k, int64_t r, int64_t s,
+                                             int32_t stride_h, int32_t stride_w, int32_t pad_h,
+                                             int32_t pad_w, int32_t frac_bits, uint32_t flags,
+                                             void *stream)
+{
+    ConvGeom g;
+    // The size limit is checked from the shape alone, before any device access.
+    if (x && w_packed && y) {
+        const int bits = flags_code_bits(flags);
+        ds_status st = check_shape(n, c, h, w, k, r, s, stride_h, stride_w, pad_h, pad_w, true, g,
+                                   bits < 0 ? 5 : bits);
+        if (st != DS_SUCCESS) return st;
+        const size_t need = conv_scratch_bytes(g);
+        if (need > size_t(DS_NOALLOC_SCRATCH_BYTES))
+            return fail(DS_ERR_UNSUPPORTED,
+                        "ds_conv2d_shift_noalloc: this problem needs %zu bytes of scratch, more than "
+                        "the %u bytes the library holds for it (use ds_conv2d_shift)",
+                        need, unsigned(DS_NOALLOC_SCRATCH_BYTES));
+    }
+    ds_status st = check_conv(x, w_packed, bias, y, n, c, h, w, k, r, s, stride_h, stride_w,
+                              pad_h, pad_w, frac_bits, flags, true, g, DS_RELU);
+    if (st != DS_SUCCESS) return st;
+    void *ws = nullptr;
+    const hipError_t e = noalloc_scratch(&ws);
+    if (e != hipSuccess) return hip_status(e, "ds_conv2d_shift_noalloc: scratch address");
+    Epilogue epi;
+    epi.relu = (flags & DS_RELU) != 0;
+    return hip_status(run_conv(g, x, w_packed, nullptr, bias, y, Inner::Shift,
+                               static_cast<hipStream_t>(stream), epi, OutMap(), Padded(),
+                               Workspace{ws, size_t(DS_NOALLOC_SCRATCH_BYTES)}),
+                      "ds_conv2d_shift_noalloc");
+}
+
+extern "C" int64_t ds_conv2d_shift_noalloc_scratch_bytes(int64_t n, int64_t c, int64_t h, int64_t w,
+                                                         int64_t k, int64_t r, int64_t s,
+                                                         int32_t stride_h, int32_t stride_w,
+                                                         int32_t pad_h, int32_t pad_w)
+{
+    ConvGeom g;
+    if (check_shape(n, c, h, w, k, r, s, stride_h, stride_w, pad_h, pad_w, true, g) != DS_SUCCESS)
+        return -1;
+    ok();
+    return int64_t(conv_scratch_bytes(g));
 }

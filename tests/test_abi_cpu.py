@@ -322,3 +322,21 @@ def test_tuning_overrides_are_explicit():
             del os.environ["DS_JIT_WSPLIT"]
         else:
             os.environ["DS_JIT_WSPLIT"] = old
+
+
+def test_noalloc_limit_checked_from_the_shape_alone():
+    """ds_conv2d_shift_noalloc rejects a problem whose scratch exceeds its array
+    before touching any buffer; the scratch query needs no GPU."""
+    lib = _native.lib()
+    need = lib.ds_conv2d_shift_noalloc_scratch_bytes(256, 4096, 1, 1, 4096, 1, 1, 1, 1, 0, 0)
+    assert need > (32 << 20)
+    assert lib.ds_conv2d_shift_noalloc_scratch_bytes(1, 128, 28, 28, 128, 3, 3, 1, 1, 1, 1) <= (32 << 20)
+    assert lib.ds_conv2d_shift_noalloc_scratch_bytes(0, 1, 1, 1, 1, 1, 1, 1, 1, 0, 0) == -1
+    x = np.zeros(16, np.int32)
+    st = lib.ds_conv2d_shift_noalloc(x.ctypes.data, x.ctypes.data, None, x.ctypes.data, 256, 4096, 1,
+                                     1, 4096, 1, 1, 1, 1, 0, 0, 16, 0, None)
+    assert st == 7 and b"scratch" in lib.ds_last_error_message()
+    # Within the limit, host buffers are rejected as for ds_conv2d_shift.
+    st = lib.ds_conv2d_shift_noalloc(x.ctypes.data, x.ctypes.data, None, x.ctypes.data, 1, 2, 2, 2,
+                                     2, 1, 1, 1, 1, 0, 0, 16, 0, None)
+    assert st == 3
