@@ -516,10 +516,18 @@ ds_status finish_spec(Spec &sp, int bits, int splits, int deep_blocks = 3072)
     // pixel tiles) whose wave shares keep at least 128 elements per part spreads
     // toward 2400 workgroups (ResNet-50's 2048 -> 512 layer at 7 x 7: 3 parts ran
     // 1.1x faster than 1 or 2).
+    // (5) A window on a grid under 256 workgroups of 256 pixels (a small batch)
+    // lets each wave's share of a part go down to 24 reduction elements: such a
+    // grid has too few waves to use the chip's SIMDs, and one wave per SIMD issues
+    // at half the rate of two. On MI355X the 128 -> 128, 3 x 3 layer at 28 x 28 and
+    // batch 1 ran its kernel in 9.9 us at 12 or 16 parts against 13.7 us at 4 (and
+    // 12.5 us at 24).
     int ns = splits;
     if (ns == 0) {
         const int64_t blocks = int64_t(sp.tiles_p) * sp.kgroups;
-        int64_t want = std::min<int64_t>((384 + blocks - 1) / blocks, g.crs / (64 * sp.wsplit));
+        const bool thin_window = base < 256 && int64_t(g.r) * g.s > 1;
+        const int64_t floor_share = thin_window ? 24 : 64;
+        int64_t want = std::min<int64_t>((384 + blocks - 1) / blocks, g.crs / (floor_share * sp.wsplit));
         if (deep_blocks > 0 && int64_t(g.r) * g.s > 1)
             want = std::max<int64_t>(want, std::min<int64_t>((deep_blocks + blocks - 1) / blocks, g.crs / 768));
         const int64_t tiles256 = (nq + kBlockPixels - 1) / kBlockPixels;
@@ -527,11 +535,12 @@ ds_status finish_spec(Spec &sp, int bits, int splits, int deep_blocks = 3072)
             want = std::max<int64_t>(want, std::min<int64_t>((2400 + blocks - 1) / blocks, g.crs / (128 * sp.wsplit)));
         // (4) Fewer than 4 tiles of 256 pixels (a LinearShift at small batch): every
         // code segment streams through the instruction cache for a few waves only,
-        // and more parts mean more code streams: at most 2 (2048 -> 1000 at batch
-        // 128: 62 us at 2 parts, 112 us at 8), and none once the grid has a
-        // workgroup per CU (4096 -> 4096 at batch 256, 256 workgroups: 175 us
-        // whole, 261 us in 2 parts).
-        if (tiles256 < 4) want = blocks >= 256 ? 1 : std::min<int64_t>(want, 2);
+        // and more parts mean more code streams: at most 4 (with a wave split of 4,
+        // 2048 -> 1000 at batch 128: 45 us at 4 parts, 49 us at 2, 57 us at 8;
+        // 512 -> 1000 at batch 32: 18 us at 4, 21 us at 2), and none once the grid
+        // has a workgroup per CU (4096 -> 4096 at batch 256, 256 workgroups: 174 us
+        // whole, 258 us in 2 parts).
+        if (tiles256 < 4) want = blocks >= 256 ? 1 : std::min<int64_t>(want, 4);
         ns = int(std::max<int64_t>(1, want));
     }
     sp.nsplit = std::min(ns, g.c);
