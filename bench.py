@@ -49,10 +49,15 @@ NETWORK_WORKLOADS = {"resnet18_infer": 32}
 # workload but the stem (the images need no gradient), on signed output gradients.
 BACKWARD_WORKLOADS = {"resnet50_bwd_data": 4, "resnet18_bwd_data": 3}
 
-# MI355X: 256 CUs at 2.4 GHz. Three-operand (VOP3) integer instructions such as
-# v_xad_u32 run 64 lanes per CU per clock; two-operand (VOP2) ones such as
-# v_add_u32 / v_sub_u32 / v_ashrrev_i32 run up to 128, the lane rate of the
-# published fp32 vector peak (157.3 TFLOP/s = 256 x 128 FMA x 2 x 2.4 GHz).
+# MI355X: 256 CUs of 4 SIMDs at 2.4 GHz; a wave64 VALU instruction occupies a
+# SIMD for 4 clocks, i.e. 64 int32 lane-ops per CU per clock (39.32 T/s). The
+# SIMDs also issue two-operand (VOP2) instructions such as v_add_u32 /
+# v_sub_u32 / v_ashrrev_i32 two at a time from different waves (the counter
+# SQ_ACTIVE_INST_VALU2): a register-only probe issued 0.39-0.45 such
+# instructions per SIMD per clock against 0.24 for three-operand ones, and the
+# generated plan code reached 0.355 per SIMD per clock with 90 % of them in pairs
+# (profiles/valu_issue_rates.md). The plans are therefore rated against 128 lane-ops per
+# CU per clock (78.64 T/s), and also reported against 39.32 T/s.
 CUS, LANES_PER_CU, CLOCK_GHZ = 256, 64, 2.4
 INT32_OPS_PEAK_T = CUS * LANES_PER_CU * CLOCK_GHZ / 1000.0        # 39.32 T int32 ops/s (VOP3)
 VOP2_OPS_PEAK_T = 2 * INT32_OPS_PEAK_T                              # 78.64 T int32 ops/s (VOP2)
@@ -69,10 +74,11 @@ def kernel_variant(layer) -> str:
                                layer.stride, layer.pad)
 
 
-def algorithmic_bytes(layer) -> int:
-    """Bytes a call must move at least: x, y, packed weights (ceil(CRS/6) words per row), bias."""
+def algorithmic_bytes(layer, act_bits: int = 32) -> int:
+    """Bytes a call must move at least: x (act_bits per element), y, packed weights
+    (ceil(CRS/6) words per row), bias."""
     wpr = (layer.crs + 5) // 6
-    b = 4 * int(np.prod(layer.x_shape)) + 4 * int(np.prod(layer.y_shape)) + 4 * layer.k * wpr
+    b = act_bits // 8 * int(np.prod(layer.x_shape)) + 4 * int(np.prod(layer.y_shape)) + 4 * layer.k * wpr
     return b + (4 * layer.k if layer.bias else 0)
 
 
@@ -104,6 +110,9 @@ def parse():
                          "run the runtime kernel); runtime: ds_conv2d_shift / ds_linear_shift")
     ap.add_argument("--no-runtime", action="store_true",
                     help="with --path jit, skip timing the runtime-weights path as well")
+    ap.add_argument("--act-bits", type=int, default=32, choices=[32, 16, 8],
+                    help="activation width of the layer workloads: 32 (int32, F=16), or the lower "
+                         "bit-widths 16 (int16 3.13) and 8 (int8 3.5), on the plan path")
     return ap.parse_args()
 
 
@@ -680,7 +689,7 @@ def time_layers(calls, steps, warmup, stream):
     return ms_per_step, d
 
 
-def roofline_of(layers, d, path, nonzero, planned=None):
+def roofline_of(layers, d, path, nonzero, planned=None, act_bits=32):
     """Roofline record of the kernel with the most time per step, from the
     per-call durations `d` [steps][layers]; planned[i]: layer i runs a plan."""
     groups = {}
@@ -691,9 +700,9 @@ def roofline_of(layers, d, path, nonzero, planned=None):
         g["nz"] += L.sac * nonzero[li]
         g["ms"] += float(d[:, li].mean())
         g["launches"] += 1
-        g["bytes"] += algorithmic_bytes(L)
+        g["bytes"] += algorithmic_bytes(L, act_bits)
     name, g = max(groups.items(), key=lambda kv: kv[1]["ms"])
-    traffic = measured_traffic(name, "jit" if name == JIT_KERNEL else "runtime")
+    traffic = measured_traffic(name, "jit" if name == JIT_KERNEL else "runtime") if act_bits == 32 else None
     common = {
         "traffic": None if traffic is None else int(traffic),
         "traffic_unit": "HBM bytes per launch (FETCH_SIZE + WRITE_SIZE, copy-calibrated)",
@@ -710,7 +719,8 @@ def roofline_of(layers, d, path, nonzero, planned=None):
         # nothing), so the roofline counts non-zero terms against the VOP2 lane-op peak.
         nz = g["nz"] / (g["ms"] * 1e-3) / 1e12
         return {"bound": "alu", "achieved": round(nz, 4), "peak": round(VOP2_OPS_PEAK_T, 4),
-                "unit": "T int32 ops/s", "frac": round(nz / VOP2_OPS_PEAK_T, 4), **common,
+                "unit": "T int32 ops/s", "frac": round(nz / VOP2_OPS_PEAK_T, 4),
+                "frac_of_64_lanes_per_cu_clk": round(nz / INT32_OPS_PEAK_T, 4), **common,
                 "work_unit": "one int32 VOP2 add/sub per non-zero weight term",
                 "entry_points": list(JIT_ENTRY_POINTS),
                 "nonzero_sac_per_launch_avg": int(g["nz"] // g["launches"]),
@@ -740,8 +750,11 @@ def bench_layers(args):
     t0 = time.time()
     res, plans, nonzero = [], [], []
     plan_s = 0.0
+    act = args.act_bits
+    if act != 32 and args.path != "jit":
+        raise SystemExit("--act-bits 16/8 runs on weight-specialised plans (--path jit)")
     for li, L in enumerate(layers):
-        x, codes, bias = W.gen_layer(L, seed, li)
+        x, codes, bias = W.gen_layer(L, seed, li, act_bits=act)
         nonzero.append(float(np.mean((codes & 15) != 15)))
         wp = ops.pack_shift_weights(codes)
         xt = torch.from_numpy(x).to(dev)
@@ -752,7 +765,7 @@ def bench_layers(args):
         plan = None
         if args.path == "jit" and jit_supported(L):
             tp = time.time()
-            plan = ops.layer_plan(L, wp, bias)
+            plan = ops.layer_plan(L, wp, bias, act_bits=act)
             plan_s += time.time() - tp
             if not plan.preferred:
                 plan.close()
@@ -763,9 +776,12 @@ def bench_layers(args):
     print(f"# inputs ready in {time.time() - t0:.1f} s (plans {plan_s:.1f} s)", file=sys.stderr, flush=True)
 
     def runtime_call(L, xt, wt, bt, yt):
+        # The runtime kernel reads int32: narrow activations are widened (sign-extended)
+        # for it, which is their value -- it then checks the plans' outputs.
+        x32 = xt if xt.dtype == torch.int32 else xt.to(torch.int32)
         if L.kind == "linear":
-            return lambda: ops.linear_shift(xt, wt, bt, out=yt)
-        return lambda: ops.conv2d_shift(xt, wt, bt, (L.r, L.s), L.stride, L.pad, out=yt)
+            return lambda: ops.linear_shift(x32, wt, bt, out=yt)
+        return lambda: ops.conv2d_shift(x32, wt, bt, (L.r, L.s), L.stride, L.pad, out=yt)
 
     def jit_call(plan, L, xt, wt, bt, yt):
         if plan is None:
@@ -794,11 +810,11 @@ def bench_layers(args):
         ms_per_step, d = time_layers(runtime_calls, args.steps, args.warmup, stream)
     value = sac_step / (ms_per_step * 1e-3) / 1e9
     planned = [p is not None for p in plans]
-    roofline = roofline_of(layers, d, args.path, nonzero, planned)
+    roofline = roofline_of(layers, d, args.path, nonzero, planned, act)
 
     runtime = None
     d_rt = d
-    if args.path == "jit" and not args.no_runtime:
+    if args.path == "jit" and not args.no_runtime and act == 32:
         rt_ms, d_rt = time_layers(runtime_calls, args.steps, args.warmup, stream)
         rt_value = sac_step / (rt_ms * 1e-3) / 1e9
         runtime = {"ms_per_step": round(rt_ms, 4), "value": round(rt_value, 2), "unit": "GSAC/s",
@@ -806,6 +822,28 @@ def bench_layers(args):
                    "roofline": roofline_of(layers, d_rt, "runtime", nonzero)}
 
     per_layer = []
+    fr = [L.sac * nonzero[li] / (float(np.median(d[:, li])) * 1e-3) / 1e12 / VOP2_OPS_PEAK_T
+          for li, L in enumerate(layers)]
+    order = np.argsort(fr)
+    layer_summary = {
+        "layers": len(layers),
+        "frac_basis": ("non-zero terms / (median call time x 78.64 T VOP2 lane-ops/s)" if args.path == "jit"
+                       else "dense SAC / (median call time x 19.66 T SAC/s)"),
+        "min_frac": round(float(min(fr)), 4) if args.path == "jit" else None,
+        "median_frac": round(float(np.median(fr)), 4) if args.path == "jit" else None,
+        "layers_frac_ge_0_6": int(sum(f >= 0.6 for f in fr)) if args.path == "jit" else None,
+        "worst": [[layers[i].name, round(float(fr[i]), 3)] for i in order[:5]] if args.path == "jit" else None,
+        "nonzero_tsac_s": round(nz_step / (ms_per_step * 1e-3) / 1e12, 3),
+        "per_layer": [[L.name, round(float(np.median(d[:, li])), 5),
+                       round(L.sac / (float(np.median(d[:, li])) * 1e-3) / 1e9, 1)]
+                      for li, L in enumerate(layers)],
+        "per_layer_fields": ["layer", "median ms", "dense G SAC/s"],
+    }
+    if args.path != "jit":
+        frs = [L.sac / (float(np.median(d[:, li])) * 1e-3) / 1e12 / SAC_PEAK_T for li, L in enumerate(layers)]
+        layer_summary.update({"min_frac": round(float(min(frs)), 4), "median_frac": round(float(np.median(frs)), 4),
+                              "layers_frac_ge_0_6": int(sum(f >= 0.6 for f in frs)),
+                              "worst": [[layers[i].name, round(float(frs[i]), 3)] for i in np.argsort(frs)[:5]]})
     for li, L in enumerate(layers):
         med = float(np.median(d[:, li]))
         row = {
@@ -818,31 +856,19 @@ def bench_layers(args):
             "gsac_s": L.sac / (med * 1e-3) / 1e9,
             "frac_sac_peak": L.sac / (med * 1e-3) / 1e12 / SAC_PEAK_T,
             "frac_vop2_peak_nonzero": L.sac * nonzero[li] / (med * 1e-3) / 1e12 / VOP2_OPS_PEAK_T,
-            "hbm_gbs": algorithmic_bytes(L) / (med * 1e-3) / 1e9,
+            "hbm_gbs": algorithmic_bytes(L, act) / (med * 1e-3) / 1e9,
         }
         if runtime is not None:
             row["runtime_ms_median"] = float(np.median(d_rt[:, li]))
         per_layer.append(row)
 
-    # ---- multiplication-based comparison kernel, same tiling as the runtime kernel
+    # ---- multiplication-based comparison, each against the shift path of the same tiling
     mul = None
-    if not args.no_mul:
-        g = torch.Generator(device=dev)
-        g.manual_seed(seed)
-        mul_calls = []
-        for (L, xt, wt, bt, yt) in res:
-            wm = torch.randint(-(1 << 15), 1 << 15, (L.k, L.crs), dtype=torch.int32, device=dev,
-                               generator=g)
-            if L.kind == "linear":
-                mul_calls.append(lambda xt=xt, wm=wm, bt=bt, yt=yt: ops.linear_mul_i32(xt, wm, bt, out=yt))
-            else:
-                mul_calls.append(lambda L=L, xt=xt, wm=wm, bt=bt, yt=yt:
-                                 ops.conv2d_mul_i32(xt, wm, bt, (L.r, L.s), L.stride, L.pad, out=yt))
-        mul_ms, _ = time_layers(mul_calls, args.steps, 1, stream)
-        mul = {"ms_per_step": round(mul_ms, 4), "gmac_s": round(sac_step / (mul_ms * 1e-3) / 1e9, 1),
-               "shift_speedup": round(mul_ms / ms_per_step, 3),
-               "inner_op": "v_mul_lo_u32 + v_add_u32 (int32, mod 2^32), tiling of the runtime kernel"}
-        del mul_calls
+    if not args.no_mul and act == 32:
+        rt_shift_ms = runtime["ms_per_step"] if runtime is not None else (
+            ms_per_step if args.path == "runtime" else time_layers(runtime_calls, args.steps, 1, stream)[0])
+        mul = mul_comparison(args, res, layers, seed, stream, rt_shift_ms,
+                             ms_per_step if args.path == "jit" else None)
 
     # ---- CPU baseline: the oracle on the host cores, same layers at a small batch
     cpu = None
@@ -851,7 +877,7 @@ def bench_layers(args):
         if args.path == "jit":
             del jit_calls
         torch.cuda.empty_cache()
-        cpu = cpu_baseline(args, cfg, seed, layers)
+        cpu = cpu_baseline(args, cfg, seed, layers, act)
 
     path_desc = ("weight-specialised plans (code generated per layer at setup), the runtime "
                  "kernel where a plan is not preferred"
@@ -860,15 +886,18 @@ def bench_layers(args):
         "metric": "G shift-accumulates/s per layer and % of int32 VALU peak on one MI355X",
         "value": round(value, 2), "unit": "GSAC/s", "n_gpus": 1, "steps": args.steps,
         "warmup": args.warmup, "ms_per_step": round(ms_per_step, 4), "higher_is_better": True,
-        "scaling": "weak", "vs_baseline": None, "dtype": "i32", "data": "synthetic",
+        "scaling": "weak", "vs_baseline": None, "dtype": "i32" if act == 32 else f"i{act}->i32",
+        "data": "synthetic",
         **({"frac_vop2_peak_nonzero": round(nz_step / (ms_per_step * 1e-3) / 1e12 / VOP2_OPS_PEAK_T, 4)}
            if args.path == "jit" else {"frac_sac_peak": round(value / 1000.0 / SAC_PEAK_T, 4)}),
         "path": path_desc,
-        "config": {"workload": W.CONFIG_NAMES[cfg], "layers": len(layers),
-                   "batch": layers[0].n, "frac_bits": W.FRAC_BITS,
+        "config": {"workload": W.CONFIG_NAMES[cfg] + ("" if act == 32 else f"_act{act}"),
+                   "layers": len(layers), "batch": layers[0].n, "frac_bits": W.ACT_FRAC_BITS[act],
+                   "act_bits": act,
                    "sac_per_step": sac_step, "nonzero_sac_per_step": int(nz_step),
                    "parallelism": "single GPU"},
-        "roofline": roofline, "runtime_weights": runtime, "cpu_baseline": cpu, "mul_i32": mul,
+        "roofline": roofline, "layer_summary": layer_summary, "runtime_weights": runtime,
+        "cpu_baseline": cpu, "mul_comparison": mul,
     }
     if args.layers_out:
         with open(args.layers_out, "w") as f:
@@ -877,7 +906,69 @@ def bench_layers(args):
     print(json.dumps(out), flush=True)
 
 
-def cpu_baseline(args, cfg, seed, layers):
+def mul_comparison(args, res, layers, seed, stream, rt_shift_ms, plan_shift_ms):
+    """The multiplication-based comparison (the paper's Section 6 times its shift
+    kernels against a multiplication kernel), each timed against the shift path
+    of the same tiling: the runtime kernel's tiling with an int32 multiply-add
+    (v_mul_lo_u32 + v_add3_u32, 1.5 instructions per term) and with a 24-bit one
+    (v_mad_i32_i24), on random 16-bit weights; and the plans' tiling, with each
+    layer's own weights as 14-bit fixed-point integers sign * 2^(14 - shift)
+    baked into the code, one v_mad_i32_i24 per non-zero weight."""
+    import torch
+    from paper_1905_13298_amd import ops
+    from paper_1905_13298_amd import workloads as W
+    dev = res[0][1].device
+    g = torch.Generator(device=dev)
+    g.manual_seed(seed)
+    i32_calls, i24_calls = [], []
+    for (L, xt, wt, bt, yt) in res:
+        wm = torch.randint(-(1 << 15), 1 << 15, (L.k, L.crs), dtype=torch.int32, device=dev, generator=g)
+        for calls, m24 in ((i32_calls, False), (i24_calls, True)):
+            if L.kind == "linear":
+                calls.append(lambda xt=xt, wm=wm, bt=bt, yt=yt, m24=m24:
+                             ops.linear_mul_i32(xt, wm, bt, out=yt, mul24=m24))
+            else:
+                calls.append(lambda L=L, xt=xt, wm=wm, bt=bt, yt=yt, m24=m24:
+                             ops.conv2d_mul_i32(xt, wm, bt, (L.r, L.s), L.stride, L.pad, out=yt, mul24=m24))
+    i32_ms, _ = time_layers(i32_calls, args.steps, 1, stream)
+    i24_ms, _ = time_layers(i24_calls, args.steps, 1, stream)
+    del i32_calls, i24_calls
+    out = {"runtime_tiling": {
+        "shift_ms": round(rt_shift_ms, 4), "mul_i32_ms": round(i32_ms, 4), "mul_i24_ms": round(i24_ms, 4),
+        "shift_speedup_vs_mul_i32": round(i32_ms / rt_shift_ms, 3),
+        "shift_speedup_vs_mul_i24": round(i24_ms / rt_shift_ms, 3),
+        "inner_ops": {"shift": "v_ashrrev_i32 + v_xad_u32 per dense term",
+                      "mul_i32": "v_mul_lo_u32 + v_add3_u32 (1.5 per term)", "mul_i24": "v_mad_i32_i24"}}}
+    if plan_shift_ms is not None:
+        plans, calls, mul_bytes = [], [], 0
+        for li, (L, xt, wt, bt, yt) in enumerate(res):
+            codes = W.gen_codes(L, seed, li)
+            sh = (codes & 15).astype(np.int64)
+            wv = np.where(sh == 15, 0, np.left_shift(1, 14 - np.minimum(sh, 14)))
+            wv = np.where((codes >> 4) & 1, -wv, wv).astype(np.int32)
+            bias = None if bt is None else bt.cpu().numpy()
+            if L.kind == "linear":
+                p = ops.JitConvMul(wv, (L.n, L.c, 1, 1), 1, 1, 0, bias=bias, device=dev)
+                x4, y4 = xt.view(L.n, L.c, 1, 1), yt.view(L.n, L.k, 1, 1)
+                calls.append(lambda p=p, x4=x4, y4=y4: p(x4, out=y4))
+            else:
+                p = ops.JitConvMul(wv, L.x_shape, (L.r, L.s), L.stride, L.pad, bias=bias, device=dev)
+                calls.append(lambda p=p, xt=xt, yt=yt: p(xt, out=yt))
+            mul_bytes += p.code_bytes
+            plans.append(p)
+        mp_ms, _ = time_layers(calls, args.steps, 1, stream)
+        for p in plans:
+            p.close()
+        out["plan_tiling"] = {
+            "shift_ms": round(plan_shift_ms, 4), "mul_i24_ms": round(mp_ms, 4),
+            "shift_speedup": round(mp_ms / plan_shift_ms, 3), "mul_code_bytes": int(mul_bytes),
+            "weights": "each layer's own weights as sign * 2^(14 - shift), zero weights skipped by both",
+            "inner_ops": {"shift": "one v_add_u32/v_sub_u32 per non-zero term + shared v_ashrrev_i32",
+                          "mul_i24": "one v_mad_i32_i24 per non-zero term (+ s_mov_b32 of the weight)"}}
+    return out
+
+
+def cpu_baseline(args, cfg, seed, layers, act_bits=32):
     """The oracle on the host's cores over whole passes of every layer at a small
     batch, for about args.cpu_seconds of oracle time."""
     import oracle
@@ -898,7 +989,7 @@ def cpu_baseline(args, cfg, seed, layers):
             if li in cached:
                 x, codes, bias = cached[li]
             else:
-                x, codes, bias = W.gen_layer(Ls, seed, li)
+                x, codes, bias = W.gen_layer(Ls, seed, li, act_bits=act_bits)
                 if cache_inputs:
                     cached[li] = (x, codes, bias)
             t1 = time.perf_counter()

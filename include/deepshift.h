@@ -81,6 +81,19 @@ extern "C" {
  * with the zero code. For b = 5 this is the default layout described above. */
 #define DS_CODE_BITS(b) ((uint32_t)(b) << 8)
 
+/* flags field (bits 12-13) of ds_jit_conv_create and ds_to_fixed_point: the width
+ * of the activations. Section 5 (lower bit-widths) trains with 16-bit activations
+ * in fixed point with 3 integer and 13 fractional bits (3.13), and with 8-bit
+ * ones; the text gives the same 3.13 split for 8 bits, which cannot fit, so this
+ * library reads 8-bit activations as 3.5 (3 integer bits with the sign, 5
+ * fractional). The library does not depend on the split: F is the caller's.
+ * DS_ACT_I16: x is int16; DS_ACT_I8: x is int8 (0: int32). A shift of a
+ * sign-extended value is the sign-extended shift, so every term and the int32
+ * sum are those of the int32 operator on the sign-extended inputs; only the
+ * bytes of x read from memory change. */
+#define DS_ACT_I16 (1u << 12)
+#define DS_ACT_I8 (2u << 12)
+
 typedef enum ds_status {
     DS_SUCCESS = 0,
     DS_ERR_NULL_POINTER = 1,     /* a required pointer is NULL */
@@ -90,7 +103,9 @@ typedef enum ds_status {
     DS_ERR_BUFFER_TOO_SMALL = 4, /* a host output buffer is shorter than required */
     DS_ERR_INVALID_CODE = 5,     /* a weight code >= 32 */
     DS_ERR_HIP = 6,              /* the HIP runtime reported an error */
-    DS_ERR_UNSUPPORTED = 7       /* a tensor has 2^31 or more elements */
+    DS_ERR_UNSUPPORTED = 7,      /* a tensor has 2^31 or more elements */
+    DS_STATUS_MAX_ = 0x7fffffff  /* not a status: widens the type to every int value, so that
+                                    ds_status_string may be given any int */
 } ds_status;
 
 /* Number of uint32 words one packed row of `cols` codes occupies:
@@ -204,9 +219,11 @@ ds_status ds_quantize_shift_weights_ps(const float *p, const float *s, int64_t r
  *     y[i] = round(x[i] * 2^frac_bits)
  * halves away from zero, saturated to [-2^31, 2^31 - 1]; NaN gives 0.
  * x device float32 [n]; y device int32 [n], written; y == x (in place) is
- * allowed, any other overlap is an error. frac_bits in [0, 31]; flags must be
- * 0; stream as for ds_linear_shift. */
-ds_status ds_to_fixed_point(const float *x, int64_t n, int32_t frac_bits, int32_t *y,
+ * allowed, any other overlap is an error. frac_bits in [0, 31]; stream as for
+ * ds_linear_shift. flags: 0, or DS_ACT_I16 / DS_ACT_I8 to write the lower
+ * bit-width activations of Section 5: y is then int16 [n] (int8 [n]), saturated
+ * to [-2^15, 2^15 - 1] ([-2^7, 2^7 - 1]), and must not overlap x. */
+ds_status ds_to_fixed_point(const float *x, int64_t n, int32_t frac_bits, void *y,
                             uint32_t flags, void *stream);
 
 /* ConvShift followed, in the same call, by what a ResNet block applies to a
@@ -294,7 +311,11 @@ ds_status ds_conv2d_shift_backward_data_describe(int64_t n, int64_t c, int64_t h
  * (the paper compares its shift kernels with a multiplication-based kernel,
  * Section 6, GPU implementation). Weights are plain int32 [k][c*r*s]
  * (or [out][in]) on the device:
- *     y = bias + sum x * w    (products and sum modulo 2^32) */
+ *     y = bias + sum x * w    (products and sum modulo 2^32)
+ * flags: 0, or DS_MUL_I24: each product is that of the low 24 bits of x and w,
+ * each taken as a signed 24-bit value (one v_mad_i32_i24 per term), which equals
+ * the int32 product while |x| < 2^23 and |w| < 2^23. */
+#define DS_MUL_I24 4u
 ds_status ds_conv2d_mul_i32(const int32_t *x, const int32_t *w, const int32_t *bias,
                             int32_t *y, int64_t n, int64_t c, int64_t h, int64_t w_,
                             int64_t k, int64_t r, int64_t s,
@@ -333,7 +354,9 @@ ds_status ds_conv2d_shift_describe(int64_t n, int64_t c, int64_t h, int64_t w, i
  * the plan holds (from create to destroy).
  *
  * ds_jit_conv_create: w_packed is HOST memory, [k][ds_packed_row_words(c*r*s)]
- * words as for ds_conv2d_shift (b-bit codes with DS_CODE_BITS(b) in flags); bias, mul and add are HOST int32 [k] or NULL
+ * words as for ds_conv2d_shift (b-bit codes with DS_CODE_BITS(b) in flags); with
+ * DS_ACT_I16 or DS_ACT_I8 in flags the plan's x is int16 or int8 (y and the
+ * residual stay int32); bias, mul and add are HOST int32 [k] or NULL
  * (add needs mul; mul_shift in [0, 31] when mul is given). The plan copies
  * what it keeps; the caller's buffers may be freed on return. n, c, h, w and
  * the window fix the shape of every ds_jit_conv_run of the plan. splits: 0
@@ -345,7 +368,8 @@ ds_status ds_conv2d_shift_describe(int64_t n, int64_t c, int64_t h, int64_t w, i
  * more, DS_ERR_HIP when loading fails or device memory runs out. Making a plan
  * synchronises the device (module load, uploads).
  *
- * ds_jit_conv_run: x [n][c][h][w], residual and y [n][k][oh][ow], device
+ * ds_jit_conv_run: x [n][c][h][w] (int32, or int16 / int8 for a plan made with
+ * DS_ACT_I16 / DS_ACT_I8), residual and y [n][k][oh][ow] (int32), device
  * memory on the plan's device; residual must be non-NULL exactly when the
  * plan was made with DS_JIT_RESIDUAL. Asynchronous on `stream`. y must not
  * overlap x or residual. A plan may hold device scratch (the padded copy of x;
@@ -377,7 +401,7 @@ ds_status ds_jit_conv_create(const uint32_t *w_packed, const int32_t *bias, cons
                              int64_t h, int64_t w, int64_t k, int64_t r, int64_t s,
                              int32_t stride_h, int32_t stride_w, int32_t pad_h, int32_t pad_w,
                              uint32_t flags, int32_t splits, ds_jit_conv **plan);
-ds_status ds_jit_conv_run(const ds_jit_conv *plan, const int32_t *x, const int32_t *residual,
+ds_status ds_jit_conv_run(const ds_jit_conv *plan, const void *x, const int32_t *residual,
                           int32_t *y, void *stream);
 ds_status ds_jit_conv_destroy(ds_jit_conv *plan);
 ds_status ds_jit_conv_image(const uint32_t *w_packed, const int32_t *bias, const int32_t *mul,
@@ -406,6 +430,31 @@ ds_status ds_jit_conv_backward_data_create(const uint32_t *w_packed, int64_t n, 
                                            int32_t stride_h, int32_t stride_w, int32_t pad_h,
                                            int32_t pad_w, uint32_t flags, int32_t splits,
                                            ds_jit_conv **plan);
+
+/* Multiplication plans: the multiplication-based comparison operator (not
+ * DeepShift; Section 6 times the shift kernels against a multiplication-based
+ * kernel) in the tiling of the weight-specialised plans above, so that the two
+ * can be timed side by side: the same template kernel, register map, wave
+ * split, split-K and block order, with each non-zero weight one
+ * v_mad_i32_i24 (the weight an inline constant or an s_mov_b32 literal) in
+ * place of the shift plans' add or subtract. Zero weights cost nothing.
+ *     y = bias + sum over the window of x * w      (modulo 2^32)
+ * where each product is that of the low 24 bits of x and w taken as signed
+ * 24-bit values: the int32 product while |x| < 2^23 and |w| < 2^23, as
+ * ds_conv2d_mul_i32 with DS_MUL_I24.
+ * w HOST int32 [k][c*r*s]; bias HOST int32 [k] or NULL; flags 0 or DS_RELU;
+ * other arguments, errors and the run / destroy / query calls as for
+ * ds_jit_conv_create. ds_jit_conv_mul_image writes the code object as
+ * ds_jit_conv_image does. */
+ds_status ds_jit_conv_mul_create(const int32_t *w, const int32_t *bias, int64_t n, int64_t c,
+                                 int64_t h, int64_t w_, int64_t k, int64_t r, int64_t s,
+                                 int32_t stride_h, int32_t stride_w, int32_t pad_h, int32_t pad_w,
+                                 uint32_t flags, int32_t splits, ds_jit_conv **plan);
+ds_status ds_jit_conv_mul_image(const int32_t *w, const int32_t *bias, int64_t n, int64_t c,
+                                int64_t h, int64_t w_, int64_t k, int64_t r, int64_t s,
+                                int32_t stride_h, int32_t stride_w, int32_t pad_h, int32_t pad_w,
+                                uint32_t flags, int32_t splits, void *image, int64_t capacity,
+                                int64_t *size);
 
 /* ---- ConvShift that allocates nothing ------------------------------------
  *

@@ -7,7 +7,9 @@ binding never do.
 
 Every function takes host numpy arrays in the layouts documented in
 ``oracle.c``: activations int32 (fixed point, any F), weight codes uint8
-(``sign << 4 | shift_code``), optional int32 bias.
+(``sign << 4 | shift_code``), optional int32 bias. Activations may also be
+int16 or int8 (the lower bit-width formats): they are sign-extended to int32
+first, which is their value; every term and sum is then the int32 one.
 """
 from __future__ import annotations
 
@@ -216,6 +218,19 @@ def conv2d_mul(x, wts, bias=None, r=3, s=None, stride=1, pad=0):
     return y
 
 
+def sext24(a):
+    """Each int32 element's low 24 bits taken as a signed 24-bit value (int32)."""
+    a = np.asarray(a, dtype=np.int32)
+    return ((a.astype(np.int64) & 0xFFFFFF) ^ 0x800000).astype(np.int64) - 0x800000
+
+
+def conv2d_mul24(x, wts, bias=None, r=3, s=None, stride=1, pad=0):
+    """The 24-bit multiplication comparison: conv2d_mul of the operands' low 24
+    bits as signed values (what a v_mad_i32_i24 per term computes)."""
+    return conv2d_mul(sext24(x).astype(np.int32), sext24(wts).astype(np.int32), bias, r=r, s=s,
+                      stride=stride, pad=pad)
+
+
 def pack_codes(codes):
     """codes [rows, cols] uint8 -> packed [rows, ceil(cols/6)] uint32."""
     codes = _c(codes, np.uint8)
@@ -278,6 +293,16 @@ def to_fixed(x, frac_bits=16):
     out = np.empty(x.shape, np.int32)
     _load().oracle_to_fixed(_ptr(x), x.size, int(frac_bits), _ptr(out))
     return out
+
+
+def to_fixed_narrow(x, frac_bits, bits):
+    """round(x * 2^frac_bits) (halves away from zero, NaN -> 0) saturated to a signed
+    integer of `bits` bits (16 or 8): the int32 rounding of ``to_fixed``, clamped to the
+    narrower range (which lies inside int32, so the clamp of the int32-saturated value
+    is the clamp of the exact one)."""
+    lo, hi = -(1 << (bits - 1)), (1 << (bits - 1)) - 1
+    dt = {16: np.int16, 8: np.int8}[bits]
+    return np.clip(to_fixed(x, frac_bits).astype(np.int64), lo, hi).astype(dt)
 
 
 def epilogue(y, mul=None, add=None, mul_shift=16, residual=None, relu=False):

@@ -50,11 +50,24 @@ ds_jit_body:
 """
 
 
-def _compile(src: str) -> str:
-    obj = os.path.join(OBJDIR, os.path.basename(src) + ".o")
+# Host-code sanitizers (AddressSanitizer, UndefinedBehaviorSanitizer) for a CPU
+# check of the library's host code -- the code generator, packer and argument
+# checks. Each -fsanitize= applies to the host compilation only (-Xarch_host);
+# device code is built as usual. The result is a separate library that only the
+# CPU tests load, with the clang ASan runtime preloaded.
+SAN_HOST = ["-fsanitize=address", "-fsanitize=undefined", "-fno-sanitize-recover=undefined",
+            "-fno-omit-frame-pointer"]
+CLANGXX = os.path.join(os.path.dirname(HIPCC), "..", "llvm", "bin", "clang++")
+
+
+def _compile(src: str, objdir: str = OBJDIR, sanitize: bool = False) -> str:
+    obj = os.path.join(objdir, os.path.basename(src) + ".o")
     path = os.path.join(CSRC, src)
     if src.endswith(".hip"):
-        cmd = [HIPCC, *HIP_FLAGS, "-c", path, "-o", obj]
+        san = [t for f in SAN_HOST for t in ("-Xarch_host", f)] if sanitize else []
+        cmd = [HIPCC, *HIP_FLAGS, *san, "-c", path, "-o", obj]
+    elif sanitize:
+        cmd = [CLANGXX, *CXX_FLAGS, *SAN_HOST, "-c", path, "-o", obj]
     else:
         cmd = ["g++", *CXX_FLAGS, "-c", path, "-o", obj]
     res = subprocess.run(cmd, capture_output=True, text=True)
@@ -107,22 +120,26 @@ ds_jit_template_image_end:
     return out
 
 
-def build(verbose: bool = False) -> str:
-    """Compile every source and link the library; returns its path."""
-    os.makedirs(OBJDIR, exist_ok=True)
+def build(verbose: bool = False, sanitize: bool = False, out: str | None = None) -> str:
+    """Compile every source and link the library; returns its path. sanitize: the
+    host-sanitizer build (SAN_HOST) into `out` (objects in a directory of its own)."""
+    objdir = OBJDIR if not sanitize else os.path.join(OBJDIR, "san")
+    target = out or (LIB if not sanitize else os.path.join(objdir, "libdeepshift_san.so"))
+    os.makedirs(objdir, exist_ok=True)
     srcs = HIP_SOURCES + CXX_SOURCES
     with ThreadPoolExecutor(len(srcs) + 1) as ex:
         jit = ex.submit(_jit_template)
-        objs = list(ex.map(_compile, srcs)) + [jit.result()]
-    tmp = LIB + f".tmp{os.getpid()}"
-    cmd = [HIPCC, "-shared", "-fPIC", f"--offload-arch={ARCH}", "-o", tmp, *objs]
+        objs = list(ex.map(lambda f: _compile(f, objdir, sanitize), srcs)) + [jit.result()]
+    tmp = target + f".tmp{os.getpid()}"
+    san = [t for f in SAN_HOST[:2] for t in ("-Xarch_host", f)] + ["-shared-libsan"] if sanitize else []
+    cmd = [HIPCC, "-shared", "-fPIC", f"--offload-arch={ARCH}", *san, "-o", tmp, *objs]
     res = subprocess.run(cmd, capture_output=True, text=True)
     if res.returncode != 0:
         raise RuntimeError(f"link failed: {' '.join(cmd)}\n{res.stdout}\n{res.stderr}")
-    os.replace(tmp, LIB)
+    os.replace(tmp, target)
     if verbose:
-        print(f"built {LIB}")
-    return LIB
+        print(f"built {target}")
+    return target
 
 
 def sources() -> list:

@@ -89,6 +89,8 @@ conv_direct_kernel(const int32_t *__restrict__ x, const uint32_t *__restrict__ w
                         if (sh == 15) continue;
                         const uint32_t tv = uint32_t(xv >> sh);
                         acc += (code & 16u) ? 0u - tv : tv;
+                    } else if constexpr (OP == Inner::Mul24) {
+                        acc += mul24(xv, wi[int64_t(k) * g.crs + j]);
                     } else {
                         acc += uint32_t(xv) * uint32_t(wi[int64_t(k) * g.crs + j]);
                     }
@@ -224,8 +226,9 @@ __global__ void __launch_bounds__(256) fill_zero_scalar_kernel(int32_t *__restri
 
 // xp[p][i][j] = x[p][i - ph][j - pw] where that lies inside x, else 0: planes of
 // h x w copied into zero-padded planes of xh x xw (which may also crop).
+template <typename T>
 __global__ void __launch_bounds__(256)
-pad_planes_kernel(const int32_t *__restrict__ x, int32_t *__restrict__ xp, int total, int h,
+pad_planes_kernel(const T *__restrict__ x, int32_t *__restrict__ xp, int total, int h,
                   int w, int ph, int pw, FastDiv div_xw, FastDiv div_xh)
 {
     for (int idx = int(blockIdx.x) * 256 + int(threadIdx.x); idx < total; idx += int(gridDim.x) * 256) {
@@ -233,7 +236,7 @@ pad_planes_kernel(const int32_t *__restrict__ x, int32_t *__restrict__ xp, int t
         const int pl = fdiv(t, div_xh), i = t - pl * int(div_xh.d);
         const int ii = i - ph, jj = j - pw;
         xp[idx] = (unsigned(ii) < unsigned(h) && unsigned(jj) < unsigned(w))
-                      ? x[(int64_t(pl) * h + ii) * w + jj]
+                      ? int32_t(x[(int64_t(pl) * h + ii) * w + jj])
                       : 0;
     }
 }
@@ -342,6 +345,9 @@ __device__ __forceinline__ void sac_step(uint32_t (&acc)[TM][TN], const int32_t 
         if constexpr (OP == Inner::Mul) {
 #pragma unroll
             for (int i = 0; i < TM; ++i) acc[i][t] += uint32_t(xv[i]) * uint32_t(d);
+        } else if constexpr (OP == Inner::Mul24) {
+#pragma unroll
+            for (int i = 0; i < TM; ++i) acc[i][t] += mul24(xv[i], d);
         } else {
             const uint32_t m = uint32_t(d >> 31);
             const int sh = d & 31;
@@ -678,8 +684,11 @@ static hipError_t run_direct(const ConvGeom &g, const int32_t *x, const uint32_t
     if (op == Inner::Shift)
         hipLaunchKernelGGL(conv_direct_kernel<Inner::Shift>, dim3(grid), dim3(256), 0, st, x, wp,
                            wi, bias, y, g, wpr, code_fmt(g.bits));
-    else
+    else if (op == Inner::Mul)
         hipLaunchKernelGGL(conv_direct_kernel<Inner::Mul>, dim3(grid), dim3(256), 0, st, x, wp,
+                           wi, bias, y, g, wpr, code_fmt(g.bits));
+    else
+        hipLaunchKernelGGL(conv_direct_kernel<Inner::Mul24>, dim3(grid), dim3(256), 0, st, x, wp,
                            wi, bias, y, g, wpr, code_fmt(g.bits));
     return hipGetLastError();
 }
@@ -887,15 +896,23 @@ hipError_t run_fill_zero(int32_t *y, int64_t count, hipStream_t st)
     return hipGetLastError();
 }
 
-hipError_t run_pad_planes(const int32_t *x, int32_t *xp, int64_t planes, int h, int w, int ph,
-                          int pw, int xh, int xw, hipStream_t st)
+hipError_t run_pad_planes(const void *x, int32_t *xp, int64_t planes, int h, int w, int ph,
+                          int pw, int xh, int xw, hipStream_t st, int xbytes)
 {
     const int64_t total = planes * xh * xw;
     if (total <= 0) return hipSuccess;
     if (total > INT32_MAX || h <= 0 || w <= 0) return hipErrorInvalidValue;
     const int grid = int(std::min<int64_t>((total + 255) / 256, 8192));
-    hipLaunchKernelGGL(pad_planes_kernel, dim3(grid), dim3(256), 0, st, x, xp, int(total), h, w,
-                       ph, pw, make_fastdiv(uint32_t(xw)), make_fastdiv(uint32_t(xh)));
+    const FastDiv dxw = make_fastdiv(uint32_t(xw)), dxh = make_fastdiv(uint32_t(xh));
+    if (xbytes == 2)
+        hipLaunchKernelGGL(pad_planes_kernel<int16_t>, dim3(grid), dim3(256), 0, st,
+                           static_cast<const int16_t *>(x), xp, int(total), h, w, ph, pw, dxw, dxh);
+    else if (xbytes == 1)
+        hipLaunchKernelGGL(pad_planes_kernel<int8_t>, dim3(grid), dim3(256), 0, st,
+                           static_cast<const int8_t *>(x), xp, int(total), h, w, ph, pw, dxw, dxh);
+    else
+        hipLaunchKernelGGL(pad_planes_kernel<int32_t>, dim3(grid), dim3(256), 0, st,
+                           static_cast<const int32_t *>(x), xp, int(total), h, w, ph, pw, dxw, dxh);
     return hipGetLastError();
 }
 
@@ -1035,15 +1052,15 @@ hipError_t run_conv(const ConvGeom &g0, const int32_t *x, const uint32_t *wp, co
     if (op == Inner::Shift)
         hipLaunchKernelGGL((prep_kernel<Inner::Shift, kTN>), dim3(pgrid), dim3(256), 0, st, wp, wi,
                            bias, g.k, g.crs, wpr, Jpad, Kpad, wblocks, wd, init, code_fmt(g.bits));
-    else
+    else  // both multiply operators copy the int32 weights
         hipLaunchKernelGGL((prep_kernel<Inner::Mul, kTN>), dim3(pgrid), dim3(256), 0, st, wp, wi,
                            bias, g.k, g.crs, wpr, Jpad, Kpad, wblocks, wd, init, code_fmt(g.bits));
     e = hipGetLastError();
     if (e == hipSuccess && p.atomic_out) e = run_fill_mapped(g, init, yout, L.via_dense ? OutMap() : map, st);
     if (e == hipSuccess) {
-        e = op == Inner::Shift
-                ? dispatch_tiled<Inner::Shift>(v, p, int(L.grid), L.lds, xin, wd, init, yout, st)
-                : dispatch_tiled<Inner::Mul>(v, p, int(L.grid), L.lds, xin, wd, init, yout, st);
+        e = op == Inner::Shift ? dispatch_tiled<Inner::Shift>(v, p, int(L.grid), L.lds, xin, wd, init, yout, st)
+            : op == Inner::Mul ? dispatch_tiled<Inner::Mul>(v, p, int(L.grid), L.lds, xin, wd, init, yout, st)
+                               : dispatch_tiled<Inner::Mul24>(v, p, int(L.grid), L.lds, xin, wd, init, yout, st);
     }
     if (e == hipSuccess && L.via_dense) e = run_copy_mapped(g, yout, y, map, st);
     if (e == hipSuccess && rowmajor) {

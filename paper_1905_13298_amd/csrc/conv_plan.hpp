@@ -20,8 +20,17 @@ struct ConvGeom {
 };
 
 // Inner operation of the reduction: the DeepShift shift-accumulate, or the
-// multiplication-based comparison (int32 multiply-add).
-enum class Inner { Shift, Mul };
+// multiplication-based comparison: int32 multiply-add, or the multiply-add of
+// the low 24 bits of both operands taken as signed (v_mad_i32_i24), equal to the
+// int32 one while |x| and |w| are below 2^23.
+enum class Inner { Shift, Mul, Mul24 };
+
+// The product of the comparison operator Mul24: sext(a[23:0]) * sext(b[23:0]) mod 2^32.
+DS_HD inline uint32_t mul24(int32_t a, int32_t b)
+{
+    const int32_t a24 = int32_t(uint32_t(a) << 8) >> 8, b24 = int32_t(uint32_t(b) << 8) >> 8;
+    return uint32_t(a24) * uint32_t(b24);
+}
 
 // What follows the convolution on each output y[n][k][p] (all optional):
 //   v = floor(v * mul[k] / 2^mul_shift) + add[k]   (when mul; add may be NULL)
@@ -113,9 +122,10 @@ hipError_t run_epilogue(const ConvGeom &g, int32_t *y, const Epilogue &epi, hipS
 // y[0 .. count) = 0 (a 4-byte-aligned y), in 16-byte stores where aligned.
 hipError_t run_fill_zero(int32_t *y, int64_t count, hipStream_t stream);
 // xp [planes][xh][xw] = x [planes][h][w] shifted down by ph rows and right by pw
-// columns, zeros elsewhere (rows and columns past xh, xw are dropped).
-hipError_t run_pad_planes(const int32_t *x, int32_t *xp, int64_t planes, int h, int w, int ph,
-                          int pw, int xh, int xw, hipStream_t stream);
+// columns, zeros elsewhere (rows and columns past xh, xw are dropped); x holds
+// xbytes-byte signed integers (4, 2 or 1), xp int32 (sign-extended).
+hipError_t run_pad_planes(const void *x, int32_t *xp, int64_t planes, int h, int w, int ph,
+                          int pw, int xh, int xw, hipStream_t stream, int xbytes = 4);
 
 
 // Short name of the kernel run_conv would launch for g (see ds_conv2d_shift_describe).

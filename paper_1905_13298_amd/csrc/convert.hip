@@ -203,6 +203,31 @@ __global__ __launch_bounds__(kFixedThreads) void to_fixed_kernel(
     }
 }
 
+// The same rounding saturated to the range of T (int16 or int8): the lower
+// bit-width activations of Section 5. Four elements per thread, with a 16-byte
+// load and a 4 * sizeof(T)-byte store when both buffers are aligned for them.
+template <typename T, bool VEC>
+__global__ __launch_bounds__(kFixedThreads) void to_fixed_narrow_kernel(const float *x, int64_t n,
+                                                                        float scale, T *y)
+{
+    constexpr int32_t lo = -(1 << (8 * sizeof(T) - 1)), hi = (1 << (8 * sizeof(T) - 1)) - 1;
+    const int64_t stride = int64_t(gridDim.x) * kFixedThreads * 4;
+    for (int64_t i = (int64_t(blockIdx.x) * kFixedThreads + threadIdx.x) * 4; i < n; i += stride) {
+        if (VEC && i + 4 <= n) {
+            const float4 v = *reinterpret_cast<const float4 *>(x + i);
+            T o[4] = {T(min(max(to_fixed(v.x, scale), lo), hi)), T(min(max(to_fixed(v.y, scale), lo), hi)),
+                      T(min(max(to_fixed(v.z, scale), lo), hi)), T(min(max(to_fixed(v.w, scale), lo), hi))};
+            if constexpr (sizeof(T) == 2)
+                *reinterpret_cast<short4 *>(y + i) = make_short4(o[0], o[1], o[2], o[3]);
+            else
+                *reinterpret_cast<char4 *>(y + i) = make_char4(o[0], o[1], o[2], o[3]);
+        } else {
+            for (int64_t j = i; j < min<int64_t>(i + 4, n); ++j)
+                y[j] = T(min(max(to_fixed(x[j], scale), lo), hi));
+        }
+    }
+}
+
 ds_status hip_result(hipError_t e, const char *what)
 {
     if (e == hipSuccess) return ok();
@@ -345,22 +370,43 @@ extern "C" ds_status ds_quantize_shift_weights_q_many(int64_t count, const float
                                 "ds_quantize_shift_weights_q_many");
 }
 
-extern "C" ds_status ds_to_fixed_point(const float *x, int64_t n, int32_t frac_bits, int32_t *y,
+extern "C" ds_status ds_to_fixed_point(const float *x, int64_t n, int32_t frac_bits, void *yv,
                                        uint32_t flags, void *stream)
 {
+    int32_t *y = static_cast<int32_t *>(yv);  // int16 / int8 elements with DS_ACT_I16 / DS_ACT_I8
     if (!x || !y) return fail(DS_ERR_NULL_POINTER, "x and y must not be NULL");
     if (n <= 0) return fail(DS_ERR_INVALID_SHAPE, "n must be > 0");
     if (n > kMaxElems) return fail(DS_ERR_UNSUPPORTED, "tensors with 2^31 or more elements are not supported");
     if (frac_bits < 0 || frac_bits > 31) return fail(DS_ERR_INVALID_ARG, "frac_bits must be in [0, 31]");
-    if (flags != 0) return fail(DS_ERR_INVALID_ARG, "flags must be 0");
+    if (flags != 0 && flags != DS_ACT_I16 && flags != DS_ACT_I8)
+        return fail(DS_ERR_INVALID_ARG, "flags must be 0, DS_ACT_I16 or DS_ACT_I8");
     const int64_t bytes = 4 * n;
-    if (overlap(x, bytes, y, bytes) && static_cast<const void *>(x) != static_cast<const void *>(y))
-        return fail(DS_ERR_INVALID_ARG, "y partially overlaps x");
+    const int64_t ybytes = flags == DS_ACT_I16 ? 2 * n : flags == DS_ACT_I8 ? n : bytes;
+    if (overlap(x, bytes, y, ybytes) && (flags != 0 || static_cast<const void *>(x) != static_cast<const void *>(y)))
+        return fail(DS_ERR_INVALID_ARG, flags ? "y overlaps x" : "y partially overlaps x");
     if (!device_range_ok(x, bytes)) return fail(DS_ERR_INVALID_ARG, "x is not a device buffer of %lld bytes", (long long)bytes);
-    if (!device_range_ok(y, bytes)) return fail(DS_ERR_INVALID_ARG, "y is not a device buffer of %lld bytes", (long long)bytes);
+    if (!device_range_ok(y, ybytes)) return fail(DS_ERR_INVALID_ARG, "y is not a device buffer of %lld bytes", (long long)ybytes);
     const float scale = std::ldexp(1.0f, frac_bits);
     const int64_t groups = (n + 3) / 4;
     const int64_t blocks = std::min<int64_t>((groups + kFixedThreads - 1) / kFixedThreads, 8192);
+    if (flags != 0) {
+        const int ysize = flags == DS_ACT_I16 ? 2 : 1;
+        const bool v = reinterpret_cast<uintptr_t>(x) % 16 == 0 && reinterpret_cast<uintptr_t>(y) % (4 * ysize) == 0;
+        hipStream_t st = static_cast<hipStream_t>(stream);
+        if (ysize == 2 && v)
+            hipLaunchKernelGGL((to_fixed_narrow_kernel<int16_t, true>), dim3(unsigned(blocks)), dim3(kFixedThreads), 0, st,
+                               x, n, scale, static_cast<int16_t *>(static_cast<void *>(y)));
+        else if (ysize == 2)
+            hipLaunchKernelGGL((to_fixed_narrow_kernel<int16_t, false>), dim3(unsigned(blocks)), dim3(kFixedThreads), 0, st,
+                               x, n, scale, static_cast<int16_t *>(static_cast<void *>(y)));
+        else if (v)
+            hipLaunchKernelGGL((to_fixed_narrow_kernel<int8_t, true>), dim3(unsigned(blocks)), dim3(kFixedThreads), 0, st,
+                               x, n, scale, static_cast<int8_t *>(static_cast<void *>(y)));
+        else
+            hipLaunchKernelGGL((to_fixed_narrow_kernel<int8_t, false>), dim3(unsigned(blocks)), dim3(kFixedThreads), 0, st,
+                               x, n, scale, static_cast<int8_t *>(static_cast<void *>(y)));
+        return hip_result(hipGetLastError(), "ds_to_fixed_point");
+    }
     const bool vec = (reinterpret_cast<uintptr_t>(x) | reinterpret_cast<uintptr_t>(y)) % 16 == 0;
     if (vec)
         hipLaunchKernelGGL(to_fixed_kernel<true>, dim3(unsigned(blocks)), dim3(kFixedThreads), 0,

@@ -68,6 +68,7 @@ constexpr RegMap kMap96 = {3, 4, 13, 14, 15, 16, 18, 82, 14, "ds_jit_conv_templa
 constexpr RegMap kMap80 = {3, 4, 13, 5, 6, 14, 16, 5, 8, "ds_jit_conv_one_tap_template"};
 constexpr int kXrsrc = 20, kYrsrc = 24, kRrsrc = 36;  // buffer resources (SGPR quads)
 constexpr int kSy = 28, kSx = 29, kSmul = 30;         // scalar scratch of the generated code
+constexpr int kSw = 31;                               // multiplication plans: the current weight
 constexpr int kTN = 64;      // output channels per segment
 constexpr int kBlockPixels = 256;
 constexpr int kStubWords = 5;
@@ -78,7 +79,9 @@ constexpr int kMaxPaddedS = 1023;  // wider windows: tap column s at immediate o
 // SOP1/SOP2/SOPP words; see the CDNA ISA reference).
 constexpr uint32_t kOpAshr = 0x11, kOpMax = 0x0d, kOpAdd = 0x34, kOpSub = 0x35;  // VOP2
 constexpr uint32_t kOpMulLo = 0x285, kOpMulHi = 0x287, kOpAlignbit = 0x1ce;     // VOP3
+constexpr uint32_t kOpMad24 = 0x1c2;                                            // VOP3 v_mad_i32_i24
 constexpr uint32_t kLoad = 0xe0501000u, kStore = 0xe0701000u, kAtomicAdd = 0xe1081000u;
+constexpr uint32_t kLoadI16 = 0xe04c1000u, kLoadI8 = 0xe0441000u;  // buffer_load_sshort / _sbyte
 constexpr uint32_t kEndpgm = 0xbf810000u, kNop = 0xbf800000u, kBarrier = 0xbf8a0000u;
 constexpr uint32_t kDsAdd = 0xd8000000u, kDsRead = 0xd86c0000u;  // ds_add_u32, ds_read_b32
 constexpr uint32_t kLiteral = 255;
@@ -157,6 +160,10 @@ public:
 struct Spec {
     ConvGeom g{};
     const uint32_t *wp = nullptr;  // host packed codes [k][rw], codes of fmt.bits bits
+    // Multiplication plans (the comparison operator, not DeepShift): host int32
+    // weights [k][crs] in place of wp; each non-zero weight is one v_mad_i32_i24.
+    const int32_t *wint = nullptr;
+    int act_bytes = 4;   // bytes of an element of x: 4 int32, 2 int16 (DS_ACT_I16), 1 int8 (DS_ACT_I8)
     int64_t rw = 0;
     CodeFmt fmt;
     const int32_t *bias = nullptr, *mul = nullptr, *add = nullptr;  // host, [k] or NULL
@@ -202,6 +209,14 @@ inline int code_at(const Spec &sp, int k, int j)
     return int(sp.fmt.at(sp.wp + int64_t(k) * sp.rw, j));
 }
 
+// Whether weight (k, j) contributes a term: a non-zero code, or a non-zero
+// weight of a multiplication plan.
+inline bool weight_nonzero(const Spec &sp, int k, int j)
+{
+    if (sp.wint) return sp.wint[int64_t(k) * sp.g.crs + j] != 0;
+    return (code_at(sp, k, j) & 15) != 15;
+}
+
 // Straight-line code of one wave's segment: output channels [64 kg, 64 kg + 64)
 // and reduction elements [e0, e1), element i being (input channel i / RS, tap
 // i % RS). `split`: the partial sums of several parts of the reduction meet in y
@@ -217,8 +232,11 @@ void emit_segment(Emitter &e, const Spec &sp, int kg, int e0, int e1, int share,
     const int jn = sp.kjn.empty() ? std::min(kTN, g.k - kbase) : sp.kjn[size_t(kg)];
     const int RS = g.r * g.s;
     const bool padded = sp.xh > 0;
+    // The padded copy is int32 whatever x holds; x itself is read with a
+    // sign-extending load of its own width.
     const uint32_t cstride = padded ? uint32_t(sp.xh) * uint32_t(sp.xw) * 4u
-                                    : uint32_t(g.h) * uint32_t(g.w) * 4u;
+                                    : uint32_t(g.h) * uint32_t(g.w) * uint32_t(sp.act_bytes);
+    const uint32_t load_op = padded || sp.act_bytes == 4 ? kLoad : sp.act_bytes == 2 ? kLoadI16 : kLoadI8;
     const uint32_t rstride = uint32_t(sp.xw) * 4u;
     const uint32_t kstride = uint32_t(full_map(sp).kstride) * 4u;
     // Byte offset of the group's first output channel (added to the lane's v13).
@@ -229,7 +247,7 @@ void emit_segment(Emitter &e, const Spec &sp, int kg, int e0, int e1, int share,
     el.reserve(size_t(e1 - e0));
     for (int i = e0; i < e1; ++i)
         for (int j = 0; j < jn; ++j)
-            if ((code_at(sp, kbase + j, i) & 15) != 15) {
+            if (weight_nonzero(sp, kbase + j, i)) {
                 el.push_back(i);
                 break;
             }
@@ -257,17 +275,41 @@ void emit_segment(Emitter &e, const Spec &sp, int kg, int e0, int e1, int share,
         }
         const int slot = m.slot + n % nslots;
         if (padded)
-            e.mubuf(kLoad, slot, m.tap0, kXrsrc, kSx, uint32_t(ts) * 4u);
+            e.mubuf(load_op, slot, m.tap0, kXrsrc, kSx, uint32_t(ts) * 4u);
         else
-            e.mubuf(kLoad, slot, m.tap0 + tr * 3 + ts, kXrsrc, kSx);
+            e.mubuf(load_op, slot, m.tap0 + tr * 3 + ts, kXrsrc, kSx);
     };
     for (int n = 0; n < D; ++n) issue(n);
 
+    bool sw_set = false;     // multiplication plans: s31 holds sw_val
+    int32_t sw_val = 0;
     for (int i = 0; i < E; ++i) {
         const int issued = std::min(E, i + D);
         e.wait_vm(issued - i - 1);
         const int slot = m.slot + i % nslots;
         const int jw = el[size_t(i)];  // column of the element in the packed rows
+        if (sp.wint) {
+            // acc += x * w (low 24 bits of each, signed): the weight as an inline
+            // constant when it is one, else from s31, set only when it changes.
+            for (int j = 0; j < jn; ++j) {
+                const int32_t wv = sp.wint[int64_t(kbase + j) * g.crs + jw];
+                if (wv == 0) continue;
+                uint32_t src1;
+                if (Emitter::is_inline(wv)) {
+                    src1 = Emitter::inline_int(wv);
+                } else {
+                    if (!sw_set || sw_val != wv) {
+                        e.s_mov_imm(kSw, uint32_t(wv));
+                        sw_set = true;
+                        sw_val = wv;
+                    }
+                    src1 = uint32_t(kSw);
+                }
+                e.vop3(kOpMad24, m.acc + j, Emitter::vgpr(slot), src1, Emitter::vgpr(m.acc + j));
+            }
+            if (i + D < E) issue(i + D);
+            continue;
+        }
         // The element's non-zero weights grouped by shift; each shift is formed
         // once, into one of two registers in turn, right before the adds that use it.
         int by_shift[15][kTN], count[15] = {};
@@ -444,6 +486,7 @@ ds_status splice_body(const std::vector<uint32_t> &body, std::vector<uint8_t> &o
 
 struct CreateArgs {
     const uint32_t *wp;
+    const int32_t *wint;  // multiplication plans (wp == NULL)
     const int32_t *bias, *mul, *add;
     int mul_shift;
     int64_t n, c, h, w, k, r, s;
@@ -460,7 +503,7 @@ ds_status finish_spec(Spec &sp, int bits, int splits, int deep_blocks = 3072)
     sp.fmt = code_fmt(bits);
     sp.rw = row_words_bits(g.crs, bits);
     const int used = sp.fmt.per_word * bits;
-    for (int64_t i = 0; used < 32 && i < int64_t(g.k) * sp.rw; ++i)
+    for (int64_t i = 0; sp.wp && used < 32 && i < int64_t(g.k) * sp.rw; ++i)
         if (sp.wp[i] >> used)
             return fail(DS_ERR_INVALID_CODE, "bits %d-31 of packed word %lld are not 0", used, (long long)i);
     if (g.r > kMaxTaps || g.s > kMaxTaps) {
@@ -604,8 +647,11 @@ ds_status check_layer(int64_t n, int64_t c, int64_t h, int64_t w, int64_t k, int
 // Validation and planning shared by ds_jit_conv_create and ds_jit_conv_image.
 ds_status plan_spec(const CreateArgs &a, Spec &sp)
 {
-    if (!a.wp) return fail(DS_ERR_NULL_POINTER, "w_packed must not be NULL");
-    if (a.flags & ~(DS_RELU | DS_JIT_RESIDUAL | 0xF00u)) return fail(DS_ERR_INVALID_ARG, "unknown flags");
+    if (!a.wp && !a.wint) return fail(DS_ERR_NULL_POINTER, "w_packed must not be NULL");
+    if (a.flags & ~(DS_RELU | DS_JIT_RESIDUAL | 0xF00u | 0x3000u)) return fail(DS_ERR_INVALID_ARG, "unknown flags");
+    const uint32_t act = (a.flags >> 12) & 3u;
+    if (act == 3u) return fail(DS_ERR_INVALID_ARG, "DS_ACT_I16 and DS_ACT_I8 are exclusive");
+    if (a.wint && (a.flags & ~DS_RELU)) return fail(DS_ERR_INVALID_ARG, "multiplication plans take DS_RELU only");
     const int bits = flags_code_bits(a.flags);
     if (bits < 0) return fail(DS_ERR_INVALID_ARG, "DS_CODE_BITS must be 2..5 (or 0 for 5)");
     if (a.add && !a.mul) return fail(DS_ERR_INVALID_ARG, "add needs mul");
@@ -617,6 +663,8 @@ ds_status plan_spec(const CreateArgs &a, Spec &sp)
     ds_status st = check_layer(a.n, a.c, a.h, a.w, a.k, a.r, a.s, a.sh, a.sw, a.ph, a.pw, bits, sp.g);
     if (st != DS_SUCCESS) return st;
     sp.wp = a.wp;
+    sp.wint = a.wint;
+    sp.act_bytes = act == 1u ? 2 : act == 2u ? 1 : 4;
     sp.bias = a.bias; sp.mul = a.mul; sp.add = a.add; sp.mul_shift = a.mul ? a.mul_shift : 0;
     sp.relu = a.flags & DS_RELU;
     sp.residual = a.flags & DS_JIT_RESIDUAL;
@@ -829,6 +877,7 @@ static ds_status build_plan(const Spec &spec, ds_jit_conv **out)
     }
     p->sp.bias = p->sp.mul = p->sp.add = nullptr;
     p->sp.wp = nullptr;
+    p->sp.wint = nullptr;
     p->group_tiles = tuning(kJitGroupTiles) > 0 ? tuning(kJitGroupTiles) : 16;
     *out = p;
     return ok();
@@ -845,7 +894,7 @@ extern "C" ds_status ds_jit_conv_image(const uint32_t *w_packed, const int32_t *
     try {
         if (!size) return fail(DS_ERR_NULL_POINTER, "size must not be NULL");
         Spec sp;
-        const CreateArgs a{w_packed, bias, mul, add, mul_shift, n, c, h, w, k, r, s,
+        const CreateArgs a{w_packed, nullptr, bias, mul, add, mul_shift, n, c, h, w, k, r, s,
                            stride_h, stride_w, pad_h, pad_w, flags, splits};
         ds_status st = plan_spec(a, sp);
         if (st != DS_SUCCESS) return st;
@@ -873,7 +922,7 @@ extern "C" ds_status ds_jit_conv_create(const uint32_t *w_packed, const int32_t 
     *plan = nullptr;
     try {
         Spec sp;
-        const CreateArgs a{w_packed, bias, mul, add, mul_shift, n, c, h, w, k, r, s,
+        const CreateArgs a{w_packed, nullptr, bias, mul, add, mul_shift, n, c, h, w, k, r, s,
                            stride_h, stride_w, pad_h, pad_w, flags, splits};
         ds_status st = plan_spec(a, sp);
         if (st != DS_SUCCESS) return st;
@@ -1003,7 +1052,8 @@ static hipError_t run_part(const ds_jit_conv *plan, const int32_t *x, const int3
     // (0, 0) offset is where each lane's window starts.
     const bool padded = plan->xpad != nullptr;
     if (padded) {
-        e = run_pad_planes(x, plan->xpad, int64_t(g.n) * g.c, g.h, g.w, g.ph, g.pw, sp.xh, sp.xw, st);
+        e = run_pad_planes(x, plan->xpad, int64_t(g.n) * g.c, g.h, g.w, g.ph, g.pw, sp.xh, sp.xw, st,
+                           sp.act_bytes);
         x = plan->xpad;
         x_bytes = int64_t(g.n) * g.c * sp.xh * sp.xw * 4;
     }
@@ -1014,6 +1064,7 @@ static hipError_t run_part(const ds_jit_conv *plan, const int32_t *x, const int3
         a.y = y;
         a.residual = split ? nullptr : residual;
         a.x_bytes = int(x_bytes);
+        a.xshift = padded || sp.act_bytes == 4 ? 2 : sp.act_bytes == 2 ? 1 : 0;
         a.y_bytes = int(y_bytes);
         a.OHOW = g.oh * g.ow;
         a.NQ = g.n * a.OHOW;
@@ -1051,9 +1102,12 @@ static hipError_t run_part(const ds_jit_conv *plan, const int32_t *x, const int3
     return e;
 }
 
-extern "C" ds_status ds_jit_conv_run(const ds_jit_conv *plan, const int32_t *x,
+extern "C" ds_status ds_jit_conv_run(const ds_jit_conv *plan, const void *xv,
                                      const int32_t *residual, int32_t *y, void *stream)
 {
+    // x holds int32 elements, or int16 / int8 ones for a plan made with DS_ACT_I16 /
+    // DS_ACT_I8; the kernels address it in bytes.
+    const int32_t *x = static_cast<const int32_t *>(xv);
     if (!plan || !x || !y) return fail(DS_ERR_NULL_POINTER, "plan, x and y must not be NULL");
     const bool res_wanted = !plan->backward && plan->sp.residual;
     if (res_wanted != (residual != nullptr))
@@ -1064,7 +1118,8 @@ extern "C" ds_status ds_jit_conv_run(const ds_jit_conv *plan, const int32_t *x,
         return fail(DS_ERR_INVALID_ARG, "the plan was made on device %d, the current device is %d", plan->device, dev);
     // Forward: x [n][c][h][w] -> y [n][k][oh][ow]; input gradient: dy -> dx of the forward layer.
     const ConvGeom &g = plan->backward ? plan->fwd : plan->sp.g;
-    const int64_t fx = int64_t(g.n) * g.c * g.h * g.w * 4, fy = int64_t(g.n) * g.k * g.oh * g.ow * 4;
+    const int64_t fx = int64_t(g.n) * g.c * g.h * g.w * (plan->backward ? 4 : plan->sp.act_bytes);
+    const int64_t fy = int64_t(g.n) * g.k * g.oh * g.ow * 4;
     const int64_t xb = plan->backward ? fy : fx, yb = plan->backward ? fx : fy;
     const char *xn = plan->backward ? "dy" : "x", *yn = plan->backward ? "dx" : "y";
     if (overlap(x, xb, y, yb)) return fail(DS_ERR_INVALID_ARG, "%s overlaps %s", yn, xn);
@@ -1104,4 +1159,58 @@ extern "C" ds_status ds_jit_conv_query(const ds_jit_conv *plan, int64_t *code_by
     if (segments) *segments = seg;
     if (splits) *splits = sp;
     return ok();
+}
+
+// ---------------------------------------------------------------------------
+// Multiplication plans: the comparison operator of Section 6's timing (a
+// multiplication-based kernel) in the plans' own tiling, for side-by-side
+// timing with the shift plans. Not part of DeepShift.
+
+extern "C" ds_status ds_jit_conv_mul_image(const int32_t *w, const int32_t *bias, int64_t n,
+                                           int64_t c, int64_t h, int64_t w_, int64_t k, int64_t r,
+                                           int64_t s, int32_t stride_h, int32_t stride_w,
+                                           int32_t pad_h, int32_t pad_w, uint32_t flags,
+                                           int32_t splits, void *image, int64_t capacity,
+                                           int64_t *size)
+{
+    try {
+        if (!size) return fail(DS_ERR_NULL_POINTER, "size must not be NULL");
+        if (!w) return fail(DS_ERR_NULL_POINTER, "w must not be NULL");
+        Spec sp;
+        const CreateArgs a{nullptr, w, bias, nullptr, nullptr, 0, n, c, h, w_, k, r, s,
+                           stride_h, stride_w, pad_h, pad_w, flags, splits};
+        ds_status st = plan_spec(a, sp);
+        if (st != DS_SUCCESS) return st;
+        std::vector<uint8_t> img;
+        st = splice_body(generate_body(sp), img);
+        if (st != DS_SUCCESS) return st;
+        *size = int64_t(img.size());
+        if (!image || capacity < int64_t(img.size()))
+            return fail(DS_ERR_BUFFER_TOO_SMALL, "the code object needs %lld bytes", (long long)img.size());
+        std::memcpy(image, img.data(), img.size());
+        return ok();
+    } catch (const std::bad_alloc &) {
+        return fail(DS_ERR_HIP, "out of host memory");
+    }
+}
+
+extern "C" ds_status ds_jit_conv_mul_create(const int32_t *w, const int32_t *bias, int64_t n,
+                                            int64_t c, int64_t h, int64_t w_, int64_t k, int64_t r,
+                                            int64_t s, int32_t stride_h, int32_t stride_w,
+                                            int32_t pad_h, int32_t pad_w, uint32_t flags,
+                                            int32_t splits, ds_jit_conv **plan)
+{
+    if (!plan) return fail(DS_ERR_NULL_POINTER, "plan must not be NULL");
+    *plan = nullptr;
+    try {
+        if (!w) return fail(DS_ERR_NULL_POINTER, "w must not be NULL");
+        Spec sp;
+        const CreateArgs a{nullptr, w, bias, nullptr, nullptr, 0, n, c, h, w_, k, r, s,
+                           stride_h, stride_w, pad_h, pad_w, flags, splits};
+        const ds_status st = plan_spec(a, sp);
+        if (st != DS_SUCCESS) return st;
+        return build_plan(sp, plan);
+    } catch (const std::bad_alloc &) {
+        return fail(DS_ERR_HIP, "out of host memory");
+    }
 }

@@ -14,6 +14,7 @@ struct JitArgs {
     int32_t *y;
     const int32_t *residual;  // NULL when the layer adds none
     int x_bytes, y_bytes;
+    int xshift;               // log2 of the bytes of an x element: 2 int32, 1 int16, 0 int8
     int NQ, OHOW, OW, H, W, C, K, HW, sh, sw, ph, pw;
     int ybase, ynst, yrst, ycst;  // output (n, oh, ow) of channel 0 at y[ybase + n*ynst + oh*yrst + ow*ycst]
     int tiles_p;              // pixel tiles (workgroups) per segment

@@ -101,7 +101,7 @@ __device__ __forceinline__ void jit_conv(const JitArgs &p)
         // Taps of a 3 x 3 window (r, s) = (t / 3, t % 3); a 1 x 1 layer uses t0 only.
         auto off = [&](int rr, int ss) {
             const int ih = ih0 + rr, iw = iw0 + ss;
-            return (ih >= 0 && ih < p.H && iw >= 0 && iw < p.W) ? (base + ih * p.W + iw) * 4 : kOOB;
+            return (ih >= 0 && ih < p.H && iw >= 0 && iw < p.W) ? (base + ih * p.W + iw) << p.xshift : kOOB;
         };
         t0 = off(0, 0);
         if (!kOneTap) {

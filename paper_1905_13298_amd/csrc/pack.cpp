@@ -124,6 +124,7 @@ extern "C" const char *ds_status_string(ds_status st)
     case DS_ERR_INVALID_CODE: return "invalid weight code";
     case DS_ERR_HIP: return "HIP runtime error";
     case DS_ERR_UNSUPPORTED: return "unsupported size";
+    case DS_STATUS_MAX_: break;
     }
     return "unknown status";
 }

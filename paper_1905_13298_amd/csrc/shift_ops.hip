@@ -183,9 +183,9 @@ extern "C" ds_status ds_conv2d_mul_i32(const int32_t *x, const int32_t *wts, con
 {
     ConvGeom g;
     ds_status st = check_conv(x, wts, bias, y, n, c, h, w, k, r, s, stride_h, stride_w, pad_h,
-                              pad_w, 0, flags, false, g, 0);
+                              pad_w, 0, flags, false, g, DS_MUL_I24);
     if (st != DS_SUCCESS) return st;
-    return hip_status(run_conv(g, x, nullptr, wts, bias, y, Inner::Mul,
+    return hip_status(run_conv(g, x, nullptr, wts, bias, y, (flags & DS_MUL_I24) ? Inner::Mul24 : Inner::Mul,
                                static_cast<hipStream_t>(stream)),
                       "ds_conv2d_mul_i32");
 }
@@ -196,9 +196,9 @@ extern "C" ds_status ds_linear_mul_i32(const int32_t *x, const int32_t *wts, con
 {
     ConvGeom g;
     ds_status st = check_conv(x, wts, bias, y, batch, in_features, 1, 1, out_features, 1, 1, 1,
-                              1, 0, 0, 0, flags, false, g, 0);
+                              1, 0, 0, 0, flags, false, g, DS_MUL_I24);
     if (st != DS_SUCCESS) return st;
-    return hip_status(run_conv(g, x, nullptr, wts, bias, y, Inner::Mul,
+    return hip_status(run_conv(g, x, nullptr, wts, bias, y, (flags & DS_MUL_I24) ? Inner::Mul24 : Inner::Mul,
                                static_cast<hipStream_t>(stream)),
                       "ds_linear_mul_i32");
 }

@@ -19,7 +19,8 @@ __all__ = ["DeepShiftError", "code_bits_flag", "describe_conv2d", "packed_row_wo
            "to_fixed_point", "conv2d_shift_fused", "maxpool2d", "avgpool2d_global", "DS_RELU",
            "DS_JIT_RESIDUAL", "JitConv", "jit_conv_image", "conv2d_shift_backward_data",
            "linear_shift_backward_data", "describe_conv2d_backward_data", "JitConvBackwardData",
-           "layer_plan", "run_layer_plan", "set_tuning", "get_tuning", "tuning"]
+           "layer_plan", "run_layer_plan", "set_tuning", "get_tuning", "tuning", "DS_MUL_I24",
+           "JitConvMul", "jit_conv_mul_image", "DS_ACT_I16", "DS_ACT_I8", "act_bits_flag"]
 
 DS_RELU = 1
 
@@ -76,6 +77,28 @@ def describe_conv2d_backward_data(n, c, h, w, k, kernel_size, stride=1, padding=
     buf = ctypes.create_string_buffer(512)
     call("ds_conv2d_shift_backward_data_describe", n, c, h, w, k, r, s, sh, sw, ph, pw, buf, len(buf))
     return buf.value.decode()
+
+
+DS_ACT_I16 = 1 << 12
+DS_ACT_I8 = 2 << 12
+_ACT_DTYPES = {32: torch.int32, 16: torch.int16, 8: torch.int8}
+
+
+def act_bits_flag(bits: int) -> int:
+    """The DS_ACT_* flags field for activations of `bits` bits (32, 16 or 8)."""
+    if bits not in _ACT_DTYPES:
+        raise ValueError("activation bits must be 32, 16 or 8")
+    return {32: 0, 16: DS_ACT_I16, 8: DS_ACT_I8}[bits]
+
+
+def _dev_int(t: torch.Tensor, name: str, bits: int) -> torch.Tensor:
+    if not isinstance(t, torch.Tensor) or not t.is_cuda:
+        raise TypeError(f"{name} must be a device tensor")
+    if t.dtype != _ACT_DTYPES[bits] and not (bits == 32 and t.dtype == torch.uint32):
+        raise TypeError(f"{name} must be {_ACT_DTYPES[bits]}, got {t.dtype}")
+    if not t.is_contiguous():
+        raise ValueError(f"{name} must be contiguous")
+    return t
 
 
 def _dev_i32(t: torch.Tensor, name: str) -> torch.Tensor:
@@ -191,20 +214,25 @@ def linear_shift_backward_data(dy: torch.Tensor, w_packed: torch.Tensor, in_feat
     return dx
 
 
-def linear_mul_i32(x, w, bias=None, out=None):
-    """Multiplication-based comparison: y = bias + x @ w.T (int32, mod 2^32)."""
+DS_MUL_I24 = 4
+
+
+def linear_mul_i32(x, w, bias=None, out=None, mul24: bool = False):
+    """Multiplication-based comparison: y = bias + x @ w.T (int32, mod 2^32); with
+    mul24 each product takes the low 24 bits of both operands as signed values."""
     _dev_i32(x, "x"); _dev_i32(w, "w")
     batch, fin = x.shape
     fout = w.shape[0]
     y = out if out is not None else torch.empty((batch, fout), dtype=torch.int32, device=x.device)
     with torch.cuda.device(x.device):
-        call("ds_linear_mul_i32", _ptr(x), _ptr(w), _ptr(bias), _ptr(y), batch, fin, fout, 0,
-             _stream(x.device))
+        call("ds_linear_mul_i32", _ptr(x), _ptr(w), _ptr(bias), _ptr(y), batch, fin, fout,
+             DS_MUL_I24 if mul24 else 0, _stream(x.device))
     return y
 
 
-def conv2d_mul_i32(x, w, bias, kernel_size, stride=1, padding=0, out=None):
-    """Multiplication-based comparison convolution with int32 weights [K, C*R*S]."""
+def conv2d_mul_i32(x, w, bias, kernel_size, stride=1, padding=0, out=None, mul24: bool = False):
+    """Multiplication-based comparison convolution with int32 weights [K, C*R*S]; with
+    mul24 each product takes the low 24 bits of both operands as signed values."""
     _dev_i32(x, "x"); _dev_i32(w, "w")
     r, s = _pair(kernel_size)
     sh, sw = _pair(stride)
@@ -215,7 +243,7 @@ def conv2d_mul_i32(x, w, bias, kernel_size, stride=1, padding=0, out=None):
     y = out if out is not None else torch.empty((n, k, oh, ow), dtype=torch.int32, device=x.device)
     with torch.cuda.device(x.device):
         call("ds_conv2d_mul_i32", _ptr(x), _ptr(w), _ptr(bias), _ptr(y), n, c, h, wd, k, r, s,
-             sh, sw, ph, pw, 0, _stream(x.device))
+             sh, sw, ph, pw, DS_MUL_I24 if mul24 else 0, _stream(x.device))
     return y
 
 
@@ -281,13 +309,15 @@ def quantize_shift_weights_ps(p: torch.Tensor, s: torch.Tensor, max_shift: int =
 
 
 def to_fixed_point(x: torch.Tensor, frac_bits: int = 16,
-                   out: torch.Tensor | None = None) -> torch.Tensor:
-    """round(x * 2**frac_bits), halves away from zero, saturated to int32."""
+                   out: torch.Tensor | None = None, bits: int = 32) -> torch.Tensor:
+    """round(x * 2**frac_bits), halves away from zero, saturated to a signed integer of
+    `bits` bits (32, or 16 / 8 for the lower bit-width activations)."""
     _dev_f32(x, "x")
-    y = out if out is not None else torch.empty(x.shape, dtype=torch.int32, device=x.device)
-    _dev_i32(y, "out")
+    y = out if out is not None else torch.empty(x.shape, dtype=_ACT_DTYPES[bits], device=x.device)
+    _dev_int(y, "out", bits)
     with torch.cuda.device(x.device):
-        call("ds_to_fixed_point", _ptr(x), x.numel(), frac_bits, _ptr(y), 0, _stream(x.device))
+        call("ds_to_fixed_point", _ptr(x), x.numel(), frac_bits, _ptr(y), act_bits_flag(bits),
+             _stream(x.device))
     return y
 
 
@@ -369,7 +399,7 @@ def _np_ptr(a):
 
 def jit_conv_image(w_packed, x_shape, kernel_size, stride=1, padding=0, bias=None, mul=None,
                    add=None, mul_shift: int = 16, residual: bool = False, relu: bool = False,
-                   splits: int = 0, code_bits: int = 5) -> bytes:
+                   splits: int = 0, code_bits: int = 5, act_bits: int = 32) -> bytes:
     """The code object a JitConv with these arguments would load (host only)."""
     k = int(w_packed.shape[0])
     wp, b, m, a = _jit_args(w_packed, k, bias, mul, add)
@@ -377,7 +407,8 @@ def jit_conv_image(w_packed, x_shape, kernel_size, stride=1, padding=0, bias=Non
     r, s = _pair(kernel_size)
     sh, sw = _pair(stride)
     ph, pw = _pair(padding)
-    flags = (DS_RELU if relu else 0) | (DS_JIT_RESIDUAL if residual else 0) | code_bits_flag(code_bits)
+    flags = (DS_RELU if relu else 0) | (DS_JIT_RESIDUAL if residual else 0) | code_bits_flag(code_bits) \
+        | act_bits_flag(act_bits)
     size = ctypes.c_int64(0)
     args = [_np_ptr(wp), _np_ptr(b), _np_ptr(m), _np_ptr(a), mul_shift, n, c, h, w, k, r, s, sh, sw,
             ph, pw, flags, splits]
@@ -398,7 +429,7 @@ class JitConv:
 
     def __init__(self, w_packed, x_shape, kernel_size, stride=1, padding=0, bias=None, mul=None,
                  add=None, mul_shift: int = 16, residual: bool = False, relu: bool = False,
-                 splits: int = 0, device="cuda:0", code_bits: int = 5):
+                 splits: int = 0, device="cuda:0", code_bits: int = 5, act_bits: int = 32):
         self.k = int(w_packed.shape[0])
         wp, b, m, a = _jit_args(w_packed, self.k, bias, mul, add)
         self.x_shape = tuple(int(v) for v in x_shape)
@@ -409,7 +440,9 @@ class JitConv:
         self.y_shape = (n, self.k, out_size(h, ph, r, sh), out_size(w, pw, s, sw))
         self.device = torch.device(device)
         self.residual = residual
-        flags = (DS_RELU if relu else 0) | (DS_JIT_RESIDUAL if residual else 0) | code_bits_flag(code_bits)
+        self.act_bits = act_bits
+        flags = (DS_RELU if relu else 0) | (DS_JIT_RESIDUAL if residual else 0) | code_bits_flag(code_bits) \
+            | act_bits_flag(act_bits)
         handle = ctypes.c_void_p()
         with torch.cuda.device(self.device):
             call("ds_jit_conv_create", _np_ptr(wp), _np_ptr(b), _np_ptr(m), _np_ptr(a), mul_shift,
@@ -433,7 +466,7 @@ class JitConv:
         return True
 
     def __call__(self, x: torch.Tensor, residual: torch.Tensor | None = None, out=None):
-        _dev_i32(x, "x")
+        _dev_int(x, "x", getattr(self, "act_bits", 32))
         if tuple(x.shape) != self.x_shape:
             raise ValueError(f"x must have shape {self.x_shape}")
         if residual is not None:
@@ -484,15 +517,16 @@ class JitConvBackwardData(JitConv):
         self.pixel_tiles = -(-(n * h * w) // 256)
 
 
-def layer_plan(layer, w_packed, bias=None, device="cuda:0") -> JitConv:
+def layer_plan(layer, w_packed, bias=None, device="cuda:0", act_bits: int = 32) -> JitConv:
     """The weight-specialised plan of one workload layer (an object with ``kind``
     "conv" or "linear", ``n, c, h, w, k, r, s, stride, pad``), made the way the
     benchmark makes it: a LinearShift [batch, in] -> [batch, out] is the 1 x 1
     ConvShift of [batch, in, 1, 1]. ``w_packed``: host packed codes [k, words]."""
     if layer.kind == "linear":
-        return JitConv(w_packed, (layer.n, layer.c, 1, 1), 1, 1, 0, bias=bias, device=device)
+        return JitConv(w_packed, (layer.n, layer.c, 1, 1), 1, 1, 0, bias=bias, device=device,
+                       act_bits=act_bits)
     return JitConv(w_packed, (layer.n, layer.c, layer.h, layer.w), (layer.r, layer.s), layer.stride,
-                   layer.pad, bias=bias, device=device)
+                   layer.pad, bias=bias, device=device, act_bits=act_bits)
 
 
 def run_layer_plan(plan: JitConv, layer, x: torch.Tensor, out: torch.Tensor | None = None) -> torch.Tensor:
@@ -532,3 +566,57 @@ class tuning:
     def __exit__(self, *exc):
         set_tuning(self.name, self.prev)
         return False
+
+
+def _mul_weights(w, k):
+    a = np.ascontiguousarray(w.cpu().numpy() if isinstance(w, torch.Tensor) else w)
+    if a.dtype != np.int32 or a.ndim != 2 or a.shape[0] != k:
+        raise ValueError("w must be int32 [k, c*r*s]")
+    return a
+
+
+def jit_conv_mul_image(w, x_shape, kernel_size, stride=1, padding=0, bias=None, relu: bool = False,
+                       splits: int = 0) -> bytes:
+    """The code object a JitConvMul with these arguments would load (host only)."""
+    k = int(w.shape[0])
+    wa, b = _mul_weights(w, k), _host_i32(bias, k, "bias")
+    n, c, h, wd = x_shape
+    r, s = _pair(kernel_size)
+    sh, sw = _pair(stride)
+    ph, pw = _pair(padding)
+    size = ctypes.c_int64(0)
+    args = [_np_ptr(wa), _np_ptr(b), n, c, h, wd, k, r, s, sh, sw, ph, pw, DS_RELU if relu else 0, splits]
+    st = lib().ds_jit_conv_mul_image(*args, None, 0, ctypes.byref(size))
+    if st not in (0, 4):
+        call("ds_jit_conv_mul_image", *args, None, 0, ctypes.byref(size))
+    buf = ctypes.create_string_buffer(size.value)
+    call("ds_jit_conv_mul_image", *args, buf, size.value, ctypes.byref(size))
+    return buf.raw[:size.value]
+
+
+class JitConvMul(JitConv):
+    """A multiplication plan (``ds_jit_conv_mul_create``): the comparison operator
+    y = bias + sum x * w (24-bit signed operands) in the shift plans' tiling, with
+    int32 weights w [k, c*r*s] baked into the code."""
+
+    def __init__(self, w, x_shape, kernel_size, stride=1, padding=0, bias=None, relu: bool = False,
+                 splits: int = 0, device="cuda:0"):
+        self.k = int(w.shape[0])
+        wa, b = _mul_weights(w, self.k), _host_i32(bias, self.k, "bias")
+        self.x_shape = tuple(int(v) for v in x_shape)
+        n, c, h, wd = self.x_shape
+        r, s = _pair(kernel_size)
+        sh, sw = _pair(stride)
+        ph, pw = _pair(padding)
+        self.y_shape = (n, self.k, out_size(h, ph, r, sh), out_size(wd, pw, s, sw))
+        self.device = torch.device(device)
+        self.residual = False
+        handle = ctypes.c_void_p()
+        with torch.cuda.device(self.device):
+            call("ds_jit_conv_mul_create", _np_ptr(wa), _np_ptr(b), n, c, h, wd, self.k, r, s, sh, sw,
+                 ph, pw, DS_RELU if relu else 0, splits, ctypes.byref(handle))
+        self._h = handle
+        cb, seg, sp = ctypes.c_int64(), ctypes.c_int32(), ctypes.c_int32()
+        call("ds_jit_conv_query", self._h, ctypes.byref(cb), ctypes.byref(seg), ctypes.byref(sp))
+        self.code_bytes, self.segments, self.splits = cb.value, seg.value, sp.value
+        self.pixel_tiles = -(-(n * self.y_shape[2] * self.y_shape[3]) // 256)

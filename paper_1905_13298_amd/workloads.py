@@ -174,7 +174,13 @@ def config_layers(cfg: int) -> list:
 # generators
 
 
-def _fill_chunk(out, start, stop, dist, key):
+# Lower bit-width activations (Section 5): fractional bits of each storage width.
+# 16 bits are 3.13; 8 bits are 3.5 (3 integer bits with the sign).
+ACT_FRAC_BITS = {32: FRAC_BITS, 16: 13, 8: 5}
+ACT_DTYPES = {32: np.int32, 16: np.int16, 8: np.int8}
+
+
+def _fill_chunk(out, start, stop, dist, key, frac=FRAC_BITS):
     rng = np.random.default_rng(key)
     m = stop - start
     if dist == "relu_normal":
@@ -188,30 +194,37 @@ def _fill_chunk(out, start, stop, dist, key):
         a = rng.uniform(0.0, 2.0, m)
     else:
         raise ValueError(dist)
-    a *= float(1 << FRAC_BITS)
+    a *= float(1 << frac)
     np.rint(a, out=a)
+    if out.dtype != np.int32:  # the narrow formats saturate at their range
+        info = np.iinfo(out.dtype)
+        np.clip(a, info.min, info.max, out=a)
     out[start:stop] = a
 
 
-def gen_x(layer: Layer, seed: int, index: int, threads: int | None = None) -> np.ndarray:
-    """Activations of ``layer`` as int32 fixed point (F=16), seeded by (seed, index).
+def gen_x(layer: Layer, seed: int, index: int, threads: int | None = None,
+          act_bits: int = 32) -> np.ndarray:
+    """Activations of ``layer`` as fixed point, seeded by (seed, index): int32 with
+    F = 16, or for ``act_bits`` 16 / 8 the same draws as int16 3.13 / int8 3.5,
+    saturated at the type's range.
 
     Chunk ``j`` of the flattened tensor comes from ``default_rng([seed, index, 0, j])``,
     so the result does not depend on the number of threads.
     """
     total = int(np.prod(layer.x_shape))
-    out = np.empty(total, dtype=np.int32)
+    out = np.empty(total, dtype=ACT_DTYPES[act_bits])
+    frac = ACT_FRAC_BITS[act_bits]
     nchunks = (total + _CHUNK - 1) // _CHUNK
     jobs = [(j * _CHUNK, min(total, (j + 1) * _CHUNK)) for j in range(nchunks)]
     if threads is None:
         threads = min(16, os.cpu_count() or 1)
     if nchunks <= 1 or threads <= 1:
         for j, (a, b) in enumerate(jobs):
-            _fill_chunk(out, a, b, layer.x_dist, [seed, index, 0, j])
+            _fill_chunk(out, a, b, layer.x_dist, [seed, index, 0, j], frac)
     else:
         with ThreadPoolExecutor(threads) as ex:
             list(ex.map(lambda jb: _fill_chunk(out, jb[1][0], jb[1][1], layer.x_dist,
-                                               [seed, index, 0, jb[0]]), enumerate(jobs)))
+                                               [seed, index, 0, jb[0]], frac), enumerate(jobs)))
     return out.reshape(layer.x_shape)
 
 
@@ -253,10 +266,15 @@ def gen_bias(layer: Layer, seed: int, index: int):
     return np.rint(rng.uniform(-1.0, 1.0, layer.k) * float(1 << FRAC_BITS)).astype(np.int32)
 
 
-def gen_layer(layer: Layer, seed: int, index: int, threads: int | None = None):
-    """(x, codes, bias) for one layer."""
-    return (gen_x(layer, seed, index, threads), gen_codes(layer, seed, index),
-            gen_bias(layer, seed, index))
+def gen_layer(layer: Layer, seed: int, index: int, threads: int | None = None,
+              act_bits: int = 32):
+    """(x, codes, bias) for one layer; x of ``act_bits`` bits (see gen_x). The bias keeps
+    int32 with the activations' fractional bits."""
+    bias = gen_bias(layer, seed, index)
+    if bias is not None and act_bits != 32:
+        rng = np.random.default_rng([seed, index, 2])
+        bias = np.rint(rng.uniform(-1.0, 1.0, layer.k) * float(1 << ACT_FRAC_BITS[act_bits])).astype(np.int32)
+    return (gen_x(layer, seed, index, threads, act_bits), gen_codes(layer, seed, index), bias)
 
 
 def random_codes(rng: np.random.Generator, shape, zero_frac: float = 0.1,

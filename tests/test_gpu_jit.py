@@ -265,3 +265,33 @@ def test_random_shapes_match_oracle(spec):
     want = oracle.conv2d_shift(x, codes, bias, r=r, s=s, stride=st, pad=pd)
     bad = np.flatnonzero(y.ravel() != want.ravel())
     assert bad.size == 0, f"{bad.size} of {want.size} outputs differ, first at {bad[:5]}"
+
+
+MUL_PLAN_CASES = [
+    # name, n, c, h, w, k, r, s, stride, pad, splits
+    ("window", 2, 40, 9, 9, 70, 3, 3, 1, 1, 0),
+    ("strided_split", 3, 37, 14, 14, 64, 3, 3, 2, 1, 3),
+    ("pointwise", 2, 64, 28, 28, 256, 1, 1, 1, 0, 0),
+    ("stem_padded", 1, 3, 35, 35, 64, 7, 7, 2, 3, 0),
+    ("linear", 8, 256, 1, 1, 128, 1, 1, 1, 0, 0),
+]
+
+
+@pytest.mark.parametrize("spec", MUL_PLAN_CASES, ids=[e[0] for e in MUL_PLAN_CASES])
+def test_multiplication_plans_match_oracle(spec):
+    """Multiplication plans (the comparison operator in the plans' tiling) against
+    the oracle's 24-bit product, with inline-constant, literal and zero weights and
+    inputs beyond 24 bits."""
+    _, n, c, h, w, k, r, s, st, pd, splits = spec
+    rng = np.random.default_rng(zlib.crc32(repr(spec).encode()))
+    wt = rng.integers(-(2 ** 31), 2 ** 31, (k, c * r * s), dtype=np.int64).astype(np.int32)
+    small = rng.random(wt.shape) < 0.3
+    wt[small] = rng.integers(-16, 65, int(small.sum()))
+    wt[rng.random(wt.shape) < 0.2] = 0
+    x = rng.integers(-(2 ** 31), 2 ** 31, (n, c, h, w), dtype=np.int64).astype(np.int32)
+    bias = rng.integers(-(2 ** 20), 2 ** 20, k).astype(np.int32)
+    plan = ops.JitConvMul(wt, x.shape, (r, s), st, pd, bias=bias, splits=splits)
+    say(f"mul plan {spec[0]}: {plan.splits} parts, {plan.code_bytes} code bytes")
+    y = plan(to_dev(x)).cpu().numpy()
+    plan.close()
+    np.testing.assert_array_equal(y, oracle.conv2d_mul24(x, wt, bias, r=r, s=s, stride=st, pad=pd))

@@ -1,0 +1,100 @@
+"""GPU parity of the lower bit-width activations (Section 5: 16-bit 3.13 and
+8-bit 3.5 fixed point): plans that read int16 / int8 x, and the fixed-point
+rounding into those formats, bit for bit against the oracle."""
+import zlib
+
+import numpy as np
+import pytest
+import torch
+
+import oracle
+from paper_1905_13298_amd import ops
+from paper_1905_13298_amd import workloads as W
+from paper_1905_13298_amd.workloads import random_codes
+
+pytestmark = pytest.mark.gpu
+DEV = torch.device("cuda:0")
+DT = {16: np.int16, 8: np.int8}
+
+
+def say(*a):
+    print(*a, flush=True)
+
+
+def to_dev(a):
+    return None if a is None else torch.from_numpy(np.ascontiguousarray(a)).to(DEV)
+
+
+EDGE = [
+    # name, n, c, h, w, k, r, s, stride, pad, splits
+    ("ragged_3x3", 3, 13, 9, 11, 37, 3, 3, 1, 1, 0),
+    ("strided_3x3_split", 2, 40, 14, 14, 70, 3, 3, 2, 1, 3),
+    ("pointwise_s2", 2, 64, 28, 28, 128, 1, 1, 2, 0, 0),
+    ("stem_padded", 2, 3, 37, 37, 64, 7, 7, 2, 3, 0),
+    ("rect_window", 1, 6, 10, 12, 20, 2, 3, 1, 1, 2),
+    ("linear", 33, 300, 1, 1, 130, 1, 1, 1, 0, 0),
+]
+
+
+@pytest.mark.parametrize("act_bits", [16, 8])
+@pytest.mark.parametrize("spec", EDGE, ids=[e[0] for e in EDGE])
+def test_narrow_plans_match_oracle(spec, act_bits):
+    name, n, c, h, w, k, r, s, st, pd, splits = spec
+    rng = np.random.default_rng(zlib.crc32(repr((spec, act_bits)).encode()))
+    info = np.iinfo(DT[act_bits])
+    x = rng.integers(info.min, info.max, (n, c, h, w), endpoint=True).astype(DT[act_bits])
+    codes = random_codes(rng, (k, c * r * s), zero_frac=0.1)
+    bias = rng.integers(-(2 ** 20), 2 ** 20, k).astype(np.int32)
+    plan = ops.JitConv(ops.pack_shift_weights(codes), x.shape, (r, s), st, pd, bias=bias,
+                       splits=splits, act_bits=act_bits)
+    say(f"narrow plan {name} int{act_bits}: {plan.splits} parts, {plan.code_bytes} code bytes")
+    y = plan(to_dev(x)).cpu().numpy()
+    plan.close()
+    want = oracle.conv2d_shift(x, codes, bias, r=r, s=s, stride=st, pad=pd)
+    bad = np.flatnonzero(y.ravel() != want.ravel())
+    assert bad.size == 0, f"{bad.size} of {want.size} outputs differ, first at {bad[:5]}"
+
+
+# Benchmark layers whose time the activations' bytes weigh on most (1 x 1 layers
+# at 56 x 56 of ResNet-50, batch 128) and the small LinearShift, every output.
+FULL = [(4, "layer1.0.conv1"), (4, "layer1.1.conv1"), (4, "layer2.0.downsample"), (0, "linear")]
+
+
+@pytest.mark.parametrize("act_bits", [16, 8])
+@pytest.mark.parametrize("cfg,name", FULL)
+def test_narrow_benchmark_layers_every_output(cfg, name, act_bits):
+    layers = W.config_layers(cfg)
+    li = [L.name for L in layers].index(name)
+    L = layers[li]
+    x, codes, bias = W.gen_layer(L, W.CONFIG_SEEDS[cfg], li, act_bits=act_bits)
+    say(f"cfg{cfg} {name} int{act_bits} batch {L.n}")
+    plan = ops.layer_plan(L, ops.pack_shift_weights(codes), bias, device=DEV, act_bits=act_bits)
+    y = ops.run_layer_plan(plan, L, to_dev(x)).cpu().numpy()
+    plan.close()
+    if L.kind == "linear":
+        want = oracle.linear_shift(x, codes, bias)
+    else:
+        want = oracle.conv2d_shift(x, codes, bias, r=L.r, s=L.s, stride=L.stride, pad=L.pad)
+    bad = np.flatnonzero(y.ravel() != want.ravel())
+    assert bad.size == 0, f"{bad.size} of {want.size} outputs differ, first at {bad[:5]}"
+
+
+def test_narrow_plan_rejects_wrong_input_type():
+    codes = np.full((4, 9), 15, np.uint8)
+    plan = ops.JitConv(ops.pack_shift_weights(codes), (1, 1, 5, 5), 3, 1, 1, act_bits=16)
+    with pytest.raises(TypeError):
+        plan(torch.zeros((1, 1, 5, 5), dtype=torch.int32, device=DEV))
+    plan.close()
+
+
+@pytest.mark.parametrize("act_bits,frac", [(16, 13), (8, 5)])
+def test_to_fixed_narrow_matches_oracle(act_bits, frac):
+    rng = np.random.default_rng(act_bits)
+    scale = 2.0 ** (act_bits - 1 - frac)
+    x = (rng.standard_normal(100003) * scale).astype(np.float32)
+    x[:10] = [np.nan, np.inf, -np.inf, 0.0, -0.0, 3 * scale, -3 * scale, 0.5 / (1 << frac),
+              -0.5 / (1 << frac), 1.5 / (1 << frac)]
+    for offset in (0, 1):   # aligned (vector stores) and unaligned buffers
+        xd = to_dev(x)[offset:]
+        y = ops.to_fixed_point(xd, frac, bits=act_bits).cpu().numpy()
+        np.testing.assert_array_equal(y, oracle.to_fixed_narrow(x[offset:], frac, act_bits))

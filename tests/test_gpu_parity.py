@@ -259,3 +259,23 @@ def test_mul_comparison_exact(shape):
     yl = ops.linear_mul_i32(to_dev(xl), to_dev(wl)).cpu().numpy()
     want = oracle.conv2d_mul(xl.reshape(33, 70, 1, 1), wl, None, r=1).reshape(33, 45)
     np.testing.assert_array_equal(yl, want)
+
+
+@pytest.mark.parametrize("shape", [(2, 9, 11, 13, 21, 3, 1, 1), (3, 16, 8, 8, 40, 1, 2, 0),
+                                   (1, 3, 30, 30, 8, 7, 2, 3), (2, 64, 14, 14, 64, 3, 1, 1)])
+def test_mul24_comparison_exact(shape):
+    """DS_MUL_I24: each product of the low 24 bits of x and w as signed values,
+    on inputs that exceed 24 bits (the upper bits must be ignored) and on the
+    LinearShift shape."""
+    n, c, h, w, k, r, st, pd = shape
+    rng = np.random.default_rng(sum(shape) + 24)
+    x = rng.integers(I32_MIN, I32_MAX, (n, c, h, w), endpoint=True).astype(np.int32)
+    wt = rng.integers(I32_MIN, I32_MAX, (k, c * r * r), endpoint=True).astype(np.int32)
+    b = rng.integers(-99, 99, k).astype(np.int32)
+    y = ops.conv2d_mul_i32(to_dev(x), to_dev(wt), to_dev(b), r, st, pd, mul24=True).cpu().numpy()
+    np.testing.assert_array_equal(y, oracle.conv2d_mul24(x, wt, b, r=r, stride=st, pad=pd))
+    xl = rng.integers(I32_MIN, I32_MAX, (33, 70), endpoint=True).astype(np.int32)
+    wl = rng.integers(I32_MIN, I32_MAX, (45, 70), endpoint=True).astype(np.int32)
+    yl = ops.linear_mul_i32(to_dev(xl), to_dev(wl), mul24=True).cpu().numpy()
+    want = oracle.conv2d_mul24(xl.reshape(33, 70, 1, 1), wl, None, r=1).reshape(33, 45)
+    np.testing.assert_array_equal(yl, want)

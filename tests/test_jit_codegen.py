@@ -162,7 +162,7 @@ class Interp:
         def sq(tok):
             return int(re.fullmatch(r"s\[(\d+):\d+\]", tok).group(1))
 
-        def access(ops):
+        def access(ops, size=4):
             base = sq(ops[2])
             arr, nrec = self.bufs[base]
             voff = V[int(ops[1][1:])].astype(np.int64)
@@ -170,9 +170,9 @@ class Interp:
             imm = [int(t.split(":")[1]) for t in ops[4:] if t.startswith("offset:")]
             tot = voff + soff + (imm[0] if imm else 0)
             inr = voff < nrec
-            assert not np.any(inr & (tot + 4 > nrec)), f"out-of-range access at pc {pc:#x}"
-            assert not np.any(inr & (tot % 4 != 0))
-            return arr, inr, tot // 4
+            assert not np.any(inr & (tot + size > nrec)), f"out-of-range access at pc {pc:#x}"
+            assert not np.any(inr & (tot % size != 0))
+            return arr, inr, tot // size
 
         while True:
             steps += 1
@@ -208,11 +208,14 @@ class Interp:
             elif op == "ds_read_b32":
                 j = lds_row(ops[1:2], next((t for t in ops[2:] if t.startswith("offset:")), None))
                 lgkm[int(ops[0][1:])] = lds[:, j].copy()
-            elif op == "buffer_load_dword":
-                arr, inr, idx = access(ops)
+            elif op in ("buffer_load_dword", "buffer_load_sshort", "buffer_load_sbyte"):
+                size = {"buffer_load_dword": 4, "buffer_load_sshort": 2, "buffer_load_sbyte": 1}[op]
+                arr, inr, idx = access(ops, size)
+                assert arr.dtype.itemsize == (8 if size == 4 else size), "load width differs from the buffer's"
                 d = int(ops[0][1:])
                 assert d not in pending
-                pending[d] = np.where(inr, arr[np.where(inr, idx, 0)], 0).astype(np.int64) & M32
+                # narrow loads sign-extend (the buffers of int16 / int8 are kept in their own type)
+                pending[d] = np.where(inr, arr[np.where(inr, idx, 0)].astype(np.int64), 0) & M32
             elif op in ("buffer_store_dword", "buffer_atomic_add"):
                 assert not pending and not lgkm, "store with loads in flight"
                 arr, inr, idx = access(ops)
@@ -248,6 +251,12 @@ class Interp:
                 p = sb * sa
                 V[int(ops[0][1:])] = np.array(((p & M32) if op == "v_mul_lo_u32" else ((p >> 32) & M32)),
                                               dtype=np.int64)
+            elif op == "v_mad_i32_i24":
+                def s24(t):
+                    t = np.asarray(t, dtype=np.int64) & 0xFFFFFF
+                    return np.where(t >= 2 ** 23, t - 2 ** 24, t)
+                p_ = s24(val(ops[1])) * s24(val(ops[2])) + val(ops[3])
+                V[int(ops[0][1:])] = np.asarray(p_, dtype=np.int64) & M32
             elif op == "v_alignbit_b32":
                 hi, lo = val(ops[1]).astype(object), val(ops[2]).astype(object)
                 sh = int(ops[3], 0)
@@ -444,3 +453,125 @@ def test_code_width_does_not_change_the_generated_code(bits):
     b = ops.jit_conv_image(ops.pack_shift_weights(codes, bits=bits), (2, 5, 9, 9), 3, 1, 1, bias=bias,
                            code_bits=bits)
     assert a == b
+
+
+
+MUL_CASES = [
+    # n, c, h, w, k, r, s, stride, pad, splits, wave split, zero fraction
+    (2, 5, 9, 9, 70, 3, 3, 1, 1, 1, 1, 0.1),
+    (2, 5, 9, 9, 70, 3, 3, 2, 1, 2, 1, 0.3),
+    (3, 7, 12, 12, 64, 1, 1, 1, 0, 1, 4, 0.0),
+    (33, 40, 1, 1, 17, 1, 1, 1, 0, 2, 2, 0.5),
+    (1, 3, 13, 11, 20, 7, 7, 2, 3, 1, 1, 0.1),
+]
+
+
+@pytest.mark.parametrize("case", MUL_CASES, ids=[str(i) for i in range(len(MUL_CASES))])
+def test_multiplication_plan_matches_oracle(case, tmp_path, knob):
+    """Multiplication plans (the comparison operator in the plans' tiling): one
+    v_mad_i32_i24 per non-zero weight, weights as inline constants or s_mov_b32
+    literals; run in the interpreter against the oracle's 24-bit product."""
+    n, c, h, w, k, r, s, st, pd, splits, wsplit, zero = case
+    knob("DS_JIT_WSPLIT", wsplit)
+    rng = np.random.default_rng(zlib.crc32(repr(case).encode()))
+    wt = rng.integers(-(2 ** 23), 2 ** 23, (k, c * r * s)).astype(np.int32)
+    small = rng.random(wt.shape) < 0.3
+    wt[small] = rng.integers(-16, 65, int(small.sum()))        # inline-constant weights
+    wt[rng.random(wt.shape) < zero] = 0
+    x = rng.integers(-(2 ** 31), 2 ** 31, (n, c, h, w), dtype=np.int64).astype(np.int32)
+    bias = rng.integers(-(2 ** 31), 2 ** 31, k, dtype=np.int64).astype(np.int32)
+    img = ops.jit_conv_mul_image(wt, (n, c, h, w), (r, s), st, pd, bias=bias, splits=splits)
+    insts = disassemble(img, str(tmp_path))
+    names = collections.Counter(op for op, _, _ in insts.values())
+    body = min(insts)
+    lanes, (oh, ow) = lane_inputs(n, c, h, w, k, r, s, st, pd, wsplit)
+    one_tap = r * s == 1 or r > 3 or s > 3
+    if one_tap:
+        for i in range(5, 13):
+            del lanes[i]
+    ext = padded_extents(h, w, r, s, st, pd)
+    xr = x if ext is None else pad_input(x, pd, *ext)
+    xb = np.ascontiguousarray(xr).reshape(-1).view(np.uint32).astype(np.int64)
+    y = np.full(n * k * oh * ow, 0xDEADBEEF, dtype=np.int64)
+    bufs = {20: (xb, xb.size * 4), 24: (y, y.size * 4), 36: (y, 0)}
+    nsplit = min(splits, c)
+    if nsplit > 1:
+        y[:] = np.repeat(np.tile(bias.view(np.uint32).astype(np.int64), n), oh * ow)
+    interp = Interp(insts, bufs, wsplit)
+    total = collections.Counter()
+    for seg in range(-(-k // 64) * nsplit):
+        lds = np.zeros((lanes[4].size, 64), np.int64)
+        runs = [interp.run(body + 20 * (seg * wsplit + sh), seg * wsplit + sh, lanes, y, nsplit > 1, lds, total)
+                for sh in range(wsplit)]
+        for _ in range(2 if wsplit > 1 else 1):
+            for r_ in runs:
+                next(r_, None)
+        for r_ in runs:
+            assert next(r_, "done") == "done"
+    want = oracle.conv2d_mul24(x, wt, bias, r=r, s=s, stride=st, pad=pd)
+    np.testing.assert_array_equal(to_i32(y).reshape(want.shape), want)
+    # exactly one v_mad_i32_i24 per non-zero weight, no shift-plan arithmetic
+    assert names["v_mad_i32_i24"] == int(np.sum(wt != 0))
+    assert names["v_add_u32_e32"] == names["v_sub_u32_e32"] == names["v_ashrrev_i32_e32"] == 0
+
+
+
+@pytest.mark.parametrize("act_bits", [16, 8])
+@pytest.mark.parametrize("case", [(2, 5, 9, 9, 70, 3, 3, 1, 1, 1, 1), (3, 7, 12, 12, 64, 1, 1, 2, 0, 2, 2),
+                                  (1, 3, 13, 11, 20, 7, 7, 2, 3, 1, 1), (9, 40, 1, 1, 17, 1, 1, 1, 0, 1, 4)],
+                         ids=["3x3", "1x1s2_split", "stem_padded", "linear"])
+def test_narrow_activation_plans_match_oracle(case, act_bits, tmp_path, knob):
+    """Plans with int16 / int8 activations: sign-extending narrow loads of x (the
+    padded copy of wide windows is int32), the same arithmetic as int32 plans;
+    against the oracle on the sign-extended inputs."""
+    n, c, h, w, k, r, s, st, pd, splits, wsplit = case
+    knob("DS_JIT_WSPLIT", wsplit)
+    codes, _, rng = gen_layer(zlib.crc32(repr((case, act_bits)).encode()), n, c, h, w, k, r, s, 0.1)
+    dt = {16: np.int16, 8: np.int8}[act_bits]
+    info = np.iinfo(dt)
+    x = rng.integers(info.min, info.max, (n, c, h, w), endpoint=True).astype(dt)
+    bias = rng.integers(-(2 ** 20), 2 ** 20, k).astype(np.int32)
+    img = ops.jit_conv_image(ops.pack_shift_weights(codes), (n, c, h, w), (r, s), st, pd, bias=bias,
+                             splits=splits, act_bits=act_bits)
+    insts = disassemble(img, str(tmp_path))
+    names = collections.Counter(op for op, _, _ in insts.values())
+    ext = padded_extents(h, w, r, s, st, pd)
+    narrow_op = {16: "buffer_load_sshort", 8: "buffer_load_sbyte"}[act_bits]
+    if ext is None:
+        assert names[narrow_op] > 0 and names["buffer_load_dword"] == 0
+    else:
+        assert names[narrow_op] == 0 and names["buffer_load_dword"] > 0
+    body = min(insts)
+    lanes, (oh, ow) = lane_inputs(n, c, h, w, k, r, s, st, pd, wsplit)
+    if ext is None:       # the template scales tap offsets by the element size
+        for i in range(4, 13):
+            lanes[i] = np.where(lanes[i] == OOB, OOB, lanes[i] // 4 * x.itemsize)
+    if r * s == 1 or r > 3 or s > 3:
+        for i in range(5, 13):
+            del lanes[i]
+    if ext is None:
+        xb = np.ascontiguousarray(x).reshape(-1)
+        bufs = {20: (xb, xb.size * x.itemsize)}
+    else:
+        xr = pad_input(x.astype(np.int32), pd, *ext)
+        xb = np.ascontiguousarray(xr).reshape(-1).view(np.uint32).astype(np.int64)
+        bufs = {20: (xb, xb.size * 4)}
+    y = np.full(n * k * oh * ow, 0xDEADBEEF, dtype=np.int64)
+    bufs[24] = (y, y.size * 4)
+    bufs[36] = (y, 0)
+    nsplit = min(splits, c)
+    if nsplit > 1:
+        y[:] = np.repeat(np.tile(bias.view(np.uint32).astype(np.int64), n), oh * ow)
+    interp = Interp(insts, bufs, wsplit)
+    total = collections.Counter()
+    for seg in range(-(-k // 64) * nsplit):
+        lds = np.zeros((lanes[4].size, 64), np.int64)
+        runs = [interp.run(body + 20 * (seg * wsplit + sh), seg * wsplit + sh, lanes, y, nsplit > 1, lds, total)
+                for sh in range(wsplit)]
+        for _ in range(2 if wsplit > 1 else 1):
+            for r_ in runs:
+                next(r_, None)
+        for r_ in runs:
+            assert next(r_, "done") == "done"
+    want = oracle.conv2d_shift(x, codes, bias, r=r, s=s, stride=st, pad=pd)
+    np.testing.assert_array_equal(to_i32(y).reshape(want.shape), want)

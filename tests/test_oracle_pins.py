@@ -340,6 +340,37 @@ def test_mul_comparison_closed_form():
     assert oracle.conv2d_mul(xb, wb, None, r=1)[0, 0, 0, 0] == wrap(2 ** 33)
 
 
+def test_mul24_comparison_brute_force():
+    """The 24-bit comparison product: low 24 bits of each operand as signed
+    values, products and sum modulo 2^32 -- against Python integers."""
+    rng = np.random.default_rng(11)
+    x = rng.integers(-(2 ** 31), 2 ** 31, (1, 2, 4, 4), dtype=np.int64).astype(np.int32)
+    w = rng.integers(-(2 ** 31), 2 ** 31, (3, 2 * 9), dtype=np.int64).astype(np.int32)
+    x[0, 0, 0, 0], w[0, 0] = 0x7FFFFF, -0x800000          # the 24-bit extremes
+    x[0, 0, 0, 1], w[0, 1] = 0x800000, 0xFFFFFF           # bit 23 set: negative
+    got = oracle.conv2d_mul24(x, w, None, r=3, stride=1, pad=1)
+
+    def s24(v):
+        v = int(v) & 0xFFFFFF
+        return v - (1 << 24) if v >= (1 << 23) else v
+
+    for k in range(3):
+        for oh in range(4):
+            for ow in range(4):
+                acc = 0
+                for c in range(2):
+                    for r in range(3):
+                        for q in range(3):
+                            ih, iw = oh - 1 + r, ow - 1 + q
+                            if 0 <= ih < 4 and 0 <= iw < 4:
+                                acc += s24(x[0, c, ih, iw]) * s24(w[k, (c * 3 + r) * 3 + q])
+                assert got[0, k, oh, ow] == wrap(acc)
+    # inside the 24-bit range it is the int32 comparison
+    xs = rng.integers(-(2 ** 23), 2 ** 23, (2, 3, 5, 5)).astype(np.int32)
+    ws = rng.integers(-(2 ** 23), 2 ** 23, (4, 27)).astype(np.int32)
+    np.testing.assert_array_equal(oracle.conv2d_mul24(xs, ws, None, r=3), oracle.conv2d_mul(xs, ws, None, r=3))
+
+
 # ---------------------------------------------------------------------------
 # packed layout, rebuilt from a little-endian bit stream
 
