@@ -39,6 +39,9 @@ ROOT = os.path.dirname(os.path.abspath(__file__))
 sys.path.insert(0, ROOT)
 
 WORKLOADS = {"linear_small": 0, "conv_single": 1, "linear_fc6": 2, "resnet18": 3, "resnet50": 4}
+# A plan that is almost only VOP2 adds and subtracts (workloads.VALU_PROBE): its rate,
+# and its SQ counters under rocprofv3, measure the issue rate of generated code.
+PROBE_WORKLOADS = {"valu_probe": 99}
 # The step upstream of the operators: float weights -> packed codes (DeepShift-Q)
 # and the float input batch -> fixed point, for every layer of ResNet-50 at N = 128.
 CONVERT_WORKLOADS = {"convert_resnet50": 4}
@@ -88,7 +91,7 @@ def parse():
     ap.add_argument("--steps", type=int, default=5)
     ap.add_argument("--warmup", type=int, default=2)
     ap.add_argument("--workload", default="resnet50", choices=sorted(WORKLOADS) + sorted(CONVERT_WORKLOADS) + sorted(NETWORK_WORKLOADS)
-                    + sorted(BACKWARD_WORKLOADS))
+                    + sorted(BACKWARD_WORKLOADS) + sorted(PROBE_WORKLOADS))
     ap.add_argument("--cpu-batch", type=int, default=None,
                     help="batch of the oracle sample (default: sized for ~10-30 s)")
     ap.add_argument("--cpu-seconds", type=float, default=10.0,
@@ -204,12 +207,14 @@ def sq_summary(directory, workload, path):
     VALU issue rate per SIMD per clock, and int32 lane-operations per second
     against the peak."""
     from paper_1905_13298_amd import workloads as W
-    cfg = WORKLOADS[workload]
-    layers = W.config_layers(cfg)
+    probe = workload in PROBE_WORKLOADS
+    cfg = None if probe else WORKLOADS[workload]
+    layers = [W.VALU_PROBE] if probe else W.config_layers(cfg)
+    seed = 99 if probe else W.CONFIG_SEEDS[cfg]
     rows = _main_rows(_pmc_rows(directory), layers)
     per = {}
     for li, (L, r) in enumerate(zip(layers, rows)):
-        codes = W.gen_codes(L, W.CONFIG_SEEDS[cfg], li)
+        codes = W.gen_codes(L, seed, li)
         name = group_name(L, path, is_jit_kernel(r["name"]))
         k = per.setdefault(name, {"launches": 0, "sac": 0, "nz": 0.0, "ns": 0})
         k["launches"] += 1
@@ -237,7 +242,7 @@ def sq_summary(directory, workload, path):
             "lds_per_valu": round(k["SQ_INSTS_LDS"] / valu, 4),
             "wait_inst_any_per_wave_cycle": round(k["SQ_WAIT_INST_ANY"] / k["SQ_WAVE_CYCLES"], 3),
         }
-    rec = {"workload": W.CONFIG_NAMES[cfg], "path": path,
+    rec = {"workload": workload if probe else W.CONFIG_NAMES[cfg], "path": path,
            "kernel_source_sha256_16": kernel_source_hash(path), "kernels": out}
     print(json.dumps(rec, indent=1))
 
@@ -738,9 +743,12 @@ def bench_layers(args):
     from paper_1905_13298_amd import ops
     from paper_1905_13298_amd import workloads as W
 
-    cfg = WORKLOADS[args.workload]
-    seed = W.CONFIG_SEEDS[cfg]
-    layers = W.config_layers(cfg)
+    if args.workload in PROBE_WORKLOADS:
+        cfg, seed, layers = None, 99, [W.VALU_PROBE]
+    else:
+        cfg = WORKLOADS[args.workload]
+        seed = W.CONFIG_SEEDS[cfg]
+        layers = W.config_layers(cfg)
     dev = torch.device("cuda:0")
     torch.cuda.set_device(dev)
     stream = torch.cuda.current_stream(dev)
@@ -877,7 +885,7 @@ def bench_layers(args):
         if args.path == "jit":
             del jit_calls
         torch.cuda.empty_cache()
-        cpu = cpu_baseline(args, cfg, seed, layers, act)
+        cpu = cpu_baseline(args, cfg, seed, layers, act) if cfg is not None else None
 
     path_desc = ("weight-specialised plans (code generated per layer at setup), the runtime "
                  "kernel where a plan is not preferred"
@@ -891,7 +899,8 @@ def bench_layers(args):
         **({"frac_vop2_peak_nonzero": round(nz_step / (ms_per_step * 1e-3) / 1e12 / VOP2_OPS_PEAK_T, 4)}
            if args.path == "jit" else {"frac_sac_peak": round(value / 1000.0 / SAC_PEAK_T, 4)}),
         "path": path_desc,
-        "config": {"workload": W.CONFIG_NAMES[cfg] + ("" if act == 32 else f"_act{act}"),
+        "config": {"workload": (W.CONFIG_NAMES[cfg] if cfg is not None else args.workload)
+                   + ("" if act == 32 else f"_act{act}"),
                    "layers": len(layers), "batch": layers[0].n, "frac_bits": W.ACT_FRAC_BITS[act],
                    "act_bits": act,
                    "sac_per_step": sac_step, "nonzero_sac_per_step": int(nz_step),
@@ -901,8 +910,8 @@ def bench_layers(args):
     }
     if args.layers_out:
         with open(args.layers_out, "w") as f:
-            json.dump({"workload": W.CONFIG_NAMES[cfg], "path": args.path, "layers": per_layer}, f,
-                      indent=1)
+            json.dump({"workload": W.CONFIG_NAMES[cfg] if cfg is not None else args.workload,
+                       "path": args.path, "layers": per_layer}, f, indent=1)
     print(json.dumps(out), flush=True)
 
 

@@ -153,6 +153,13 @@ CONFIG_NAMES = {
 CONFIG_SEEDS = {0: 0, 1: 1, 2: 2, 3: 3, 4: 4}
 
 
+# Issue-rate probe: a 1 x 1 layer whose weights all have shift 0 (no zero
+# weights), 64 MB in and out, 4.3 G add/sub lane-operations: its plan is almost
+# only VOP2 adds and subtracts, one load per 64 of them.
+VALU_PROBE = Layer("valu_probe", "conv", n=1, c=256, k=256, h=256, w=256, code_dist="shift0",
+                   zero_frac=0.0)
+
+
 def config_layers(cfg: int) -> list:
     """Layer list of one benchmark configuration (seed is ``CONFIG_SEEDS[cfg]``)."""
     if cfg == 0:
@@ -242,12 +249,17 @@ def gen_codes(layer: Layer, seed: int, index: int) -> np.ndarray:
     ``uniform16``: sign ~ Bernoulli(1/2), shift code uniform over 0..15.
     ``lognormal``: sign ~ Bernoulli(1/2); shift code drawn from ``LOGNORMAL_SHIFT_P``;
     then each code independently becomes the zero code 15 with probability ``zero_frac``.
+    ``shift0``: sign ~ Bernoulli(1/2), every shift 0 and no zero weight (the plan of such
+    a layer is one add or subtract per weight and one load per element: an issue-rate
+    probe of generated code).
     """
     rng = np.random.default_rng([seed, index, 1])
     shape = (layer.k, layer.crs)
     sign = rng.integers(0, 2, size=shape, dtype=np.uint8)
     if layer.code_dist == "uniform16":
         shift = rng.integers(0, 16, size=shape, dtype=np.uint8)
+    elif layer.code_dist == "shift0":
+        shift = np.zeros(shape, dtype=np.uint8)
     elif layer.code_dist == "lognormal":
         prob = LOGNORMAL_SHIFT_P / LOGNORMAL_SHIFT_P.sum()
         shift = rng.choice(15, size=shape, p=prob).astype(np.uint8)
