@@ -69,7 +69,7 @@ constexpr RegMap kMap80 = {3, 4, 13, 5, 6, 14, 16, 5, 8, "ds_jit_conv_one_tap_te
 constexpr int kXrsrc = 20, kYrsrc = 24, kRrsrc = 36;  // buffer resources (SGPR quads)
 constexpr int kSy = 28, kSx = 29, kSmul = 30;         // scalar scratch of the generated code
 constexpr int kSw = 31;                               // multiplication plans: the current weight
-constexpr int kTN = 64;      // output channels per segment
+constexpr int kTN = 64;      // output channels per segment (at most; see Spec::tn)
 constexpr int kBlockPixels = 256;
 constexpr int kStubWords = 5;
 constexpr int kMaxTaps = 3;  // R, S <= 3: the template computes a 3 x 3 window of taps
@@ -177,10 +177,14 @@ struct Spec {
     // window then starts at one offset and every tap sits at a uniform distance
     // from it. Zero: x itself, with per-tap offsets from the template.
     int xh = 0, xw = 0;
-    // Waves per 64 pixels (1, 2 or 4), each with a contiguous share of every
-    // part's reduction elements, meeting in LDS; a workgroup covers 256 / wsplit
-    // pixels.
+    // Waves per 64 pixels (1, 2, 4, 8 or 16), each with a contiguous share of
+    // every part's reduction elements, meeting in LDS; a workgroup covers
+    // 256 / wsplit pixels (64 from a split of 4 up, with 4 x ... x 16 waves).
     int wsplit = 1;
+    // Output channels per segment: 64, or 32 / 16 on grids too small to fill the
+    // chip (more segments, each with less code, at the price of forming each
+    // shift for fewer channels).
+    int tn = kTN;
     // Fused stride phases of an input gradient: output-channel group kg stores
     // its first channel at element kout[kg] + (pixel's map offset) and has kjn[kg]
     // channels (empty: group kg stores channel 64 kg + j at its map offset).
@@ -217,6 +221,33 @@ inline bool weight_nonzero(const Spec &sp, int k, int j)
     return (code_at(sp, k, j) & 15) != 15;
 }
 
+// Instruction words of the code of all segments of an unsplit plan with `tn`
+// output channels per segment (shift codes): per element with a non-zero weight
+// in the group, its load, wait and offset update (5 words), a word per distinct
+// non-zero shift and a word per non-zero weight; per segment its accumulator
+// set-up and epilogue (about 3 words per channel and 16 more).
+int64_t code_words(const Spec &sp, int tn)
+{
+    const ConvGeom &g = sp.g;
+    int64_t words = 0;
+    for (int kb = 0; kb < g.k; kb += tn) {
+        const int jn = std::min(tn, g.k - kb);
+        for (int i = 0; i < g.crs; ++i) {
+            uint32_t shifts = 0;
+            int nz = 0;
+            for (int j = 0; j < jn; ++j) {
+                const int code = code_at(sp, kb + j, i);
+                if ((code & 15) == 15) continue;
+                ++nz;
+                shifts |= 1u << (code & 15);
+            }
+            if (nz) words += 5 + nz + __builtin_popcount(shifts & ~1u);
+        }
+        words += 3 * jn + 16;
+    }
+    return words;
+}
+
 // Straight-line code of one wave's segment: output channels [64 kg, 64 kg + 64)
 // and reduction elements [e0, e1), element i being (input channel i / RS, tap
 // i % RS). `split`: the partial sums of several parts of the reduction meet in y
@@ -224,12 +255,12 @@ inline bool weight_nonzero(const Spec &sp, int k, int j)
 // afterwards, as separate passes). With a wave split W = sp.wsplit > 1, the W
 // waves sharing 64 pixels run shares 0..W-1 of a part's elements: each adds its
 // 64 sums into LDS, waits for the others at a barrier and finishes channels
-// [64 share / W, 64 (share + 1) / W) of the totals.
+// [tn share / W, tn (share + 1) / W) of the totals (tn: channels per segment).
 void emit_segment(Emitter &e, const Spec &sp, int kg, int e0, int e1, int share, bool split)
 {
     const ConvGeom &g = sp.g;
-    const int kbase = kg * kTN;
-    const int jn = sp.kjn.empty() ? std::min(kTN, g.k - kbase) : sp.kjn[size_t(kg)];
+    const int kbase = kg * sp.tn;
+    const int jn = sp.kjn.empty() ? std::min(sp.tn, g.k - kbase) : sp.kjn[size_t(kg)];
     const int RS = g.r * g.s;
     const bool padded = sp.xh > 0;
     // The padded copy is int32 whatever x holds; x itself is read with a
@@ -342,8 +373,8 @@ void emit_segment(Emitter &e, const Spec &sp, int kg, int e0, int e1, int share,
         for (int j = 0; j < jn; ++j) e.ds_add(m.lds, m.acc + j, uint32_t(j) * 256u);
         e.wait_lgkm0();
         e.w.push_back(kBarrier);
-        j0 = std::min(jn, share * kTN / sp.wsplit);
-        j1 = std::min(jn, (share + 1) * kTN / sp.wsplit);
+        j0 = std::min(jn, share * sp.tn / sp.wsplit);
+        j1 = std::min(jn, (share + 1) * sp.tn / sp.wsplit);
         for (int j = j0; j < j1; ++j) e.ds_read(m.acc + j, m.lds, uint32_t(j) * 256u);
         e.wait_lgkm0();
     }
@@ -517,7 +548,13 @@ ds_status finish_spec(Spec &sp, int bits, int splits, int deep_blocks = 3072)
         sp.xw = int(xw);
     }
     const int64_t nq = int64_t(g.n) * g.oh * g.ow;
-    sp.kgroups = (g.k + kTN - 1) / kTN;
+    // Channels per segment: 64, unless forced (fused input-gradient phases keep
+    // their own groups of 64).
+    {
+        const int forced = tuning(kJitTn);
+        sp.tn = sp.kjn.empty() && (forced == 16 || forced == 32) ? forced : kTN;
+    }
+    sp.kgroups = (g.k + sp.tn - 1) / sp.tn;
     // One tap per element (1 x 1 windows, or wider ones through the padded copy):
     // the 80-VGPR entry point, 6 waves per SIMD instead of 5.
     sp.one_tap = (int64_t(g.r) * g.s == 1 || sp.xh > 0) && tuning(kJitMap) != 96;
@@ -542,9 +579,11 @@ ds_status finish_spec(Spec &sp, int bits, int splits, int deep_blocks = 3072)
         if (base < 2048)
             while (ws < cap && g.crs / (2 * ws) >= min_share) ws *= 2;
         const int forced = tuning(kJitWsplit);
-        sp.wsplit = forced == 1 || forced == 2 || forced == 4 ? forced : ws;
+        sp.wsplit = forced == 1 || forced == 2 || forced == 4 || forced == 8 || forced == 16 ? forced : ws;
     }
-    const int tile_pixels = kBlockPixels / sp.wsplit;
+    // A workgroup covers 256 pixels with 4 waves, 128 with 2 x 4, and 64 with
+    // 4, 8 or 16 waves sharing them.
+    const int tile_pixels = kBlockPixels / std::min(sp.wsplit, 4);
     sp.tiles_p = int((nq + tile_pixels - 1) / tile_pixels);
     // Split-K: the parts' partial sums meet in y through int32 atomics after a fill
     // pass, a round trip of y per part, so splitting is kept to what the grid needs.
@@ -585,6 +624,40 @@ ds_status finish_spec(Spec &sp, int bits, int splits, int deep_blocks = 3072)
         // whole, 258 us in 2 parts).
         if (tiles256 < 4) want = blocks >= 256 ? 1 : std::min<int64_t>(want, 4);
         ns = int(std::max<int64_t>(1, want));
+        // (6) Grids of under 2048 waves (2 per SIMD) are bound by how fast each
+        // wave streams its straight-line code, and a split of the reduction adds a
+        // fill pass and atomics. When the choice above splits, or leaves a wave
+        // more than 14 KiB of code, segments of 16 channels run unsplit with a wave
+        // split of 4, or 8 where 4 would leave a wave more than 14 KiB (up to 112
+        // KiB per workgroup): more, shorter code streams on more CUs, at the price
+        // of forming each shift for 16 channels only. On MI355X (calls timed back
+        // to back): 128 -> 128, 3 x 3, 28 x 28, batch 1: 13.6 -> 10.7 us (split 8);
+        // 512 -> 1000 at batch 32: 14.2 -> 11.0 us; 256 -> 128 at batch 8: 12.2 ->
+        // 10.7 us. 2048 -> 1000 at batch 128 (190 KiB per group of 16 channels)
+        // ran 61-65 us unsplit with any wave split or segment width, against 40 us
+        // in 4 parts. The new grid must stay under 2048 waves as well: ResNet-18's
+        // 128 -> 256, 3 x 3 / 2 layer at batch 32 (98 tiles of 64 pixels, 12544
+        // waves in that form) went from 52 to 76 us, its 256 -> 512, 1 x 1 / 2
+        // layer (3200 waves) from 18 to 20 us.
+        const int64_t waves = blocks * ns * std::max(4, sp.wsplit);
+        if (base < 256 && waves < 2048 && !sp.wint && sp.kjn.empty() && tuning(kJitTn) < 0 &&
+            tuning(kJitWsplit) < 0) {
+            const int64_t per_wave = code_words(sp, kTN) * 4 / (int64_t(sp.kgroups) * ns * sp.wsplit);
+            if (ns > 1 || per_wave > 14 * 1024) {
+                const int tn = 16;
+                const int64_t kg = (g.k + tn - 1) / tn;
+                const int64_t per_group = code_words(sp, tn) * 4 / kg;
+                const int ws = per_group <= 56 * 1024 ? 4 : 8;
+                const int64_t new_waves = (nq + 63) / 64 * kg * ws;
+                if (per_group <= 112 * 1024 && g.crs >= 8 * ws && new_waves < 2048) {
+                    sp.tn = tn;
+                    sp.kgroups = int(kg);
+                    sp.wsplit = ws;
+                    sp.tiles_p = int((nq + 63) / 64);
+                    ns = 1;
+                }
+            }
+        }
     }
     sp.nsplit = std::min(ns, g.c);
     const int64_t nseg = int64_t(sp.kgroups) * sp.nsplit;
@@ -1077,17 +1150,20 @@ static hipError_t run_part(const ds_jit_conv *plan, const int32_t *x, const int3
         a.pw = padded ? 0 : g.pw;
         a.ybase = int(m.base); a.ynst = m.nstride; a.yrst = m.rstride; a.ycst = m.cstride;
         a.tiles_p = sp.tiles_p;
-        a.group_tiles = std::min(plan->group_tiles * sp.wsplit, sp.tiles_p);
+        const int per256 = std::min(sp.wsplit, 4);  // pixel tiles per 256 pixels
+        a.group_tiles = std::min(plan->group_tiles * per256, sp.tiles_p);
         a.nseg = sp.nseg;
-        a.wsplit_log2 = sp.wsplit == 4 ? 2 : sp.wsplit == 2 ? 1 : 0;
+        a.wsplit_log2 = sp.wsplit == 16 ? 4 : sp.wsplit == 8 ? 3 : sp.wsplit == 4 ? 2 : sp.wsplit == 2 ? 1 : 0;
         const int order = tuning(kJitOrder);
         a.tile_major = order < 0 ? sp.tile_major : order >= 0 && order <= 2 ? order : 0;
         a.div_ohow = make_fastdiv(uint32_t(a.OHOW));
         a.div_ow = make_fastdiv(uint32_t(a.OW));
         void *args[] = {&a};
-        const unsigned lds = sp.wsplit > 1 ? unsigned(4 / sp.wsplit) * 16384u : 0u;
+        // LDS: 16 KiB of partial sums per group of 64 pixels in the workgroup.
+        const unsigned lds = sp.wsplit > 1 ? unsigned(4 / per256) * 16384u : 0u;
+        const unsigned threads = 64u * unsigned(std::max(sp.wsplit, 4));
         e = hipModuleLaunchKernel(plan->fn, unsigned(int64_t(sp.tiles_p) * sp.nseg), 1, 1,
-                                  kBlockPixels, 1, 1, lds, st, args, nullptr);
+                                  threads, 1, 1, lds, st, args, nullptr);
     }
     if (e == hipSuccess && split) {
         Epilogue epi;

@@ -25,14 +25,14 @@
 // v14, v15 the shifted values and v16..v79 the accumulators; 80 VGPRs, 6
 // waves per SIMD.
 //
-// A workgroup is 4 waves. Without a wave split each wave covers 64 pixels of a
-// 256-pixel tile with the whole reduction of its segment. With a split of 2 or
-// 4 (grids too small to fill the chip otherwise), that many waves share 64
-// pixels, each with a contiguous share of the reduction in code of its own;
-// they add their partial sums into LDS, which the prologue zeroes, and after a
-// barrier each finishes its share of the 64 channels. v3 holds the lane's LDS
-// byte offset: (pixel group in the workgroup) * 16 KiB + lane * 4, channel j
-// at j * 256 above it.
+// A workgroup is 4 waves, or 8 or 16 with a split of that many. Without a wave
+// split each wave covers 64 pixels of a 256-pixel tile with the whole reduction
+// of its segment. With a split of 2, 4, 8 or 16 (grids too small to fill the
+// chip otherwise), that many waves share 64 pixels, each with a contiguous
+// share of the reduction in code of its own; they add their partial sums into
+// LDS, which the prologue zeroes, and after a barrier each finishes its share
+// of the segment's channels. v3 holds the lane's LDS byte offset: (pixel group
+// in the workgroup) * 16 KiB + lane * 4, channel j at j * 256 above it.
 #include <hip/hip_runtime.h>
 
 #include <cstdint>
@@ -44,7 +44,7 @@ using ds::JitArgs;
 template <bool kOneTap>
 __device__ __forceinline__ void jit_conv(const JitArgs &p)
 {
-    extern __shared__ int32_t red[];  // wave split: [4 >> wsplit_log2][64 channels][64 lanes]
+    extern __shared__ int32_t red[];  // wave split: [pixel groups][64 channels][64 lanes]
     const int lane = threadIdx.x & 63;
     const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
     const int wl = p.wsplit_log2;
@@ -79,7 +79,7 @@ __device__ __forceinline__ void jit_conv(const JitArgs &p)
         tile = grp * p.group_tiles + (r - sg * gsize);
     }
     const int seg = __builtin_amdgcn_readfirstlane((sg << wl) + share);
-    const int q = ((tile << (2 - wl)) + pg) * 64 + lane;
+    const int q = ((wl >= 2 ? tile : tile << (2 - wl)) + pg) * 64 + lane;
     const int lds = pg * 16384 + lane * 4;
     if (wl > 0) {
         // Each wave zeroes 64 >> wl channels of its pixel group's partial sums.
@@ -147,13 +147,14 @@ __device__ __forceinline__ void jit_conv(const JitArgs &p)
 }
 
 // Layers with up to 3 x 3 taps per element: 96 VGPRs, 5 waves per SIMD.
-extern "C" __global__ void __launch_bounds__(256) ds_jit_conv_template(const JitArgs p)
+// Workgroups of 256 threads, or 512 / 1024 with a wave split of 8 / 16.
+extern "C" __global__ void __launch_bounds__(1024) ds_jit_conv_template(const JitArgs p)
 {
     jit_conv<false>(p);
 }
 
 // Layers with one tap per element: 80 VGPRs, 6 waves per SIMD.
-extern "C" __global__ void __launch_bounds__(256) ds_jit_conv_one_tap_template(const JitArgs p)
+extern "C" __global__ void __launch_bounds__(1024) ds_jit_conv_one_tap_template(const JitArgs p)
 {
     jit_conv<true>(p);
 }

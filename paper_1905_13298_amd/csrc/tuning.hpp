@@ -9,11 +9,12 @@ namespace ds {
 
 enum Knob {
     kForceVariant,   // DS_FORCE_VARIANT: 0 one-thread-per-output kernel, 8 tiled with 8 pixels per lane
-    kJitWsplit,      // DS_JIT_WSPLIT: waves per 64 pixels in a plan (1, 2, 4)
+    kJitWsplit,      // DS_JIT_WSPLIT: waves per 64 pixels in a plan (1, 2, 4, 8, 16)
     kJitSlots,       // DS_JIT_SLOTS: loads in flight per wave in a plan
     kJitMap,         // DS_JIT_MAP: 96 = the 96-register code for one-tap layers too
     kJitGroupTiles,  // DS_JIT_GROUP_TILES: pixel tiles per group of the grouped block order
     kJitOrder,       // DS_JIT_ORDER: 0 grouped, 1 tile-major, 2 XCD-local tile-major
+    kJitTn,          // DS_JIT_TN: output channels per code segment in a plan (16, 32, 64)
     kKnobs
 };
 

@@ -540,8 +540,8 @@ def run_layer_plan(plan: JitConv, layer, x: torch.Tensor, out: torch.Tensor | No
 
 def set_tuning(name: str, value: int) -> None:
     """Sets a tuning override of the library (``ds_set_tuning``): "DS_FORCE_VARIANT",
-    "DS_JIT_WSPLIT", "DS_JIT_SLOTS", "DS_JIT_MAP", "DS_JIT_GROUP_TILES" or
-    "DS_JIT_ORDER"; a negative value restores the library's own choice."""
+    "DS_JIT_WSPLIT", "DS_JIT_SLOTS", "DS_JIT_MAP", "DS_JIT_GROUP_TILES",
+    "DS_JIT_ORDER" or "DS_JIT_TN"; a negative value restores the library's own choice."""
     call("ds_set_tuning", name.encode(), int(value))
 
 

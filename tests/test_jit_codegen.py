@@ -110,8 +110,9 @@ def lane_inputs(n, c, h, w, k, r, s, st, pd, wsplit=1):
             ok = valid & (ih >= 0) & (ih < h) & (iw >= 0) & (iw < w)
             regs[4 + rr * 3 + ss] = np.where(ok, (nn * c * h * w + ih * w + iw) * 4, OOB).astype(np.int64)
     regs[13] = np.where(valid, (nn * k * oh * ow + pix) * 4, OOB).astype(np.int64)
-    # v3: LDS byte offset of the lane's pixel in its workgroup (wave split)
-    within = q % (256 // wsplit)
+    # v3: LDS byte offset of the lane's pixel in its workgroup (wave split; a
+    # workgroup covers 256 // wsplit pixels, and 64 from a split of 4 up)
+    within = q % (256 // min(wsplit, 4))
     regs[3] = ((within // 64) * 16384 + (within % 64) * 4).astype(np.int64)
     return regs, (oh, ow)
 
@@ -138,7 +139,7 @@ class Interp:
         pending = collections.OrderedDict()   # vgpr -> value, in issue order
         lgkm = {}                              # vgpr -> value of an LDS read in flight
         q = np.arange(V[3].size)
-        tile_px = 256 // self.wsplit
+        tile_px = 256 // min(self.wsplit, 4)
         pc = start
         steps = 0
 
@@ -295,14 +296,23 @@ CASES = [
     (2, 5, 9, 9, 33, 3, 3, 1, 1, 2, "none", 4),     # with split-K: atomics of each share
     (1, 300, 3, 5, 130, 1, 1, 1, 0, 1, "mul", 4),
     (1, 3, 13, 11, 20, 7, 7, 2, 3, 1, "relu", 2),   # padded copy and wave split
+    # splits of 8 and 16 waves (workgroups of 512 / 1024 threads), and segments
+    # of 16 or 32 output channels
+    (2, 40, 9, 9, 70, 3, 3, 1, 1, 1, "full", 8),
+    (1, 300, 3, 5, 130, 1, 1, 1, 0, 1, "full", 16),
+    (2, 37, 7, 6, 70, 3, 3, 2, 1, 2, "none", 16),   # with split-K
+    (2, 40, 9, 9, 70, 3, 3, 1, 1, 1, "full", 1, 16),
+    (2, 13, 9, 9, 50, 3, 3, 1, 1, 3, "none", 4, 32),
+    (33, 90, 1, 1, 37, 1, 1, 1, 0, 1, "full", 16, 16),
+    (1, 3, 13, 11, 40, 7, 7, 2, 3, 1, "relu", 8, 16),  # padded copy
 ]
 
 
 @pytest.mark.parametrize("case", CASES, ids=[str(i) for i in range(len(CASES))])
 def test_generated_code_matches_oracle(case, tmp_path, knob):
-    n, c, h, w, k, r, s, st, pd, splits, epi = case[:11]
     wsplit = case[11] if len(case) > 11 else 1
-    run_generated(case[:11] + (wsplit,), zlib.crc32(str(case).encode()), 0.1, tmp_path, knob)
+    tn = case[12] if len(case) > 12 else 64
+    run_generated(case[:11] + (wsplit, tn), zlib.crc32(str(case).encode()), 0.1, tmp_path, knob)
 
 
 def random_cases(count, seed=1905):
@@ -320,10 +330,11 @@ def random_cases(count, seed=1905):
         if h + 2 * pd < r or w + 2 * pd < s:
             continue
         splits = int(rng.choice([1, 2, 3]))
-        wsplit = int(rng.choice([1, 2, 4]))
+        wsplit = int(rng.choice([1, 2, 4, 8, 16]))
+        tn = int(rng.choice([16, 32, 64, 64]))
         epi = str(rng.choice(["none", "relu", "mul", "full"]))
         zero = float(rng.choice([0.0, 0.1, 0.5, 0.95]))
-        out.append(((n, c, h, w, k, r, s, st, pd, splits, epi, wsplit), zero))
+        out.append(((n, c, h, w, k, r, s, st, pd, splits, epi, wsplit, tn), zero))
     return out
 
 
@@ -337,10 +348,11 @@ def test_generated_code_matches_oracle_random_shapes(case, zero, tmp_path, knob)
 
 def run_generated(case, seed, zero_frac, tmp_path, knob):
     """Generate a plan's code object for `case` (n, c, h, w, k, r, s, stride, pad,
-    splits, epilogue, wave split), run it in the interpreter over every lane, and
-    compare with the oracle."""
-    n, c, h, w, k, r, s, st, pd, splits, epi, wsplit = case
+    splits, epilogue, wave split, channels per segment), run it in the
+    interpreter over every lane, and compare with the oracle."""
+    n, c, h, w, k, r, s, st, pd, splits, epi, wsplit, tn = case
     knob("DS_JIT_WSPLIT", wsplit)
+    knob("DS_JIT_TN", tn)
     codes, x, rng = gen_layer(seed, n, c, h, w, k, r, s, zero_frac)
     bias = rng.integers(-(2 ** 31), 2 ** 31, k, dtype=np.int64).astype(np.int32)
     mul = add = res = None
@@ -379,7 +391,7 @@ def run_generated(case, seed, zero_frac, tmp_path, knob):
     bufs = {20: (xb, xb.size * 4), 24: (y, y.size * 4)}
     bufs[36] = (res.reshape(-1).view(np.uint32).astype(np.int64), y.size * 4) if res is not None else (y, 0)
     nsplit = min(splits, c)
-    kgroups = -(-k // 64)
+    kgroups = -(-k // tn)
     split = nsplit > 1
     if split:
         y[:] = np.repeat(np.tile(bias.view(np.uint32).astype(np.int64), n), oh * ow)
@@ -437,6 +449,26 @@ def test_zero_weights_emit_no_arithmetic(tmp_path):
     names = collections.Counter(op for op, _, _ in disassemble(img, str(tmp_path)).values())
     assert names["buffer_load_dword"] == 1 and names["v_ashrrev_i32_e32"] == 1
     assert names["v_sub_u32_e32"] == 1 and names["v_add_u32_e32"] == 0
+
+
+def test_small_grids_run_unsplit_in_16_channel_segments(tmp_path, knob):
+    """A grid of a few waves whose default plan would split the reduction runs
+    unsplit in segments of 16 channels with a wave split of 4 (no fill pass, no
+    atomics): the same code as that configuration forced, and correct."""
+    codes, _, _ = gen_layer(7, 1, 32, 10, 10, 40, 3, 3)
+    wp = ops.pack_shift_weights(codes)
+    auto = ops.jit_conv_image(wp, (1, 32, 10, 10), 3, 1, 1)
+    names = collections.Counter(op for op, _, _ in disassemble(auto, str(tmp_path)).values())
+    assert names["s_getpc_b64"] == 3 * 4 and names["buffer_atomic_add"] == 0
+    knob("DS_JIT_TN", 16)
+    knob("DS_JIT_WSPLIT", 4)
+    assert ops.jit_conv_image(wp, (1, 32, 10, 10), 3, 1, 1, splits=1) == auto
+    knob("DS_JIT_TN", 64)     # segments of 64 forced: the split plan of the older rule
+    knob("DS_JIT_WSPLIT", -1)
+    old = ops.jit_conv_image(wp, (1, 32, 10, 10), 3, 1, 1)
+    names = collections.Counter(op for op, _, _ in disassemble(old, str(tmp_path)).values())
+    assert names["buffer_atomic_add"] > 0
+    run_generated((1, 32, 10, 10, 40, 3, 3, 1, 1, 1, "full", 4, 16), 7, 0.1, tmp_path, knob)
 
 
 @pytest.mark.parametrize("bits", [2, 3, 4])
