@@ -5,8 +5,9 @@ inputs: edge shapes (ragged channels, pixels and output channels; strides,
 padding, rectangular windows; LinearShift as 1 x 1 on 1 x 1 images), each with
 the reduction whole, split automatically and split by force (the split-K path
 adds partial sums atomically and runs the epilogue as a pass of its own); the
-fused epilogue (affine map, residual, ReLU) against the oracle's; every block
-order of the grid; the single-
+fused epilogue (affine map, residual, ReLU) against the oracle's; segments of
+16, 32 and 64 channels with wave splits up to 16; every block order of the grid;
+the single-
 layer workloads in full; and every ResNet-50 convolution (the 7 x 7 stem through
 a padded copy of x) at batch 128 in full against the production kernel, plus
 sampled outputs against the oracle.
@@ -79,6 +80,53 @@ def test_edge_shapes_match_oracle(spec, splits):
     want = oracle.conv2d_shift(x, codes, bias, r=r, s=s, stride=st, pad=pd)
     bad = np.flatnonzero(y.ravel() != want.ravel())
     assert bad.size == 0, f"{bad.size} of {want.size} outputs differ, first at {bad[:5]}"
+
+
+LAYOUTS = [(16, 4), (16, 8), (16, 16), (32, 16), (64, 8), (64, 16), (32, 2)]
+LAYOUT_SHAPES = ["ragged_k_c_pix", "1x1_s2", "linear_like", "7x7_s2_stem_like", "big_c_small_k",
+                 "tiny", "many_tiles"]
+
+
+@pytest.mark.parametrize("splits", [1, 3])
+@pytest.mark.parametrize("layout", LAYOUTS, ids=[f"tn{a}_ws{b}" for a, b in LAYOUTS])
+@pytest.mark.parametrize("name", LAYOUT_SHAPES)
+def test_segment_widths_and_wave_splits_match_oracle(name, layout, splits, knob):
+    """Segments of 16, 32 or 64 output channels with wave splits up to 16 (workgroups
+    of up to 1024 threads meeting in LDS), whole and split, against the oracle."""
+    spec = next(e for e in EDGE if e[0] == name)
+    _, n, c, h, w, k, r, s, st, pd = spec
+    tn, ws = layout
+    knob("DS_JIT_TN", tn)
+    knob("DS_JIT_WSPLIT", ws)
+    codes, x, bias, _ = rand_case(zlib.crc32(repr((spec, layout, splits)).encode()), n, c, h, w, k, r, s)
+    plan = ops.JitConv(ops.pack_shift_weights(codes), x.shape, (r, s), st, pd, bias=bias, splits=splits)
+    say(f"jit layout tn{tn} ws{ws} {name} splits={splits}: {plan.splits} parts, {plan.segments} segments")
+    y = plan(to_dev(x)).cpu().numpy()
+    plan.close()
+    want = oracle.conv2d_shift(x, codes, bias, r=r, s=s, stride=st, pad=pd)
+    bad = np.flatnonzero(y.ravel() != want.ravel())
+    assert bad.size == 0, f"{bad.size} of {want.size} outputs differ, first at {bad[:5]}"
+
+
+@pytest.mark.parametrize("layout", [(16, 16), (32, 8), (16, 4)])
+def test_epilogue_in_narrow_segments_matches_oracle(layout, knob):
+    """The fused epilogue (affine map, residual, ReLU) when each of up to 16 waves
+    finishes one or a few channels of a 16- or 32-channel segment."""
+    tn, ws = layout
+    knob("DS_JIT_TN", tn)
+    knob("DS_JIT_WSPLIT", ws)
+    n, c, h, w, k, r, s, st, pd = 2, 40, 11, 11, 70, 3, 3, 1, 1
+    codes, x, bias, rng = rand_case(zlib.crc32(repr(layout).encode()), n, c, h, w, k, r, s, small_x=True)
+    mul = rng.integers(-(2 ** 17), 2 ** 17, k).astype(np.int32)
+    add = rng.integers(-(2 ** 20), 2 ** 20, k).astype(np.int32)
+    res = rng.integers(-(2 ** 24), 2 ** 24, (n, k, h, w)).astype(np.int32)
+    plan = ops.JitConv(ops.pack_shift_weights(codes), x.shape, 3, st, pd, bias=bias, mul=mul, add=add,
+                       mul_shift=16, residual=True, relu=True, splits=1)
+    say(f"jit epilogue tn{tn} ws{ws}")
+    y = plan(to_dev(x), residual=to_dev(res)).cpu().numpy()
+    plan.close()
+    conv = oracle.conv2d_shift(x, codes, bias, r=r, s=s, stride=st, pad=pd)
+    np.testing.assert_array_equal(y, oracle.epilogue(conv, mul, add, 16, residual=res, relu=True))
 
 
 @pytest.mark.parametrize("splits", [1, 2])
