@@ -5,8 +5,8 @@ LinearShift call on its own seeded input, all inputs resident in HBM).
 Two paths compute the same outputs bit for bit (checked before timing):
   jit      (default) a weight-specialised plan per layer, its code generated
            at setup from the fixed weights (Section 6's run-time compilation);
-           a layer whose plan is not preferred (JitConv.preferred, true for
-           every shape measured on MI355X) runs the runtime kernel
+           a layer whose plan is not preferred (JitConv.preferred: a cost
+           model of both paths, in the per-layer JSON) runs the runtime kernel
   runtime  ds_conv2d_shift / ds_linear_shift with the packed weights as data
 Prints ONE JSON line:
   value       whole-step throughput in G shift-accumulates/s (dense SAC =
@@ -42,6 +42,10 @@ WORKLOADS = {"linear_small": 0, "conv_single": 1, "linear_fc6": 2, "resnet18": 3
 # A plan that is almost only VOP2 adds and subtracts (workloads.VALU_PROBE): its rate,
 # and its SQ counters under rocprofv3, measure the issue rate of generated code.
 PROBE_WORKLOADS = {"valu_probe": 99}
+# A layer where the plans' cost model prefers the runtime kernel: VGG16's fc6
+# (25088 -> 4096) at batch 1, about 450 MB of generated code for one row. With
+# --time-rejected the rejected plan is timed too, to check the model's choice.
+MODEL_WORKLOADS = {"linear_25088_b1": 98}
 # The step upstream of the operators: float weights -> packed codes (DeepShift-Q)
 # and the float input batch -> fixed point, for every layer of ResNet-50 at N = 128.
 CONVERT_WORKLOADS = {"convert_resnet50": 4}
@@ -91,7 +95,9 @@ def parse():
     ap.add_argument("--steps", type=int, default=5)
     ap.add_argument("--warmup", type=int, default=2)
     ap.add_argument("--workload", default="resnet50", choices=sorted(WORKLOADS) + sorted(CONVERT_WORKLOADS) + sorted(NETWORK_WORKLOADS)
-                    + sorted(BACKWARD_WORKLOADS) + sorted(PROBE_WORKLOADS))
+                    + sorted(BACKWARD_WORKLOADS) + sorted(PROBE_WORKLOADS) + sorted(MODEL_WORKLOADS))
+    ap.add_argument("--time-rejected", action="store_true",
+                    help="with --path jit, also time the plans the cost model rejects (per-layer JSON)")
     ap.add_argument("--cpu-batch", type=int, default=None,
                     help="batch of the oracle sample (default: sized for ~10-30 s)")
     ap.add_argument("--cpu-seconds", type=float, default=10.0,
@@ -745,6 +751,8 @@ def bench_layers(args):
 
     if args.workload in PROBE_WORKLOADS:
         cfg, seed, layers = None, 99, [W.VALU_PROBE]
+    elif args.workload in MODEL_WORKLOADS:
+        cfg, seed, layers = None, 98, [W.LINEAR_25088_B1]
     else:
         cfg = WORKLOADS[args.workload]
         seed = W.CONFIG_SEEDS[cfg]
@@ -756,7 +764,7 @@ def bench_layers(args):
     # ---- inputs resident in HBM before timing; weight-specialised plans are made
     # here too (host code generation, once per layer, like packing the weights)
     t0 = time.time()
-    res, plans, nonzero = [], [], []
+    res, plans, nonzero, model, rejected = [], [], [], [], []
     plan_s = 0.0
     act = args.act_bits
     if act != 32 and args.path != "jit":
@@ -775,9 +783,17 @@ def bench_layers(args):
             tp = time.time()
             plan = ops.layer_plan(L, wp, bias, act_bits=act)
             plan_s += time.time() - tp
+            model.append((plan.estimate_us(), plan.runtime_estimate_us(), plan.preferred,
+                          {"code_bytes": plan.code_bytes, "segments": plan.segments, "splits": plan.splits,
+                           "channels": plan.channels, "wsplit": plan.wsplit, "pixel_tiles": plan.pixel_tiles}))
             if not plan.preferred:
-                plan.close()
+                if args.time_rejected:
+                    rejected.append((len(plans), plan))
+                else:
+                    plan.close()
                 plan = None
+        else:
+            model.append(None)
         plans.append(plan)
         del x, codes, bias
     torch.cuda.synchronize()
@@ -868,7 +884,26 @@ def bench_layers(args):
         }
         if runtime is not None:
             row["runtime_ms_median"] = float(np.median(d_rt[:, li]))
+        if model[li] is not None:
+            row["plan_model_us"] = round(model[li][0], 2)
+            row["runtime_model_us"] = round(model[li][1], 2)
+            row["plan_preferred"] = model[li][2]
+            row["plan_layout"] = model[li][3]
         per_layer.append(row)
+    # Plans the cost model rejected, timed on their own (each checked first).
+    for li, plan in rejected:
+        L, xt, wt, bt, yt = res[li]
+        ref = yt.clone()
+        runtime_call(L, xt, wt, bt, yt)()
+        ref.copy_(yt)
+        ops.run_layer_plan(plan, L, xt, out=yt)
+        torch.cuda.synchronize()
+        if not torch.equal(yt, ref):
+            raise SystemExit(f"{L.name}: rejected plan and runtime outputs differ")
+        _, d_rej = time_layers([lambda plan=plan, L=L, xt=xt, yt=yt: ops.run_layer_plan(plan, L, xt, out=yt)],
+                               args.steps, args.warmup, stream)
+        per_layer[li]["rejected_plan_ms_median"] = float(np.median(d_rej[:, 0]))
+        plan.close()
 
     # ---- multiplication-based comparison, each against the shift path of the same tiling
     mul = None

@@ -1237,6 +1237,17 @@ extern "C" ds_status ds_jit_conv_query(const ds_jit_conv *plan, int64_t *code_by
     return ok();
 }
 
+extern "C" ds_status ds_jit_conv_layout(const ds_jit_conv *plan, int32_t *channels, int32_t *wsplit,
+                                        int32_t *pixel_tiles)
+{
+    if (!plan) return fail(DS_ERR_NULL_POINTER, "plan must not be NULL");
+    const ds_jit_conv *k = plan->backward ? (plan->parts.empty() ? nullptr : plan->parts.front()) : plan;
+    if (channels) *channels = k ? k->sp.tn : kTN;
+    if (wsplit) *wsplit = k ? k->sp.wsplit : 1;
+    if (pixel_tiles) *pixel_tiles = k ? k->sp.tiles_p : 0;
+    return ok();
+}
+
 // ---------------------------------------------------------------------------
 // Multiplication plans: the comparison operator of Section 6's timing (a
 // multiplication-based kernel) in the plans' own tiling, for side-by-side

@@ -448,22 +448,73 @@ class JitConv:
             call("ds_jit_conv_create", _np_ptr(wp), _np_ptr(b), _np_ptr(m), _np_ptr(a), mul_shift,
                  n, c, h, w, self.k, r, s, sh, sw, ph, pw, flags, splits, ctypes.byref(handle))
         self._h = handle
+        self._query()
+        self.crs = c * r * s
+        self.out_pixels, self.out_channels = n * self.y_shape[2] * self.y_shape[3], self.k
+        self.sac = self.out_pixels * self.k * self.crs
+        self.linear = h == w == r == s == 1 and ph == pw == 0
+
+    def _query(self):
         cb, seg, sp = ctypes.c_int64(), ctypes.c_int32(), ctypes.c_int32()
         call("ds_jit_conv_query", self._h, ctypes.byref(cb), ctypes.byref(seg), ctypes.byref(sp))
         self.code_bytes, self.segments, self.splits = cb.value, seg.value, sp.value
-        # Workgroups of 256 output pixels that run each code segment.
-        self.pixel_tiles = -(-(n * self.y_shape[2] * self.y_shape[3]) // 256)
+        tn, ws, tiles = ctypes.c_int32(), ctypes.c_int32(), ctypes.c_int32()
+        call("ds_jit_conv_layout", self._h, ctypes.byref(tn), ctypes.byref(ws), ctypes.byref(tiles))
+        # Output channels per segment, waves per 64 pixels (each streaming code of
+        # its own), and the pixel tiles (workgroups) that run each segment.
+        self.channels, self.wsplit, self.pixel_tiles = tn.value, ws.value, tiles.value
+
+    # Cost model of the two paths on MI355X (microseconds), fitted to calls timed
+    # back to back. A plan's waves each stream their share of the straight-line
+    # code at about 1.6 GB/s when few waves share it (instruction fetch: a 64-byte
+    # line per L2 round trip with a few in flight; the 4096 -> 4096 LinearShift
+    # at batch 256, 290 KB per wave, 174 us), and the chip issues at most 0.355
+    # wave-instructions per SIMD per clock (872 G/s: the ResNet-50 plans, whose
+    # waves share their code, and a probe of adds). Code words are about 1.05 per
+    # instruction; each segment's code runs once per wave of each pixel tile
+    # (4, 2 or 1 waves per tile for a wave split of 1, 2 or 4+ with its shares).
+    # Launch and set-up add about 3 us, a split reduction (fill pass, atomics) 3
+    # us more. The runtime kernel decodes its weights and launches 2-5 kernels per
+    # call (about 25 us for a convolution, 40 us for a LinearShift, whose operands
+    # it transposes), then runs at up to 15 T dense SACs/s on full tiles of 256
+    # output pixels (batch rows for a LinearShift; a ragged last tile wastes its
+    # lanes), reading its packed weights at 4 TB/s.
+    PLAN_STREAM_BPUS = 1.6e3        # code bytes per us per wave
+    PLAN_ISSUE_PER_US = 872e3       # wave-instructions per us, whole chip
+    RUNTIME_SAC_PER_US = 15e6       # dense SACs per us on full tiles
+
+    def estimate_us(self) -> float:
+        """Modelled duration of one run of this plan on MI355X (see the cost
+        model above)."""
+        streams = max(1, self.segments * self.wsplit)
+        waves_per_tile = 4 // min(max(self.wsplit, 1), 4)
+        executed = self.code_bytes / 4.2 * max(1, self.pixel_tiles) * waves_per_tile
+        t = max(self.code_bytes / streams / self.PLAN_STREAM_BPUS, executed / self.PLAN_ISSUE_PER_US)
+        return 3.0 + (3.0 if self.splits > 1 else 0.0) + t
+
+    def runtime_estimate_us(self) -> float:
+        """Modelled duration of the same layer on the runtime kernel
+        (ds_conv2d_shift / ds_linear_shift)."""
+        nq = max(1, self.out_pixels)
+        fill = nq / (-(-nq // 256) * 256)
+        weight_bytes = self.out_channels * packed_row_words(self.crs) * 4
+        return ((40.0 if self.linear else 25.0) + self.sac / (self.RUNTIME_SAC_PER_US * fill)
+                + weight_bytes / 4e6)
 
     @property
     def preferred(self) -> bool:
-        """Whether this plan is expected to beat the runtime kernel: on MI355X
-        every measured case. Each code segment is straight-line code that a few
-        waves stream through the instruction cache, so when only one pixel tile
-        shares a segment (a LinearShift at small batch) most of that code comes
-        from memory with no reuse; even so the plans ran faster: 4096 -> 4096 at
-        batch 256 (71 MiB of code) 175 us against 361 us, 2048 -> 1000 at batch
-        128 62 us against 83 us, 256 -> 128 at batch 8 12.5 us against 45 us."""
-        return True
+        """Whether this plan is expected to beat the runtime kernel, by the cost
+        model above. Measured on MI355X (model in brackets), plan against runtime
+        kernel: 4096 -> 4096 at batch 256 178 us (184) against 354 us (329); 128 ->
+        128 3 x 3 at 28 x 28, batch 1 12.6 us (11.5) against 42 us (35); 256 -> 128
+        at batch 8 9.3 us (7.9) against 45 us (41); 25088 -> 4096 at batch 1 (450
+        MB of code for one row) 346 us (282) against 1960 us (1811: one row in a
+        256-row tile). Over the layers of ResNet-18 (batch 32) and ResNet-50
+        (batch 128) measured / modelled plan durations have medians 1.16 and 1.04
+        (0.93-2.0), runtime-kernel ones 0.97 and 0.92 (0.87-1.3); every one of
+        those layers is a plan. The runtime kernel wins where code would dwarf the
+        work (e.g. 8x the code the planner makes for a layer)."""
+        return self.estimate_us() < self.runtime_estimate_us()
 
     def __call__(self, x: torch.Tensor, residual: torch.Tensor | None = None, out=None):
         _dev_int(x, "x", getattr(self, "act_bits", 32))
@@ -511,10 +562,11 @@ class JitConvBackwardData(JitConv):
             call("ds_jit_conv_backward_data_create", _np_ptr(wp), n, c, h, w, self.k, r, s, sh, sw,
                  ph, pw, code_bits_flag(code_bits), splits, ctypes.byref(handle))
         self._h = handle
-        cb, seg, sp = ctypes.c_int64(), ctypes.c_int32(), ctypes.c_int32()
-        call("ds_jit_conv_query", self._h, ctypes.byref(cb), ctypes.byref(seg), ctypes.byref(sp))
-        self.code_bytes, self.segments, self.splits = cb.value, seg.value, sp.value
-        self.pixel_tiles = -(-(n * h * w) // 256)
+        self._query()
+        self.crs = self.k * r * s       # weights per input channel of the forward layer
+        self.out_pixels, self.out_channels = n * h * w, c
+        self.sac = n * self.k * self.x_shape[2] * self.x_shape[3] * c * r * s
+        self.linear = False
 
 
 def layer_plan(layer, w_packed, bias=None, device="cuda:0", act_bits: int = 32) -> JitConv:
@@ -616,7 +668,8 @@ class JitConvMul(JitConv):
             call("ds_jit_conv_mul_create", _np_ptr(wa), _np_ptr(b), n, c, h, wd, self.k, r, s, sh, sw,
                  ph, pw, DS_RELU if relu else 0, splits, ctypes.byref(handle))
         self._h = handle
-        cb, seg, sp = ctypes.c_int64(), ctypes.c_int32(), ctypes.c_int32()
-        call("ds_jit_conv_query", self._h, ctypes.byref(cb), ctypes.byref(seg), ctypes.byref(sp))
-        self.code_bytes, self.segments, self.splits = cb.value, seg.value, sp.value
-        self.pixel_tiles = -(-(n * self.y_shape[2] * self.y_shape[3]) // 256)
+        self._query()
+        self.crs = c * r * s
+        self.out_pixels, self.out_channels = n * self.y_shape[2] * self.y_shape[3], self.k
+        self.sac = self.out_pixels * self.k * self.crs
+        self.linear = h == wd == r == s == 1 and ph == pw == 0

@@ -159,6 +159,11 @@ CONFIG_SEEDS = {0: 0, 1: 1, 2: 2, 3: 3, 4: 4}
 VALU_PROBE = Layer("valu_probe", "conv", n=1, c=256, k=256, h=256, w=256, code_dist="shift0",
                    zero_frac=0.0)
 
+# VGG16's fc6 (25088 -> 4096) at batch 1: much generated code for little work,
+# where the runtime kernel is the faster path.
+LINEAR_25088_B1 = Layer("fc6_b1", "linear", n=1, c=25088, k=4096, bias=True, x_dist="uniform_0_2",
+                        zero_frac=0.10)
+
 
 def config_layers(cfg: int) -> list:
     """Layer list of one benchmark configuration (seed is ``CONFIG_SEEDS[cfg]``)."""

@@ -1,0 +1,49 @@
+"""The cost model behind JitConv.preferred (host arithmetic only): the plan and
+runtime-kernel estimates for layouts the planner produces on the benchmark
+shapes, against the durations measured on MI355X that the model was fitted to,
+and the choice it makes."""
+import pytest
+
+from paper_1905_13298_amd import ops
+
+
+def fake_plan(n, c, h, w, k, r, s, oh, ow, code_bytes, segments, splits, channels, wsplit, tiles):
+    p = object.__new__(ops.JitConv)
+    p.k = k
+    p.crs = c * r * s
+    p.out_pixels, p.out_channels = n * oh * ow, k
+    p.sac = p.out_pixels * k * p.crs
+    p.linear = h == w == r == s == 1
+    p.code_bytes, p.segments, p.splits = code_bytes, segments, splits
+    p.channels, p.wsplit, p.pixel_tiles = channels, wsplit, tiles
+    return p
+
+
+# (shape, layout as the planner makes it, measured plan us, measured runtime us)
+CASES = [
+    # 128 -> 128, 3 x 3 at 28 x 28, batch 1: 16-channel segments, wave split 8, unsplit
+    ((1, 128, 28, 28, 128, 3, 3, 28, 28), (868000, 8, 1, 16, 8, 13), 12.6, 42.1),
+    # 256 -> 128 at batch 8: 16-channel segments, wave split 4
+    ((8, 256, 1, 1, 128, 1, 1, 1, 1), (249000, 8, 1, 16, 4, 1), 9.3, 45.2),
+    # 4096 -> 4096 at batch 256: 64-channel segments, wave split 4, 4 tiles of 64 rows
+    ((256, 4096, 1, 1, 4096, 1, 1, 1, 1), (74041044, 64, 1, 64, 4, 4), 178.4, 354.0),
+    # 25088 -> 4096 at batch 1: split in 4
+    ((1, 25088, 1, 1, 4096, 1, 1, 1, 1), (450e6, 256, 4, 64, 4, 1), 346.2, 1960.1),
+]
+
+
+@pytest.mark.parametrize("case", CASES, ids=["conv_n1", "linear_b8", "fc_b256", "fc6_b1"])
+def test_model_tracks_measured_durations_and_picks_the_faster_path(case):
+    shape, layout, plan_us, rt_us = case
+    p = fake_plan(*shape, *layout)
+    est, rt = p.estimate_us(), p.runtime_estimate_us()
+    assert 0.7 * plan_us <= est <= 1.3 * plan_us, (est, plan_us)
+    assert 0.7 * rt_us <= rt <= 1.3 * rt_us, (rt, rt_us)
+    assert p.preferred == (plan_us < rt_us)
+
+
+def test_model_prefers_the_runtime_kernel_for_much_code_and_little_work():
+    # 4096 -> 4096 at batch 256 with 600 MB of code (a contrived plan, 8x what
+    # the planner makes): the runtime kernel is estimated faster
+    p = fake_plan(256, 4096, 1, 1, 4096, 1, 1, 1, 1, 600e6, 64, 1, 64, 4, 4)
+    assert p.estimate_us() > p.runtime_estimate_us() and not p.preferred
