@@ -96,6 +96,8 @@ def parse():
     ap.add_argument("--warmup", type=int, default=2)
     ap.add_argument("--workload", default="resnet50", choices=sorted(WORKLOADS) + sorted(CONVERT_WORKLOADS) + sorted(NETWORK_WORKLOADS)
                     + sorted(BACKWARD_WORKLOADS) + sorted(PROBE_WORKLOADS) + sorted(MODEL_WORKLOADS))
+    ap.add_argument("--eager", action="store_true",
+                    help="path jit: time eager calls instead of replays of a HIP graph of the step")
     ap.add_argument("--time-rejected", action="store_true",
                     help="with --path jit, also time the plans the cost model rejects (per-layer JSON)")
     ap.add_argument("--cpu-batch", type=int, default=None,
@@ -667,6 +669,58 @@ def group_name(L, path: str, planned: bool | None = None) -> str:
     return kernel_variant(L).rsplit(" splits", 1)[0]
 
 
+def time_graph(calls, outs, steps, warmup):
+    """The step (every call in order) captured in a HIP graph and replayed.
+    Launching a step from the host costs microseconds per call, which for the
+    shortest layers is more than their kernels; a graph launches the same
+    kernels (plans use no memset and allocate nothing when run). A graph launch
+    itself costs tens of microseconds, so a graph holds R consecutive steps, R
+    the largest divisor of `steps` that keeps it within 64 calls: `warmup`
+    untimed steps, then steps / R replays between two HIP events. The outputs
+    of the first and the last replay must equal those of the eager calls.
+    Returns (ms per step, R)."""
+    import torch
+    per = max(1, 64 // max(1, len(calls)))
+    rep = max(r for r in range(1, min(per, steps) + 1) if steps % r == 0)
+    for c in calls:
+        c()
+    torch.cuda.synchronize()
+    ref = [o.clone() for o in outs]
+    side = torch.cuda.Stream()
+    side.wait_stream(torch.cuda.current_stream())
+    g = torch.cuda.CUDAGraph()
+    with torch.cuda.stream(side):
+        with torch.cuda.graph(g, stream=side):
+            for _ in range(rep):
+                for c in calls:
+                    c()
+    torch.cuda.synchronize()
+
+    def check(when):
+        for o, r in zip(outs, ref):
+            if not torch.equal(o, r):
+                raise SystemExit(f"graph replay ({when}) differs from the eager calls")
+    for o in outs:
+        o.fill_(-1)
+    g.replay()
+    torch.cuda.synchronize()
+    check("first")
+    for _ in range(-(-warmup // rep)):
+        g.replay()
+    torch.cuda.synchronize()
+    stream = torch.cuda.current_stream()
+    t_start = torch.cuda.Event(enable_timing=True)
+    t_end = torch.cuda.Event(enable_timing=True)
+    t_start.record(stream)
+    for _ in range(steps // rep):
+        g.replay()
+    t_end.record(stream)
+    torch.cuda.synchronize()
+    check("last")
+    del g
+    return t_start.elapsed_time(t_end) / steps, rep
+
+
 def time_layers(calls, steps, warmup, stream):
     """Run every call `warmup` times untimed, then `steps` timed passes between
     two HIP events on `stream` (the step time), then `steps` more passes with
@@ -785,7 +839,8 @@ def bench_layers(args):
             plan_s += time.time() - tp
             model.append((plan.estimate_us(), plan.runtime_estimate_us(), plan.preferred,
                           {"code_bytes": plan.code_bytes, "segments": plan.segments, "splits": plan.splits,
-                           "channels": plan.channels, "wsplit": plan.wsplit, "pixel_tiles": plan.pixel_tiles}))
+                           "channels": plan.channels, "wsplit": plan.wsplit, "pixel_groups": plan.pixel_groups,
+                           "pixel_tiles": plan.pixel_tiles}))
             if not plan.preferred:
                 if args.time_rejected:
                     rejected.append((len(plans), plan))
@@ -832,6 +887,11 @@ def bench_layers(args):
         ms_per_step, d = time_layers(jit_calls, args.steps, args.warmup, stream)
     else:
         ms_per_step, d = time_layers(runtime_calls, args.steps, args.warmup, stream)
+    timing = {"mode": "eager", "eager_ms_per_step": round(ms_per_step, 5)}
+    if args.path == "jit" and not args.eager and all(p is not None for p in plans):
+        ms_per_step, rep = time_graph(jit_calls, [r[4] for r in res], args.steps, args.warmup)
+        timing = {"mode": "HIP graph of consecutive steps, replayed", "steps_per_graph": rep,
+                  "graph_ms_per_step": round(ms_per_step, 5), "eager_ms_per_step": timing["eager_ms_per_step"]}
     value = sac_step / (ms_per_step * 1e-3) / 1e9
     planned = [p is not None for p in plans]
     roofline = roofline_of(layers, d, args.path, nonzero, planned, act)
@@ -910,8 +970,9 @@ def bench_layers(args):
     if not args.no_mul and act == 32:
         rt_shift_ms = runtime["ms_per_step"] if runtime is not None else (
             ms_per_step if args.path == "runtime" else time_layers(runtime_calls, args.steps, 1, stream)[0])
+        # (both sides of each comparison timed as eager calls)
         mul = mul_comparison(args, res, layers, seed, stream, rt_shift_ms,
-                             ms_per_step if args.path == "jit" else None)
+                             timing["eager_ms_per_step"] if args.path == "jit" else None)
 
     # ---- CPU baseline: the oracle on the host cores, same layers at a small batch
     cpu = None
@@ -940,6 +1001,7 @@ def bench_layers(args):
                    "act_bits": act,
                    "sac_per_step": sac_step, "nonzero_sac_per_step": int(nz_step),
                    "parallelism": "single GPU"},
+        "timing": timing,
         "roofline": roofline, "layer_summary": layer_summary, "runtime_weights": runtime,
         "cpu_baseline": cpu, "mul_comparison": mul,
     }

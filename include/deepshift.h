@@ -389,15 +389,17 @@ ds_status ds_conv2d_shift_describe(int64_t n, int64_t c, int64_t h, int64_t w, i
  * ds_jit_conv_layout: how the plan's grid is laid out: output channels per
  * segment (16, 32 or 64), waves sharing each group of 64 pixels (the wave
  * split: 1, 2, 4, 8 or 16; each runs code of its own for a share of the
- * reduction), and pixel tiles (workgroups per segment: 256 pixels each with no
- * wave split, 128 with 2, 64 from 4 up). Each segment's code is executed once
- * per pixel tile; segments x wave split waves stream distinct code. For an
- * input-gradient plan: its first kernel. Any output may be NULL.
+ * reduction), groups of 64 pixels per workgroup (1, 2 or 4; a workgroup has
+ * groups x wave split <= 16 waves), and pixel tiles (workgroups per segment).
+ * Each share's code runs once per group of 64 pixels; segments x wave split
+ * distinct code streams. For an input-gradient plan: its first kernel. Any
+ * output may be NULL.
  *
  * Tuning overrides (ds_set_tuning, below) used when a plan is made (wave split,
  * loads in flight, register map, tile grouping, segment width) or run (block
  * order); for measurements only: DS_JIT_WSPLIT (1, 2, 4, 8 or 16 waves per 64
- * pixels), DS_JIT_TN (16, 32 or 64 output channels per segment),
+ * pixels), DS_JIT_TN (16, 32 or 64 output channels per segment), DS_JIT_PGROUPS
+ * (1, 2 or 4 groups of 64 pixels per workgroup, at most 16 waves in all),
  * DS_JIT_SLOTS (loads in flight: 1-14, at most 8 in the 80-register code of
  * layers with one tap per element), DS_JIT_MAP (96: the 96-register code for
  * those layers too), DS_JIT_GROUP_TILES (tiles per group), DS_JIT_ORDER (0
@@ -422,7 +424,7 @@ ds_status ds_jit_conv_image(const uint32_t *w_packed, const int32_t *bias, const
 ds_status ds_jit_conv_query(const ds_jit_conv *plan, int64_t *code_bytes, int32_t *segments,
                             int32_t *splits);
 ds_status ds_jit_conv_layout(const ds_jit_conv *plan, int32_t *channels, int32_t *wsplit,
-                             int32_t *pixel_tiles);
+                             int32_t *pixel_groups, int32_t *pixel_tiles);
 
 /* A plan for the input gradient of a ConvShift layer (the result of
  * ds_conv2d_shift_backward_data, bit for bit), with the weights baked into

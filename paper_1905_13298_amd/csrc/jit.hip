@@ -185,6 +185,9 @@ struct Spec {
     // chip (more segments, each with less code, at the price of forming each
     // shift for fewer channels).
     int tn = kTN;
+    // Groups of 64 pixels per workgroup (1, 2 or 4; pgroups * wsplit <= 16 waves):
+    // a workgroup covers 64 * pgroups pixels.
+    int pgroups = 4;
     // Fused stride phases of an input gradient: output-channel group kg stores
     // its first channel at element kout[kg] + (pixel's map offset) and has kjn[kg]
     // channels (empty: group kg stores channel 64 kg + j at its map offset).
@@ -581,9 +584,14 @@ ds_status finish_spec(Spec &sp, int bits, int splits, int deep_blocks = 3072)
         const int forced = tuning(kJitWsplit);
         sp.wsplit = forced == 1 || forced == 2 || forced == 4 || forced == 8 || forced == 16 ? forced : ws;
     }
-    // A workgroup covers 256 pixels with 4 waves, 128 with 2 x 4, and 64 with
-    // 4, 8 or 16 waves sharing them.
-    const int tile_pixels = kBlockPixels / std::min(sp.wsplit, 4);
+    // A workgroup covers 256 pixels with 4 waves, 128 with 2 x 2, and 64 with 4,
+    // 8 or 16 waves sharing them, unless forced otherwise.
+    {
+        const int forced = tuning(kJitPgroups);
+        const int dflt = sp.wsplit <= 4 ? 4 / sp.wsplit : 1;
+        sp.pgroups = (forced == 1 || forced == 2 || forced == 4) && forced * sp.wsplit <= 16 ? forced : dflt;
+    }
+    const int tile_pixels = 64 * sp.pgroups;
     sp.tiles_p = int((nq + tile_pixels - 1) / tile_pixels);
     // Split-K: the parts' partial sums meet in y through int32 atomics after a fill
     // pass, a round trip of y per part, so splitting is kept to what the grid needs.
@@ -639,7 +647,7 @@ ds_status finish_spec(Spec &sp, int bits, int splits, int deep_blocks = 3072)
         // 128 -> 256, 3 x 3 / 2 layer at batch 32 (98 tiles of 64 pixels, 12544
         // waves in that form) went from 52 to 76 us, its 256 -> 512, 1 x 1 / 2
         // layer (3200 waves) from 18 to 20 us.
-        const int64_t waves = blocks * ns * std::max(4, sp.wsplit);
+        const int64_t waves = blocks * ns * sp.pgroups * sp.wsplit;
         if (base < 256 && waves < 2048 && !sp.wint && sp.kjn.empty() && tuning(kJitTn) < 0 &&
             tuning(kJitWsplit) < 0) {
             const int64_t per_wave = code_words(sp, kTN) * 4 / (int64_t(sp.kgroups) * ns * sp.wsplit);
@@ -653,6 +661,7 @@ ds_status finish_spec(Spec &sp, int bits, int splits, int deep_blocks = 3072)
                     sp.tn = tn;
                     sp.kgroups = int(kg);
                     sp.wsplit = ws;
+                    sp.pgroups = 1;
                     sp.tiles_p = int((nq + 63) / 64);
                     ns = 1;
                 }
@@ -1150,18 +1159,19 @@ static hipError_t run_part(const ds_jit_conv *plan, const int32_t *x, const int3
         a.pw = padded ? 0 : g.pw;
         a.ybase = int(m.base); a.ynst = m.nstride; a.yrst = m.rstride; a.ycst = m.cstride;
         a.tiles_p = sp.tiles_p;
-        const int per256 = std::min(sp.wsplit, 4);  // pixel tiles per 256 pixels
+        const int per256 = 4 / sp.pgroups;  // pixel tiles per 256 pixels
         a.group_tiles = std::min(plan->group_tiles * per256, sp.tiles_p);
         a.nseg = sp.nseg;
         a.wsplit_log2 = sp.wsplit == 16 ? 4 : sp.wsplit == 8 ? 3 : sp.wsplit == 4 ? 2 : sp.wsplit == 2 ? 1 : 0;
+        a.pgroups_log2 = sp.pgroups == 4 ? 2 : sp.pgroups == 2 ? 1 : 0;
         const int order = tuning(kJitOrder);
         a.tile_major = order < 0 ? sp.tile_major : order >= 0 && order <= 2 ? order : 0;
         a.div_ohow = make_fastdiv(uint32_t(a.OHOW));
         a.div_ow = make_fastdiv(uint32_t(a.OW));
         void *args[] = {&a};
         // LDS: 16 KiB of partial sums per group of 64 pixels in the workgroup.
-        const unsigned lds = sp.wsplit > 1 ? unsigned(4 / per256) * 16384u : 0u;
-        const unsigned threads = 64u * unsigned(std::max(sp.wsplit, 4));
+        const unsigned lds = sp.wsplit > 1 ? unsigned(sp.pgroups) * 16384u : 0u;
+        const unsigned threads = 64u * unsigned(sp.pgroups * sp.wsplit);
         e = hipModuleLaunchKernel(plan->fn, unsigned(int64_t(sp.tiles_p) * sp.nseg), 1, 1,
                                   threads, 1, 1, lds, st, args, nullptr);
     }
@@ -1238,12 +1248,13 @@ extern "C" ds_status ds_jit_conv_query(const ds_jit_conv *plan, int64_t *code_by
 }
 
 extern "C" ds_status ds_jit_conv_layout(const ds_jit_conv *plan, int32_t *channels, int32_t *wsplit,
-                                        int32_t *pixel_tiles)
+                                        int32_t *pixel_groups, int32_t *pixel_tiles)
 {
     if (!plan) return fail(DS_ERR_NULL_POINTER, "plan must not be NULL");
     const ds_jit_conv *k = plan->backward ? (plan->parts.empty() ? nullptr : plan->parts.front()) : plan;
     if (channels) *channels = k ? k->sp.tn : kTN;
     if (wsplit) *wsplit = k ? k->sp.wsplit : 1;
+    if (pixel_groups) *pixel_groups = k ? k->sp.pgroups : 4;
     if (pixel_tiles) *pixel_tiles = k ? k->sp.tiles_p : 0;
     return ok();
 }

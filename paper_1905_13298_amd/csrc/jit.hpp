@@ -21,6 +21,7 @@ struct JitArgs {
     int group_tiles;          // pixel tiles that run all segments before the next tiles
     int nseg;
     int wsplit_log2;          // waves per 64 pixels: 1, 2, 4, 8 or 16, each a share of the reduction
+    int pgroups_log2;         // groups of 64 pixels per workgroup: 1, 2 or 4
     int tile_major;           // block order: 0 grouped, 1 tile-major, 2 XCD-local tile-major
     FastDiv div_ohow, div_ow;
 };

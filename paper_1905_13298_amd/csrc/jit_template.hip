@@ -25,14 +25,17 @@
 // v14, v15 the shifted values and v16..v79 the accumulators; 80 VGPRs, 6
 // waves per SIMD.
 //
-// A workgroup is 4 waves, or 8 or 16 with a split of that many. Without a wave
-// split each wave covers 64 pixels of a 256-pixel tile with the whole reduction
-// of its segment. With a split of 2, 4, 8 or 16 (grids too small to fill the
-// chip otherwise), that many waves share 64 pixels, each with a contiguous
-// share of the reduction in code of its own; they add their partial sums into
-// LDS, which the prologue zeroes, and after a barrier each finishes its share
-// of the segment's channels. v3 holds the lane's LDS byte offset: (pixel group
-// in the workgroup) * 16 KiB + lane * 4, channel j at j * 256 above it.
+// A workgroup covers P groups of 64 pixels (P = 1, 2 or 4) with W waves each
+// (the wave split, W = 1, 2, 4, 8 or 16; P * W <= 16 waves). Without a wave
+// split each wave covers its 64 pixels with the whole reduction of its
+// segment. With a split (grids too small to fill the chip otherwise), the W
+// waves of a pixel group each run a contiguous share of the reduction in code
+// of their own; they add their partial sums into LDS, which the prologue
+// zeroes, and after a barrier each finishes its share of the segment's
+// channels. The P waves running one share's code (one per pixel group) share
+// its instruction fetch on their CU. v3 holds the lane's LDS byte offset:
+// (pixel group in the workgroup) * 16 KiB + lane * 4, channel j at j * 256
+// above it.
 #include <hip/hip_runtime.h>
 
 #include <cstdint>
@@ -79,7 +82,7 @@ __device__ __forceinline__ void jit_conv(const JitArgs &p)
         tile = grp * p.group_tiles + (r - sg * gsize);
     }
     const int seg = __builtin_amdgcn_readfirstlane((sg << wl) + share);
-    const int q = ((wl >= 2 ? tile : tile << (2 - wl)) + pg) * 64 + lane;
+    const int q = ((tile << p.pgroups_log2) + pg) * 64 + lane;
     const int lds = pg * 16384 + lane * 4;
     if (wl > 0) {
         // Each wave zeroes 64 >> wl channels of its pixel group's partial sums.

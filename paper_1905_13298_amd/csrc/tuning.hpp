@@ -15,6 +15,7 @@ enum Knob {
     kJitGroupTiles,  // DS_JIT_GROUP_TILES: pixel tiles per group of the grouped block order
     kJitOrder,       // DS_JIT_ORDER: 0 grouped, 1 tile-major, 2 XCD-local tile-major
     kJitTn,          // DS_JIT_TN: output channels per code segment in a plan (16, 32, 64)
+    kJitPgroups,     // DS_JIT_PGROUPS: groups of 64 pixels per workgroup in a plan (1, 2, 4)
     kKnobs
 };
 

@@ -458,11 +458,13 @@ class JitConv:
         cb, seg, sp = ctypes.c_int64(), ctypes.c_int32(), ctypes.c_int32()
         call("ds_jit_conv_query", self._h, ctypes.byref(cb), ctypes.byref(seg), ctypes.byref(sp))
         self.code_bytes, self.segments, self.splits = cb.value, seg.value, sp.value
-        tn, ws, tiles = ctypes.c_int32(), ctypes.c_int32(), ctypes.c_int32()
-        call("ds_jit_conv_layout", self._h, ctypes.byref(tn), ctypes.byref(ws), ctypes.byref(tiles))
+        tn, ws, pg, tiles = ctypes.c_int32(), ctypes.c_int32(), ctypes.c_int32(), ctypes.c_int32()
+        call("ds_jit_conv_layout", self._h, ctypes.byref(tn), ctypes.byref(ws), ctypes.byref(pg),
+             ctypes.byref(tiles))
         # Output channels per segment, waves per 64 pixels (each streaming code of
-        # its own), and the pixel tiles (workgroups) that run each segment.
-        self.channels, self.wsplit, self.pixel_tiles = tn.value, ws.value, tiles.value
+        # its own), groups of 64 pixels per workgroup, and the pixel tiles
+        # (workgroups) that run each segment.
+        self.channels, self.wsplit, self.pixel_groups, self.pixel_tiles = tn.value, ws.value, pg.value, tiles.value
 
     # Cost model of the two paths on MI355X (microseconds), fitted to calls timed
     # back to back. A plan's waves each stream their share of the straight-line
@@ -471,8 +473,8 @@ class JitConv:
     # at batch 256, 290 KB per wave, 174 us), and the chip issues at most 0.355
     # wave-instructions per SIMD per clock (872 G/s: the ResNet-50 plans, whose
     # waves share their code, and a probe of adds). Code words are about 1.05 per
-    # instruction; each segment's code runs once per wave of each pixel tile
-    # (4, 2 or 1 waves per tile for a wave split of 1, 2 or 4+ with its shares).
+    # instruction; each share's code runs once per group of 64 pixels (a pixel
+    # tile holds 1, 2 or 4 of them).
     # Launch and set-up add about 3 us, a split reduction (fill pass, atomics) 3
     # us more. The runtime kernel decodes its weights and launches 2-5 kernels per
     # call (about 25 us for a convolution, 40 us for a LinearShift, whose operands
@@ -487,8 +489,7 @@ class JitConv:
         """Modelled duration of one run of this plan on MI355X (see the cost
         model above)."""
         streams = max(1, self.segments * self.wsplit)
-        waves_per_tile = 4 // min(max(self.wsplit, 1), 4)
-        executed = self.code_bytes / 4.2 * max(1, self.pixel_tiles) * waves_per_tile
+        executed = self.code_bytes / 4.2 * max(1, self.pixel_tiles) * max(1, self.pixel_groups)
         t = max(self.code_bytes / streams / self.PLAN_STREAM_BPUS, executed / self.PLAN_ISSUE_PER_US)
         return 3.0 + (3.0 if self.splits > 1 else 0.0) + t
 
@@ -524,8 +525,12 @@ class JitConv:
             _dev_i32(residual, "residual")
         y = out if out is not None else torch.empty(self.y_shape, dtype=torch.int32, device=x.device)
         _dev_i32(y, "out")
-        with torch.cuda.device(x.device):
-            call("ds_jit_conv_run", self._h, _ptr(x), _ptr(residual), _ptr(y), _stream(x.device))
+        args = (self._h, _ptr(x), _ptr(residual), _ptr(y), _stream(x.device))
+        if x.device.index == torch.cuda.current_device():
+            call("ds_jit_conv_run", *args)   # (entering the device context costs microseconds)
+        else:
+            with torch.cuda.device(x.device):
+                call("ds_jit_conv_run", *args)
         return y
 
     def close(self):
@@ -593,7 +598,8 @@ def run_layer_plan(plan: JitConv, layer, x: torch.Tensor, out: torch.Tensor | No
 def set_tuning(name: str, value: int) -> None:
     """Sets a tuning override of the library (``ds_set_tuning``): "DS_FORCE_VARIANT",
     "DS_JIT_WSPLIT", "DS_JIT_SLOTS", "DS_JIT_MAP", "DS_JIT_GROUP_TILES",
-    "DS_JIT_ORDER" or "DS_JIT_TN"; a negative value restores the library's own choice."""
+    "DS_JIT_ORDER", "DS_JIT_TN" or "DS_JIT_PGROUPS"; a negative value restores the
+    library's own choice."""
     call("ds_set_tuning", name.encode(), int(value))
 
 

@@ -16,6 +16,7 @@ def fake_plan(n, c, h, w, k, r, s, oh, ow, code_bytes, segments, splits, channel
     p.linear = h == w == r == s == 1
     p.code_bytes, p.segments, p.splits = code_bytes, segments, splits
     p.channels, p.wsplit, p.pixel_tiles = channels, wsplit, tiles
+    p.pixel_groups = 4 // wsplit if wsplit <= 4 else 1
     return p
 
 

@@ -87,7 +87,11 @@ def pad_input(x, pd, xh, xw):
     return xp[:, :, :xh, :xw]
 
 
-def lane_inputs(n, c, h, w, k, r, s, st, pd, wsplit=1):
+def default_pgroups(wsplit):
+    return 4 // wsplit if wsplit <= 4 else 1
+
+
+def lane_inputs(n, c, h, w, k, r, s, st, pd, wsplit=1, pgroups=None):
     """Per lane (pixel q of every 256-pixel tile): tap byte offsets v4..v12 of
     the 3 x 3 window at channel 0 and the output byte offset v13, as the
     template kernel computes them (past-the-end marker for padding and for
@@ -111,8 +115,8 @@ def lane_inputs(n, c, h, w, k, r, s, st, pd, wsplit=1):
             regs[4 + rr * 3 + ss] = np.where(ok, (nn * c * h * w + ih * w + iw) * 4, OOB).astype(np.int64)
     regs[13] = np.where(valid, (nn * k * oh * ow + pix) * 4, OOB).astype(np.int64)
     # v3: LDS byte offset of the lane's pixel in its workgroup (wave split; a
-    # workgroup covers 256 // wsplit pixels, and 64 from a split of 4 up)
-    within = q % (256 // min(wsplit, 4))
+    # workgroup covers 64 pixels per pixel group)
+    within = q % (64 * (pgroups or default_pgroups(wsplit)))
     regs[3] = ((within // 64) * 16384 + (within % 64) * 4).astype(np.int64)
     return regs, (oh, ow)
 
@@ -124,9 +128,10 @@ class Interp:
     row of 64 channels per lane (pixel); an LDS access must land in the lane's
     own row."""
 
-    def __init__(self, insts, bufs, wsplit=1):
+    def __init__(self, insts, bufs, wsplit=1, pgroups=None):
         self.insts, self.bufs = insts, bufs   # bufs: sgpr base -> (uint32 array, num_records)
         self.wsplit = wsplit
+        self.pgroups = pgroups or default_pgroups(wsplit)
 
     @staticmethod
     def reg(tok):
@@ -139,7 +144,7 @@ class Interp:
         pending = collections.OrderedDict()   # vgpr -> value, in issue order
         lgkm = {}                              # vgpr -> value of an LDS read in flight
         q = np.arange(V[3].size)
-        tile_px = 256 // min(self.wsplit, 4)
+        tile_px = 64 * self.pgroups
         pc = start
         steps = 0
 
@@ -305,6 +310,12 @@ CASES = [
     (2, 13, 9, 9, 50, 3, 3, 1, 1, 3, "none", 4, 32),
     (33, 90, 1, 1, 37, 1, 1, 1, 0, 1, "full", 16, 16),
     (1, 3, 13, 11, 40, 7, 7, 2, 3, 1, "relu", 8, 16),  # padded copy
+    # several groups of 64 pixels per workgroup, each with a wave split
+    (2, 40, 9, 9, 70, 3, 3, 1, 1, 1, "full", 4, 64, 4),   # 16 waves: 4 groups x 4 shares
+    (33, 300, 1, 1, 130, 1, 1, 1, 0, 2, "none", 4, 64, 4),
+    (2, 37, 7, 6, 70, 3, 3, 2, 1, 1, "full", 8, 32, 2),
+    (3, 13, 9, 9, 50, 3, 3, 1, 1, 1, "relu", 1, 64, 1),   # one wave per workgroup
+    (1, 3, 13, 11, 40, 7, 7, 2, 3, 1, "mul", 2, 16, 4),   # padded copy
 ]
 
 
@@ -312,7 +323,8 @@ CASES = [
 def test_generated_code_matches_oracle(case, tmp_path, knob):
     wsplit = case[11] if len(case) > 11 else 1
     tn = case[12] if len(case) > 12 else 64
-    run_generated(case[:11] + (wsplit, tn), zlib.crc32(str(case).encode()), 0.1, tmp_path, knob)
+    pgroups = case[13] if len(case) > 13 else None
+    run_generated(case[:11] + (wsplit, tn, pgroups), zlib.crc32(str(case).encode()), 0.1, tmp_path, knob)
 
 
 def random_cases(count, seed=1905):
@@ -334,7 +346,8 @@ def random_cases(count, seed=1905):
         tn = int(rng.choice([16, 32, 64, 64]))
         epi = str(rng.choice(["none", "relu", "mul", "full"]))
         zero = float(rng.choice([0.0, 0.1, 0.5, 0.95]))
-        out.append(((n, c, h, w, k, r, s, st, pd, splits, epi, wsplit, tn), zero))
+        pg = int(rng.choice([p for p in (1, 2, 4) if p * wsplit <= 16]))
+        out.append(((n, c, h, w, k, r, s, st, pd, splits, epi, wsplit, tn, pg), zero))
     return out
 
 
@@ -350,9 +363,10 @@ def run_generated(case, seed, zero_frac, tmp_path, knob):
     """Generate a plan's code object for `case` (n, c, h, w, k, r, s, stride, pad,
     splits, epilogue, wave split, channels per segment), run it in the
     interpreter over every lane, and compare with the oracle."""
-    n, c, h, w, k, r, s, st, pd, splits, epi, wsplit, tn = case
+    n, c, h, w, k, r, s, st, pd, splits, epi, wsplit, tn, pgroups = case
     knob("DS_JIT_WSPLIT", wsplit)
     knob("DS_JIT_TN", tn)
+    knob("DS_JIT_PGROUPS", pgroups or -1)
     codes, x, rng = gen_layer(seed, n, c, h, w, k, r, s, zero_frac)
     bias = rng.integers(-(2 ** 31), 2 ** 31, k, dtype=np.int64).astype(np.int32)
     mul = add = res = None
@@ -362,7 +376,7 @@ def run_generated(case, seed, zero_frac, tmp_path, knob):
         add = rng.integers(-(2 ** 31), 2 ** 31, k, dtype=np.int64).astype(np.int32)
         add[0] = 0
     wp = ops.pack_shift_weights(codes)
-    lanes, (oh, ow) = lane_inputs(n, c, h, w, k, r, s, st, pd, wsplit)
+    lanes, (oh, ow) = lane_inputs(n, c, h, w, k, r, s, st, pd, wsplit, pgroups)
     if epi == "full":
         res = rng.integers(-(2 ** 31), 2 ** 31, (n, k, oh, ow), dtype=np.int64).astype(np.int32)
     img = ops.jit_conv_image(wp, (n, c, h, w), (r, s), st, pd, bias=bias, mul=mul, add=add,
@@ -397,7 +411,7 @@ def run_generated(case, seed, zero_frac, tmp_path, knob):
         y[:] = np.repeat(np.tile(bias.view(np.uint32).astype(np.int64), n), oh * ow)
     stubs = sum(1 for op, _, _ in insts.values() if op == "s_getpc_b64")
     assert stubs == kgroups * nsplit * wsplit
-    interp = Interp(insts, bufs, wsplit)
+    interp = Interp(insts, bufs, wsplit, pgroups)
     total = collections.Counter()
     for seg in range(kgroups * nsplit):
         # the waves of one pixel group: each share up to the barrier, then each to the end
@@ -468,7 +482,7 @@ def test_small_grids_run_unsplit_in_16_channel_segments(tmp_path, knob):
     old = ops.jit_conv_image(wp, (1, 32, 10, 10), 3, 1, 1)
     names = collections.Counter(op for op, _, _ in disassemble(old, str(tmp_path)).values())
     assert names["buffer_atomic_add"] > 0
-    run_generated((1, 32, 10, 10, 40, 3, 3, 1, 1, 1, "full", 4, 16), 7, 0.1, tmp_path, knob)
+    run_generated((1, 32, 10, 10, 40, 3, 3, 1, 1, 1, "full", 4, 16, 1), 7, 0.1, tmp_path, knob)
 
 
 @pytest.mark.parametrize("bits", [2, 3, 4])
