@@ -399,11 +399,14 @@ def bench_network(args):
     nz = sum(graph[i]["layer"].sac * float(np.mean((params[graph[i]["layer"].name]["codes"] & 15) != 15))
              for i in conv_idx)
 
-    def timed(net):
+    step_calls = {}
+
+    def timed(net, name):
         calls = []
         buf = {"x": x}
         for op in graph:
             calls.append(lambda op=op: net.run_op(op, buf))
+        step_calls[name] = (calls, buf)
         return time_layers(calls, args.steps, args.warmup, stream)
 
     nets = {"runtime": ShiftNetwork(graph, params, device=dev)}
@@ -415,8 +418,16 @@ def bench_network(args):
             if not torch.equal(a_out[op["dst"]], b_out[op["dst"]]):
                 raise SystemExit(f"{op['dst']}: weight-specialised and runtime outputs differ")
         del a_out, b_out
-    results = {p: timed(net) for p, net in nets.items()}
+    results = {p: timed(net, p) for p, net in nets.items()}
     ms_per_step, d = results[args.path]
+    timing = {"mode": "eager", "eager_ms_per_step": round(ms_per_step, 5)}
+    if args.path == "jit" and not args.eager:
+        # every op writes a buffer of its own that the network keeps: the graph's
+        # outputs are those buffers
+        calls, buf = step_calls["jit"]
+        ms_per_step, rep = time_graph(calls, [buf[op["dst"]] for op in graph], args.steps, args.warmup)
+        timing = {"mode": "HIP graph of consecutive steps, replayed", "steps_per_graph": rep,
+                  "graph_ms_per_step": round(ms_per_step, 5), "eager_ms_per_step": timing["eager_ms_per_step"]}
     op_ms = d.mean(axis=0)
     conv_ms = float(sum(op_ms[i] for i in conv_idx))
     per_kind = {}
@@ -467,6 +478,7 @@ def bench_network(args):
         "config": {"workload": f"resnet18_forward_n{n}_224", "batch": n, "ops": len(graph),
                    "sac_per_step": sac, "nonzero_sac_per_step": int(nz), "frac_bits": W.FRAC_BITS,
                    "parallelism": "single GPU"},
+        "timing": timing,
         "ms_by_op": per_kind, "roofline": roofline, "runtime_weights": runtime, "cpu_baseline": cpu,
     }
     print(json.dumps(out), flush=True)
@@ -537,6 +549,11 @@ def bench_backward(args):
                 raise SystemExit(f"{layers[i][1].name}: plan and runtime input gradients differ")
         torch.cuda.synchronize()
     ms_per_step, d = time_layers(calls, args.steps, args.warmup, stream)
+    timing = {"mode": "eager", "eager_ms_per_step": round(ms_per_step, 5)}
+    if args.path == "jit" and not args.eager and all(p is not None for p in plans):
+        ms_per_step, rep = time_graph(calls, [k[2] for k in keep], args.steps, args.warmup)
+        timing = {"mode": "HIP graph of consecutive steps, replayed", "steps_per_graph": rep,
+                  "graph_ms_per_step": round(ms_per_step, 5), "eager_ms_per_step": timing["eager_ms_per_step"]}
     sac_step = sum(L.sac for _, L in layers)
     nz_step = sum(L.sac * f for (_, L), f in zip(layers, nonzero))
     value = sac_step / (ms_per_step * 1e-3) / 1e9
@@ -617,6 +634,7 @@ def bench_backward(args):
         "config": {"workload": W.CONFIG_NAMES[cfg] + "_backward_data", "layers": len(layers),
                    "batch": layers[0][1].n, "frac_bits": W.FRAC_BITS, "sac_per_step": sac_step,
                    "grad": "rint(N(0,1) * 2^16), signed", "parallelism": "single GPU"},
+        "timing": timing,
         "roofline": roofline, "runtime_weights": runtime, "cpu_baseline": cpu,
     }
     if args.layers_out:
