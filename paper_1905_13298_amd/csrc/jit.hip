@@ -633,37 +633,49 @@ ds_status finish_spec(Spec &sp, int bits, int splits, int deep_blocks = 3072)
         if (tiles256 < 4) want = blocks >= 256 ? 1 : std::min<int64_t>(want, 4);
         ns = int(std::max<int64_t>(1, want));
         // (6) Grids of under 2048 waves (2 per SIMD) are bound by how fast each
-        // wave streams its straight-line code, and a split of the reduction adds a
-        // fill pass and atomics. When the choice above splits, or leaves a wave
-        // more than 14 KiB of code, segments of 16 channels run unsplit with a wave
-        // split of 4, or 8 where 4 would leave a wave more than 14 KiB (up to 112
-        // KiB per workgroup): more, shorter code streams on more CUs, at the price
-        // of forming each shift for 16 channels only. On MI355X (calls timed back
-        // to back): 128 -> 128, 3 x 3, 28 x 28, batch 1: 13.6 -> 10.7 us (split 8);
-        // 512 -> 1000 at batch 32: 14.2 -> 11.0 us; 256 -> 128 at batch 8: 12.2 ->
-        // 10.7 us. 2048 -> 1000 at batch 128 (190 KiB per group of 16 channels)
-        // ran 61-65 us unsplit with any wave split or segment width, against 40 us
-        // in 4 parts. The new grid must stay under 2048 waves as well: ResNet-18's
-        // 128 -> 256, 3 x 3 / 2 layer at batch 32 (98 tiles of 64 pixels, 12544
-        // waves in that form) went from 52 to 76 us, its 256 -> 512, 1 x 1 / 2
-        // layer (3200 waves) from 18 to 20 us.
+        // wave streams its straight-line code. When the choice above splits the
+        // reduction or leaves a wave more than 14 KiB of code, segments of 16
+        // channels run with a wave split of 4, or 8 where 4 would leave a wave
+        // more than 14 KiB (up to 112 KiB per workgroup): more, shorter code
+        // streams on more CUs, at the price of forming each shift for 16 channels
+        // only. A grid of at most 32 waves doubles the split while it stays within
+        // 64 waves, and a grid of 4 or more pixel tiles that fits one workgroup per
+        // CU twice over is split in 2 parts (its tiles share each code stream, so
+        // the shorter streams pay for the fill pass). On MI355X, kernels replayed
+        // in a HIP graph: 128 -> 128, 3 x 3 at 28 x 28, batch 1 (13 tiles): 10.8
+        // us (64 channels, 12 parts) -> 9.7 (16 channels, split 8) -> 8.2 us (in
+        // 2 parts; 3 parts, 312 workgroups on 256 CUs: 10.2 us); 256 -> 128 at
+        // batch 8: 11.6 (64 channels, split 4) -> 5.4 -> 4.0 us (split 8); 512 ->
+        // 1000 at batch 32 (one tile): 14.2 -> 10.0 us (2 parts: 10.4). 2048 ->
+        // 1000 at batch 128 (190 KiB per group of 16 channels) ran 61-65 us unsplit
+        // with any wave split or segment width, against 40 us in 4 parts. The new
+        // grid stays under 2048 waves too: ResNet-18's 128 -> 256, 3 x 3 / 2 layer
+        // at batch 32 (98 tiles, 12544 waves in that form) went from 52 to 76 us,
+        // its 256 -> 512, 1 x 1 / 2 layer (3200 waves) from 18 to 20 us.
         const int64_t waves = blocks * ns * sp.pgroups * sp.wsplit;
         if (base < 256 && waves < 2048 && !sp.wint && sp.kjn.empty() && tuning(kJitTn) < 0 &&
-            tuning(kJitWsplit) < 0) {
+            tuning(kJitWsplit) < 0 && tuning(kJitPgroups) < 0) {
             const int64_t per_wave = code_words(sp, kTN) * 4 / (int64_t(sp.kgroups) * ns * sp.wsplit);
             if (ns > 1 || per_wave > 14 * 1024) {
                 const int tn = 16;
                 const int64_t kg = (g.k + tn - 1) / tn;
                 const int64_t per_group = code_words(sp, tn) * 4 / kg;
-                const int ws = per_group <= 56 * 1024 ? 4 : 8;
-                const int64_t new_waves = (nq + 63) / 64 * kg * ws;
-                if (per_group <= 112 * 1024 && g.crs >= 8 * ws && new_waves < 2048) {
+                const int64_t tiles = (nq + 63) / 64;
+                int ws = per_group <= 56 * 1024 ? 4 : 8;
+                int64_t w = tiles * kg * ws;
+                if (per_group <= 112 * 1024 && g.crs >= 8 * ws && w < 2048) {
+                    while (ws < 16 && w <= 32 && g.crs >= 16 * ws) {
+                        ws *= 2;
+                        w *= 2;
+                    }
+                    const bool two = tiles >= 4 && tiles * kg * 2 <= 256 && per_group / ws > 4 * 1024 &&
+                                     g.c >= 2;
                     sp.tn = tn;
                     sp.kgroups = int(kg);
                     sp.wsplit = ws;
                     sp.pgroups = 1;
-                    sp.tiles_p = int((nq + 63) / 64);
-                    ns = 1;
+                    sp.tiles_p = int(tiles);
+                    ns = two ? 2 : 1;
                 }
             }
         }

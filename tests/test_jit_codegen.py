@@ -467,22 +467,39 @@ def test_zero_weights_emit_no_arithmetic(tmp_path):
 
 def test_small_grids_run_unsplit_in_16_channel_segments(tmp_path, knob):
     """A grid of a few waves whose default plan would split the reduction runs
-    unsplit in segments of 16 channels with a wave split of 4 (no fill pass, no
-    atomics): the same code as that configuration forced, and correct."""
+    unsplit in segments of 16 channels with a wave split of 8 (24 waves at a split
+    of 4 double to 48; no fill pass, no atomics): the same code as that
+    configuration forced, and correct."""
     codes, _, _ = gen_layer(7, 1, 32, 10, 10, 40, 3, 3)
     wp = ops.pack_shift_weights(codes)
     auto = ops.jit_conv_image(wp, (1, 32, 10, 10), 3, 1, 1)
     names = collections.Counter(op for op, _, _ in disassemble(auto, str(tmp_path)).values())
-    assert names["s_getpc_b64"] == 3 * 4 and names["buffer_atomic_add"] == 0
+    assert names["s_getpc_b64"] == 3 * 8 and names["buffer_atomic_add"] == 0
     knob("DS_JIT_TN", 16)
-    knob("DS_JIT_WSPLIT", 4)
+    knob("DS_JIT_WSPLIT", 8)
     assert ops.jit_conv_image(wp, (1, 32, 10, 10), 3, 1, 1, splits=1) == auto
     knob("DS_JIT_TN", 64)     # segments of 64 forced: the split plan of the older rule
     knob("DS_JIT_WSPLIT", -1)
     old = ops.jit_conv_image(wp, (1, 32, 10, 10), 3, 1, 1)
     names = collections.Counter(op for op, _, _ in disassemble(old, str(tmp_path)).values())
     assert names["buffer_atomic_add"] > 0
-    run_generated((1, 32, 10, 10, 40, 3, 3, 1, 1, 1, "full", 4, 16, 1), 7, 0.1, tmp_path, knob)
+    run_generated((1, 32, 10, 10, 40, 3, 3, 1, 1, 1, "full", 8, 16, 1), 7, 0.1, tmp_path, knob)
+
+
+def test_small_grids_of_several_tiles_split_in_two(tmp_path, knob):
+    """Four or more pixel tiles sharing each code stream, one workgroup per CU
+    twice over: 16-channel segments in 2 parts (fill pass and atomics), the code
+    of that configuration forced."""
+    codes, _, _ = gen_layer(8, 1, 64, 20, 20, 64, 3, 3)
+    wp = ops.pack_shift_weights(codes)
+    auto = ops.jit_conv_image(wp, (1, 64, 20, 20), 3, 1, 1)
+    names = collections.Counter(op for op, _, _ in disassemble(auto, str(tmp_path)).values())
+    # 7 tiles of 64 pixels x 4 groups of 16 channels; about 60 KiB of code per
+    # group, so a wave split of 8 (7.5 KiB per wave)
+    knob("DS_JIT_TN", 16)
+    knob("DS_JIT_WSPLIT", 8)
+    assert ops.jit_conv_image(wp, (1, 64, 20, 20), 3, 1, 1, splits=2) == auto
+    assert names["s_getpc_b64"] == 4 * 2 * 8 and names["buffer_atomic_add"] > 0
 
 
 @pytest.mark.parametrize("bits", [2, 3, 4])
