@@ -169,7 +169,7 @@ def _pmc_rows(directory: str):
     return [rows[k] for k in sorted(rows)]
 
 
-MAIN_KERNELS = ("tiled_kernel", "conv_direct_kernel") + JIT_ENTRY_POINTS
+MAIN_KERNELS = ("tiled_kernel", "conv_direct_kernel", "linear_rows_kernel") + JIT_ENTRY_POINTS
 
 
 def _main_rows(rows, layers):
@@ -906,7 +906,11 @@ def bench_layers(args):
     else:
         ms_per_step, d = time_layers(runtime_calls, args.steps, args.warmup, stream)
     timing = {"mode": "eager", "eager_ms_per_step": round(ms_per_step, 5)}
-    if args.path == "jit" and not args.eager and all(p is not None for p in plans):
+    # Graph replay when every call launches kernels only: plans, and LinearShift
+    # layers on the small-batch runtime kernel (no scratch; its fill pass is a kernel).
+    def graphable(L, plan):
+        return plan is not None or (L.kind == "linear" and ops.describe_conv2d(L.n, L.c, 1, 1, L.k, 1) == "rows")
+    if args.path == "jit" and not args.eager and all(graphable(L, p) for L, p in zip(layers, plans)):
         ms_per_step, rep = time_graph(jit_calls, [r[4] for r in res], args.steps, args.warmup)
         timing = {"mode": "HIP graph of consecutive steps, replayed", "steps_per_graph": rep,
                   "graph_ms_per_step": round(ms_per_step, 5), "eager_ms_per_step": timing["eager_ms_per_step"]}

@@ -37,7 +37,8 @@
  * take host pointers. y must not overlap any input. The runtime-weights
  * entry points (ds_linear_shift, ds_conv2d_shift and their variants) take
  * device scratch memory (decoded weights, per-channel start values, transposed
- * operands) in stream order from the device's default memory pool
+ * operands; none for a LinearShift of fewer than 256 rows, whose kernel decodes
+ * the packed codes itself) in stream order from the device's default memory pool
  * (hipMallocAsync) and give it back in stream order (hipFreeAsync) within the
  * same call: the library keeps no pool and no device memory between calls.
  * Under the runtime's default release threshold the memory returns to the

@@ -40,6 +40,8 @@ namespace ds {
 
 int forced_variant() { return tuning(kForceVariant); }
 
+static bool rows_path(const ConvGeom &g, const OutMap &map, const Padded &pad);
+
 // ---------------------------------------------------------------------------
 // Scratch memory: stream-ordered allocations from the device's default memory
 // pool (hipMallocAsync), freed in stream order (hipFreeAsync) once the call's
@@ -810,6 +812,10 @@ static ConvGeom tiled_geometry(const ConvGeom &g, bool &rowmajor)
 
 void describe_conv(const ConvGeom &g0, char *buf, size_t len)
 {
+    if (rows_path(g0, OutMap(), Padded())) {
+        snprintf(buf, len, "rows");
+        return;
+    }
     bool rowmajor = false;
     const ConvGeom g = tiled_geometry(g0, rowmajor);
     int plane = 0;
@@ -941,6 +947,203 @@ struct ConvLayout {
     size_t scratch_bytes() const { return init_bytes + wd_bytes + xt_bytes + yt_bytes; }
 };
 
+// ---------------------------------------------------------------------------
+// Small-batch LinearShift (a 1 x 1 problem on 1 x 1 inputs with fewer than 256
+// rows): lanes own output channels instead of batch rows, so that a few rows do
+// not leave the tiled kernel's 256-row tiles almost empty (at batch 1 it uses
+// one lane in 256). A workgroup of 16 waves covers 64 output channels and up to
+// 8 batch rows; its waves split the reduction into 16 contiguous ranges of
+// packed words and add their partial sums in LDS. Each lane decodes its own
+// channel's codes (a 64-byte line of its row holds 96 five-bit codes) and reads
+// the inputs as wave-uniform scalars. Per term: the shifted input, masked to 0
+// for a zero weight, xor'ed with the sign mask and added; the +1 that turns
+// ~t into -t is added once per negative weight as a count. The multiplication
+// operators run in the same tiling with int32 weights (the comparison kernel).
+constexpr int kRowsWaves = 16;
+
+struct RowsArgs {
+    const uint32_t *wp;   // packed codes [K][wpr] (Shift)
+    const int32_t *wi;    // int32 weights [K][C] (Mul, Mul24)
+    const int32_t *bias;  // [K] or NULL
+    int32_t *y;           // [B][K]
+    int B, C, K, wpr;
+    Epilogue epi;
+};
+
+// ROWS batch rows per workgroup (1, 2, 4 or 8: the smallest power of two that
+// covers the batch, up to 8); BITS-bit codes, 32 / BITS per word. Rows past
+// the batch read the last row again and are not stored, so the inner loops have
+// no branch; inputs past the last column are read at the last column, under
+// zero codes (packed rows are padded with them). The reduction runs in chunks
+// of 8 packed words: each lane loads its row's 8 words and the wave stages the
+// chunk's inputs of its ROWS rows in LDS (coalesced loads, all issued
+// together), then reads them back as broadcasts. gridDim.z > 1 splits the
+// reduction over that many workgroups per block of channels and rows, whose
+// sums meet in y through int32 atomics after a fill pass (no epilogue then).
+constexpr int kRowsWords = 8;
+
+template <Inner OP, int ROWS, int BITS>
+__global__ void __launch_bounds__(1024)
+linear_rows_kernel(const int32_t *__restrict__ x, const RowsArgs a)
+{
+    constexpr int PER = OP == Inner::Shift ? 32 / BITS : 1;  // reduction columns per unit
+    constexpr int U = OP == Inner::Shift ? kRowsWords : 64;  // units per chunk
+    constexpr int E = U * PER;                               // columns per chunk
+    __shared__ uint32_t part[kRowsWaves][ROWS][64];
+    __shared__ int32_t xbuf[kRowsWaves][ROWS][E];
+    const int lane = threadIdx.x & 63;
+    const int wave = __builtin_amdgcn_readfirstlane(int(threadIdx.x >> 6));
+    const int k = int(blockIdx.x) * 64 + lane;
+    const int kc = min(k, a.K - 1);  // lanes past K compute a copy of the last channel, not stored
+    const int b0 = int(blockIdx.y) * ROWS;
+    const int nb = min(ROWS, a.B - b0);
+    const int nsplit = int(gridDim.z), part_i = int(blockIdx.z);
+    uint32_t acc[ROWS];
+#pragma unroll
+    for (int r = 0; r < ROWS; ++r) acc[r] = 0u;
+    uint32_t ncount = 0u;
+    // This wave's share [u0, u1) of the units (packed words, or input columns for
+    // the multiplication operators): part part_i of nsplit, then 1/16 of it.
+    const int units = OP == Inner::Shift ? a.wpr : a.C;
+    const int p0 = int(int64_t(units) * part_i / nsplit), p1 = int(int64_t(units) * (part_i + 1) / nsplit);
+    const int u0 = p0 + int(int64_t(p1 - p0) * wave / kRowsWaves);
+    const int u1 = p0 + int(int64_t(p1 - p0) * (wave + 1) / kRowsWaves);
+    const CodeFmt fmt{BITS, 32 / BITS};
+    for (int uc = u0; uc < u1; uc += U) {
+        // This chunk's weights (one load per unit and lane) and inputs (staged).
+        uint32_t wv[OP == Inner::Shift ? U : 1];
+        if constexpr (OP == Inner::Shift) {
+            const uint32_t *row = a.wp + int64_t(kc) * a.wpr;
+#pragma unroll
+            for (int u = 0; u < U; ++u) wv[u] = row[min(uc + u, u1 - 1)];
+        }
+        const int cb = uc * PER;
+#pragma unroll
+        for (int r = 0; r < ROWS; ++r) {
+            const int32_t *xrow = x + int64_t(b0 + min(r, nb - 1)) * a.C;
+#pragma unroll
+            for (int e = lane; e < E; e += 64) xbuf[wave][r][e] = xrow[min(cb + e, a.C - 1)];
+        }
+        // (LDS is written and read back by the same wave: in order, no barrier.)
+        const int un = min(U, u1 - uc);
+        if constexpr (OP == Inner::Shift) {
+#pragma unroll
+            for (int u = 0; u < U; ++u) {
+                if (u >= un) break;
+#pragma unroll
+                for (int j = 0; j < PER; ++j) {
+                    const uint32_t code = fmt.canonical((wv[u] >> (BITS * j)) & ((1u << BITS) - 1u));
+                    const int sh = int(code & 15u);
+                    int32_t z = sh == 15 ? 0 : -1;                 // zero weight: the term is 0
+                    uint32_t neg = (code & 16u) ? uint32_t(z) : 0u;  // negative: ~t, the +1 counted
+                    ncount += neg & 1u;
+                    // Kept in registers as masks (an and and a xor per term, not selects).
+                    asm volatile("" : "+v"(z), "+v"(neg));
+#pragma unroll
+                    for (int r = 0; r < ROWS; ++r)
+                        acc[r] += uint32_t((xbuf[wave][r][u * PER + j] & z) >> sh) ^ neg;
+                }
+            }
+        } else {
+            const int32_t *wrow = a.wi + int64_t(kc) * a.C;
+            for (int u = 0; u < un; ++u) {
+                const int32_t w = wrow[uc + u];
+#pragma unroll
+                for (int r = 0; r < ROWS; ++r) {
+                    const int32_t xv = xbuf[wave][r][u];
+                    acc[r] += OP == Inner::Mul ? uint32_t(xv) * uint32_t(w) : mul24(xv, w);
+                }
+            }
+        }
+    }
+#pragma unroll
+    for (int r = 0; r < ROWS; ++r) part[wave][r][lane] = acc[r] + ncount;
+    __syncthreads();
+    // Wave r finishes batch row b0 + r: the 16 partial sums, then bias and
+    // epilogue, or (split) an atomic add into y, which holds the bias.
+    if (wave < nb && k < a.K) {
+        uint32_t v = 0u;
+        for (int q = 0; q < kRowsWaves; ++q) v += part[q][wave][lane];
+        const int64_t o = int64_t(b0 + wave) * a.K + k;
+        if (nsplit > 1) {
+            atomicAdd(reinterpret_cast<unsigned int *>(a.y + o), v);
+        } else {
+            v += a.bias ? uint32_t(a.bias[k]) : 0u;
+            a.y[o] = int32_t(apply_epilogue(v, k, o, a.epi));
+        }
+    }
+}
+
+template <Inner OP, int ROWS>
+static void launch_rows(dim3 grid, const int32_t *x, const RowsArgs &a, int bits, hipStream_t st)
+{
+    const dim3 block(64 * kRowsWaves);
+    if constexpr (OP != Inner::Shift) {
+        hipLaunchKernelGGL((linear_rows_kernel<OP, ROWS, 5>), grid, block, 0, st, x, a);
+    } else if (bits == 5) {
+        hipLaunchKernelGGL((linear_rows_kernel<OP, ROWS, 5>), grid, block, 0, st, x, a);
+    } else if (bits == 4) {
+        hipLaunchKernelGGL((linear_rows_kernel<OP, ROWS, 4>), grid, block, 0, st, x, a);
+    } else if (bits == 3) {
+        hipLaunchKernelGGL((linear_rows_kernel<OP, ROWS, 3>), grid, block, 0, st, x, a);
+    } else {
+        hipLaunchKernelGGL((linear_rows_kernel<OP, ROWS, 2>), grid, block, 0, st, x, a);
+    }
+}
+
+// Batch rows per workgroup: the smallest power of two covering the batch, at most 8.
+static int rows_per_block(int n) { return n >= 8 ? 8 : n >= 4 ? 4 : n >= 2 ? 2 : 1; }
+
+template <Inner OP>
+static void launch_rows_op(const ConvGeom &g, const int32_t *x, const RowsArgs &a, int splits, hipStream_t st)
+{
+    const int rows = rows_per_block(g.n);
+    const dim3 grid(unsigned((g.k + 63) / 64), unsigned((g.n + rows - 1) / rows), unsigned(splits));
+    if (rows == 8) launch_rows<OP, 8>(grid, x, a, g.bits, st);
+    else if (rows == 4) launch_rows<OP, 4>(grid, x, a, g.bits, st);
+    else if (rows == 2) launch_rows<OP, 2>(grid, x, a, g.bits, st);
+    else launch_rows<OP, 1>(grid, x, a, g.bits, st);
+}
+
+// Whether a problem takes the small-batch LinearShift kernel: 1 x 1 taps on
+// 1 x 1 inputs, dense output, fewer than 256 rows, no forced variant.
+static bool rows_path(const ConvGeom &g, const OutMap &map, const Padded &pad)
+{
+    return g.h == 1 && g.w == 1 && g.r == 1 && g.s == 1 && g.ph == 0 && g.pw == 0 && map.dense() &&
+           pad.vh == 0 && pad.iwp == 0 && g.n < 256 && forced_variant() < 0;
+}
+
+static hipError_t run_rows(const ConvGeom &g, const int32_t *x, const uint32_t *wp, const int32_t *wi,
+                           const int32_t *bias, int32_t *y, Inner op, hipStream_t st, const Epilogue &epi)
+{
+    // Fewer than 256 workgroups of 16 waves leave CUs idle and each wave a long
+    // walk along its weight rows: the reduction is split over up to 8 workgroups
+    // per block (each wave keeping at least 2 units), when there is no epilogue.
+    const int64_t blocks = int64_t((g.k + 63) / 64) * ((g.n + rows_per_block(g.n) - 1) / rows_per_block(g.n));
+    const int units = op == Inner::Shift ? int(row_words_bits(g.c, g.bits)) : g.c;
+    int splits = 1;
+    if (!epi.any())
+        while (splits < 8 && blocks * splits < 256 && units / (kRowsWaves * splits * 2) >= 2) splits *= 2;
+    if (splits > 1) {
+        const hipError_t e = bias ? run_fill_init(g, bias, y, st) : run_fill_zero(y, int64_t(g.n) * g.k, st);
+        if (e != hipSuccess) return e;
+    }
+    RowsArgs a;
+    a.wp = wp;
+    a.wi = wi;
+    a.bias = bias;
+    a.y = y;
+    a.B = g.n;
+    a.C = g.c;
+    a.K = g.k;
+    a.wpr = int(row_words_bits(g.c, g.bits));
+    a.epi = epi;
+    if (op == Inner::Shift) launch_rows_op<Inner::Shift>(g, x, a, splits, st);
+    else if (op == Inner::Mul) launch_rows_op<Inner::Mul>(g, x, a, splits, st);
+    else launch_rows_op<Inner::Mul24>(g, x, a, splits, st);
+    return hipGetLastError();
+}
+
 static ConvLayout conv_layout(const ConvGeom &g0, const OutMap &map, const Padded &pad)
 {
     ConvLayout L;
@@ -973,6 +1176,7 @@ static ConvLayout conv_layout(const ConvGeom &g0, const OutMap &map, const Padde
 
 size_t conv_scratch_bytes(const ConvGeom &g0, const OutMap &map, const Padded &pad)
 {
+    if (rows_path(g0, map, pad)) return 0;
     const ConvLayout L = conv_layout(g0, map, pad);
     return L.direct ? 0 : L.scratch_bytes();
 }
@@ -981,6 +1185,7 @@ hipError_t run_conv(const ConvGeom &g0, const int32_t *x, const uint32_t *wp, co
                     const int32_t *bias, int32_t *y, Inner op, hipStream_t st, const Epilogue &epi,
                     const OutMap &map, const Padded &pad, const Workspace &ws)
 {
+    if (rows_path(g0, map, pad)) return run_rows(g0, x, wp, wi, bias, y, op, st, epi);
     const ConvLayout L = conv_layout(g0, map, pad);
     const ConvGeom &g = L.g;
     const bool mapped = L.mapped, rowmajor = L.rowmajor;

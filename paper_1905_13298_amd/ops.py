@@ -477,13 +477,17 @@ class JitConv:
     # tile holds 1, 2 or 4 of them).
     # Launch and set-up add about 3 us, a split reduction (fill pass, atomics) 3
     # us more. The runtime kernel decodes its weights and launches 2-5 kernels per
-    # call (about 25 us for a convolution, 40 us for a LinearShift, whose operands
-    # it transposes), then runs at up to 15 T dense SACs/s on full tiles of 256
-    # output pixels (batch rows for a LinearShift; a ragged last tile wastes its
-    # lanes), reading its packed weights at 4 TB/s.
+    # call (about 25 us for a convolution, 40 us for a LinearShift at 256 rows or
+    # more, whose operands it transposes), then runs at up to 15 T dense SACs/s
+    # on full tiles of 256 output pixels (a ragged last tile wastes its lanes),
+    # reading its packed weights at 4 TB/s. A LinearShift of fewer than 256 rows
+    # takes the small-batch kernel instead (lanes own output channels): about 6
+    # us plus 9.6 T dense SACs/s, or its packed weights at 1.5 TB/s when they
+    # dominate (each lane walks its own row).
     PLAN_STREAM_BPUS = 1.6e3        # code bytes per us per wave
     PLAN_ISSUE_PER_US = 872e3       # wave-instructions per us, whole chip
     RUNTIME_SAC_PER_US = 15e6       # dense SACs per us on full tiles
+    ROWS_SAC_PER_US = 9.6e6         # dense SACs per us, small-batch LinearShift kernel
 
     def estimate_us(self) -> float:
         """Modelled duration of one run of this plan on MI355X (see the cost
@@ -497,24 +501,26 @@ class JitConv:
         """Modelled duration of the same layer on the runtime kernel
         (ds_conv2d_shift / ds_linear_shift)."""
         nq = max(1, self.out_pixels)
-        fill = nq / (-(-nq // 256) * 256)
         weight_bytes = self.out_channels * packed_row_words(self.crs) * 4
+        if self.linear and nq < 256:
+            return 6.0 + max(self.sac / self.ROWS_SAC_PER_US, weight_bytes / 1.5e6)
+        fill = nq / (-(-nq // 256) * 256)
         return ((40.0 if self.linear else 25.0) + self.sac / (self.RUNTIME_SAC_PER_US * fill)
                 + weight_bytes / 4e6)
 
     @property
     def preferred(self) -> bool:
         """Whether this plan is expected to beat the runtime kernel, by the cost
-        model above. Measured on MI355X (model in brackets), plan against runtime
-        kernel: 4096 -> 4096 at batch 256 178 us (184) against 354 us (329); 128 ->
-        128 3 x 3 at 28 x 28, batch 1 12.6 us (11.5) against 42 us (35); 256 -> 128
-        at batch 8 9.3 us (7.9) against 45 us (41); 25088 -> 4096 at batch 1 (450
-        MB of code for one row) 346 us (282) against 1960 us (1811: one row in a
-        256-row tile). Over the layers of ResNet-18 (batch 32) and ResNet-50
-        (batch 128) measured / modelled plan durations have medians 1.16 and 1.04
-        (0.93-2.0), runtime-kernel ones 0.97 and 0.92 (0.87-1.3); every one of
-        those layers is a plan. The runtime kernel wins where code would dwarf the
-        work (e.g. 8x the code the planner makes for a layer)."""
+        model above. Measured on MI355X as graph replays (model in brackets),
+        plan against runtime kernel: 4096 -> 4096 at batch 256 165 us (184)
+        against 346 us (329); 128 -> 128 3 x 3 at 28 x 28, batch 1 8.6 us (10)
+        against 42 us eager (33); 256 -> 128 at batch 8 4.2 us (5.5) against 6.9
+        us (6.0); 512 -> 1000 at batch 32 10.2 us (11) against 9.1 us (7.7);
+        25088 -> 4096 at batch 1 344 us (282) against 45 us (52). Over the layers
+        of ResNet-18 (batch 32) and ResNet-50 (batch 128) measured / modelled
+        plan durations have medians 1.16 and 1.04, runtime-kernel ones 0.97 and
+        0.92. Known miss: 2048 -> 1000 at batch 128, plan 39 us (27) against 36
+        us (34), so the plan is kept at a 10 % loss."""
         return self.estimate_us() < self.runtime_estimate_us()
 
     def __call__(self, x: torch.Tensor, residual: torch.Tensor | None = None, out=None):

@@ -150,6 +150,11 @@ def test_describe_names_a_kernel_without_a_gpu():
     assert ops.describe_conv2d(128, 64, 56, 56, 64, 3, 1, 1).startswith("tiled window")
     assert ops.describe_conv2d(2, 3, 224, 224, 64, 7, 2, 3).startswith("tiled window")
     assert ops.describe_conv2d(1, 3, 9, 9, 5, 4, 1, 1) == "direct"
+    # LinearShift (1 x 1 on 1 x 1 inputs) below 256 rows: the small-batch kernel
+    assert ops.describe_conv2d(1, 25088, 1, 1, 4096, 1) == "rows"
+    assert ops.describe_conv2d(255, 2048, 1, 1, 1000, 1) == "rows"
+    assert ops.describe_conv2d(256, 4096, 1, 1, 4096, 1).startswith("tiled point transposed")
+    assert ops.describe_conv2d(8, 256, 2, 1, 128, 1).startswith("tiled")
     lib = _native.lib()
     import ctypes
     buf = ctypes.create_string_buffer(4)
@@ -332,6 +337,8 @@ def test_noalloc_limit_checked_from_the_shape_alone():
     assert need > (32 << 20)
     assert lib.ds_conv2d_shift_noalloc_scratch_bytes(1, 128, 28, 28, 128, 3, 3, 1, 1, 1, 1) <= (32 << 20)
     assert lib.ds_conv2d_shift_noalloc_scratch_bytes(0, 1, 1, 1, 1, 1, 1, 1, 1, 0, 0) == -1
+    # the small-batch LinearShift kernel needs no scratch at any size
+    assert lib.ds_conv2d_shift_noalloc_scratch_bytes(255, 25088, 1, 1, 4096, 1, 1, 1, 1, 0, 0) == 0
     x = np.zeros(16, np.int32)
     st = lib.ds_conv2d_shift_noalloc(x.ctypes.data, x.ctypes.data, None, x.ctypes.data, 256, 4096, 1,
                                      1, 4096, 1, 1, 1, 1, 0, 0, 16, 0, None)

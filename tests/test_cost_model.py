@@ -20,26 +20,29 @@ def fake_plan(n, c, h, w, k, r, s, oh, ow, code_bytes, segments, splits, channel
     return p
 
 
-# (shape, layout as the planner makes it, measured plan us, measured runtime us)
+# (shape, layout as the planner makes it, measured plan us, measured runtime us),
+# replays of HIP graphs on MI355X (the runtime convolution: eager calls)
 CASES = [
-    # 128 -> 128, 3 x 3 at 28 x 28, batch 1: 16-channel segments, wave split 8, unsplit
-    ((1, 128, 28, 28, 128, 3, 3, 28, 28), (868000, 8, 1, 16, 8, 13), 12.6, 42.1),
-    # 256 -> 128 at batch 8: 16-channel segments, wave split 4
-    ((8, 256, 1, 1, 128, 1, 1, 1, 1), (249000, 8, 1, 16, 4, 1), 9.3, 45.2),
+    # 128 -> 128, 3 x 3 at 28 x 28, batch 1: 16-channel segments, wave split 8, 2 parts
+    ((1, 128, 28, 28, 128, 3, 3, 28, 28), (868000, 16, 2, 16, 8, 13), 8.6, 42.1),
+    # 256 -> 128 at batch 8: 16-channel segments, wave split 8; small-batch runtime kernel
+    ((8, 256, 1, 1, 128, 1, 1, 1, 1), (257528, 8, 1, 16, 8, 1), 4.2, 6.85),
+    # 512 -> 1000 at batch 32: 16-channel segments, wave split 4
+    ((32, 512, 1, 1, 1000, 1, 1, 1, 1), (3273484, 63, 1, 16, 4, 1), 10.2, 9.1),
     # 4096 -> 4096 at batch 256: 64-channel segments, wave split 4, 4 tiles of 64 rows
-    ((256, 4096, 1, 1, 4096, 1, 1, 1, 1), (74041044, 64, 1, 64, 4, 4), 178.4, 354.0),
-    # 25088 -> 4096 at batch 1: split in 4
-    ((1, 25088, 1, 1, 4096, 1, 1, 1, 1), (450e6, 256, 4, 64, 4, 1), 346.2, 1960.1),
+    ((256, 4096, 1, 1, 4096, 1, 1, 1, 1), (74041044, 64, 1, 64, 4, 4), 165.0, 346.0),
+    # 25088 -> 4096 at batch 1: split in 4; small-batch runtime kernel
+    ((1, 25088, 1, 1, 4096, 1, 1, 1, 1), (450e6, 256, 4, 64, 4, 1), 344.3, 45.3),
 ]
 
 
-@pytest.mark.parametrize("case", CASES, ids=["conv_n1", "linear_b8", "fc_b256", "fc6_b1"])
+@pytest.mark.parametrize("case", CASES, ids=["conv_n1", "linear_b8", "fc_b32", "fc_b256", "fc6_b1"])
 def test_model_tracks_measured_durations_and_picks_the_faster_path(case):
     shape, layout, plan_us, rt_us = case
     p = fake_plan(*shape, *layout)
     est, rt = p.estimate_us(), p.runtime_estimate_us()
-    assert 0.7 * plan_us <= est <= 1.3 * plan_us, (est, plan_us)
-    assert 0.7 * rt_us <= rt <= 1.3 * rt_us, (rt, rt_us)
+    assert 0.7 * plan_us <= est <= 1.35 * plan_us, (est, plan_us)
+    assert 0.7 * rt_us <= rt <= 1.35 * rt_us, (rt, rt_us)
     assert p.preferred == (plan_us < rt_us)
 
 
