@@ -215,10 +215,13 @@ def sq_summary(directory, workload, path):
     VALU issue rate per SIMD per clock, and int32 lane-operations per second
     against the peak."""
     from paper_1905_13298_amd import workloads as W
-    probe = workload in PROBE_WORKLOADS
+    probe = workload in PROBE_WORKLOADS or workload in MODEL_WORKLOADS
     cfg = None if probe else WORKLOADS[workload]
-    layers = [W.VALU_PROBE] if probe else W.config_layers(cfg)
-    seed = 99 if probe else W.CONFIG_SEEDS[cfg]
+    if probe:
+        layers = [W.VALU_PROBE] if workload in PROBE_WORKLOADS else [W.LINEAR_25088_B1]
+        seed = 99 if workload in PROBE_WORKLOADS else 98
+    else:
+        layers, seed = W.config_layers(cfg), W.CONFIG_SEEDS[cfg]
     rows = _main_rows(_pmc_rows(directory), layers)
     per = {}
     for li, (L, r) in enumerate(zip(layers, rows)):
