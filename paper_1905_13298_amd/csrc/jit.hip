@@ -4,18 +4,18 @@
 // With the weight codes known when the plan is made, the inner loop needs no
 // weight loads, no decode and no work for zero weights. For each reduction
 // element (input channel c, tap (r, s)) a lane loads its input x, forms each
-// right shift x >> s that the 64 output channels of the segment use at that
-// element (once, into one of two registers in turn), and adds or subtracts it
-// into the accumulators of the channels with that shift: one v_add_u32 /
-// v_sub_u32 per non-zero weight, with the register and the sign fixed in the
-// instruction. The term of a weight with sign bit set
-// is -(x >> shift) (Eq. 1 with the sign applied after the shift), so the
+// right shift x >> s that the output channels of the segment (64, or 16 / 32
+// on small grids) use at that element (once, into one of two registers in
+// turn), and adds or subtracts it into the accumulators of the channels with
+// that shift: one v_add_u32 / v_sub_u32 per non-zero weight, with the register
+// and the sign fixed in the instruction. The term of a weight with sign bit
+// set is -(x >> shift) (Eq. 1 with the sign applied after the shift), so the
 // results equal those of ds_conv2d_shift bit for bit.
 //
 // Code layout. A plan is one code object: the template kernel built with the
 // library (jit_template.hip), whose last loadable segment `.jitbody` is
 // replaced by the generated code: a table of jump stubs, then one block of
-// straight-line code per segment (64 output channels x a range of reduction
+// straight-line code per segment (up to 64 output channels x a range of reduction
 // elements; with a wave split, one per share of that range). The template
 // computes the lane's tap and output offsets and jumps through the table; each
 // segment ends the wave. Segments are spliced into the template image in
@@ -23,8 +23,8 @@
 // with hipModuleLoadData.
 //
 // Variants of the same code: windows over 3 x 3 read a zero-padded copy of x
-// (uniform tap offsets); small grids split each 64 pixels' reduction over 2 or
-// 4 waves that meet in LDS, and long reductions over segments that meet in y
+// (uniform tap offsets); small grids split each 64 pixels' reduction over 2 to
+// 16 waves that meet in LDS, and long reductions over segments that meet in y
 // through atomics; the stride phases of an input gradient run as output-channel
 // groups of one problem (fuse_phases).
 #include <hip/hip_runtime.h>
@@ -179,7 +179,8 @@ struct Spec {
     int xh = 0, xw = 0;
     // Waves per 64 pixels (1, 2, 4, 8 or 16), each with a contiguous share of
     // every part's reduction elements, meeting in LDS; a workgroup covers
-    // 256 / wsplit pixels (64 from a split of 4 up, with 4 x ... x 16 waves).
+    // 64 * pgroups pixels with pgroups * wsplit waves (by default 256 / wsplit
+    // pixels up to a split of 4, 64 beyond).
     int wsplit = 1;
     // Output channels per segment: 64, or 32 / 16 on grids too small to fill the
     // chip (more segments, each with less code, at the price of forming each

@@ -14,7 +14,7 @@
 // padding; the byte offset of its output pixel in y) and hands them over in
 // fixed registers at the JITBODY marker. At run time the generator replaces
 // the marker with a jump, through a table, to the code of this wave's segment
-// (64 output channels and a range of input channels), assembled from
+// (up to 64 output channels and a range of input channels), assembled from
 // generated machine words; each segment ends the wave itself. Register use of
 // the generated code (the clobbers below): v14..v95 (v16, v17 the shifted
 // values, v18..v81 the accumulators, v82..v95 the loads in flight), s28..s31;
