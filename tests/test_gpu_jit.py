@@ -343,3 +343,56 @@ def test_multiplication_plans_match_oracle(spec):
     y = plan(to_dev(x)).cpu().numpy()
     plan.close()
     np.testing.assert_array_equal(y, oracle.conv2d_mul24(x, wt, bias, r=r, s=s, stride=st, pad=pd))
+
+
+def _graph_us(fn, reps=10, outer=5):
+    fn()
+    torch.cuda.synchronize()
+    side = torch.cuda.Stream()
+    side.wait_stream(torch.cuda.current_stream())
+    g = torch.cuda.CUDAGraph()
+    with torch.cuda.stream(side):
+        with torch.cuda.graph(g, stream=side):
+            for _ in range(reps):
+                fn()
+    torch.cuda.synchronize()
+    g.replay()
+    torch.cuda.synchronize()
+    a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    a.record()
+    for _ in range(outer):
+        g.replay()
+    b.record()
+    torch.cuda.synchronize()
+    return a.elapsed_time(b) / (reps * outer) * 1000.0
+
+
+@pytest.mark.parametrize("n,c,k", [(256, 4096, 4096), (1, 25088, 4096)], ids=["fc_b256", "fc6_b1"])
+def test_cost_model_choice_matches_measurement(n, c, k):
+    """JitConv.preferred against both paths timed (as graph replays) on two
+    LinearShift shapes whose measured gap is wide (2x and 7x on MI355X): the
+    path the model picks must be the faster one by at least 1.3x, and both paths
+    must give the oracle's result on sampled outputs."""
+    rng = np.random.default_rng(c)
+    x = rng.integers(0, 2 ** 17, (n, c)).astype(np.int32)
+    codes = W.random_codes(rng, (k, c), zero_frac=0.1)
+    bias = rng.integers(-(2 ** 16), 2 ** 16, k).astype(np.int32)
+    wp = ops.pack_shift_weights(codes)
+    xt, wt, bt = to_dev(x), to_dev(wp.view(np.int32)), to_dev(bias)
+    plan = ops.JitConv(wp, (n, c, 1, 1), 1, 1, 0, bias=bias)
+    y_rt = torch.empty((n, k), dtype=torch.int32, device=DEV)
+    y_pl = torch.empty((n, k, 1, 1), dtype=torch.int32, device=DEV)
+    t_rt = _graph_us(lambda: ops.linear_shift(xt, wt, bt, out=y_rt))
+    t_pl = _graph_us(lambda: plan(xt.view(n, c, 1, 1), out=y_pl))
+    say(f"cost model {n}x{c}->{k}: plan {t_pl:.1f} us (model {plan.estimate_us():.1f}), "
+        f"runtime {t_rt:.1f} us (model {plan.runtime_estimate_us():.1f}), preferred {plan.preferred}")
+    assert torch.equal(y_rt, y_pl.view(n, k))
+    idx = rng.integers(0, n * k, 200)
+    got = y_rt.cpu().numpy().ravel()[idx]
+    want = oracle.linear_shift_points(x, codes, bias, idx)
+    np.testing.assert_array_equal(got, want)
+    plan_faster = t_pl * 1.3 < t_rt
+    runtime_faster = t_rt * 1.3 < t_pl
+    assert plan_faster or runtime_faster, "the two paths are too close to judge"
+    assert plan.preferred == plan_faster
+    plan.close()
