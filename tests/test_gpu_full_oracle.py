@@ -95,10 +95,10 @@ def check_band(L, y_flat, x, codes, bias, idx):
         assert lo_ok and hi_ok, (q, yq, d14 / 16384.0, npos, nneg)
 
 
-@pytest.mark.parametrize("cfg,li,name", CASES, ids=[f"cfg{c}-{n}" for c, _, n in CASES])
+@pytest.mark.parametrize("cfg,li,name", CASES, ids=[f"{W.CONFIG_NAMES[c]}-{n}" for c, _, n in CASES])
 def test_every_output_at_benchmark_batch(cfg, li, name):
     L = W.config_layers(cfg)[li]
-    say(f"cfg{cfg} layer {li} {name} batch {L.n}: oracle on {oracle.max_threads()} threads")
+    say(f"{W.CONFIG_NAMES[cfg]} layer {li} {name} batch {L.n}: oracle on {oracle.max_threads()} threads")
     x, codes, bias = W.gen_layer(L, W.CONFIG_SEEDS[cfg], li)
     want = oracle_full(L, x, codes, bias).reshape(-1)
     wp = ops.pack_shift_weights(codes)

@@ -158,7 +158,7 @@ def test_single_layer_configs_exact(cfg):
     x, codes, bias = W.gen_layer(layer, W.CONFIG_SEEDS[cfg], 0)
     lin = layer.kind == "linear"
     shape = (layer.n, layer.c, 1, 1) if lin else x.shape
-    say(f"jit cfg{cfg} {layer.name}")
+    say(f"jit {W.CONFIG_NAMES[cfg]} {layer.name}")
     plan = ops.JitConv(ops.pack_shift_weights(codes), shape, (1, 1) if lin else (layer.r, layer.s),
                        1 if lin else layer.stride, 0 if lin else layer.pad, bias=bias)
     y = plan(to_dev(x.reshape(shape))).cpu().numpy()

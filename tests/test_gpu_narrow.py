@@ -67,7 +67,7 @@ def test_narrow_benchmark_layers_every_output(cfg, name, act_bits):
     li = [L.name for L in layers].index(name)
     L = layers[li]
     x, codes, bias = W.gen_layer(L, W.CONFIG_SEEDS[cfg], li, act_bits=act_bits)
-    say(f"cfg{cfg} {name} int{act_bits} batch {L.n}")
+    say(f"{W.CONFIG_NAMES[cfg]} {name} int{act_bits} batch {L.n}")
     plan = ops.layer_plan(L, ops.pack_shift_weights(codes), bias, device=DEV, act_bits=act_bits)
     y = ops.run_layer_plan(plan, L, to_dev(x)).cpu().numpy()
     plan.close()

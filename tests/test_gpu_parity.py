@@ -82,8 +82,8 @@ def check_full(layer, x, codes, bias, what):
 def test_single_layer_configs_exact(cfg):
     (layer,) = W.config_layers(cfg)
     x, codes, bias = W.gen_layer(layer, W.CONFIG_SEEDS[cfg], 0)
-    say(f"cfg{cfg} {layer}")
-    check_full(layer, x, codes, bias, f"cfg{cfg}")
+    say(f"{W.CONFIG_NAMES[cfg]} {layer}")
+    check_full(layer, x, codes, bias, W.CONFIG_NAMES[cfg])
 
 
 @pytest.mark.parametrize("cfg,batch", [(3, 2), (4, 2)])
@@ -91,8 +91,8 @@ def test_network_layers_small_batch_exact(cfg, batch):
     for li, layer in enumerate(W.config_layers(cfg)):
         small = layer.with_batch(batch)
         x, codes, bias = W.gen_layer(small, W.CONFIG_SEEDS[cfg], li)
-        say(f"cfg{cfg} layer {li} {small.name} n={batch}")
-        check_full(small, x, codes, bias, f"cfg{cfg}/{small.name}")
+        say(f"{W.CONFIG_NAMES[cfg]} layer {li} {small.name} n={batch}")
+        check_full(small, x, codes, bias, f"{W.CONFIG_NAMES[cfg]}/{small.name}")
 
 
 # ---------------------------------------------------------------------------
