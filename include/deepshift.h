@@ -501,7 +501,9 @@ int64_t ds_conv2d_shift_noalloc_scratch_bytes(int64_t n, int64_t c, int64_t h, i
  * variant, wave split, block order or load depth the library uses, never a
  * result. Knobs: "DS_FORCE_VARIANT" (0: the one-thread-per-output kernel for
  * ds_conv2d_shift and the input gradients; 8: the tiled kernel with 8 pixels
- * per lane where one exists) and the plan knobs listed with ds_jit_conv_create.
+ * per lane where one exists), "DS_ROWS_BATCH" (1, 2, 4 or 8 batch rows per
+ * workgroup of the kernel that runs a LinearShift below 256 rows) and the plan
+ * knobs listed with ds_jit_conv_create.
  * Each starts from the environment variable of the same name, read once when
  * the library is loaded (unset: -1, the library's own choice); no entry point
  * reads the environment afterwards. value < 0 resets a knob to -1. Errors:

@@ -1091,13 +1091,42 @@ static void launch_rows(dim3 grid, const int32_t *x, const RowsArgs &a, int bits
     }
 }
 
-// Batch rows per workgroup: the smallest power of two covering the batch, at most 8.
-static int rows_per_block(int n) { return n >= 8 ? 8 : n >= 4 ? 4 : n >= 2 ? 2 : 1; }
+// Workgroups per block of the small-batch kernel: fewer than 256 workgroups of
+// 16 waves leave CUs idle and each wave a long walk along its weight rows, so the
+// reduction is split over up to 8 workgroups per block (each wave keeping at
+// least 4 units: a split adds a fill pass, which a shorter reduction does not
+// repay), when there is no epilogue.
+static int rows_splits(int64_t blocks, int units, bool may_split)
+{
+    int splits = 1;
+    if (may_split)
+        while (splits < 8 && blocks * splits < 256 && units / (kRowsWaves * splits * 2) >= 4) splits *= 2;
+    return splits;
+}
+
+// Batch rows per workgroup: the most (a power of two up to 8 that the batch fills)
+// with which the grid, split as above, still has 256 workgroups; else 1. More rows
+// share each decoded code, fewer give more workgroups: on MI355X 2048 -> 1000 ran
+// fastest with 8 rows at batch 32-128 (13.2, 20.0, 32.6 us against 15.1, 22.3,
+// 36.0 with 4), 512 -> 1000 at batch 32 with 2 (6.5 us against 8.9 with 8),
+// 256 -> 128 at batch 8 with 1 (4.5 us against 6.8 with 8). The DS_ROWS_BATCH
+// override is for measurements.
+static int rows_per_block(const ConvGeom &g, int units, bool may_split)
+{
+    const int forced = tuning(kRowsBatch);
+    if (forced == 1 || forced == 2 || forced == 4 || forced == 8) return forced;
+    const int64_t kg = (g.k + 63) / 64;
+    for (int rows = g.n >= 8 ? 8 : g.n >= 4 ? 4 : g.n >= 2 ? 2 : 1; rows > 1; rows /= 2) {
+        const int64_t blocks = kg * ((g.n + rows - 1) / rows);
+        if (blocks * rows_splits(blocks, units, may_split) >= 256) return rows;
+    }
+    return 1;
+}
 
 template <Inner OP>
-static void launch_rows_op(const ConvGeom &g, const int32_t *x, const RowsArgs &a, int splits, hipStream_t st)
+static void launch_rows_op(const ConvGeom &g, const int32_t *x, const RowsArgs &a, int rows, int splits,
+                           hipStream_t st)
 {
-    const int rows = rows_per_block(g.n);
     const dim3 grid(unsigned((g.k + 63) / 64), unsigned((g.n + rows - 1) / rows), unsigned(splits));
     if (rows == 8) launch_rows<OP, 8>(grid, x, a, g.bits, st);
     else if (rows == 4) launch_rows<OP, 4>(grid, x, a, g.bits, st);
@@ -1116,14 +1145,10 @@ static bool rows_path(const ConvGeom &g, const OutMap &map, const Padded &pad)
 static hipError_t run_rows(const ConvGeom &g, const int32_t *x, const uint32_t *wp, const int32_t *wi,
                            const int32_t *bias, int32_t *y, Inner op, hipStream_t st, const Epilogue &epi)
 {
-    // Fewer than 256 workgroups of 16 waves leave CUs idle and each wave a long
-    // walk along its weight rows: the reduction is split over up to 8 workgroups
-    // per block (each wave keeping at least 2 units), when there is no epilogue.
-    const int64_t blocks = int64_t((g.k + 63) / 64) * ((g.n + rows_per_block(g.n) - 1) / rows_per_block(g.n));
     const int units = op == Inner::Shift ? int(row_words_bits(g.c, g.bits)) : g.c;
-    int splits = 1;
-    if (!epi.any())
-        while (splits < 8 && blocks * splits < 256 && units / (kRowsWaves * splits * 2) >= 2) splits *= 2;
+    const int rows = rows_per_block(g, units, !epi.any());
+    const int64_t blocks = int64_t((g.k + 63) / 64) * ((g.n + rows - 1) / rows);
+    const int splits = rows_splits(blocks, units, !epi.any());
     if (splits > 1) {
         const hipError_t e = bias ? run_fill_init(g, bias, y, st) : run_fill_zero(y, int64_t(g.n) * g.k, st);
         if (e != hipSuccess) return e;
@@ -1138,9 +1163,9 @@ static hipError_t run_rows(const ConvGeom &g, const int32_t *x, const uint32_t *
     a.K = g.k;
     a.wpr = int(row_words_bits(g.c, g.bits));
     a.epi = epi;
-    if (op == Inner::Shift) launch_rows_op<Inner::Shift>(g, x, a, splits, st);
-    else if (op == Inner::Mul) launch_rows_op<Inner::Mul>(g, x, a, splits, st);
-    else launch_rows_op<Inner::Mul24>(g, x, a, splits, st);
+    if (op == Inner::Shift) launch_rows_op<Inner::Shift>(g, x, a, rows, splits, st);
+    else if (op == Inner::Mul) launch_rows_op<Inner::Mul>(g, x, a, rows, splits, st);
+    else launch_rows_op<Inner::Mul24>(g, x, a, rows, splits, st);
     return hipGetLastError();
 }
 

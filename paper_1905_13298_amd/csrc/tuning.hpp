@@ -16,6 +16,7 @@ enum Knob {
     kJitOrder,       // DS_JIT_ORDER: 0 grouped, 1 tile-major, 2 XCD-local tile-major
     kJitTn,          // DS_JIT_TN: output channels per code segment in a plan (16, 32, 64)
     kJitPgroups,     // DS_JIT_PGROUPS: groups of 64 pixels per workgroup in a plan (1, 2, 4)
+    kRowsBatch,      // DS_ROWS_BATCH: batch rows per workgroup of the small-batch LinearShift (1, 2, 4, 8)
     kKnobs
 };
 

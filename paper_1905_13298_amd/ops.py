@@ -503,7 +503,7 @@ class JitConv:
         nq = max(1, self.out_pixels)
         weight_bytes = self.out_channels * packed_row_words(self.crs) * 4
         if self.linear and nq < 256:
-            return 6.0 + max(self.sac / self.ROWS_SAC_PER_US, weight_bytes / 1.5e6)
+            return 5.5 + max(self.sac / self.ROWS_SAC_PER_US, weight_bytes / 1.5e6)
         fill = nq / (-(-nq // 256) * 256)
         return ((40.0 if self.linear else 25.0) + self.sac / (self.RUNTIME_SAC_PER_US * fill)
                 + weight_bytes / 4e6)
@@ -514,13 +514,13 @@ class JitConv:
         model above. Measured on MI355X as graph replays (model in brackets),
         plan against runtime kernel: 4096 -> 4096 at batch 256 165 us (184)
         against 346 us (329); 128 -> 128 3 x 3 at 28 x 28, batch 1 8.6 us (10)
-        against 42 us eager (33); 256 -> 128 at batch 8 4.2 us (5.5) against 6.9
-        us (6.0); 512 -> 1000 at batch 32 10.2 us (11) against 9.1 us (7.7);
-        25088 -> 4096 at batch 1 344 us (282) against 45 us (52). Over the layers
+        against 42 us eager (33); 256 -> 128 at batch 8 4.2 us (5.5) against 4.5
+        us (5.5); 512 -> 1000 at batch 32 10.2 us (11) against 6.5 us (7.2);
+        25088 -> 4096 at batch 1 344 us (282) against 45 us (48). Over the layers
         of ResNet-18 (batch 32) and ResNet-50 (batch 128) measured / modelled
         plan durations have medians 1.16 and 1.04, runtime-kernel ones 0.97 and
-        0.92. Known miss: 2048 -> 1000 at batch 128, plan 39 us (27) against 36
-        us (34), so the plan is kept at a 10 % loss."""
+        0.92. Known miss: 2048 -> 1000 at batch 128, plan 39 us (27) against 32.5
+        us (33), so the plan is kept at a 20 % loss on that layer."""
         return self.estimate_us() < self.runtime_estimate_us()
 
     def __call__(self, x: torch.Tensor, residual: torch.Tensor | None = None, out=None):
@@ -604,8 +604,8 @@ def run_layer_plan(plan: JitConv, layer, x: torch.Tensor, out: torch.Tensor | No
 def set_tuning(name: str, value: int) -> None:
     """Sets a tuning override of the library (``ds_set_tuning``): "DS_FORCE_VARIANT",
     "DS_JIT_WSPLIT", "DS_JIT_SLOTS", "DS_JIT_MAP", "DS_JIT_GROUP_TILES",
-    "DS_JIT_ORDER", "DS_JIT_TN" or "DS_JIT_PGROUPS"; a negative value restores the
-    library's own choice."""
+    "DS_JIT_ORDER", "DS_JIT_TN", "DS_JIT_PGROUPS" or "DS_ROWS_BATCH"; a negative
+    value restores the library's own choice."""
     call("ds_set_tuning", name.encode(), int(value))
 
 

@@ -59,6 +59,23 @@ def test_small_batch_linear_matches_oracle(shape):
     np.testing.assert_array_equal(y, np.maximum(oracle.linear_shift(x, codes, None), 0))
 
 
+# batch, in, out: a long reduction that splits over workgroups, a short one that does not
+FORCED = [(13, 4100, 70), (11, 333, 129)]
+
+
+@pytest.mark.parametrize("rows", [1, 2, 4, 8])
+@pytest.mark.parametrize("shape", FORCED, ids=[f"{b}x{c}to{k}" for b, c, k in FORCED])
+def test_small_batch_rows_per_workgroup_match_oracle(shape, rows):
+    """Every batch-rows tiling (the batch not a multiple of it) gives the oracle's
+    result, with the reduction split over workgroups or not."""
+    b, c, k = shape
+    x, codes, bias, _ = draw(zlib.crc32(repr((shape, rows)).encode()), b, c, k)
+    wt = to_dev(ops.pack_shift_weights(codes).view(np.int32))
+    with ops.tuning("DS_ROWS_BATCH", rows):
+        y = ops.linear_shift(to_dev(x), wt, to_dev(bias)).cpu().numpy()
+    np.testing.assert_array_equal(y, oracle.linear_shift(x, codes, bias))
+
+
 @pytest.mark.parametrize("bits", [2, 3, 4])
 def test_small_batch_linear_code_widths(bits):
     b, c, k = 5, 203, 77
