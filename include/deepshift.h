@@ -352,7 +352,12 @@ ds_status ds_conv2d_shift_describe(int64_t n, int64_t c, int64_t h, int64_t w, i
  * LinearShift is the case h = w = r = s = 1. Windows over 3 x 3 read a
  * zero-padded copy of x, [n][c][xh][xw] with xh = (oh - 1) * stride_h + r and
  * xw = (ow - 1) * stride_w + s, that each run writes first into device memory
- * the plan holds (from create to destroy).
+ * the plan holds (from create to destroy). A LinearShift of batch n >= 64 runs
+ * on x^T: each run first transposes x into an int32 copy [c][n] the plan holds
+ * (so that a load reads consecutive batch rows), the generated kernel writes
+ * y^T [k][n] into a buffer the plan holds, and a last pass transposes it into
+ * y (with the residual and the ReLU of a layer with a residual, and the whole
+ * epilogue of a split reduction).
  *
  * ds_jit_conv_create: w_packed is HOST memory, [k][ds_packed_row_words(c*r*s)]
  * words as for ds_conv2d_shift (b-bit codes with DS_CODE_BITS(b) in flags); with
@@ -373,8 +378,9 @@ ds_status ds_conv2d_shift_describe(int64_t n, int64_t c, int64_t h, int64_t w, i
  * DS_ACT_I16 / DS_ACT_I8), residual and y [n][k][oh][ow] (int32), device
  * memory on the plan's device; residual must be non-NULL exactly when the
  * plan was made with DS_JIT_RESIDUAL. Asynchronous on `stream`. y must not
- * overlap x or residual. A plan may hold device scratch (the padded copy of x;
- * the partial sums of split strided phases of an input-gradient plan), so runs
+ * overlap x or residual. A plan may hold device scratch (the padded or
+ * transposed copy of x; y^T; the partial sums of split strided phases of an
+ * input-gradient plan), so runs
  * of one plan must not overlap in time: issue them on one stream, or order
  * them with events.
  *
@@ -391,10 +397,12 @@ ds_status ds_conv2d_shift_describe(int64_t n, int64_t c, int64_t h, int64_t w, i
  * segment (16, 32 or 64), waves sharing each group of 64 pixels (the wave
  * split: 1, 2, 4, 8 or 16; each runs code of its own for a share of the
  * reduction), groups of 64 pixels per workgroup (1, 2 or 4; a workgroup has
- * groups x wave split <= 16 waves), and pixel tiles (workgroups per segment).
- * Each share's code runs once per group of 64 pixels; segments x wave split
- * distinct code streams. For an input-gradient plan: its first kernel. Any
- * output may be NULL.
+ * groups x wave split <= 16 waves), pixel tiles (workgroups per segment), and
+ * whether the plan runs a LinearShift on x^T (1) or not (0; its pixels are
+ * then the batch rows of x, else the n pixels of x^T's one image). Each share's
+ * code runs once per group of 64 pixels; segments x wave split distinct code
+ * streams. For an input-gradient plan: its first kernel. Any output may be
+ * NULL.
  *
  * Tuning overrides (ds_set_tuning, below) used when a plan is made (wave split,
  * loads in flight, register map, tile grouping, segment width) or run (block
@@ -404,7 +412,8 @@ ds_status ds_conv2d_shift_describe(int64_t n, int64_t c, int64_t h, int64_t w, i
  * DS_JIT_SLOTS (loads in flight: 1-14, at most 8 in the 80-register code of
  * layers with one tap per element), DS_JIT_MAP (96: the 96-register code for
  * those layers too), DS_JIT_GROUP_TILES (tiles per group), DS_JIT_ORDER (0
- * grouped, 1 tile-major, 2 tile-major with each tile's workgroups on one XCD).
+ * grouped, 1 tile-major, 2 tile-major with each tile's workgroups on one XCD),
+ * DS_JIT_TRANSPOSE (LinearShift plans on x^T: 0 never, 1 from batch 2).
  * The results do not depend on them. */
 typedef struct ds_jit_conv ds_jit_conv;
 
@@ -425,7 +434,7 @@ ds_status ds_jit_conv_image(const uint32_t *w_packed, const int32_t *bias, const
 ds_status ds_jit_conv_query(const ds_jit_conv *plan, int64_t *code_bytes, int32_t *segments,
                             int32_t *splits);
 ds_status ds_jit_conv_layout(const ds_jit_conv *plan, int32_t *channels, int32_t *wsplit,
-                             int32_t *pixel_groups, int32_t *pixel_tiles);
+                             int32_t *pixel_groups, int32_t *pixel_tiles, int32_t *transposed);
 
 /* A plan for the input gradient of a ConvShift layer (the result of
  * ds_conv2d_shift_backward_data, bit for bit), with the weights baked into

@@ -44,7 +44,7 @@ SIGNATURES = {
     "ds_jit_conv_destroy": (ctypes.c_int, [_P]),
     "ds_jit_conv_image": (ctypes.c_int, [_P, _P, _P, _P, _I32] + [_I64] * 7 + [_I32] * 4 + [_U32, _I32, _P, _I64, _P]),
     "ds_jit_conv_query": (ctypes.c_int, [_P, _P, _P, _P]),
-    "ds_jit_conv_layout": (ctypes.c_int, [_P, _P, _P, _P, _P]),
+    "ds_jit_conv_layout": (ctypes.c_int, [_P, _P, _P, _P, _P, _P]),
     "ds_jit_conv_mul_create": (ctypes.c_int, [_P, _P] + [_I64] * 7 + [_I32] * 4 + [_U32, _I32, _P]),
     "ds_jit_conv_mul_image": (ctypes.c_int, [_P, _P] + [_I64] * 7 + [_I32] * 4 + [_U32, _I32, _P, _I64, _P]),
     "ds_jit_conv_backward_data_create": (ctypes.c_int, [_P] + [_I64] * 7 + [_I32] * 4 + [_U32, _I32, _P]),

@@ -198,6 +198,16 @@ struct Spec {
     // other, instead of groups of tiles passing through the segments one by one.
     int tile_major = 0;         // 0 grouped, 1 tile-major, 2 XCD-local tile-major
     bool one_tap = false;       // the 80-VGPR entry point (one tap register)
+    // A LinearShift of batch > 1 (x [N][C] -> y [N][K]) runs as a 1 x 1 layer over
+    // x^T viewed as one image of 1 x N pixels, so that the 64 lanes of a load read
+    // 64 consecutive batch rows of one input channel (coalesced) instead of 64 rows
+    // C elements apart, and store y^T [K][N] as coalesced (lanes C or K elements
+    // apart made 4096 -> 4096 at batch 256 run 1.5-2.7x slower on MI355X). The
+    // plan transposes x into an int32 copy of its own before the kernel and y^T
+    // back into y after it; that last pass adds the residual and applies the ReLU
+    // of a layer with a residual. `lin` keeps the layer as given.
+    bool xt = false;
+    ConvGeom lin{};
 };
 
 // Element strides of the output map of a spec (the dense layout when unset).
@@ -267,11 +277,12 @@ void emit_segment(Emitter &e, const Spec &sp, int kg, int e0, int e1, int share,
     const int jn = sp.kjn.empty() ? std::min(sp.tn, g.k - kbase) : sp.kjn[size_t(kg)];
     const int RS = g.r * g.s;
     const bool padded = sp.xh > 0;
-    // The padded copy is int32 whatever x holds; x itself is read with a
-    // sign-extending load of its own width.
+    // The padded and transposed copies are int32 whatever x holds; x itself is
+    // read with a sign-extending load of its own width.
+    const bool wide = padded || sp.xt || sp.act_bytes == 4;
     const uint32_t cstride = padded ? uint32_t(sp.xh) * uint32_t(sp.xw) * 4u
-                                    : uint32_t(g.h) * uint32_t(g.w) * uint32_t(sp.act_bytes);
-    const uint32_t load_op = padded || sp.act_bytes == 4 ? kLoad : sp.act_bytes == 2 ? kLoadI16 : kLoadI8;
+                                    : uint32_t(g.h) * uint32_t(g.w) * uint32_t(wide ? 4 : sp.act_bytes);
+    const uint32_t load_op = wide ? kLoad : sp.act_bytes == 2 ? kLoadI16 : kLoadI8;
     const uint32_t rstride = uint32_t(sp.xw) * 4u;
     const uint32_t kstride = uint32_t(full_map(sp).kstride) * 4u;
     // Byte offset of the group's first output channel (added to the lane's v13).
@@ -396,7 +407,7 @@ void emit_segment(Emitter &e, const Spec &sp, int kg, int e0, int e1, int share,
                 if (a != 0) e.vop2_imm(kOpAdd, m.acc + j, a, m.acc + j);
             }
         }
-        if (sp.residual) {
+        if (sp.residual && !sp.xt) {
             for (int jb = j0; jb < j1; jb += nslots) {
                 const int nb = std::min(nslots, j1 - jb);
                 e.s_mov_imm(kSy, out0 + uint32_t(jb) * kstride);
@@ -409,7 +420,7 @@ void emit_segment(Emitter &e, const Spec &sp, int kg, int e0, int e1, int share,
                     e.vop2(kOpAdd, m.acc + jb + b, Emitter::vgpr(m.slot + b), m.acc + jb + b);
             }
         }
-        if (sp.relu)
+        if (sp.relu && !(sp.xt && sp.residual))
             for (int j = j0; j < j1; ++j) e.vop2(kOpMax, m.acc + j, Emitter::inline_int(0), m.acc + j);
     }
     e.s_mov_imm(kSy, out0 + uint32_t(j0) * kstride);
@@ -614,6 +625,29 @@ ds_status finish_spec(Spec &sp, int bits, int splits, int deep_blocks = 3072)
     // batch 1 ran its kernel in 9.9 us at 12 or 16 parts against 13.7 us at 4 (and
     // 12.5 us at 24).
     int ns = splits;
+    // A transposed LinearShift (x^T as one image of 1 x N pixels): 32-channel
+    // segments below 4 tiles of 64 rows (64 from there), one group of 64 rows per
+    // workgroup, a wave split of 16 while each share keeps 64 input channels,
+    // and parts toward 4096 waves while each wave keeps 16 input channels. Layout
+    // sweeps of 3 x 5 x 3 x 4 segment widths, wave splits, pixel groups and parts
+    // on MI355X (graph replays, transposing passes included): 4096 -> 4096 at
+    // batch 256 116 us at best, 117 us by this rule (16 / 1 / 1), 182 us by the
+    // convolution rules below; 2048 -> 1000 at batch 128 25.1 / 25.5 (16 / 1 /
+    // 4) / 36.6 us; 1024 -> 1024 at batch 64 19.5 / 20.9 (16 / 1 / 4) / 26.6 us.
+    if (sp.xt && sp.kjn.empty() && tuning(kJitTn) < 0 && tuning(kJitWsplit) < 0 && tuning(kJitPgroups) < 0) {
+        sp.tn = nq >= 4 * 64 ? kTN : 32;
+        sp.kgroups = (g.k + sp.tn - 1) / sp.tn;
+        int ws = 16;
+        while (ws > 1 && g.c / ws < 64) ws /= 2;
+        sp.wsplit = ws;
+        sp.pgroups = 1;
+        sp.tiles_p = int((nq + 63) / 64);
+        if (ns == 0) {
+            const int64_t w1 = int64_t(sp.tiles_p) * sp.kgroups * ws;
+            ns = 1;
+            while (ns < 8 && w1 * ns < 4096 && g.c / (ws * ns * 2) >= 16) ns *= 2;
+        }
+    }
     if (ns == 0) {
         const int64_t blocks = int64_t(sp.tiles_p) * sp.kgroups;
         const bool thin_window = base < 256 && int64_t(g.r) * g.s > 1;
@@ -763,6 +797,18 @@ ds_status plan_spec(const CreateArgs &a, Spec &sp)
     sp.bias = a.bias; sp.mul = a.mul; sp.add = a.add; sp.mul_shift = a.mul ? a.mul_shift : 0;
     sp.relu = a.flags & DS_RELU;
     sp.residual = a.flags & DS_JIT_RESIDUAL;
+    // Transposed from batch 64 up: the two transposing passes cost about 10 us
+    // (MI355X, graph replays), more than they save at small batches (8 x 256 ->
+    // 128: 15 against 4.2 us; 32 x 512 -> 1000: 17 against 10 us).
+    const ConvGeom &g = sp.g;
+    const int forced = tuning(kJitTranspose);
+    const bool want_xt = forced == 0 ? false : forced == 1 ? g.n > 1 : g.n >= 64;
+    if (want_xt && g.h == 1 && g.w == 1 && g.r == 1 && g.s == 1 && int64_t(g.n) * g.c <= kMaxElems / 4 &&
+        int64_t(g.n) * g.k <= kMaxElems / 4) {
+        sp.xt = true;
+        sp.lin = g;
+        sp.g = ConvGeom{1, g.c, 1, g.n, g.k, 1, 1, 1, 1, 0, 0, 1, g.n, g.c, bits};
+    }
     return finish_spec(sp, bits, a.splits);
 }
 
@@ -888,8 +934,10 @@ struct ds_jit_conv {
     int32_t *mul = nullptr, *add = nullptr;
     bool backward = false;
     ConvGeom fwd;                   // backward: the forward layer
-    int32_t *xpad = nullptr;        // windows over 3 x 3: the zero-padded input [n][c][xh][xw]
-    int32_t *dense = nullptr;       // split phase: its partial sums, dense [n][k][oh][ow]
+    int32_t *xpad = nullptr;        // windows over 3 x 3: the zero-padded input [n][c][xh][xw];
+                                    // a transposed LinearShift: x^T [c][n] (int32)
+    int32_t *dense = nullptr;       // split phase: its partial sums, dense [n][k][oh][ow];
+                                    // a transposed LinearShift: y^T [k][n]
     OutMap scatter;                 // ... and where they go in dx
     std::vector<ds_jit_conv *> parts;
     std::vector<GradPhase> zeros;   // backward: phases whose dx positions are 0
@@ -963,11 +1011,20 @@ static ds_status build_plan(const Spec &spec, ds_jit_conv **out)
             return fail(st, "%s", msg.c_str());
         }
     }
-    if (p->sp.xh > 0) {
-        const size_t bytes = size_t(p->sp.g.n) * p->sp.g.c * p->sp.xh * p->sp.xw * 4;
+    if (p->sp.xh > 0 || p->sp.xt) {
+        const size_t bytes = p->sp.xt ? size_t(p->sp.g.c) * p->sp.g.w * 4
+                                      : size_t(p->sp.g.n) * p->sp.g.c * p->sp.xh * p->sp.xw * 4;
         if (hipMalloc(&p->xpad, bytes) != hipSuccess) {
             destroy_plan(p);
-            return fail(DS_ERR_HIP, "hipMalloc of %zu bytes (padded input) failed", bytes);
+            return fail(DS_ERR_HIP, "hipMalloc of %zu bytes (%s input) failed", bytes,
+                        p->sp.xt ? "transposed" : "padded");
+        }
+    }
+    if (p->sp.xt) {
+        const size_t bytes = size_t(p->sp.g.k) * p->sp.g.w * 4;
+        if (hipMalloc(&p->dense, bytes) != hipSuccess) {
+            destroy_plan(p);
+            return fail(DS_ERR_HIP, "hipMalloc of %zu bytes (transposed output) failed", bytes);
         }
     }
     p->sp.bias = p->sp.mul = p->sp.add = nullptr;
@@ -1129,6 +1186,101 @@ extern "C" ds_status ds_jit_conv_backward_data_create(const uint32_t *w_packed, 
     }
 }
 
+// The first pass of a transposed LinearShift: xt [c][n] = x [n][c] as int32
+// (sign-extended from int16 / int8 elements), in 64 x 64 tiles through LDS
+// (reads and writes coalesced), and with a split reduction y^T [k][n] = init[k],
+// the start of the parts' atomic adds, in the workgroups after the tiles.
+// 256 threads.
+template <typename T>
+__global__ void __launch_bounds__(256)
+transpose_in_kernel(const T *__restrict__ x, int32_t *__restrict__ xt, int rows, int cols, int tiles_c,
+                    int tiles, const int32_t *__restrict__ init, int32_t *__restrict__ yt, int k)
+{
+    __shared__ int32_t tile[64][65];
+    const int b = int(blockIdx.x);
+    if (b >= tiles) {
+        // fill: y^T [k][rows] = init[k], 256 elements per workgroup
+        const int64_t i = int64_t(b - tiles) * 256 + threadIdx.x;
+        if (i < int64_t(k) * rows) yt[i] = init[i / rows];
+        return;
+    }
+    const int c0 = (b % tiles_c) * 64, r0 = (b / tiles_c) * 64;
+    const int tx = threadIdx.x & 63, ty = threadIdx.x >> 6;
+    for (int i = ty; i < 64; i += 4) {
+        const int r = r0 + i, c = c0 + tx;
+        if (r < rows && c < cols) tile[i][tx] = int32_t(x[int64_t(r) * cols + c]);
+    }
+    __syncthreads();
+    for (int i = ty; i < 64; i += 4) {
+        const int c = c0 + i, r = r0 + tx;
+        if (c < cols && r < rows) xt[int64_t(c) * rows + r] = tile[tx][i];
+    }
+}
+
+static hipError_t run_transpose_in(const int32_t *x, int32_t *xt, int rows, int cols, int xbytes,
+                                   const int32_t *init, int32_t *yt, int k, hipStream_t st)
+{
+    const int tiles_c = (cols + 63) / 64;
+    const int64_t tiles = int64_t(tiles_c) * ((rows + 63) / 64);
+    const int64_t fills = init ? (int64_t(k) * rows + 255) / 256 : 0;
+    if (tiles + fills > INT32_MAX) return hipErrorInvalidValue;
+    if (tiles + fills == 0) return hipSuccess;
+    const dim3 grid{unsigned(tiles + fills)}, block{256u};
+    if (xbytes == 2)
+        hipLaunchKernelGGL(transpose_in_kernel<int16_t>, grid, block, 0, st, reinterpret_cast<const int16_t *>(x),
+                           xt, rows, cols, tiles_c, int(tiles), init, yt, k);
+    else if (xbytes == 1)
+        hipLaunchKernelGGL(transpose_in_kernel<int8_t>, grid, block, 0, st, reinterpret_cast<const int8_t *>(x),
+                           xt, rows, cols, tiles_c, int(tiles), init, yt, k);
+    else
+        hipLaunchKernelGGL(transpose_in_kernel<int32_t>, grid, block, 0, st, x, xt, rows, cols, tiles_c,
+                           int(tiles), init, yt, k);
+    return hipGetLastError();
+}
+
+// The last pass of a transposed LinearShift: y [n][k] = yt [k][n] in 64 x 64
+// tiles through LDS, with what the generated kernel left of the epilogue: for a
+// split reduction all of it (v * mul[k] >> mul_shift, floor, + add[k]), and
+// then, for a layer with a residual, + res[n][k] and the ReLU. 256 threads.
+__global__ void __launch_bounds__(256)
+transpose_back_kernel(const int32_t *__restrict__ yt, int32_t *__restrict__ y, int rows, int cols,
+                      int tiles_c, const int32_t *__restrict__ mul, const int32_t *__restrict__ add,
+                      int mul_shift, const int32_t *__restrict__ res, int relu)
+{
+    __shared__ int32_t tile[64][65];
+    const int n0 = int(blockIdx.x % unsigned(tiles_c)) * 64, k0 = int(blockIdx.x / unsigned(tiles_c)) * 64;
+    const int tx = threadIdx.x & 63, ty = threadIdx.x >> 6;
+    for (int i = ty; i < 64; i += 4) {
+        const int k = k0 + i, n = n0 + tx;
+        if (k < cols && n < rows) tile[i][tx] = yt[int64_t(k) * rows + n];
+    }
+    __syncthreads();
+    for (int i = ty; i < 64; i += 4) {
+        const int n = n0 + i, k = k0 + tx;
+        if (n < rows && k < cols) {
+            const int64_t o = int64_t(n) * cols + k;
+            uint32_t v = uint32_t(tile[tx][i]);
+            if (mul) v = uint32_t(int32_t((int64_t(int32_t(v)) * mul[k]) >> mul_shift)) + (add ? uint32_t(add[k]) : 0u);
+            if (res) v += uint32_t(res[o]);
+            if (relu && int32_t(v) < 0) v = 0u;
+            y[o] = int32_t(v);
+        }
+    }
+}
+
+static hipError_t run_transpose_back(const int32_t *yt, int32_t *y, int rows, int cols, const int32_t *mul,
+                                     const int32_t *add, int mul_shift, const int32_t *res, bool relu,
+                                     hipStream_t st)
+{
+    const int tiles_c = (rows + 63) / 64;
+    const int64_t tiles = int64_t(tiles_c) * ((cols + 63) / 64);
+    if (tiles <= 0) return hipSuccess;
+    if (tiles > INT32_MAX) return hipErrorInvalidValue;
+    hipLaunchKernelGGL(transpose_back_kernel, dim3{unsigned(tiles)}, dim3{256u}, 0, st, yt, y, rows, cols,
+                       tiles_c, mul, add, mul_shift, res, relu ? 1 : 0);
+    return hipGetLastError();
+}
+
 // Enqueues one generated kernel (with its split-K fill and epilogue passes).
 static hipError_t run_part(const ds_jit_conv *plan, const int32_t *x, const int32_t *residual,
                            int32_t *y, int64_t x_bytes, int64_t y_bytes, hipStream_t st)
@@ -1138,28 +1290,34 @@ static hipError_t run_part(const ds_jit_conv *plan, const int32_t *x, const int3
     const OutMap m = full_map(sp);
     const bool split = sp.nsplit > 1;
     int32_t *const dst = y;
-    if (plan->dense) {  // accumulate densely, scatter below
+    if (plan->dense) {  // accumulate densely (y^T for a transposed LinearShift), scatter below
         y = plan->dense;
         y_bytes = int64_t(g.n) * g.k * g.oh * g.ow * 4;
     }
     hipError_t e = hipSuccess;
     // Padded input: the template sees the copy as x with no padding, and its tap
     // (0, 0) offset is where each lane's window starts.
-    const bool padded = plan->xpad != nullptr;
+    const bool padded = sp.xh > 0;
     if (padded) {
         e = run_pad_planes(x, plan->xpad, int64_t(g.n) * g.c, g.h, g.w, g.ph, g.pw, sp.xh, sp.xw, st,
                            sp.act_bytes);
         x = plan->xpad;
         x_bytes = int64_t(g.n) * g.c * sp.xh * sp.xw * 4;
+    } else if (sp.xt) {
+        // with a split reduction, y^T starts at the bias in the same pass
+        e = run_transpose_in(x, plan->xpad, sp.lin.n, sp.lin.c, sp.act_bytes, split ? plan->init : nullptr, y,
+                             sp.lin.k, st);
+        x = plan->xpad;
+        x_bytes = int64_t(sp.lin.n) * sp.lin.c * 4;
     }
-    if (e == hipSuccess && split) e = run_fill_mapped(g, plan->init, y, sp.map, st);
+    if (e == hipSuccess && split && !sp.xt) e = run_fill_mapped(g, plan->init, y, sp.map, st);
     if (e == hipSuccess) {
         JitArgs a;
         a.x = x;
         a.y = y;
-        a.residual = split ? nullptr : residual;
+        a.residual = split || sp.xt ? nullptr : residual;
         a.x_bytes = int(x_bytes);
-        a.xshift = padded || sp.act_bytes == 4 ? 2 : sp.act_bytes == 2 ? 1 : 0;
+        a.xshift = padded || sp.xt || sp.act_bytes == 4 ? 2 : sp.act_bytes == 2 ? 1 : 0;
         a.y_bytes = int(y_bytes);
         a.OHOW = g.oh * g.ow;
         a.NQ = g.n * a.OHOW;
@@ -1188,7 +1346,7 @@ static hipError_t run_part(const ds_jit_conv *plan, const int32_t *x, const int3
         e = hipModuleLaunchKernel(plan->fn, unsigned(int64_t(sp.tiles_p) * sp.nseg), 1, 1,
                                   threads, 1, 1, lds, st, args, nullptr);
     }
-    if (e == hipSuccess && split) {
+    if (e == hipSuccess && split && !sp.xt) {
         Epilogue epi;
         epi.mul = plan->mul;
         epi.add = plan->add;
@@ -1197,7 +1355,14 @@ static hipError_t run_part(const ds_jit_conv *plan, const int32_t *x, const int3
         epi.relu = sp.relu;
         if (epi.any()) e = run_epilogue(g, y, epi, st);
     }
-    if (e == hipSuccess && plan->dense) e = run_copy_mapped(g, plan->dense, dst, plan->scatter, st);
+    // A transposed LinearShift ends in the pass that transposes y^T into y, with
+    // the whole epilogue of a split reduction, else the residual and its ReLU.
+    if (e == hipSuccess && sp.xt)
+        e = run_transpose_back(plan->dense, dst, sp.lin.n, sp.lin.k, split ? plan->mul : nullptr,
+                               split ? plan->add : nullptr, sp.mul_shift, residual,
+                               (split || residual) && sp.relu, st);
+    else if (e == hipSuccess && plan->dense)
+        e = run_copy_mapped(g, plan->dense, dst, plan->scatter, st);
     return e;
 }
 
@@ -1261,7 +1426,7 @@ extern "C" ds_status ds_jit_conv_query(const ds_jit_conv *plan, int64_t *code_by
 }
 
 extern "C" ds_status ds_jit_conv_layout(const ds_jit_conv *plan, int32_t *channels, int32_t *wsplit,
-                                        int32_t *pixel_groups, int32_t *pixel_tiles)
+                                        int32_t *pixel_groups, int32_t *pixel_tiles, int32_t *transposed)
 {
     if (!plan) return fail(DS_ERR_NULL_POINTER, "plan must not be NULL");
     const ds_jit_conv *k = plan->backward ? (plan->parts.empty() ? nullptr : plan->parts.front()) : plan;
@@ -1269,6 +1434,7 @@ extern "C" ds_status ds_jit_conv_layout(const ds_jit_conv *plan, int32_t *channe
     if (wsplit) *wsplit = k ? k->sp.wsplit : 1;
     if (pixel_groups) *pixel_groups = k ? k->sp.pgroups : 4;
     if (pixel_tiles) *pixel_tiles = k ? k->sp.tiles_p : 0;
+    if (transposed) *transposed = k && k->sp.xt ? 1 : 0;
     return ok();
 }
 

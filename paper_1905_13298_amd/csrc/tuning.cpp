@@ -13,7 +13,7 @@ namespace {
 
 const char *const kNames[kKnobs] = {"DS_FORCE_VARIANT",   "DS_JIT_WSPLIT", "DS_JIT_SLOTS", "DS_JIT_MAP",
                                     "DS_JIT_GROUP_TILES", "DS_JIT_ORDER",  "DS_JIT_TN",    "DS_JIT_PGROUPS",
-                                    "DS_ROWS_BATCH"};
+                                    "DS_ROWS_BATCH", "DS_JIT_TRANSPOSE"};
 
 struct Knobs {
     std::atomic<int> v[kKnobs];

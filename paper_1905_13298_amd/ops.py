@@ -458,13 +458,14 @@ class JitConv:
         cb, seg, sp = ctypes.c_int64(), ctypes.c_int32(), ctypes.c_int32()
         call("ds_jit_conv_query", self._h, ctypes.byref(cb), ctypes.byref(seg), ctypes.byref(sp))
         self.code_bytes, self.segments, self.splits = cb.value, seg.value, sp.value
-        tn, ws, pg, tiles = ctypes.c_int32(), ctypes.c_int32(), ctypes.c_int32(), ctypes.c_int32()
+        tn, ws, pg, tiles, tr = (ctypes.c_int32() for _ in range(5))
         call("ds_jit_conv_layout", self._h, ctypes.byref(tn), ctypes.byref(ws), ctypes.byref(pg),
-             ctypes.byref(tiles))
+             ctypes.byref(tiles), ctypes.byref(tr))
         # Output channels per segment, waves per 64 pixels (each streaming code of
-        # its own), groups of 64 pixels per workgroup, and the pixel tiles
-        # (workgroups) that run each segment.
+        # its own), groups of 64 pixels per workgroup, the pixel tiles (workgroups)
+        # that run each segment, and whether a LinearShift runs on x^T.
         self.channels, self.wsplit, self.pixel_groups, self.pixel_tiles = tn.value, ws.value, pg.value, tiles.value
+        self.transposed = bool(tr.value)
 
     # Cost model of the two paths on MI355X (microseconds), fitted to calls timed
     # back to back. A plan's waves each stream their share of the straight-line
@@ -483,7 +484,9 @@ class JitConv:
     # reading its packed weights at 4 TB/s. A LinearShift of fewer than 256 rows
     # takes the small-batch kernel instead (lanes own output channels): about 6
     # us plus 9.6 T dense SACs/s, or its packed weights at 1.5 TB/s when they
-    # dominate (each lane walks its own row).
+    # dominate (each lane walks its own row). A LinearShift plan on x^T adds its
+    # two transposing passes and runs its kernel about 15 % slower than modelled
+    # (8 us + 1.15 x the plan's own estimate fits batches 64-256 within 15 %).
     PLAN_STREAM_BPUS = 1.6e3        # code bytes per us per wave
     PLAN_ISSUE_PER_US = 872e3       # wave-instructions per us, whole chip
     RUNTIME_SAC_PER_US = 15e6       # dense SACs per us on full tiles
@@ -495,7 +498,8 @@ class JitConv:
         streams = max(1, self.segments * self.wsplit)
         executed = self.code_bytes / 4.2 * max(1, self.pixel_tiles) * max(1, self.pixel_groups)
         t = max(self.code_bytes / streams / self.PLAN_STREAM_BPUS, executed / self.PLAN_ISSUE_PER_US)
-        return 3.0 + (3.0 if self.splits > 1 else 0.0) + t
+        est = 3.0 + (3.0 if self.splits > 1 else 0.0) + t
+        return 8.0 + 1.15 * est if getattr(self, "transposed", False) else est
 
     def runtime_estimate_us(self) -> float:
         """Modelled duration of the same layer on the runtime kernel
@@ -512,15 +516,16 @@ class JitConv:
     def preferred(self) -> bool:
         """Whether this plan is expected to beat the runtime kernel, by the cost
         model above. Measured on MI355X as graph replays (model in brackets),
-        plan against runtime kernel: 4096 -> 4096 at batch 256 165 us (184)
-        against 346 us (329); 128 -> 128 3 x 3 at 28 x 28, batch 1 8.6 us (10)
-        against 42 us eager (33); 256 -> 128 at batch 8 4.2 us (5.5) against 4.5
-        us (5.5); 512 -> 1000 at batch 32 10.2 us (11) against 6.5 us (7.2);
-        25088 -> 4096 at batch 1 344 us (282) against 45 us (48). Over the layers
-        of ResNet-18 (batch 32) and ResNet-50 (batch 128) measured / modelled
-        plan durations have medians 1.16 and 1.04, runtime-kernel ones 0.97 and
-        0.92. Known miss: 2048 -> 1000 at batch 128, plan 39 us (27) against 32.5
-        us (33), so the plan is kept at a 20 % loss on that layer."""
+        plan against runtime kernel: 4096 -> 4096 at batch 256 on x^T 109-118 us
+        (105) against 346 us (329); 2048 -> 1000 at batch 128 on x^T 22.8-24 us
+        (21.5) against 32.5-36 us (33); 1024 -> 1024 at batch 64 on x^T 19.1 us
+        (17) against 13.8 us (12.5); 128 -> 128 3 x 3 at 28 x 28, batch 1 8.6 us
+        (10) against 42 us eager (33); 256 -> 128 at batch 8 4.2 us (5.5)
+        against 4.5 us (5.5); 512 -> 1000 at batch 32 10.2 us (11) against 6.5
+        us (7.2); 25088 -> 4096 at batch 1 344 us (282) against 45 us (48). Over
+        the layers of ResNet-18 (batch 32) and ResNet-50 (batch 128) measured /
+        modelled plan durations have medians 1.16 and 1.04, runtime-kernel ones
+        0.97 and 0.92."""
         return self.estimate_us() < self.runtime_estimate_us()
 
     def __call__(self, x: torch.Tensor, residual: torch.Tensor | None = None, out=None):
@@ -604,8 +609,8 @@ def run_layer_plan(plan: JitConv, layer, x: torch.Tensor, out: torch.Tensor | No
 def set_tuning(name: str, value: int) -> None:
     """Sets a tuning override of the library (``ds_set_tuning``): "DS_FORCE_VARIANT",
     "DS_JIT_WSPLIT", "DS_JIT_SLOTS", "DS_JIT_MAP", "DS_JIT_GROUP_TILES",
-    "DS_JIT_ORDER", "DS_JIT_TN", "DS_JIT_PGROUPS" or "DS_ROWS_BATCH"; a negative
-    value restores the library's own choice."""
+    "DS_JIT_ORDER", "DS_JIT_TN", "DS_JIT_PGROUPS", "DS_JIT_TRANSPOSE" or
+    "DS_ROWS_BATCH"; a negative value restores the library's own choice."""
     call("ds_set_tuning", name.encode(), int(value))
 
 

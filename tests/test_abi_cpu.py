@@ -313,7 +313,7 @@ def test_tuning_overrides_are_explicit():
     finally:
         ops.set_tuning("DS_JIT_ORDER", before)
     for name in ("DS_FORCE_VARIANT", "DS_JIT_WSPLIT", "DS_JIT_SLOTS", "DS_JIT_MAP", "DS_JIT_GROUP_TILES",
-                 "DS_JIT_ORDER", "DS_JIT_TN", "DS_JIT_PGROUPS", "DS_ROWS_BATCH"):
+                 "DS_JIT_ORDER", "DS_JIT_TN", "DS_JIT_PGROUPS", "DS_JIT_TRANSPOSE", "DS_ROWS_BATCH"):
         ops.get_tuning(name)   # every documented knob is known
     assert lib.ds_set_tuning(b"DS_NO_SUCH_KNOB", 1) == 3
     assert lib.ds_set_tuning(None, 1) == 1

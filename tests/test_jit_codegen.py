@@ -121,6 +121,55 @@ def lane_inputs(n, c, h, w, k, r, s, st, pd, wsplit=1, pgroups=None):
     return regs, (oh, ow)
 
 
+def transposed_linear(n, h, w, r, s):
+    """A LinearShift plan of batch >= 64 (>= 2 with DS_JIT_TRANSPOSE = 1, none with
+    0) runs its kernel on x^T [c][n] (an int32 copy the plan makes) as one image of
+    1 x n pixels, writing y^T [k][n]; a last pass transposes y^T into y, adding the
+    residual and applying the ReLU of a layer with a residual (the kernel then
+    applies neither)."""
+    forced = ops.get_tuning("DS_JIT_TRANSPOSE")
+    least = {0: 1 << 62, 1: 2}.get(forced, 64)
+    return h == w == r == s == 1 and n >= least
+
+
+def plan_lanes(n, c, h, w, k, r, s, st, pd, wsplit=1, pgroups=None):
+    """lane_inputs for the problem the plan's kernel sees (see transposed_linear)."""
+    if not transposed_linear(n, h, w, r, s):
+        return lane_inputs(n, c, h, w, k, r, s, st, pd, wsplit, pgroups)
+    lanes, _ = lane_inputs(1, c, 1, n, k, 1, 1, 1, 0, wsplit, pgroups)
+    return lanes, (1, 1)
+
+
+def y_start(bias, n, k, oh, ow, transposed):
+    """y (or y^T) as the split-K fill pass leaves it: the bias of each channel."""
+    b = bias.view(np.uint32).astype(np.int64)
+    return np.repeat(b, n) if transposed else np.repeat(np.tile(b, n), oh * ow)
+
+
+def transpose_back(y, n, k, res=None, relu=False):
+    """The last pass of a transposed LinearShift: y^T [k][n] -> y [n][k], plus the
+    residual, then the ReLU when there is a residual."""
+    out = to_i32(y).reshape(k, n).T.astype(np.int64)
+    if res is not None:
+        out = out + res.reshape(n, k).astype(np.int64)
+        if relu:
+            out = np.maximum(to_i32(out), 0)
+    return np.ascontiguousarray(out).reshape(-1).astype(np.int64) & M32
+
+
+def x_buffer(x, r, s, st, pd):
+    """The buffer the kernel reads x from (uint32 words as int64) and its bytes:
+    x itself, its zero-padded copy (windows over 3 x 3) or its transposed copy."""
+    n, c, h, w = x.shape
+    if transposed_linear(n, h, w, r, s):
+        xr = np.ascontiguousarray(x.reshape(n, c).T.astype(np.int32))
+    else:
+        ext = padded_extents(h, w, r, s, st, pd)
+        xr = x if ext is None else pad_input(x, pd, *ext)
+    xb = np.ascontiguousarray(xr).reshape(-1).view(np.uint32).astype(np.int64)
+    return xb, xb.size * 4
+
+
 class Interp:
     """The generated code, run for all lanes of one segment. ``run`` is a
     generator that stops at each s_barrier, so that the waves sharing pixels
@@ -289,7 +338,8 @@ CASES = [
     (3, 7, 12, 12, 64, 1, 1, 1, 0, 1, "relu"),
     (1, 6, 7, 8, 20, 2, 3, 1, 1, 3, "full"),
     (1, 3, 10, 10, 5, 3, 3, 2, 0, 1, "mul"),
-    (33, 40, 1, 1, 17, 1, 1, 1, 0, 1, "full"),     # a LinearShift [33 x 40] -> 17
+    (33, 40, 1, 1, 17, 1, 1, 1, 0, 1, "full"),     # a LinearShift [33 x 40] -> 17 (on x^T)
+    (1, 70, 1, 1, 20, 1, 1, 1, 0, 2, "full"),      # a LinearShift of one row (on x)
     (2, 64, 4, 4, 3, 3, 3, 1, 1, 4, "full"),
     (2, 3, 13, 11, 70, 7, 7, 2, 3, 1, "full"),     # a padded copy of x (windows over 3 x 3)
     (1, 4, 9, 10, 20, 5, 4, 1, 2, 2, "none"),
@@ -317,6 +367,22 @@ CASES = [
     (3, 13, 9, 9, 50, 3, 3, 1, 1, 1, "relu", 1, 64, 1),   # one wave per workgroup
     (1, 3, 13, 11, 40, 7, 7, 2, 3, 1, "mul", 2, 16, 4),   # padded copy
 ]
+
+
+LINEAR_CASES = [
+    # n, c, h, w, k, r, s, stride, pad, splits, epilogue, wave split, channels, pixel groups
+    (33, 40, 1, 1, 17, 1, 1, 1, 0, 1, "full", 1, 64, None),
+    (70, 300, 1, 1, 130, 1, 1, 1, 0, 2, "full", 4, 64, None),
+    (130, 90, 1, 1, 70, 1, 1, 1, 0, 1, "relu", 16, 16, 1),
+    (65, 200, 1, 1, 33, 1, 1, 1, 0, 3, "none", 2, 32, 4),
+]
+
+
+@pytest.mark.parametrize("transpose", [0, 1])
+@pytest.mark.parametrize("case", LINEAR_CASES, ids=[str(i) for i in range(len(LINEAR_CASES))])
+def test_linear_plans_on_x_and_on_x_transposed(case, transpose, tmp_path, knob):
+    knob("DS_JIT_TRANSPOSE", transpose)
+    run_generated(case, zlib.crc32(str((case, transpose)).encode()), 0.1, tmp_path, knob)
 
 
 @pytest.mark.parametrize("case", CASES, ids=[str(i) for i in range(len(CASES))])
@@ -376,7 +442,7 @@ def run_generated(case, seed, zero_frac, tmp_path, knob):
         add = rng.integers(-(2 ** 31), 2 ** 31, k, dtype=np.int64).astype(np.int32)
         add[0] = 0
     wp = ops.pack_shift_weights(codes)
-    lanes, (oh, ow) = lane_inputs(n, c, h, w, k, r, s, st, pd, wsplit, pgroups)
+    lanes, (oh, ow) = plan_lanes(n, c, h, w, k, r, s, st, pd, wsplit, pgroups)
     if epi == "full":
         res = rng.integers(-(2 ** 31), 2 ** 31, (n, k, oh, ow), dtype=np.int64).astype(np.int32)
     img = ops.jit_conv_image(wp, (n, c, h, w), (r, s), st, pd, bias=bias, mul=mul, add=add,
@@ -398,17 +464,18 @@ def run_generated(case, seed, zero_frac, tmp_path, knob):
     top = max(int(t[1:]) for _, ops_, _ in insts.values() for t in ops_ if re.fullmatch(r"v\d+", t))
     assert top < (80 if one_tap else 96), f"v{top} is outside the entry point's registers"
     conv = oracle.conv2d_shift(x, codes, bias, r=r, s=s, stride=st, pad=pd)
-    ext = padded_extents(h, w, r, s, st, pd)
-    xr = x if ext is None else pad_input(x, pd, *ext)
-    xb = np.ascontiguousarray(xr).reshape(-1).view(np.uint32).astype(np.int64)
+    xb, xbytes = x_buffer(x, r, s, st, pd)
     y = np.full(n * k * oh * ow, 0xDEADBEEF, dtype=np.int64)
-    bufs = {20: (xb, xb.size * 4), 24: (y, y.size * 4)}
+    bufs = {20: (xb, xbytes), 24: (y, y.size * 4)}
     bufs[36] = (res.reshape(-1).view(np.uint32).astype(np.int64), y.size * 4) if res is not None else (y, 0)
     nsplit = min(splits, c)
     kgroups = -(-k // tn)
     split = nsplit > 1
+    tr = transposed_linear(n, h, w, r, s)
+    if tr:      # the kernel reads no residual (the last pass adds it)
+        bufs[36] = (y, 0)
     if split:
-        y[:] = np.repeat(np.tile(bias.view(np.uint32).astype(np.int64), n), oh * ow)
+        y[:] = y_start(bias, n, k, oh, ow, tr)
     stubs = sum(1 for op, _, _ in insts.values() if op == "s_getpc_b64")
     assert stubs == kgroups * nsplit * wsplit
     interp = Interp(insts, bufs, wsplit, pgroups)
@@ -424,6 +491,8 @@ def run_generated(case, seed, zero_frac, tmp_path, knob):
         for r_ in runs:
             assert next(r_, "done") == "done", "a second barrier"
     assert len(total) == y.size and set(total.values()) == {nsplit}
+    if tr:
+        y = transpose_back(y, n, k, None if split else res, relu and not split)
     got = to_i32(y).reshape(n, k, oh, ow)
     if split:
         np.testing.assert_array_equal(got, conv)
@@ -547,19 +616,18 @@ def test_multiplication_plan_matches_oracle(case, tmp_path, knob):
     insts = disassemble(img, str(tmp_path))
     names = collections.Counter(op for op, _, _ in insts.values())
     body = min(insts)
-    lanes, (oh, ow) = lane_inputs(n, c, h, w, k, r, s, st, pd, wsplit)
+    lanes, (oh, ow) = plan_lanes(n, c, h, w, k, r, s, st, pd, wsplit)
     one_tap = r * s == 1 or r > 3 or s > 3
     if one_tap:
         for i in range(5, 13):
             del lanes[i]
-    ext = padded_extents(h, w, r, s, st, pd)
-    xr = x if ext is None else pad_input(x, pd, *ext)
-    xb = np.ascontiguousarray(xr).reshape(-1).view(np.uint32).astype(np.int64)
+    xb, xbytes = x_buffer(x, r, s, st, pd)
     y = np.full(n * k * oh * ow, 0xDEADBEEF, dtype=np.int64)
-    bufs = {20: (xb, xb.size * 4), 24: (y, y.size * 4), 36: (y, 0)}
+    bufs = {20: (xb, xbytes), 24: (y, y.size * 4), 36: (y, 0)}
     nsplit = min(splits, c)
+    tr = transposed_linear(n, h, w, r, s)
     if nsplit > 1:
-        y[:] = np.repeat(np.tile(bias.view(np.uint32).astype(np.int64), n), oh * ow)
+        y[:] = y_start(bias, n, k, oh, ow, tr)
     interp = Interp(insts, bufs, wsplit)
     total = collections.Counter()
     for seg in range(-(-k // 64) * nsplit):
@@ -571,6 +639,8 @@ def test_multiplication_plan_matches_oracle(case, tmp_path, knob):
                 next(r_, None)
         for r_ in runs:
             assert next(r_, "done") == "done"
+    if tr:
+        y = transpose_back(y, n, k)
     want = oracle.conv2d_mul24(x, wt, bias, r=r, s=s, stride=st, pad=pd)
     np.testing.assert_array_equal(to_i32(y).reshape(want.shape), want)
     # exactly one v_mad_i32_i24 per non-zero weight, no shift-plan arithmetic
@@ -599,32 +669,34 @@ def test_narrow_activation_plans_match_oracle(case, act_bits, tmp_path, knob):
     insts = disassemble(img, str(tmp_path))
     names = collections.Counter(op for op, _, _ in insts.values())
     ext = padded_extents(h, w, r, s, st, pd)
+    # x itself is read narrow; the padded and transposed copies are int32
+    narrow = ext is None and not transposed_linear(n, h, w, r, s)
     narrow_op = {16: "buffer_load_sshort", 8: "buffer_load_sbyte"}[act_bits]
-    if ext is None:
+    if narrow:
         assert names[narrow_op] > 0 and names["buffer_load_dword"] == 0
     else:
         assert names[narrow_op] == 0 and names["buffer_load_dword"] > 0
     body = min(insts)
-    lanes, (oh, ow) = lane_inputs(n, c, h, w, k, r, s, st, pd, wsplit)
-    if ext is None:       # the template scales tap offsets by the element size
+    lanes, (oh, ow) = plan_lanes(n, c, h, w, k, r, s, st, pd, wsplit)
+    if narrow:            # the template scales tap offsets by the element size
         for i in range(4, 13):
             lanes[i] = np.where(lanes[i] == OOB, OOB, lanes[i] // 4 * x.itemsize)
     if r * s == 1 or r > 3 or s > 3:
         for i in range(5, 13):
             del lanes[i]
-    if ext is None:
+    if narrow:
         xb = np.ascontiguousarray(x).reshape(-1)
         bufs = {20: (xb, xb.size * x.itemsize)}
     else:
-        xr = pad_input(x.astype(np.int32), pd, *ext)
-        xb = np.ascontiguousarray(xr).reshape(-1).view(np.uint32).astype(np.int64)
-        bufs = {20: (xb, xb.size * 4)}
+        xb, xbytes = x_buffer(x.astype(np.int32), r, s, st, pd)
+        bufs = {20: (xb, xbytes)}
     y = np.full(n * k * oh * ow, 0xDEADBEEF, dtype=np.int64)
     bufs[24] = (y, y.size * 4)
     bufs[36] = (y, 0)
     nsplit = min(splits, c)
+    tr = transposed_linear(n, h, w, r, s)
     if nsplit > 1:
-        y[:] = np.repeat(np.tile(bias.view(np.uint32).astype(np.int64), n), oh * ow)
+        y[:] = y_start(bias, n, k, oh, ow, tr)
     interp = Interp(insts, bufs, wsplit)
     total = collections.Counter()
     for seg in range(-(-k // 64) * nsplit):
@@ -636,5 +708,7 @@ def test_narrow_activation_plans_match_oracle(case, act_bits, tmp_path, knob):
                 next(r_, None)
         for r_ in runs:
             assert next(r_, "done") == "done"
+    if tr:
+        y = transpose_back(y, n, k)
     want = oracle.conv2d_shift(x, codes, bias, r=r, s=s, stride=st, pad=pd)
     np.testing.assert_array_equal(to_i32(y).reshape(want.shape), want)
