@@ -811,7 +811,7 @@ def roofline_of(layers, d, path, nonzero, planned=None, act_bits=32):
                 "entry_points": list(JIT_ENTRY_POINTS),
                 "nonzero_sac_per_launch_avg": int(g["nz"] // g["launches"]),
                 "dense_tsac_s": round(dense, 4),
-                "timed_span": "library call per launch (split-K fill pass + generated kernel)"}
+                "timed_span": "library call per launch (split-K fill pass, or for a LinearShift on x^T the transposing passes, + generated kernel)"}
     return {"bound": "alu", "achieved": round(dense, 4), "peak": round(SAC_PEAK_T, 4),
             "unit": "TSAC/s", "frac": round(dense / SAC_PEAK_T, 4), **common,
             "work_unit": "dense shift-accumulate, 2 int32 VALU ops each",

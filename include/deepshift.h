@@ -352,7 +352,7 @@ ds_status ds_conv2d_shift_describe(int64_t n, int64_t c, int64_t h, int64_t w, i
  * LinearShift is the case h = w = r = s = 1. Windows over 3 x 3 read a
  * zero-padded copy of x, [n][c][xh][xw] with xh = (oh - 1) * stride_h + r and
  * xw = (ow - 1) * stride_w + s, that each run writes first into device memory
- * the plan holds (from create to destroy). A LinearShift of batch n >= 64 runs
+ * the plan holds (from create to destroy). A LinearShift of batch n >= 32 runs
  * on x^T: each run first transposes x into an int32 copy [c][n] the plan holds
  * (so that a load reads consecutive batch rows), the generated kernel writes
  * y^T [k][n] into a buffer the plan holds, and a last pass transposes it into

@@ -630,10 +630,11 @@ ds_status finish_spec(Spec &sp, int bits, int splits, int deep_blocks = 3072)
     // workgroup, a wave split of 16 while each share keeps 64 input channels,
     // and parts toward 4096 waves while each wave keeps 16 input channels. Layout
     // sweeps of 3 x 5 x 3 x 4 segment widths, wave splits, pixel groups and parts
-    // on MI355X (graph replays, transposing passes included): 4096 -> 4096 at
-    // batch 256 116 us at best, 117 us by this rule (16 / 1 / 1), 182 us by the
-    // convolution rules below; 2048 -> 1000 at batch 128 25.1 / 25.5 (16 / 1 /
-    // 4) / 36.6 us; 1024 -> 1024 at batch 64 19.5 / 20.9 (16 / 1 / 4) / 26.6 us.
+    // on MI355X (graph replays, transposing passes of 64 x 64 tiles included):
+    // 4096 -> 4096 at batch 256 116 us at best, 117 us by this rule (16 / 1 / 1),
+    // 182 us by the convolution rules below; 2048 -> 1000 at batch 128 25.1 /
+    // 25.5 (16 / 1 / 4) / 36.6 us; 1024 -> 1024 at batch 64 19.5 / 20.9 (16 / 1
+    // / 4) / 26.6 us.
     if (sp.xt && sp.kjn.empty() && tuning(kJitTn) < 0 && tuning(kJitWsplit) < 0 && tuning(kJitPgroups) < 0) {
         sp.tn = nq >= 4 * 64 ? kTN : 32;
         sp.kgroups = (g.k + sp.tn - 1) / sp.tn;
@@ -797,12 +798,12 @@ ds_status plan_spec(const CreateArgs &a, Spec &sp)
     sp.bias = a.bias; sp.mul = a.mul; sp.add = a.add; sp.mul_shift = a.mul ? a.mul_shift : 0;
     sp.relu = a.flags & DS_RELU;
     sp.residual = a.flags & DS_JIT_RESIDUAL;
-    // Transposed from batch 64 up: the two transposing passes cost about 10 us
-    // (MI355X, graph replays), more than they save at small batches (8 x 256 ->
-    // 128: 15 against 4.2 us; 32 x 512 -> 1000: 17 against 10 us).
+    // Transposed from batch 32 up (MI355X, graph replays, both passes included:
+    // 2048 -> 1000 at batch 32 12.4 against 26.9 us on x, 512 -> 1000 at batch 32
+    // 10.2 against 10.3 us); at batch 8 the passes cost more than they save.
     const ConvGeom &g = sp.g;
     const int forced = tuning(kJitTranspose);
-    const bool want_xt = forced == 0 ? false : forced == 1 ? g.n > 1 : g.n >= 64;
+    const bool want_xt = forced == 0 ? false : forced == 1 ? g.n > 1 : g.n >= 32;
     if (want_xt && g.h == 1 && g.w == 1 && g.r == 1 && g.s == 1 && int64_t(g.n) * g.c <= kMaxElems / 4 &&
         int64_t(g.n) * g.k <= kMaxElems / 4) {
         sp.xt = true;
@@ -1187,16 +1188,19 @@ extern "C" ds_status ds_jit_conv_backward_data_create(const uint32_t *w_packed, 
 }
 
 // The first pass of a transposed LinearShift: xt [c][n] = x [n][c] as int32
-// (sign-extended from int16 / int8 elements), in 64 x 64 tiles through LDS
-// (reads and writes coalesced), and with a split reduction y^T [k][n] = init[k],
-// the start of the parts' atomic adds, in the workgroups after the tiles.
-// 256 threads.
+// (sign-extended from int16 / int8 elements), in 32 x 32 tiles through LDS
+// (reads and writes coalesced; 64 x 64 tiles, a quarter as many workgroups, ran
+// 4096 -> 4096 at batch 256 at 0.9 TB/s), and with a split reduction y^T [k][n]
+// = init[k], the start of the parts' atomic adds, in the workgroups after the
+// tiles. 256 threads.
+constexpr int kTT = 32;  // transpose tile
+
 template <typename T>
 __global__ void __launch_bounds__(256)
 transpose_in_kernel(const T *__restrict__ x, int32_t *__restrict__ xt, int rows, int cols, int tiles_c,
                     int tiles, const int32_t *__restrict__ init, int32_t *__restrict__ yt, int k)
 {
-    __shared__ int32_t tile[64][65];
+    __shared__ int32_t tile[kTT][kTT + 1];
     const int b = int(blockIdx.x);
     if (b >= tiles) {
         // fill: y^T [k][rows] = init[k], 256 elements per workgroup
@@ -1204,14 +1208,14 @@ transpose_in_kernel(const T *__restrict__ x, int32_t *__restrict__ xt, int rows,
         if (i < int64_t(k) * rows) yt[i] = init[i / rows];
         return;
     }
-    const int c0 = (b % tiles_c) * 64, r0 = (b / tiles_c) * 64;
-    const int tx = threadIdx.x & 63, ty = threadIdx.x >> 6;
-    for (int i = ty; i < 64; i += 4) {
+    const int c0 = (b % tiles_c) * kTT, r0 = (b / tiles_c) * kTT;
+    const int tx = threadIdx.x % kTT, ty = threadIdx.x / kTT;
+    for (int i = ty; i < kTT; i += 256 / kTT) {
         const int r = r0 + i, c = c0 + tx;
         if (r < rows && c < cols) tile[i][tx] = int32_t(x[int64_t(r) * cols + c]);
     }
     __syncthreads();
-    for (int i = ty; i < 64; i += 4) {
+    for (int i = ty; i < kTT; i += 256 / kTT) {
         const int c = c0 + i, r = r0 + tx;
         if (c < cols && r < rows) xt[int64_t(c) * rows + r] = tile[tx][i];
     }
@@ -1220,8 +1224,8 @@ transpose_in_kernel(const T *__restrict__ x, int32_t *__restrict__ xt, int rows,
 static hipError_t run_transpose_in(const int32_t *x, int32_t *xt, int rows, int cols, int xbytes,
                                    const int32_t *init, int32_t *yt, int k, hipStream_t st)
 {
-    const int tiles_c = (cols + 63) / 64;
-    const int64_t tiles = int64_t(tiles_c) * ((rows + 63) / 64);
+    const int tiles_c = (cols + kTT - 1) / kTT;
+    const int64_t tiles = int64_t(tiles_c) * ((rows + kTT - 1) / kTT);
     const int64_t fills = init ? (int64_t(k) * rows + 255) / 256 : 0;
     if (tiles + fills > INT32_MAX) return hipErrorInvalidValue;
     if (tiles + fills == 0) return hipSuccess;
@@ -1238,7 +1242,7 @@ static hipError_t run_transpose_in(const int32_t *x, int32_t *xt, int rows, int 
     return hipGetLastError();
 }
 
-// The last pass of a transposed LinearShift: y [n][k] = yt [k][n] in 64 x 64
+// The last pass of a transposed LinearShift: y [n][k] = yt [k][n] in 32 x 32
 // tiles through LDS, with what the generated kernel left of the epilogue: for a
 // split reduction all of it (v * mul[k] >> mul_shift, floor, + add[k]), and
 // then, for a layer with a residual, + res[n][k] and the ReLU. 256 threads.
@@ -1247,15 +1251,15 @@ transpose_back_kernel(const int32_t *__restrict__ yt, int32_t *__restrict__ y, i
                       int tiles_c, const int32_t *__restrict__ mul, const int32_t *__restrict__ add,
                       int mul_shift, const int32_t *__restrict__ res, int relu)
 {
-    __shared__ int32_t tile[64][65];
-    const int n0 = int(blockIdx.x % unsigned(tiles_c)) * 64, k0 = int(blockIdx.x / unsigned(tiles_c)) * 64;
-    const int tx = threadIdx.x & 63, ty = threadIdx.x >> 6;
-    for (int i = ty; i < 64; i += 4) {
+    __shared__ int32_t tile[kTT][kTT + 1];
+    const int n0 = int(blockIdx.x % unsigned(tiles_c)) * kTT, k0 = int(blockIdx.x / unsigned(tiles_c)) * kTT;
+    const int tx = threadIdx.x % kTT, ty = threadIdx.x / kTT;
+    for (int i = ty; i < kTT; i += 256 / kTT) {
         const int k = k0 + i, n = n0 + tx;
         if (k < cols && n < rows) tile[i][tx] = yt[int64_t(k) * rows + n];
     }
     __syncthreads();
-    for (int i = ty; i < 64; i += 4) {
+    for (int i = ty; i < kTT; i += 256 / kTT) {
         const int n = n0 + i, k = k0 + tx;
         if (n < rows && k < cols) {
             const int64_t o = int64_t(n) * cols + k;
@@ -1272,8 +1276,8 @@ static hipError_t run_transpose_back(const int32_t *yt, int32_t *y, int rows, in
                                      const int32_t *add, int mul_shift, const int32_t *res, bool relu,
                                      hipStream_t st)
 {
-    const int tiles_c = (rows + 63) / 64;
-    const int64_t tiles = int64_t(tiles_c) * ((cols + 63) / 64);
+    const int tiles_c = (rows + kTT - 1) / kTT;
+    const int64_t tiles = int64_t(tiles_c) * ((cols + kTT - 1) / kTT);
     if (tiles <= 0) return hipSuccess;
     if (tiles > INT32_MAX) return hipErrorInvalidValue;
     hipLaunchKernelGGL(transpose_back_kernel, dim3{unsigned(tiles)}, dim3{256u}, 0, st, yt, y, rows, cols,

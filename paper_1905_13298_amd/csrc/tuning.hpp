@@ -17,7 +17,7 @@ enum Knob {
     kJitTn,          // DS_JIT_TN: output channels per code segment in a plan (16, 32, 64)
     kJitPgroups,     // DS_JIT_PGROUPS: groups of 64 pixels per workgroup in a plan (1, 2, 4)
     kRowsBatch,      // DS_ROWS_BATCH: batch rows per workgroup of the small-batch LinearShift (1, 2, 4, 8)
-    kJitTranspose,   // DS_JIT_TRANSPOSE: LinearShift plans on x^T: 0 never, 1 from batch 2 (default: batch >= 64)
+    kJitTranspose,   // DS_JIT_TRANSPOSE: LinearShift plans on x^T: 0 never, 1 from batch 2 (default: batch >= 32)
     kKnobs
 };
 

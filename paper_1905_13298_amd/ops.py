@@ -486,7 +486,7 @@ class JitConv:
     # us plus 9.6 T dense SACs/s, or its packed weights at 1.5 TB/s when they
     # dominate (each lane walks its own row). A LinearShift plan on x^T adds its
     # two transposing passes and runs its kernel about 15 % slower than modelled
-    # (8 us + 1.15 x the plan's own estimate fits batches 64-256 within 15 %).
+    # (2.5 us + 1.16 x the plan's own estimate fits batches 64-256 within 15 %).
     PLAN_STREAM_BPUS = 1.6e3        # code bytes per us per wave
     PLAN_ISSUE_PER_US = 872e3       # wave-instructions per us, whole chip
     RUNTIME_SAC_PER_US = 15e6       # dense SACs per us on full tiles
@@ -499,7 +499,7 @@ class JitConv:
         executed = self.code_bytes / 4.2 * max(1, self.pixel_tiles) * max(1, self.pixel_groups)
         t = max(self.code_bytes / streams / self.PLAN_STREAM_BPUS, executed / self.PLAN_ISSUE_PER_US)
         est = 3.0 + (3.0 if self.splits > 1 else 0.0) + t
-        return 8.0 + 1.15 * est if getattr(self, "transposed", False) else est
+        return 2.5 + 1.16 * est if getattr(self, "transposed", False) else est
 
     def runtime_estimate_us(self) -> float:
         """Modelled duration of the same layer on the runtime kernel
@@ -516,10 +516,11 @@ class JitConv:
     def preferred(self) -> bool:
         """Whether this plan is expected to beat the runtime kernel, by the cost
         model above. Measured on MI355X as graph replays (model in brackets),
-        plan against runtime kernel: 4096 -> 4096 at batch 256 on x^T 109-118 us
-        (105) against 346 us (329); 2048 -> 1000 at batch 128 on x^T 22.8-24 us
-        (21.5) against 32.5-36 us (33); 1024 -> 1024 at batch 64 on x^T 19.1 us
-        (17) against 13.8 us (12.5); 128 -> 128 3 x 3 at 28 x 28, batch 1 8.6 us
+        plan against runtime kernel: 4096 -> 4096 at batch 256 on x^T 104-109
+        us (108) against 346 us (329); 2048 -> 1000 at batch 128 on x^T 17.0 us
+        (17.5) against 32.5-36 us (33); 1024 -> 1024 at batch 64 on x^T 11.9 us
+        (12.0) against 13.7 us (12.5); 512 -> 512 at batch 128 on x^T 10.3 us
+        (12.0) against 8.4 us (9.0); 128 -> 128 3 x 3 at 28 x 28, batch 1 8.6 us
         (10) against 42 us eager (33); 256 -> 128 at batch 8 4.2 us (5.5)
         against 4.5 us (5.5); 512 -> 1000 at batch 32 10.2 us (11) against 6.5
         us (7.2); 25088 -> 4096 at batch 1 344 us (282) against 45 us (48). Over

@@ -35,16 +35,18 @@ CASES = [
     ((1, 25088, 1, 1, 4096, 1, 1, 1, 1), (450e6, 256, 4, 64, 4, 1), 344.3, 45.3),
     # On x^T (batch >= 64): 4096 -> 4096 at batch 256, 64-channel segments, wave
     # split 16, 4 tiles of 64 rows
-    ((256, 4096, 1, 1, 4096, 1, 1, 1, 1), (74.3e6, 64, 1, 64, 16, 4, True), 118.4, 347.8),
+    ((256, 4096, 1, 1, 4096, 1, 1, 1, 1), (74.3e6, 64, 1, 64, 16, 4, True), 108.7, 346.9),
     # 2048 -> 1000 at batch 128: 32-channel segments, wave split 16, 4 parts
-    ((128, 2048, 1, 1, 1000, 1, 1, 1, 1), (10.7e6, 128, 4, 32, 16, 2, True), 24.0, 36.2),
-    # 1024 -> 1024 at batch 64: the same layout; small-batch runtime kernel
-    ((64, 1024, 1, 1, 1024, 1, 1, 1, 1), (5.95e6, 128, 4, 32, 16, 1, True), 19.1, 13.8),
+    ((128, 2048, 1, 1, 1000, 1, 1, 1, 1), (10.7e6, 128, 4, 32, 16, 2, True), 17.0, 35.7),
+    # 1024 -> 1024 at batch 64: the same layout
+    ((64, 1024, 1, 1, 1024, 1, 1, 1, 1), (5.95e6, 128, 4, 32, 16, 1, True), 11.9, 13.7),
+    # 512 -> 512 at batch 128: wave split 8, 4 parts; small-batch runtime kernel
+    ((128, 512, 1, 1, 512, 1, 1, 1, 1), (1.5e6, 64, 4, 32, 8, 2, True), 10.3, 8.44),
 ]
 
 
 @pytest.mark.parametrize("case", CASES, ids=["conv_n1", "linear_b8", "fc_b32", "fc6_b1", "fc_b256_xt",
-                                              "fc_b128_xt", "fc_b64_xt"])
+                                              "fc_b128_xt", "fc_b64_xt", "fc_b128_small_xt"])
 def test_model_tracks_measured_durations_and_picks_the_faster_path(case):
     shape, layout, plan_us, rt_us = case
     p = fake_plan(*shape, *layout)

@@ -1,5 +1,5 @@
 """GPU parity of weight-specialised LinearShift plans on x^T (the default from
-batch 64, forced here from batch 2 with DS_JIT_TRANSPOSE = 1), which run their
+batch 32, forced here from batch 2 with DS_JIT_TRANSPOSE = 1), which run their
 kernel on an int32 copy of x^T (loads of 64 consecutive batch rows of one input
 channel) and write y^T, transposed back into y by a last pass that adds the
 residual and applies the ReLU of a layer with one.

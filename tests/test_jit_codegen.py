@@ -122,13 +122,13 @@ def lane_inputs(n, c, h, w, k, r, s, st, pd, wsplit=1, pgroups=None):
 
 
 def transposed_linear(n, h, w, r, s):
-    """A LinearShift plan of batch >= 64 (>= 2 with DS_JIT_TRANSPOSE = 1, none with
+    """A LinearShift plan of batch >= 32 (>= 2 with DS_JIT_TRANSPOSE = 1, none with
     0) runs its kernel on x^T [c][n] (an int32 copy the plan makes) as one image of
     1 x n pixels, writing y^T [k][n]; a last pass transposes y^T into y, adding the
     residual and applying the ReLU of a layer with a residual (the kernel then
     applies neither)."""
     forced = ops.get_tuning("DS_JIT_TRANSPOSE")
-    least = {0: 1 << 62, 1: 2}.get(forced, 64)
+    least = {0: 1 << 62, 1: 2}.get(forced, 32)
     return h == w == r == s == 1 and n >= least
 
 
