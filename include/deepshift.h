@@ -444,8 +444,9 @@ ds_status ds_jit_conv_layout(const ds_jit_conv *plan, int32_t *channels, int32_t
  * kernel writing its own rows and columns of dx; ds_jit_conv_run(plan, dy,
  * NULL, dx, stream) then takes dy [n][k][oh][ow] and writes all of dx
  * [n][c][h][w] (residual must be NULL). A LinearShift is the case
- * h = w = r = s = 1. Phases with windows over 3 x 3 read a padded copy of dy
- * as forward plans do. DS_ERR_UNSUPPORTED when a phase is wider than 1023
+ * h = w = r = s = 1; from batch 32 its plan runs on dy^T as a forward
+ * LinearShift plan runs on x^T. Phases with windows over 3 x 3 read a padded
+ * copy of dy as forward plans do. DS_ERR_UNSUPPORTED when a phase is wider than 1023
  * columns. ds_jit_conv_query reports the code of all phases. Other errors as
  * for ds_jit_conv_create. */
 ds_status ds_jit_conv_backward_data_create(const uint32_t *w_packed, int64_t n, int64_t c,

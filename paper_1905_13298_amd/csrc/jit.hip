@@ -774,6 +774,23 @@ ds_status check_layer(int64_t n, int64_t c, int64_t h, int64_t w, int64_t k, int
     return DS_SUCCESS;
 }
 
+// A LinearShift (a 1 x 1 window on 1 x 1 inputs, output dense) runs on x^T from
+// batch 32 up (see Spec::xt; MI355X, graph replays, both passes included: 2048 ->
+// 1000 at batch 32 12.4 against 26.9 us on x, 512 -> 1000 at batch 32 10.2
+// against 10.3 us); at batch 8 the passes cost more than they save.
+void transpose_linear(Spec &sp)
+{
+    const ConvGeom g = sp.g;
+    const int forced = tuning(kJitTranspose);
+    const bool want = forced == 0 ? false : forced == 1 ? g.n > 1 : g.n >= 32;
+    if (want && g.h == 1 && g.w == 1 && g.r == 1 && g.s == 1 && g.ph == 0 && g.pw == 0 && sp.map.dense() &&
+        int64_t(g.n) * g.c <= kMaxElems / 4 && int64_t(g.n) * g.k <= kMaxElems / 4) {
+        sp.xt = true;
+        sp.lin = g;
+        sp.g = ConvGeom{1, g.c, 1, g.n, g.k, 1, 1, 1, 1, 0, 0, 1, g.n, g.c, g.bits};
+    }
+}
+
 // Validation and planning shared by ds_jit_conv_create and ds_jit_conv_image.
 ds_status plan_spec(const CreateArgs &a, Spec &sp)
 {
@@ -798,18 +815,7 @@ ds_status plan_spec(const CreateArgs &a, Spec &sp)
     sp.bias = a.bias; sp.mul = a.mul; sp.add = a.add; sp.mul_shift = a.mul ? a.mul_shift : 0;
     sp.relu = a.flags & DS_RELU;
     sp.residual = a.flags & DS_JIT_RESIDUAL;
-    // Transposed from batch 32 up (MI355X, graph replays, both passes included:
-    // 2048 -> 1000 at batch 32 12.4 against 26.9 us on x, 512 -> 1000 at batch 32
-    // 10.2 against 10.3 us); at batch 8 the passes cost more than they save.
-    const ConvGeom &g = sp.g;
-    const int forced = tuning(kJitTranspose);
-    const bool want_xt = forced == 0 ? false : forced == 1 ? g.n > 1 : g.n >= 32;
-    if (want_xt && g.h == 1 && g.w == 1 && g.r == 1 && g.s == 1 && int64_t(g.n) * g.c <= kMaxElems / 4 &&
-        int64_t(g.n) * g.k <= kMaxElems / 4) {
-        sp.xt = true;
-        sp.lin = g;
-        sp.g = ConvGeom{1, g.c, 1, g.n, g.k, 1, 1, 1, 1, 0, 0, 1, g.n, g.c, bits};
-    }
+    transpose_linear(sp);
     return finish_spec(sp, bits, a.splits);
 }
 
@@ -1150,6 +1156,7 @@ extern "C" ds_status ds_jit_conv_backward_data_create(const uint32_t *w_packed, 
             sp.g = ph.g;
             sp.wp = codes.data();
             sp.map = ph.map;
+            transpose_linear(sp);  // the input gradient of a LinearShift: dx = dy W, on dy^T
             // A strided phase that splits pays a dense buffer's round trip (below), so
             // it splits only toward the 384-block floor (MI355X: a 3x3 stride-2 layer's
             // phases ran 1.3x faster unsplit at 392 blocks than at 2 parts, and 1.1x

@@ -138,3 +138,20 @@ def test_transposed_linear_plan_runs_twice_on_new_inputs():
         y = plan(to_dev(xi.reshape(n, c, 1, 1))).cpu().numpy().reshape(n, k)
         np.testing.assert_array_equal(y, oracle.linear_shift(xi, codes, bias))
     plan.close()
+
+
+@pytest.mark.parametrize("splits", [0, 1, 3])
+@pytest.mark.parametrize("shape", [(2, 7, 3), (33, 300, 70), (130, 97, 200), (256, 512, 300)],
+                         ids=["2x7to3", "33x300to70", "130x97to200", "256x512to300"])
+def test_transposed_linear_input_gradient_plans(shape, splits):
+    """Input-gradient plans of a LinearShift (dx [n][c] = dy [n][k] through the
+    codes): on dy^T, transposed back into dx."""
+    n, c, k = shape
+    rng = np.random.default_rng(zlib.crc32(repr((shape, splits)).encode()))
+    codes = (rng.integers(0, 2, (k, c)) << 4 | rng.integers(0, 16, (k, c))).astype(np.uint8)
+    dy = rng.integers(-(2 ** 31), 2 ** 31, (n, k), dtype=np.int64).astype(np.int32)
+    say(f"jit linear input gradient {shape} splits={splits}")
+    plan = ops.JitConvBackwardData(ops.pack_shift_weights(codes), (n, c, 1, 1), 1, splits=splits)
+    dx = plan(to_dev(dy.reshape(n, k, 1, 1))).cpu().numpy().reshape(n, c)
+    plan.close()
+    np.testing.assert_array_equal(dx, oracle.linear_shift_backward_data(dy, codes))
