@@ -201,10 +201,13 @@ def test_plans_replay_in_a_captured_graph():
     three replays, with the outputs overwritten eagerly between them, each equal
     to the eager result, itself equal to the oracle."""
     rng = np.random.default_rng(77)
-    cases = [  # n, c, h, w, k, r, s, stride, pad, splits: padded 5x5, wave split, split-K
+    cases = [  # n, c, h, w, k, r, s, stride, pad, splits: padded 5x5, wave split, split-K,
+        # LinearShifts on x^T (transposing passes; the first pass also fills y^T when split)
         (2, 3, 15, 13, 40, 5, 5, 2, 2, 0),
         (2, 40, 9, 9, 70, 3, 3, 1, 1, 0),
         (3, 300, 6, 6, 9, 1, 1, 1, 0, 3),
+        (70, 300, 1, 1, 130, 1, 1, 1, 0, 1),
+        (64, 200, 1, 1, 90, 1, 1, 1, 0, 3),
     ]
     runs, wants = [], []
     for (n, c, h, w, k, r, s, st, pd, sp) in cases:
@@ -241,7 +244,7 @@ def test_plans_replay_in_a_captured_graph():
         torch.cuda.synchronize()
         for (_, _, y), want in zip(runs, wants):
             np.testing.assert_array_equal(y.cpu().numpy(), want, err_msg=f"replay {rep}")
-    say("graph of 3 plans: 3 replays equal the oracle")
+    say(f"graph of {len(runs)} plans: 3 replays equal the oracle")
     del graph
     for plan, _, _ in runs:
         plan.close()
