@@ -625,6 +625,8 @@ static const Variant kVariants[] = {
     {MODE_WINDOW, 4, 2, 7, 24}, {MODE_WINDOW, 4, 1, 7, 24},
     {MODE_WINDOW, 4, 2, 1, 16}, {MODE_WINDOW, 4, 2, 2, 16}, {MODE_WINDOW, 4, 2, 5, 16},
     {MODE_WINDOW, 4, 1, 5, 24},
+    // 4 taps per row: the 4-tap stride phases of a 7 x 7 / 2 layer's input gradient
+    {MODE_WINDOW, 4, 2, 4, 16}, {MODE_WINDOW, 4, 1, 4, 24},
 };
 
 template <Inner OP, int MODE, int TM, int CC, int SK, int GW>
@@ -657,6 +659,8 @@ static hipError_t dispatch_tiled(const Variant &v, const TiledParams &p, int gri
     DS_CASE(MODE_WINDOW, 4, 2, 2, 16)
     DS_CASE(MODE_WINDOW, 4, 2, 5, 16)
     DS_CASE(MODE_WINDOW, 4, 1, 5, 24)
+    DS_CASE(MODE_WINDOW, 4, 2, 4, 16)
+    DS_CASE(MODE_WINDOW, 4, 1, 4, 24)
 #undef DS_CASE
     return hipErrorInvalidValue;
 }

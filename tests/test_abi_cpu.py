@@ -149,7 +149,8 @@ def test_describe_names_a_kernel_without_a_gpu():
     assert ops.describe_conv2d(128, 64, 56, 56, 256, 1).startswith("tiled point")
     assert ops.describe_conv2d(128, 64, 56, 56, 64, 3, 1, 1).startswith("tiled window")
     assert ops.describe_conv2d(2, 3, 224, 224, 64, 7, 2, 3).startswith("tiled window")
-    assert ops.describe_conv2d(1, 3, 9, 9, 5, 4, 1, 1) == "direct"
+    assert ops.describe_conv2d(1, 3, 9, 9, 5, 4, 1, 1).startswith("tiled window tm4 cc1 s4")
+    assert ops.describe_conv2d(1, 3, 12, 12, 5, 6, 1, 1) == "direct"   # no instance for 6 taps per row
     # LinearShift (1 x 1 on 1 x 1 inputs) below 256 rows: the small-batch kernel
     assert ops.describe_conv2d(1, 25088, 1, 1, 4096, 1) == "rows"
     assert ops.describe_conv2d(255, 2048, 1, 1, 1000, 1) == "rows"
@@ -290,7 +291,8 @@ def test_backward_describe_plans_phases_without_a_gpu():
     ds = d(128, 1024, 14, 14, 2048, 1, 2, 0)
     assert ds.startswith("phases4; 1x1 tiled point") and ds.count("zero") == 3
     assert d(256, 4096, 1, 1, 4096, 1).startswith("phases1; 1x1 tiled point transposed")
-    assert d(2, 3, 224, 224, 64, 7, 2, 3) == "direct"          # tap width 4 has no instance
+    stem = d(2, 3, 224, 224, 64, 7, 2, 3)                       # phases of 3 and 4 taps per row
+    assert stem.startswith("phases4") and stem.count("tiled") == 4 and stem.count(" s4 ") == 2
     assert d(1, 3, 6, 6, 2, 1, 1, 1) == "direct"               # padding beyond the window
     with pytest.raises(ops.DeepShiftError, match="INVALID_SHAPE"):
         d(1, 1, 2, 2, 1, 3, 1, 0)

@@ -56,7 +56,7 @@ EDGE = [
     ("s1_1x1", 2, 9, 7, 5, 70, 1, 1, 1, 0),
     ("rect_2x3", 2, 5, 10, 12, 6, (2, 3), (2, 3), 1, 1),
     ("rect_stride", 2, 5, 9, 8, 3, (2, 3), (2, 3), (2, 1), (1, 0)),   # negative-pad phase: gather
-    ("s2_7x7_stem", 2, 3, 30, 30, 16, 7, 7, 2, 3),                    # tap width 4: gather; plans: padded
+    ("s2_7x7_stem", 2, 3, 30, 30, 16, 7, 7, 2, 3),                    # 3- and 4-tap phases; plans: padded
     ("pad_beyond_1x1", 1, 3, 6, 6, 2, 1, 1, 1, 1),                    # gather
     ("big_k_small_c", 2, 3, 12, 12, 300, 3, 3, 2, 1),
     ("many_tiles", 4, 64, 20, 20, 128, 3, 3, 1, 1),
@@ -99,7 +99,8 @@ def test_plans_cover_the_expected_paths():
     assert d(2, 64, 56, 56, 64, 3, 1, 1).startswith("phases1")
     assert "zero" in d(8, 64, 14, 14, 70, 1, 2, 0)
     assert d(2, 5, 9, 8, 3, (2, 3), (2, 1), (1, 0)) == "direct"
-    assert d(2, 3, 30, 30, 16, 7, 2, 3) == "direct"
+    stem = d(2, 3, 30, 30, 16, 7, 2, 3)
+    assert stem.startswith("phases4") and stem.count("tiled") == 4
 
 
 @pytest.mark.parametrize("shape", [(8, 256, 128), (33, 300, 70), (256, 4096, 4096), (1, 1, 1)])
@@ -197,6 +198,38 @@ def test_resnet50_full_batch_against_gather_kernel_and_oracle(knob):
                                                         stride=L.stride, pad=L.pad)
         np.testing.assert_array_equal(got, want, err_msg=L.name)
         del dx, ref, dyd
+
+
+def test_stem_gradient_on_tiled_phases_full_size(knob):
+    """The 7 x 7 / 2 stem's input gradient at 224 x 224 (batch 4) on the runtime
+    path: four stride phases of 3 and 4 taps per row on the tiled kernel. All
+    elements equal the gather kernel's and the plan's, 400 sampled elements the
+    oracle's."""
+    L = W.config_layers(4)[0]
+    n = 4
+    x_shape = (n,) + tuple(L.x_shape[1:])
+    codes = W.gen_codes(L, W.CONFIG_SEEDS[4], 0)
+    g = np.random.default_rng(17)
+    dy = np.rint(g.standard_normal((n, L.k) + tuple(L.y_shape[2:]), dtype=np.float32) * 2 ** 16).astype(np.int32)
+    path = ops.describe_conv2d_backward_data(*x_shape, L.k, (L.r, L.s), L.stride, L.pad)
+    assert path.startswith("phases4") and path.count("tiled") == 4, path
+    say(f"backward stem {x_shape}: {path}")
+    wp = to_dev(ops.pack_shift_weights(codes).view(np.int32))
+    dyd = to_dev(dy)
+    dx = ops.conv2d_shift_backward_data(dyd, wp, x_shape, (L.r, L.s), L.stride, L.pad)
+    knob("DS_FORCE_VARIANT", 0)
+    ref = ops.conv2d_shift_backward_data(dyd, wp, x_shape, (L.r, L.s), L.stride, L.pad)
+    knob("DS_FORCE_VARIANT", -1)
+    assert int((dx != ref).sum()) == 0
+    plan = ops.JitConvBackwardData(ops.pack_shift_weights(codes), x_shape, (L.r, L.s), L.stride, L.pad)
+    assert int((plan(dyd) != dx).sum()) == 0
+    plan.close()
+    total = int(np.prod(x_shape))
+    idx = np.unique(np.concatenate([np.random.default_rng(3).choice(total, 400, replace=False), [0, total - 1]]))
+    got = dx.reshape(-1)[torch.from_numpy(idx).to(DEV)].cpu().numpy()
+    want = oracle.conv2d_shift_backward_data_points(dy, codes, x_shape, idx, r=L.r, s=L.s, stride=L.stride,
+                                                    pad=L.pad)
+    np.testing.assert_array_equal(got, want)
 
 
 JIT_EDGE = EDGE

@@ -110,7 +110,8 @@ EDGE = [
     ("3x3_s3_pad2", 1, 6, 17, 17, 8, 3, 3, 3, 2),
     ("rect_2x3", 2, 5, 10, 12, 6, (2, 3), None, (1, 2), (0, 1)),
     ("5x5", 1, 4, 12, 12, 9, 5, 5, 1, 2),
-    ("s4_direct", 1, 3, 9, 9, 5, 4, 4, 1, 1),
+    ("4x4", 1, 3, 9, 9, 5, 4, 4, 1, 1),
+    ("6x6_direct", 1, 3, 12, 12, 5, 6, 6, 1, 1),
     ("7x7_images", 5, 16, 7, 7, 40, 3, 3, 1, 1),
     ("batch1_1x1_image", 1, 64, 1, 1, 10, 1, 1, 1, 0),
     ("tiny", 1, 1, 1, 1, 1, 1, 1, 1, 0),
