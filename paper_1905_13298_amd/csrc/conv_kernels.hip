@@ -995,6 +995,10 @@ linear_rows_kernel(const int32_t *__restrict__ x, const RowsArgs a)
     constexpr int E = U * PER;                               // columns per chunk
     __shared__ uint32_t part[kRowsWaves][ROWS][64];
     __shared__ int32_t xbuf[kRowsWaves][ROWS][E];
+    // A chunk's packed words of the wave's 64 weight rows, loaded 8 rows of U
+    // consecutive words per instruction (lanes U words apart would touch 64 cache
+    // lines per load) and read back row by row (odd row pitch: no bank conflicts).
+    __shared__ uint32_t wbuf[OP == Inner::Shift ? kRowsWaves : 1][64][U + 1];
     const int lane = threadIdx.x & 63;
     const int wave = __builtin_amdgcn_readfirstlane(int(threadIdx.x >> 6));
     const int k = int(blockIdx.x) * 64 + lane;
@@ -1013,24 +1017,58 @@ linear_rows_kernel(const int32_t *__restrict__ x, const RowsArgs a)
     const int u0 = p0 + int(int64_t(p1 - p0) * wave / kRowsWaves);
     const int u1 = p0 + int(int64_t(p1 - p0) * (wave + 1) / kRowsWaves);
     const CodeFmt fmt{BITS, 32 / BITS};
-    for (int uc = u0; uc < u1; uc += U) {
-        // This chunk's weights (one load per unit and lane) and inputs (staged).
-        uint32_t wv[OP == Inner::Shift ? U : 1];
-        if constexpr (OP == Inner::Shift) {
-            const uint32_t *row = a.wp + int64_t(kc) * a.wpr;
+    if constexpr (OP == Inner::Shift) {
+        // Each chunk's weight words and inputs are loaded into registers, then
+        // staged through LDS: the weight words 8 rows of U consecutive words per
+        // load instruction (lanes U words apart would touch 64 cache lines per
+        // load), read back row by row. With one batch row per workgroup (the least
+        // arithmetic per load) they are loaded one chunk ahead, so that their
+        // latency overlaps the previous chunk's arithmetic: on MI355X 25088 ->
+        // 4096 at batch 1 ran in 41.6 instead of 45.9 us, while the multi-row
+        // tilings ran 1-4 % slower that way (fewer waves fit their registers).
+        constexpr bool kAhead = ROWS == 1;
+        constexpr int XE = (E + 63) / 64;  // input columns per lane and row
+        uint32_t nw[U];
+        int32_t nx[ROWS][XE];
+        auto fetch = [&](int uc) {
 #pragma unroll
-            for (int u = 0; u < U; ++u) wv[u] = row[min(uc + u, u1 - 1)];
-        }
-        const int cb = uc * PER;
+            for (int i = 0; i < U; ++i) {
+                const int e = i * 64 + lane, rr = e / U, ww = e % U;
+                const int kr = min(int(blockIdx.x) * 64 + rr, a.K - 1);
+                nw[i] = a.wp[int64_t(kr) * a.wpr + min(uc + ww, u1 - 1)];
+            }
+            const int cb = uc * PER;
 #pragma unroll
-        for (int r = 0; r < ROWS; ++r) {
-            const int32_t *xrow = x + int64_t(b0 + min(r, nb - 1)) * a.C;
+            for (int r = 0; r < ROWS; ++r) {
+                const int32_t *xrow = x + int64_t(b0 + min(r, nb - 1)) * a.C;
 #pragma unroll
-            for (int e = lane; e < E; e += 64) xbuf[wave][r][e] = xrow[min(cb + e, a.C - 1)];
-        }
-        // (LDS is written and read back by the same wave: in order, no barrier.)
-        const int un = min(U, u1 - uc);
-        if constexpr (OP == Inner::Shift) {
+                for (int t = 0; t < XE; ++t) {
+                    const int e = lane + 64 * t;
+                    if (e < E) nx[r][t] = xrow[min(cb + e, a.C - 1)];
+                }
+            }
+        };
+        if (kAhead && u0 < u1) fetch(u0);
+        for (int uc = u0; uc < u1; uc += U) {
+            if (!kAhead) fetch(uc);
+#pragma unroll
+            for (int i = 0; i < U; ++i) {
+                const int e = i * 64 + lane;
+                wbuf[wave][e / U][e % U] = nw[i];
+            }
+#pragma unroll
+            for (int r = 0; r < ROWS; ++r)
+#pragma unroll
+                for (int t = 0; t < XE; ++t)
+                    if (lane + 64 * t < E) xbuf[wave][r][lane + 64 * t] = nx[r][t];
+            // Written and read back by the same wave, whose LDS accesses run in
+            // order; the wave barrier keeps the compiler from moving the reads up.
+            __builtin_amdgcn_wave_barrier();
+            uint32_t wv[U];
+#pragma unroll
+            for (int u = 0; u < U; ++u) wv[u] = wbuf[wave][lane][u];
+            if (kAhead && uc + U < u1) fetch(uc + U);
+            const int un = min(U, u1 - uc);
 #pragma unroll
             for (int u = 0; u < U; ++u) {
                 if (u >= un) break;
@@ -1048,7 +1086,22 @@ linear_rows_kernel(const int32_t *__restrict__ x, const RowsArgs a)
                         acc[r] += uint32_t((xbuf[wave][r][u * PER + j] & z) >> sh) ^ neg;
                 }
             }
-        } else {
+            // The next chunk overwrites wbuf and xbuf after these reads (in order).
+            __builtin_amdgcn_wave_barrier();
+        }
+    } else {
+        for (int uc = u0; uc < u1; uc += U) {
+            const int cb = uc * PER;
+#pragma unroll
+            for (int r = 0; r < ROWS; ++r) {
+                const int32_t *xrow = x + int64_t(b0 + min(r, nb - 1)) * a.C;
+#pragma unroll
+                for (int e = lane; e < E; e += 64) xbuf[wave][r][e] = xrow[min(cb + e, a.C - 1)];
+            }
+            // (LDS is written and read back by the same wave: in order, no barrier;
+            // the wave barrier keeps the compiler from moving the reads up.)
+            __builtin_amdgcn_wave_barrier();
+            const int un = min(U, u1 - uc);
             const int32_t *wrow = a.wi + int64_t(kc) * a.C;
             for (int u = 0; u < un; ++u) {
                 const int32_t w = wrow[uc + u];
@@ -1058,6 +1111,7 @@ linear_rows_kernel(const int32_t *__restrict__ x, const RowsArgs a)
                     acc[r] += OP == Inner::Mul ? uint32_t(xv) * uint32_t(w) : mul24(xv, w);
                 }
             }
+            __builtin_amdgcn_wave_barrier();
         }
     }
 #pragma unroll
@@ -1108,23 +1162,35 @@ static int rows_splits(int64_t blocks, int units, bool may_split)
     return splits;
 }
 
-// Batch rows per workgroup: the most (a power of two up to 8 that the batch fills)
-// with which the grid, split as above, still has 256 workgroups; else 1. More rows
-// share each decoded code, fewer give more workgroups: on MI355X 2048 -> 1000 ran
-// fastest with 8 rows at batch 32-128 (13.2, 20.0, 32.6 us against 15.1, 22.3,
-// 36.0 with 4), 512 -> 1000 at batch 32 with 2 (6.5 us against 8.9 with 8),
-// 256 -> 128 at batch 8 with 1 (4.5 us against 6.8 with 8). The DS_ROWS_BATCH
-// override is for measurements.
+// Batch rows per workgroup (1, 2, 4 or 8, at most the batch): the one with the
+// least estimated time, rounds of 256 workgroups (one 1024-thread workgroup per
+// CU) times each workgroup's work, (1.5 + rows) / parts (a code's decode costs
+// about 1.5 times a row's term). More rows share each decoded code, fewer give
+// more workgroups. The measured best on MI355X (graph replays), which this
+// picks: 2048 -> 1000 with 8 rows at batch 32-128 (12.3, 19.5, 31.9 us against
+// 13.7, 20.5, 34.1 with 4), with 4 at batch 16 and 192 (9.2 against 12.1 with
+// 8; 48.1 against 61.3: 384 workgroups of 8 rows fill the chip one and a half
+// times), with 2 at batch 8 (7.7 us); 512 -> 1000 at batch 32 with 2 (6.2 us
+// against 10.4 with 8); 256 -> 128 at batch 8 with 1 (3.8 us against 6.5 with
+// 8). The DS_ROWS_BATCH override is for measurements.
 static int rows_per_block(const ConvGeom &g, int units, bool may_split)
 {
     const int forced = tuning(kRowsBatch);
     if (forced == 1 || forced == 2 || forced == 4 || forced == 8) return forced;
     const int64_t kg = (g.k + 63) / 64;
-    for (int rows = g.n >= 8 ? 8 : g.n >= 4 ? 4 : g.n >= 2 ? 2 : 1; rows > 1; rows /= 2) {
+    int best = 1;
+    double best_cost = 0.0;
+    for (int rows = 1; rows <= 8 && rows <= g.n; rows *= 2) {
         const int64_t blocks = kg * ((g.n + rows - 1) / rows);
-        if (blocks * rows_splits(blocks, units, may_split) >= 256) return rows;
+        const int splits = rows_splits(blocks, units, may_split);
+        const int64_t rounds = std::max<int64_t>(1, (blocks * splits + 255) / 256);
+        const double cost = double(rounds) * (1.5 + rows) / splits;
+        if (rows == 1 || cost <= best_cost) {
+            best = rows;
+            best_cost = cost;
+        }
     }
-    return 1;
+    return best;
 }
 
 template <Inner OP>

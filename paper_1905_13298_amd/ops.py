@@ -483,8 +483,8 @@ class JitConv:
     # on full tiles of 256 output pixels (a ragged last tile wastes its lanes),
     # reading its packed weights at 4 TB/s. A LinearShift of fewer than 256 rows
     # takes the small-batch kernel instead (lanes own output channels): about 6
-    # us plus 9.6 T dense SACs/s, or its packed weights at 1.5 TB/s when they
-    # dominate (each lane walks its own row). A LinearShift plan on x^T adds its
+    # us plus 9.6 T dense SACs/s, or its packed weights at 1.75 TB/s when they
+    # dominate (batch 1: each code decoded for one row). A LinearShift plan on x^T adds its
     # two transposing passes and runs its kernel about 15 % slower than modelled
     # (2.5 us + 1.16 x the plan's own estimate fits batches 64-256 within 15 %).
     PLAN_STREAM_BPUS = 1.6e3        # code bytes per us per wave
@@ -507,7 +507,7 @@ class JitConv:
         nq = max(1, self.out_pixels)
         weight_bytes = self.out_channels * packed_row_words(self.crs) * 4
         if self.linear and nq < 256:
-            return 5.5 + max(self.sac / self.ROWS_SAC_PER_US, weight_bytes / 1.5e6)
+            return 5.5 + max(self.sac / self.ROWS_SAC_PER_US, weight_bytes / 1.75e6)
         fill = nq / (-(-nq // 256) * 256)
         return ((40.0 if self.linear else 25.0) + self.sac / (self.RUNTIME_SAC_PER_US * fill)
                 + weight_bytes / 4e6)
@@ -523,7 +523,7 @@ class JitConv:
         (12.0) against 8.4 us (9.0); 128 -> 128 3 x 3 at 28 x 28, batch 1 8.6 us
         (10) against 42 us eager (33); 256 -> 128 at batch 8 4.2 us (5.5)
         against 4.5 us (5.5); 512 -> 1000 at batch 32 10.2 us (11) against 6.5
-        us (7.2); 25088 -> 4096 at batch 1 344 us (282) against 45 us (48). Over
+        us (7.2); 25088 -> 4096 at batch 1 344 us (282) against 41 us (42). Over
         the layers of ResNet-18 (batch 32) and ResNet-50 (batch 128) measured /
         modelled plan durations have medians 1.16 and 1.04, runtime-kernel ones
         0.97 and 0.92."""

@@ -32,7 +32,7 @@ CASES = [
     # 512 -> 1000 at batch 32: 16-channel segments, wave split 4; small-batch runtime kernel
     ((32, 512, 1, 1, 1000, 1, 1, 1, 1), (3273484, 63, 1, 16, 4, 1), 10.2, 6.53),
     # 25088 -> 4096 at batch 1: split in 4; small-batch runtime kernel
-    ((1, 25088, 1, 1, 4096, 1, 1, 1, 1), (450e6, 256, 4, 64, 4, 1), 344.3, 45.3),
+    ((1, 25088, 1, 1, 4096, 1, 1, 1, 1), (450e6, 256, 4, 64, 4, 1), 344.3, 41.2),
     # On x^T (batch >= 64): 4096 -> 4096 at batch 256, 64-channel segments, wave
     # split 16, 4 tiles of 64 rows
     ((256, 4096, 1, 1, 4096, 1, 1, 1, 1), (74.3e6, 64, 1, 64, 16, 4, True), 108.7, 346.9),
