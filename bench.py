@@ -861,7 +861,7 @@ def bench_layers(args):
             model.append((plan.estimate_us(), plan.runtime_estimate_us(), plan.preferred,
                           {"code_bytes": plan.code_bytes, "segments": plan.segments, "splits": plan.splits,
                            "channels": plan.channels, "wsplit": plan.wsplit, "pixel_groups": plan.pixel_groups,
-                           "pixel_tiles": plan.pixel_tiles}))
+                           "pixel_tiles": plan.pixel_tiles, "transposed": plan.transposed}))
             if not plan.preferred:
                 if args.time_rejected:
                     rejected.append((len(plans), plan))
