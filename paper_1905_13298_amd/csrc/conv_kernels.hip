@@ -253,6 +253,31 @@ pad_planes_kernel(const T *__restrict__ x, int32_t *__restrict__ xp, int total, 
     }
 }
 
+// The same into a 16-byte aligned xp: four consecutive elements per lane (a row
+// or plane boundary may fall between them) in one 16-byte store; the total % 4
+// last elements are written by the first lanes of the grid.
+template <typename T>
+__global__ void __launch_bounds__(256)
+pad_planes4_kernel(const T *__restrict__ x, int32_t *__restrict__ xp, int total, int h, int w,
+                   int ph, int pw, FastDiv div_xw, FastDiv div_xh)
+{
+    auto at = [&](int idx) {
+        const int t = fdiv(idx, div_xw), j = idx - t * int(div_xw.d);
+        const int pl = fdiv(t, div_xh), i = t - pl * int(div_xh.d);
+        const int ii = i - ph, jj = j - pw;
+        return (unsigned(ii) < unsigned(h) && unsigned(jj) < unsigned(w))
+                   ? int32_t(x[(int64_t(pl) * h + ii) * w + jj])
+                   : 0;
+    };
+    const int quads = total >> 2;
+    const int first = int(blockIdx.x) * 256 + int(threadIdx.x);
+    for (int qd = first; qd < quads; qd += int(gridDim.x) * 256) {
+        const int idx = qd * 4;
+        reinterpret_cast<int4 *>(xp)[qd] = make_int4(at(idx), at(idx + 1), at(idx + 2), at(idx + 3));
+    }
+    if (first < (total & 3)) xp[quads * 4 + first] = at(quads * 4 + first);
+}
+
 // The epilogue on one output value v of channel k at flat index o.
 __device__ __forceinline__ uint32_t apply_epilogue(uint32_t v, int k, int64_t o, const Epilogue &e)
 {
@@ -924,8 +949,21 @@ hipError_t run_pad_planes(const void *x, int32_t *xp, int64_t planes, int h, int
     const int64_t total = planes * xh * xw;
     if (total <= 0) return hipSuccess;
     if (total > INT32_MAX || h <= 0 || w <= 0) return hipErrorInvalidValue;
-    const int grid = int(std::min<int64_t>((total + 255) / 256, 8192));
     const FastDiv dxw = make_fastdiv(uint32_t(xw)), dxh = make_fastdiv(uint32_t(xh));
+    if (reinterpret_cast<uintptr_t>(xp) % 16 == 0) {
+        const int grid = std::max(1, int(std::min<int64_t>((total / 4 + 255) / 256, 4096)));
+        if (xbytes == 2)
+            hipLaunchKernelGGL(pad_planes4_kernel<int16_t>, dim3(grid), dim3(256), 0, st,
+                               static_cast<const int16_t *>(x), xp, int(total), h, w, ph, pw, dxw, dxh);
+        else if (xbytes == 1)
+            hipLaunchKernelGGL(pad_planes4_kernel<int8_t>, dim3(grid), dim3(256), 0, st,
+                               static_cast<const int8_t *>(x), xp, int(total), h, w, ph, pw, dxw, dxh);
+        else
+            hipLaunchKernelGGL(pad_planes4_kernel<int32_t>, dim3(grid), dim3(256), 0, st,
+                               static_cast<const int32_t *>(x), xp, int(total), h, w, ph, pw, dxw, dxh);
+        return hipGetLastError();
+    }
+    const int grid = int(std::min<int64_t>((total + 255) / 256, 8192));
     if (xbytes == 2)
         hipLaunchKernelGGL(pad_planes_kernel<int16_t>, dim3(grid), dim3(256), 0, st,
                            static_cast<const int16_t *>(x), xp, int(total), h, w, ph, pw, dxw, dxh);
