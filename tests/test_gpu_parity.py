@@ -5,6 +5,7 @@ on seeded inputs and compares the int32 outputs with the oracle element by
 element. Small batches of the benchmark layers are checked here; every layer at the
 benchmark batch is checked in full in test_gpu_full_oracle.
 """
+import re
 import zlib
 
 import numpy as np
@@ -207,6 +208,57 @@ def test_output_canaries_untouched():
         assert np.all(b[:1024] == 0x5A5A5A5A) and np.all(b[1024 + size:] == 0x5A5A5A5A)
         np.testing.assert_array_equal(out.cpu().numpy(),
                                       oracle.conv2d_shift(x, codes, None, r=r, stride=st, pad=pd))
+
+
+@pytest.mark.parametrize("offset", [0, 1], ids=["aligned", "offset_4_bytes"])
+def test_split_outputs_ragged_and_unaligned(offset):
+    """Split reductions whose output count is not a multiple of 4, written into a
+    buffer on a 16-byte boundary and 4 bytes past one: the fill pass before the
+    atomics in its vector form with its tail, and in its element-wise form; the
+    runtime kernel and a plan with a forced split, both against the oracle, with
+    canaries on both sides of y."""
+    rng = np.random.default_rng(77 + offset)
+    n, c, h, w, k = 1, 256, 7, 7, 255
+    assert int(re.search(r"splits(\d+)", ops.describe_conv2d(n, c, h, w, k, 3, 1, 1)).group(1)) > 1
+    x = rng.integers(0, 2 ** 20, (n, c, h, w)).astype(np.int32)
+    codes = random_codes(rng, (k, c * 9), zero_frac=0.2)
+    bias = rng.integers(-(2 ** 20), 2 ** 20, k).astype(np.int32)
+    want = oracle.conv2d_shift(x, codes, bias, r=3, s=3, stride=1, pad=1)
+    size = want.size
+    assert size % 4 == 3
+    wp = ops.pack_shift_weights(codes)
+    xt, bt = to_dev(x), to_dev(bias)
+    plan = ops.JitConv(wp, x.shape, 3, 1, 1, bias=bias, splits=2)
+    try:
+        assert plan.splits == 2
+        for name, run in [("runtime", lambda out: ops.conv2d_shift(xt, to_dev(wp.view(np.int32)), bt, 3,
+                                                                   1, 1, out=out)),
+                          ("plan", lambda out: plan(xt, out=out))]:
+            big = torch.full((size + 2048,), 0x5A5A5A5A, dtype=torch.int32, device=DEV)
+            lo = 1024 + offset
+            out = big[lo:lo + size].view(want.shape)
+            run(out)
+            b = big.cpu().numpy()
+            say(name, "offset", offset)
+            assert np.all(b[:lo] == 0x5A5A5A5A) and np.all(b[lo + size:] == 0x5A5A5A5A), name
+            np.testing.assert_array_equal(b[lo:lo + size].reshape(want.shape), want, err_msg=name)
+    finally:
+        plan.close()
+
+
+def test_padded_copy_ragged():
+    """A plan reading a 5 x 5 window through its zero-padded copy of x, whose
+    element count (3 planes of 13 x 13) is not a multiple of 4: the copy's vector
+    stores and its tail, against the oracle."""
+    rng = np.random.default_rng(5)
+    x = rng.integers(-(2 ** 20), 2 ** 20, (1, 3, 9, 9)).astype(np.int32)
+    codes = random_codes(rng, (7, 3 * 25), zero_frac=0.2)
+    want = oracle.conv2d_shift(x, codes, None, r=5, s=5, stride=1, pad=2)
+    plan = ops.JitConv(ops.pack_shift_weights(codes), x.shape, 5, 1, 2)
+    try:
+        np.testing.assert_array_equal(plan(to_dev(x)).cpu().numpy(), want)
+    finally:
+        plan.close()
 
 
 def test_nondefault_stream_and_repeat():
