@@ -146,7 +146,6 @@ def test_fp64_band_single_layer_configs_every_output(cfg):
         ref = F.conv2d(torch.from_numpy(x.astype(np.float64)),
                        torch.from_numpy(wf.reshape(L.k, L.c, L.r, L.s)),
                        stride=L.stride, padding=L.pad).numpy()
-        ref = ref
     if bias is not None:
         ref = ref + (bias.reshape(1, -1) if L.kind == "linear" else bias.reshape(1, -1, 1, 1))
     for name, y in ys.items():
