@@ -92,7 +92,9 @@ def algorithmic_bytes(layer, act_bits: int = 32) -> int:
 def parse():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
-    ap.add_argument("--steps", type=int, default=5)
+    ap.add_argument("--steps", type=int, default=None,
+                    help="timed steps (default: 640 for a single layer, whose step lasts microseconds, "
+                         "so that graph launches are a small part of the timed region; 5 otherwise)")
     ap.add_argument("--warmup", type=int, default=2)
     ap.add_argument("--workload", default="resnet50", choices=sorted(WORKLOADS) + sorted(CONVERT_WORKLOADS) + sorted(NETWORK_WORKLOADS)
                     + sorted(BACKWARD_WORKLOADS) + sorted(PROBE_WORKLOADS) + sorted(MODEL_WORKLOADS))
@@ -663,6 +665,9 @@ def main():
               file=sys.stderr)
         sys.exit(2)
 
+    if args.steps is None and args.workload not in WORKLOADS and args.workload not in PROBE_WORKLOADS \
+            and args.workload not in MODEL_WORKLOADS:
+        args.steps = 5
     if args.workload in CONVERT_WORKLOADS:
         bench_convert(args)
         return
@@ -832,6 +837,11 @@ def bench_layers(args):
         cfg = WORKLOADS[args.workload]
         seed = W.CONFIG_SEEDS[cfg]
         layers = W.config_layers(cfg)
+    if args.steps is None:
+        # A single layer's step lasts microseconds and a graph launch tens of
+        # them: 640 steps (10 graphs of 64) keep launches a small part of the
+        # timed region. A network's step lasts milliseconds.
+        args.steps = 640 if len(layers) == 1 else 5
     dev = torch.device("cuda:0")
     torch.cuda.set_device(dev)
     stream = torch.cuda.current_stream(dev)
