@@ -260,14 +260,15 @@ def sq_summary(directory, workload, path):
     print(json.dumps(rec, indent=1))
 
 
-def measured_traffic(kernel: str, family: str):
+def measured_traffic(kernel: str, family: str, workload: str):
     """HBM bytes per launch of `kernel` from the committed counter record, or None
-    when there is none or the kernel source changed since it was taken."""
+    when there is none, it was taken on another workload, or the kernel source
+    changed since it was taken."""
     try:
         rec = json.load(open(FAMILIES[family][1]))
     except (OSError, ValueError):
         return None
-    if rec.get("kernel_source_sha256_16") != kernel_source_hash(family):
+    if rec.get("workload") != workload or rec.get("kernel_source_sha256_16") != kernel_source_hash(family):
         return None
     k = rec["kernels"].get(kernel)
     if not k:
@@ -780,7 +781,7 @@ def time_layers(calls, steps, warmup, stream):
     return ms_per_step, d
 
 
-def roofline_of(layers, d, path, nonzero, planned=None, act_bits=32):
+def roofline_of(layers, d, path, nonzero, planned=None, act_bits=32, workload=None):
     """Roofline record of the kernel with the most time per step, from the
     per-call durations `d` [steps][layers]; planned[i]: layer i runs a plan."""
     groups = {}
@@ -793,7 +794,8 @@ def roofline_of(layers, d, path, nonzero, planned=None, act_bits=32):
         g["launches"] += 1
         g["bytes"] += algorithmic_bytes(L, act_bits)
     name, g = max(groups.items(), key=lambda kv: kv[1]["ms"])
-    traffic = measured_traffic(name, "jit" if name == JIT_KERNEL else "runtime") if act_bits == 32 else None
+    traffic = measured_traffic(name, "jit" if name == JIT_KERNEL else "runtime", workload) \
+        if act_bits == 32 and workload else None
     common = {
         "traffic": None if traffic is None else int(traffic),
         "traffic_unit": "HBM bytes per launch (FETCH_SIZE + WRITE_SIZE, copy-calibrated)",
@@ -929,7 +931,8 @@ def bench_layers(args):
                   "graph_ms_per_step": round(ms_per_step, 5), "eager_ms_per_step": timing["eager_ms_per_step"]}
     value = sac_step / (ms_per_step * 1e-3) / 1e9
     planned = [p is not None for p in plans]
-    roofline = roofline_of(layers, d, args.path, nonzero, planned, act)
+    wl_name = W.CONFIG_NAMES[cfg] if cfg is not None else args.workload
+    roofline = roofline_of(layers, d, args.path, nonzero, planned, act, workload=wl_name)
 
     runtime = None
     d_rt = d
@@ -938,7 +941,7 @@ def bench_layers(args):
         rt_value = sac_step / (rt_ms * 1e-3) / 1e9
         runtime = {"ms_per_step": round(rt_ms, 4), "value": round(rt_value, 2), "unit": "GSAC/s",
                    "frac_sac_peak": round(rt_value / 1000.0 / SAC_PEAK_T, 4),
-                   "roofline": roofline_of(layers, d_rt, "runtime", nonzero)}
+                   "roofline": roofline_of(layers, d_rt, "runtime", nonzero, workload=wl_name)}
 
     per_layer = []
     fr = [L.sac * nonzero[li] / (float(np.median(d[:, li])) * 1e-3) / 1e12 / VOP2_OPS_PEAK_T
