@@ -94,7 +94,7 @@ def parse():
     ap.add_argument("--gpus", type=int, default=1)
     ap.add_argument("--steps", type=int, default=None,
                     help="timed steps (default: 640 for a single layer, whose step lasts microseconds, "
-                         "so that graph launches are a small part of the timed region; 5 otherwise)")
+                         "24 for a network, so that graph launches are a small part of the timed region)")
     ap.add_argument("--warmup", type=int, default=2)
     ap.add_argument("--workload", default="resnet50", choices=sorted(WORKLOADS) + sorted(CONVERT_WORKLOADS) + sorted(NETWORK_WORKLOADS)
                     + sorted(BACKWARD_WORKLOADS) + sorted(PROBE_WORKLOADS) + sorted(MODEL_WORKLOADS))
@@ -668,7 +668,7 @@ def main():
 
     if args.steps is None and args.workload not in WORKLOADS and args.workload not in PROBE_WORKLOADS \
             and args.workload not in MODEL_WORKLOADS:
-        args.steps = 5
+        args.steps = 24
     if args.workload in CONVERT_WORKLOADS:
         bench_convert(args)
         return
@@ -842,8 +842,10 @@ def bench_layers(args):
     if args.steps is None:
         # A single layer's step lasts microseconds and a graph launch tens of
         # them: 640 steps (10 graphs of 64) keep launches a small part of the
-        # timed region. A network's step lasts milliseconds.
-        args.steps = 640 if len(layers) == 1 else 5
+        # timed region. A network's step lasts milliseconds: 24 steps, in graphs
+        # of up to 64 calls (3 steps of ResNet-18, which read 5-8 % faster per
+        # step than graphs of one step on MI355X).
+        args.steps = 640 if len(layers) == 1 else 24
     dev = torch.device("cuda:0")
     torch.cuda.set_device(dev)
     stream = torch.cuda.current_stream(dev)
