@@ -19,11 +19,15 @@ Prints ONE JSON line:
   runtime_weights  the runtime path timed on the same inputs (path jit)
   cpu_baseline the oracle on the host cores, on a prefix (small batch) of
               the same seeded inputs
-  mul_i32     the multiplication-based comparison kernel (tiling of the
-              runtime kernel) on the same layers
+  mul_comparison  the multiplication-based comparison on the same layers, at
+              the tiling of each shift path: int32 and 24-bit multiply-adds in
+              the runtime kernel's tiling, 24-bit multiply-adds baked into
+              plans like the shifts
 
 Usage: python bench.py [--gpus 1] [--steps K] [--warmup W] [--workload resnet50]
                        [--path jit|runtime]
+K defaults to 24 for a network and 640 for a single layer (whose steps last
+microseconds), W to 2.
 """
 from __future__ import annotations
 
