@@ -4,8 +4,9 @@ Each case draws a ConvShift (with or without the fused epilogue: per-channel
 affine, residual, ReLU), a LinearShift, or a ConvShift input gradient, with
 random shapes, strides, padding, signs, zero-weight fractions, weight codes of
 2 to 5 bits, plan inputs of 32, 16 or 8 bits, forced plan
-layouts (segment width, wave split, pixel groups, block order, split-K parts,
-x^T or x for LinearShift, batch rows per workgroup of the small-batch kernel),
+layouts (segment width, wave split, pixel groups, block order and its tile
+groups, loads in flight, register map, split-K parts, x^T or x for LinearShift,
+batch rows per workgroup of the small-batch kernel),
 and compares the runtime-weights call and the weight-specialised plan with the
 oracle bit for bit. The layouts are the ones the planner can be forced into
 for measurements; every one of them must give the oracle's output.
@@ -21,7 +22,7 @@ from paper_1905_13298_amd.workloads import random_codes
 pytestmark = pytest.mark.gpu
 DEV = torch.device("cuda:0")
 KNOBS = ("DS_JIT_TN", "DS_JIT_WSPLIT", "DS_JIT_PGROUPS", "DS_JIT_ORDER", "DS_JIT_TRANSPOSE",
-         "DS_ROWS_BATCH")
+         "DS_ROWS_BATCH", "DS_JIT_SLOTS", "DS_JIT_MAP", "DS_JIT_GROUP_TILES")
 CASES = 400
 
 
@@ -68,6 +69,9 @@ def draw_knobs(rng, knob):
         v["DS_JIT_ORDER"] = int(rng.choice([-1, 0, 1, 2]))
     v["DS_JIT_TRANSPOSE"] = int(rng.choice([-1, -1, 0, 1]))
     v["DS_ROWS_BATCH"] = int(rng.choice([-1, -1, 1, 2, 4, 8]))
+    v["DS_JIT_SLOTS"] = int(rng.choice([-1, -1, 1, 2, 3, 5, 8, 14]))
+    v["DS_JIT_MAP"] = int(rng.choice([-1, -1, -1, 96]))
+    v["DS_JIT_GROUP_TILES"] = int(rng.choice([-1, -1, 1, 2, 7, 64]))
     for k, x in v.items():
         knob(k, x)
     return v
