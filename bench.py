@@ -706,12 +706,12 @@ def time_graph(calls, outs, steps, warmup):
     shortest layers is more than their kernels; a graph launches the same
     kernels (plans use no memset and allocate nothing when run). A graph launch
     itself costs tens of microseconds, so a graph holds R consecutive steps, R
-    the largest divisor of `steps` that keeps it within 128 calls: `warmup`
+    the largest divisor of `steps` that keeps it within 64 calls: `warmup`
     untimed steps, then steps / R replays between two HIP events. The outputs
     of the first and the last replay must equal those of the eager calls.
     Returns (ms per step, R)."""
     import torch
-    per = max(1, 128 // max(1, len(calls)))
+    per = max(1, 64 // max(1, len(calls)))
     rep = max(r for r in range(1, min(per, steps) + 1) if steps % r == 0)
     for c in calls:
         c()
@@ -845,11 +845,10 @@ def bench_layers(args):
         layers = W.config_layers(cfg)
     if args.steps is None:
         # A single layer's step lasts microseconds and a graph launch tens of
-        # them: 640 steps (5 graphs of 128) keep launches a small part of the
+        # them: 640 steps (10 graphs of 64) keep launches a small part of the
         # timed region. A network's step lasts milliseconds: 24 steps, in graphs
-        # of up to 128 calls (6 steps of ResNet-18: on MI355X graphs of 3 steps
-        # read 5-8 % faster per step than graphs of one, and of 6 steps 1-2 %
-        # faster than of 3).
+        # of up to 64 calls (3 steps of ResNet-18, which read 5-8 % faster per
+        # step than graphs of one step on MI355X).
         args.steps = 640 if len(layers) == 1 else 24
     dev = torch.device("cuda:0")
     torch.cuda.set_device(dev)
